@@ -1,0 +1,186 @@
+/*
+ * painn.h - C ABI of the MI355X (gfx950) batched PaiNN screening forward pass.
+ *
+ * The operation is the one the paper runs over 1.1 billion structures
+ * (section "Inference on Billions of Atomistic Structures on Frontier"): for a
+ * batch of many small molecules and periodic cells, build the radius graph
+ * (lead model: cutoff radius, Table 5), run the PaiNN interaction layers
+ * (PaiNN is the lead backbone chosen in section "Flagship Training of Top HPO
+ * Models"; message and update blocks as published by Schuett et al. 2021),
+ * and read out one energy per structure through per-dataset heads (Table 5:
+ * shared layers + branch layers, 16 graph-level branches; section "Multi-task
+ * learning for imbalanced, heterogeneous multi-fidelity data").  Precision is
+ * a per-call choice among FP64, FP32 and BF16 (section "Precision-sensitivity
+ * characterization at inference and fine-tuning stage").
+ *
+ * Conventions for every entry point:
+ *  - Return value: PAINN_OK (0) or a negative painn_status.  Nothing throws or
+ *    aborts; after an error, painn_last_error(ctx) describes it.
+ *  - Array arguments are DEVICE pointers (memory of the context's device),
+ *    owned by the caller, unless a comment says "host".  They are read in the
+ *    order of the context's stream; the caller keeps them alive and unchanged
+ *    until that stream has passed the call.
+ *  - Opaque objects (context, model, graph) are owned by the library and are
+ *    released only by the matching *_free / painn_destroy.
+ *  - All work is enqueued on the context's HIP stream.  The only host
+ *    synchronisation is inside painn_build_graph (it reads back the edge
+ *    count) and painn_synchronize.
+ *  - A context is not thread-safe; use one context per host thread.
+ */
+#ifndef PAINN_H
+#define PAINN_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+  PAINN_OK = 0,
+  PAINN_E_ARG = -1,          /* invalid argument (null pointer, size, cutoff, struct_ptr) */
+  PAINN_E_OOM = -2,          /* device or host allocation failed */
+  PAINN_E_HIP = -3,          /* a HIP runtime call failed */
+  PAINN_E_FILE = -4,         /* weight file cannot be opened or read */
+  PAINN_E_FORMAT = -5,       /* weight file malformed (magic, header, size) */
+  PAINN_E_SPECIES = -6,      /* a species index is outside [0, n_species) */
+  PAINN_E_COINCIDENT = -7,   /* two atoms (or an atom and a periodic image) at distance 0 */
+  PAINN_E_UNSUPPORTED = -8   /* shape or option the kernels do not implement */
+} painn_status;
+
+typedef enum {
+  PAINN_FP64 = 0,            /* weights, features and accumulation in FP64 */
+  PAINN_FP32 = 1,            /* weights, features and accumulation in FP32 */
+  PAINN_BF16 = 2             /* BF16 weights and stored features, FP32 accumulation */
+} painn_precision;
+
+typedef struct painn_ctx painn_ctx;
+typedef struct painn_model painn_model;
+typedef struct painn_graph painn_graph;
+
+/* ---- context ---------------------------------------------------------- */
+
+/* Create a context on HIP device `device`, enqueueing on `hip_stream` (a
+ * hipStream_t; NULL = the device's null stream).  The library does not take
+ * ownership of the stream.  *out receives the context. */
+painn_status painn_create(int device, void* hip_stream, painn_ctx** out);
+/* Change the stream of an existing context (same device). */
+painn_status painn_set_stream(painn_ctx* ctx, void* hip_stream);
+/* Release the context and its workspace.  Models and graphs created on it
+ * must be freed first.  NULL is accepted. */
+painn_status painn_destroy(painn_ctx* ctx);
+/* Message of the last error on this context (never NULL; "" after success). */
+const char* painn_last_error(const painn_ctx* ctx);
+/* Static name of a status code. */
+const char* painn_status_string(int status);
+/* Block the host until all work enqueued by the context has finished. */
+painn_status painn_synchronize(painn_ctx* ctx);
+
+/* ---- model -------------------------------------------------------------- */
+
+/* Load an FP64 weight file (host path).  Format, little-endian:
+ *   char magic[8] = "PAINNW01";
+ *   int32 F, K, L, n_species, n_heads, rbf_type (0 = Gaussian), n_shared, n_branch;
+ *   float64 cutoff;
+ *   int32 shared_dims[n_shared];   output width of each shared head layer
+ *   int32 branch_dims[n_branch];   output width of each branch layer (last = 1)
+ *   zero padding to a multiple of 8 bytes;
+ *   float64 arrays, row-major, dense weights stored [out, in]:
+ *     emb[n_species, F];
+ *     per layer: phi_w1[F,F] phi_b1[F] phi_w2[3F,F] phi_b2[3F]
+ *                filt_w[3F,K] filt_b[3F] U[F,F] V[F,F]
+ *                upd_w1[F,2F] upd_b1[F] upd_w2[3F,F] upd_b2[3F];
+ *     per shared layer m: w[shared_dims[m], in] b[shared_dims[m]];
+ *     per head h, per branch layer m: w[branch_dims[m], in] b[branch_dims[m]].
+ * The split of phi's output is [s | v | rhat] and of the update MLP's output
+ * [a_vv | a_sv | a_ss].  Supported: F in {64, 128, 256}, 2 <= K <= 64,
+ * 1 <= L <= 16, n_heads <= 64, branch_dims[last] = 1. */
+painn_status painn_model_load(painn_ctx* ctx, const char* path, painn_model** out);
+/* Same, from a host buffer holding the file's bytes (copied; the buffer may
+ * be released after the call). */
+painn_status painn_model_load_buffer(painn_ctx* ctx, const void* data, size_t nbytes,
+                                     painn_model** out);
+/* Hyperparameters of a model (host outputs; any pointer may be NULL). */
+painn_status painn_model_info(const painn_model* model, int32_t* F, int32_t* K, int32_t* L,
+                              int32_t* n_species, int32_t* n_heads, double* cutoff);
+painn_status painn_model_free(painn_model* model);
+
+/* ---- graph -------------------------------------------------------------- */
+
+/* Build the radius graph of a batch of B structures with N atoms in total.
+ * Edges are all (i <- j, n) with i, j in the same structure, n an integer
+ * image vector (n_k = 0 on non-periodic axes), (i, j, n) != (i, i, 0), and
+ *   t = (n0*a + n1*b) + n2*c,  r = (x_j - x_i) + t,
+ *   d2 = (r.x*r.x + r.y*r.y) + r.z*r.z  <  cutoff*cutoff
+ * evaluated in IEEE FP64 in exactly this order without fused multiply-add, so
+ * the edge set is bit-exact.  Every periodic image within the cutoff is kept.
+ * The CSR is sorted by receiver i, then sender j, then (n0, n1, n2).
+ *   struct_ptr [B+1] int32: atoms of structure b are [struct_ptr[b], struct_ptr[b+1]);
+ *                           struct_ptr[0] = 0, non-decreasing, struct_ptr[B] = N.
+ *   pos        [N,3] float64, Angstrom.
+ *   species    [N]   int32, checked against the model at painn_forward.
+ *   cell       [B,3,3] float64, rows are the lattice vectors a, b, c; may be
+ *              NULL when pbc is NULL.
+ *   pbc        [B,3] uint8, nonzero = periodic along that lattice vector; NULL
+ *              = no periodic axis anywhere.  A periodic cell must be non-singular.
+ * The graph copies what it needs (positions, species, cells), so the inputs
+ * may change after the call's stream position.  If *inout is NULL a new graph
+ * is created; otherwise *inout is rebuilt in place, reusing its memory.
+ * Synchronises the stream once.  Errors: PAINN_E_ARG (bad sizes, cutoff not
+ * finite and > 0, malformed struct_ptr, singular periodic cell, more than
+ * 2^31-1 edges, image range beyond +-127), PAINN_E_COINCIDENT. */
+painn_status painn_build_graph(painn_ctx* ctx, int32_t n_struct, int32_t n_atoms,
+                               const int32_t* struct_ptr, const double* pos,
+                               const int32_t* species, const double* cell,
+                               const uint8_t* pbc, double cutoff, painn_graph** inout);
+/* Borrow the CSR of a graph (device pointers valid until the graph is rebuilt
+ * or freed): row_ptr [N+1] int32, col [E] int32 (batch-global sender index),
+ * shift [E] int32 packing (n0, n1, n2) as signed bytes 0, 1, 2 (byte 3 = 0).
+ * Host outputs; any may be NULL. */
+painn_status painn_graph_csr(const painn_graph* graph, int64_t* n_edges, int32_t* n_atoms,
+                             int32_t* n_struct, const int32_t** row_ptr, const int32_t** col,
+                             const int32_t** shift);
+painn_status painn_graph_free(painn_graph* graph);
+
+/* ---- forward ------------------------------------------------------------ */
+
+/* Per-structure energies E_b = sum over atoms i of structure b of e_i, where
+ * e_i is the head of the structure's dataset applied to atom i's final
+ * scalar features.
+ *   dataset_id [B] int32 in [0, n_heads), or NULL = head 0 for every structure.
+ *   energies   [B] float64 output, written on the stream.
+ * The graph must have been built with the model's cutoff.  Errors:
+ * PAINN_E_ARG (cutoff mismatch, null pointers), PAINN_E_SPECIES,
+ * PAINN_E_UNSUPPORTED.  Asynchronous, so a dataset id outside [0, n_heads)
+ * cannot be reported as a status: that structure's energy is written as NaN. */
+painn_status painn_forward(painn_ctx* ctx, const painn_model* model, const painn_graph* graph,
+                           const int32_t* dataset_id, painn_precision precision,
+                           double* energies);
+
+/* Test hook: run layers 0..layer (layer = -1: embedding only) and write the
+ * scalar features s [N,F] and vector features v [N,3,F] (float64) reached
+ * there.  Same arguments and errors as painn_forward. */
+painn_status painn_forward_features(painn_ctx* ctx, const painn_model* model,
+                                    const painn_graph* graph, painn_precision precision,
+                                    int32_t layer, double* s_out, double* v_out);
+
+/* ---- tracing ------------------------------------------------------------ */
+
+/* Per-kernel timing with HIP events on the context's stream (the build's
+ * counterpart of the paper's application timers, section "How Performance
+ * Was Measured").  While enabled, every kernel launch is bracketed by two
+ * event records on the stream; nothing synchronises until painn_profile_read.
+ * enable = 0 stops recording (accumulated results are kept). */
+painn_status painn_profile_enable(painn_ctx* ctx, int enable);
+/* Synchronise the stream, then write per kernel class (at most n_max): its
+ * name (static string), accumulated GPU milliseconds and launch count since
+ * the last read; reset the accumulators.  names, ms, launches are host arrays
+ * of n_max entries; *n_out receives the number of classes written. */
+painn_status painn_profile_read(painn_ctx* ctx, int32_t n_max, const char** names, double* ms,
+                                int64_t* launches, int32_t* n_out);
+
+#ifdef __cplusplus
+}
+#endif
+#endif /* PAINN_H */

@@ -1,0 +1,157 @@
+// Internal declarations shared by the host runtime and the kernel files.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include <string>
+#include <vector>
+
+#include "painn.h"
+
+typedef uint16_t bf16_t;  // bfloat16 storage (upper half of an IEEE float)
+
+// ---- error bits written by the graph kernels into DevStatus::err ----------
+enum : int32_t {
+  ERR_STRUCT_PTR = 1,   // struct_ptr not a partition of [0, N)
+  ERR_CELL = 2,         // singular or non-finite periodic cell
+  ERR_IMAGES = 4,       // image range beyond +-127 or n_atoms*n_images >= 2^31
+  ERR_COINCIDENT = 8,   // d2 == 0 for a pair other than (i, i, 0)
+  ERR_EDGES = 16,       // more than 2^31 - 1 edges
+};
+
+struct DevStatus {      // read back once per build_graph
+  long long n_edges;
+  int32_t err;
+  int32_t species_min;
+  int32_t species_max;
+  int32_t pad;
+};
+
+struct StructInfo {     // per structure: atom range and periodic image range
+  int32_t lo, n;
+  int32_t m0, m1, m2;   // |n_k| <= m_k
+  int32_t nimg;         // (2 m0 + 1)(2 m1 + 1)(2 m2 + 1)
+};
+
+// ---- dense-layer packing ---------------------------------------------------
+// A dense layer W [dout, din] is stored padded to (pad32(dout), pad32(din))
+// with zeros, in the operand order of a 16x16xKC MFMA: block (ct, kb) holds 64
+// lanes x KPL consecutive elements, lane l carrying
+// W[16 ct + l % 16][KC kb + KPL (l / 16) + e], e < KPL.
+// (FP64/FP32: KC = 4, KPL = 1; BF16: KC = 32, KPL = 8.)
+inline __host__ __device__ int pad32(int d) { return (d + 31) & ~31; }
+
+// Number of radial basis slots compiled into the message kernel for K basis
+// functions (the filter rows are zero-padded from K to this).
+inline int filter_kp(int K) {
+  const int opts[] = {4, 8, 12, 16, 20, 24, 32, 40, 48, 64};
+  for (int o : opts)
+    if (K <= o) return o;
+  return -1;
+}
+
+struct DenseDev {       // one packed layer on the device
+  void* w = nullptr;    // packed weights, storage type of the precision
+  void* b = nullptr;    // bias [pad32(dout)], accumulation type (zero padded)
+  int din = 0, dout = 0, din_p = 0, dout_p = 0;
+};
+
+struct LayerDev {       // one interaction layer
+  DenseDev phi1, phi2;  // F -> F (silu), F -> 3F
+  DenseDev uv;          // [U; V] stacked: F -> 2F
+  DenseDev upd1, upd2;  // 2F -> F (silu), F -> 3F
+  void* filt = nullptr; // [3F][KP+1] accumulation type, KP = filter_kp(K):
+                        // columns K..KP-1 zero, column KP the bias
+};
+
+struct PrecModel {      // the model cast and packed for one precision
+  int prec = -1;
+  void* emb = nullptr;  // [n_species][F] storage type
+  std::vector<LayerDev> layers;
+  std::vector<DenseDev> shared;                 // shared head layers
+  std::vector<std::vector<DenseDev>> branch;    // [head][layer]
+  void* head_table = nullptr;                   // device [head][layer][2] = (w, b)
+  std::vector<void*> allocs;
+};
+
+struct Hyper {
+  int F, K, L, n_species, n_heads, rbf_type;
+  double cutoff;
+  std::vector<int> shared_dims, branch_dims;
+};
+
+// ---- per-kernel event timing (painn_profile_*) ------------------------------
+enum KernelClass {
+  KC_GRAPH_PREP, KC_GRAPH_COUNT, KC_GRAPH_SCAN, KC_GRAPH_FILL, KC_EMBED, KC_PHI,
+  KC_MESSAGE, KC_UPDATE, KC_HEADS, KC_ENERGY, KC_EXPORT, KC_COUNT
+};
+struct Profiler;
+// Record the start (begin = true) or end of a kernel of class `kc` on `s`;
+// a no-op when `p` is null or disabled.
+void prof_mark(Profiler* p, hipStream_t s, int kc, bool begin);
+
+struct painn_ctx {
+  int device = 0;
+  Profiler* prof = nullptr;
+  hipStream_t stream = nullptr;
+  std::string err;
+  DevStatus* h_status = nullptr;   // pinned host mirror of the graph status
+  // forward workspace (grown on demand)
+  void* ws = nullptr;
+  size_t ws_bytes = 0;
+};
+
+struct painn_model {
+  painn_ctx* ctx = nullptr;
+  Hyper hp;
+  std::vector<double> master;      // FP64 weights in file order
+  std::vector<size_t> offsets;     // offset of each array in `master`
+  PrecModel* prec[3] = {nullptr, nullptr, nullptr};
+};
+
+struct painn_graph {
+  painn_ctx* ctx = nullptr;
+  int32_t B = 0, N = 0;
+  long long E = 0;
+  double cutoff = 0.0;
+  int32_t species_min = 0, species_max = -1;
+  bool any_pbc = false;
+  // device buffers (capacities in elements)
+  int32_t* row_ptr = nullptr;  int32_t* counts = nullptr;
+  int32_t* col = nullptr;      int32_t* shift = nullptr;
+  double* pos = nullptr;       int32_t* species = nullptr;
+  int32_t* atom_struct = nullptr;
+  double* cell = nullptr;      StructInfo* sinfo = nullptr;
+  int32_t* struct_ptr = nullptr;
+  long long* scan_tmp = nullptr;
+  DevStatus* d_status = nullptr;
+  size_t cap_atoms = 0, cap_struct = 0, cap_edges = 0, cap_scan = 0;
+};
+
+// ---- kernel launchers (each enqueues on `s`, returns hipGetLastError) ------
+hipError_t launch_graph_prep(hipStream_t s, Profiler* p, int B, int N, const int32_t* struct_ptr,
+                             const double* pos, const int32_t* species, const double* cell,
+                             const uint8_t* pbc, double cutoff, painn_graph* g);
+hipError_t launch_graph_count(hipStream_t s, Profiler* p, painn_graph* g);
+hipError_t launch_graph_scan(hipStream_t s, Profiler* p, painn_graph* g);
+hipError_t launch_graph_fill(hipStream_t s, Profiler* p, painn_graph* g);
+
+struct ForwardArgs {
+  const painn_model* m;
+  const PrecModel* pm;
+  const painn_graph* g;
+  const int32_t* dataset_id;
+  double* energies;
+  // workspace
+  void* s;      // [N][F] storage
+  void* v[2];   // [N][3][F] storage, double buffered
+  void* h;      // [N][3F] storage
+  void* e;      // [N] accumulation type
+  int stop_layer;          // run layers 0..stop_layer (forward: L-1)
+  Profiler* prof;
+  double* s_out;           // feature export (may be null)
+  double* v_out;
+};
+size_t forward_workspace_bytes(int prec, int N, int F);
+hipError_t launch_forward(hipStream_t s, int prec, ForwardArgs& a);

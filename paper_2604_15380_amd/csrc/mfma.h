@@ -1,0 +1,111 @@
+// Precision traits and the workgroup dense-layer routine used by the per-atom
+// kernels (message MLP phi, the update block's U/V and gate MLP, the heads).
+//
+// A dense layer Y[rows, dout] = X[rows, din] W^T + b runs on 16x16 MFMA tiles
+// (gfx950): v_mfma_f64_16x16x4f64, v_mfma_f32_16x16x4f32 and
+// v_mfma_f32_16x16x32_bf16.  Operand layout for one 16x16xKC instruction,
+// lane l of the wavefront, KPL = KC / 4 consecutive k per lane:
+//   A: row l % 16,  k = KPL (l / 16) + e        (activations, from LDS)
+//   B: col l % 16,  k = KPL (l / 16) + e        (weights, pre-packed in HBM)
+//   C: col l % 16; register i < 4 holds row 4 (l / 16) + i for the FP32 and
+//      BF16 instructions but row 4 i + l / 16 for the FP64 one (measured on
+//      gfx950); P::row(l, i) gives it.
+// Weights are packed on the host in exactly the B order, so a B fragment is
+// one coalesced load per lane that the whole chip re-reads from L2.
+#pragma once
+
+#include "internal.h"
+
+typedef double d4_t __attribute__((ext_vector_type(4)));
+typedef float f4_t __attribute__((ext_vector_type(4)));
+typedef __bf16 bf8_t __attribute__((ext_vector_type(8)));
+
+__device__ __forceinline__ float bf16_to_f(bf16_t h) { return __uint_as_float((uint32_t)h << 16); }
+// round to nearest even; NaN stays NaN
+__device__ __forceinline__ bf16_t f_to_bf16(float f) {
+  uint32_t u = __float_as_uint(f);
+  if ((u & 0x7fffffffu) > 0x7f800000u) return (bf16_t)0x7fc0;
+  u += 0x7fffu + ((u >> 16) & 1u);
+  return (bf16_t)(u >> 16);
+}
+
+struct P64 {
+  using T = double;  // storage
+  using A = double;  // accumulation
+  using C = d4_t;
+  using Fr = double;
+  static constexpr int KC = 4, KPL = 1, PAD = 2, PREC = PAINN_FP64;
+  __device__ static __forceinline__ Fr frag(const T* p) { return *p; }
+  __device__ static __forceinline__ C mfma(Fr a, Fr b, C c) {
+    return __builtin_amdgcn_mfma_f64_16x16x4f64(a, b, c, 0, 0, 0);
+  }
+  __device__ static __forceinline__ A ld(T x) { return x; }
+  __device__ static __forceinline__ T st(A x) { return x; }
+  __device__ static __forceinline__ A ex(A x) { return exp(x); }
+  __device__ static __forceinline__ int row(int lane, int i) { return 4 * i + (lane >> 4); }
+};
+
+struct P32 {
+  using T = float;
+  using A = float;
+  using C = f4_t;
+  using Fr = float;
+  static constexpr int KC = 4, KPL = 1, PAD = 4, PREC = PAINN_FP32;
+  __device__ static __forceinline__ Fr frag(const T* p) { return *p; }
+  __device__ static __forceinline__ C mfma(Fr a, Fr b, C c) {
+    return __builtin_amdgcn_mfma_f32_16x16x4f32(a, b, c, 0, 0, 0);
+  }
+  __device__ static __forceinline__ A ld(T x) { return x; }
+  __device__ static __forceinline__ T st(A x) { return x; }
+  __device__ static __forceinline__ A ex(A x) { return expf(x); }
+  __device__ static __forceinline__ int row(int lane, int i) { return 4 * (lane >> 4) + i; }
+};
+
+struct PB16 {
+  using T = bf16_t;
+  using A = float;
+  using C = f4_t;
+  using Fr = bf8_t;
+  static constexpr int KC = 32, KPL = 8, PAD = 8, PREC = PAINN_BF16;
+  __device__ static __forceinline__ Fr frag(const T* p) { return *(const bf8_t*)p; }
+  __device__ static __forceinline__ C mfma(Fr a, Fr b, C c) {
+    return __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, b, c, 0, 0, 0);
+  }
+  __device__ static __forceinline__ A ld(T x) { return bf16_to_f(x); }
+  __device__ static __forceinline__ T st(A x) { return f_to_bf16(x); }
+  __device__ static __forceinline__ A ex(A x) { return expf(x); }
+  __device__ static __forceinline__ int row(int lane, int i) { return 4 * (lane >> 4) + i; }
+};
+
+template <class A>
+__device__ __forceinline__ A silu(A x) {
+  return x / (A(1) + (sizeof(A) == 8 ? (A)exp((double)-x) : (A)expf((float)-x)));
+}
+
+// Dense layer over RT row tiles (16 rows each) held in LDS at X (row stride
+// ldx elements).  Column tiles are dealt round-robin to the NW waves of the
+// workgroup; for each finished column tile `epi(ct, acc)` receives the RT
+// accumulator fragments.  Every wave of the workgroup must call this.
+template <class P, int RT, int NW, class Epi>
+__device__ __forceinline__ void dense_tiles(const typename P::T* X, int ldx, const DenseDev& L,
+                                            Epi&& epi) {
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int nct = L.dout_p / 16, nkb = L.din_p / P::KC;
+  const typename P::T* W = (const typename P::T*)L.w;
+  for (int ct = wave; ct < nct; ct += NW) {
+    typename P::C acc[RT];
+    for (int r = 0; r < RT; ++r)
+      for (int i = 0; i < 4; ++i) acc[r][i] = 0;
+    const typename P::T* wp = W + (size_t)ct * nkb * 64 * P::KPL + (size_t)lane * P::KPL;
+    const typename P::T* xp = X + (size_t)(lane & 15) * ldx + (lane >> 4) * P::KPL;
+    for (int kb = 0; kb < nkb; ++kb) {
+      typename P::Fr b = P::frag(wp + (size_t)kb * 64 * P::KPL);
+#pragma unroll
+      for (int r = 0; r < RT; ++r) {
+        typename P::Fr a = P::frag(xp + (size_t)r * 16 * ldx + kb * P::KC);
+        acc[r] = P::mfma(a, b, acc[r]);
+      }
+    }
+    epi(ct, acc);
+  }
+}

@@ -1,0 +1,724 @@
+// Host runtime of the C ABI: contexts, weight files, per-precision weight
+// packing, graph buffers and the orchestration of the graph and forward
+// kernels.  No arithmetic of the model runs here.
+#include <math.h>
+#include <stdio.h>
+#include <string.h>
+
+#include <fstream>
+#include <new>
+
+#include "internal.h"
+
+namespace {
+
+painn_status fail(painn_ctx* ctx, painn_status st, const std::string& msg) {
+  if (ctx) ctx->err = msg;
+  return st;
+}
+
+painn_status hip_fail(painn_ctx* ctx, hipError_t e, const char* what) {
+  return fail(ctx, PAINN_E_HIP, std::string(what) + ": " + hipGetErrorString(e));
+}
+
+#define HIP_TRY(ctx, expr)                                   \
+  do {                                                       \
+    hipError_t e_ = (expr);                                  \
+    if (e_ != hipSuccess) return hip_fail((ctx), e_, #expr); \
+  } while (0)
+
+// Grow a device buffer to hold at least `n` elements (contents not kept).
+template <typename T>
+hipError_t ensure(T** p, size_t* cap, size_t n) {
+  if (n <= *cap && *p) return hipSuccess;
+  if (*p) {
+    hipError_t e = hipFree(*p);
+    if (e != hipSuccess) return e;
+    *p = nullptr;
+  }
+  size_t want = n < 16 ? 16 : n + n / 4;
+  hipError_t e = hipMalloc((void**)p, want * sizeof(T));
+  if (e != hipSuccess) {
+    *cap = 0;
+    return e;
+  }
+  *cap = want;
+  return hipSuccess;
+}
+
+// Round-to-nearest-even of an FP64 value to bfloat16 (8 significant bits).
+bf16_t to_bf16(double x) {
+  if (isnan(x)) return 0x7FC0;
+  if (x == 0.0) return signbit(x) ? 0x8000 : 0x0000;
+  int e;
+  double m = frexp(x, &e);                      // x = m 2^e, 0.5 <= |m| < 1
+  double r = nearbyint(ldexp(m, 8));            // keep 8 significant bits, ties to even
+  float f = (float)ldexp(r, e - 8);             // exact (or inf / subnormal at the range ends)
+  uint32_t u;
+  memcpy(&u, &f, 4);
+  return (bf16_t)(u >> 16);
+}
+
+double bf16_value(bf16_t h) {
+  uint32_t u = (uint32_t)h << 16;
+  float f;
+  memcpy(&f, &u, 4);
+  return (double)f;
+}
+
+// Value of an FP64 weight after rounding to the precision's storage type.
+double stored(double x, int prec) {
+  if (prec == PAINN_FP64) return x;
+  if (prec == PAINN_FP32) return (double)(float)x;
+  return bf16_value(to_bf16(x));
+}
+
+size_t elem_bytes(int prec) { return prec == PAINN_FP64 ? 8 : prec == PAINN_FP32 ? 4 : 2; }
+size_t acc_bytes(int prec) { return prec == PAINN_FP64 ? 8 : 4; }
+
+// Write `vals` (doubles) to host bytes of the storage type.
+void put_storage(std::vector<unsigned char>& out, size_t idx, double x, int prec) {
+  if (prec == PAINN_FP64) {
+    memcpy(&out[idx * 8], &x, 8);
+  } else if (prec == PAINN_FP32) {
+    float f = (float)x;
+    memcpy(&out[idx * 4], &f, 4);
+  } else {
+    bf16_t h = to_bf16(x);
+    memcpy(&out[idx * 2], &h, 2);
+  }
+}
+
+void put_acc(std::vector<unsigned char>& out, size_t idx, double x, int prec) {
+  if (prec == PAINN_FP64) {
+    memcpy(&out[idx * 8], &x, 8);
+  } else {
+    float f = (float)x;
+    memcpy(&out[idx * 4], &f, 4);
+  }
+}
+
+hipError_t upload(PrecModel* pm, const std::vector<unsigned char>& host, void** dst) {
+  hipError_t e = hipMalloc(dst, host.size() ? host.size() : 16);
+  if (e != hipSuccess) return e;
+  pm->allocs.push_back(*dst);
+  if (host.empty()) return hipSuccess;
+  return hipMemcpy(*dst, host.data(), host.size(), hipMemcpyHostToDevice);
+}
+
+// Pack W [dout][din] (FP64, row-major) and bias [dout] (or null) for `prec`.
+hipError_t pack_dense(PrecModel* pm, int prec, const double* W, const double* b, int dout,
+                      int din, DenseDev* out) {
+  const int KC = prec == PAINN_BF16 ? 32 : 4;
+  const int KPL = KC / 4;
+  const int dout_p = pad32(dout), din_p = pad32(din);
+  const int nkb = din_p / KC, nct = dout_p / 16;
+  std::vector<unsigned char> wh((size_t)dout_p * din_p * elem_bytes(prec), 0);
+  for (int ct = 0; ct < nct; ++ct)
+    for (int kb = 0; kb < nkb; ++kb)
+      for (int l = 0; l < 64; ++l)
+        for (int e = 0; e < KPL; ++e) {
+          int row = 16 * ct + l % 16, k = KC * kb + KPL * (l / 16) + e;
+          double x = (row < dout && k < din) ? W[(size_t)row * din + k] : 0.0;
+          size_t idx = (((size_t)ct * nkb + kb) * 64 + l) * KPL + e;
+          put_storage(wh, idx, x, prec);
+        }
+  std::vector<unsigned char> bh((size_t)dout_p * acc_bytes(prec), 0);
+  for (int r = 0; r < dout; ++r) put_acc(bh, r, b ? stored(b[r], prec) : 0.0, prec);
+  out->din = din;
+  out->dout = dout;
+  out->din_p = din_p;
+  out->dout_p = dout_p;
+  hipError_t e = upload(pm, wh, &out->w);
+  if (e != hipSuccess) return e;
+  return upload(pm, bh, &out->b);
+}
+
+void free_prec(PrecModel* pm) {
+  if (!pm) return;
+  for (void* p : pm->allocs) (void)hipFree(p);
+  delete pm;
+}
+
+// Names of the per-layer arrays in file order.
+enum { A_PHI_W1, A_PHI_B1, A_PHI_W2, A_PHI_B2, A_FILT_W, A_FILT_B, A_U, A_V,
+       A_UPD_W1, A_UPD_B1, A_UPD_W2, A_UPD_B2, A_PER_LAYER };
+
+painn_status build_prec(painn_model* m, int prec, PrecModel** out) {
+  painn_ctx* ctx = m->ctx;
+  const Hyper& hp = m->hp;
+  const int F = hp.F, K = hp.K;
+  PrecModel* pm = new (std::nothrow) PrecModel();
+  if (!pm) return fail(ctx, PAINN_E_OOM, "host allocation failed");
+  pm->prec = prec;
+  const double* M = m->master.data();
+  auto arr = [&](size_t i) { return M + m->offsets[i]; };
+  hipError_t e = hipSuccess;
+  {
+    std::vector<unsigned char> h((size_t)hp.n_species * F * elem_bytes(prec));
+    for (size_t i = 0; i < (size_t)hp.n_species * F; ++i) put_storage(h, i, arr(0)[i], prec);
+    e = upload(pm, h, &pm->emb);
+  }
+  pm->layers.resize(hp.L);
+  for (int l = 0; l < hp.L && e == hipSuccess; ++l) {
+    size_t base = 1 + (size_t)A_PER_LAYER * l;
+    LayerDev& L = pm->layers[l];
+    e = pack_dense(pm, prec, arr(base + A_PHI_W1), arr(base + A_PHI_B1), F, F, &L.phi1);
+    if (e == hipSuccess)
+      e = pack_dense(pm, prec, arr(base + A_PHI_W2), arr(base + A_PHI_B2), 3 * F, F, &L.phi2);
+    if (e == hipSuccess) {
+      std::vector<double> uv((size_t)2 * F * F);
+      memcpy(uv.data(), arr(base + A_U), sizeof(double) * F * F);
+      memcpy(uv.data() + (size_t)F * F, arr(base + A_V), sizeof(double) * F * F);
+      e = pack_dense(pm, prec, uv.data(), nullptr, 2 * F, F, &L.uv);
+    }
+    if (e == hipSuccess)
+      e = pack_dense(pm, prec, arr(base + A_UPD_W1), arr(base + A_UPD_B1), F, 2 * F, &L.upd1);
+    if (e == hipSuccess)
+      e = pack_dense(pm, prec, arr(base + A_UPD_W2), arr(base + A_UPD_B2), 3 * F, F, &L.upd2);
+    if (e == hipSuccess) {
+      const int KP = filter_kp(K);
+      std::vector<unsigned char> h((size_t)3 * F * (KP + 1) * acc_bytes(prec), 0);
+      for (int c = 0; c < 3 * F; ++c) {
+        for (int k = 0; k < K; ++k)
+          put_acc(h, (size_t)c * (KP + 1) + k, stored(arr(base + A_FILT_W)[(size_t)c * K + k], prec), prec);
+        put_acc(h, (size_t)c * (KP + 1) + KP, stored(arr(base + A_FILT_B)[c], prec), prec);
+      }
+      e = upload(pm, h, &L.filt);
+    }
+  }
+  size_t idx = 1 + (size_t)A_PER_LAYER * hp.L;
+  int din = F;
+  for (size_t mm = 0; mm < hp.shared_dims.size() && e == hipSuccess; ++mm) {
+    DenseDev d;
+    e = pack_dense(pm, prec, arr(idx), arr(idx + 1), hp.shared_dims[mm], din, &d);
+    pm->shared.push_back(d);
+    din = hp.shared_dims[mm];
+    idx += 2;
+  }
+  pm->branch.resize(hp.n_heads);
+  for (int h = 0; h < hp.n_heads && e == hipSuccess; ++h) {
+    int di = din;
+    for (size_t mm = 0; mm < hp.branch_dims.size() && e == hipSuccess; ++mm) {
+      DenseDev d;
+      e = pack_dense(pm, prec, arr(idx), arr(idx + 1), hp.branch_dims[mm], di, &d);
+      pm->branch[h].push_back(d);
+      di = hp.branch_dims[mm];
+      idx += 2;
+    }
+  }
+  if (e == hipSuccess) {
+    const size_t nb = hp.branch_dims.size();
+    std::vector<unsigned char> tab((size_t)hp.n_heads * nb * 2 * sizeof(void*));
+    void** tp = (void**)tab.data();
+    for (int h = 0; h < hp.n_heads; ++h)
+      for (size_t mm = 0; mm < nb; ++mm) {
+        tp[(h * nb + mm) * 2] = pm->branch[h][mm].w;
+        tp[(h * nb + mm) * 2 + 1] = pm->branch[h][mm].b;
+      }
+    e = upload(pm, tab, &pm->head_table);
+  }
+  if (e != hipSuccess) {
+    free_prec(pm);
+    return hip_fail(ctx, e, "uploading packed weights");
+  }
+  *out = pm;
+  return PAINN_OK;
+}
+
+painn_status parse_model(painn_ctx* ctx, const unsigned char* buf, size_t n, painn_model** out) {
+  if (n < 48 || memcmp(buf, "PAINNW01", 8) != 0)
+    return fail(ctx, PAINN_E_FORMAT, "weight file: bad magic or truncated header");
+  int32_t h[8];
+  memcpy(h, buf + 8, sizeof(h));
+  Hyper hp;
+  hp.F = h[0]; hp.K = h[1]; hp.L = h[2]; hp.n_species = h[3]; hp.n_heads = h[4];
+  hp.rbf_type = h[5];
+  const int ns = h[6], nb = h[7];
+  memcpy(&hp.cutoff, buf + 40, 8);
+  if (ns < 0 || ns > 16 || nb < 1 || nb > 16)
+    return fail(ctx, PAINN_E_FORMAT, "weight file: bad head layer counts");
+  size_t off = 48;
+  if (n < off + 4 * (size_t)(ns + nb)) return fail(ctx, PAINN_E_FORMAT, "weight file: truncated");
+  for (int i = 0; i < ns; ++i) { int32_t d; memcpy(&d, buf + off, 4); off += 4; hp.shared_dims.push_back(d); }
+  for (int i = 0; i < nb; ++i) { int32_t d; memcpy(&d, buf + off, 4); off += 4; hp.branch_dims.push_back(d); }
+  off += (8 - off % 8) % 8;
+  if (hp.F != 64 && hp.F != 128 && hp.F != 256)
+    return fail(ctx, PAINN_E_UNSUPPORTED, "F must be 64, 128 or 256");
+  if (hp.K < 2 || hp.K > 64) return fail(ctx, PAINN_E_UNSUPPORTED, "K must be in [2, 64]");
+  if (hp.L < 1 || hp.L > 16) return fail(ctx, PAINN_E_UNSUPPORTED, "L must be in [1, 16]");
+  if (hp.n_species < 1 || hp.n_species > 1024) return fail(ctx, PAINN_E_FORMAT, "bad n_species");
+  if (hp.n_heads < 1 || hp.n_heads > 64) return fail(ctx, PAINN_E_UNSUPPORTED, "n_heads must be in [1, 64]");
+  if (hp.rbf_type != 0) return fail(ctx, PAINN_E_UNSUPPORTED, "only the Gaussian radial basis is implemented");
+  if (!(hp.cutoff > 0.0) || !isfinite(hp.cutoff)) return fail(ctx, PAINN_E_FORMAT, "bad cutoff");
+  for (int d : hp.shared_dims)
+    if (d < 1 || d > 1024) return fail(ctx, PAINN_E_UNSUPPORTED, "head widths must be in [1, 1024]");
+  for (int d : hp.branch_dims)
+    if (d < 1 || d > 1024) return fail(ctx, PAINN_E_UNSUPPORTED, "head widths must be in [1, 1024]");
+  if (hp.branch_dims.back() != 1) return fail(ctx, PAINN_E_FORMAT, "last branch layer must have width 1");
+  // array sizes in file order
+  std::vector<size_t> sizes;
+  const size_t F = hp.F, K = hp.K;
+  sizes.push_back(hp.n_species * F);
+  for (int l = 0; l < hp.L; ++l) {
+    size_t per[A_PER_LAYER] = {F * F, F, 3 * F * F, 3 * F, 3 * F * K, 3 * F, F * F, F * F,
+                               2 * F * F, F, 3 * F * F, 3 * F};
+    for (size_t s : per) sizes.push_back(s);
+  }
+  size_t din = F;
+  for (int d : hp.shared_dims) { sizes.push_back((size_t)d * din); sizes.push_back(d); din = d; }
+  for (int hh = 0; hh < hp.n_heads; ++hh) {
+    size_t di = din;
+    for (int d : hp.branch_dims) { sizes.push_back((size_t)d * di); sizes.push_back(d); di = d; }
+  }
+  size_t total = 0;
+  for (size_t s : sizes) total += s;
+  if (n != off + 8 * total)
+    return fail(ctx, PAINN_E_FORMAT, "weight file: size does not match its header");
+  painn_model* m = new (std::nothrow) painn_model();
+  if (!m) return fail(ctx, PAINN_E_OOM, "host allocation failed");
+  m->ctx = ctx;
+  m->hp = hp;
+  m->master.resize(total);
+  memcpy(m->master.data(), buf + off, 8 * total);
+  size_t o = 0;
+  for (size_t s : sizes) { m->offsets.push_back(o); o += s; }
+  for (double x : m->master)
+    if (!isfinite(x)) { delete m; return fail(ctx, PAINN_E_FORMAT, "weight file: non-finite weight"); }
+  *out = m;
+  return PAINN_OK;
+}
+
+}  // namespace
+
+size_t forward_workspace_bytes(int prec, int N, int F) {
+  const size_t eb = elem_bytes(prec), ab = acc_bytes(prec);
+  auto al = [](size_t x) { return (x + 255) & ~(size_t)255; };
+  size_t n = (size_t)N;
+  return al(n * F * eb) + 3 * al(n * 3 * F * eb) + al(n * ab) + 256;
+}
+
+
+// ---- per-kernel event timing ------------------------------------------------
+struct Profiler {
+  bool on = false;
+  std::vector<hipEvent_t> pool;
+  struct Rec { int kc; hipEvent_t a, b; };
+  std::vector<Rec> recs;
+  hipEvent_t open[KC_COUNT] = {};
+  double ms[KC_COUNT] = {};
+  long long launches[KC_COUNT] = {};
+};
+
+static const char* kc_name(int kc) {
+  static const char* names[KC_COUNT] = {"graph_prep", "graph_count", "graph_scan", "graph_fill",
+                                        "embed", "phi", "message", "update", "heads", "energy",
+                                        "export"};
+  return names[kc];
+}
+
+void prof_mark(Profiler* p, hipStream_t s, int kc, bool begin) {
+  if (!p || !p->on) return;
+  hipEvent_t ev;
+  if (p->pool.empty()) {
+    if (hipEventCreate(&ev) != hipSuccess) return;
+  } else {
+    ev = p->pool.back();
+    p->pool.pop_back();
+  }
+  if (hipEventRecord(ev, s) != hipSuccess) {
+    p->pool.push_back(ev);
+    return;
+  }
+  if (begin) {
+    if (p->open[kc]) p->pool.push_back(p->open[kc]);
+    p->open[kc] = ev;
+  } else if (p->open[kc]) {
+    p->recs.push_back({kc, p->open[kc], ev});
+    p->open[kc] = nullptr;
+  } else {
+    p->pool.push_back(ev);
+  }
+}
+
+static void prof_collect(Profiler* p) {
+  for (auto& r : p->recs) {
+    float t = 0.f;
+    if (hipEventElapsedTime(&t, r.a, r.b) == hipSuccess) {
+      p->ms[r.kc] += t;
+      p->launches[r.kc] += 1;
+    }
+    p->pool.push_back(r.a);
+    p->pool.push_back(r.b);
+  }
+  p->recs.clear();
+}
+
+static void prof_free(Profiler* p) {
+  if (!p) return;
+  for (auto& r : p->recs) { (void)hipEventDestroy(r.a); (void)hipEventDestroy(r.b); }
+  for (hipEvent_t e : p->pool) (void)hipEventDestroy(e);
+  for (hipEvent_t e : p->open) if (e) (void)hipEventDestroy(e);
+  delete p;
+}
+
+extern "C" {
+
+const char* painn_status_string(int st) {
+  switch (st) {
+    case PAINN_OK: return "PAINN_OK";
+    case PAINN_E_ARG: return "PAINN_E_ARG";
+    case PAINN_E_OOM: return "PAINN_E_OOM";
+    case PAINN_E_HIP: return "PAINN_E_HIP";
+    case PAINN_E_FILE: return "PAINN_E_FILE";
+    case PAINN_E_FORMAT: return "PAINN_E_FORMAT";
+    case PAINN_E_SPECIES: return "PAINN_E_SPECIES";
+    case PAINN_E_COINCIDENT: return "PAINN_E_COINCIDENT";
+    case PAINN_E_UNSUPPORTED: return "PAINN_E_UNSUPPORTED";
+    default: return "PAINN_E_UNKNOWN";
+  }
+}
+
+painn_status painn_create(int device, void* stream, painn_ctx** out) {
+  if (!out) return PAINN_E_ARG;
+  *out = nullptr;
+  int n = 0;
+  if (hipGetDeviceCount(&n) != hipSuccess || device < 0 || device >= n) return PAINN_E_ARG;
+  if (hipSetDevice(device) != hipSuccess) return PAINN_E_HIP;
+  painn_ctx* ctx = new (std::nothrow) painn_ctx();
+  if (!ctx) return PAINN_E_OOM;
+  ctx->device = device;
+  ctx->stream = (hipStream_t)stream;
+  if (hipHostMalloc((void**)&ctx->h_status, sizeof(DevStatus), hipHostMallocDefault) != hipSuccess) {
+    delete ctx;
+    return PAINN_E_OOM;
+  }
+  *out = ctx;
+  return PAINN_OK;
+}
+
+painn_status painn_set_stream(painn_ctx* ctx, void* stream) {
+  if (!ctx) return PAINN_E_ARG;
+  ctx->stream = (hipStream_t)stream;
+  ctx->err.clear();
+  return PAINN_OK;
+}
+
+painn_status painn_destroy(painn_ctx* ctx) {
+  if (!ctx) return PAINN_OK;
+  (void)hipSetDevice(ctx->device);
+  (void)hipStreamSynchronize(ctx->stream);
+  if (ctx->ws) (void)hipFree(ctx->ws);
+  if (ctx->h_status) (void)hipHostFree(ctx->h_status);
+  prof_free(ctx->prof);
+  delete ctx;
+  return PAINN_OK;
+}
+
+const char* painn_last_error(const painn_ctx* ctx) { return ctx ? ctx->err.c_str() : "null context"; }
+
+painn_status painn_synchronize(painn_ctx* ctx) {
+  if (!ctx) return PAINN_E_ARG;
+  (void)hipSetDevice(ctx->device);
+  HIP_TRY(ctx, hipStreamSynchronize(ctx->stream));
+  return PAINN_OK;
+}
+
+painn_status painn_model_load_buffer(painn_ctx* ctx, const void* data, size_t nbytes,
+                                     painn_model** out) {
+  if (!ctx || !data || !out) return fail(ctx, PAINN_E_ARG, "null argument");
+  *out = nullptr;
+  ctx->err.clear();
+  return parse_model(ctx, (const unsigned char*)data, nbytes, out);
+}
+
+painn_status painn_model_load(painn_ctx* ctx, const char* path, painn_model** out) {
+  if (!ctx || !path || !out) return fail(ctx, PAINN_E_ARG, "null argument");
+  *out = nullptr;
+  std::ifstream f(path, std::ios::binary);
+  if (!f) return fail(ctx, PAINN_E_FILE, std::string("cannot open ") + path);
+  std::vector<unsigned char> buf((std::istreambuf_iterator<char>(f)), std::istreambuf_iterator<char>());
+  if (f.bad()) return fail(ctx, PAINN_E_FILE, std::string("cannot read ") + path);
+  return painn_model_load_buffer(ctx, buf.data(), buf.size(), out);
+}
+
+painn_status painn_model_info(const painn_model* m, int32_t* F, int32_t* K, int32_t* L,
+                              int32_t* n_species, int32_t* n_heads, double* cutoff) {
+  if (!m) return PAINN_E_ARG;
+  if (F) *F = m->hp.F;
+  if (K) *K = m->hp.K;
+  if (L) *L = m->hp.L;
+  if (n_species) *n_species = m->hp.n_species;
+  if (n_heads) *n_heads = m->hp.n_heads;
+  if (cutoff) *cutoff = m->hp.cutoff;
+  return PAINN_OK;
+}
+
+painn_status painn_model_free(painn_model* m) {
+  if (!m) return PAINN_OK;
+  if (m->ctx) {
+    (void)hipSetDevice(m->ctx->device);
+    (void)hipStreamSynchronize(m->ctx->stream);
+  }
+  for (PrecModel* pm : m->prec) free_prec(pm);
+  delete m;
+  return PAINN_OK;
+}
+
+painn_status painn_graph_free(painn_graph* g) {
+  if (!g) return PAINN_OK;
+  if (g->ctx) {
+    (void)hipSetDevice(g->ctx->device);
+    (void)hipStreamSynchronize(g->ctx->stream);
+  }
+  void* bufs[] = {g->row_ptr, g->counts, g->col, g->shift, g->pos, g->species, g->atom_struct,
+                  g->cell, g->sinfo, g->struct_ptr, g->scan_tmp, g->d_status};
+  for (void* p : bufs)
+    if (p) (void)hipFree(p);
+  delete g;
+  return PAINN_OK;
+}
+
+painn_status painn_build_graph(painn_ctx* ctx, int32_t B, int32_t N, const int32_t* struct_ptr,
+                               const double* pos, const int32_t* species, const double* cell,
+                               const uint8_t* pbc, double cutoff, painn_graph** inout) {
+  if (!ctx) return PAINN_E_ARG;
+  ctx->err.clear();
+  if (!inout) return fail(ctx, PAINN_E_ARG, "inout is null");
+  if (B < 0 || N < 0) return fail(ctx, PAINN_E_ARG, "negative size");
+  if (B == 0 && N != 0) return fail(ctx, PAINN_E_ARG, "atoms given without structures");
+  if (!struct_ptr || (N > 0 && (!pos || !species)))
+    return fail(ctx, PAINN_E_ARG, "null input pointer");
+  if (pbc && !cell) return fail(ctx, PAINN_E_ARG, "pbc given without cell");
+  if (!(cutoff > 0.0) || !isfinite(cutoff)) return fail(ctx, PAINN_E_ARG, "cutoff must be finite and > 0");
+  (void)hipSetDevice(ctx->device);
+  painn_graph* g = *inout;
+  bool fresh = false;
+  if (!g) {
+    g = new (std::nothrow) painn_graph();
+    if (!g) return fail(ctx, PAINN_E_OOM, "host allocation failed");
+    g->ctx = ctx;
+    fresh = true;
+  }
+  auto bail = [&](painn_status st, const std::string& msg) {
+    if (fresh) painn_graph_free(g);
+    return fail(ctx, st, msg);
+  };
+  g->B = B;
+  g->N = N;
+  g->cutoff = cutoff;
+  g->any_pbc = pbc != nullptr;
+  hipError_t e = hipSuccess;
+  size_t capa = g->cap_atoms, caps = g->cap_struct, capsc = g->cap_scan;
+  // per-atom buffers share one capacity
+  if (N + 1 > (long long)g->cap_atoms || !g->row_ptr) {
+    size_t c0 = 0, c1 = 0, c2 = 0, c3 = 0, c4 = 0;
+    if (g->row_ptr) { (void)hipFree(g->row_ptr); g->row_ptr = nullptr; }
+    if (g->counts) { (void)hipFree(g->counts); g->counts = nullptr; }
+    if (g->pos) { (void)hipFree(g->pos); g->pos = nullptr; }
+    if (g->species) { (void)hipFree(g->species); g->species = nullptr; }
+    if (g->atom_struct) { (void)hipFree(g->atom_struct); g->atom_struct = nullptr; }
+    e = ensure(&g->row_ptr, &c0, (size_t)N + 1);
+    if (e == hipSuccess) e = ensure(&g->counts, &c1, c0);
+    if (e == hipSuccess) e = ensure(&g->pos, &c2, 3 * c0);
+    if (e == hipSuccess) e = ensure(&g->species, &c3, c0);
+    if (e == hipSuccess) e = ensure(&g->atom_struct, &c4, c0);
+    capa = c0;
+  }
+  if (e == hipSuccess && (B + 1 > (long long)g->cap_struct || !g->sinfo)) {
+    size_t c0 = 0, c1 = 0, c2 = 0;
+    if (g->sinfo) { (void)hipFree(g->sinfo); g->sinfo = nullptr; }
+    if (g->cell) { (void)hipFree(g->cell); g->cell = nullptr; }
+    if (g->struct_ptr) { (void)hipFree(g->struct_ptr); g->struct_ptr = nullptr; }
+    e = ensure(&g->sinfo, &c0, (size_t)B + 1);
+    if (e == hipSuccess) e = ensure(&g->cell, &c1, 9 * c0);
+    if (e == hipSuccess) e = ensure(&g->struct_ptr, &c2, c0);
+    caps = c0;
+  }
+  size_t nblk = ((size_t)N + 1023) / 1024 + 1;
+  if (e == hipSuccess) e = ensure(&g->scan_tmp, &capsc, nblk);
+  if (e == hipSuccess && !g->d_status) e = hipMalloc((void**)&g->d_status, sizeof(DevStatus));
+  if (e != hipSuccess) return bail(PAINN_E_OOM, std::string("device allocation: ") + hipGetErrorString(e));
+  g->cap_atoms = capa;
+  g->cap_struct = caps;
+  g->cap_scan = capsc;
+
+  (void)hipGetLastError();   // do not report an error left by earlier, unrelated calls
+  e = launch_graph_prep(ctx->stream, ctx->prof, B, N, struct_ptr, pos, species, cell, pbc, cutoff, g);
+  if (e == hipSuccess) e = launch_graph_count(ctx->stream, ctx->prof, g);
+  if (e == hipSuccess) e = launch_graph_scan(ctx->stream, ctx->prof, g);
+  if (e == hipSuccess)
+    e = hipMemcpyAsync(ctx->h_status, g->d_status, sizeof(DevStatus), hipMemcpyDeviceToHost, ctx->stream);
+  if (e == hipSuccess) e = hipStreamSynchronize(ctx->stream);
+  if (e != hipSuccess) {
+    (void)hipGetLastError();
+    return bail(PAINN_E_HIP, std::string("graph build: ") + hipGetErrorString(e));
+  }
+  DevStatus st = *ctx->h_status;
+  if (st.err) {
+    std::string msg;
+    painn_status code = PAINN_E_ARG;
+    if (st.err & ERR_STRUCT_PTR) msg += "struct_ptr is not a partition of [0, n_atoms); ";
+    if (st.err & ERR_CELL) msg += "singular or non-finite periodic cell; ";
+    if (st.err & ERR_IMAGES) msg += "periodic image range too large; ";
+    if (st.err & ERR_EDGES) msg += "more than 2^31-1 edges; ";
+    if (st.err & ERR_COINCIDENT) {
+      msg += "coincident atoms (distance 0); ";
+      if (!(st.err & ~ERR_COINCIDENT)) code = PAINN_E_COINCIDENT;
+    }
+    g->E = 0;
+    return bail(code, msg);
+  }
+  g->E = st.n_edges;
+  g->species_min = st.species_min;
+  g->species_max = st.species_max;
+  size_t cape = g->cap_edges;
+  if ((size_t)g->E > g->cap_edges || !g->col) {
+    size_t c2 = 0;
+    if (g->col) { (void)hipFree(g->col); g->col = nullptr; }
+    if (g->shift) { (void)hipFree(g->shift); g->shift = nullptr; }
+    e = ensure(&g->col, &cape, (size_t)g->E);
+    if (e == hipSuccess) e = ensure(&g->shift, &c2, cape);
+    if (e != hipSuccess) {
+      g->cap_edges = 0;
+      return bail(PAINN_E_OOM, std::string("edge allocation: ") + hipGetErrorString(e));
+    }
+    g->cap_edges = cape;
+  }
+  e = launch_graph_fill(ctx->stream, ctx->prof, g);
+  if (e != hipSuccess) {
+    (void)hipGetLastError();
+    return bail(PAINN_E_HIP, std::string("graph fill: ") + hipGetErrorString(e));
+  }
+  *inout = g;
+  return PAINN_OK;
+}
+
+painn_status painn_graph_csr(const painn_graph* g, int64_t* n_edges, int32_t* n_atoms,
+                             int32_t* n_struct, const int32_t** row_ptr, const int32_t** col,
+                             const int32_t** shift) {
+  if (!g) return PAINN_E_ARG;
+  if (n_edges) *n_edges = g->E;
+  if (n_atoms) *n_atoms = g->N;
+  if (n_struct) *n_struct = g->B;
+  if (row_ptr) *row_ptr = g->row_ptr;
+  if (col) *col = g->col;
+  if (shift) *shift = g->shift;
+  return PAINN_OK;
+}
+
+static painn_status run_forward(painn_ctx* ctx, const painn_model* model, const painn_graph* g,
+                                const int32_t* dataset_id, painn_precision prec, int stop_layer,
+                                double* energies, double* s_out, double* v_out) {
+  if (!ctx) return PAINN_E_ARG;
+  ctx->err.clear();
+  if (!model || !g) return fail(ctx, PAINN_E_ARG, "null model or graph");
+  if (model->ctx != ctx || g->ctx != ctx) return fail(ctx, PAINN_E_ARG, "model or graph from another context");
+  if (prec != PAINN_FP64 && prec != PAINN_FP32 && prec != PAINN_BF16)
+    return fail(ctx, PAINN_E_ARG, "unknown precision");
+  if (g->cutoff != model->hp.cutoff)
+    return fail(ctx, PAINN_E_ARG, "graph cutoff differs from the model's cutoff");
+  if (g->N > 0 && (g->species_min < 0 || g->species_max >= model->hp.n_species))
+    return fail(ctx, PAINN_E_SPECIES, "species index outside [0, n_species)");
+  (void)hipSetDevice(ctx->device);
+  painn_model* m = const_cast<painn_model*>(model);
+  if (!m->prec[prec]) {
+    painn_status st = build_prec(m, prec, &m->prec[prec]);
+    if (st != PAINN_OK) return st;
+  }
+  size_t need = forward_workspace_bytes(prec, g->N, m->hp.F);
+  if (need > ctx->ws_bytes) {
+    if (ctx->ws) {
+      (void)hipStreamSynchronize(ctx->stream);
+      (void)hipFree(ctx->ws);
+      ctx->ws = nullptr;
+      ctx->ws_bytes = 0;
+    }
+    size_t want = need + need / 4;
+    hipError_t e = hipMalloc(&ctx->ws, want);
+    if (e != hipSuccess) return fail(ctx, PAINN_E_OOM, "forward workspace allocation failed");
+    ctx->ws_bytes = want;
+  }
+  ForwardArgs a{};
+  a.m = m;
+  a.pm = m->prec[prec];
+  a.g = g;
+  a.dataset_id = dataset_id;
+  a.energies = energies;
+  a.stop_layer = stop_layer;
+  a.prof = ctx->prof;
+  a.s_out = s_out;
+  a.v_out = v_out;
+  // carve the workspace
+  const size_t eb = elem_bytes(prec), ab = acc_bytes(prec);
+  const size_t N = g->N, F = m->hp.F;
+  auto al = [](size_t x) { return (x + 255) & ~(size_t)255; };
+  char* p = (char*)ctx->ws;
+  a.s = p; p += al(N * F * eb);
+  a.v[0] = p; p += al(N * 3 * F * eb);
+  a.v[1] = p; p += al(N * 3 * F * eb);
+  a.h = p; p += al(N * 3 * F * eb);
+  a.e = p; p += al(N * ab);
+  if (g->B == 0 && !s_out) return PAINN_OK;
+  (void)hipGetLastError();   // do not report an error left by earlier, unrelated calls
+  hipError_t e = launch_forward(ctx->stream, prec, a);
+  if (e != hipSuccess) {
+    (void)hipGetLastError();  // leave no sticky error for the caller's next HIP call
+    return hip_fail(ctx, e, "forward launch");
+  }
+  return PAINN_OK;
+}
+
+painn_status painn_forward(painn_ctx* ctx, const painn_model* model, const painn_graph* graph,
+                           const int32_t* dataset_id, painn_precision precision, double* energies) {
+  if (ctx && graph && graph->B > 0 && !energies) return fail(ctx, PAINN_E_ARG, "energies is null");
+  return run_forward(ctx, model, graph, dataset_id, precision, model ? model->hp.L - 1 : 0,
+                     energies, nullptr, nullptr);
+}
+
+painn_status painn_forward_features(painn_ctx* ctx, const painn_model* model,
+                                    const painn_graph* graph, painn_precision precision,
+                                    int32_t layer, double* s_out, double* v_out) {
+  if (!ctx) return PAINN_E_ARG;
+  if (!model || !graph) return fail(ctx, PAINN_E_ARG, "null model or graph");
+  if (layer < -1 || layer >= model->hp.L) return fail(ctx, PAINN_E_ARG, "layer out of range");
+  if (graph->N > 0 && (!s_out || !v_out)) return fail(ctx, PAINN_E_ARG, "null output");
+  return run_forward(ctx, model, graph, nullptr, precision, layer, nullptr, s_out, v_out);
+}
+
+painn_status painn_profile_enable(painn_ctx* ctx, int enable) {
+  if (!ctx) return PAINN_E_ARG;
+  ctx->err.clear();
+  if (!ctx->prof) {
+    ctx->prof = new (std::nothrow) Profiler();
+    if (!ctx->prof) return fail(ctx, PAINN_E_OOM, "host allocation failed");
+  }
+  ctx->prof->on = enable != 0;
+  return PAINN_OK;
+}
+
+painn_status painn_profile_read(painn_ctx* ctx, int32_t n_max, const char** names, double* ms,
+                                int64_t* launches, int32_t* n_out) {
+  if (!ctx || n_max < 0 || (n_max > 0 && (!names || !ms || !launches)) || !n_out)
+    return fail(ctx, PAINN_E_ARG, "bad profile_read arguments");
+  ctx->err.clear();
+  *n_out = 0;
+  if (!ctx->prof) return PAINN_OK;
+  (void)hipSetDevice(ctx->device);
+  HIP_TRY(ctx, hipStreamSynchronize(ctx->stream));
+  prof_collect(ctx->prof);
+  int n = 0;
+  for (int k = 0; k < KC_COUNT && n < n_max; ++k) {
+    if (!ctx->prof->launches[k]) continue;
+    names[n] = kc_name(k);
+    ms[n] = ctx->prof->ms[k];
+    launches[n] = ctx->prof->launches[k];
+    ++n;
+  }
+  for (int k = 0; k < KC_COUNT; ++k) { ctx->prof->ms[k] = 0; ctx->prof->launches[k] = 0; }
+  *n_out = n;
+  return PAINN_OK;
+}
+
+}  // extern "C"
+

@@ -1,0 +1,152 @@
+"""GPU radius graph vs the oracle: the CSR (row_ptr, col, shift) must be
+bit-exact, including its order (receiver, sender, shift)."""
+import sys
+
+import numpy as np
+import pytest
+
+import synth
+from oracle.neighbors import batch_graph, radius_graph
+
+pytestmark = pytest.mark.gpu
+
+
+@pytest.fixture(scope="module")
+def rt():
+    from paper_2604_15380_amd import Runtime
+    r = Runtime(0)
+    yield r
+    r.close()
+
+
+def say(msg):
+    print(msg, flush=True)
+    sys.stdout.flush()
+
+
+def gpu_csr(rt, batch, cutoff):
+    g = rt.build_graph(rt.upload_batch(batch), cutoff)
+    try:
+        return g.csr()
+    finally:
+        g.free()
+
+
+def assert_same_csr(got, want):
+    rp, col, sh = got
+    wrp, wcol, wsh = want
+    assert np.array_equal(rp, wrp)
+    assert np.array_equal(col, wcol)
+    assert np.array_equal(sh, wsh)
+
+
+@pytest.mark.parametrize("name", ["tiny_molecules", "molecules_4096"])
+def test_molecules_full_batch(rt, name):
+    say(f"graph parity {name}")
+    b = synth.make_batch(name)
+    rc = synth.WORKLOADS[name]["cutoff"]
+    assert_same_csr(gpu_csr(rt, b, rc), batch_graph(b, rc))
+
+
+def test_bulk_full_batch_sampled_rows(rt):
+    """All 1024 periodic cells built at once; rows of 40 sampled structures
+    compared with the oracle's per-structure graphs."""
+    name = "bulk_1024"
+    say(f"graph parity {name}")
+    b = synth.make_batch(name)
+    rc = synth.WORKLOADS[name]["cutoff"]
+    rp, col, sh = gpu_csr(rt, b, rc)
+    assert rp[-1] == len(col)
+    rng = np.random.default_rng(0)
+    for s in sorted(set(rng.choice(b.n_struct, 40, replace=False).tolist()) | {0, b.n_struct - 1}):
+        lo, hi = int(b.struct_ptr[s]), int(b.struct_ptr[s + 1])
+        pos, z, cell, pbc, _ = b.structure(s)
+        recv, send, shift = radius_graph(pos, cell, pbc, rc)
+        e0, e1 = rp[lo], rp[hi]
+        assert e1 - e0 == len(recv), s
+        counts = np.bincount(recv, minlength=hi - lo)
+        assert np.array_equal(np.diff(rp[lo:hi + 1]), counts)
+        assert np.array_equal(col[e0:e1], send + lo)
+        assert np.array_equal(sh[e0:e1], shift)
+    # ~50-70 neighbours per atom with all images (a stated property of this workload)
+    assert 50 <= len(col) / b.n_atoms <= 90
+
+
+def test_screening_first_batch(rt):
+    name = "screening"
+    say(f"graph parity {name} first batch")
+    start, cnt = synth.screening_batches(3000)[0]
+    b = synth.make_batch(name, start, cnt)
+    rc = synth.WORKLOADS[name]["cutoff"]
+    assert_same_csr(gpu_csr(rt, b, rc), batch_graph(b, rc))
+
+
+def test_tiny_triclinic_slabs_and_edge_cases(rt):
+    say("graph parity: triclinic cells, slabs, empty and single-atom structures")
+    rng = np.random.default_rng(5)
+    structs = []
+    for k in range(24):
+        cell = np.eye(3) * (2.4 + rng.random()) + rng.uniform(-0.7, 0.7, (3, 3))
+        n = int(rng.integers(1, 6))
+        pos = rng.random((n, 3)) @ cell
+        if k % 5 == 0:
+            pos[0] += 3 * cell[1] - 2 * cell[2]        # outside the home cell
+        pbc = np.array([1, 1, k % 2], np.uint8)
+        structs.append((pos, rng.integers(0, 4, n), cell, pbc, 0))
+    structs.insert(3, (np.zeros((0, 3)), np.zeros(0, np.int32), np.eye(3) * 5, np.ones(3, np.uint8), 0))
+    structs.insert(7, (np.array([[0.1, 0.2, 0.3]]), np.array([1]), np.zeros((3, 3)), np.zeros(3, np.uint8), 0))
+    structs.append((np.zeros((0, 3)), np.zeros(0, np.int32), np.zeros((3, 3)), np.zeros(3, np.uint8), 0))
+    b = synth.concat(structs)
+    assert_same_csr(gpu_csr(rt, b, 4.3), batch_graph(b, 4.3))
+
+
+def test_rebuild_in_place_and_cutoff_boundary(rt):
+    say("graph rebuild in place")
+    b1 = synth.make_batch("molecules_4096", 0, 300)
+    b2 = synth.make_batch("tiny_molecules")
+    g = rt.build_graph(rt.upload_batch(b1), 5.0)
+    try:
+        assert_same_csr(g.csr(), batch_graph(b1, 5.0))
+        rt.build_graph(rt.upload_batch(b2), 5.0, graph=g)
+        assert_same_csr(g.csr(), batch_graph(b2, 5.0))
+        # exactly r_c apart: not an edge; one ulp closer: an edge
+        pair = synth.concat([(np.array([[0.0, 0, 0], [5.0, 0, 0]]), np.array([0, 1]), np.zeros((3, 3)),
+                              np.zeros(3, np.uint8), 0),
+                             (np.array([[0.0, 0, 0], [np.nextafter(5.0, 0), 0, 0]]), np.array([0, 1]),
+                              np.zeros((3, 3)), np.zeros(3, np.uint8), 0)])
+        rt.build_graph(rt.upload_batch(pair), 5.0, graph=g)
+        rp, col, sh = g.csr()
+        assert list(rp) == [0, 0, 0, 1, 2] and list(col) == [3, 2]
+    finally:
+        g.free()
+
+
+def test_errors(rt):
+    from paper_2604_15380_amd import PainnError
+    say("graph error paths")
+    # coincident atoms
+    b = synth.concat([(np.array([[0.0, 0, 0], [1.0, 0, 0], [0.0, 0, 0]]), np.array([0, 1, 2]),
+                       np.zeros((3, 3)), np.zeros(3, np.uint8), 0)])
+    with pytest.raises(PainnError, match="COINCIDENT"):
+        gpu_csr(rt, b, 5.0)
+    # an atom on a periodic image of another
+    b = synth.concat([(np.array([[0.0, 0, 0], [3.0, 0, 0]]), np.array([0, 1]), np.eye(3) * 3,
+                       np.ones(3, np.uint8), 0)])
+    with pytest.raises(PainnError, match="COINCIDENT"):
+        gpu_csr(rt, b, 2.0)
+    # singular periodic cell
+    b = synth.concat([(np.array([[0.0, 0, 0], [1.0, 0, 0]]), np.array([0, 1]), np.zeros((3, 3)),
+                       np.ones(3, np.uint8), 0)])
+    with pytest.raises(PainnError, match="E_ARG"):
+        gpu_csr(rt, b, 2.0)
+    # malformed struct_ptr
+    good = synth.make_batch("tiny_molecules")
+    inp = rt.upload_batch(good)
+    inp["struct_ptr"][3] = 1000
+    with pytest.raises(PainnError, match="E_ARG"):
+        rt.build_graph(inp, 5.0)
+    # non-positive cutoff
+    with pytest.raises(PainnError, match="E_ARG"):
+        rt.build_graph(rt.upload_batch(good), 0.0)
+    # the context still works after errors
+    assert_same_csr(gpu_csr(rt, good, 5.0), batch_graph(good, 5.0))
