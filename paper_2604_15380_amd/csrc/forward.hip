@@ -49,14 +49,14 @@ __device__ __forceinline__ void phi_tile(const typename P::T* X, int ldx, typena
   using A = typename P::A;
   constexpr int LD = F + P::PAD;
   const int lane = threadIdx.x & 63;
-  dense_tiles<P, RT, 4>(X, ldx, d1, [&](int ct, typename P::C* acc) {
+  dense_tiles<P, RT, 4, F / P::KC>(X, ldx, d1, [&](int ct, typename P::C* acc) {
     const int col = ct * 16 + (lane & 15);
     const A bias = ((const A*)d1.b)[col];
     for (int r = 0; r < RT; ++r)
       for (int i = 0; i < 4; ++i) H[(r * 16 + P::row(lane, i)) * LD + col] = P::st(silu<A>(acc[r][i] + bias));
   });
   __syncthreads();
-  dense_tiles<P, RT, 4>(H, LD, d2, [&](int ct, typename P::C* acc) {
+  dense_tiles<P, RT, 4, F / P::KC>(H, LD, d2, [&](int ct, typename P::C* acc) {
     const int col = ct * 16 + (lane & 15);
     const A bias = ((const A*)d2.b)[col];
     for (int r = 0; r < RT; ++r)
@@ -80,126 +80,219 @@ __global__ void __launch_bounds__(256) k_phi(int N, const typename P::T* __restr
 }
 
 // -------------------------------------------------------------- message ----
-// One workgroup of F threads per receiver i; thread f owns channel f of
-// every part.  Per edge e = (i <- j, n):
-//   w_e = f_c(d) (Wf g(d) + bf)                 filter, 3F channels
+// Per edge e = (i <- j, n) and channel c:
+//   w_e = f_c(d) (Wf g(d) + bf)                         radial filter, 3F channels
 //   ds_i    += h^s_j w^s_e
 //   dv_i[c] += v_j[c] h^v_j w^v_e + rhat[c] h^r_j w^r_e
-// The K Gaussians times f_c of a chunk of edges are computed once per edge
-// (spread over the workgroup) into LDS and broadcast; the filter rows live in
-// registers.  The sum over the receiver's edges is a plain in-register
-// reduction (the CSR is sorted by receiver), so there are no atomics and the
-// result is deterministic.
+// summed per receiver (the CSR is sorted by receiver, so this is a plain
+// in-register reduction: no atomics, deterministic).
+//
+// The filter runs on the matrix cores: for 16 edges of one receiver
+//   Wt[16 edges, 3F] = Gh[16, K+1] [Wf | bf]^T,
+//   Gh[e] = (f_c g_0(d_e), ..., f_c g_{K-1}(d_e), f_c(d_e))
+// (the bias column carries f_c, so Wt = f_c (Wf g + bf)).  Gh does not depend
+// on the layer: k_edge_prep writes it once per forward, in the MFMA operand
+// type (BF16 as two terms [hi | lo] against the filter stored twice along K),
+// next to each edge's rhat and sender index.
 struct MsgArgs {
   int N, F, K;
   const int32_t* row_ptr;
-  const int32_t* col;
-  const int32_t* shift;
-  const int32_t* atom_struct;
-  const double* pos;
-  const double* cell;
-  double rc, gamma, delta;
-  const void* filt;  // [3F][KP+1], accumulation type, column KP = bias
+  const void* basis;   // [E + 16][kcols] storage type (16 zero rows of padding)
+  const void* einfo;   // [E][4] accumulation type: rhat x, y, z, sender index
+  DenseDev filt_mma;   // the filter packed for MFMA (K+1 -> 3F, or 2(K+1) for BF16)
   const void* h;
   const void* v_in;
   void* s;
   void* v_out;
 };
 
-constexpr int MSG_CH = 64;  // edges per chunk
+constexpr int MSG_RB = 4;   // receivers per workgroup (MSG_RB < 64)
 
-template <class P, int KP>
-__global__ void __launch_bounds__(256) k_message(MsgArgs a) {
+// An int32 carried in an accumulation-type slot: its bits in a float, its
+// value in a double.
+template <class A>
+__device__ __forceinline__ A index_to_acc(int j) {
+  if constexpr (sizeof(A) == 4) return __int_as_float(j);
+  else return (A)j;
+}
+__device__ __forceinline__ int acc_to_index(float x) { return __float_as_int(x); }
+__device__ __forceinline__ int acc_to_index(double x) { return (int)x; }
+
+// Once per forward: geometry and radial basis of every edge.
+//   r = (x_j - x_i) + (n0 a + n1 b) + n2 c  (FP64),  d = |r|,  rhat = r / d,
+//   f_c = (cos(pi d / r_c) + 1) / 2,  g_k = exp(-gamma (d - k Delta)^2).
+template <class P>
+__global__ void __launch_bounds__(256) k_edge_prep(long long E, int K, int kcols, double rc,
+                                                  double gamma, double delta,
+                                                  const int32_t* __restrict__ recv,
+                                                  const int32_t* __restrict__ col,
+                                                  const int32_t* __restrict__ shift,
+                                                  const int32_t* __restrict__ atom_struct,
+                                                  const double* __restrict__ pos,
+                                                  const double* __restrict__ cell,
+                                                  typename P::T* __restrict__ basis,
+                                                  typename P::A* __restrict__ einfo) {
   using T = typename P::T;
   using A = typename P::A;
-  constexpr int RS = KP + 4;  // LDS row: KP Gaussians, f_c, 3 zeros
-  __shared__ __attribute__((aligned(16))) A eg[MSG_CH * RS];
-  __shared__ A er[MSG_CH * 4];
-  __shared__ int ej[MSG_CH];
-  const int i = blockIdx.x;
-  const int f = threadIdx.x;
-  const int F = a.F;
-  const A* filt = (const A*)a.filt;
-  A wS[KP + 1], wV[KP + 1], wR[KP + 1];
-#pragma unroll
-  for (int k = 0; k <= KP; ++k) {
-    wS[k] = filt[(size_t)f * (KP + 1) + k];
-    wV[k] = filt[(size_t)(F + f) * (KP + 1) + k];
-    wR[k] = filt[(size_t)(2 * F + f) * (KP + 1) + k];
+  constexpr bool SPLIT = P::KC == 32;
+  const long long e = blockIdx.x * (long long)blockDim.x + threadIdx.x;
+  if (e >= E + 16) return;
+  T* g = basis + (size_t)e * kcols;
+  if (e >= E) {                                  // padding rows read by partial chunks
+    for (int k = 0; k < kcols; ++k) g[k] = P::st(0);
+    return;
   }
+  const int i = recv[e], j = col[e], sh = shift[e];
+  const double* Cl = cell + 9 * atom_struct[i];
+  const double n0 = (double)(int8_t)(sh & 0xff), n1 = (double)(int8_t)((sh >> 8) & 0xff),
+               n2 = (double)(int8_t)((sh >> 16) & 0xff);
+  const double rx = (pos[3 * j] - pos[3 * i]) + ((n0 * Cl[0] + n1 * Cl[3]) + n2 * Cl[6]);
+  const double ry = (pos[3 * j + 1] - pos[3 * i + 1]) + ((n0 * Cl[1] + n1 * Cl[4]) + n2 * Cl[7]);
+  const double rz = (pos[3 * j + 2] - pos[3 * i + 2]) + ((n0 * Cl[2] + n1 * Cl[5]) + n2 * Cl[8]);
+  const double d = sqrt(rx * rx + ry * ry + rz * rz);
+  const double inv = 1.0 / d;
+  A* o = einfo + 4 * e;
+  o[0] = (A)(rx * inv);
+  o[1] = (A)(ry * inv);
+  o[2] = (A)(rz * inv);
+  o[3] = index_to_acc<A>(j);                     // the sender index, bit-exact
+  const A dd = (A)d;
+  const A fc = (A)(d < rc ? 0.5 * (cos(d * (3.14159265358979323846 / rc)) + 1.0) : 0.0);
+  for (int k = 0; k < kcols; ++k) {
+    const bool lo = SPLIT && k > K;
+    const int kk = lo ? k - (K + 1) : k;
+    A val = 0;
+    if (kk < K) {
+      const A t = dd - (A)(kk * delta);
+      val = P::ex(-(A)gamma * t * t) * fc;
+    } else if (kk == K) {
+      val = fc;
+    }
+    g[k] = lo ? P::st(val - P::ld(P::st(val))) : P::st(val);
+  }
+}
+
+// Per layer.  A workgroup owns MSG_RB consecutive receivers and NW waves;
+// wave w owns the feature tiles ft = w + NW q (q < FTW) and keeps their
+// filter B fragments (s, v and r column tiles) in registers.  Waves never
+// synchronise: each streams its receivers' 16-edge chunks (basis fragments ->
+// MFMA -> sender gathers), with the accumulator layout (row = edge, col =
+// channel) letting every lane combine the filter with the gathered sender
+// features of its edges directly; a receiver's per-lane partial sums are
+// reduced across the four row groups of the wavefront at its last edge.
+template <class P, int F, int NW, int KBM>
+__global__ void __launch_bounds__(NW * 64) k_message(MsgArgs a) {
+  using T = typename P::T;
+  using A = typename P::A;
+  using C = typename P::C;
+  using Fr = typename P::Fr;
+  constexpr int NFT = F / 16, FTW = NFT / NW;
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  constexpr int nkb = KBM;            // the filter input is padded to KBM k-blocks
+  constexpr int kcols = KBM * P::KC;
+  const T* Wf = (const T*)a.filt_mma.w;
+  Fr Bf[FTW][3][KBM];
+#pragma unroll
+  for (int q = 0; q < FTW; ++q)
+#pragma unroll
+    for (int part = 0; part < 3; ++part)
+#pragma unroll
+      for (int kb = 0; kb < KBM; ++kb) {
+        const int ct = part * NFT + wave + NW * q;
+        Bf[q][part][kb] = P::frag(Wf + ((size_t)(ct * nkb + kb) * 64 + lane) * P::KPL);
+      }
   const T* h = (const T*)a.h;
   const T* vin = (const T*)a.v_in;
-  const int b = a.atom_struct[i];
-  double C[9];
-  for (int k = 0; k < 9; ++k) C[k] = a.cell[9 * b + k];
-  const double xi = a.pos[3 * i], yi = a.pos[3 * i + 1], zi = a.pos[3 * i + 2];
-  const int e_begin = a.row_ptr[i], e_end = a.row_ptr[i + 1];
-  A acc_s = 0, acc_v0 = 0, acc_v1 = 0, acc_v2 = 0;
-  const double pi_rc = 3.14159265358979323846 / a.rc;
-  for (int e0 = e_begin; e0 < e_end; e0 += MSG_CH) {
-    const int cnt = min(MSG_CH, e_end - e0);
-    for (int t = f; t < cnt; t += F) {
-      const int e = e0 + t;
-      const int j = a.col[e];
-      const int sh = a.shift[e];
-      const double n0 = (double)(int8_t)(sh & 0xff), n1 = (double)(int8_t)((sh >> 8) & 0xff),
-                   n2 = (double)(int8_t)((sh >> 16) & 0xff);
-      const double rx = (a.pos[3 * j] - xi) + ((n0 * C[0] + n1 * C[3]) + n2 * C[6]);
-      const double ry = (a.pos[3 * j + 1] - yi) + ((n0 * C[1] + n1 * C[4]) + n2 * C[7]);
-      const double rz = (a.pos[3 * j + 2] - zi) + ((n0 * C[2] + n1 * C[5]) + n2 * C[8]);
-      const double d = sqrt(rx * rx + ry * ry + rz * rz);
-      const double inv = 1.0 / d;
-      er[4 * t + 0] = (A)(rx * inv);
-      er[4 * t + 1] = (A)(ry * inv);
-      er[4 * t + 2] = (A)(rz * inv);
-      er[4 * t + 3] = (A)d;
-      ej[t] = j;
-      const double fc = d < a.rc ? 0.5 * (cos(d * pi_rc) + 1.0) : 0.0;
-      eg[t * RS + KP] = (A)fc;
-      eg[t * RS + KP + 1] = 0;
-      eg[t * RS + KP + 2] = 0;
-      eg[t * RS + KP + 3] = 0;
-    }
-    __syncthreads();
-    for (int x = f; x < cnt * KP; x += F) {
-      const int t = x / KP, k = x % KP;
-      A g = 0;
-      if (k < a.K) {
-        const A dd = er[4 * t + 3] - (A)(k * a.delta);
-        g = P::ex(-(A)a.gamma * dd * dd) * eg[t * RS + KP];
-      }
-      eg[t * RS + k] = g;
-    }
-    __syncthreads();
-    for (int t = 0; t < cnt; ++t) {
-      const int j = ej[t];
-      const A* gp = eg + t * RS;
-      A ws = wS[KP] * gp[KP], wv = wV[KP] * gp[KP], wr = wR[KP] * gp[KP];
-#pragma unroll
-      for (int k = 0; k < KP; ++k) {
-        const A gk = gp[k];
-        ws += wS[k] * gk;
-        wv += wV[k] * gk;
-        wr += wR[k] * gk;
-      }
-      const size_t hb = (size_t)j * 3 * F;
-      const A hs = P::ld(h[hb + f]), hv = P::ld(h[hb + F + f]), hr = P::ld(h[hb + 2 * F + f]);
-      const A vj0 = P::ld(vin[hb + f]), vj1 = P::ld(vin[hb + F + f]), vj2 = P::ld(vin[hb + 2 * F + f]);
-      acc_s += hs * ws;
-      const A pv = hv * wv, pr = hr * wr;
-      acc_v0 += vj0 * pv + er[4 * t + 0] * pr;
-      acc_v1 += vj1 * pv + er[4 * t + 1] * pr;
-      acc_v2 += vj2 * pv + er[4 * t + 2] * pr;
-    }
-    __syncthreads();
-  }
+  const T* basis = (const T*)a.basis;
+  const A* einfo = (const A*)a.einfo;
   T* s = (T*)a.s;
   T* vout = (T*)a.v_out;
-  const size_t ib = (size_t)i * 3 * F;
-  s[(size_t)i * F + f] = P::st(P::ld(s[(size_t)i * F + f]) + acc_s);
-  vout[ib + f] = P::st(P::ld(vin[ib + f]) + acc_v0);
-  vout[ib + F + f] = P::st(P::ld(vin[ib + F + f]) + acc_v1);
-  vout[ib + 2 * F + f] = P::st(P::ld(vin[ib + 2 * F + f]) + acc_v2);
+  // Workgroups are dealt round-robin to the 8 XCDs.  Renumber them so each
+  // XCD walks one contiguous range of receivers: a molecule's receivers then
+  // share one L2, which serves the repeated gathers of its sender rows.
+  const int per_xcd = gridDim.x / 8;
+  const int lb = (blockIdx.x % 8) * per_xcd + blockIdx.x / 8;
+  const int i0 = lb * MSG_RB;
+  if (i0 >= a.N) return;
+  const int i1 = min(a.N, i0 + MSG_RB);
+  // the block's row_ptr slice, one load per lane, read back by shuffles
+  const int rp_lane = a.row_ptr[i0 + min(lane, i1 - i0)];
+  for (int i = i0; i < i1; ++i) {
+    const int ea = __shfl(rp_lane, i - i0);
+    const int eb = __shfl(rp_lane, i - i0 + 1);
+    // operands of the final update, fetched early
+    T s_old[FTW], v_old[FTW][3];
+    const size_t ib = (size_t)i * 3 * F;
+#pragma unroll
+    for (int q = 0; q < FTW; ++q) {
+      const int f = (wave + NW * q) * 16 + (lane & 15);
+      s_old[q] = s[(size_t)i * F + f];
+      v_old[q][0] = vin[ib + f];
+      v_old[q][1] = vin[ib + F + f];
+      v_old[q][2] = vin[ib + 2 * F + f];
+    }
+    A acc_s[FTW], acc_v[FTW][3];
+#pragma unroll
+    for (int q = 0; q < FTW; ++q) acc_s[q] = acc_v[q][0] = acc_v[q][1] = acc_v[q][2] = 0;
+    for (int c0 = ea; c0 < eb; c0 += 16) {
+      const int cnt = min(16, eb - c0);
+      const T* gp = basis + (size_t)(c0 + (lane & 15)) * kcols + (lane >> 4) * P::KPL;
+      Fr Ga[KBM];
+#pragma unroll
+      for (int kb = 0; kb < KBM; ++kb) Ga[kb] = P::frag(gp + kb * P::KC);
+      A rh[4][3];
+      int jj[4];
+#pragma unroll
+      for (int ii = 0; ii < 4; ++ii) {
+        const int row = P::row(lane, ii);
+        const A* ei = einfo + 4 * (size_t)(c0 + (row < cnt ? row : 0));
+        rh[ii][0] = ei[0];
+        rh[ii][1] = ei[1];
+        rh[ii][2] = ei[2];
+        jj[ii] = acc_to_index(ei[3]);
+      }
+#pragma unroll
+      for (int q = 0; q < FTW; ++q) {
+        const int f = (wave + NW * q) * 16 + (lane & 15);
+        C w[3];
+#pragma unroll
+        for (int part = 0; part < 3; ++part) {
+          for (int r = 0; r < 4; ++r) w[part][r] = 0;
+#pragma unroll
+          for (int kb = 0; kb < KBM; ++kb) w[part] = P::mfma(Ga[kb], Bf[q][part][kb], w[part]);
+        }
+#pragma unroll
+        for (int ii = 0; ii < 4; ++ii) {
+          if (P::row(lane, ii) < cnt) {
+            const size_t hb = (size_t)jj[ii] * 3 * F;
+            const A hs = P::ld(h[hb + f]), hv = P::ld(h[hb + F + f]), hr = P::ld(h[hb + 2 * F + f]);
+            const A v0 = P::ld(vin[hb + f]), v1 = P::ld(vin[hb + F + f]), v2 = P::ld(vin[hb + 2 * F + f]);
+            acc_s[q] += hs * w[0][ii];
+            const A pv = hv * w[1][ii], pr = hr * w[2][ii];
+            acc_v[q][0] += v0 * pv + rh[ii][0] * pr;
+            acc_v[q][1] += v1 * pv + rh[ii][1] * pr;
+            acc_v[q][2] += v2 * pv + rh[ii][2] * pr;
+          }
+        }
+      }
+    }
+#pragma unroll
+    for (int q = 0; q < FTW; ++q) {
+      for (int o = 16; o < 64; o *= 2) {
+        acc_s[q] += __shfl_xor(acc_s[q], o);
+        acc_v[q][0] += __shfl_xor(acc_v[q][0], o);
+        acc_v[q][1] += __shfl_xor(acc_v[q][1], o);
+        acc_v[q][2] += __shfl_xor(acc_v[q][2], o);
+      }
+      if (lane < 16) {
+        const int f = (wave + NW * q) * 16 + lane;
+        s[(size_t)i * F + f] = P::st(P::ld(s_old[q]) + acc_s[q]);
+        vout[ib + f] = P::st(P::ld(v_old[q][0]) + acc_v[q][0]);
+        vout[ib + F + f] = P::st(P::ld(v_old[q][1]) + acc_v[q][1]);
+        vout[ib + 2 * F + f] = P::st(P::ld(v_old[q][2]) + acc_v[q][2]);
+      }
+    }
+  }
 }
 
 // --------------------------------------------------------------- update ----
@@ -218,108 +311,138 @@ struct UpdArgs {
   DenseDev uv, upd1, upd2, phi1, phi2;
 };
 
-template <class P, int F, bool FUSE_PHI>
+template <class P, int F, int RT, bool FUSE_PHI>
 __global__ void __launch_bounds__(256) k_update(UpdArgs a) {
   using T = typename P::T;
   using A = typename P::A;
   using C = typename P::C;
+  using Fr = typename P::Fr;
   constexpr int NFT = F / 16;        // feature tiles
   constexpr int FTW = NFT / 4;       // per wave
+  constexpr int TM = 16 * RT;        // atoms per workgroup
   constexpr int LD1 = F + P::PAD, LD2 = 2 * F + P::PAD;
-  __shared__ __attribute__((aligned(16))) T VS[16 * LD1];   // v[c] slice, later the MLP hidden
-  __shared__ __attribute__((aligned(16))) T SN[16 * LD2];   // [s ; |V|]
+  __shared__ __attribute__((aligned(16))) T VS[TM * LD1];   // v[c] slice, later the MLP hidden
+  __shared__ __attribute__((aligned(16))) T SN[TM * LD2];   // [s ; |V|]
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-  const size_t row0 = (size_t)blockIdx.x * 16;
+  const size_t row0 = (size_t)blockIdx.x * TM;
   const int N = a.N;
   T* s = (T*)a.s;
   T* v = (T*)a.v;
-  for (int x = threadIdx.x; x < 16 * F; x += blockDim.x) {
+  for (int x = threadIdx.x; x < TM * F; x += blockDim.x) {
     const int r = x / F, c = x % F;
     SN[r * LD2 + c] = row0 + r < (size_t)N ? s[(row0 + r) * F + c] : P::st(0);
   }
-  C U[FTW][3], nsq[FTW], pd[FTW];
+  C U[FTW][3][RT], nsq[FTW][RT], pd[FTW][RT];
   for (int q = 0; q < FTW; ++q)
-    for (int i = 0; i < 4; ++i) nsq[q][i] = pd[q][i] = 0;
-  const int nkb = a.uv.din_p / P::KC;
+    for (int r = 0; r < RT; ++r)
+      for (int i = 0; i < 4; ++i) nsq[q][r][i] = pd[q][r][i] = 0;
+  constexpr int nkb = F / P::KC;
   const T* Wuv = (const T*)a.uv.w;
   for (int c = 0; c < 3; ++c) {
     __syncthreads();
-    for (int x = threadIdx.x; x < 16 * F; x += blockDim.x) {
+    for (int x = threadIdx.x; x < TM * F; x += blockDim.x) {
       const int r = x / F, col = x % F;
       VS[r * LD1 + col] = row0 + r < (size_t)N ? v[(row0 + r) * 3 * F + c * F + col] : P::st(0);
     }
     __syncthreads();
     const T* xp = VS + (lane & 15) * LD1 + (lane >> 4) * P::KPL;
+#pragma unroll
     for (int q = 0; q < FTW; ++q) {
       const int ft = wave + 4 * q;
-      C au, av;
-      for (int i = 0; i < 4; ++i) au[i] = av[i] = 0;
+      C au[RT], av[RT];
+      for (int r = 0; r < RT; ++r)
+        for (int i = 0; i < 4; ++i) au[r][i] = av[r][i] = 0;
       const T* wu = Wuv + (size_t)ft * nkb * 64 * P::KPL + (size_t)lane * P::KPL;
       const T* wv = Wuv + (size_t)(NFT + ft) * nkb * 64 * P::KPL + (size_t)lane * P::KPL;
+#pragma unroll P::UNROLL
       for (int kb = 0; kb < nkb; ++kb) {
-        typename P::Fr x = P::frag(xp + kb * P::KC);
-        au = P::mfma(x, P::frag(wu + (size_t)kb * 64 * P::KPL), au);
-        av = P::mfma(x, P::frag(wv + (size_t)kb * 64 * P::KPL), av);
+        const Fr bu = P::frag(wu + (size_t)kb * 64 * P::KPL);
+        const Fr bv = P::frag(wv + (size_t)kb * 64 * P::KPL);
+#pragma unroll
+        for (int r = 0; r < RT; ++r) {
+          const Fr x = P::frag(xp + r * 16 * LD1 + kb * P::KC);
+          au[r] = P::mfma(x, bu, au[r]);
+          av[r] = P::mfma(x, bv, av[r]);
+        }
       }
-      U[q][c] = au;
-      for (int i = 0; i < 4; ++i) {
-        nsq[q][i] += av[i] * av[i];
-        pd[q][i] += au[i] * av[i];
-      }
-    }
-  }
-  for (int q = 0; q < FTW; ++q) {
-    const int col = (wave + 4 * q) * 16 + (lane & 15);
-    for (int i = 0; i < 4; ++i) SN[(P::row(lane, i)) * LD2 + F + col] = P::st(sqrt(nsq[q][i]));
-  }
-  __syncthreads();
-  T* H = VS;
-  dense_tiles<P, 1, 4>(SN, LD2, a.upd1, [&](int ct, C* acc) {
-    const int col = ct * 16 + (lane & 15);
-    const A bias = ((const A*)a.upd1.b)[col];
-    for (int i = 0; i < 4; ++i) H[(P::row(lane, i)) * LD1 + col] = P::st(silu<A>(acc[0][i] + bias));
-  });
-  __syncthreads();
-  {
-    const int nkb2 = a.upd2.din_p / P::KC;
-    const T* W2 = (const T*)a.upd2.w;
-    const A* b2 = (const A*)a.upd2.b;
-    const T* xp = H + (lane & 15) * LD1 + (lane >> 4) * P::KPL;
-    for (int q = 0; q < FTW; ++q) {
-      const int ft = wave + 4 * q;
-      C avv, asv, ass;
-      for (int i = 0; i < 4; ++i) avv[i] = asv[i] = ass[i] = 0;
-      const T* w0 = W2 + (size_t)ft * nkb2 * 64 * P::KPL + (size_t)lane * P::KPL;
-      const T* w1 = W2 + (size_t)(NFT + ft) * nkb2 * 64 * P::KPL + (size_t)lane * P::KPL;
-      const T* w2 = W2 + (size_t)(2 * NFT + ft) * nkb2 * 64 * P::KPL + (size_t)lane * P::KPL;
-      for (int kb = 0; kb < nkb2; ++kb) {
-        typename P::Fr x = P::frag(xp + kb * P::KC);
-        avv = P::mfma(x, P::frag(w0 + (size_t)kb * 64 * P::KPL), avv);
-        asv = P::mfma(x, P::frag(w1 + (size_t)kb * 64 * P::KPL), asv);
-        ass = P::mfma(x, P::frag(w2 + (size_t)kb * 64 * P::KPL), ass);
-      }
-      const int col = ft * 16 + (lane & 15);
-      const A bvv = b2[col], bsv = b2[F + col], bss = b2[2 * F + col];
-      for (int i = 0; i < 4; ++i) {
-        const int r = P::row(lane, i);
-        const size_t row = row0 + r;
-        const A g_vv = avv[i] + bvv, g_sv = asv[i] + bsv, g_ss = ass[i] + bss;
-        const A sn = P::ld(SN[r * LD2 + col]) + g_sv * pd[q][i] + g_ss;
-        const T st = P::st(sn);
-        SN[r * LD2 + col] = st;
-        if (row < (size_t)N) {
-          s[row * F + col] = st;
-          for (int c = 0; c < 3; ++c) {
-            const size_t o = row * 3 * F + c * F + col;
-            v[o] = P::st(P::ld(v[o]) + g_vv * U[q][c][i]);
-          }
+#pragma unroll
+      for (int r = 0; r < RT; ++r) {
+        U[q][c][r] = au[r];
+        for (int i = 0; i < 4; ++i) {
+          nsq[q][r][i] += av[r][i] * av[r][i];
+          pd[q][r][i] += au[r][i] * av[r][i];
         }
       }
     }
   }
+#pragma unroll
+  for (int q = 0; q < FTW; ++q) {
+    const int col = (wave + 4 * q) * 16 + (lane & 15);
+    for (int r = 0; r < RT; ++r)
+      for (int i = 0; i < 4; ++i)
+        SN[(r * 16 + P::row(lane, i)) * LD2 + F + col] = P::st(sqrt(nsq[q][r][i]));
+  }
+  __syncthreads();
+  T* H = VS;
+  dense_tiles<P, RT, 4, 2 * F / P::KC>(SN, LD2, a.upd1, [&](int ct, C* acc) {
+    const int col = ct * 16 + (lane & 15);
+    const A bias = ((const A*)a.upd1.b)[col];
+    for (int r = 0; r < RT; ++r)
+      for (int i = 0; i < 4; ++i)
+        H[(r * 16 + P::row(lane, i)) * LD1 + col] = P::st(silu<A>(acc[r][i] + bias));
+  });
+  __syncthreads();
+  {
+    constexpr int nkb2 = F / P::KC;
+    const T* W2 = (const T*)a.upd2.w;
+    const A* b2 = (const A*)a.upd2.b;
+    const T* xp = H + (lane & 15) * LD1 + (lane >> 4) * P::KPL;
+#pragma unroll
+    for (int q = 0; q < FTW; ++q) {
+      const int ft = wave + 4 * q;
+      C avv[RT], asv[RT], ass[RT];
+      for (int r = 0; r < RT; ++r)
+        for (int i = 0; i < 4; ++i) avv[r][i] = asv[r][i] = ass[r][i] = 0;
+      const T* w0 = W2 + (size_t)ft * nkb2 * 64 * P::KPL + (size_t)lane * P::KPL;
+      const T* w1 = W2 + (size_t)(NFT + ft) * nkb2 * 64 * P::KPL + (size_t)lane * P::KPL;
+      const T* w2 = W2 + (size_t)(2 * NFT + ft) * nkb2 * 64 * P::KPL + (size_t)lane * P::KPL;
+#pragma unroll P::UNROLL
+      for (int kb = 0; kb < nkb2; ++kb) {
+        const Fr b0 = P::frag(w0 + (size_t)kb * 64 * P::KPL);
+        const Fr b1 = P::frag(w1 + (size_t)kb * 64 * P::KPL);
+        const Fr b2f = P::frag(w2 + (size_t)kb * 64 * P::KPL);
+#pragma unroll
+        for (int r = 0; r < RT; ++r) {
+          const Fr x = P::frag(xp + r * 16 * LD1 + kb * P::KC);
+          avv[r] = P::mfma(x, b0, avv[r]);
+          asv[r] = P::mfma(x, b1, asv[r]);
+          ass[r] = P::mfma(x, b2f, ass[r]);
+        }
+      }
+      const int col = ft * 16 + (lane & 15);
+      const A bvv = b2[col], bsv = b2[F + col], bss = b2[2 * F + col];
+#pragma unroll
+      for (int r = 0; r < RT; ++r)
+        for (int i = 0; i < 4; ++i) {
+          const int rr = r * 16 + P::row(lane, i);
+          const size_t row = row0 + rr;
+          const A g_vv = avv[r][i] + bvv, g_sv = asv[r][i] + bsv, g_ss = ass[r][i] + bss;
+          const A sn = P::ld(SN[rr * LD2 + col]) + g_sv * pd[q][r][i] + g_ss;
+          const T st = P::st(sn);
+          SN[rr * LD2 + col] = st;
+          if (row < (size_t)N) {
+            s[row * F + col] = st;
+            for (int c = 0; c < 3; ++c) {
+              const size_t o = row * 3 * F + c * F + col;
+              v[o] = P::st(P::ld(v[o]) + g_vv * U[q][c][r][i]);
+            }
+          }
+        }
+    }
+  }
   if (FUSE_PHI) {
     __syncthreads();
-    phi_tile<P, F, 1>(SN, LD2, VS, row0, N, a.phi1, a.phi2, (T*)a.h);
+    phi_tile<P, F, RT>(SN, LD2, VS, row0, N, a.phi1, a.phi2, (T*)a.h);
   }
 }
 
@@ -471,25 +594,174 @@ inline int grid_for(size_t n, int per) {
   return (int)(g ? g : 1);
 }
 
-template <class P, int KP>
-void launch_message_kp(hipStream_t st, const MsgArgs& a) {
-  k_message<P, KP><<<a.N, a.F, 0, st>>>(a);
+// Channel-per-lane form (FP32 / BF16 storage).  A workgroup of F/64 waves
+// owns MSG_RB2 consecutive receivers; wave w owns channels [64 w, 64 w + 64)
+// = feature tiles 4w..4w+3 and keeps their filter B fragments in registers.
+// Per 16-edge chunk the wave forms Wt for its channels on the matrix cores
+// and parks it in its own LDS tile (edge-major); then every lane, one
+// channel, walks the chunk's edges: the sender index is wave-uniform, so each
+// gather reads 256 contiguous bytes of a sender row, and the filter values
+// come back from LDS.  Sums stay in the lane (no cross-lane reduction) and no
+// wave waits for another.
+constexpr int MSG_RB2 = 8;
+
+template <class A>
+__device__ __forceinline__ A bcast(A x, int lane) {
+  if constexpr (sizeof(A) == 4) {
+    return __int_as_float(__builtin_amdgcn_readlane(__float_as_int(x), lane));
+  } else {
+    const long long b = __double_as_longlong(x);
+    const int lo = __builtin_amdgcn_readlane((int)(b & 0xffffffff), lane);
+    const int hi = __builtin_amdgcn_readlane((int)(b >> 32), lane);
+    return __longlong_as_double(((long long)hi << 32) | (unsigned)lo);
+  }
 }
 
-template <class P>
-hipError_t launch_message(hipStream_t st, int KP, const MsgArgs& a) {
-  switch (KP) {
-    case 4: launch_message_kp<P, 4>(st, a); break;
-    case 8: launch_message_kp<P, 8>(st, a); break;
-    case 12: launch_message_kp<P, 12>(st, a); break;
-    case 16: launch_message_kp<P, 16>(st, a); break;
-    case 20: launch_message_kp<P, 20>(st, a); break;
-    case 24: launch_message_kp<P, 24>(st, a); break;
-    case 32: launch_message_kp<P, 32>(st, a); break;
-    case 40: launch_message_kp<P, 40>(st, a); break;
-    case 48: launch_message_kp<P, 48>(st, a); break;
-    case 64: launch_message_kp<P, 64>(st, a); break;
-    default: return hipErrorInvalidValue;
+template <class P, int F, int KBM>
+__global__ void __launch_bounds__(F) k_message_lane(MsgArgs a) {
+  using T = typename P::T;
+  using A = typename P::A;
+  using C = typename P::C;
+  using Fr = typename P::Fr;
+  constexpr int NW = F / 64, NFT = F / 16;
+  constexpr int WLD = 64 + 4;                   // LDS row of one part, one edge
+  constexpr int kcols = KBM * P::KC;
+  __shared__ A Wt[NW][3][16 * WLD];
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int c = 64 * wave + lane;               // this lane's channel
+  const T* Wf = (const T*)a.filt_mma.w;
+  Fr Bf[4][3][KBM];
+#pragma unroll
+  for (int q = 0; q < 4; ++q)
+#pragma unroll
+    for (int part = 0; part < 3; ++part)
+#pragma unroll
+      for (int kb = 0; kb < KBM; ++kb) {
+        const int ct = part * NFT + 4 * wave + q;
+        Bf[q][part][kb] = P::frag(Wf + ((size_t)(ct * KBM + kb) * 64 + lane) * P::KPL);
+      }
+  const T* h = (const T*)a.h;
+  const T* vin = (const T*)a.v_in;
+  const T* basis = (const T*)a.basis;
+  const A* einfo = (const A*)a.einfo;
+  T* s = (T*)a.s;
+  T* vout = (T*)a.v_out;
+  A* wt0 = Wt[wave][0];
+  A* wt1 = Wt[wave][1];
+  A* wt2 = Wt[wave][2];
+  // XCD-contiguous receiver ranges (see k_message)
+  const int per_xcd = gridDim.x / 8;
+  const int lb = (blockIdx.x % 8) * per_xcd + blockIdx.x / 8;
+  const int i0 = lb * MSG_RB2;
+  if (i0 >= a.N) return;
+  const int i1 = min(a.N, i0 + MSG_RB2);
+  const int rp_lane = a.row_ptr[i0 + min(lane, i1 - i0)];
+  for (int i = i0; i < i1; ++i) {
+    const int ea = __builtin_amdgcn_readlane(rp_lane, i - i0);
+    const int eb = __builtin_amdgcn_readlane(rp_lane, i - i0 + 1);
+    const size_t ib = (size_t)i * 3 * F;
+    const T s_old = s[(size_t)i * F + c];
+    const T v_old0 = vin[ib + c], v_old1 = vin[ib + F + c], v_old2 = vin[ib + 2 * F + c];
+    A acc_s = 0, acc_v0 = 0, acc_v1 = 0, acc_v2 = 0;
+    for (int c0 = ea; c0 < eb; c0 += 16) {
+      const int cnt = min(16, eb - c0);
+      const T* gp = basis + (size_t)(c0 + (lane & 15)) * kcols + (lane >> 4) * P::KPL;
+      Fr Ga[KBM];
+#pragma unroll
+      for (int kb = 0; kb < KBM; ++kb) Ga[kb] = P::frag(gp + kb * P::KC);
+      // lanes e < cnt hold edge c0 + e: rhat and the sender index
+      A ex = 0, ey = 0, ez = 0, ej = 0;
+      if (lane < cnt) {
+        const A* ei = einfo + 4 * (size_t)(c0 + lane);
+        ex = ei[0];
+        ey = ei[1];
+        ez = ei[2];
+        ej = ei[3];
+      }
+#pragma unroll
+      for (int q = 0; q < 4; ++q) {
+        C w0, w1, w2;
+        for (int r = 0; r < 4; ++r) w0[r] = w1[r] = w2[r] = 0;
+#pragma unroll
+        for (int kb = 0; kb < KBM; ++kb) {
+          w0 = P::mfma(Ga[kb], Bf[q][0][kb], w0);
+          w1 = P::mfma(Ga[kb], Bf[q][1][kb], w1);
+          w2 = P::mfma(Ga[kb], Bf[q][2][kb], w2);
+        }
+        const int col = 16 * q + (lane & 15);
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+          const int row = P::row(lane, r);
+          wt0[row * WLD + col] = w0[r];
+          wt1[row * WLD + col] = w1[r];
+          wt2[row * WLD + col] = w2[r];
+        }
+      }
+      __builtin_amdgcn_wave_barrier();
+      __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+      __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+      for (int e4 = 0; e4 < cnt; e4 += 4)
+#pragma unroll
+      for (int u = 0; u < 4; ++u) {
+        const int e = e4 + u;
+        if (e >= cnt) break;
+        const int j = acc_to_index(bcast(ej, e));
+        const A rx = bcast(ex, e), ry = bcast(ey, e), rz = bcast(ez, e);
+        const T* hj = h + (size_t)j * 3 * F + c;
+        const T* vj = vin + (size_t)j * 3 * F + c;
+        const A hs = P::ld(hj[0]), hv = P::ld(hj[F]), hr = P::ld(hj[2 * F]);
+        const A v0 = P::ld(vj[0]), v1 = P::ld(vj[F]), v2 = P::ld(vj[2 * F]);
+        const A ws = wt0[e * WLD + lane], wv = wt1[e * WLD + lane], wr = wt2[e * WLD + lane];
+        acc_s += hs * ws;
+        const A pv = hv * wv, pr = hr * wr;
+        acc_v0 += v0 * pv + rx * pr;
+        acc_v1 += v1 * pv + ry * pr;
+        acc_v2 += v2 * pv + rz * pr;
+      }
+      __builtin_amdgcn_wave_barrier();
+      __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+      __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+    }
+    s[(size_t)i * F + c] = P::st(P::ld(s_old) + acc_s);
+    vout[ib + c] = P::st(P::ld(v_old0) + acc_v0);
+    vout[ib + F + c] = P::st(P::ld(v_old1) + acc_v1);
+    vout[ib + 2 * F + c] = P::st(P::ld(v_old2) + acc_v2);
+  }
+}
+
+template <class P, int F, int KBM>
+void launch_message_kbm(hipStream_t st, const MsgArgs& a) {
+  if constexpr (sizeof(typename P::T) == 8) {
+    constexpr int NW = F / 32;      // two feature tiles per wave
+    const int blocks = ((a.N + MSG_RB - 1) / MSG_RB + 7) / 8 * 8;   // a multiple of the 8 XCDs
+    k_message<P, F, NW, KBM><<<blocks, NW * 64, 0, st>>>(a);
+  } else {
+    const int blocks = ((a.N + MSG_RB2 - 1) / MSG_RB2 + 7) / 8 * 8;
+    k_message_lane<P, F, KBM><<<blocks, F, 0, st>>>(a);
+  }
+}
+
+// The filter's input is padded to one of the compiled k-block counts.
+template <class P, int F>
+hipError_t launch_message(hipStream_t st, const MsgArgs& a) {
+  const int nkb = a.filt_mma.din_p / P::KC;
+  if constexpr (P::KC == 32) {
+    switch (nkb) {
+      case 1: launch_message_kbm<P, F, 1>(st, a); break;
+      case 2: launch_message_kbm<P, F, 2>(st, a); break;
+      case 3: launch_message_kbm<P, F, 3>(st, a); break;
+      case 5: launch_message_kbm<P, F, 5>(st, a); break;
+      default: return hipErrorInvalidValue;
+    }
+  } else {
+    switch (nkb) {
+      case 3: launch_message_kbm<P, F, 3>(st, a); break;
+      case 6: launch_message_kbm<P, F, 6>(st, a); break;
+      case 9: launch_message_kbm<P, F, 9>(st, a); break;
+      case 12: launch_message_kbm<P, F, 12>(st, a); break;
+      case 17: launch_message_kbm<P, F, 17>(st, a); break;
+      default: return hipErrorInvalidValue;
+    }
   }
   return hipSuccess;
 }
@@ -503,6 +775,8 @@ hipError_t forward_impl(hipStream_t st, ForwardArgs& fa) {
   const Hyper& hp = fa.m->hp;
   const int N = g->N;
   constexpr int RT = (sizeof(T) == 8 && F == 256) ? 1 : 2;
+  // atoms per update tile / 16: U, |V|^2 and <U, V> of the tile live in registers
+  constexpr int URT = (F == 256 || (sizeof(T) == 8 && F == 128)) ? 1 : 2;
   T* s = (T*)fa.s;
   T* v[2] = {(T*)fa.v[0], (T*)fa.v[1]};
   T* h = (T*)fa.h;
@@ -518,7 +792,15 @@ hipError_t forward_impl(hipStream_t st, ForwardArgs& fa) {
     }
   }
   int cur = 0;
-  const int KP = filter_kp(hp.K);
+  const int kcols = pm->layers.empty() ? 0 : pm->layers[0].filt_mma.din_p;
+  if (N > 0 && fa.stop_layer >= 0) {
+    prof_mark(fa.prof, st, KC_EDGE_PREP, true);
+    const double delta = hp.cutoff / (hp.K - 1);
+    k_edge_prep<P><<<(unsigned)((g->E + 16 + 255) / 256), 256, 0, st>>>(
+        g->E, hp.K, kcols, hp.cutoff, 1.0 / (2.0 * delta * delta), delta, g->recv, g->col, g->shift,
+        g->atom_struct, g->pos, g->cell, (T*)fa.basis, (A*)fa.einfo);
+    prof_mark(fa.prof, st, KC_EDGE_PREP, false);
+  }
   for (int l = 0; l <= fa.stop_layer && N > 0; ++l) {
     const LayerDev& Ld = pm->layers[l];
     MsgArgs ma;
@@ -526,21 +808,15 @@ hipError_t forward_impl(hipStream_t st, ForwardArgs& fa) {
     ma.F = F;
     ma.K = hp.K;
     ma.row_ptr = g->row_ptr;
-    ma.col = g->col;
-    ma.shift = g->shift;
-    ma.atom_struct = g->atom_struct;
-    ma.pos = g->pos;
-    ma.cell = g->cell;
-    ma.rc = hp.cutoff;
-    ma.delta = hp.cutoff / (hp.K - 1);
-    ma.gamma = 1.0 / (2.0 * ma.delta * ma.delta);
-    ma.filt = Ld.filt;
+    ma.basis = fa.basis;
+    ma.einfo = fa.einfo;
+    ma.filt_mma = Ld.filt_mma;
     ma.h = h;
     ma.v_in = v[cur];
     ma.s = s;
     ma.v_out = v[cur ^ 1];
     prof_mark(fa.prof, st, KC_MESSAGE, true);
-    hipError_t e = launch_message<P>(st, KP, ma);
+    hipError_t e = launch_message<P, F>(st, ma);
     prof_mark(fa.prof, st, KC_MESSAGE, false);
     if (e != hipSuccess) return e;
     cur ^= 1;
@@ -557,9 +833,9 @@ hipError_t forward_impl(hipStream_t st, ForwardArgs& fa) {
     if (fuse) {
       ua.phi1 = pm->layers[l + 1].phi1;
       ua.phi2 = pm->layers[l + 1].phi2;
-      k_update<P, F, true><<<(N + 15) / 16, 256, 0, st>>>(ua);
+      k_update<P, F, URT, true><<<(N + 16 * URT - 1) / (16 * URT), 256, 0, st>>>(ua);
     } else {
-      k_update<P, F, false><<<(N + 15) / 16, 256, 0, st>>>(ua);
+      k_update<P, F, URT, false><<<(N + 16 * URT - 1) / (16 * URT), 256, 0, st>>>(ua);
     }
     prof_mark(fa.prof, st, KC_UPDATE, false);
   }

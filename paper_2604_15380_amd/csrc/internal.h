@@ -42,12 +42,19 @@ struct StructInfo {     // per structure: atom range and periodic image range
 // (FP64/FP32: KC = 4, KPL = 1; BF16: KC = 32, KPL = 8.)
 inline __host__ __device__ int pad32(int d) { return (d + 31) & ~31; }
 
-// Number of radial basis slots compiled into the message kernel for K basis
-// functions (the filter rows are zero-padded from K to this).
-inline int filter_kp(int K) {
-  const int opts[] = {4, 8, 12, 16, 20, 24, 32, 40, 48, 64};
-  for (int o : opts)
-    if (K <= o) return o;
+// MFMA k-blocks of the radial filter's input (K+1 basis columns, or 2(K+1)
+// for BF16), rounded up to the counts the message kernel is compiled for
+// (the padding columns are zero); -1 if too large.
+inline int filter_kblocks(int din, int prec) {
+  const int kc = prec == PAINN_BF16 ? 32 : 4;
+  const int need = (din + kc - 1) / kc;
+  static const int f[] = {3, 6, 9, 12, 17};
+  static const int b[] = {1, 2, 3, 5};
+  if (prec == PAINN_BF16) {
+    for (int x : b) if (need <= x) return x;
+  } else {
+    for (int x : f) if (need <= x) return x;
+  }
   return -1;
 }
 
@@ -61,8 +68,10 @@ struct LayerDev {       // one interaction layer
   DenseDev phi1, phi2;  // F -> F (silu), F -> 3F
   DenseDev uv;          // [U; V] stacked: F -> 2F
   DenseDev upd1, upd2;  // 2F -> F (silu), F -> 3F
-  void* filt = nullptr; // [3F][KP+1] accumulation type, KP = filter_kp(K):
-                        // columns K..KP-1 zero, column KP the bias
+  DenseDev filt_mma;    // radial filter as a dense layer K+1 -> 3F for MFMA:
+                        // input column K is the bias (multiplied by f_c), din
+                        // padded to a multiple of the MFMA K step only; BF16
+                        // stores it twice along K (input [hi | lo] terms)
 };
 
 struct PrecModel {      // the model cast and packed for one precision
@@ -84,7 +93,7 @@ struct Hyper {
 // ---- per-kernel event timing (painn_profile_*) ------------------------------
 enum KernelClass {
   KC_GRAPH_PREP, KC_GRAPH_COUNT, KC_GRAPH_SCAN, KC_GRAPH_FILL, KC_EMBED, KC_PHI,
-  KC_MESSAGE, KC_UPDATE, KC_HEADS, KC_ENERGY, KC_EXPORT, KC_COUNT
+  KC_EDGE_PREP, KC_MESSAGE, KC_UPDATE, KC_HEADS, KC_ENERGY, KC_EXPORT, KC_COUNT
 };
 struct Profiler;
 // Record the start (begin = true) or end of a kernel of class `kc` on `s`;
@@ -120,6 +129,7 @@ struct painn_graph {
   // device buffers (capacities in elements)
   int32_t* row_ptr = nullptr;  int32_t* counts = nullptr;
   int32_t* col = nullptr;      int32_t* shift = nullptr;
+  int32_t* recv = nullptr;     // receiver of each edge (the CSR row, expanded)
   double* pos = nullptr;       int32_t* species = nullptr;
   int32_t* atom_struct = nullptr;
   double* cell = nullptr;      StructInfo* sinfo = nullptr;
@@ -148,10 +158,12 @@ struct ForwardArgs {
   void* v[2];   // [N][3][F] storage, double buffered
   void* h;      // [N][3F] storage
   void* e;      // [N] accumulation type
+  void* basis;           // [E + 16][kcols] storage type: radial basis rows
+  void* einfo;           // [E][4] accumulation type: rhat, sender index
   int stop_layer;          // run layers 0..stop_layer (forward: L-1)
   Profiler* prof;
   double* s_out;           // feature export (may be null)
   double* v_out;
 };
-size_t forward_workspace_bytes(int prec, int N, int F);
+size_t forward_workspace_bytes(int prec, int N, long long E, int F, int kcols);
 hipError_t launch_forward(hipStream_t s, int prec, ForwardArgs& a);

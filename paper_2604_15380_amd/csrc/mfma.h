@@ -34,7 +34,7 @@ struct P64 {
   using A = double;  // accumulation
   using C = d4_t;
   using Fr = double;
-  static constexpr int KC = 4, KPL = 1, PAD = 2, PREC = PAINN_FP64;
+  static constexpr int KC = 4, KPL = 1, PAD = 2, PREC = PAINN_FP64, UNROLL = 8;
   __device__ static __forceinline__ Fr frag(const T* p) { return *p; }
   __device__ static __forceinline__ C mfma(Fr a, Fr b, C c) {
     return __builtin_amdgcn_mfma_f64_16x16x4f64(a, b, c, 0, 0, 0);
@@ -50,7 +50,7 @@ struct P32 {
   using A = float;
   using C = f4_t;
   using Fr = float;
-  static constexpr int KC = 4, KPL = 1, PAD = 4, PREC = PAINN_FP32;
+  static constexpr int KC = 4, KPL = 1, PAD = 4, PREC = PAINN_FP32, UNROLL = 8;
   __device__ static __forceinline__ Fr frag(const T* p) { return *p; }
   __device__ static __forceinline__ C mfma(Fr a, Fr b, C c) {
     return __builtin_amdgcn_mfma_f32_16x16x4f32(a, b, c, 0, 0, 0);
@@ -66,7 +66,7 @@ struct PB16 {
   using A = float;
   using C = f4_t;
   using Fr = bf8_t;
-  static constexpr int KC = 32, KPL = 8, PAD = 8, PREC = PAINN_BF16;
+  static constexpr int KC = 32, KPL = 8, PAD = 8, PREC = PAINN_BF16, UNROLL = 2;
   __device__ static __forceinline__ Fr frag(const T* p) { return *(const bf8_t*)p; }
   __device__ static __forceinline__ C mfma(Fr a, Fr b, C c) {
     return __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, b, c, 0, 0, 0);
@@ -86,11 +86,12 @@ __device__ __forceinline__ A silu(A x) {
 // ldx elements).  Column tiles are dealt round-robin to the NW waves of the
 // workgroup; for each finished column tile `epi(ct, acc)` receives the RT
 // accumulator fragments.  Every wave of the workgroup must call this.
-template <class P, int RT, int NW, class Epi>
+// NKB > 0 fixes the number of K blocks (din_p / KC) at compile time.
+template <class P, int RT, int NW, int NKB = 0, class Epi>
 __device__ __forceinline__ void dense_tiles(const typename P::T* X, int ldx, const DenseDev& L,
                                             Epi&& epi) {
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-  const int nct = L.dout_p / 16, nkb = L.din_p / P::KC;
+  const int nct = L.dout_p / 16, nkb = NKB > 0 ? NKB : L.din_p / P::KC;
   const typename P::T* W = (const typename P::T*)L.w;
   for (int ct = wave; ct < nct; ct += NW) {
     typename P::C acc[RT];
@@ -98,13 +99,20 @@ __device__ __forceinline__ void dense_tiles(const typename P::T* X, int ldx, con
       for (int i = 0; i < 4; ++i) acc[r][i] = 0;
     const typename P::T* wp = W + (size_t)ct * nkb * 64 * P::KPL + (size_t)lane * P::KPL;
     const typename P::T* xp = X + (size_t)(lane & 15) * ldx + (lane >> 4) * P::KPL;
-    for (int kb = 0; kb < nkb; ++kb) {
+    auto step = [&](int kb) {
       typename P::Fr b = P::frag(wp + (size_t)kb * 64 * P::KPL);
 #pragma unroll
       for (int r = 0; r < RT; ++r) {
         typename P::Fr a = P::frag(xp + (size_t)r * 16 * ldx + kb * P::KC);
         acc[r] = P::mfma(a, b, acc[r]);
       }
+    };
+    if constexpr (NKB > 0) {
+      // several weight fragments in flight ahead of their MFMAs
+#pragma unroll P::UNROLL
+      for (int kb = 0; kb < NKB; ++kb) step(kb);
+    } else {
+      for (int kb = 0; kb < nkb; ++kb) step(kb);
     }
     epi(ct, acc);
   }

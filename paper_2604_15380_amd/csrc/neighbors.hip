@@ -215,6 +215,7 @@ __global__ void __launch_bounds__(256) k_edges(painn_graph g, double rc2) {
         int pre = __popcll(mask & ((1ull << lane) - 1ull));
         g.col[out + pre] = c.j;
         g.shift[out + pre] = c.packed;
+        g.recv[out + pre] = i;
       }
       out += __popcll(mask);
     } else {

@@ -107,11 +107,12 @@ hipError_t upload(PrecModel* pm, const std::vector<unsigned char>& host, void** 
 }
 
 // Pack W [dout][din] (FP64, row-major) and bias [dout] (or null) for `prec`.
+// din_p: pad32(din), or filter_kblocks(din, prec) MFMA k-blocks for the radial filter.
 hipError_t pack_dense(PrecModel* pm, int prec, const double* W, const double* b, int dout,
-                      int din, DenseDev* out) {
+                      int din, DenseDev* out, bool filter = false) {
   const int KC = prec == PAINN_BF16 ? 32 : 4;
   const int KPL = KC / 4;
-  const int dout_p = pad32(dout), din_p = pad32(din);
+  const int dout_p = pad32(dout), din_p = filter ? filter_kblocks(din, prec) * KC : pad32(din);
   const int nkb = din_p / KC, nct = dout_p / 16;
   std::vector<unsigned char> wh((size_t)dout_p * din_p * elem_bytes(prec), 0);
   for (int ct = 0; ct < nct; ++ct)
@@ -177,14 +178,23 @@ painn_status build_prec(painn_model* m, int prec, PrecModel** out) {
     if (e == hipSuccess)
       e = pack_dense(pm, prec, arr(base + A_UPD_W2), arr(base + A_UPD_B2), 3 * F, F, &L.upd2);
     if (e == hipSuccess) {
-      const int KP = filter_kp(K);
-      std::vector<unsigned char> h((size_t)3 * F * (KP + 1) * acc_bytes(prec), 0);
+      // [Wf | bf] as one K+1 -> 3F layer; its input row is [f_c g_0 .. f_c g_{K-1}, f_c]
+      std::vector<double> wf((size_t)3 * F * (K + 1));
       for (int c = 0; c < 3 * F; ++c) {
-        for (int k = 0; k < K; ++k)
-          put_acc(h, (size_t)c * (KP + 1) + k, stored(arr(base + A_FILT_W)[(size_t)c * K + k], prec), prec);
-        put_acc(h, (size_t)c * (KP + 1) + KP, stored(arr(base + A_FILT_B)[c], prec), prec);
+        for (int k = 0; k < K; ++k) wf[(size_t)c * (K + 1) + k] = arr(base + A_FILT_W)[(size_t)c * K + k];
+        wf[(size_t)c * (K + 1) + K] = arr(base + A_FILT_B)[c];
       }
-      e = upload(pm, h, &L.filt);
+      if (prec == PAINN_BF16) {
+        // BF16 feeds the basis as hi + lo bf16 terms: the layer sees the
+        // input [hi | lo] (2K+2 columns) and the filter twice along K.
+        std::vector<double> w2((size_t)3 * F * 2 * (K + 1));
+        for (int c = 0; c < 3 * F; ++c)
+          for (int k = 0; k < 2 * (K + 1); ++k)
+            w2[(size_t)c * 2 * (K + 1) + k] = wf[(size_t)c * (K + 1) + k % (K + 1)];
+        e = pack_dense(pm, prec, w2.data(), nullptr, 3 * F, 2 * (K + 1), &L.filt_mma, true);
+      } else {
+        e = pack_dense(pm, prec, wf.data(), nullptr, 3 * F, K + 1, &L.filt_mma, true);
+      }
     }
   }
   size_t idx = 1 + (size_t)A_PER_LAYER * hp.L;
@@ -291,11 +301,15 @@ painn_status parse_model(painn_ctx* ctx, const unsigned char* buf, size_t n, pai
 
 }  // namespace
 
-size_t forward_workspace_bytes(int prec, int N, int F) {
+// Workspace of one forward pass, carved in this order: s [N][F], v[0], v[1],
+// h [N][3F] (storage type), e [N] (accumulation type), the radial basis rows
+// [E + 16][kcols] (storage type) and the edge info [E][4] (accumulation type).
+size_t forward_workspace_bytes(int prec, int N, long long E, int F, int kcols) {
   const size_t eb = elem_bytes(prec), ab = acc_bytes(prec);
   auto al = [](size_t x) { return (x + 255) & ~(size_t)255; };
-  size_t n = (size_t)N;
-  return al(n * F * eb) + 3 * al(n * 3 * F * eb) + al(n * ab) + 256;
+  const size_t n = (size_t)N, ne = (size_t)E;
+  return al(n * F * eb) + 3 * al(n * 3 * F * eb) + al(n * ab) + al((ne + 16) * kcols * eb) +
+         al(ne * 4 * ab);
 }
 
 
@@ -312,8 +326,8 @@ struct Profiler {
 
 static const char* kc_name(int kc) {
   static const char* names[KC_COUNT] = {"graph_prep", "graph_count", "graph_scan", "graph_fill",
-                                        "embed", "phi", "message", "update", "heads", "energy",
-                                        "export"};
+                                        "embed", "phi", "edge_prep", "message", "update", "heads",
+                                        "energy", "export"};
   return names[kc];
 }
 
@@ -471,7 +485,7 @@ painn_status painn_graph_free(painn_graph* g) {
     (void)hipSetDevice(g->ctx->device);
     (void)hipStreamSynchronize(g->ctx->stream);
   }
-  void* bufs[] = {g->row_ptr, g->counts, g->col, g->shift, g->pos, g->species, g->atom_struct,
+  void* bufs[] = {g->row_ptr, g->counts, g->col, g->shift, g->recv, g->pos, g->species, g->atom_struct,
                   g->cell, g->sinfo, g->struct_ptr, g->scan_tmp, g->d_status};
   for (void* p : bufs)
     if (p) (void)hipFree(p);
@@ -577,8 +591,11 @@ painn_status painn_build_graph(painn_ctx* ctx, int32_t B, int32_t N, const int32
     size_t c2 = 0;
     if (g->col) { (void)hipFree(g->col); g->col = nullptr; }
     if (g->shift) { (void)hipFree(g->shift); g->shift = nullptr; }
+    if (g->recv) { (void)hipFree(g->recv); g->recv = nullptr; }
+    size_t c3 = 0;
     e = ensure(&g->col, &cape, (size_t)g->E);
     if (e == hipSuccess) e = ensure(&g->shift, &c2, cape);
+    if (e == hipSuccess) e = ensure(&g->recv, &c3, cape);
     if (e != hipSuccess) {
       g->cap_edges = 0;
       return bail(PAINN_E_OOM, std::string("edge allocation: ") + hipGetErrorString(e));
@@ -626,7 +643,8 @@ static painn_status run_forward(painn_ctx* ctx, const painn_model* model, const 
     painn_status st = build_prec(m, prec, &m->prec[prec]);
     if (st != PAINN_OK) return st;
   }
-  size_t need = forward_workspace_bytes(prec, g->N, m->hp.F);
+  const int kcols = m->prec[prec]->layers[0].filt_mma.din_p;
+  size_t need = forward_workspace_bytes(prec, g->N, g->E, m->hp.F, kcols);
   if (need > ctx->ws_bytes) {
     if (ctx->ws) {
       (void)hipStreamSynchronize(ctx->stream);
@@ -659,6 +677,8 @@ static painn_status run_forward(painn_ctx* ctx, const painn_model* model, const 
   a.v[1] = p; p += al(N * 3 * F * eb);
   a.h = p; p += al(N * 3 * F * eb);
   a.e = p; p += al(N * ab);
+  a.basis = p; p += al(((size_t)g->E + 16) * kcols * eb);
+  a.einfo = p; p += al((size_t)g->E * 4 * ab);
   if (g->B == 0 && !s_out) return PAINN_OK;
   (void)hipGetLastError();   // do not report an error left by earlier, unrelated calls
   hipError_t e = launch_forward(ctx->stream, prec, a);
