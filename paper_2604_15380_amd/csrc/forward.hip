@@ -603,7 +603,7 @@ inline int grid_for(size_t n, int per) {
 // gather reads 256 contiguous bytes of a sender row, and the filter values
 // come back from LDS.  Sums stay in the lane (no cross-lane reduction) and no
 // wave waits for another.
-constexpr int MSG_RB2 = 8;
+constexpr int MSG_RB2 = 4;
 
 template <class A>
 __device__ __forceinline__ A bcast(A x, int lane) {
