@@ -626,6 +626,10 @@ __global__ void __launch_bounds__(F) k_message_lane(MsgArgs a) {
   constexpr int NW = F / 64, NFT = F / 16;
   constexpr int WLD = 64 + 4;                   // LDS row of one part, one edge
   constexpr int kcols = KBM * P::KC;
+  // VGPRs held by the filter's B fragments decide how much else is in flight
+  constexpr int BF_REGS = 12 * KBM * (int)sizeof(Fr) / 4;
+  constexpr int QI = BF_REGS > 100 ? 1 : 4;     // MFMA chains issued together (feature tiles)
+  constexpr int EG = BF_REGS > 100 ? 4 : 8;     // edges gathered per group
   __shared__ A Wt[NW][3][16 * WLD];
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int c = 64 * wave + lane;               // this lane's channel
@@ -678,46 +682,66 @@ __global__ void __launch_bounds__(F) k_message_lane(MsgArgs a) {
         ez = ei[2];
         ej = ei[3];
       }
+      // The filter of 4 feature tiles x 3 parts, parked in LDS.  With few
+      // registers held by the B fragments all 12 MFMA chains are issued
+      // together (QI = 4); otherwise one feature tile at a time (QI = 1).
 #pragma unroll
-      for (int q = 0; q < 4; ++q) {
-        C w0, w1, w2;
-        for (int r = 0; r < 4; ++r) w0[r] = w1[r] = w2[r] = 0;
+      for (int q0 = 0; q0 < 4; q0 += QI) {
+        C w[QI][3];
 #pragma unroll
-        for (int kb = 0; kb < KBM; ++kb) {
-          w0 = P::mfma(Ga[kb], Bf[q][0][kb], w0);
-          w1 = P::mfma(Ga[kb], Bf[q][1][kb], w1);
-          w2 = P::mfma(Ga[kb], Bf[q][2][kb], w2);
-        }
-        const int col = 16 * q + (lane & 15);
+        for (int q = 0; q < QI; ++q)
 #pragma unroll
-        for (int r = 0; r < 4; ++r) {
-          const int row = P::row(lane, r);
-          wt0[row * WLD + col] = w0[r];
-          wt1[row * WLD + col] = w1[r];
-          wt2[row * WLD + col] = w2[r];
+          for (int part = 0; part < 3; ++part)
+            for (int r = 0; r < 4; ++r) w[q][part][r] = 0;
+#pragma unroll
+        for (int kb = 0; kb < KBM; ++kb)
+#pragma unroll
+          for (int q = 0; q < QI; ++q)
+#pragma unroll
+            for (int part = 0; part < 3; ++part)
+              w[q][part] = P::mfma(Ga[kb], Bf[q0 + q][part][kb], w[q][part]);
+#pragma unroll
+        for (int q = 0; q < QI; ++q) {
+          const int col = 16 * (q0 + q) + (lane & 15);
+#pragma unroll
+          for (int r = 0; r < 4; ++r) {
+            const int row = P::row(lane, r);
+            wt0[row * WLD + col] = w[q][0][r];
+            wt1[row * WLD + col] = w[q][1][r];
+            wt2[row * WLD + col] = w[q][2][r];
+          }
         }
       }
       __builtin_amdgcn_wave_barrier();
       __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
       __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
-      for (int e4 = 0; e4 < cnt; e4 += 4)
+      // Edges are taken EG at a time with no early exit, so all 6 EG gathers
+      // of a group can be in flight together: past the chunk's end the sender
+      // is row 0 (lanes >= cnt hold index 0) and the filter values are zeroed.
+      auto edges = [&](int ebase) {
 #pragma unroll
-      for (int u = 0; u < 4; ++u) {
-        const int e = e4 + u;
-        if (e >= cnt) break;
-        const int j = acc_to_index(bcast(ej, e));
-        const A rx = bcast(ex, e), ry = bcast(ey, e), rz = bcast(ez, e);
-        const T* hj = h + (size_t)j * 3 * F + c;
-        const T* vj = vin + (size_t)j * 3 * F + c;
-        const A hs = P::ld(hj[0]), hv = P::ld(hj[F]), hr = P::ld(hj[2 * F]);
-        const A v0 = P::ld(vj[0]), v1 = P::ld(vj[F]), v2 = P::ld(vj[2 * F]);
-        const A ws = wt0[e * WLD + lane], wv = wt1[e * WLD + lane], wr = wt2[e * WLD + lane];
-        acc_s += hs * ws;
-        const A pv = hv * wv, pr = hr * wr;
-        acc_v0 += v0 * pv + rx * pr;
-        acc_v1 += v1 * pv + ry * pr;
-        acc_v2 += v2 * pv + rz * pr;
-      }
+        for (int u = 0; u < EG; ++u) {
+          const int e = ebase + u;
+          const bool ok = e < cnt;
+          const int j = acc_to_index(bcast(ej, e));
+          const A rx = bcast(ex, e), ry = bcast(ey, e), rz = bcast(ez, e);
+          const T* hj = h + (size_t)j * 3 * F + c;
+          const T* vj = vin + (size_t)j * 3 * F + c;
+          const A hs = P::ld(hj[0]), hv = P::ld(hj[F]), hr = P::ld(hj[2 * F]);
+          const A v0 = P::ld(vj[0]), v1 = P::ld(vj[F]), v2 = P::ld(vj[2 * F]);
+          const A ws = ok ? wt0[e * WLD + lane] : (A)0;
+          const A wv = ok ? wt1[e * WLD + lane] : (A)0;
+          const A wr = ok ? wt2[e * WLD + lane] : (A)0;
+          acc_s += hs * ws;
+          const A pv = hv * wv, pr = hr * wr;
+          acc_v0 += v0 * pv + rx * pr;
+          acc_v1 += v1 * pv + ry * pr;
+          acc_v2 += v2 * pv + rz * pr;
+        }
+      };
+#pragma unroll
+      for (int eb0 = 0; eb0 < 16; eb0 += EG)
+        if (eb0 < cnt) edges(eb0);
       __builtin_amdgcn_wave_barrier();
       __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
       __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
