@@ -311,8 +311,18 @@ struct UpdArgs {
   DenseDev uv, upd1, upd2, phi1, phi2;
 };
 
+// Waves per SIMD the update kernel is compiled for: three at F = 128, where
+// the registers allow it without spilling and three 256-thread workgroups
+// still fit the 160 KiB of LDS; at F = 256 the measured best is two (one in
+// FP64, whose accumulators need the whole register file).
+template <class P, int F>
+constexpr int update_waves() {
+  return F == 128 ? 3 : F == 64 ? (P::PREC == PAINN_FP64 ? 2 : 3) : (P::PREC == PAINN_FP64 ? 1 : 2);
+}
+
 template <class P, int F, int RT, bool FUSE_PHI>
-__global__ void __launch_bounds__(256) k_update(UpdArgs a) {
+__global__ void __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(update_waves<P, F>())))
+k_update(UpdArgs a) {
   using T = typename P::T;
   using A = typename P::A;
   using C = typename P::C;
