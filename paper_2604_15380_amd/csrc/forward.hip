@@ -627,8 +627,15 @@ __device__ __forceinline__ A bcast(A x, int lane) {
   }
 }
 
+// Two waves per SIMD while the filter's B fragments leave room for them.
+template <class P, int KBM>
+constexpr int message_waves() {
+  return 12 * KBM * (int)sizeof(typename P::Fr) / 4 > 150 ? 1 : 2;
+}
+
 template <class P, int F, int KBM>
-__global__ void __launch_bounds__(F) k_message_lane(MsgArgs a) {
+__global__ void __launch_bounds__(F) __attribute__((amdgpu_waves_per_eu(message_waves<P, KBM>())))
+k_message_lane(MsgArgs a) {
   using T = typename P::T;
   using A = typename P::A;
   using C = typename P::C;
@@ -680,9 +687,14 @@ __global__ void __launch_bounds__(F) k_message_lane(MsgArgs a) {
     for (int c0 = ea; c0 < eb; c0 += 16) {
       const int cnt = min(16, eb - c0);
       const T* gp = basis + (size_t)(c0 + (lane & 15)) * kcols + (lane >> 4) * P::KPL;
+      // A rows past the chunk's end are zeroed, so are their filter rows
+      const bool row_ok = (lane & 15) < cnt;
       Fr Ga[KBM];
 #pragma unroll
-      for (int kb = 0; kb < KBM; ++kb) Ga[kb] = P::frag(gp + kb * P::KC);
+      for (int kb = 0; kb < KBM; ++kb) {
+        const Fr g = P::frag(gp + kb * P::KC);
+        Ga[kb] = row_ok ? g : Fr{};
+      }
       // lanes e < cnt hold edge c0 + e: rhat and the sender index
       A ex = 0, ey = 0, ez = 0, ej = 0;
       if (lane < cnt) {
@@ -727,21 +739,18 @@ __global__ void __launch_bounds__(F) k_message_lane(MsgArgs a) {
       __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
       // Edges are taken EG at a time with no early exit, so all 6 EG gathers
       // of a group can be in flight together: past the chunk's end the sender
-      // is row 0 (lanes >= cnt hold index 0) and the filter values are zeroed.
+      // is row 0 (lanes >= cnt hold index 0) and the filter rows are zero.
       auto edges = [&](int ebase) {
 #pragma unroll
         for (int u = 0; u < EG; ++u) {
           const int e = ebase + u;
-          const bool ok = e < cnt;
           const int j = acc_to_index(bcast(ej, e));
           const A rx = bcast(ex, e), ry = bcast(ey, e), rz = bcast(ez, e);
           const T* hj = h + (size_t)j * 3 * F + c;
           const T* vj = vin + (size_t)j * 3 * F + c;
           const A hs = P::ld(hj[0]), hv = P::ld(hj[F]), hr = P::ld(hj[2 * F]);
           const A v0 = P::ld(vj[0]), v1 = P::ld(vj[F]), v2 = P::ld(vj[2 * F]);
-          const A ws = ok ? wt0[e * WLD + lane] : (A)0;
-          const A wv = ok ? wt1[e * WLD + lane] : (A)0;
-          const A wr = ok ? wt2[e * WLD + lane] : (A)0;
+          const A ws = wt0[e * WLD + lane], wv = wt1[e * WLD + lane], wr = wt2[e * WLD + lane];
           acc_s += hs * ws;
           const A pv = hv * wv, pr = hr * wr;
           acc_v0 += v0 * pv + rx * pr;
