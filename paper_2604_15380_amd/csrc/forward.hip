@@ -459,120 +459,250 @@ k_update(UpdArgs a) {
 // ---------------------------------------------------------------- heads ----
 // Per atom: shared MLP (silu after every layer), then the branch MLP of the
 // structure's dataset (silu between layers, last layer linear to a scalar).
-// A tile of 16 atoms runs each distinct branch present in it.
+//
+// With dataset ids the atoms are first grouped by head on the device (a
+// counting sort: count, plan, scatter), so that one workgroup runs ONE branch
+// over a tile of TM = 16 RT atoms and every weight fragment it streams serves
+// TM rows.  The branch's last layer has a single output; it is folded into
+// the epilogue of the layer before it as a dot product, so the widest hidden
+// layer never goes through LDS.  Every atom's result depends only on its own
+// row, so the grouping order does not change any value.
+constexpr int HEADS_MAX = 64;
+constexpr int HEADS_NW = 8;   // waves per heads workgroup
+
+struct HeadPlan {
+  int32_t count[HEADS_MAX];   // valid atoms per head
+  int32_t start[HEADS_MAX];   // first slot of the head in the atom order
+  int32_t cursor[HEADS_MAX];  // scatter cursor
+  int32_t n_tiles;
+};
+struct HeadTile {
+  int32_t head, begin, end, pad;   // slots [begin, end) of the atom order
+};
+static_assert(sizeof(HeadPlan) <= 1024, "head plan workspace is 1 KiB");
+static_assert(sizeof(HeadTile) == 16, "head tile workspace is 16 bytes per tile");
+
+__device__ __forceinline__ int atom_head(const int32_t* dataset_id, const int32_t* atom_struct,
+                                         int n_heads, int atom) {
+  const int h = dataset_id[atom_struct[atom]];
+  return h < 0 || h >= n_heads ? -1 : h;
+}
+
+__global__ void __launch_bounds__(64) k_head_clear(HeadPlan* p) {
+  const int t = threadIdx.x;
+  p->count[t] = 0;
+  p->cursor[t] = 0;
+  if (t == 0) p->n_tiles = 0;
+}
+
+// per-head atom counts; atoms with an invalid dataset id get a NaN energy
+template <class A>
+__global__ void __launch_bounds__(256) k_head_count(int N, int n_heads, const int32_t* dataset_id,
+                                                    const int32_t* atom_struct, HeadPlan* p,
+                                                    A* e) {
+  __shared__ int hist[HEADS_MAX];
+  if (threadIdx.x < HEADS_MAX) hist[threadIdx.x] = 0;
+  __syncthreads();
+  const int atom = blockIdx.x * 256 + threadIdx.x;
+  if (atom < N) {
+    const int h = atom_head(dataset_id, atom_struct, n_heads, atom);
+    if (h < 0) e[atom] = (A)NAN;
+    else atomicAdd(&hist[h], 1);
+  }
+  __syncthreads();
+  if (threadIdx.x < n_heads && hist[threadIdx.x] > 0) atomicAdd(&p->count[threadIdx.x], hist[threadIdx.x]);
+}
+
+// head offsets in the atom order and the tile list (one wave)
+__global__ void __launch_bounds__(64) k_head_plan(int n_heads, int TM, HeadPlan* p, HeadTile* tiles) {
+  __shared__ int start[HEADS_MAX], tbase[HEADS_MAX];
+  const int h = threadIdx.x;
+  if (h == 0) {
+    int s = 0, t = 0;
+    for (int q = 0; q < n_heads; ++q) {
+      start[q] = s;
+      tbase[q] = t;
+      s += p->count[q];
+      t += (p->count[q] + TM - 1) / TM;
+    }
+    p->n_tiles = t;
+  }
+  __syncthreads();
+  if (h < n_heads) {
+    const int c = p->count[h], s0 = start[h];
+    p->start[h] = s0;
+    for (int k = 0; k * TM < c; ++k) {
+      HeadTile tl;
+      tl.head = h;
+      tl.begin = s0 + k * TM;
+      tl.end = min(s0 + (k + 1) * TM, s0 + c);
+      tl.pad = 0;
+      tiles[tbase[h] + k] = tl;
+    }
+  }
+}
+
+// atom order grouped by head: block-local ranks, one global reservation per head
+__global__ void __launch_bounds__(256) k_head_scatter(int N, int n_heads, const int32_t* dataset_id,
+                                                      const int32_t* atom_struct, HeadPlan* p,
+                                                      int32_t* order) {
+  __shared__ int hist[HEADS_MAX], base[HEADS_MAX];
+  if (threadIdx.x < HEADS_MAX) hist[threadIdx.x] = 0;
+  __syncthreads();
+  const int atom = blockIdx.x * 256 + threadIdx.x;
+  int h = -1, rank = 0;
+  if (atom < N) {
+    h = atom_head(dataset_id, atom_struct, n_heads, atom);
+    if (h >= 0) rank = atomicAdd(&hist[h], 1);
+  }
+  __syncthreads();
+  if (threadIdx.x < n_heads && hist[threadIdx.x] > 0)
+    base[threadIdx.x] = p->start[threadIdx.x] + atomicAdd(&p->cursor[threadIdx.x], hist[threadIdx.x]);
+  __syncthreads();
+  if (h >= 0) order[base[h] + rank] = atom;
+}
+
 struct HeadArgs {
-  int N, F, n_heads, ns, nb, lds_s, lds_b;   // row strides of the shared / branch buffers
+  int N, ns, nb;
+  int lds_s, lds_b;                    // row strides of the shared / branch buffers
+  int off_sa, off_sb, off_b0, off_b1;  // buffer offsets in the dynamic LDS (elements)
   const void* s;
-  const int32_t* atom_struct;
-  const int32_t* dataset_id;
+  const int32_t* order;    // null: tiles of consecutive atoms, head 0
+  const HeadTile* tiles;
+  const HeadPlan* plan;
   const void* const* table;  // [n_heads][nb][2] = (packed w, bias)
   DenseDev shared[16];
   int bdin[16], bdout[16];
   void* e;
 };
 
-// LDS: X [16][F+PAD] (final s), SA/SB [16][lds_s] (shared layers), B0/B1
-// [16][lds_b] (branch hidden layers).
-template <class P, int F>
-__global__ void __launch_bounds__(256) k_heads(HeadArgs a) {
+// Element k of output row 0 of a packed dense layer (the B fragment order).
+template <class P>
+__device__ __forceinline__ typename P::A packed_row0(const DenseDev& L, int k) {
+  const int kb = k / P::KC, r = k % P::KC;
+  return P::ld(((const typename P::T*)L.w)[((size_t)kb * 64 + 16 * (r / P::KPL)) * P::KPL + r % P::KPL]);
+}
+
+// LDS: X [TM][F+PAD] (the tile's final s), SA/SB [TM][lds_s] (shared
+// layers), B0/B1 [TM][lds_b] (stored branch hidden layers); with shared
+// layers B0 reuses X, which is dead after the first of them.
+template <class P, int F, int RT>
+__global__ void __launch_bounds__(64 * HEADS_NW) k_heads(HeadArgs a) {
   using T = typename P::T;
   using A = typename P::A;
+  using C = typename P::C;
+  constexpr int TM = 16 * RT, LDX = F + P::PAD;
   extern __shared__ __attribute__((aligned(16))) unsigned char smem[];
-  constexpr int LDX = F + P::PAD;
-  T* X = (T*)smem;
-  T* SA = X + 16 * LDX;
-  T* SB = SA + 16 * a.lds_s;
-  T* B0 = SB + 16 * a.lds_s;
-  T* B1 = B0 + 16 * a.lds_b;
-  __shared__ int hd[16];
-  __shared__ int heads[16];
-  __shared__ int nh;
-  __shared__ A eo[16];
-  const int lane = threadIdx.x & 63;
-  const size_t row0 = (size_t)blockIdx.x * 16;
-  const int N = a.N;
-  load_rows<P, F>(X, LDX, (const T*)a.s, row0, 16, N);
-  if (threadIdx.x < 16) {
-    const size_t row = row0 + threadIdx.x;
-    int h = -2;                                  // padding row
-    if (row < (size_t)N) {
-      h = a.dataset_id ? a.dataset_id[a.atom_struct[row]] : 0;
-      if (h < 0 || h >= a.n_heads) h = -1;       // invalid id -> NaN energy
-    }
-    hd[threadIdx.x] = h;
+  T* lds = (T*)smem;
+  __shared__ int idx[TM];
+  __shared__ A part[HEADS_NW][TM];
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  int head = 0, begin, end;
+  if (a.tiles) {
+    if ((int)blockIdx.x >= a.plan->n_tiles) return;
+    const HeadTile tl = a.tiles[blockIdx.x];
+    head = tl.head;
+    begin = tl.begin;
+    end = tl.end;
+  } else {
+    begin = blockIdx.x * TM;
+    end = min(a.N, begin + TM);
+  }
+  if (threadIdx.x < TM) {
+    const int k = begin + threadIdx.x;
+    idx[threadIdx.x] = k < end ? (a.order ? a.order[k] : k) : -1;
   }
   __syncthreads();
-  if (threadIdx.x == 0) {
-    int n = 0;
-    for (int r = 0; r < 16; ++r) {
-      const int h = hd[r];
-      if (h < 0) continue;
-      bool seen = false;
-      for (int q = 0; q < n; ++q) seen |= heads[q] == h;
-      if (!seen) heads[n++] = h;
-    }
-    nh = n;
+  T* X = lds;
+  const T* s = (const T*)a.s;
+  for (int x = threadIdx.x; x < TM * F; x += blockDim.x) {
+    const int r = x / F, c = x % F;
+    const int g = idx[r];
+    X[r * LDX + c] = g >= 0 ? s[(size_t)g * F + c] : P::st(0);
   }
   __syncthreads();
   // shared layers: X -> SA -> SB -> SA ...
   const T* S = X;
   int ld_S = LDX;
   for (int m = 0; m < a.ns; ++m) {
-    T* dst = (m & 1) ? SB : SA;
-    const int lds = a.lds_s;
-    dense_tiles<P, 1, 4>(S, ld_S, a.shared[m], [&](int ct, typename P::C* acc) {
+    T* dst = lds + ((m & 1) ? a.off_sb : a.off_sa);
+    const int ld = a.lds_s;
+    const DenseDev& L = a.shared[m];
+    dense_tiles<P, RT, HEADS_NW>(S, ld_S, L, [&](int ct, C* acc) {
       const int col = ct * 16 + (lane & 15);
-      const A bias = ((const A*)a.shared[m].b)[col];
-      for (int i = 0; i < 4; ++i) dst[(P::row(lane, i)) * lds + col] = P::st(silu<A>(acc[0][i] + bias));
+      const A bias = ((const A*)L.b)[col];
+      for (int r = 0; r < RT; ++r)
+        for (int i = 0; i < 4; ++i)
+          dst[(r * 16 + P::row(lane, i)) * ld + col] = P::st(silu<A>(acc[r][i] + bias));
     });
     __syncthreads();
     S = dst;
-    ld_S = lds;
+    ld_S = ld;
   }
-  A e_row = 0;
-  const int rtid = threadIdx.x;
-  for (int q = 0; q < nh; ++q) {
-    const int head = heads[q];
+  auto branch = [&](int m) {
+    DenseDev L;
+    L.w = (void*)a.table[((size_t)head * a.nb + m) * 2];
+    L.b = (void*)a.table[((size_t)head * a.nb + m) * 2 + 1];
+    L.din = a.bdin[m];
+    L.dout = a.bdout[m];
+    L.din_p = pad32(a.bdin[m]);
+    L.dout_p = pad32(a.bdout[m]);
+    return L;
+  };
+  const int rt = threadIdx.x;
+  A y = 0;
+  if (a.nb == 1) {
+    // one linear layer: a dot product per row, straight from S
+    const DenseDev Lz = branch(0);
+    if (rt < TM) {
+      y = ((const A*)Lz.b)[0];
+      for (int k = 0; k < Lz.din; ++k) y += P::ld(S[rt * ld_S + k]) * packed_row0<P>(Lz, k);
+    }
+  } else {
     const T* in = S;
     int ld_in = ld_S;
-    for (int m = 0; m < a.nb; ++m) {
-      DenseDev L;
-      L.w = (void*)a.table[((size_t)head * a.nb + m) * 2];
-      L.b = (void*)a.table[((size_t)head * a.nb + m) * 2 + 1];
-      L.din = a.bdin[m];
-      L.dout = a.bdout[m];
-      L.din_p = pad32(a.bdin[m]);
-      L.dout_p = pad32(a.bdout[m]);
-      const bool last = m == a.nb - 1;
-      T* dst = (m & 1) ? B1 : B0;
-      const int ldb = a.lds_b;
-      dense_tiles<P, 1, 4>(in, ld_in, L, [&](int ct, typename P::C* acc) {
+    for (int m = 0; m + 2 < a.nb; ++m) {
+      T* dst = lds + ((m & 1) ? a.off_b1 : a.off_b0);
+      const int ld = a.lds_b;
+      const DenseDev L = branch(m);
+      dense_tiles<P, RT, HEADS_NW>(in, ld_in, L, [&](int ct, C* acc) {
         const int col = ct * 16 + (lane & 15);
         const A bias = ((const A*)L.b)[col];
-        for (int i = 0; i < 4; ++i) {
-          const int r = P::row(lane, i);
-          const A y = acc[0][i] + bias;
-          if (last) {
-            if (col == 0) eo[r] = y;
-          } else {
-            dst[r * ldb + col] = P::st(silu<A>(y));
-          }
-        }
+        for (int r = 0; r < RT; ++r)
+          for (int i = 0; i < 4; ++i)
+            dst[(r * 16 + P::row(lane, i)) * ld + col] = P::st(silu<A>(acc[r][i] + bias));
       });
       __syncthreads();
       in = dst;
-      ld_in = ldb;
+      ld_in = ld;
     }
-    if (rtid < 16 && hd[rtid] == head) e_row = eo[rtid];
+    // last hidden layer with the output layer folded in: every lane sums
+    // silu(.) * w_out over the columns it holds, in a fixed order
+    const DenseDev L = branch(a.nb - 2), Lz = branch(a.nb - 1);
+    A p[RT][4];
+    for (int r = 0; r < RT; ++r)
+      for (int i = 0; i < 4; ++i) p[r][i] = 0;
+    dense_tiles<P, RT, HEADS_NW>(in, ld_in, L, [&](int ct, C* acc) {
+      const int col = ct * 16 + (lane & 15);
+      const A bias = ((const A*)L.b)[col];
+      const A wz = packed_row0<P>(Lz, col);
+      for (int r = 0; r < RT; ++r)
+        for (int i = 0; i < 4; ++i) p[r][i] += silu<A>(acc[r][i] + bias) * wz;
+    });
+    // the 16 lanes of a group hold the same rows: butterfly over them
+    for (int r = 0; r < RT; ++r)
+      for (int i = 0; i < 4; ++i)
+        for (int off = 1; off < 16; off <<= 1) p[r][i] += __shfl_xor(p[r][i], off);
+    if ((lane & 15) == 0)
+      for (int r = 0; r < RT; ++r)
+        for (int i = 0; i < 4; ++i) part[wave][r * 16 + P::row(lane, i)] = p[r][i];
     __syncthreads();
-  }
-  if (rtid < 16) {
-    const size_t row = row0 + rtid;
-    if (row < (size_t)N) {
-      A* e = (A*)a.e;
-      e[row] = hd[rtid] == -1 ? (A)NAN : e_row;
+    if (rt < TM) {
+      y = ((const A*)Lz.b)[0];
+      for (int w = 0; w < HEADS_NW; ++w) y += part[w][rt];
     }
   }
+  if (rt < TM && idx[rt] >= 0) ((A*)a.e)[idx[rt]] = y;
 }
 
 // ------------------------------------------------------------ energies ----
@@ -809,6 +939,121 @@ hipError_t launch_message(hipStream_t st, const MsgArgs& a) {
   return hipSuccess;
 }
 
+// Dynamic LDS beyond 64 KiB must be allowed once per kernel.
+template <class P, int F, int RT>
+hipError_t heads_allow_lds(size_t smem) {
+  static size_t allowed = 64 * 1024;
+  if (smem <= allowed) return hipSuccess;
+  hipError_t e = hipFuncSetAttribute((const void*)k_heads<P, F, RT>,
+                                     hipFuncAttributeMaxDynamicSharedMemorySize, (int)smem);
+  if (e != hipSuccess) {
+    (void)hipGetLastError();
+    return e;
+  }
+  allowed = smem;
+  return hipSuccess;
+}
+
+template <class P, int F, int RT>
+hipError_t launch_heads_rt(hipStream_t st, HeadArgs& ha, int grid, size_t smem) {
+  hipError_t e = heads_allow_lds<P, F, RT>(smem);
+  if (e != hipSuccess) return e;
+  k_heads<P, F, RT><<<grid, 64 * HEADS_NW, smem, st>>>(ha);
+  return hipGetLastError();
+}
+
+// Heads and per-atom energies: bin atoms by head (when dataset ids are
+// given), then one workgroup per tile of the largest TM whose buffers fit
+// the LDS.
+template <class P, int F>
+hipError_t launch_heads(hipStream_t st, ForwardArgs& fa) {
+  using T = typename P::T;
+  using A = typename P::A;
+  const PrecModel* pm = fa.pm;
+  const auto& hp = fa.m->hp;
+  const int N = fa.g->N;
+  HeadArgs ha;
+  ha.N = N;
+  ha.ns = (int)pm->shared.size();
+  ha.nb = (int)hp.branch_dims.size();
+  if (hp.n_heads > HEADS_MAX || ha.ns > 16 || ha.nb > 16) return hipErrorInvalidValue;
+  int ws = 0, wb = 0;   // widest shared / stored branch layer (padded)
+  for (int m = 0; m < ha.ns; ++m) {
+    ha.shared[m] = pm->shared[m];
+    ws = ws > pad32(hp.shared_dims[m]) ? ws : pad32(hp.shared_dims[m]);
+  }
+  int di = ha.ns == 0 ? F : hp.shared_dims.back();
+  for (int m = 0; m < ha.nb; ++m) {
+    ha.bdin[m] = di;
+    ha.bdout[m] = hp.branch_dims[m];
+    if (m + 2 < ha.nb) wb = wb > pad32(hp.branch_dims[m]) ? wb : pad32(hp.branch_dims[m]);
+    di = hp.branch_dims[m];
+  }
+  const int nstored = ha.nb > 2 ? ha.nb - 2 : 0;
+  ha.lds_s = ha.ns ? ws + P::PAD : 0;
+  ha.lds_b = nstored ? wb + P::PAD : 0;
+  constexpr int LDX = F + P::PAD;
+  // buffer layout for TM rows; returns the dynamic LDS bytes
+  auto layout = [&](int TM) {
+    auto al = [](size_t x) { return (x + 7) & ~(size_t)7; };   // 16-byte aligned for bf16
+    size_t o;
+    if (ha.ns > 0) {
+      const size_t r0 = al((size_t)TM * (nstored && ha.lds_b > LDX ? ha.lds_b : LDX));
+      ha.off_b0 = 0;
+      ha.off_sa = (int)r0;
+      ha.off_sb = (int)(r0 + al((size_t)TM * ha.lds_s));
+      o = ha.off_sb + al((size_t)TM * ha.lds_s);
+    } else {
+      ha.off_sa = ha.off_sb = 0;
+      ha.off_b0 = (int)al((size_t)TM * LDX);
+      o = ha.off_b0 + (nstored ? al((size_t)TM * ha.lds_b) : 0);
+    }
+    ha.off_b1 = (int)o;
+    if (nstored > 1) o += al((size_t)TM * ha.lds_b);
+    return o * sizeof(T);
+  };
+  constexpr size_t LDS_LIMIT = 150 * 1024;
+  int RT = 4;
+  size_t smem = 0;
+  for (; RT >= 1; RT /= 2) {
+    const int TM = 16 * RT;
+    smem = layout(TM);
+    const size_t fixed = (size_t)TM * sizeof(int) + (size_t)HEADS_NW * TM * sizeof(A);
+    if (smem + fixed <= LDS_LIMIT) break;
+  }
+  if (RT < 1) return hipErrorInvalidValue;
+  const int TM = 16 * RT;
+  ha.s = fa.s;
+  ha.table = (const void* const*)pm->head_table;
+  ha.e = fa.e;
+  int grid = (N + TM - 1) / TM;
+  prof_mark(fa.prof, st, KC_HEADS, true);
+  if (fa.dataset_id) {
+    HeadPlan* plan = (HeadPlan*)fa.head_plan;
+    HeadTile* tiles = (HeadTile*)fa.head_tiles;
+    const int nb256 = (N + 255) / 256;
+    k_head_clear<<<1, 64, 0, st>>>(plan);
+    k_head_count<A><<<nb256, 256, 0, st>>>(N, hp.n_heads, fa.dataset_id, fa.g->atom_struct, plan, (A*)fa.e);
+    k_head_plan<<<1, 64, 0, st>>>(hp.n_heads, TM, plan, tiles);
+    k_head_scatter<<<nb256, 256, 0, st>>>(N, hp.n_heads, fa.dataset_id, fa.g->atom_struct, plan,
+                                          fa.head_order);
+    ha.order = fa.head_order;
+    ha.tiles = tiles;
+    ha.plan = plan;
+    grid += hp.n_heads;
+  } else {
+    ha.order = nullptr;
+    ha.tiles = nullptr;
+    ha.plan = nullptr;
+  }
+  hipError_t e;
+  if (RT == 4) e = launch_heads_rt<P, F, 4>(st, ha, grid, smem);
+  else if (RT == 2) e = launch_heads_rt<P, F, 2>(st, ha, grid, smem);
+  else e = launch_heads_rt<P, F, 1>(st, ha, grid, smem);
+  prof_mark(fa.prof, st, KC_HEADS, false);
+  return e;
+}
+
 template <class P, int F>
 hipError_t forward_impl(hipStream_t st, ForwardArgs& fa) {
   using T = typename P::T;
@@ -891,48 +1136,8 @@ hipError_t forward_impl(hipStream_t st, ForwardArgs& fa) {
   }
   if (g->B == 0) return hipGetLastError();
   if (N > 0) {
-    HeadArgs ha;
-    ha.N = N;
-    ha.F = F;
-    ha.n_heads = hp.n_heads;
-    ha.ns = (int)pm->shared.size();
-    ha.nb = (int)hp.branch_dims.size();
-    int ds = 32, db = 32;
-    for (size_t m = 0; m < pm->shared.size(); ++m) {
-      ha.shared[m] = pm->shared[m];
-      ds = ds > pad32(hp.shared_dims[m]) ? ds : pad32(hp.shared_dims[m]);
-    }
-    int di = pm->shared.empty() ? F : hp.shared_dims.back();
-    for (int m = 0; m < ha.nb; ++m) {
-      ha.bdin[m] = di;
-      ha.bdout[m] = hp.branch_dims[m];
-      di = hp.branch_dims[m];
-      db = db > pad32(di) ? db : pad32(di);
-    }
-    ha.lds_s = pm->shared.empty() ? 0 : ds + P::PAD;
-    ha.lds_b = db + P::PAD;
-    ha.s = s;
-    ha.atom_struct = g->atom_struct;
-    ha.dataset_id = fa.dataset_id;
-    ha.table = (const void* const*)pm->head_table;
-    ha.e = fa.e;
-    const size_t smem = (size_t)16 * ((F + P::PAD) + 2 * ha.lds_s + 2 * ha.lds_b) * sizeof(T);
-    // dynamic LDS beyond 64 KiB must be allowed explicitly (the kernel also
-    // holds a few hundred bytes of static LDS; 160 KiB per CU in total)
-    static size_t lds_allowed = 64 * 1024;
-    if (smem > lds_allowed) {
-      if (smem > 150 * 1024) return hipErrorInvalidValue;
-      hipError_t e = hipFuncSetAttribute((const void*)k_heads<P, F>,
-                                         hipFuncAttributeMaxDynamicSharedMemorySize, (int)smem);
-      if (e != hipSuccess) {
-        (void)hipGetLastError();
-        return e;
-      }
-      lds_allowed = smem;
-    }
-    prof_mark(fa.prof, st, KC_HEADS, true);
-    k_heads<P, F><<<(N + 15) / 16, 256, smem, st>>>(ha);
-    prof_mark(fa.prof, st, KC_HEADS, false);
+    hipError_t e = launch_heads<P, F>(st, fa);
+    if (e != hipSuccess) return e;
   }
   prof_mark(fa.prof, st, KC_ENERGY, true);
   k_energy<A><<<(g->B + 255) / 256, 256, 0, st>>>(g->B, g->struct_ptr, (const A*)fa.e, fa.energies);

@@ -160,6 +160,9 @@ struct ForwardArgs {
   void* e;      // [N] accumulation type
   void* basis;           // [E + 16][kcols] storage type: radial basis rows
   void* einfo;           // [E][4] accumulation type: rhat, sender index
+  void* head_plan;       // per-head counts and offsets (a few hundred bytes)
+  void* head_tiles;      // [N / 16 + 65] tiles of one head each (16 bytes)
+  int32_t* head_order;   // [N] atoms grouped by head
   int stop_layer;          // run layers 0..stop_layer (forward: L-1)
   Profiler* prof;
   double* s_out;           // feature export (may be null)

@@ -112,7 +112,13 @@ __device__ __forceinline__ void dense_tiles(const typename P::T* X, int ldx, con
 #pragma unroll P::UNROLL
       for (int kb = 0; kb < NKB; ++kb) step(kb);
     } else {
-      for (int kb = 0; kb < nkb; ++kb) step(kb);
+      // groups of UNROLL steps, so their weight loads are issued together
+      int kb = 0;
+      for (; kb + P::UNROLL <= nkb; kb += P::UNROLL) {
+#pragma unroll
+        for (int u = 0; u < P::UNROLL; ++u) step(kb + u);
+      }
+      for (; kb < nkb; ++kb) step(kb);
     }
     epi(ct, acc);
   }

@@ -303,13 +303,17 @@ painn_status parse_model(painn_ctx* ctx, const unsigned char* buf, size_t n, pai
 
 // Workspace of one forward pass, carved in this order: s [N][F], v[0], v[1],
 // h [N][3F] (storage type), e [N] (accumulation type), the radial basis rows
-// [E + 16][kcols] (storage type) and the edge info [E][4] (accumulation type).
+// [E + 16][kcols] (storage type), the edge info [E][4] (accumulation type),
+// then the head binning: plan (1 KiB), tiles [N / 16 + 65][4] and the atom
+// order [N] (int32).
+static size_t head_tiles_bytes(size_t n) { return (n / 16 + 65) * 16; }
+
 size_t forward_workspace_bytes(int prec, int N, long long E, int F, int kcols) {
   const size_t eb = elem_bytes(prec), ab = acc_bytes(prec);
   auto al = [](size_t x) { return (x + 255) & ~(size_t)255; };
   const size_t n = (size_t)N, ne = (size_t)E;
   return al(n * F * eb) + 3 * al(n * 3 * F * eb) + al(n * ab) + al((ne + 16) * kcols * eb) +
-         al(ne * 4 * ab);
+         al(ne * 4 * ab) + al(1024) + al(head_tiles_bytes(n)) + al(n * 4);
 }
 
 
@@ -679,6 +683,9 @@ static painn_status run_forward(painn_ctx* ctx, const painn_model* model, const 
   a.e = p; p += al(N * ab);
   a.basis = p; p += al(((size_t)g->E + 16) * kcols * eb);
   a.einfo = p; p += al((size_t)g->E * 4 * ab);
+  a.head_plan = p; p += al(1024);
+  a.head_tiles = p; p += al(head_tiles_bytes(N));
+  a.head_order = (int32_t*)p; p += al(N * 4);
   if (g->B == 0 && !s_out) return PAINN_OK;
   (void)hipGetLastError();   // do not report an error left by earlier, unrelated calls
   hipError_t e = launch_forward(ctx->stream, prec, a);
