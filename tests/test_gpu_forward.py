@@ -127,6 +127,47 @@ def test_screening_first_batch(rt, precision):
     check_energies(E[idx], Er, Ar, TOL[precision], f"{name} {precision}")
 
 
+def test_heads_grouping(rt):
+    """Atoms are grouped by dataset head before the heads run: one head over
+    many tiles, a sparse mix of heads with ragged tile ends, and no dataset ids
+    on a 16-head model (head 0 for all) all match the oracle, and a
+    structure's energy does not depend on how its batch is grouped."""
+    import torch
+    name = "screening"
+    say("heads grouping")
+    start, _ = synth.screening_batches(3000)[0]
+    b = synth.make_batch(name, start, 300)
+    m = model(rt, name)
+    hp, _ = synth.workload_weights(name)
+    g = rt.build_graph(rt.upload_batch(b), hp.cutoff)
+    rng = np.random.default_rng(11)
+    cases = {
+        "one head": np.full(b.n_struct, 5, np.int32),
+        "sparse mix": rng.choice(np.array([0, 3, 15], np.int32), size=b.n_struct),
+    }
+    idx = _sample(b.n_struct, 24, seed=4)
+    energies = {}
+    for label, ds in cases.items():
+        bb = synth.Batch(b.pos, b.species, b.struct_ptr, b.cell, b.pbc, ds)
+        E = rt.forward(m, g, "fp32", dataset_id=torch.as_tensor(ds, device=rt.device)).cpu().numpy()
+        Er, Ar = oracle_energies(name, bb, idx)
+        check_energies(E[idx], Er, Ar, TOL["fp32"], f"{name} {label}")
+        energies[label] = E
+    # no dataset ids: every atom runs head 0
+    E0 = rt.forward(m, g, "fp32").cpu().numpy()
+    b0 = synth.Batch(b.pos, b.species, b.struct_ptr, b.cell, b.pbc, np.zeros(b.n_struct, np.int32))
+    Er, Ar = oracle_energies(name, b0, idx)
+    check_energies(E0[idx], Er, Ar, TOL["fp32"], f"{name} no dataset ids")
+    # structures on head 5 give the same bits alone in a one-head batch and
+    # mixed with other heads
+    mix = np.where(cases["sparse mix"] == 15, 5, cases["sparse mix"]).astype(np.int32)
+    Em = rt.forward(m, g, "fp32", dataset_id=torch.as_tensor(mix, device=rt.device)).cpu().numpy()
+    sel = mix == 5
+    assert sel.any()
+    assert np.array_equal(Em[sel].view(np.uint64), energies["one head"][sel].view(np.uint64))
+    g.free()
+
+
 def test_invariance_and_equivariance_on_gpu(rt):
     name = "tiny_molecules"
     say("GPU invariance / equivariance")
