@@ -364,17 +364,19 @@ k_update(UpdArgs a) {
         for (int i = 0; i < 4; ++i) au[r][i] = av[r][i] = 0;
       const T* wu = Wuv + (size_t)ft * nkb * 64 * P::KPL + (size_t)lane * P::KPL;
       const T* wv = Wuv + (size_t)(NFT + ft) * nkb * 64 * P::KPL + (size_t)lane * P::KPL;
-#pragma unroll P::UNROLL
-      for (int kb = 0; kb < nkb; ++kb) {
-        const Fr bu = P::frag(wu + (size_t)kb * 64 * P::KPL);
-        const Fr bv = P::frag(wv + (size_t)kb * 64 * P::KPL);
+      kloop<nkb, ring_depth<P, 2>(), 2, Fr>(
+          [&](int kb, Fr* f) {
+            f[0] = P::frag(wu + (size_t)kb * 64 * P::KPL);
+            f[1] = P::frag(wv + (size_t)kb * 64 * P::KPL);
+          },
+          [&](int kb, Fr* f) {
 #pragma unroll
-        for (int r = 0; r < RT; ++r) {
-          const Fr x = P::frag(xp + r * 16 * LD1 + kb * P::KC);
-          au[r] = P::mfma(x, bu, au[r]);
-          av[r] = P::mfma(x, bv, av[r]);
-        }
-      }
+            for (int r = 0; r < RT; ++r) {
+              const Fr x = P::frag(xp + r * 16 * LD1 + kb * P::KC);
+              au[r] = P::mfma(x, f[0], au[r]);
+              av[r] = P::mfma(x, f[1], av[r]);
+            }
+          });
 #pragma unroll
       for (int r = 0; r < RT; ++r) {
         U[q][c][r] = au[r];
@@ -416,19 +418,21 @@ k_update(UpdArgs a) {
       const T* w0 = W2 + (size_t)ft * nkb2 * 64 * P::KPL + (size_t)lane * P::KPL;
       const T* w1 = W2 + (size_t)(NFT + ft) * nkb2 * 64 * P::KPL + (size_t)lane * P::KPL;
       const T* w2 = W2 + (size_t)(2 * NFT + ft) * nkb2 * 64 * P::KPL + (size_t)lane * P::KPL;
-#pragma unroll P::UNROLL
-      for (int kb = 0; kb < nkb2; ++kb) {
-        const Fr b0 = P::frag(w0 + (size_t)kb * 64 * P::KPL);
-        const Fr b1 = P::frag(w1 + (size_t)kb * 64 * P::KPL);
-        const Fr b2f = P::frag(w2 + (size_t)kb * 64 * P::KPL);
+      kloop<nkb2, ring_depth<P, 3>(), 3, Fr>(
+          [&](int kb, Fr* f) {
+            f[0] = P::frag(w0 + (size_t)kb * 64 * P::KPL);
+            f[1] = P::frag(w1 + (size_t)kb * 64 * P::KPL);
+            f[2] = P::frag(w2 + (size_t)kb * 64 * P::KPL);
+          },
+          [&](int kb, Fr* f) {
 #pragma unroll
-        for (int r = 0; r < RT; ++r) {
-          const Fr x = P::frag(xp + r * 16 * LD1 + kb * P::KC);
-          avv[r] = P::mfma(x, b0, avv[r]);
-          asv[r] = P::mfma(x, b1, asv[r]);
-          ass[r] = P::mfma(x, b2f, ass[r]);
-        }
-      }
+            for (int r = 0; r < RT; ++r) {
+              const Fr x = P::frag(xp + r * 16 * LD1 + kb * P::KC);
+              avv[r] = P::mfma(x, f[0], avv[r]);
+              asv[r] = P::mfma(x, f[1], asv[r]);
+              ass[r] = P::mfma(x, f[2], ass[r]);
+            }
+          });
       const int col = ft * 16 + (lane & 15);
       const A bvv = b2[col], bsv = b2[F + col], bss = b2[2 * F + col];
 #pragma unroll

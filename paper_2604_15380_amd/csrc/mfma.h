@@ -34,7 +34,7 @@ struct P64 {
   using A = double;  // accumulation
   using C = d4_t;
   using Fr = double;
-  static constexpr int KC = 4, KPL = 1, PAD = 2, PREC = PAINN_FP64, UNROLL = 8;
+  static constexpr int KC = 4, KPL = 1, PAD = 2, PREC = PAINN_FP64, UNROLL = 8, RING = 16;
   __device__ static __forceinline__ Fr frag(const T* p) { return *p; }
   __device__ static __forceinline__ C mfma(Fr a, Fr b, C c) {
     return __builtin_amdgcn_mfma_f64_16x16x4f64(a, b, c, 0, 0, 0);
@@ -50,7 +50,7 @@ struct P32 {
   using A = float;
   using C = f4_t;
   using Fr = float;
-  static constexpr int KC = 4, KPL = 1, PAD = 4, PREC = PAINN_FP32, UNROLL = 8;
+  static constexpr int KC = 4, KPL = 1, PAD = 4, PREC = PAINN_FP32, UNROLL = 8, RING = 24;
   __device__ static __forceinline__ Fr frag(const T* p) { return *p; }
   __device__ static __forceinline__ C mfma(Fr a, Fr b, C c) {
     return __builtin_amdgcn_mfma_f32_16x16x4f32(a, b, c, 0, 0, 0);
@@ -66,7 +66,7 @@ struct PB16 {
   using A = float;
   using C = f4_t;
   using Fr = bf8_t;
-  static constexpr int KC = 32, KPL = 8, PAD = 8, PREC = PAINN_BF16, UNROLL = 2;
+  static constexpr int KC = 32, KPL = 8, PAD = 8, PREC = PAINN_BF16, UNROLL = 2, RING = 8;
   __device__ static __forceinline__ Fr frag(const T* p) { return *(const bf8_t*)p; }
   __device__ static __forceinline__ C mfma(Fr a, Fr b, C c) {
     return __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, b, c, 0, 0, 0);
@@ -80,6 +80,50 @@ struct PB16 {
 template <class A>
 __device__ __forceinline__ A silu(A x) {
   return x / (A(1) + (sizeof(A) == 8 ? (A)exp((double)-x) : (A)expf((float)-x)));
+}
+
+// A K loop with its operand loads running D steps ahead: use(kb, f) is
+// called for kb = 0 .. NKB-1 in order with the NS fragments load(kb, f)
+// fetched.  The loop runs over groups of D steps; step u of a group uses
+// ring slot u and refills it with the fragments D steps ahead, so the ring
+// is carried from group to group and D steps of loads stay in flight.
+// Short loops (NKB <= D) are unrolled whole with every load issued first.
+template <int NKB, int D, int NS, class Fr, class Load, class Use>
+__device__ __forceinline__ void kloop(Load&& load, Use&& use) {
+  if constexpr (NKB <= D) {
+    Fr all[NKB][NS];
+#pragma unroll
+    for (int kb = 0; kb < NKB; ++kb) load(kb, all[kb]);
+#pragma unroll
+    for (int kb = 0; kb < NKB; ++kb) use(kb, all[kb]);
+  } else {
+    static_assert(NKB % D == 0, "K steps must be a multiple of the prefetch distance");
+    Fr ring[D][NS];
+#pragma unroll
+    for (int u = 0; u < D; ++u) load(u, ring[u]);
+#pragma unroll 1
+    for (int k0 = 0; k0 < NKB - D; k0 += D) {
+#pragma unroll
+      for (int u = 0; u < D; ++u) {
+        Fr cur[NS];
+#pragma unroll
+        for (int q = 0; q < NS; ++q) cur[q] = ring[u][q];
+        load(k0 + D + u, ring[u]);
+        use(k0 + u, cur);
+      }
+    }
+#pragma unroll
+    for (int u = 0; u < D; ++u) use(NKB - D + u, ring[u]);
+  }
+}
+
+// Prefetch distance of a K loop over NS fragment streams: as many steps as
+// fit a ring of P::RING VGPRs (measured per precision: more spills the
+// update kernel at three waves per SIMD), a power of two from 1 to 8.
+template <class P, int NS>
+constexpr int ring_depth() {
+  constexpr int n = P::RING / (NS * (int)sizeof(typename P::Fr) / 4);
+  return n >= 8 ? 8 : n >= 4 ? 4 : n >= 2 ? 2 : 1;
 }
 
 // Dense layer over RT row tiles (16 rows each) held in LDS at X (row stride
@@ -108,9 +152,17 @@ __device__ __forceinline__ void dense_tiles(const typename P::T* X, int ldx, con
       }
     };
     if constexpr (NKB > 0) {
-      // several weight fragments in flight ahead of their MFMAs
-#pragma unroll P::UNROLL
-      for (int kb = 0; kb < NKB; ++kb) step(kb);
+      // weight fragments in flight P::UNROLL steps ahead of their MFMAs
+      using Fr = typename P::Fr;
+      kloop<NKB, ring_depth<P, 1>(), 1, Fr>(
+          [&](int kb, Fr* f) { f[0] = P::frag(wp + (size_t)kb * 64 * P::KPL); },
+          [&](int kb, Fr* f) {
+#pragma unroll
+            for (int r = 0; r < RT; ++r) {
+              const Fr a = P::frag(xp + (size_t)r * 16 * ldx + kb * P::KC);
+              acc[r] = P::mfma(a, f[0], acc[r]);
+            }
+          });
     } else {
       // groups of UNROLL steps, so their weight loads are issued together
       int kb = 0;
