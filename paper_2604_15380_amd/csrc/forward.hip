@@ -364,17 +364,17 @@ k_update(UpdArgs a) {
         for (int i = 0; i < 4; ++i) au[r][i] = av[r][i] = 0;
       const T* wu = Wuv + (size_t)ft * nkb * 64 * P::KPL + (size_t)lane * P::KPL;
       const T* wv = Wuv + (size_t)(NFT + ft) * nkb * 64 * P::KPL + (size_t)lane * P::KPL;
-      kloop<nkb, ring_depth<P, 2>(), 2, Fr>(
+      kloop<P, nkb, ring_depth<P, 2>(), 2, RT>(
+          xp, LD1,
           [&](int kb, Fr* f) {
             f[0] = P::frag(wu + (size_t)kb * 64 * P::KPL);
             f[1] = P::frag(wv + (size_t)kb * 64 * P::KPL);
           },
-          [&](int kb, Fr* f) {
+          [&](int kb, const Fr* x, const Fr* f) {
 #pragma unroll
             for (int r = 0; r < RT; ++r) {
-              const Fr x = P::frag(xp + r * 16 * LD1 + kb * P::KC);
-              au[r] = P::mfma(x, f[0], au[r]);
-              av[r] = P::mfma(x, f[1], av[r]);
+              au[r] = P::mfma(x[r], f[0], au[r]);
+              av[r] = P::mfma(x[r], f[1], av[r]);
             }
           });
 #pragma unroll
@@ -418,19 +418,19 @@ k_update(UpdArgs a) {
       const T* w0 = W2 + (size_t)ft * nkb2 * 64 * P::KPL + (size_t)lane * P::KPL;
       const T* w1 = W2 + (size_t)(NFT + ft) * nkb2 * 64 * P::KPL + (size_t)lane * P::KPL;
       const T* w2 = W2 + (size_t)(2 * NFT + ft) * nkb2 * 64 * P::KPL + (size_t)lane * P::KPL;
-      kloop<nkb2, ring_depth<P, 3>(), 3, Fr>(
+      kloop<P, nkb2, ring_depth<P, 3>(), 3, RT>(
+          xp, LD1,
           [&](int kb, Fr* f) {
             f[0] = P::frag(w0 + (size_t)kb * 64 * P::KPL);
             f[1] = P::frag(w1 + (size_t)kb * 64 * P::KPL);
             f[2] = P::frag(w2 + (size_t)kb * 64 * P::KPL);
           },
-          [&](int kb, Fr* f) {
+          [&](int kb, const Fr* x, const Fr* f) {
 #pragma unroll
             for (int r = 0; r < RT; ++r) {
-              const Fr x = P::frag(xp + r * 16 * LD1 + kb * P::KC);
-              avv[r] = P::mfma(x, f[0], avv[r]);
-              asv[r] = P::mfma(x, f[1], asv[r]);
-              ass[r] = P::mfma(x, f[2], ass[r]);
+              avv[r] = P::mfma(x[r], f[0], avv[r]);
+              asv[r] = P::mfma(x[r], f[1], asv[r]);
+              ass[r] = P::mfma(x[r], f[2], ass[r]);
             }
           });
       const int col = ft * 16 + (lane & 15);

@@ -12,6 +12,11 @@
 //      gfx950); P::row(l, i) gives it.
 // Weights are packed on the host in exactly the B order, so a B fragment is
 // one coalesced load per lane that the whole chip re-reads from L2.
+//
+// PAD is the LDS row padding (elements) of activation tiles, chosen so that
+// the 16 rows of one A-fragment read fall in distinct banks of the 32-bank
+// LDS: a row stride of 2 words (mod 32) for FP32, 1 double (mod 16) for
+// FP64 and 4 words for the 16-byte BF16 reads.
 #pragma once
 
 #include "internal.h"
@@ -34,7 +39,7 @@ struct P64 {
   using A = double;  // accumulation
   using C = d4_t;
   using Fr = double;
-  static constexpr int KC = 4, KPL = 1, PAD = 2, PREC = PAINN_FP64, UNROLL = 8, RING = 16;
+  static constexpr int KC = 4, KPL = 1, PAD = 1, PREC = PAINN_FP64, UNROLL = 8, RING = 16;
   __device__ static __forceinline__ Fr frag(const T* p) { return *p; }
   __device__ static __forceinline__ C mfma(Fr a, Fr b, C c) {
     return __builtin_amdgcn_mfma_f64_16x16x4f64(a, b, c, 0, 0, 0);
@@ -50,7 +55,7 @@ struct P32 {
   using A = float;
   using C = f4_t;
   using Fr = float;
-  static constexpr int KC = 4, KPL = 1, PAD = 4, PREC = PAINN_FP32, UNROLL = 8, RING = 24;
+  static constexpr int KC = 4, KPL = 1, PAD = 2, PREC = PAINN_FP32, UNROLL = 8, RING = 24;
   __device__ static __forceinline__ Fr frag(const T* p) { return *p; }
   __device__ static __forceinline__ C mfma(Fr a, Fr b, C c) {
     return __builtin_amdgcn_mfma_f32_16x16x4f32(a, b, c, 0, 0, 0);
@@ -82,38 +87,64 @@ __device__ __forceinline__ A silu(A x) {
   return x / (A(1) + (sizeof(A) == 8 ? (A)exp((double)-x) : (A)expf((float)-x)));
 }
 
-// A K loop with its operand loads running D steps ahead: use(kb, f) is
-// called for kb = 0 .. NKB-1 in order with the NS fragments load(kb, f)
-// fetched.  The loop runs over groups of D steps; step u of a group uses
-// ring slot u and refills it with the fragments D steps ahead, so the ring
-// is carried from group to group and D steps of loads stay in flight.
-// Short loops (NKB <= D) are unrolled whole with every load issued first.
-template <int NKB, int D, int NS, class Fr, class Load, class Use>
-__device__ __forceinline__ void kloop(Load&& load, Use&& use) {
+// A K loop of MFMA steps with its operands fetched ahead: mma(kb, a, b) runs
+// step kb with the RT activation fragments a (rows 16 r of xp, read from
+// LDS) and the NS weight fragments b = loadB(kb).  Weight loads run D steps
+// ahead on a ring of D x NS registers that is carried from one group of D
+// steps to the next; activation reads run one step ahead.  Scheduling
+// barriers around every step's MFMAs keep that order: left alone, the
+// scheduler sinks the ring refills to the end of the group (exposing the L2
+// latency once per group) and the next step's LDS reads below this step's
+// MFMAs.  Loops of at most D steps issue every load first.
+template <class P, int NKB, int D, int NS, int RT, class LoadB, class Mma>
+__device__ __forceinline__ void kloop(const typename P::T* xp, int ldx, LoadB&& loadB, Mma&& mma) {
+  using Fr = typename P::Fr;
+  auto loadA = [&](int kb, Fr* a) {
+#pragma unroll
+    for (int r = 0; r < RT; ++r) a[r] = P::frag(xp + (size_t)r * 16 * ldx + kb * P::KC);
+  };
   if constexpr (NKB <= D) {
-    Fr all[NKB][NS];
+    Fr b[NKB][NS], a[NKB][RT];
 #pragma unroll
-    for (int kb = 0; kb < NKB; ++kb) load(kb, all[kb]);
+    for (int kb = 0; kb < NKB; ++kb) loadB(kb, b[kb]);
 #pragma unroll
-    for (int kb = 0; kb < NKB; ++kb) use(kb, all[kb]);
+    for (int kb = 0; kb < NKB; ++kb) loadA(kb, a[kb]);
+#pragma unroll
+    for (int kb = 0; kb < NKB; ++kb) mma(kb, a[kb], b[kb]);
   } else {
     static_assert(NKB % D == 0, "K steps must be a multiple of the prefetch distance");
-    Fr ring[D][NS];
+    Fr ring[D][NS], a0[RT];
 #pragma unroll
-    for (int u = 0; u < D; ++u) load(u, ring[u]);
+    for (int u = 0; u < D; ++u) {
+      loadB(u, ring[u]);
+      __builtin_amdgcn_sched_barrier(0);   // keep the ring in step order
+    }
+    loadA(0, a0);
 #pragma unroll 1
     for (int k0 = 0; k0 < NKB - D; k0 += D) {
 #pragma unroll
       for (int u = 0; u < D; ++u) {
-        Fr cur[NS];
+        Fr an[RT];
+        loadA(k0 + u + 1, an);
+        __builtin_amdgcn_sched_barrier(0);
+        mma(k0 + u, a0, ring[u]);
+        loadB(k0 + u + D, ring[u]);
 #pragma unroll
-        for (int q = 0; q < NS; ++q) cur[q] = ring[u][q];
-        load(k0 + D + u, ring[u]);
-        use(k0 + u, cur);
+        for (int r = 0; r < RT; ++r) a0[r] = an[r];
+        __builtin_amdgcn_sched_barrier(0);
       }
     }
 #pragma unroll
-    for (int u = 0; u < D; ++u) use(NKB - D + u, ring[u]);
+    for (int u = 0; u < D; ++u) {
+      Fr an[RT];
+      if (u + 1 < D) loadA(NKB - D + u + 1, an);
+      __builtin_amdgcn_sched_barrier(0);
+      mma(NKB - D + u, a0, ring[u]);
+      if (u + 1 < D)
+#pragma unroll
+        for (int r = 0; r < RT; ++r) a0[r] = an[r];
+      __builtin_amdgcn_sched_barrier(0);
+    }
   }
 }
 
@@ -154,14 +185,11 @@ __device__ __forceinline__ void dense_tiles(const typename P::T* X, int ldx, con
     if constexpr (NKB > 0) {
       // weight fragments in flight P::UNROLL steps ahead of their MFMAs
       using Fr = typename P::Fr;
-      kloop<NKB, ring_depth<P, 1>(), 1, Fr>(
-          [&](int kb, Fr* f) { f[0] = P::frag(wp + (size_t)kb * 64 * P::KPL); },
-          [&](int kb, Fr* f) {
+      kloop<P, NKB, ring_depth<P, 1>(), 1, RT>(
+          xp, ldx, [&](int kb, Fr* f) { f[0] = P::frag(wp + (size_t)kb * 64 * P::KPL); },
+          [&](int kb, const Fr* a, const Fr* f) {
 #pragma unroll
-            for (int r = 0; r < RT; ++r) {
-              const Fr a = P::frag(xp + (size_t)r * 16 * ldx + kb * P::KC);
-              acc[r] = P::mfma(a, f[0], acc[r]);
-            }
+            for (int r = 0; r < RT; ++r) acc[r] = P::mfma(a[r], f[0], acc[r]);
           });
     } else {
       // groups of UNROLL steps, so their weight loads are issued together
