@@ -811,98 +811,136 @@ k_message_lane(MsgArgs a) {
   if (i0 >= a.N) return;
   const int i1 = min(a.N, i0 + MSG_RB2);
   const int rp_lane = a.row_ptr[i0 + min(lane, i1 - i0)];
-  for (int i = i0; i < i1; ++i) {
-    const int ea = __builtin_amdgcn_readlane(rp_lane, i - i0);
-    const int eb = __builtin_amdgcn_readlane(rp_lane, i - i0 + 1);
-    const size_t ib = (size_t)i * 3 * F;
-    const T s_old = s[(size_t)i * F + c];
-    const T v_old0 = vin[ib + c], v_old1 = vin[ib + F + c], v_old2 = vin[ib + 2 * F + c];
-    A acc_s = 0, acc_v0 = 0, acc_v1 = 0, acc_v2 = 0;
-    for (int c0 = ea; c0 < eb; c0 += 16) {
-      const int cnt = min(16, eb - c0);
-      const T* gp = basis + (size_t)(c0 + (lane & 15)) * kcols + (lane >> 4) * P::KPL;
-      // A rows past the chunk's end are zeroed, so are their filter rows
-      const bool row_ok = (lane & 15) < cnt;
-      Fr Ga[KBM];
+  auto rp = [&](int i) { return __builtin_amdgcn_readlane(rp_lane, i - i0); };
+  // receivers without edges: v_out = v_in, s unchanged
+  for (int i = i0; i < i1; ++i)
+    if (rp(i) == rp(i + 1)) {
+      const size_t ib = (size_t)i * 3 * F;
+      vout[ib + c] = vin[ib + c];
+      vout[ib + F + c] = vin[ib + F + c];
+      vout[ib + 2 * F + c] = vin[ib + 2 * F + c];
+    }
+  auto first_with_edges = [&](int i) {
+    while (i < i1 && rp(i) == rp(i + 1)) ++i;
+    return i;
+  };
+  // The block's receivers are walked as one stream of chunks of up to 16
+  // edges of one receiver.  The next chunk's basis rows and edge info are
+  // loaded while the current one is processed (the basis streams from HBM).
+  Fr Gn[KBM];
+  A exn = 0, eyn = 0, ezn = 0, ejn = 0;
+  auto prefetch = [&](int cc0, int ccnt) {
+    const T* gp = basis + (size_t)(cc0 + (lane & 15)) * kcols + (lane >> 4) * P::KPL;
 #pragma unroll
-      for (int kb = 0; kb < KBM; ++kb) {
-        const Fr g = P::frag(gp + kb * P::KC);
-        Ga[kb] = row_ok ? g : Fr{};
-      }
-      // lanes e < cnt hold edge c0 + e: rhat and the sender index
-      A ex = 0, ey = 0, ez = 0, ej = 0;
-      if (lane < cnt) {
-        const A* ei = einfo + 4 * (size_t)(c0 + lane);
-        ex = ei[0];
-        ey = ei[1];
-        ez = ei[2];
-        ej = ei[3];
-      }
-      // The filter of 4 feature tiles x 3 parts, parked in LDS.  With few
-      // registers held by the B fragments all 12 MFMA chains are issued
-      // together (QI = 4); otherwise one feature tile at a time (QI = 1).
+    for (int kb = 0; kb < KBM; ++kb) Gn[kb] = P::frag(gp + kb * P::KC);
+    exn = eyn = ezn = ejn = 0;
+    if (lane < ccnt) {
+      const A* ei = einfo + 4 * (size_t)(cc0 + lane);
+      exn = ei[0];
+      eyn = ei[1];
+      ezn = ei[2];
+      ejn = ei[3];
+    }
+  };
+  int i = first_with_edges(i0);
+  if (i >= i1) return;
+  int c0 = rp(i);
+  prefetch(c0, min(16, rp(i + 1) - c0));
+  size_t ib = (size_t)i * 3 * F;
+  T s_old = s[(size_t)i * F + c];
+  T v_old0 = vin[ib + c], v_old1 = vin[ib + F + c], v_old2 = vin[ib + 2 * F + c];
+  A acc_s = 0, acc_v0 = 0, acc_v1 = 0, acc_v2 = 0;
+  while (true) {
+    const int eb = rp(i + 1);
+    const int cnt = min(16, eb - c0);
+    // A rows past the chunk's end are zeroed, so are their filter rows
+    const bool row_ok = (lane & 15) < cnt;
+    Fr Ga[KBM];
 #pragma unroll
-      for (int q0 = 0; q0 < 4; q0 += QI) {
-        C w[QI][3];
+    for (int kb = 0; kb < KBM; ++kb) Ga[kb] = row_ok ? Gn[kb] : Fr{};
+    // lanes e < cnt hold edge c0 + e: rhat and the sender index
+    const A ex = exn, ey = eyn, ez = ezn, ej = ejn;
+    // the next chunk: this receiver's next 16 edges, else the next receiver
+    const bool last = c0 + 16 >= eb;
+    const int in = last ? first_with_edges(i + 1) : i;
+    const bool more = in < i1;
+    const int cn = last ? (more ? rp(in) : 0) : c0 + 16;
+    if (more) prefetch(cn, min(16, rp(in + 1) - cn));
+    // The filter of 4 feature tiles x 3 parts, parked in LDS.  With few
+    // registers held by the B fragments all 12 MFMA chains are issued
+    // together (QI = 4); otherwise one feature tile at a time (QI = 1).
+#pragma unroll
+    for (int q0 = 0; q0 < 4; q0 += QI) {
+      C w[QI][3];
+#pragma unroll
+      for (int q = 0; q < QI; ++q)
+#pragma unroll
+        for (int part = 0; part < 3; ++part)
+          for (int r = 0; r < 4; ++r) w[q][part][r] = 0;
+#pragma unroll
+      for (int kb = 0; kb < KBM; ++kb)
 #pragma unroll
         for (int q = 0; q < QI; ++q)
 #pragma unroll
           for (int part = 0; part < 3; ++part)
-            for (int r = 0; r < 4; ++r) w[q][part][r] = 0;
+            w[q][part] = P::mfma(Ga[kb], Bf[q0 + q][part][kb], w[q][part]);
 #pragma unroll
-        for (int kb = 0; kb < KBM; ++kb)
+      for (int q = 0; q < QI; ++q) {
+        const int col = 16 * (q0 + q) + (lane & 15);
 #pragma unroll
-          for (int q = 0; q < QI; ++q)
-#pragma unroll
-            for (int part = 0; part < 3; ++part)
-              w[q][part] = P::mfma(Ga[kb], Bf[q0 + q][part][kb], w[q][part]);
-#pragma unroll
-        for (int q = 0; q < QI; ++q) {
-          const int col = 16 * (q0 + q) + (lane & 15);
-#pragma unroll
-          for (int r = 0; r < 4; ++r) {
-            const int row = P::row(lane, r);
-            wt0[row * WLD + col] = w[q][0][r];
-            wt1[row * WLD + col] = w[q][1][r];
-            wt2[row * WLD + col] = w[q][2][r];
-          }
+        for (int r = 0; r < 4; ++r) {
+          const int row = P::row(lane, r);
+          wt0[row * WLD + col] = w[q][0][r];
+          wt1[row * WLD + col] = w[q][1][r];
+          wt2[row * WLD + col] = w[q][2][r];
         }
       }
-      __builtin_amdgcn_wave_barrier();
-      __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
-      __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
-      // Edges are taken EG at a time with no early exit, so all 6 EG gathers
-      // of a group can be in flight together: past the chunk's end the sender
-      // is row 0 (lanes >= cnt hold index 0) and the filter rows are zero.
-      auto edges = [&](int ebase) {
-#pragma unroll
-        for (int u = 0; u < EG; ++u) {
-          const int e = ebase + u;
-          const int j = acc_to_index(bcast(ej, e));
-          const A rx = bcast(ex, e), ry = bcast(ey, e), rz = bcast(ez, e);
-          const T* hj = h + (size_t)j * 3 * F + c;
-          const T* vj = vin + (size_t)j * 3 * F + c;
-          const A hs = P::ld(hj[0]), hv = P::ld(hj[F]), hr = P::ld(hj[2 * F]);
-          const A v0 = P::ld(vj[0]), v1 = P::ld(vj[F]), v2 = P::ld(vj[2 * F]);
-          const A ws = wt0[e * WLD + lane], wv = wt1[e * WLD + lane], wr = wt2[e * WLD + lane];
-          acc_s += hs * ws;
-          const A pv = hv * wv, pr = hr * wr;
-          acc_v0 += v0 * pv + rx * pr;
-          acc_v1 += v1 * pv + ry * pr;
-          acc_v2 += v2 * pv + rz * pr;
-        }
-      };
-#pragma unroll
-      for (int eb0 = 0; eb0 < 16; eb0 += EG)
-        if (eb0 < cnt) edges(eb0);
-      __builtin_amdgcn_wave_barrier();
-      __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
-      __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
     }
-    s[(size_t)i * F + c] = P::st(P::ld(s_old) + acc_s);
-    vout[ib + c] = P::st(P::ld(v_old0) + acc_v0);
-    vout[ib + F + c] = P::st(P::ld(v_old1) + acc_v1);
-    vout[ib + 2 * F + c] = P::st(P::ld(v_old2) + acc_v2);
+    __builtin_amdgcn_wave_barrier();
+    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+    // Edges are taken EG at a time with no early exit, so all 6 EG gathers
+    // of a group can be in flight together: past the chunk's end the sender
+    // is row 0 (lanes >= cnt hold index 0) and the filter rows are zero.
+    auto edges = [&](int ebase) {
+#pragma unroll
+      for (int u = 0; u < EG; ++u) {
+        const int e = ebase + u;
+        const int j = acc_to_index(bcast(ej, e));
+        const A rx = bcast(ex, e), ry = bcast(ey, e), rz = bcast(ez, e);
+        const T* hj = h + (size_t)j * 3 * F + c;
+        const T* vj = vin + (size_t)j * 3 * F + c;
+        const A hs = P::ld(hj[0]), hv = P::ld(hj[F]), hr = P::ld(hj[2 * F]);
+        const A v0 = P::ld(vj[0]), v1 = P::ld(vj[F]), v2 = P::ld(vj[2 * F]);
+        const A ws = wt0[e * WLD + lane], wv = wt1[e * WLD + lane], wr = wt2[e * WLD + lane];
+        acc_s += hs * ws;
+        const A pv = hv * wv, pr = hr * wr;
+        acc_v0 += v0 * pv + rx * pr;
+        acc_v1 += v1 * pv + ry * pr;
+        acc_v2 += v2 * pv + rz * pr;
+      }
+    };
+#pragma unroll
+    for (int eb0 = 0; eb0 < 16; eb0 += EG)
+      if (eb0 < cnt) edges(eb0);
+    __builtin_amdgcn_wave_barrier();
+    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+    if (last) {
+      s[(size_t)i * F + c] = P::st(P::ld(s_old) + acc_s);
+      vout[ib + c] = P::st(P::ld(v_old0) + acc_v0);
+      vout[ib + F + c] = P::st(P::ld(v_old1) + acc_v1);
+      vout[ib + 2 * F + c] = P::st(P::ld(v_old2) + acc_v2);
+      if (!more) break;
+      acc_s = acc_v0 = acc_v1 = acc_v2 = 0;
+      ib = (size_t)in * 3 * F;
+      s_old = s[(size_t)in * F + c];
+      v_old0 = vin[ib + c];
+      v_old1 = vin[ib + F + c];
+      v_old2 = vin[ib + 2 * F + c];
+    }
+    i = in;
+    c0 = cn;
   }
 }
 
