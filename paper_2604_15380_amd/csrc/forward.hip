@@ -781,6 +781,10 @@ k_message_lane(MsgArgs a) {
   constexpr int BF_REGS = 12 * KBM * (int)sizeof(Fr) / 4;
   constexpr int QI = BF_REGS > 100 ? 1 : 4;     // MFMA chains issued together (feature tiles)
   constexpr int EG = BF_REGS > 100 ? 4 : 8;     // edges gathered per group
+  // Issue the first group's gathers ahead of the filter MFMAs.  Measured: a
+  // gain for BF16 with a short filter (few K blocks), a loss for FP32, whose
+  // gathers move twice the bytes behind a long MFMA phase.
+  constexpr bool EARLY = sizeof(T) == 2 && BF_REGS <= 100;
   __shared__ A Wt[NW][3][16 * WLD];
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int c = 64 * wave + lane;               // this lane's channel
@@ -866,6 +870,44 @@ k_message_lane(MsgArgs a) {
     const bool more = in < i1;
     const int cn = last ? (more ? rp(in) : 0) : c0 + 16;
     if (more) prefetch(cn, min(16, rp(in + 1) - cn));
+    // Gathers of EG edges: sender rows h_j (3 parts) and v_j (3 components)
+    // at this lane's channel.  Past the chunk's end the sender is row 0
+    // (lanes >= cnt hold index 0) and the filter rows are zero, so a group
+    // needs no early exit and all its 6 EG loads can be in flight together.
+    T gb[6][EG];
+    auto gather = [&](int ebase) {
+#pragma unroll
+      for (int u = 0; u < EG; ++u) {
+        const int j = acc_to_index(bcast(ej, ebase + u));
+        const T* hj = h + (size_t)j * 3 * F + c;
+        const T* vj = vin + (size_t)j * 3 * F + c;
+        gb[0][u] = hj[0];
+        gb[1][u] = hj[F];
+        gb[2][u] = hj[2 * F];
+        gb[3][u] = vj[0];
+        gb[4][u] = vj[F];
+        gb[5][u] = vj[2 * F];
+      }
+    };
+    auto consume = [&](int ebase) {
+#pragma unroll
+      for (int u = 0; u < EG; ++u) {
+        const int e = ebase + u;
+        const A rx = bcast(ex, e), ry = bcast(ey, e), rz = bcast(ez, e);
+        const A ws = wt0[e * WLD + lane], wv = wt1[e * WLD + lane], wr = wt2[e * WLD + lane];
+        acc_s += P::ld(gb[0][u]) * ws;
+        const A pv = P::ld(gb[1][u]) * wv, pr = P::ld(gb[2][u]) * wr;
+        acc_v0 += P::ld(gb[3][u]) * pv + rx * pr;
+        acc_v1 += P::ld(gb[4][u]) * pv + ry * pr;
+        acc_v2 += P::ld(gb[5][u]) * pv + rz * pr;
+      }
+    };
+    // the first group's gathers do not depend on the filter: issued before
+    // the MFMAs, they arrive while the matrix cores run
+    if constexpr (EARLY) {
+      gather(0);
+      __builtin_amdgcn_sched_barrier(0);
+    }
     // The filter of 4 feature tiles x 3 parts, parked in LDS.  With few
     // registers held by the B fragments all 12 MFMA chains are issued
     // together (QI = 4); otherwise one feature tile at a time (QI = 1).
@@ -899,30 +941,13 @@ k_message_lane(MsgArgs a) {
     __builtin_amdgcn_wave_barrier();
     __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
     __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
-    // Edges are taken EG at a time with no early exit, so all 6 EG gathers
-    // of a group can be in flight together: past the chunk's end the sender
-    // is row 0 (lanes >= cnt hold index 0) and the filter rows are zero.
-    auto edges = [&](int ebase) {
+    if constexpr (EARLY) consume(0);
 #pragma unroll
-      for (int u = 0; u < EG; ++u) {
-        const int e = ebase + u;
-        const int j = acc_to_index(bcast(ej, e));
-        const A rx = bcast(ex, e), ry = bcast(ey, e), rz = bcast(ez, e);
-        const T* hj = h + (size_t)j * 3 * F + c;
-        const T* vj = vin + (size_t)j * 3 * F + c;
-        const A hs = P::ld(hj[0]), hv = P::ld(hj[F]), hr = P::ld(hj[2 * F]);
-        const A v0 = P::ld(vj[0]), v1 = P::ld(vj[F]), v2 = P::ld(vj[2 * F]);
-        const A ws = wt0[e * WLD + lane], wv = wt1[e * WLD + lane], wr = wt2[e * WLD + lane];
-        acc_s += hs * ws;
-        const A pv = hv * wv, pr = hr * wr;
-        acc_v0 += v0 * pv + rx * pr;
-        acc_v1 += v1 * pv + ry * pr;
-        acc_v2 += v2 * pv + rz * pr;
+    for (int eb0 = EARLY ? EG : 0; eb0 < 16; eb0 += EG)
+      if (eb0 < cnt) {
+        gather(eb0);
+        consume(eb0);
       }
-    };
-#pragma unroll
-    for (int eb0 = 0; eb0 < 16; eb0 += EG)
-      if (eb0 < cnt) edges(eb0);
     __builtin_amdgcn_wave_barrier();
     __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
     __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
