@@ -25,13 +25,28 @@ struct DevStatus {      // read back once per build_graph
   int32_t err;
   int32_t species_min;
   int32_t species_max;
-  int32_t pad;
+  int32_t cells;        // structures searched with a cell list
 };
 
 struct StructInfo {     // per structure: atom range and periodic image range
   int32_t lo, n;
   int32_t m0, m1, m2;   // |n_k| <= m_k
   int32_t nimg;         // (2 m0 + 1)(2 m1 + 1)(2 m2 + 1)
+};
+
+// Cell-list binning of one structure (nb[0] == 0: every pair is tested).
+// Bins are at least r_c wide, so every neighbour of an atom lies in the 27
+// bins around its own.  Molecules bin Cartesian coordinates over their
+// bounding box; periodic cells (all three axes periodic, >= 3 bins each) bin
+// the wrapped fractional coordinates.
+struct CellGrid {
+  int32_t nb[3];
+  int32_t base;         // first bin of the structure in the batch's bin arrays
+  int32_t periodic;
+  int32_t pad;
+  double o[3];          // molecules: bin coordinate u_k = (x_k - o_k) s_k
+  double s[3];          // periodic:  u_k = (f_k - floor f_k) s_k
+  double fr[9];         // periodic:  fractional coordinates f_k = x . fr_k
 };
 
 // ---- dense-layer packing ---------------------------------------------------
@@ -136,7 +151,15 @@ struct painn_graph {
   int32_t* struct_ptr = nullptr;
   long long* scan_tmp = nullptr;
   DevStatus* d_status = nullptr;
-  size_t cap_atoms = 0, cap_struct = 0, cap_edges = 0, cap_scan = 0;
+  // cell lists: per structure grid, per atom bin and wrap (fractional floor),
+  // per bin count and start.  Structure b owns bins [2 lo_b + 27 b, ...) and
+  // uses at most 2 n_b + 27 of them, so n_bins = 2 N + 27 B covers a batch.
+  CellGrid* grid = nullptr;
+  int32_t* bin_of = nullptr;   int32_t* wrap = nullptr;   int32_t* bin_atoms = nullptr;
+  int32_t* bin_count = nullptr; int32_t* bin_start = nullptr;
+  long long* bin_scan_tmp = nullptr;
+  size_t n_bins = 0;
+  size_t cap_atoms = 0, cap_struct = 0, cap_edges = 0, cap_scan = 0, cap_bins = 0, cap_bin_scan = 0;
 };
 
 // ---- kernel launchers (each enqueues on `s`, returns hipGetLastError) ------

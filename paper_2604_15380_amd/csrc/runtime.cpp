@@ -490,7 +490,8 @@ painn_status painn_graph_free(painn_graph* g) {
     (void)hipStreamSynchronize(g->ctx->stream);
   }
   void* bufs[] = {g->row_ptr, g->counts, g->col, g->shift, g->recv, g->pos, g->species, g->atom_struct,
-                  g->cell, g->sinfo, g->struct_ptr, g->scan_tmp, g->d_status};
+                  g->cell, g->sinfo, g->struct_ptr, g->scan_tmp, g->d_status, g->grid, g->bin_of,
+                  g->wrap, g->bin_atoms, g->bin_count, g->bin_start, g->bin_scan_tmp};
   for (void* p : bufs)
     if (p) (void)hipFree(p);
   delete g;
@@ -530,31 +531,49 @@ painn_status painn_build_graph(painn_ctx* ctx, int32_t B, int32_t N, const int32
   size_t capa = g->cap_atoms, caps = g->cap_struct, capsc = g->cap_scan;
   // per-atom buffers share one capacity
   if (N + 1 > (long long)g->cap_atoms || !g->row_ptr) {
-    size_t c0 = 0, c1 = 0, c2 = 0, c3 = 0, c4 = 0;
-    if (g->row_ptr) { (void)hipFree(g->row_ptr); g->row_ptr = nullptr; }
-    if (g->counts) { (void)hipFree(g->counts); g->counts = nullptr; }
-    if (g->pos) { (void)hipFree(g->pos); g->pos = nullptr; }
-    if (g->species) { (void)hipFree(g->species); g->species = nullptr; }
-    if (g->atom_struct) { (void)hipFree(g->atom_struct); g->atom_struct = nullptr; }
+    size_t c0 = 0, c1 = 0, c2 = 0, c3 = 0, c4 = 0, c5 = 0, c6 = 0, c7 = 0;
+    void** old[] = {(void**)&g->row_ptr, (void**)&g->counts, (void**)&g->pos, (void**)&g->species,
+                    (void**)&g->atom_struct, (void**)&g->bin_of, (void**)&g->wrap, (void**)&g->bin_atoms};
+    for (void** q : old)
+      if (*q) { (void)hipFree(*q); *q = nullptr; }
     e = ensure(&g->row_ptr, &c0, (size_t)N + 1);
     if (e == hipSuccess) e = ensure(&g->counts, &c1, c0);
     if (e == hipSuccess) e = ensure(&g->pos, &c2, 3 * c0);
     if (e == hipSuccess) e = ensure(&g->species, &c3, c0);
     if (e == hipSuccess) e = ensure(&g->atom_struct, &c4, c0);
+    if (e == hipSuccess) e = ensure(&g->bin_of, &c5, c0);
+    if (e == hipSuccess) e = ensure(&g->wrap, &c6, 3 * c0);
+    if (e == hipSuccess) e = ensure(&g->bin_atoms, &c7, c0);
     capa = c0;
   }
   if (e == hipSuccess && (B + 1 > (long long)g->cap_struct || !g->sinfo)) {
-    size_t c0 = 0, c1 = 0, c2 = 0;
+    size_t c0 = 0, c1 = 0, c2 = 0, c3 = 0;
     if (g->sinfo) { (void)hipFree(g->sinfo); g->sinfo = nullptr; }
     if (g->cell) { (void)hipFree(g->cell); g->cell = nullptr; }
     if (g->struct_ptr) { (void)hipFree(g->struct_ptr); g->struct_ptr = nullptr; }
+    if (g->grid) { (void)hipFree(g->grid); g->grid = nullptr; }
     e = ensure(&g->sinfo, &c0, (size_t)B + 1);
     if (e == hipSuccess) e = ensure(&g->cell, &c1, 9 * c0);
     if (e == hipSuccess) e = ensure(&g->struct_ptr, &c2, c0);
+    if (e == hipSuccess) e = ensure(&g->grid, &c3, c0);
     caps = c0;
   }
   size_t nblk = ((size_t)N + 1023) / 1024 + 1;
   if (e == hipSuccess) e = ensure(&g->scan_tmp, &capsc, nblk);
+  // cell-list bins: structure b owns [2 lo_b + 27 b, 2 hi_b + 27 (b + 1))
+  g->n_bins = 2 * (size_t)N + 27 * (size_t)B;
+  size_t capb = g->cap_bins, capbs = g->cap_bin_scan;
+  if (e == hipSuccess && (g->n_bins + 1 > g->cap_bins || !g->bin_count)) {
+    size_t c0 = 0, c1 = 0;
+    if (g->bin_count) { (void)hipFree(g->bin_count); g->bin_count = nullptr; }
+    if (g->bin_start) { (void)hipFree(g->bin_start); g->bin_start = nullptr; }
+    e = ensure(&g->bin_count, &c0, g->n_bins + 1);
+    if (e == hipSuccess) e = ensure(&g->bin_start, &c1, c0);
+    capb = c0;
+  }
+  if (e == hipSuccess) e = ensure(&g->bin_scan_tmp, &capbs, (g->n_bins + 1023) / 1024 + 1);
+  g->cap_bins = capb;
+  g->cap_bin_scan = capbs;
   if (e == hipSuccess && !g->d_status) e = hipMalloc((void**)&g->d_status, sizeof(DevStatus));
   if (e != hipSuccess) return bail(PAINN_E_OOM, std::string("device allocation: ") + hipGetErrorString(e));
   g->cap_atoms = capa;

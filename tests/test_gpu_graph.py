@@ -150,3 +150,55 @@ def test_errors(rt):
         rt.build_graph(rt.upload_batch(good), 0.0)
     # the context still works after errors
     assert_same_csr(gpu_csr(rt, good, 5.0), batch_graph(good, 5.0))
+
+
+def _large_structures():
+    """Structures large enough for the cell-list search (>= 64 bins of width
+    r_c = 5): a molecule, a periodic cube with some atoms stored up to two
+    cells outside, a triclinic cell and a flat molecule; plus small molecules
+    that keep the all-pairs search in the same batch."""
+    rng = np.random.default_rng(5)
+    out = []
+    n = 900
+    a = 2.5 * n ** (1 / 3)
+    out.append((rng.uniform(0, a, (n, 3)), np.zeros((3, 3)), np.zeros(3, np.uint8)))
+    n = 700
+    L = (n / 0.08) ** (1 / 3)
+    p = rng.uniform(0, L, (n, 3))
+    p[:50] += L * rng.integers(-2, 3, (50, 3))
+    out.append((p, np.eye(3) * L, np.ones(3, np.uint8)))
+    cell = np.array([[22.0, 0, 0], [4.0, 21.0, 0], [-3.0, 2.5, 23.0]])
+    out.append((rng.uniform(0, 1, (600, 3)) @ cell, cell, np.ones(3, np.uint8)))
+    p = rng.uniform(0, 40, (500, 3))
+    p[:, 2] = 1.0
+    out.append((p, np.zeros((3, 3)), np.zeros(3, np.uint8)))
+    for _ in range(3):
+        n = int(rng.integers(5, 30))
+        out.append((rng.uniform(0, 2.5 * n ** (1 / 3), (n, 3)), np.zeros((3, 3)), np.zeros(3, np.uint8)))
+    return [(p, rng.integers(0, 10, len(p)).astype(np.int32), c, f, 0) for p, c, f in out]
+
+
+def test_cell_list_matches_brute_force(rt):
+    """The cell-list search gives the oracle's CSR bit for bit (set and order),
+    including periodic wraps of atoms stored outside the cell, a triclinic
+    cell and a degenerate (flat) bounding box, next to all-pairs structures."""
+    say("graph parity: cell lists")
+    b = synth.concat(_large_structures())
+    assert_same_csr(gpu_csr(rt, b, 5.0), batch_graph(b, 5.0))
+
+
+def test_cell_list_dense_receivers(rt):
+    """Receivers with more neighbours than the fill pass ranks in LDS (a
+    dense cluster inside a large sparse molecule) are filled by the all-pairs
+    enumeration; the CSR is still the oracle's."""
+    say("graph parity: cell list, dense cluster")
+    rng = np.random.default_rng(9)
+    sparse = rng.uniform(0, 40, (800, 3))
+    v = rng.normal(size=(300, 3))
+    dense = 20.0 + v / np.linalg.norm(v, axis=1, keepdims=True) * rng.uniform(0, 1, (300, 1)) ** (1 / 3) * 2.4
+    pos = np.concatenate([sparse, dense])
+    s = (pos, np.zeros(len(pos), np.int32), np.zeros((3, 3)), np.zeros(3, np.uint8), 0)
+    b = synth.concat([s])
+    rp, col, sh = gpu_csr(rt, b, 5.0)
+    assert np.diff(rp).max() > 256
+    assert_same_csr((rp, col, sh), batch_graph(b, 5.0))
