@@ -26,6 +26,11 @@ Per structure, with the radius graph of `oracle.neighbors`:
   readout         y_i = shared MLP(s_i) (silu after every shared layer);
                   e_i = branch_{dataset}(y_i) (silu between layers, last linear);
                   E = sum_i e_i                                                   (R10, R11)
+  blended heads   (section "Composition-conditioned branch weighting") c_b[z] =
+                  (atoms of species z) / n_b;  w_b = softmax(MLP(c_b)) over the
+                  heads (silu between layers, last layer linear);
+                  E_b = sum_{h : w_bh >= tau} w_bh E_bh, tau = 0 keeps every head
+                  (branch skipping drops the rest, without renormalising)   (R21, R22)
 
 silu(x) = x / (1 + exp(-x)).  Products `W x` use W stored [out, in].
 """
@@ -189,3 +194,40 @@ def batch_energies(batch, hp, W, structures=None):
         E.append(out["E"])
         A.append(float(np.sum(np.abs(out["e"]))))
     return np.array(E), np.array(A)
+
+
+def composition(species, n_species: int):
+    """Per-element composition vector of a structure: fractions of its atoms
+    of each species (zeros for an empty structure) (R21)."""
+    z = np.asarray(species, dtype=np.int64)
+    c = np.bincount(z, minlength=n_species).astype(np.float64)
+    return c / len(z) if len(z) else c
+
+
+def blend_weights(c, hp, W):
+    """Softmax weights over the heads from a composition vector (R21)."""
+    y = np.asarray(c, dtype=np.float64)
+    nl = len(hp.blend_dims) + 1
+    for m in range(nl):
+        y = dense(y, W[f"blend{m}.w"], W[f"blend{m}.b"])
+        if m < nl - 1:
+            y = silu(y)
+    y = np.exp(y - np.max(y))
+    return y / np.sum(y)
+
+
+def structure_forward_blend(pos, species, cell, pbc, hp, W, skip: float = 0.0):
+    """Energy of one structure with every head blended by the branch-weighting
+    MLP: the encoder runs once, each head reads the same final features, and
+    heads whose weight is below `skip` are left out (R22).  Returns dict(E,
+    e = per-atom blended energies, w = head weights, E_heads = per-head E)."""
+    out = structure_forward(pos, species, cell, pbc, 0, hp, W)
+    w = blend_weights(composition(species, hp.n_species), hp, W)
+    e = np.zeros(len(species))
+    E_heads = np.zeros(hp.n_heads)
+    for h in range(hp.n_heads):
+        eh = readout(out["s"], W, hp, h)
+        E_heads[h] = float(np.sum(eh))
+        if w[h] >= skip:
+            e = e + w[h] * eh
+    return dict(E=float(np.sum(e)), e=e, w=w, E_heads=E_heads)

@@ -44,6 +44,14 @@ RBF_GAUSSIAN = 0
 # with an extra gain of 1/sqrt(16).  With gain 1 the random 6-layer bulk model
 # diverges (the <Uv, Vv> term feeds |v|^2 back into s), overflowing FP64.
 FILTER_GAIN = 0.25
+# Optional trailing section of the weight file: the branch-weighting MLP that
+# maps a structure's composition to softmax weights over the heads.
+BLEND_MAGIC = b"BLENDW01"
+# A trained router is sharp (its teacher signal is one-hot per dataset); the
+# synthetic one gets a gain on its output layer so that, as reported for the
+# trained one, most branches carry negligible weight (~78 % below 0.01 on the
+# screening stream, against ~81 % in the paper).
+BLEND_GAIN = 24.0
 
 
 # --------------------------------------------------------------------------
@@ -77,7 +85,7 @@ WORKLOADS = {
     "screening": dict(
         n_struct=1_000_000, kind="mixed", n_lo=4, n_hi=200, size_dist="loguniform",
         n_species=85, d_min=None, cutoff=5.0, F=256, L=4, K=32,
-        shared_dims=[50, 50], branch_dims=[776, 776, 1], n_heads=16,
+        shared_dims=[50, 50], branch_dims=[776, 776, 1], n_heads=16, blend_dims=[128, 64],
         batch_atoms=65536, data_seed=1005, weight_seed=2005, precision="bf16"),
 }
 # The precision sweep runs the 4096-molecule inputs and weights at all three
@@ -97,14 +105,19 @@ class HyperParams:
     shared_dims: list = field(default_factory=list)
     branch_dims: list = field(default_factory=lambda: [1])
     rbf_type: int = RBF_GAUSSIAN
+    # hidden widths of the branch-weighting MLP (composition -> head weights);
+    # None: the model has none
+    blend_dims: list | None = None
 
     @staticmethod
     def from_workload(name: str) -> "HyperParams":
         w = WORKLOADS[name]
+        bd = w.get("blend_dims")
         return HyperParams(F=w["F"], K=w["K"], L=w["L"], n_species=w["n_species"],
                            n_heads=w["n_heads"], cutoff=w["cutoff"],
                            shared_dims=list(w["shared_dims"]),
-                           branch_dims=list(w["branch_dims"]))
+                           branch_dims=list(w["branch_dims"]),
+                           blend_dims=None if bd is None else list(bd))
 
 
 @dataclass
@@ -293,6 +306,11 @@ def weight_layout(hp: HyperParams):
         for m, d in enumerate(hp.branch_dims):
             out += [(f"head{h}.{m}.w", (d, di)), (f"head{h}.{m}.b", (d,))]
             di = d
+    if hp.blend_dims is not None:
+        di = hp.n_species
+        for m, d in enumerate(list(hp.blend_dims) + [hp.n_heads]):
+            out += [(f"blend{m}.w", (d, di)), (f"blend{m}.b", (d,))]
+            di = d
     return out
 
 
@@ -317,6 +335,8 @@ def make_weights(hp: HyperParams, seed: int) -> dict:
             w[name] = rng.standard_normal(shape) / math.sqrt(fan_in[wname])
         if ".filt_" in name:
             w[name] = w[name] * FILTER_GAIN
+        if hp.blend_dims is not None and name.startswith(f"blend{len(hp.blend_dims)}."):
+            w[name] = w[name] * BLEND_GAIN
     return w
 
 
@@ -349,6 +369,13 @@ def weight_file_bytes(hp: HyperParams, weights: dict) -> bytes:
     hdr += b"\0" * ((-len(hdr)) % 8)
     parts = [hdr]
     for name, shape in weight_layout(hp):
+        if name == "blend0.w":
+            # optional section: magic 'BLENDW01'; int32 n_hidden, hidden dims;
+            # zero padding to 8 bytes; then the blend arrays
+            bh = BLEND_MAGIC + struct.pack("<i", len(hp.blend_dims))
+            bh += struct.pack(f"<{len(hp.blend_dims)}i", *hp.blend_dims)
+            bh += b"\0" * ((-len(bh)) % 8)
+            parts.append(bh)
         a = np.ascontiguousarray(weights[name], dtype="<f8")
         if a.shape != tuple(shape):
             raise ValueError(f"{name}: shape {a.shape} != {shape}")
@@ -378,10 +405,23 @@ def read_weight_file(path_or_bytes) -> tuple[HyperParams, dict]:
     hp = HyperParams(F=F, K=K, L=L, n_species=S, n_heads=H, cutoff=cutoff,
                      shared_dims=shared, branch_dims=branch, rbf_type=rbf)
     w = {}
-    for name, shape in weight_layout(hp):
-        cnt = int(np.prod(shape))
-        w[name] = np.frombuffer(buf, dtype="<f8", count=cnt, offset=off).reshape(shape).copy()
-        off += 8 * cnt
+
+    def take(layout):
+        nonlocal off
+        for name, shape in layout:
+            cnt = int(np.prod(shape))
+            w[name] = np.frombuffer(buf, dtype="<f8", count=cnt, offset=off).reshape(shape).copy()
+            off += 8 * cnt
+
+    take(weight_layout(hp))
+    if off < len(buf):
+        if buf[off:off + 8] != BLEND_MAGIC:
+            raise ValueError("trailing bytes in weight file")
+        (nh,) = struct.unpack_from("<i", buf, off + 8)
+        hp.blend_dims = list(struct.unpack_from(f"<{nh}i", buf, off + 12))
+        off += 12 + 4 * nh
+        off += (-off) % 8
+        take([(n, sh) for n, sh in weight_layout(hp) if n.startswith("blend")])
     if off != len(buf):
         raise ValueError("trailing bytes in weight file")
     return hp, w
