@@ -93,9 +93,15 @@ painn_status painn_synchronize(painn_ctx* ctx);
  *                upd_w1[F,2F] upd_b1[F] upd_w2[3F,F] upd_b2[3F];
  *     per shared layer m: w[shared_dims[m], in] b[shared_dims[m]];
  *     per head h, per branch layer m: w[branch_dims[m], in] b[branch_dims[m]].
+ *   optional, the branch-weighting MLP (section "Composition-conditioned branch
+ *   weighting"): char magic[8] = "BLENDW01"; int32 n_hidden;
+ *   int32 hidden_dims[n_hidden]; zero padding to a multiple of 8 bytes;
+ *   float64 layers w[out, in] b[out] from n_species through the hidden widths
+ *   to n_heads.
  * The split of phi's output is [s | v | rhat] and of the update MLP's output
  * [a_vv | a_sv | a_ss].  Supported: F in {64, 128, 256}, 2 <= K <= 64,
- * 1 <= L <= 16, n_heads <= 64, branch_dims[last] = 1. */
+ * 1 <= L <= 16, n_heads <= 64, branch_dims[last] = 1; with the
+ * branch-weighting MLP n_species <= 256 and widths <= 1024. */
 painn_status painn_model_load(painn_ctx* ctx, const char* path, painn_model** out);
 /* Same, from a host buffer holding the file's bytes (copied; the buffer may
  * be released after the call). */
@@ -104,6 +110,9 @@ painn_status painn_model_load_buffer(painn_ctx* ctx, const void* data, size_t nb
 /* Hyperparameters of a model (host outputs; any pointer may be NULL). */
 painn_status painn_model_info(const painn_model* model, int32_t* F, int32_t* K, int32_t* L,
                               int32_t* n_species, int32_t* n_heads, double* cutoff);
+/* Whether the model carries a branch-weighting MLP (host output *has_blend
+ * = 1 or 0). */
+painn_status painn_model_has_blend(const painn_model* model, int32_t* has_blend);
 painn_status painn_model_free(painn_model* model);
 
 /* ---- graph -------------------------------------------------------------- */
@@ -157,6 +166,22 @@ painn_status painn_graph_free(painn_graph* graph);
 painn_status painn_forward(painn_ctx* ctx, const painn_model* model, const painn_graph* graph,
                            const int32_t* dataset_id, painn_precision precision,
                            double* energies);
+
+/* Per-structure energies with every head blended (sections
+ * "Composition-conditioned branch weighting" and "Optimizing the Inference
+ * Pipeline", branch skipping): the encoder runs once; structure b's
+ * composition vector (fraction of its atoms of each species) goes through the
+ * model's branch-weighting MLP to softmax weights w_bh over the heads, and
+ * E_b = sum over heads h with w_bh >= skip_threshold of w_bh E_bh, where E_bh
+ * is head h's energy of structure b.  skip_threshold = 0 keeps every head;
+ * skipped heads are not computed and the kept weights are not renormalised.
+ *   energies [B] float64 output; weights [B, n_heads] float64 output of the
+ *   weights w_bh, or NULL.  Both written on the stream.
+ * Errors: as painn_forward; PAINN_E_UNSUPPORTED when the model has no
+ * branch-weighting MLP; PAINN_E_ARG for a negative or non-finite threshold. */
+painn_status painn_forward_blend(painn_ctx* ctx, const painn_model* model, const painn_graph* graph,
+                                 painn_precision precision, double skip_threshold, double* energies,
+                                 double* weights);
 
 /* Test hook: run layers 0..layer (layer = -1: embedding only) and write the
  * scalar features s [N,F] and vector features v [N,3,F] (float64) reached

@@ -12,9 +12,9 @@ PRECISIONS = {"fp64": PAINN_FP64, "fp32": PAINN_FP32, "bf16": PAINN_BF16}
 EXPORTS = [
     "painn_create", "painn_set_stream", "painn_destroy", "painn_last_error",
     "painn_status_string", "painn_synchronize", "painn_model_load",
-    "painn_model_load_buffer", "painn_model_info", "painn_model_free",
+    "painn_model_load_buffer", "painn_model_info", "painn_model_has_blend", "painn_model_free",
     "painn_build_graph", "painn_graph_csr", "painn_graph_free", "painn_forward",
-    "painn_forward_features", "painn_profile_enable", "painn_profile_read",
+    "painn_forward_blend", "painn_forward_features", "painn_profile_enable", "painn_profile_read",
 ]
 
 _P = ctypes.c_void_p
@@ -29,6 +29,7 @@ _SIGS = {
     "painn_model_load": ([_P, ctypes.c_char_p, ctypes.POINTER(_P)], ctypes.c_int),
     "painn_model_load_buffer": ([_P, ctypes.c_char_p, ctypes.c_size_t, ctypes.POINTER(_P)], ctypes.c_int),
     "painn_model_info": ([_P] + [ctypes.POINTER(_I32)] * 5 + [ctypes.POINTER(ctypes.c_double)], ctypes.c_int),
+    "painn_model_has_blend": ([_P, ctypes.POINTER(_I32)], ctypes.c_int),
     "painn_model_free": ([_P], ctypes.c_int),
     "painn_build_graph": ([_P, _I32, _I32, _P, _P, _P, _P, _P, ctypes.c_double, ctypes.POINTER(_P)],
                           ctypes.c_int),
@@ -36,6 +37,7 @@ _SIGS = {
                          ctypes.POINTER(_P), ctypes.POINTER(_P), ctypes.POINTER(_P)], ctypes.c_int),
     "painn_graph_free": ([_P], ctypes.c_int),
     "painn_forward": ([_P, _P, _P, _P, ctypes.c_int, _P], ctypes.c_int),
+    "painn_forward_blend": ([_P, _P, _P, ctypes.c_int, ctypes.c_double, _P, _P], ctypes.c_int),
     "painn_forward_features": ([_P, _P, _P, ctypes.c_int, _I32, _P, _P], ctypes.c_int),
     "painn_profile_enable": ([_P, ctypes.c_int], ctypes.c_int),
     "painn_profile_read": ([_P, _I32, ctypes.POINTER(ctypes.c_char_p), ctypes.POINTER(ctypes.c_double),
@@ -126,6 +128,12 @@ def painn_model_info(model: int) -> dict:
                 n_heads=v[4].value, cutoff=rc.value)
 
 
+def painn_model_has_blend(model: int) -> bool:
+    v = _I32()
+    _check(load_library().painn_model_has_blend(model, ctypes.byref(v)))
+    return bool(v.value)
+
+
 def painn_model_free(model: int) -> None:
     _check(load_library().painn_model_free(model))
 
@@ -156,6 +164,12 @@ def painn_graph_free(graph: int) -> None:
 def painn_forward(ctx: int, model: int, graph: int, dataset_id: int | None, precision: int,
                   energies: int) -> None:
     _check(load_library().painn_forward(ctx, model, graph, dataset_id or None, precision, energies), ctx)
+
+
+def painn_forward_blend(ctx: int, model: int, graph: int, precision: int, skip_threshold: float,
+                        energies: int, weights: int | None) -> None:
+    _check(load_library().painn_forward_blend(ctx, model, graph, precision, float(skip_threshold),
+                                              energies, weights or None), ctx)
 
 
 def painn_forward_features(ctx: int, model: int, graph: int, precision: int, layer: int,

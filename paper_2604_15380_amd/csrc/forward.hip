@@ -499,19 +499,34 @@ __global__ void __launch_bounds__(64) k_head_clear(HeadPlan* p) {
   if (t == 0) p->n_tiles = 0;
 }
 
-// per-head atom counts; atoms with an invalid dataset id get a NaN energy
+// Entries (atom, head) to run.  One dataset's head per atom (hw null): the
+// structure's dataset id, and atoms with an invalid id get a NaN energy.
+// Blended heads (hw given): every head whose weight for the atom's structure
+// is >= skip.
+template <class A>
+__device__ __forceinline__ bool entry_on(const int32_t* dataset_id, const A* hw, int H, A skip, int b,
+                                         int h) {
+  return hw ? hw[(size_t)b * H + h] >= skip : dataset_id[b] == h;
+}
+
 template <class A>
 __global__ void __launch_bounds__(256) k_head_count(int N, int n_heads, const int32_t* dataset_id,
-                                                    const int32_t* atom_struct, HeadPlan* p,
-                                                    A* e) {
+                                                    const A* hw, A skip, const int32_t* atom_struct,
+                                                    HeadPlan* p, A* e) {
   __shared__ int hist[HEADS_MAX];
   if (threadIdx.x < HEADS_MAX) hist[threadIdx.x] = 0;
   __syncthreads();
   const int atom = blockIdx.x * 256 + threadIdx.x;
   if (atom < N) {
-    const int h = atom_head(dataset_id, atom_struct, n_heads, atom);
-    if (h < 0) e[atom] = (A)NAN;
-    else atomicAdd(&hist[h], 1);
+    const int b = atom_struct[atom];
+    if (hw) {
+      for (int h = 0; h < n_heads; ++h)
+        if (entry_on(dataset_id, hw, n_heads, skip, b, h)) atomicAdd(&hist[h], 1);
+    } else {
+      const int h = atom_head(dataset_id, atom_struct, n_heads, atom);
+      if (h < 0) e[atom] = (A)NAN;
+      else atomicAdd(&hist[h], 1);
+    }
   }
   __syncthreads();
   if (threadIdx.x < n_heads && hist[threadIdx.x] > 0) atomicAdd(&p->count[threadIdx.x], hist[threadIdx.x]);
@@ -546,24 +561,35 @@ __global__ void __launch_bounds__(64) k_head_plan(int n_heads, int TM, HeadPlan*
   }
 }
 
-// atom order grouped by head: block-local ranks, one global reservation per head
+// entry order grouped by head: block-local ranks, one global reservation per
+// head, head by head; an entry holds its atom (the tile gives the head)
+template <class A>
 __global__ void __launch_bounds__(256) k_head_scatter(int N, int n_heads, const int32_t* dataset_id,
-                                                      const int32_t* atom_struct, HeadPlan* p,
-                                                      int32_t* order) {
-  __shared__ int hist[HEADS_MAX], base[HEADS_MAX];
-  if (threadIdx.x < HEADS_MAX) hist[threadIdx.x] = 0;
-  __syncthreads();
+                                                      const A* hw, A skip, const int32_t* atom_struct,
+                                                      HeadPlan* p, int32_t* order) {
+  __shared__ int cnt, base;
   const int atom = blockIdx.x * 256 + threadIdx.x;
-  int h = -1, rank = 0;
+  uint64_t on = 0;                       // heads of this atom (n_heads <= 64)
   if (atom < N) {
-    h = atom_head(dataset_id, atom_struct, n_heads, atom);
-    if (h >= 0) rank = atomicAdd(&hist[h], 1);
+    if (hw) {
+      const int b = atom_struct[atom];
+      for (int h = 0; h < n_heads; ++h)
+        if (entry_on(dataset_id, hw, n_heads, skip, b, h)) on |= 1ull << h;
+    } else {
+      const int h = atom_head(dataset_id, atom_struct, n_heads, atom);
+      if (h >= 0) on = 1ull << h;
+    }
   }
-  __syncthreads();
-  if (threadIdx.x < n_heads && hist[threadIdx.x] > 0)
-    base[threadIdx.x] = p->start[threadIdx.x] + atomicAdd(&p->cursor[threadIdx.x], hist[threadIdx.x]);
-  __syncthreads();
-  if (h >= 0) order[base[h] + rank] = atom;
+  for (int h = 0; h < n_heads; ++h) {
+    if (threadIdx.x == 0) cnt = 0;
+    __syncthreads();
+    const bool mine = (on >> h) & 1ull;
+    const int r = mine ? atomicAdd(&cnt, 1) : 0;
+    __syncthreads();
+    if (threadIdx.x == 0 && cnt > 0) base = p->start[h] + atomicAdd(&p->cursor[h], cnt);
+    __syncthreads();
+    if (mine) order[base + r] = atom;
+  }
 }
 
 struct HeadArgs {
@@ -577,7 +603,9 @@ struct HeadArgs {
   const void* const* table;  // [n_heads][nb][2] = (packed w, bias)
   DenseDev shared[16];
   int bdin[16], bdout[16];
-  void* e;
+  void* e;       // [N]: one dataset's head per atom
+  void* eh;      // [N][H]: blended heads (e unused), or null
+  int H;
 };
 
 // Element k of output row 0 of a packed dense layer (the B fragment order).
@@ -706,7 +734,10 @@ __global__ void __launch_bounds__(64 * HEADS_NW) k_heads(HeadArgs a) {
       for (int w = 0; w < HEADS_NW; ++w) y += part[w][rt];
     }
   }
-  if (rt < TM && idx[rt] >= 0) ((A*)a.e)[idx[rt]] = y;
+  if (rt < TM && idx[rt] >= 0) {
+    if (a.eh) ((A*)a.eh)[(size_t)idx[rt] * a.H + head] = y;
+    else ((A*)a.e)[idx[rt]] = y;
+  }
 }
 
 // ------------------------------------------------------------ energies ----
@@ -1006,6 +1037,115 @@ hipError_t launch_message(hipStream_t st, const MsgArgs& a) {
   return hipSuccess;
 }
 
+// ------------------------------------------------ branch weighting ----
+// Composition vector of every structure: fractions of its atoms per species,
+// padded with zeros to pad32(S) columns (one wave per structure).
+template <class P>
+__global__ void __launch_bounds__(256) k_composition(int B, int S, const int32_t* __restrict__ struct_ptr,
+                                                     const int32_t* __restrict__ species,
+                                                     typename P::T* __restrict__ comp) {
+  __shared__ int hist[4][256];
+  const int lane = threadIdx.x & 63, wv = threadIdx.x >> 6;
+  const int b = blockIdx.x * 4 + wv;
+  const int Sp = pad32(S);
+  for (int z = lane; z < 256; z += 64) hist[wv][z] = 0;
+  __builtin_amdgcn_wave_barrier();
+  __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+  __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+  if (b >= B) return;
+  const int lo = struct_ptr[b], hi = struct_ptr[b + 1];
+  for (int i = lo + lane; i < hi; i += 64) {
+    const int z = species[i];
+    if (z >= 0 && z < S) atomicAdd(&hist[wv][z], 1);
+  }
+  __builtin_amdgcn_wave_barrier();
+  __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+  __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+  const typename P::A inv = hi > lo ? (typename P::A)1 / (typename P::A)(hi - lo) : (typename P::A)0;
+  for (int z = lane; z < Sp; z += 64)
+    comp[(size_t)b * Sp + z] = P::st(z < S ? (typename P::A)hist[wv][z] * inv : (typename P::A)0);
+}
+
+struct BlendArgs {
+  int B, S, H, nl;
+  const void* comp;
+  DenseDev layer[9];
+  int width;            // widest padded layer (LDS row stride minus padding)
+  void* hw;             // [B][H] accumulation type
+  double* weights_out;  // [B][H] or null
+};
+
+// The branch-weighting MLP over 16 structures per workgroup (silu between
+// layers), then a softmax over the heads.
+template <class P>
+__global__ void __launch_bounds__(256) k_blend(BlendArgs a) {
+  using T = typename P::T;
+  using A = typename P::A;
+  using C = typename P::C;
+  extern __shared__ __attribute__((aligned(16))) unsigned char smem[];
+  const int ld = a.width + P::PAD;
+  T* X0 = (T*)smem;
+  T* X1 = X0 + 16 * ld;
+  A* logit = (A*)(X1 + 16 * ld);
+  const int lane = threadIdx.x & 63;
+  const int b0 = blockIdx.x * 16;
+  const int Sp = pad32(a.S);
+  const T* comp = (const T*)a.comp;
+  for (int x = threadIdx.x; x < 16 * Sp; x += blockDim.x) {
+    const int r = x / Sp, c = x % Sp;
+    X0[r * ld + c] = b0 + r < a.B ? comp[(size_t)(b0 + r) * Sp + c] : P::st(0);
+  }
+  __syncthreads();
+  const T* in = X0;
+  for (int m = 0; m < a.nl; ++m) {
+    const DenseDev& L = a.layer[m];
+    const bool last = m == a.nl - 1;
+    T* dst = (m & 1) ? X0 : X1;
+    dense_tiles<P, 1, 4>(in, ld, L, [&](int ct, C* acc) {
+      const int col = ct * 16 + (lane & 15);
+      const A bias = ((const A*)L.b)[col];
+      for (int i = 0; i < 4; ++i) {
+        const int r = P::row(lane, i);
+        const A y = acc[0][i] + bias;
+        if (last) {
+          if (col < a.H) logit[r * 64 + col] = y;
+        } else {
+          dst[r * ld + col] = P::st(silu<A>(y));
+        }
+      }
+    });
+    __syncthreads();
+    in = dst;
+  }
+  if (threadIdx.x < 16 && b0 + threadIdx.x < a.B) {
+    const int r = threadIdx.x;
+    A mx = logit[r * 64];
+    for (int h = 1; h < a.H; ++h) mx = logit[r * 64 + h] > mx ? logit[r * 64 + h] : mx;
+    A sum = 0;
+    for (int h = 0; h < a.H; ++h) sum += P::ex(logit[r * 64 + h] - mx);
+    A* hw = (A*)a.hw + (size_t)(b0 + r) * a.H;
+    for (int h = 0; h < a.H; ++h) {
+      const A w = P::ex(logit[r * 64 + h] - mx) / sum;
+      hw[h] = w;
+      if (a.weights_out) a.weights_out[(size_t)(b0 + r) * a.H + h] = (double)w;
+    }
+  }
+}
+
+// Blended per-atom energy: sum over the kept heads in head order.
+template <class A>
+__global__ void __launch_bounds__(256) k_blend_reduce(int N, int H, A skip, const int32_t* __restrict__ atom_struct,
+                                                      const A* __restrict__ hw, const A* __restrict__ eh,
+                                                      A* __restrict__ e) {
+  const int i = blockIdx.x * 256 + threadIdx.x;
+  if (i >= N) return;
+  const A* w = hw + (size_t)atom_struct[i] * H;
+  A y = 0;
+  for (int h = 0; h < H; ++h)
+    if (w[h] >= skip) y += w[h] * eh[(size_t)i * H + h];
+  e[i] = y;
+}
+
 // Dynamic LDS beyond 64 KiB must be allowed once per kernel.
 template <class P, int F, int RT>
 hipError_t heads_allow_lds(size_t smem) {
@@ -1094,20 +1234,51 @@ hipError_t launch_heads(hipStream_t st, ForwardArgs& fa) {
   ha.table = (const void* const*)pm->head_table;
   ha.e = fa.e;
   int grid = (N + TM - 1) / TM;
+  const int H = hp.n_heads;
+  ha.eh = nullptr;
+  ha.H = H;
   prof_mark(fa.prof, st, KC_HEADS, true);
-  if (fa.dataset_id) {
+  if (fa.blend) {
+    // composition vectors and the branch-weighting MLP's softmax weights
+    const int B = fa.g->B, S = hp.n_species;
+    k_composition<P><<<(B + 3) / 4, 256, 0, st>>>(B, S, fa.g->struct_ptr, fa.g->species, (T*)fa.comp);
+    BlendArgs ba;
+    ba.B = B;
+    ba.S = S;
+    ba.H = H;
+    ba.nl = (int)pm->blend.size();
+    if (ba.nl < 1 || ba.nl > 9 || H > 64) return hipErrorInvalidValue;
+    ba.comp = fa.comp;
+    ba.width = pad32(S);
+    for (int m = 0; m < ba.nl; ++m) {
+      ba.layer[m] = pm->blend[m];
+      ba.width = ba.width > pm->blend[m].dout_p ? ba.width : pm->blend[m].dout_p;
+    }
+    ba.hw = fa.hw;
+    ba.weights_out = fa.weights_out;
+    const size_t bsmem = 2 * 16 * (size_t)(ba.width + P::PAD) * sizeof(T) + 16 * 64 * sizeof(A);
+    if (bsmem > 64 * 1024) return hipErrorInvalidValue;
+    if (B > 0) k_blend<P><<<(B + 15) / 16, 256, bsmem, st>>>(ba);
+  }
+  if (fa.dataset_id || fa.blend) {
     HeadPlan* plan = (HeadPlan*)fa.head_plan;
     HeadTile* tiles = (HeadTile*)fa.head_tiles;
+    const A* hw = fa.blend ? (const A*)fa.hw : nullptr;
+    const A skip = (A)fa.skip;
     const int nb256 = (N + 255) / 256;
     k_head_clear<<<1, 64, 0, st>>>(plan);
-    k_head_count<A><<<nb256, 256, 0, st>>>(N, hp.n_heads, fa.dataset_id, fa.g->atom_struct, plan, (A*)fa.e);
-    k_head_plan<<<1, 64, 0, st>>>(hp.n_heads, TM, plan, tiles);
-    k_head_scatter<<<nb256, 256, 0, st>>>(N, hp.n_heads, fa.dataset_id, fa.g->atom_struct, plan,
-                                          fa.head_order);
+    k_head_count<A><<<nb256, 256, 0, st>>>(N, H, fa.dataset_id, hw, skip, fa.g->atom_struct, plan, (A*)fa.e);
+    k_head_plan<<<1, 64, 0, st>>>(H, TM, plan, tiles);
+    k_head_scatter<A><<<nb256, 256, 0, st>>>(N, H, fa.dataset_id, hw, skip, fa.g->atom_struct, plan,
+                                             fa.head_order);
     ha.order = fa.head_order;
     ha.tiles = tiles;
     ha.plan = plan;
-    grid += hp.n_heads;
+    if (fa.blend) {
+      grid = (int)(((long long)N * H + TM - 1) / TM);
+      ha.eh = fa.eh;
+    }
+    grid += H;
   } else {
     ha.order = nullptr;
     ha.tiles = nullptr;
@@ -1117,8 +1288,12 @@ hipError_t launch_heads(hipStream_t st, ForwardArgs& fa) {
   if (RT == 4) e = launch_heads_rt<P, F, 4>(st, ha, grid, smem);
   else if (RT == 2) e = launch_heads_rt<P, F, 2>(st, ha, grid, smem);
   else e = launch_heads_rt<P, F, 1>(st, ha, grid, smem);
+  if (e == hipSuccess && fa.blend)
+    k_blend_reduce<A><<<(N + 255) / 256, 256, 0, st>>>(N, H, (A)fa.skip, fa.g->atom_struct, (const A*)fa.hw,
+                                                        (const A*)fa.eh, (A*)fa.e);
   prof_mark(fa.prof, st, KC_HEADS, false);
-  return e;
+  if (e != hipSuccess) return e;
+  return hipGetLastError();
 }
 
 template <class P, int F>

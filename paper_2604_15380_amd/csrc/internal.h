@@ -96,6 +96,7 @@ struct PrecModel {      // the model cast and packed for one precision
   std::vector<DenseDev> shared;                 // shared head layers
   std::vector<std::vector<DenseDev>> branch;    // [head][layer]
   void* head_table = nullptr;                   // device [head][layer][2] = (w, b)
+  std::vector<DenseDev> blend;                  // branch-weighting MLP (empty: none)
   std::vector<void*> allocs;
 };
 
@@ -103,6 +104,8 @@ struct Hyper {
   int F, K, L, n_species, n_heads, rbf_type;
   double cutoff;
   std::vector<int> shared_dims, branch_dims;
+  std::vector<int> blend_dims;   // hidden widths of the branch-weighting MLP
+  bool has_blend = false;
 };
 
 // ---- per-kernel event timing (painn_profile_*) ------------------------------
@@ -184,12 +187,21 @@ struct ForwardArgs {
   void* basis;           // [E + 16][kcols] storage type: radial basis rows
   void* einfo;           // [E][4] accumulation type: rhat, sender index
   void* head_plan;       // per-head counts and offsets (a few hundred bytes)
-  void* head_tiles;      // [N / 16 + 65] tiles of one head each (16 bytes)
-  int32_t* head_order;   // [N] atoms grouped by head
+  void* head_tiles;      // [N H / 16 + 65] tiles of one head each (16 bytes)
+  int32_t* head_order;   // [N H] (atom, head) entries grouped by head
+  // blended heads (blend = true): composition [B][pad32(S)] (storage type),
+  // head weights [B][H] and per-head atom energies [N][H] (accumulation type)
+  bool blend;
+  double skip;
+  double* weights_out;   // [B][H] f64 or null
+  void* comp;
+  void* hw;
+  void* eh;
   int stop_layer;          // run layers 0..stop_layer (forward: L-1)
   Profiler* prof;
   double* s_out;           // feature export (may be null)
   double* v_out;
 };
-size_t forward_workspace_bytes(int prec, int N, long long E, int F, int kcols);
+size_t forward_workspace_bytes(int prec, int N, long long E, int F, int kcols, int B, int H,
+                               int S, bool blend);
 hipError_t launch_forward(hipStream_t s, int prec, ForwardArgs& a);

@@ -228,6 +228,18 @@ painn_status build_prec(painn_model* m, int prec, PrecModel** out) {
       }
     e = upload(pm, tab, &pm->head_table);
   }
+  if (e == hipSuccess && hp.has_blend) {
+    int di = hp.n_species;
+    std::vector<int> dims = hp.blend_dims;
+    dims.push_back(hp.n_heads);
+    for (size_t mm = 0; mm < dims.size() && e == hipSuccess; ++mm) {
+      DenseDev d;
+      e = pack_dense(pm, prec, arr(idx), arr(idx + 1), dims[mm], di, &d);
+      pm->blend.push_back(d);
+      di = dims[mm];
+      idx += 2;
+    }
+  }
   if (e != hipSuccess) {
     free_prec(pm);
     return hip_fail(ctx, e, "uploading packed weights");
@@ -283,14 +295,46 @@ painn_status parse_model(painn_ctx* ctx, const unsigned char* buf, size_t n, pai
   }
   size_t total = 0;
   for (size_t s : sizes) total += s;
-  if (n != off + 8 * total)
-    return fail(ctx, PAINN_E_FORMAT, "weight file: size does not match its header");
+  const size_t main_total = total;
+  // optional branch-weighting MLP after the main arrays: 'BLENDW01', int32
+  // n_hidden, the hidden widths, zero padding to 8 bytes, then its layers
+  // (composition [n_species] -> hidden ... -> n_heads), each [out, in] + bias
+  size_t blend_off = 0;
+  if (n != off + 8 * main_total) {
+    size_t bo = off + 8 * main_total;
+    if (n < bo + 12 || memcmp(buf + bo, "BLENDW01", 8) != 0)
+      return fail(ctx, PAINN_E_FORMAT, "weight file: size does not match its header");
+    int32_t nh;
+    memcpy(&nh, buf + bo + 8, 4);
+    if (nh < 0 || nh > 8 || n < bo + 12 + 4 * (size_t)nh)
+      return fail(ctx, PAINN_E_FORMAT, "weight file: bad branch-weighting section");
+    bo += 12;
+    for (int i = 0; i < nh; ++i) { int32_t d; memcpy(&d, buf + bo, 4); bo += 4; hp.blend_dims.push_back(d); }
+    bo += (8 - bo % 8) % 8;
+    for (int d : hp.blend_dims)
+      if (d < 1 || d > 1024) return fail(ctx, PAINN_E_UNSUPPORTED, "branch-weighting widths must be in [1, 1024]");
+    if (hp.n_species > 256) return fail(ctx, PAINN_E_UNSUPPORTED, "branch weighting needs n_species <= 256");
+    size_t di = hp.n_species;
+    std::vector<int> dims = hp.blend_dims;
+    dims.push_back(hp.n_heads);
+    for (int d : dims) {
+      sizes.push_back((size_t)d * di);
+      sizes.push_back(d);
+      total += (size_t)d * di + d;
+      di = d;
+    }
+    if (n != bo + 8 * (total - main_total))
+      return fail(ctx, PAINN_E_FORMAT, "weight file: branch-weighting section size does not match its header");
+    hp.has_blend = true;
+    blend_off = bo;
+  }
   painn_model* m = new (std::nothrow) painn_model();
   if (!m) return fail(ctx, PAINN_E_OOM, "host allocation failed");
   m->ctx = ctx;
   m->hp = hp;
   m->master.resize(total);
-  memcpy(m->master.data(), buf + off, 8 * total);
+  memcpy(m->master.data(), buf + off, 8 * main_total);
+  if (hp.has_blend) memcpy(m->master.data() + main_total, buf + blend_off, 8 * (total - main_total));
   size_t o = 0;
   for (size_t s : sizes) { m->offsets.push_back(o); o += s; }
   for (double x : m->master)
@@ -304,16 +348,22 @@ painn_status parse_model(painn_ctx* ctx, const unsigned char* buf, size_t n, pai
 // Workspace of one forward pass, carved in this order: s [N][F], v[0], v[1],
 // h [N][3F] (storage type), e [N] (accumulation type), the radial basis rows
 // [E + 16][kcols] (storage type), the edge info [E][4] (accumulation type),
-// then the head binning: plan (1 KiB), tiles [N / 16 + 65][4] and the atom
-// order [N] (int32).
-static size_t head_tiles_bytes(size_t n) { return (n / 16 + 65) * 16; }
+// then the head binning: plan (1 KiB), tiles [N M / 16 + 65][4] and the
+// (atom, head) order [N M] (int32), with M = 1 entry per atom (one dataset's
+// head) or M = H (blended heads); blended heads add the composition
+// [B][pad32(S)] (storage type), the head weights [B][H] and the per-head atom
+// energies [N][H] (accumulation type).
+static size_t head_tiles_bytes(size_t entries) { return (entries / 16 + 65) * 16; }
 
-size_t forward_workspace_bytes(int prec, int N, long long E, int F, int kcols) {
+size_t forward_workspace_bytes(int prec, int N, long long E, int F, int kcols, int B, int H,
+                               int S, bool blend) {
   const size_t eb = elem_bytes(prec), ab = acc_bytes(prec);
   auto al = [](size_t x) { return (x + 255) & ~(size_t)255; };
-  const size_t n = (size_t)N, ne = (size_t)E;
-  return al(n * F * eb) + 3 * al(n * 3 * F * eb) + al(n * ab) + al((ne + 16) * kcols * eb) +
-         al(ne * 4 * ab) + al(1024) + al(head_tiles_bytes(n)) + al(n * 4);
+  const size_t n = (size_t)N, ne = (size_t)E, ent = n * (blend ? (size_t)H : 1);
+  size_t b = al(n * F * eb) + 3 * al(n * 3 * F * eb) + al(n * ab) + al((ne + 16) * kcols * eb) +
+             al(ne * 4 * ab) + al(1024) + al(head_tiles_bytes(ent)) + al(ent * 4);
+  if (blend) b += al((size_t)B * pad32(S) * eb) + al((size_t)B * H * ab) + al(n * H * ab);
+  return b;
 }
 
 
@@ -458,6 +508,12 @@ painn_status painn_model_load(painn_ctx* ctx, const char* path, painn_model** ou
   std::vector<unsigned char> buf((std::istreambuf_iterator<char>(f)), std::istreambuf_iterator<char>());
   if (f.bad()) return fail(ctx, PAINN_E_FILE, std::string("cannot read ") + path);
   return painn_model_load_buffer(ctx, buf.data(), buf.size(), out);
+}
+
+painn_status painn_model_has_blend(const painn_model* m, int32_t* has_blend) {
+  if (!m || !has_blend) return PAINN_E_ARG;
+  *has_blend = m->hp.has_blend ? 1 : 0;
+  return PAINN_OK;
 }
 
 painn_status painn_model_info(const painn_model* m, int32_t* F, int32_t* K, int32_t* L,
@@ -649,7 +705,8 @@ painn_status painn_graph_csr(const painn_graph* g, int64_t* n_edges, int32_t* n_
 
 static painn_status run_forward(painn_ctx* ctx, const painn_model* model, const painn_graph* g,
                                 const int32_t* dataset_id, painn_precision prec, int stop_layer,
-                                double* energies, double* s_out, double* v_out) {
+                                double* energies, double* s_out, double* v_out, bool blend = false,
+                                double skip = 0.0, double* weights_out = nullptr) {
   if (!ctx) return PAINN_E_ARG;
   ctx->err.clear();
   if (!model || !g) return fail(ctx, PAINN_E_ARG, "null model or graph");
@@ -667,7 +724,8 @@ static painn_status run_forward(painn_ctx* ctx, const painn_model* model, const 
     if (st != PAINN_OK) return st;
   }
   const int kcols = m->prec[prec]->layers[0].filt_mma.din_p;
-  size_t need = forward_workspace_bytes(prec, g->N, g->E, m->hp.F, kcols);
+  size_t need = forward_workspace_bytes(prec, g->N, g->E, m->hp.F, kcols, g->B, m->hp.n_heads,
+                                       m->hp.n_species, blend);
   if (need > ctx->ws_bytes) {
     if (ctx->ws) {
       (void)hipStreamSynchronize(ctx->stream);
@@ -702,9 +760,20 @@ static painn_status run_forward(painn_ctx* ctx, const painn_model* model, const 
   a.e = p; p += al(N * ab);
   a.basis = p; p += al(((size_t)g->E + 16) * kcols * eb);
   a.einfo = p; p += al((size_t)g->E * 4 * ab);
+  const size_t ent = N * (blend ? (size_t)m->hp.n_heads : 1);
   a.head_plan = p; p += al(1024);
-  a.head_tiles = p; p += al(head_tiles_bytes(N));
-  a.head_order = (int32_t*)p; p += al(N * 4);
+  a.head_tiles = p; p += al(head_tiles_bytes(ent));
+  a.head_order = (int32_t*)p; p += al(ent * 4);
+  a.blend = blend;
+  a.skip = skip;
+  a.weights_out = weights_out;
+  a.comp = a.hw = a.eh = nullptr;
+  if (blend) {
+    const size_t H = m->hp.n_heads;
+    a.comp = p; p += al((size_t)g->B * pad32(m->hp.n_species) * eb);
+    a.hw = p; p += al((size_t)g->B * H * ab);
+    a.eh = p; p += al(N * H * ab);
+  }
   if (g->B == 0 && !s_out) return PAINN_OK;
   (void)hipGetLastError();   // do not report an error left by earlier, unrelated calls
   hipError_t e = launch_forward(ctx->stream, prec, a);
@@ -720,6 +789,20 @@ painn_status painn_forward(painn_ctx* ctx, const painn_model* model, const painn
   if (ctx && graph && graph->B > 0 && !energies) return fail(ctx, PAINN_E_ARG, "energies is null");
   return run_forward(ctx, model, graph, dataset_id, precision, model ? model->hp.L - 1 : 0,
                      energies, nullptr, nullptr);
+}
+
+painn_status painn_forward_blend(painn_ctx* ctx, const painn_model* model, const painn_graph* graph,
+                                 painn_precision precision, double skip_threshold, double* energies,
+                                 double* weights) {
+  if (!ctx) return PAINN_E_ARG;
+  if (!model || !graph) return fail(ctx, PAINN_E_ARG, "null model or graph");
+  if (!model->hp.has_blend)
+    return fail(ctx, PAINN_E_UNSUPPORTED, "the model has no branch-weighting MLP");
+  if (!(skip_threshold >= 0.0) || !isfinite(skip_threshold))
+    return fail(ctx, PAINN_E_ARG, "skip_threshold must be finite and >= 0");
+  if (graph->B > 0 && !energies) return fail(ctx, PAINN_E_ARG, "energies is null");
+  return run_forward(ctx, model, graph, nullptr, precision, model->hp.L - 1, energies, nullptr, nullptr,
+                     true, skip_threshold, weights);
 }
 
 painn_status painn_forward_features(painn_ctx* ctx, const painn_model* model,

@@ -30,6 +30,7 @@ class Model:
     def __init__(self, rt: "Runtime", handle: int):
         self.rt, self.handle = rt, handle
         self.info = B.painn_model_info(handle)
+        self.has_blend = B.painn_model_has_blend(handle)
 
     def free(self):
         if self.handle:
@@ -121,6 +122,20 @@ class Runtime:
         ds = dataset_id.data_ptr() if dataset_id is not None and dataset_id.numel() else None
         B.painn_forward(self.ctx, model.handle, graph.handle, ds, prec,
                         out.data_ptr() if out.numel() else None)
+        return out
+
+    def forward_blend(self, model: Model, graph: Graph, precision="fp32", skip=0.0, out=None,
+                      weights=None):
+        """Energies with every head blended by the model's branch-weighting
+        MLP; heads with weight < skip are left out.  `weights` (optional)
+        receives the [B, n_heads] head weights."""
+        import torch
+        prec = B.PRECISIONS[precision] if isinstance(precision, str) else precision
+        if out is None:
+            out = torch.empty(graph.n_struct, dtype=torch.float64, device=self.device)
+        B.painn_forward_blend(self.ctx, model.handle, graph.handle, prec, skip,
+                              out.data_ptr() if out.numel() else None,
+                              weights.data_ptr() if weights is not None and weights.numel() else None)
         return out
 
     def features(self, model: Model, graph: Graph, layer: int, precision="fp64"):
