@@ -45,7 +45,7 @@ def source_digest() -> str:
     return h.hexdigest()[:16]
 
 
-def kernel_work(kernel: str, hp, N: int, E: int, prec: str):
+def kernel_work(kernel: str, hp, N: int, E: int, prec: str, head_entries: int | None = None):
     """Algorithmic work of ONE launch of a kernel class: (bound, flops, bytes).
 
     message: per edge 6KF (radial filter contraction over K Gaussians for 3F
@@ -55,6 +55,8 @@ def kernel_work(kernel: str, hp, N: int, E: int, prec: str):
     update:  per atom 22 F^2 (U/V 12F^2, gate MLP 10F^2) + 8 F^2 for the next
              layer's phi fused behind it (all but the last layer).
     phi:     per atom 8 F^2.
+    heads:   per (atom, head) entry the shared and branch MLP flops (one entry
+             per atom, or every kept head of the atom's structure when blended).
     """
     F, K, L = hp.F, hp.K, hp.L
     b = ELEM[prec]
@@ -67,7 +69,8 @@ def kernel_work(kernel: str, hp, N: int, E: int, prec: str):
         return "mfma", N * 8.0 * F * F, N * 4.0 * F * b
     if kernel == "heads":
         dims = [F] + list(hp.shared_dims) + list(hp.branch_dims)
-        return "mfma", N * sum(2.0 * a * c for a, c in zip(dims[:-1], dims[1:])), N * F * b
+        n = N if head_entries is None else head_entries
+        return "mfma", n * sum(2.0 * a * c for a, c in zip(dims[:-1], dims[1:])), N * F * b
     return None, 0.0, 0.0
 
 
@@ -82,9 +85,10 @@ def load_traffic(key: str, digest: str, launches_kernel: str):
     return t.get("bytes_per_launch")
 
 
-def cpu_baseline(name: str, batch, sample: int):
+def cpu_baseline(name: str, batch, sample: int, blend_skip=None):
     """Time the oracle (as it stands) on the first `sample` structures, one
-    single-threaded worker per available core."""
+    single-threaded worker per available core (blended heads when blend_skip
+    is given)."""
     os.environ.setdefault("OMP_NUM_THREADS", "1")
     from concurrent.futures import ProcessPoolExecutor
     sys.path.insert(0, os.path.join(ROOT, "tests"))
@@ -93,7 +97,7 @@ def cpu_baseline(name: str, batch, sample: int):
     cores = min(cores, 16)
     idx = list(range(min(sample, batch.n_struct)))
     t0 = time.perf_counter()
-    helpers.oracle_energies(name, batch, idx, workers=cores)
+    helpers.oracle_energies(name, batch, idx, workers=cores, blend_skip=blend_skip)
     dt = time.perf_counter() - t0
     return dict(value=len(idx) / dt, unit="structures/s", cores=cores, kind="oracle",
                 sample=f"first {len(idx)} structures of the {name} batch, oracle (brute-force graph + "
@@ -108,6 +112,10 @@ def main():
     ap.add_argument("--workload", default="molecules_4096",
                     choices=["molecules_4096", "bulk_1024", "screening", "tiny_molecules"])
     ap.add_argument("--precision", default=None, choices=["fp64", "fp32", "bf16"])
+    ap.add_argument("--blend", action="store_true",
+                    help="blend every head with the model's branch-weighting MLP (screening model)")
+    ap.add_argument("--skip", type=float, default=0.0,
+                    help="with --blend: leave out heads whose weight is below this threshold")
     ap.add_argument("--cpu-sample", type=int, default=768)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-profile", action="store_true", help="time without per-kernel events")
@@ -150,14 +158,30 @@ def main():
     graph = rt.build_graph(inp, hp.cutoff)
     out = torch.empty(batch.n_struct, dtype=torch.float64, device=rt.device)
 
+    if args.blend and hp.blend_dims is None:
+        print(f"--blend needs a model with a branch-weighting MLP ({name} has none)", file=sys.stderr)
+        sys.exit(2)
+
     def step():
         rt.build_graph(inp, hp.cutoff, graph=graph)
-        rt.forward(model, graph, prec, dataset_id=ds, out=out)
+        if args.blend:
+            rt.forward_blend(model, graph, prec, skip=args.skip, out=out)
+        else:
+            rt.forward(model, graph, prec, dataset_id=ds, out=out)
 
     log(f"{batch.n_struct} structures, {batch.n_atoms} atoms, {graph.n_edges} edges; warmup {args.warmup}")
     for _ in range(args.warmup):
         step()
     torch.cuda.synchronize()
+    head_entries = None
+    if args.blend:
+        # (atom, head) entries the heads run: every kept head of each structure
+        w = torch.empty((batch.n_struct, hp.n_heads), dtype=torch.float64, device=rt.device)
+        rt.forward_blend(model, graph, prec, skip=args.skip, out=out, weights=w)
+        kept = (w >= args.skip).sum(dim=1).cpu().numpy()
+        head_entries = int(np.sum(np.diff(batch.struct_ptr) * kept))
+        log(f"blended heads: {head_entries / max(1, batch.n_atoms):.2f} kept heads per atom")
+        torch.cuda.synchronize()
     if not args.no_profile:
         painn_profile_read(rt.ctx)
         painn_profile_enable(rt.ctx, True)
@@ -193,10 +217,10 @@ def main():
     kernel_ms = {k: round(ms / K, 4) for k, (ms, n) in prof.items()}
     roofline = None
     if prof:
-        cand = {k: v for k, v in prof.items() if kernel_work(k, hp, N, E, prec)[0]}
+        cand = {k: v for k, v in prof.items() if kernel_work(k, hp, N, E, prec, head_entries)[0]}
         dom = max(cand, key=lambda k: cand[k][0])
         ms, launches = cand[dom]
-        bound, flops, nbytes = kernel_work(dom, hp, N, E, prec)
+        bound, flops, nbytes = kernel_work(dom, hp, N, E, prec, head_entries)
         avg_s = ms / launches / 1e3
         achieved = flops / avg_s / 1e12
         peak = PEAK[bound][prec]
@@ -210,7 +234,7 @@ def main():
     cpu = None
     if not args.no_cpu_baseline:
         log("timing the CPU oracle baseline")
-        cpu = cpu_baseline(name, batch, args.cpu_sample)
+        cpu = cpu_baseline(name, batch, args.cpu_sample, args.skip if args.blend else None)
 
     res = {
         "metric": METRIC, "value": round(value, 2), "unit": "structures/s", "n_gpus": 1,
@@ -219,11 +243,14 @@ def main():
         "dtype": DTYPE[prec], "data": "synthetic",
         "config": {"workload": name, "n_struct": B, "n_atoms": N, "n_edges": E, "F": hp.F,
                    "layers": hp.L, "rbf": hp.K, "cutoff": hp.cutoff, "heads": hp.n_heads,
-                   "precision": prec},
+                   "precision": prec,
+                   "head_mode": (f"blended, skip < {args.skip:g}" if args.blend else
+                                 ("dataset id" if hp.n_heads > 1 else "single"))},
         "edges_per_s": round(E * K / T, 1),
         "edge_messages_per_s": round(E * hp.L * K / T, 1),
         "pcie_inclusive_structures_per_s": round(B * K / T_pcie, 2),
         "kernel_ms_per_step": kernel_ms,
+        "heads_per_atom": None if head_entries is None else round(head_entries / max(1, N), 3),
         "roofline": roofline,
         "cpu_baseline": cpu,
     }

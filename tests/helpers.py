@@ -26,22 +26,26 @@ def _single_thread_blas():
 
 
 def _oracle_job(args):
-    from oracle.painn import structure_forward
-    name, batch_tuple, idx = args
+    from oracle.painn import structure_forward, structure_forward_blend
+    name, batch_tuple, idx, blend_skip = args
     hp, W = synth.workload_weights(name)
     out = []
     for k, (pos, z, cell, pbc, ds) in zip(idx, batch_tuple):
-        o = structure_forward(pos, z, cell, pbc, ds if hp.n_heads > 1 else 0, hp, W)
+        if blend_skip is None:
+            o = structure_forward(pos, z, cell, pbc, ds if hp.n_heads > 1 else 0, hp, W)
+        else:
+            o = structure_forward_blend(pos, z, cell, pbc, hp, W, skip=blend_skip)
         out.append((k, o["E"], float(np.sum(np.abs(o["e"])))))
     return out
 
 
-def oracle_energies(name: str, batch, idx, workers: int | None = None):
-    """Oracle (E, sum|e|) of structures `idx` of `batch`, in a process pool."""
+def oracle_energies(name: str, batch, idx, workers: int | None = None, blend_skip=None):
+    """Oracle (E, sum|e|) of structures `idx` of `batch`, in a process pool;
+    blend_skip given: every head blended, heads below it left out."""
     idx = [int(i) for i in idx]
     workers = workers or min(16, os.cpu_count() or 1, max(1, len(idx)))
     chunks = [idx[w::workers] for w in range(workers)]
-    jobs = [(name, [batch.structure(k) for k in c], c) for c in chunks if c]
+    jobs = [(name, [batch.structure(k) for k in c], c, blend_skip) for c in chunks if c]
     res = {}
     if workers == 1:
         for j in jobs:
