@@ -17,6 +17,11 @@ which equals the minimum-image graph whenever each cell width is >= 2 r_c.
 Edges are returned sorted by (receiver, sender, n0, n1, n2).  The image range
 enumerated here is deliberately generous (a superset of every image that can
 hold a neighbour); it does not change the set.
+
+With a neighbour cap (the lead model keeps at most 20 neighbours, Table 5),
+each receiver keeps its max_neighbors edges smallest in (d2, sender, n0, n1,
+n2) -- the exact d2 above, ties to the lower sender and shift -- and the
+kept edges stay in (sender, shift) order (R25).
 """
 from __future__ import annotations
 
@@ -62,8 +67,8 @@ def image_range(pos: np.ndarray, cell: np.ndarray, pbc, cutoff: float) -> list[i
     return m
 
 
-def radius_graph(pos, cell, pbc, cutoff: float):
-    """All edges of one structure.
+def radius_graph(pos, cell, pbc, cutoff: float, max_neighbors: int = 0):
+    """All edges of one structure (at most max_neighbors per receiver when > 0).
 
     Returns (recv, send, shift) with recv/send int64 [E] (structure-local atom
     indices) and shift int64 [E,3], sorted by (recv, send, shift).
@@ -101,7 +106,23 @@ def radius_graph(pos, cell, pbc, cutoff: float):
     send = np.concatenate(S) if S else np.zeros(0, np.int64)
     shift = np.concatenate(T) if T else np.zeros((0, 3), np.int64)
     order = np.lexsort((shift[:, 2], shift[:, 1], shift[:, 0], send, recv))
-    return recv[order].astype(np.int64), send[order].astype(np.int64), shift[order]
+    recv, send, shift = recv[order].astype(np.int64), send[order].astype(np.int64), shift[order]
+    if max_neighbors > 0:
+        recv, send, shift = cap_neighbors(x, a, recv, send, shift, max_neighbors)
+    return recv, send, shift
+
+
+def cap_neighbors(x, a, recv, send, shift, max_neighbors: int):
+    """Keep, per receiver, the max_neighbors edges smallest in (d2, sender,
+    shift); the result keeps the input's (receiver, sender, shift) order."""
+    r = edge_vectors(x, a, recv, send, shift)
+    d2 = (r[:, 0] * r[:, 0] + r[:, 1] * r[:, 1]) + r[:, 2] * r[:, 2]
+    order = np.lexsort((shift[:, 2], shift[:, 1], shift[:, 0], send, d2, recv))
+    rank = np.empty(len(recv), np.int64)
+    first = np.searchsorted(recv[order], recv[order], side="left")
+    rank[order] = np.arange(len(recv)) - first
+    keep = rank < max_neighbors
+    return recv[keep], send[keep], shift[keep]
 
 
 def edge_vectors(pos, cell, recv, send, shift) -> np.ndarray:
@@ -113,7 +134,7 @@ def edge_vectors(pos, cell, recv, send, shift) -> np.ndarray:
     return (x[send] - x[recv]) + t
 
 
-def batch_graph(batch, cutoff: float):
+def batch_graph(batch, cutoff: float, max_neighbors: int = 0):
     """Radius graph of a whole batch as a CSR with batch-global atom indices:
     (row_ptr int64 [N+1], col int64 [E], shift int64 [E,3])."""
     N = batch.n_atoms
@@ -121,7 +142,7 @@ def batch_graph(batch, cutoff: float):
     for b in range(batch.n_struct):
         lo = int(batch.struct_ptr[b])
         pos, _, cell, pbc, _ = batch.structure(b)
-        recv, send, shift = radius_graph(pos, cell, pbc, cutoff)
+        recv, send, shift = radius_graph(pos, cell, pbc, cutoff, max_neighbors)
         np.add.at(counts, recv + lo, 1)
         cols.append(send + lo)
         shifts.append(shift)

@@ -13,6 +13,8 @@ Per structure, with the radius graph of `oracle.neighbors`:
 
   edge features   d = |r|, rhat = r/d;  g_k(d) = exp(-gamma (d - mu_k)^2),
                   mu_k = k r_c/(K-1), gamma = 1/(2 Delta^2), Delta = r_c/(K-1)   (R6)
+                  or the Bessel basis (the lead model, Table 5)
+                  g_n(d) = sin(n pi d / r_c) / d, n = 1..K                       (R24)
                   f_c(d) = (cos(pi d / r_c) + 1)/2 for d < r_c                   (R7)
   init            s_i = Emb[z_i] in R^F,  v_i = 0 in R^{3 x F}
   layer, message  h_j = W2 silu(W1 s_j + b1) + b2 = [h^s | h^v | h^r]            (R8)
@@ -54,6 +56,25 @@ def gaussian_rbf(d, K: int, cutoff: float):
     mu = np.arange(K, dtype=np.float64) * delta
     gamma = 1.0 / (2.0 * delta * delta)
     return np.exp(-gamma * (d[..., None] - mu) ** 2)
+
+
+def bessel_rbf(d, K: int, cutoff: float):
+    """g_n(d) = sin(n pi d / r_c) / d for n = 1..K (PaiNN's radial basis; the
+    lead model of Table 5 uses 4 of them) (R24)."""
+    d = np.asarray(d, dtype=np.float64)
+    n = np.arange(1, K + 1, dtype=np.float64)
+    return np.sin(n * (np.pi / cutoff) * d[..., None]) / d[..., None]
+
+
+RBF_GAUSSIAN, RBF_BESSEL = 0, 1
+
+
+def radial_basis(d, K: int, cutoff: float, rbf_type: int = RBF_GAUSSIAN):
+    if rbf_type == RBF_GAUSSIAN:
+        return gaussian_rbf(d, K, cutoff)
+    if rbf_type == RBF_BESSEL:
+        return bessel_rbf(d, K, cutoff)
+    raise ValueError(f"unknown radial basis {rbf_type}")
 
 
 def cosine_cutoff(d, cutoff: float):
@@ -106,12 +127,12 @@ def structure_forward(pos, species, cell, pbc, dataset_id, hp, W, keep_layers: b
     z = np.asarray(species)
     if len(z) and (z.min() < 0 or z.max() >= hp.n_species):
         raise ValueError("species out of range")
-    recv, send, shift = radius_graph(pos, cell, pbc, rc)
+    recv, send, shift = radius_graph(pos, cell, pbc, rc, getattr(hp, "max_neighbors", 0))
     r = edge_vectors(pos, cell, recv, send, shift)
     d2 = (r[:, 0] * r[:, 0] + r[:, 1] * r[:, 1]) + r[:, 2] * r[:, 2]
     d = np.sqrt(d2)
     rhat = r / d[:, None]
-    g = gaussian_rbf(d, K, rc)                 # [E, K]
+    g = radial_basis(d, K, rc, hp.rbf_type)    # [E, K]
     fc = cosine_cutoff(d, rc)                  # [E]
     n = len(z)
     s = W["emb"][z].copy()
@@ -142,6 +163,8 @@ def structure_forward_dense(pos, species, cell, pbc, dataset_id, hp, W):
     is a masked sum over every (i, j, image) triple held as dense tensors,
     with no edge list.  Returns dict(E, e, s, v)."""
     F, K, rc = hp.F, hp.K, hp.cutoff
+    if getattr(hp, "max_neighbors", 0) > 0:
+        raise NotImplementedError("the dense formulation has no neighbour cap")
     x = np.asarray(pos, dtype=np.float64)
     a = np.asarray(cell, dtype=np.float64).reshape(3, 3)
     n = x.shape[0]
@@ -164,7 +187,7 @@ def structure_forward_dense(pos, species, cell, pbc, dataset_id, hp, W):
         raise CoincidentAtoms("coincident atoms")
     D = np.sqrt(np.where(mask, D2, 1.0))
     Rh = R / D[..., None]
-    G = gaussian_rbf(D, K, rc)                          # [n, n, P, K]
+    G = radial_basis(D, K, rc, hp.rbf_type)             # [n, n, P, K]
     Fc = np.where(mask, cosine_cutoff(D, rc), 0.0)      # [n, n, P]
     s = W["emb"][np.asarray(species)].copy()
     v = np.zeros((n, 3, F))

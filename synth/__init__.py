@@ -47,6 +47,8 @@ FILTER_GAIN = 0.25
 # Optional trailing section of the weight file: the branch-weighting MLP that
 # maps a structure's composition to softmax weights over the heads.
 BLEND_MAGIC = b"BLENDW01"
+# Optional section: a cap on the neighbours kept per receiver (Table 5: 20).
+NBRCAP_MAGIC = b"NBRCAP01"
 # A trained router is sharp (its teacher signal is one-hot per dataset); the
 # synthetic one gets a gain on its output layer so that, as reported for the
 # trained one, most branches carry negligible weight (~78 % below 0.01 on the
@@ -108,6 +110,8 @@ class HyperParams:
     # hidden widths of the branch-weighting MLP (composition -> head weights);
     # None: the model has none
     blend_dims: list | None = None
+    # neighbours kept per receiver, nearest first (0: every neighbour)
+    max_neighbors: int = 0
 
     @staticmethod
     def from_workload(name: str) -> "HyperParams":
@@ -117,7 +121,9 @@ class HyperParams:
                            n_heads=w["n_heads"], cutoff=w["cutoff"],
                            shared_dims=list(w["shared_dims"]),
                            branch_dims=list(w["branch_dims"]),
-                           blend_dims=None if bd is None else list(bd))
+                           rbf_type=w.get("rbf_type", RBF_GAUSSIAN),
+                           blend_dims=None if bd is None else list(bd),
+                           max_neighbors=w.get("max_neighbors", 0))
 
 
 @dataclass
@@ -380,6 +386,9 @@ def weight_file_bytes(hp: HyperParams, weights: dict) -> bytes:
         if a.shape != tuple(shape):
             raise ValueError(f"{name}: shape {a.shape} != {shape}")
         parts.append(a.tobytes())
+    if hp.max_neighbors > 0:
+        # optional section: magic 'NBRCAP01'; int32 max_neighbors, int32 0
+        parts.append(NBRCAP_MAGIC + struct.pack("<2i", hp.max_neighbors, 0))
     return b"".join(parts)
 
 
@@ -414,14 +423,19 @@ def read_weight_file(path_or_bytes) -> tuple[HyperParams, dict]:
             off += 8 * cnt
 
     take(weight_layout(hp))
-    if off < len(buf):
-        if buf[off:off + 8] != BLEND_MAGIC:
+    while off < len(buf):
+        magic = buf[off:off + 8]
+        if magic == BLEND_MAGIC and hp.blend_dims is None:
+            (nh,) = struct.unpack_from("<i", buf, off + 8)
+            hp.blend_dims = list(struct.unpack_from(f"<{nh}i", buf, off + 12))
+            off += 12 + 4 * nh
+            off += (-off) % 8
+            take([(n, sh) for n, sh in weight_layout(hp) if n.startswith("blend")])
+        elif magic == NBRCAP_MAGIC and hp.max_neighbors == 0:
+            hp.max_neighbors = struct.unpack_from("<i", buf, off + 8)[0]
+            off += 16
+        else:
             raise ValueError("trailing bytes in weight file")
-        (nh,) = struct.unpack_from("<i", buf, off + 8)
-        hp.blend_dims = list(struct.unpack_from(f"<{nh}i", buf, off + 12))
-        off += 12 + 4 * nh
-        off += (-off) % 8
-        take([(n, sh) for n, sh in weight_layout(hp) if n.startswith("blend")])
     if off != len(buf):
         raise ValueError("trailing bytes in weight file")
     return hp, w

@@ -135,3 +135,68 @@ def test_batch_graph_offsets_and_cutoff_edge_cases():
     assert len(radius_graph(pos, np.zeros((3, 3)), [0, 0, 0], 5.0)[0]) == 2
     # single atom, no pbc: no edges
     assert len(radius_graph(np.zeros((1, 3)), np.zeros((3, 3)), [0, 0, 0], 5.0)[0]) == 0
+
+
+# ---- neighbour cap (lead model: 20 neighbours, Table 5) ---------------------
+
+def _capped_by_loops(pos, cell, pbc, rc, cap):
+    """Independent brute force: every (i, j, n) in a small image box, the
+    exact d2, sorted tuples; the `cap` smallest (d2, j, n) per receiver,
+    returned in (i, j, n) order."""
+    x = np.asarray(pos, float)
+    a = np.asarray(cell, float)
+    m = [2 if p else 0 for p in pbc]
+    edges = []
+    for i in range(len(x)):
+        cand = []
+        for j in range(len(x)):
+            for n0 in range(-m[0], m[0] + 1):
+                for n1 in range(-m[1], m[1] + 1):
+                    for n2 in range(-m[2], m[2] + 1):
+                        if i == j and (n0, n1, n2) == (0, 0, 0):
+                            continue
+                        t = (float(n0) * a[0] + float(n1) * a[1]) + float(n2) * a[2]
+                        r = (x[j] - x[i]) + t
+                        d2 = (r[0] * r[0] + r[1] * r[1]) + r[2] * r[2]
+                        if d2 < rc * rc:
+                            cand.append((d2, j, n0, n1, n2))
+        for d2, j, n0, n1, n2 in sorted(cand)[:cap]:
+            edges.append((i, j, n0, n1, n2))
+    edges.sort()
+    e = np.array(edges, dtype=np.int64).reshape(-1, 5)
+    return e[:, 0], e[:, 1], e[:, 2:]
+
+
+def test_cap_matches_loops_molecule_and_cell():
+    rng = np.random.default_rng(12)
+    pos = rng.uniform(0, 5.0, (14, 3))
+    for cap in (1, 3, 6):
+        got = radius_graph(pos, np.zeros((3, 3)), [0, 0, 0], 3.5, cap)
+        want = _capped_by_loops(pos, np.zeros((3, 3)), [0, 0, 0], 3.5, cap)
+        for g, w in zip(got, want):
+            assert np.array_equal(g, w), cap
+    cell = np.array([[4.1, 0, 0], [0.6, 3.9, 0], [0.3, -0.4, 4.4]])
+    pos = rng.uniform(0, 1, (6, 3)) @ cell
+    got = radius_graph(pos, cell, [1, 1, 1], 3.0, 5)
+    want = _capped_by_loops(pos, cell, [1, 1, 1], 3.0, 5)
+    for g, w in zip(got, want):
+        assert np.array_equal(g, w)
+
+
+def test_cap_above_degree_changes_nothing_and_ties_go_to_lower_index():
+    rng = np.random.default_rng(13)
+    pos = rng.uniform(0, 6.0, (30, 3))
+    full = radius_graph(pos, np.zeros((3, 3)), [0, 0, 0], 3.0)
+    big = radius_graph(pos, np.zeros((3, 3)), [0, 0, 0], 3.0, 1000)
+    assert all(np.array_equal(a, b) for a, b in zip(full, big))
+    # simple cubic lattice, spacing 1: the centre's 6 nearest are equidistant
+    g = np.array([(i, j, k) for i in range(3) for j in range(3) for k in range(3)], float)
+    centre = 13
+    recv, send, shift = radius_graph(g, np.zeros((3, 3)), [0, 0, 0], 1.2, 3)
+    kept = send[recv == centre]
+    six = sorted(j for j in range(27) if abs(np.abs(g[j] - g[centre]).sum() - 1.0) < 1e-12)
+    assert kept.tolist() == six[:3]
+    # periodic: an atom alone in a cubic cell of side 1 has 6 images at distance 1;
+    # with cap 2 the lowest shifts in (n0, n1, n2) order are kept
+    r, s, t = radius_graph(np.zeros((1, 3)), np.eye(3), [1, 1, 1], 1.2, 2)
+    assert t.tolist() == [[-1, 0, 0], [0, -1, 0]]
