@@ -81,7 +81,10 @@ painn_status painn_synchronize(painn_ctx* ctx);
 
 /* Load an FP64 weight file (host path).  Format, little-endian:
  *   char magic[8] = "PAINNW01";
- *   int32 F, K, L, n_species, n_heads, rbf_type (0 = Gaussian), n_shared, n_branch;
+ *   int32 F, K, L, n_species, n_heads, rbf_type, n_shared, n_branch;
+ *     rbf_type 0: Gaussians exp(-gamma (d - mu_k)^2), mu_k = k r_c / (K - 1),
+ *     gamma = 1 / (2 Delta^2), Delta = r_c / (K - 1); 1: Bessel sin(n pi d / r_c) / d,
+ *     n = 1..K (the lead model's basis, Table 5); both under the cosine cutoff;
  *   float64 cutoff;
  *   int32 shared_dims[n_shared];   output width of each shared head layer
  *   int32 branch_dims[n_branch];   output width of each branch layer (last = 1)
@@ -98,6 +101,9 @@ painn_status painn_synchronize(painn_ctx* ctx);
  *   int32 hidden_dims[n_hidden]; zero padding to a multiple of 8 bytes;
  *   float64 layers w[out, in] b[out] from n_species through the hidden widths
  *   to n_heads.
+ *   optional, a neighbour cap: char magic[8] = "NBRCAP01"; int32 max_neighbors;
+ *   int32 0.  Optional sections follow the arrays, each at most once, in any
+ *   order.
  * The split of phi's output is [s | v | rhat] and of the update MLP's output
  * [a_vv | a_sv | a_ss].  Supported: F in {64, 128, 256}, 2 <= K <= 64,
  * 1 <= L <= 16, n_heads <= 64, branch_dims[last] = 1; with the
@@ -110,9 +116,10 @@ painn_status painn_model_load_buffer(painn_ctx* ctx, const void* data, size_t nb
 /* Hyperparameters of a model (host outputs; any pointer may be NULL). */
 painn_status painn_model_info(const painn_model* model, int32_t* F, int32_t* K, int32_t* L,
                               int32_t* n_species, int32_t* n_heads, double* cutoff);
-/* Whether the model carries a branch-weighting MLP (host output *has_blend
- * = 1 or 0). */
-painn_status painn_model_has_blend(const painn_model* model, int32_t* has_blend);
+/* Optional parts of a model (host outputs; either pointer may be NULL):
+ * *has_blend = 1 when it carries a branch-weighting MLP, else 0;
+ * *max_neighbors = its neighbour cap (0: none). */
+painn_status painn_model_options(const painn_model* model, int32_t* has_blend, int32_t* max_neighbors);
 painn_status painn_model_free(painn_model* model);
 
 /* ---- graph -------------------------------------------------------------- */
@@ -143,6 +150,16 @@ painn_status painn_build_graph(painn_ctx* ctx, int32_t n_struct, int32_t n_atoms
                                const int32_t* struct_ptr, const double* pos,
                                const int32_t* species, const double* cell,
                                const uint8_t* pbc, double cutoff, painn_graph** inout);
+/* Same, keeping at most max_neighbors edges per receiver (0: every edge): the
+ * nearest ones, by the exact d2 above, ties to the lower sender and then the
+ * lower shift (n0, n1, n2); the kept edges stay in (sender, shift) order.
+ * The lead model keeps 20 (Table 5).  A model whose weight file carries a
+ * neighbour cap runs only on a graph built with that cap. */
+painn_status painn_build_graph_capped(painn_ctx* ctx, int32_t n_struct, int32_t n_atoms,
+                                      const int32_t* struct_ptr, const double* pos,
+                                      const int32_t* species, const double* cell,
+                                      const uint8_t* pbc, double cutoff, int32_t max_neighbors,
+                                      painn_graph** inout);
 /* Borrow the CSR of a graph (device pointers valid until the graph is rebuilt
  * or freed): row_ptr [N+1] int32, col [E] int32 (batch-global sender index),
  * shift [E] int32 packing (n0, n1, n2) as signed bytes 0, 1, 2 (byte 3 = 0).

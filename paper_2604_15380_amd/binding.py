@@ -12,8 +12,8 @@ PRECISIONS = {"fp64": PAINN_FP64, "fp32": PAINN_FP32, "bf16": PAINN_BF16}
 EXPORTS = [
     "painn_create", "painn_set_stream", "painn_destroy", "painn_last_error",
     "painn_status_string", "painn_synchronize", "painn_model_load",
-    "painn_model_load_buffer", "painn_model_info", "painn_model_has_blend", "painn_model_free",
-    "painn_build_graph", "painn_graph_csr", "painn_graph_free", "painn_forward",
+    "painn_model_load_buffer", "painn_model_info", "painn_model_options", "painn_model_free",
+    "painn_build_graph", "painn_build_graph_capped", "painn_graph_csr", "painn_graph_free", "painn_forward",
     "painn_forward_blend", "painn_forward_features", "painn_profile_enable", "painn_profile_read",
 ]
 
@@ -29,10 +29,12 @@ _SIGS = {
     "painn_model_load": ([_P, ctypes.c_char_p, ctypes.POINTER(_P)], ctypes.c_int),
     "painn_model_load_buffer": ([_P, ctypes.c_char_p, ctypes.c_size_t, ctypes.POINTER(_P)], ctypes.c_int),
     "painn_model_info": ([_P] + [ctypes.POINTER(_I32)] * 5 + [ctypes.POINTER(ctypes.c_double)], ctypes.c_int),
-    "painn_model_has_blend": ([_P, ctypes.POINTER(_I32)], ctypes.c_int),
+    "painn_model_options": ([_P, ctypes.POINTER(_I32), ctypes.POINTER(_I32)], ctypes.c_int),
     "painn_model_free": ([_P], ctypes.c_int),
     "painn_build_graph": ([_P, _I32, _I32, _P, _P, _P, _P, _P, ctypes.c_double, ctypes.POINTER(_P)],
                           ctypes.c_int),
+    "painn_build_graph_capped": ([_P, _I32, _I32, _P, _P, _P, _P, _P, ctypes.c_double, _I32,
+                                  ctypes.POINTER(_P)], ctypes.c_int),
     "painn_graph_csr": ([_P, ctypes.POINTER(ctypes.c_int64), ctypes.POINTER(_I32), ctypes.POINTER(_I32),
                          ctypes.POINTER(_P), ctypes.POINTER(_P), ctypes.POINTER(_P)], ctypes.c_int),
     "painn_graph_free": ([_P], ctypes.c_int),
@@ -128,10 +130,10 @@ def painn_model_info(model: int) -> dict:
                 n_heads=v[4].value, cutoff=rc.value)
 
 
-def painn_model_has_blend(model: int) -> bool:
-    v = _I32()
-    _check(load_library().painn_model_has_blend(model, ctypes.byref(v)))
-    return bool(v.value)
+def painn_model_options(model: int) -> dict:
+    hb, mn = _I32(), _I32()
+    _check(load_library().painn_model_options(model, ctypes.byref(hb), ctypes.byref(mn)))
+    return dict(has_blend=bool(hb.value), max_neighbors=mn.value)
 
 
 def painn_model_free(model: int) -> None:
@@ -144,6 +146,16 @@ def painn_build_graph(ctx: int, n_struct: int, n_atoms: int, struct_ptr: int, po
     g = _P(graph)
     _check(load_library().painn_build_graph(ctx, n_struct, n_atoms, struct_ptr, pos, species,
                                             cell or None, pbc or None, cutoff, ctypes.byref(g)), ctx)
+    return g.value
+
+
+def painn_build_graph_capped(ctx: int, n_struct: int, n_atoms: int, struct_ptr: int, pos: int,
+                             species: int, cell: int | None, pbc: int | None, cutoff: float,
+                             max_neighbors: int, graph: int | None = None) -> int:
+    g = _P(graph)
+    _check(load_library().painn_build_graph_capped(ctx, n_struct, n_atoms, struct_ptr, pos, species,
+                                                   cell or None, pbc or None, cutoff, max_neighbors,
+                                                   ctypes.byref(g)), ctx)
     return g.value
 
 

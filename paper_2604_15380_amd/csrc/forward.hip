@@ -122,7 +122,7 @@ __device__ __forceinline__ int acc_to_index(double x) { return (int)x; }
 //   r = (x_j - x_i) + (n0 a + n1 b) + n2 c  (FP64),  d = |r|,  rhat = r / d,
 //   f_c = (cos(pi d / r_c) + 1) / 2,  g_k = exp(-gamma (d - k Delta)^2).
 template <class P>
-__global__ void __launch_bounds__(256) k_edge_prep(long long E, int K, int kcols, double rc,
+__global__ void __launch_bounds__(256) k_edge_prep(long long E, int K, int kcols, double rc, int rbf,
                                                   double gamma, double delta,
                                                   const int32_t* __restrict__ recv,
                                                   const int32_t* __restrict__ col,
@@ -162,9 +162,12 @@ __global__ void __launch_bounds__(256) k_edge_prep(long long E, int K, int kcols
     const bool lo = SPLIT && k > K;
     const int kk = lo ? k - (K + 1) : k;
     A val = 0;
-    if (kk < K) {
+    if (kk < K && rbf == 0) {                    // Gaussian
       const A t = dd - (A)(kk * delta);
       val = P::ex(-(A)gamma * t * t) * fc;
+    } else if (kk < K) {                         // Bessel: sin(n pi d / r_c) / d
+      const A arg = (A)((kk + 1) * (3.14159265358979323846 / rc)) * dd;
+      val = (sizeof(A) == 8 ? (A)sin((double)arg) : (A)sinf((float)arg)) / dd * fc;
     } else if (kk == K) {
       val = fc;
     }
@@ -1327,7 +1330,7 @@ hipError_t forward_impl(hipStream_t st, ForwardArgs& fa) {
     prof_mark(fa.prof, st, KC_EDGE_PREP, true);
     const double delta = hp.cutoff / (hp.K - 1);
     k_edge_prep<P><<<(unsigned)((g->E + 16 + 255) / 256), 256, 0, st>>>(
-        g->E, hp.K, kcols, hp.cutoff, 1.0 / (2.0 * delta * delta), delta, g->recv, g->col, g->shift,
+        g->E, hp.K, kcols, hp.cutoff, hp.rbf_type, 1.0 / (2.0 * delta * delta), delta, g->recv, g->col, g->shift,
         g->atom_struct, g->pos, g->cell, (T*)fa.basis, (A*)fa.einfo);
     prof_mark(fa.prof, st, KC_EDGE_PREP, false);
   }

@@ -26,6 +26,7 @@ struct DevStatus {      // read back once per build_graph
   int32_t species_min;
   int32_t species_max;
   int32_t cells;        // structures searched with a cell list
+  long long n_edges_cap;  // edges kept under a neighbour cap
 };
 
 struct StructInfo {     // per structure: atom range and periodic image range
@@ -106,6 +107,7 @@ struct Hyper {
   std::vector<int> shared_dims, branch_dims;
   std::vector<int> blend_dims;   // hidden widths of the branch-weighting MLP
   bool has_blend = false;
+  int max_neighbors = 0;         // neighbour cap the model was trained with (0: none)
 };
 
 // ---- per-kernel event timing (painn_profile_*) ------------------------------
@@ -162,6 +164,13 @@ struct painn_graph {
   int32_t* bin_count = nullptr; int32_t* bin_start = nullptr;
   long long* bin_scan_tmp = nullptr;
   size_t n_bins = 0;
+  // neighbour cap (0: none): the full CSR is built first, then each
+  // receiver keeps its max_neighbors nearest edges in the public arrays above
+  int32_t max_neighbors = 0;
+  long long E_full = 0;
+  int32_t* counts_cap = nullptr;  int32_t* row_ptr_full = nullptr;
+  int32_t* col_full = nullptr;    int32_t* shift_full = nullptr;  int32_t* recv_full = nullptr;
+  size_t cap_edges_full = 0, cap_atoms_cap = 0;
   size_t cap_atoms = 0, cap_struct = 0, cap_edges = 0, cap_scan = 0, cap_bins = 0, cap_bin_scan = 0;
 };
 
@@ -172,6 +181,10 @@ hipError_t launch_graph_prep(hipStream_t s, Profiler* p, int B, int N, const int
 hipError_t launch_graph_count(hipStream_t s, Profiler* p, painn_graph* g);
 hipError_t launch_graph_scan(hipStream_t s, Profiler* p, painn_graph* g);
 hipError_t launch_graph_fill(hipStream_t s, Profiler* p, painn_graph* g);
+// neighbour cap: capped counts and their scan (before the readback), then
+// the nearest-neighbour selection (after the full fill)
+hipError_t launch_graph_cap_scan(hipStream_t s, Profiler* p, painn_graph* g);
+hipError_t launch_graph_cap_select(hipStream_t s, Profiler* p, painn_graph* g);
 
 struct ForwardArgs {
   const painn_model* m;

@@ -223,6 +223,7 @@ __global__ void k_status_init(DevStatus* st) {
   st->species_min = 0x7fffffff;
   st->species_max = -0x7fffffff - 1;
   st->cells = 0;
+  st->n_edges_cap = 0;
 }
 
 // The candidate test shared by the count and fill passes.  Candidate index t
@@ -518,7 +519,7 @@ __global__ void __launch_bounds__(256) k_scan_blocks(long long n, const int32_t*
   if (threadIdx.x == 0) bsum[blockIdx.x] = sh[0];
 }
 
-template <bool EDGES>
+template <bool EDGES, bool CAPPED = false>
 __global__ void __launch_bounds__(256) k_scan_top(int nblk, long long* __restrict__ bsum,
                                                  DevStatus* st, int32_t* __restrict__ out,
                                                  long long n) {
@@ -541,7 +542,9 @@ __global__ void __launch_bounds__(256) k_scan_top(int nblk, long long* __restric
     __syncthreads();
   }
   if (threadIdx.x == 0) {
-    if (EDGES) {
+    if (EDGES && CAPPED) {
+      st->n_edges_cap = carry;
+    } else if (EDGES) {
       st->n_edges = carry;
       if (carry > 0x7fffffffLL) atomicOr(&st->err, ERR_EDGES);
     }
@@ -574,6 +577,101 @@ __global__ void __launch_bounds__(256) k_scan_apply(long long n, const int32_t* 
   for (int k = 0; k < 4; ++k) {
     if (base + k < n) out[base + k] = (int32_t)run;
     run += v[k];
+  }
+}
+
+// ---------------------------------------------------------- neighbour cap ----
+__global__ void __launch_bounds__(256) k_cap_counts(int N, int cap, const int32_t* __restrict__ counts,
+                                                   int32_t* __restrict__ counts_cap) {
+  const int i = blockIdx.x * 256 + threadIdx.x;
+  if (i < N) counts_cap[i] = min(counts[i], cap);
+}
+
+// Squared length of edge (i <- j, packed shift) by the neighbour test's
+// exact expression.
+__device__ inline double edge_d2(const painn_graph& g, int i, int j, int packed) {
+#pragma clang fp contract(off)
+  int b = g.atom_struct[i];
+  b = b < 0 ? 0 : (b >= g.B ? g.B - 1 : b);
+  const double* A = g.cell + 9 * b;
+  const double f0 = (double)(int8_t)(packed & 0xff), f1 = (double)(int8_t)((packed >> 8) & 0xff),
+               f2 = (double)(int8_t)((packed >> 16) & 0xff);
+  const double tx = (f0 * A[0] + f1 * A[3]) + f2 * A[6];
+  const double ty = (f0 * A[1] + f1 * A[4]) + f2 * A[7];
+  const double tz = (f0 * A[2] + f1 * A[5]) + f2 * A[8];
+  const double rx = (g.pos[3 * j + 0] - g.pos[3 * i + 0]) + tx;
+  const double ry = (g.pos[3 * j + 1] - g.pos[3 * i + 1]) + ty;
+  const double rz = (g.pos[3 * j + 2] - g.pos[3 * i + 2]) + tz;
+  return (rx * rx + ry * ry) + rz * rz;
+}
+
+// (d2, sender, shift) order; keys within a row are distinct
+__device__ inline bool cap_less(double da, int ja, uint32_t sa, double db, int jb, uint32_t sb) {
+  return da < db || (da == db && (ja < jb || (ja == jb && sa < sb)));
+}
+
+constexpr int CAP_LDS = 256;   // edges of a row a wave ranks from LDS
+
+// Each receiver (one wave) keeps the max_neighbors edges of its full row
+// smallest in (d2, sender, shift) and writes them, in row order (sender,
+// shift), to its capped row.  Rows longer than CAP_LDS recompute the keys.
+__global__ void __launch_bounds__(256) k_cap_select(painn_graph g) {
+  __shared__ double kd[4][CAP_LDS];
+  __shared__ int kj[4][CAP_LDS];
+  __shared__ uint32_t ks[4][CAP_LDS];
+  const int lane = threadIdx.x % WAVE, wv = threadIdx.x / WAVE;
+  const int i = blockIdx.x * 4 + wv;
+  if (i >= g.N) return;
+  const int a = g.row_ptr_full[i], deg = g.row_ptr_full[i + 1] - a;
+  const int out0 = g.row_ptr[i];
+  const int cap = g.max_neighbors;
+  if (deg <= cap) {
+    for (int e = lane; e < deg; e += WAVE) {
+      g.col[out0 + e] = g.col_full[a + e];
+      g.shift[out0 + e] = g.shift_full[a + e];
+      g.recv[out0 + e] = i;
+    }
+    return;
+  }
+  const bool lds = deg <= CAP_LDS;
+  if (lds) {
+    for (int e = lane; e < deg; e += WAVE) {
+      const int j = g.col_full[a + e], p = g.shift_full[a + e];
+      kd[wv][e] = edge_d2(g, i, j, p);
+      kj[wv][e] = j;
+      ks[wv][e] = shift_key(p);
+    }
+    __builtin_amdgcn_wave_barrier();
+    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+  }
+  int out = out0;
+  for (int t0 = 0; t0 < deg; t0 += WAVE) {
+    const int e = t0 + lane;
+    bool keep = false;
+    int j = 0, p = 0;
+    if (e < deg) {
+      j = g.col_full[a + e];
+      p = g.shift_full[a + e];
+      const double d = lds ? kd[wv][e] : edge_d2(g, i, j, p);
+      const uint32_t sk = shift_key(p);
+      int rank = 0;
+      for (int f = 0; f < deg && rank < cap; ++f) {
+        const double df = lds ? kd[wv][f] : edge_d2(g, i, g.col_full[a + f], g.shift_full[a + f]);
+        const int jf = lds ? kj[wv][f] : g.col_full[a + f];
+        const uint32_t sf = lds ? ks[wv][f] : shift_key(g.shift_full[a + f]);
+        rank += cap_less(df, jf, sf, d, j, sk);
+      }
+      keep = rank < cap;
+    }
+    const unsigned long long mask = ballot(keep);
+    if (keep) {
+      const int at = out + __popcll(mask & ((1ull << lane) - 1ull));
+      g.col[at] = j;
+      g.shift[at] = p;
+      g.recv[at] = i;
+    }
+    out += __popcll(mask);
   }
 }
 
@@ -622,6 +720,24 @@ hipError_t launch_graph_scan(hipStream_t s, Profiler* p, painn_graph* g) {
 hipError_t launch_graph_fill(hipStream_t s, Profiler* p, painn_graph* g) {
   prof_mark(p, s, KC_GRAPH_FILL, true);
   if (g->N > 0 && g->E > 0) k_edges<true><<<(g->N + 3) / 4, 256, 0, s>>>(*g, g->cutoff * g->cutoff);
+  prof_mark(p, s, KC_GRAPH_FILL, false);
+  return hipGetLastError();
+}
+
+hipError_t launch_graph_cap_scan(hipStream_t s, Profiler* p, painn_graph* g) {
+  const int nblk = (g->N + 1023) / 1024;
+  prof_mark(p, s, KC_GRAPH_SCAN, true);
+  if (g->N > 0) k_cap_counts<<<(g->N + 255) / 256, 256, 0, s>>>(g->N, g->max_neighbors, g->counts, g->counts_cap);
+  if (nblk > 0) k_scan_blocks<true><<<nblk, 256, 0, s>>>(g->N, g->counts_cap, g->scan_tmp, g->d_status);
+  k_scan_top<true, true><<<1, 256, 0, s>>>(nblk, g->scan_tmp, g->d_status, g->row_ptr, g->N);
+  if (nblk > 0) k_scan_apply<true><<<nblk, 256, 0, s>>>(g->N, g->counts_cap, g->scan_tmp, g->row_ptr, g->d_status);
+  prof_mark(p, s, KC_GRAPH_SCAN, false);
+  return hipGetLastError();
+}
+
+hipError_t launch_graph_cap_select(hipStream_t s, Profiler* p, painn_graph* g) {
+  prof_mark(p, s, KC_GRAPH_FILL, true);
+  if (g->N > 0 && g->E > 0) k_cap_select<<<(g->N + 3) / 4, 256, 0, s>>>(*g);
   prof_mark(p, s, KC_GRAPH_FILL, false);
   return hipGetLastError();
 }

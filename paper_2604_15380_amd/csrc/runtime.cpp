@@ -271,7 +271,8 @@ painn_status parse_model(painn_ctx* ctx, const unsigned char* buf, size_t n, pai
   if (hp.L < 1 || hp.L > 16) return fail(ctx, PAINN_E_UNSUPPORTED, "L must be in [1, 16]");
   if (hp.n_species < 1 || hp.n_species > 1024) return fail(ctx, PAINN_E_FORMAT, "bad n_species");
   if (hp.n_heads < 1 || hp.n_heads > 64) return fail(ctx, PAINN_E_UNSUPPORTED, "n_heads must be in [1, 64]");
-  if (hp.rbf_type != 0) return fail(ctx, PAINN_E_UNSUPPORTED, "only the Gaussian radial basis is implemented");
+  if (hp.rbf_type != 0 && hp.rbf_type != 1)
+    return fail(ctx, PAINN_E_UNSUPPORTED, "radial basis must be 0 (Gaussian) or 1 (Bessel)");
   if (!(hp.cutoff > 0.0) || !isfinite(hp.cutoff)) return fail(ctx, PAINN_E_FORMAT, "bad cutoff");
   for (int d : hp.shared_dims)
     if (d < 1 || d > 1024) return fail(ctx, PAINN_E_UNSUPPORTED, "head widths must be in [1, 1024]");
@@ -296,38 +297,54 @@ painn_status parse_model(painn_ctx* ctx, const unsigned char* buf, size_t n, pai
   size_t total = 0;
   for (size_t s : sizes) total += s;
   const size_t main_total = total;
-  // optional branch-weighting MLP after the main arrays: 'BLENDW01', int32
-  // n_hidden, the hidden widths, zero padding to 8 bytes, then its layers
-  // (composition [n_species] -> hidden ... -> n_heads), each [out, in] + bias
+  // optional sections after the main arrays, each at most once, any order:
+  //   'BLENDW01', int32 n_hidden, the hidden widths, zero padding to 8 bytes,
+  //     then the branch-weighting MLP's layers (composition [n_species] ->
+  //     hidden ... -> n_heads), each [out, in] + bias;
+  //   'NBRCAP01', int32 max_neighbors, int32 0.
   size_t blend_off = 0;
-  if (n != off + 8 * main_total) {
-    size_t bo = off + 8 * main_total;
-    if (n < bo + 12 || memcmp(buf + bo, "BLENDW01", 8) != 0)
+  size_t bo = off + 8 * main_total;
+  bool has_cap = false;
+  while (bo < n) {
+    if (n < bo + 16) return fail(ctx, PAINN_E_FORMAT, "weight file: size does not match its header");
+    if (memcmp(buf + bo, "BLENDW01", 8) == 0 && !hp.has_blend) {
+      int32_t nh;
+      memcpy(&nh, buf + bo + 8, 4);
+      if (nh < 0 || nh > 8 || n < bo + 12 + 4 * (size_t)nh)
+        return fail(ctx, PAINN_E_FORMAT, "weight file: bad branch-weighting section");
+      bo += 12;
+      for (int i = 0; i < nh; ++i) { int32_t d; memcpy(&d, buf + bo, 4); bo += 4; hp.blend_dims.push_back(d); }
+      bo += (8 - bo % 8) % 8;
+      for (int d : hp.blend_dims)
+        if (d < 1 || d > 1024) return fail(ctx, PAINN_E_UNSUPPORTED, "branch-weighting widths must be in [1, 1024]");
+      if (hp.n_species > 256) return fail(ctx, PAINN_E_UNSUPPORTED, "branch weighting needs n_species <= 256");
+      size_t di = hp.n_species, cnt = 0;
+      std::vector<int> dims = hp.blend_dims;
+      dims.push_back(hp.n_heads);
+      for (int d : dims) {
+        sizes.push_back((size_t)d * di);
+        sizes.push_back(d);
+        cnt += (size_t)d * di + d;
+        di = d;
+      }
+      if (n < bo + 8 * cnt)
+        return fail(ctx, PAINN_E_FORMAT, "weight file: branch-weighting section is truncated");
+      total += cnt;
+      hp.has_blend = true;
+      blend_off = bo;
+      bo += 8 * cnt;
+    } else if (memcmp(buf + bo, "NBRCAP01", 8) == 0 && !has_cap) {
+      int32_t c;
+      memcpy(&c, buf + bo + 8, 4);
+      if (c < 1) return fail(ctx, PAINN_E_FORMAT, "weight file: neighbour cap must be >= 1");
+      hp.max_neighbors = c;
+      has_cap = true;
+      bo += 16;
+    } else {
       return fail(ctx, PAINN_E_FORMAT, "weight file: size does not match its header");
-    int32_t nh;
-    memcpy(&nh, buf + bo + 8, 4);
-    if (nh < 0 || nh > 8 || n < bo + 12 + 4 * (size_t)nh)
-      return fail(ctx, PAINN_E_FORMAT, "weight file: bad branch-weighting section");
-    bo += 12;
-    for (int i = 0; i < nh; ++i) { int32_t d; memcpy(&d, buf + bo, 4); bo += 4; hp.blend_dims.push_back(d); }
-    bo += (8 - bo % 8) % 8;
-    for (int d : hp.blend_dims)
-      if (d < 1 || d > 1024) return fail(ctx, PAINN_E_UNSUPPORTED, "branch-weighting widths must be in [1, 1024]");
-    if (hp.n_species > 256) return fail(ctx, PAINN_E_UNSUPPORTED, "branch weighting needs n_species <= 256");
-    size_t di = hp.n_species;
-    std::vector<int> dims = hp.blend_dims;
-    dims.push_back(hp.n_heads);
-    for (int d : dims) {
-      sizes.push_back((size_t)d * di);
-      sizes.push_back(d);
-      total += (size_t)d * di + d;
-      di = d;
     }
-    if (n != bo + 8 * (total - main_total))
-      return fail(ctx, PAINN_E_FORMAT, "weight file: branch-weighting section size does not match its header");
-    hp.has_blend = true;
-    blend_off = bo;
   }
+  if (bo != n) return fail(ctx, PAINN_E_FORMAT, "weight file: size does not match its header");
   painn_model* m = new (std::nothrow) painn_model();
   if (!m) return fail(ctx, PAINN_E_OOM, "host allocation failed");
   m->ctx = ctx;
@@ -510,9 +527,10 @@ painn_status painn_model_load(painn_ctx* ctx, const char* path, painn_model** ou
   return painn_model_load_buffer(ctx, buf.data(), buf.size(), out);
 }
 
-painn_status painn_model_has_blend(const painn_model* m, int32_t* has_blend) {
-  if (!m || !has_blend) return PAINN_E_ARG;
-  *has_blend = m->hp.has_blend ? 1 : 0;
+painn_status painn_model_options(const painn_model* m, int32_t* has_blend, int32_t* max_neighbors) {
+  if (!m) return PAINN_E_ARG;
+  if (has_blend) *has_blend = m->hp.has_blend ? 1 : 0;
+  if (max_neighbors) *max_neighbors = m->hp.max_neighbors;
   return PAINN_OK;
 }
 
@@ -547,7 +565,8 @@ painn_status painn_graph_free(painn_graph* g) {
   }
   void* bufs[] = {g->row_ptr, g->counts, g->col, g->shift, g->recv, g->pos, g->species, g->atom_struct,
                   g->cell, g->sinfo, g->struct_ptr, g->scan_tmp, g->d_status, g->grid, g->bin_of,
-                  g->wrap, g->bin_atoms, g->bin_count, g->bin_start, g->bin_scan_tmp};
+                  g->wrap, g->bin_atoms, g->bin_count, g->bin_start, g->bin_scan_tmp,
+                  g->counts_cap, g->row_ptr_full, g->col_full, g->shift_full, g->recv_full};
   for (void* p : bufs)
     if (p) (void)hipFree(p);
   delete g;
@@ -557,8 +576,16 @@ painn_status painn_graph_free(painn_graph* g) {
 painn_status painn_build_graph(painn_ctx* ctx, int32_t B, int32_t N, const int32_t* struct_ptr,
                                const double* pos, const int32_t* species, const double* cell,
                                const uint8_t* pbc, double cutoff, painn_graph** inout) {
+  return painn_build_graph_capped(ctx, B, N, struct_ptr, pos, species, cell, pbc, cutoff, 0, inout);
+}
+
+painn_status painn_build_graph_capped(painn_ctx* ctx, int32_t B, int32_t N, const int32_t* struct_ptr,
+                                      const double* pos, const int32_t* species, const double* cell,
+                                      const uint8_t* pbc, double cutoff, int32_t max_neighbors,
+                                      painn_graph** inout) {
   if (!ctx) return PAINN_E_ARG;
   ctx->err.clear();
+  if (max_neighbors < 0) return fail(ctx, PAINN_E_ARG, "max_neighbors must be >= 0");
   if (!inout) return fail(ctx, PAINN_E_ARG, "inout is null");
   if (B < 0 || N < 0) return fail(ctx, PAINN_E_ARG, "negative size");
   if (B == 0 && N != 0) return fail(ctx, PAINN_E_ARG, "atoms given without structures");
@@ -630,6 +657,17 @@ painn_status painn_build_graph(painn_ctx* ctx, int32_t B, int32_t N, const int32
   if (e == hipSuccess) e = ensure(&g->bin_scan_tmp, &capbs, (g->n_bins + 1023) / 1024 + 1);
   g->cap_bins = capb;
   g->cap_bin_scan = capbs;
+  g->max_neighbors = max_neighbors;
+  if (e == hipSuccess && max_neighbors > 0 &&
+      ((size_t)N + 1 > g->cap_atoms_cap || !g->row_ptr_full || !g->counts_cap)) {
+    size_t c0 = 0, c1 = 0;
+    if (g->row_ptr_full) { (void)hipFree(g->row_ptr_full); g->row_ptr_full = nullptr; }
+    if (g->counts_cap) { (void)hipFree(g->counts_cap); g->counts_cap = nullptr; }
+    g->cap_atoms_cap = 0;
+    e = ensure(&g->row_ptr_full, &c0, (size_t)N + 1);
+    if (e == hipSuccess) e = ensure(&g->counts_cap, &c1, c0);
+    if (e == hipSuccess) g->cap_atoms_cap = c0;
+  }
   if (e == hipSuccess && !g->d_status) e = hipMalloc((void**)&g->d_status, sizeof(DevStatus));
   if (e != hipSuccess) return bail(PAINN_E_OOM, std::string("device allocation: ") + hipGetErrorString(e));
   g->cap_atoms = capa;
@@ -637,9 +675,14 @@ painn_status painn_build_graph(painn_ctx* ctx, int32_t B, int32_t N, const int32
   g->cap_scan = capsc;
 
   (void)hipGetLastError();   // do not report an error left by earlier, unrelated calls
+  // with a cap, the full CSR lives in the *_full arrays: a copy of the
+  // descriptor points the count/scan/fill launches at them
+  painn_graph full = *g;
+  if (max_neighbors > 0) full.row_ptr = g->row_ptr_full;
   e = launch_graph_prep(ctx->stream, ctx->prof, B, N, struct_ptr, pos, species, cell, pbc, cutoff, g);
   if (e == hipSuccess) e = launch_graph_count(ctx->stream, ctx->prof, g);
-  if (e == hipSuccess) e = launch_graph_scan(ctx->stream, ctx->prof, g);
+  if (e == hipSuccess) e = launch_graph_scan(ctx->stream, ctx->prof, max_neighbors > 0 ? &full : g);
+  if (e == hipSuccess && max_neighbors > 0) e = launch_graph_cap_scan(ctx->stream, ctx->prof, g);
   if (e == hipSuccess)
     e = hipMemcpyAsync(ctx->h_status, g->d_status, sizeof(DevStatus), hipMemcpyDeviceToHost, ctx->stream);
   if (e == hipSuccess) e = hipStreamSynchronize(ctx->stream);
@@ -662,9 +705,24 @@ painn_status painn_build_graph(painn_ctx* ctx, int32_t B, int32_t N, const int32
     g->E = 0;
     return bail(code, msg);
   }
-  g->E = st.n_edges;
+  g->E_full = st.n_edges;
+  g->E = max_neighbors > 0 ? st.n_edges_cap : st.n_edges;
   g->species_min = st.species_min;
   g->species_max = st.species_max;
+  if (max_neighbors > 0 && ((size_t)g->E_full > g->cap_edges_full || !g->col_full)) {
+    size_t c1 = 0, c2 = 0, c3 = 0;
+    if (g->col_full) { (void)hipFree(g->col_full); g->col_full = nullptr; }
+    if (g->shift_full) { (void)hipFree(g->shift_full); g->shift_full = nullptr; }
+    if (g->recv_full) { (void)hipFree(g->recv_full); g->recv_full = nullptr; }
+    e = ensure(&g->col_full, &c1, (size_t)g->E_full);
+    if (e == hipSuccess) e = ensure(&g->shift_full, &c2, c1);
+    if (e == hipSuccess) e = ensure(&g->recv_full, &c3, c1);
+    if (e != hipSuccess) {
+      g->cap_edges_full = 0;
+      return bail(PAINN_E_OOM, std::string("edge allocation: ") + hipGetErrorString(e));
+    }
+    g->cap_edges_full = c1;
+  }
   size_t cape = g->cap_edges;
   if ((size_t)g->E > g->cap_edges || !g->col) {
     size_t c2 = 0;
@@ -681,7 +739,18 @@ painn_status painn_build_graph(painn_ctx* ctx, int32_t B, int32_t N, const int32
     }
     g->cap_edges = cape;
   }
-  e = launch_graph_fill(ctx->stream, ctx->prof, g);
+  if (max_neighbors > 0) {
+    full = *g;
+    full.row_ptr = g->row_ptr_full;
+    full.col = g->col_full;
+    full.shift = g->shift_full;
+    full.recv = g->recv_full;
+    full.E = g->E_full;
+    e = launch_graph_fill(ctx->stream, ctx->prof, &full);
+    if (e == hipSuccess) e = launch_graph_cap_select(ctx->stream, ctx->prof, g);
+  } else {
+    e = launch_graph_fill(ctx->stream, ctx->prof, g);
+  }
   if (e != hipSuccess) {
     (void)hipGetLastError();
     return bail(PAINN_E_HIP, std::string("graph fill: ") + hipGetErrorString(e));
@@ -715,6 +784,8 @@ static painn_status run_forward(painn_ctx* ctx, const painn_model* model, const 
     return fail(ctx, PAINN_E_ARG, "unknown precision");
   if (g->cutoff != model->hp.cutoff)
     return fail(ctx, PAINN_E_ARG, "graph cutoff differs from the model's cutoff");
+  if (g->max_neighbors != model->hp.max_neighbors)
+    return fail(ctx, PAINN_E_ARG, "graph neighbour cap differs from the model's");
   if (g->N > 0 && (g->species_min < 0 || g->species_max >= model->hp.n_species))
     return fail(ctx, PAINN_E_SPECIES, "species index outside [0, n_species)");
   (void)hipSetDevice(ctx->device);

@@ -30,7 +30,9 @@ class Model:
     def __init__(self, rt: "Runtime", handle: int):
         self.rt, self.handle = rt, handle
         self.info = B.painn_model_info(handle)
-        self.has_blend = B.painn_model_has_blend(handle)
+        opts = B.painn_model_options(handle)
+        self.has_blend = opts["has_blend"]
+        self.max_neighbors = opts["max_neighbors"]
 
     def free(self):
         if self.handle:
@@ -100,14 +102,17 @@ class Runtime:
             return Model(self, B.painn_model_load_buffer(self.ctx, bytes(src)))
         return Model(self, B.painn_model_load(self.ctx, str(src)))
 
-    def build_graph(self, inp: dict, cutoff: float, graph: Graph | None = None) -> Graph:
+    def build_graph(self, inp: dict, cutoff: float, graph: Graph | None = None,
+                    max_neighbors: int = 0) -> Graph:
+        """Radius graph of an uploaded batch; max_neighbors > 0 keeps that
+        many nearest neighbours per receiver (a capped model needs its cap)."""
         ptr = lambda t: t.data_ptr() if t is not None and t.numel() else None
         use_pbc = inp.get("any_pbc", True)
-        h = B.painn_build_graph(self.ctx, inp["n_struct"], inp["n_atoms"], ptr(inp["struct_ptr"]),
-                                ptr(inp["pos"]), ptr(inp["species"]),
-                                ptr(inp["cell"]) if use_pbc else None,
-                                ptr(inp["pbc"]) if use_pbc else None, cutoff,
-                                graph.handle if graph else None)
+        h = B.painn_build_graph_capped(self.ctx, inp["n_struct"], inp["n_atoms"], ptr(inp["struct_ptr"]),
+                                       ptr(inp["pos"]), ptr(inp["species"]),
+                                       ptr(inp["cell"]) if use_pbc else None,
+                                       ptr(inp["pbc"]) if use_pbc else None, cutoff, max_neighbors,
+                                       graph.handle if graph else None)
         if graph is not None:
             graph.inputs = inp
             graph.refresh()

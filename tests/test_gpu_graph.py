@@ -202,3 +202,40 @@ def test_cell_list_dense_receivers(rt):
     rp, col, sh = gpu_csr(rt, b, 5.0)
     assert np.diff(rp).max() > 256
     assert_same_csr((rp, col, sh), batch_graph(b, 5.0))
+
+
+def gpu_csr_capped(rt, batch, cutoff, cap):
+    g = rt.build_graph(rt.upload_batch(batch), cutoff, max_neighbors=cap)
+    try:
+        return g.csr()
+    finally:
+        g.free()
+
+
+@pytest.mark.parametrize("cap", [8, 20])
+def test_neighbor_cap_molecules(rt, cap):
+    """Lead-model neighbour cap (Table 5: 20): each receiver keeps its nearest
+    edges by (d2, sender, shift), in (sender, shift) order, bit for bit."""
+    say(f"graph parity: cap {cap}, molecules")
+    b = synth.make_batch("molecules_4096", 0, 256)
+    assert_same_csr(gpu_csr_capped(rt, b, 5.0, cap), batch_graph(b, 5.0, cap))
+
+
+def test_neighbor_cap_periodic_and_cell_lists(rt):
+    say("graph parity: cap 20, periodic cells; cap 10, cell-list structures")
+    b = synth.make_batch("bulk_1024", 0, 12)
+    assert_same_csr(gpu_csr_capped(rt, b, 6.0, 20), batch_graph(b, 6.0, 20))
+    b = synth.concat(_large_structures())
+    assert_same_csr(gpu_csr_capped(rt, b, 5.0, 10), batch_graph(b, 5.0, 10))
+
+
+def test_neighbor_cap_long_rows(rt):
+    """Rows longer than the selection's LDS buffer (a dense cluster)."""
+    say("graph parity: cap 20, rows over 256 edges")
+    rng = np.random.default_rng(9)
+    sparse = rng.uniform(0, 40, (800, 3))
+    v = rng.normal(size=(300, 3))
+    dense = 20.0 + v / np.linalg.norm(v, axis=1, keepdims=True) * rng.uniform(0, 1, (300, 1)) ** (1 / 3) * 2.4
+    pos = np.concatenate([sparse, dense])
+    b = synth.concat([(pos, np.zeros(len(pos), np.int32), np.zeros((3, 3)), np.zeros(3, np.uint8), 0)])
+    assert_same_csr(gpu_csr_capped(rt, b, 5.0, 20), batch_graph(b, 5.0, 20))
