@@ -110,7 +110,7 @@ def main():
     ap.add_argument("--steps", type=int, default=20)
     ap.add_argument("--warmup", type=int, default=3)
     ap.add_argument("--workload", default="molecules_4096",
-                    choices=["molecules_4096", "bulk_1024", "screening", "tiny_molecules"])
+                    choices=["molecules_4096", "bulk_1024", "screening", "lead_model", "tiny_molecules"])
     ap.add_argument("--precision", default=None, choices=["fp64", "fp32", "bf16"])
     ap.add_argument("--blend", action="store_true",
                     help="blend every head with the model's branch-weighting MLP (screening model)")
@@ -146,8 +146,9 @@ def main():
     prec = args.precision or spec["precision"]
     hp, W = synth.workload_weights(name)
     log(f"generating {name}")
-    if name == "screening":
-        start, cnt = synth.screening_batches(3000)[0]
+    if spec.get("batch_atoms"):
+        # a stream workload: its first batch (closed before 65,536 atoms)
+        start, cnt = synth.screening_batches(3000, name=name)[0]
         batch = synth.make_batch(name, start, cnt)
     else:
         batch = synth.make_batch(name)
@@ -155,7 +156,7 @@ def main():
     model = rt.load_model(synth.weight_file_bytes(hp, W))
     inp = rt.upload_batch(batch)
     ds = inp["dataset_id"] if hp.n_heads > 1 else None
-    graph = rt.build_graph(inp, hp.cutoff)
+    graph = rt.build_graph(inp, hp.cutoff, max_neighbors=hp.max_neighbors)
     out = torch.empty(batch.n_struct, dtype=torch.float64, device=rt.device)
 
     if args.blend and hp.blend_dims is None:
@@ -163,7 +164,7 @@ def main():
         sys.exit(2)
 
     def step():
-        rt.build_graph(inp, hp.cutoff, graph=graph)
+        rt.build_graph(inp, hp.cutoff, graph=graph, max_neighbors=hp.max_neighbors)
         if args.blend:
             rt.forward_blend(model, graph, prec, skip=args.skip, out=out)
         else:
@@ -242,7 +243,8 @@ def main():
         "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
         "dtype": DTYPE[prec], "data": "synthetic",
         "config": {"workload": name, "n_struct": B, "n_atoms": N, "n_edges": E, "F": hp.F,
-                   "layers": hp.L, "rbf": hp.K, "cutoff": hp.cutoff, "heads": hp.n_heads,
+                   "layers": hp.L, "rbf": hp.K, "rbf_type": ["gaussian", "bessel"][hp.rbf_type],
+                   "cutoff": hp.cutoff, "max_neighbors": hp.max_neighbors, "heads": hp.n_heads,
                    "precision": prec,
                    "head_mode": (f"blended, skip < {args.skip:g}" if args.blend else
                                  ("dataset id" if hp.n_heads > 1 else "single"))},

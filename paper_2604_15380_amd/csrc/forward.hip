@@ -42,21 +42,21 @@ __device__ __forceinline__ void load_rows(typename P::T* dst, int ld, const type
 
 // ------------------------------------------------------------------ phi ----
 // h = W2 silu(W1 s + b1) + b2 for a tile of 16 RT atoms.
-template <class P, int F, int RT>
+template <class P, int F, int RT, int NW = 4>
 __device__ __forceinline__ void phi_tile(const typename P::T* X, int ldx, typename P::T* H,
                                          size_t row0, int N, const DenseDev& d1,
                                          const DenseDev& d2, typename P::T* __restrict__ h) {
   using A = typename P::A;
   constexpr int LD = F + P::PAD;
   const int lane = threadIdx.x & 63;
-  dense_tiles<P, RT, 4, F / P::KC>(X, ldx, d1, [&](int ct, typename P::C* acc) {
+  dense_tiles<P, RT, NW, F / P::KC>(X, ldx, d1, [&](int ct, typename P::C* acc) {
     const int col = ct * 16 + (lane & 15);
     const A bias = ((const A*)d1.b)[col];
     for (int r = 0; r < RT; ++r)
       for (int i = 0; i < 4; ++i) H[(r * 16 + P::row(lane, i)) * LD + col] = P::st(silu<A>(acc[r][i] + bias));
   });
   __syncthreads();
-  dense_tiles<P, RT, 4, F / P::KC>(H, LD, d2, [&](int ct, typename P::C* acc) {
+  dense_tiles<P, RT, NW, F / P::KC>(H, LD, d2, [&](int ct, typename P::C* acc) {
     const int col = ct * 16 + (lane & 15);
     const A bias = ((const A*)d2.b)[col];
     for (int r = 0; r < RT; ++r)
@@ -323,15 +323,23 @@ constexpr int update_waves() {
   return F == 128 ? 3 : F == 64 ? (P::PREC == PAINN_FP64 ? 2 : 3) : (P::PREC == PAINN_FP64 ? 1 : 2);
 }
 
+// Waves of an update workgroup: 4, or F / 64 above F = 256 (each wave keeps
+// the same 4 feature tiles in registers as at F = 256).
+template <int F>
+constexpr int update_nw() {
+  return F > 256 ? F / 64 : 4;
+}
+
 template <class P, int F, int RT, bool FUSE_PHI>
-__global__ void __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(update_waves<P, F>())))
+__global__ void __launch_bounds__(64 * update_nw<F>()) __attribute__((amdgpu_waves_per_eu(update_waves<P, F>())))
 k_update(UpdArgs a) {
   using T = typename P::T;
   using A = typename P::A;
   using C = typename P::C;
   using Fr = typename P::Fr;
   constexpr int NFT = F / 16;        // feature tiles
-  constexpr int FTW = NFT / 4;       // per wave
+  constexpr int NW = update_nw<F>();
+  constexpr int FTW = NFT / NW;      // per wave
   constexpr int TM = 16 * RT;        // atoms per workgroup
   constexpr int LD1 = F + P::PAD, LD2 = 2 * F + P::PAD;
   __shared__ __attribute__((aligned(16))) T VS[TM * LD1];   // v[c] slice, later the MLP hidden
@@ -361,7 +369,7 @@ k_update(UpdArgs a) {
     const T* xp = VS + (lane & 15) * LD1 + (lane >> 4) * P::KPL;
 #pragma unroll
     for (int q = 0; q < FTW; ++q) {
-      const int ft = wave + 4 * q;
+      const int ft = wave + NW * q;
       C au[RT], av[RT];
       for (int r = 0; r < RT; ++r)
         for (int i = 0; i < 4; ++i) au[r][i] = av[r][i] = 0;
@@ -392,14 +400,14 @@ k_update(UpdArgs a) {
   }
 #pragma unroll
   for (int q = 0; q < FTW; ++q) {
-    const int col = (wave + 4 * q) * 16 + (lane & 15);
+    const int col = (wave + NW * q) * 16 + (lane & 15);
     for (int r = 0; r < RT; ++r)
       for (int i = 0; i < 4; ++i)
         SN[(r * 16 + P::row(lane, i)) * LD2 + F + col] = P::st(sqrt(nsq[q][r][i]));
   }
   __syncthreads();
   T* H = VS;
-  dense_tiles<P, RT, 4, 2 * F / P::KC>(SN, LD2, a.upd1, [&](int ct, C* acc) {
+  dense_tiles<P, RT, NW, 2 * F / P::KC>(SN, LD2, a.upd1, [&](int ct, C* acc) {
     const int col = ct * 16 + (lane & 15);
     const A bias = ((const A*)a.upd1.b)[col];
     for (int r = 0; r < RT; ++r)
@@ -414,7 +422,7 @@ k_update(UpdArgs a) {
     const T* xp = H + (lane & 15) * LD1 + (lane >> 4) * P::KPL;
 #pragma unroll
     for (int q = 0; q < FTW; ++q) {
-      const int ft = wave + 4 * q;
+      const int ft = wave + NW * q;
       C avv[RT], asv[RT], ass[RT];
       for (int r = 0; r < RT; ++r)
         for (int i = 0; i < 4; ++i) avv[r][i] = asv[r][i] = ass[r][i] = 0;
@@ -459,7 +467,7 @@ k_update(UpdArgs a) {
   }
   if (FUSE_PHI) {
     __syncthreads();
-    phi_tile<P, F, RT>(SN, LD2, VS, row0, N, a.phi1, a.phi2, (T*)a.h);
+    phi_tile<P, F, RT, NW>(SN, LD2, VS, row0, N, a.phi1, a.phi2, (T*)a.h);
   }
 }
 
@@ -754,15 +762,17 @@ __global__ void __launch_bounds__(256) k_energy(int B, const int32_t* __restrict
   E[b] = acc;
 }
 
+// s [N][Fl] and v [N][3][Fl] in FP64 from the working arrays of width F >= Fl
+// (the model's own channels; the rest is zero padding)
 template <class P>
-__global__ void __launch_bounds__(256) k_export(int N, int F, const typename P::T* __restrict__ s,
+__global__ void __launch_bounds__(256) k_export(int N, int F, int Fl, const typename P::T* __restrict__ s,
                                                const typename P::T* __restrict__ v,
                                                double* __restrict__ so, double* __restrict__ vo) {
-  const size_t tot = (size_t)N * F;
+  const size_t tot = (size_t)N * Fl;
   for (size_t x = blockIdx.x * (size_t)blockDim.x + threadIdx.x; x < tot; x += (size_t)gridDim.x * blockDim.x) {
-    so[x] = (double)P::ld(s[x]);
-    const size_t i = x / F, f = x % F;
-    for (int c = 0; c < 3; ++c) vo[(3 * i + c) * F + f] = (double)P::ld(v[(3 * i + c) * F + f]);
+    const size_t i = x / Fl, f = x % Fl;
+    so[x] = (double)P::ld(s[i * F + f]);
+    for (int c = 0; c < 3; ++c) vo[(3 * i + c) * Fl + f] = (double)P::ld(v[(3 * i + c) * F + f]);
   }
 }
 
@@ -1006,7 +1016,9 @@ k_message_lane(MsgArgs a) {
 template <class P, int F, int KBM>
 void launch_message_kbm(hipStream_t st, const MsgArgs& a) {
   if constexpr (sizeof(typename P::T) == 8) {
-    constexpr int NW = F / 32;      // two feature tiles per wave
+    // two feature tiles per wave; four above F = 256 (a 768-thread group
+    // would leave each wave too few registers)
+    constexpr int NW = F > 256 ? F / 64 : F / 32;
     const int blocks = ((a.N + MSG_RB - 1) / MSG_RB + 7) / 8 * 8;   // a multiple of the 8 XCDs
     k_message<P, F, NW, KBM><<<blocks, NW * 64, 0, st>>>(a);
   } else {
@@ -1307,9 +1319,9 @@ hipError_t forward_impl(hipStream_t st, ForwardArgs& fa) {
   const PrecModel* pm = fa.pm;
   const Hyper& hp = fa.m->hp;
   const int N = g->N;
-  constexpr int RT = (sizeof(T) == 8 && F == 256) ? 1 : 2;
+  constexpr int RT = ((sizeof(T) == 8 && F >= 256) || F > 256) ? 1 : 2;
   // atoms per update tile / 16: U, |V|^2 and <U, V> of the tile live in registers
-  constexpr int URT = (F == 256 || (sizeof(T) == 8 && F == 128)) ? 1 : 2;
+  constexpr int URT = (F >= 256 || (sizeof(T) == 8 && F == 128)) ? 1 : 2;
   T* s = (T*)fa.s;
   T* v[2] = {(T*)fa.v[0], (T*)fa.v[1]};
   T* h = (T*)fa.h;
@@ -1366,16 +1378,17 @@ hipError_t forward_impl(hipStream_t st, ForwardArgs& fa) {
     if (fuse) {
       ua.phi1 = pm->layers[l + 1].phi1;
       ua.phi2 = pm->layers[l + 1].phi2;
-      k_update<P, F, URT, true><<<(N + 16 * URT - 1) / (16 * URT), 256, 0, st>>>(ua);
+      k_update<P, F, URT, true><<<(N + 16 * URT - 1) / (16 * URT), 64 * update_nw<F>(), 0, st>>>(ua);
     } else {
-      k_update<P, F, URT, false><<<(N + 16 * URT - 1) / (16 * URT), 256, 0, st>>>(ua);
+      k_update<P, F, URT, false><<<(N + 16 * URT - 1) / (16 * URT), 64 * update_nw<F>(), 0, st>>>(ua);
     }
     prof_mark(fa.prof, st, KC_UPDATE, false);
   }
   if (fa.s_out) {
     prof_mark(fa.prof, st, KC_EXPORT, true);
     if (N > 0)
-      k_export<P><<<grid_for((size_t)N * F, 256), 256, 0, st>>>(N, F, s, v[cur], fa.s_out, fa.v_out);
+      k_export<P><<<grid_for((size_t)N * F, 256), 256, 0, st>>>(N, F, hp.F_logical, s, v[cur], fa.s_out,
+                                                                 fa.v_out);
     prof_mark(fa.prof, st, KC_EXPORT, false);
     return hipGetLastError();
   }
@@ -1396,6 +1409,7 @@ hipError_t forward_prec(hipStream_t st, ForwardArgs& fa) {
     case 64: return forward_impl<P, 64>(st, fa);
     case 128: return forward_impl<P, 128>(st, fa);
     case 256: return forward_impl<P, 256>(st, fa);
+    case 384: return forward_impl<P, 384>(st, fa);
     default: return hipErrorInvalidValue;
   }
 }

@@ -102,7 +102,9 @@ struct PrecModel {      // the model cast and packed for one precision
 };
 
 struct Hyper {
-  int F, K, L, n_species, n_heads, rbf_type;
+  int F;            // feature width the kernels run at (64, 128, 256, 384)
+  int F_logical;    // the model's own width (<= F; the rest is zero padding)
+  int K, L, n_species, n_heads, rbf_type;
   double cutoff;
   std::vector<int> shared_dims, branch_dims;
   std::vector<int> blend_dims;   // hidden widths of the branch-weighting MLP

@@ -248,6 +248,61 @@ painn_status build_prec(painn_model* m, int prec, PrecModel** out) {
   return PAINN_OK;
 }
 
+// The kernels run at feature widths 64, 128, 256 and 384.  A model of any
+// other width F <= 384 is padded with zeros to the next of them: padded
+// channels of s, v and h stay exactly 0 (zero embedding columns, zero rows
+// and biases of every layer producing them) and never reach a real channel
+// (zero columns of every layer reading them), so the energies are those of
+// the F-wide model.  Every array of the master copy is re-laid out at the
+// padded width; dimensions made of P blocks of F channels ([h_s | h_v | h_r],
+// [s ; |Vv|], [a_vv | a_sv | a_ss]) are padded block by block.
+static int padded_width(int F) { return F <= 64 ? 64 : F <= 128 ? 128 : F <= 256 ? 256 : 384; }
+
+static void pad_feature_width(painn_model* m) {
+  Hyper& hp = m->hp;
+  const int F = hp.F, Fp = padded_width(F);
+  if (Fp == F) return;
+  // (rows, cols) of each array in file order; a dimension given as -P means
+  // P blocks of F channels
+  struct Dim { int rows, cols; };
+  std::vector<Dim> dims;
+  dims.push_back({hp.n_species, -1});
+  for (int l = 0; l < hp.L; ++l) {
+    const Dim per[A_PER_LAYER] = {{-1, -1}, {-1, 1}, {-3, -1}, {-3, 1}, {-3, hp.K}, {-3, 1},
+                                  {-1, -1}, {-1, -1}, {-1, -2}, {-1, 1}, {-3, -1}, {-3, 1}};
+    for (const Dim& d : per) dims.push_back(d);
+  }
+  int din = -1;
+  for (int d : hp.shared_dims) { dims.push_back({d, din}); dims.push_back({d, 1}); din = d; }
+  for (int h = 0; h < hp.n_heads; ++h) {
+    int di = din;
+    for (int d : hp.branch_dims) { dims.push_back({d, di}); dims.push_back({d, 1}); di = d; }
+  }
+  const size_t n_main = dims.size();
+  auto ext = [&](int d, int w) { return d < 0 ? (size_t)(-d) * w : (size_t)d; };
+  auto map = [&](int d, size_t x) { return d < 0 ? (x / F) * Fp + x % F : x; };
+  std::vector<double> out;
+  std::vector<size_t> offs;
+  for (size_t a = 0; a < m->offsets.size(); ++a) {
+    const double* src = m->master.data() + m->offsets[a];
+    offs.push_back(out.size());
+    if (a >= n_main) {                       // branch-weighting MLP: unchanged
+      const size_t n = (a + 1 < m->offsets.size() ? m->offsets[a + 1] : m->master.size()) - m->offsets[a];
+      out.insert(out.end(), src, src + n);
+      continue;
+    }
+    const Dim d = dims[a];
+    const size_t R = ext(d.rows, F), C = ext(d.cols, F), Rp = ext(d.rows, Fp), Cp = ext(d.cols, Fp);
+    const size_t o = out.size();
+    out.resize(o + Rp * Cp, 0.0);
+    for (size_t r = 0; r < R; ++r)
+      for (size_t c = 0; c < C; ++c) out[o + map(d.rows, r) * Cp + map(d.cols, c)] = src[r * C + c];
+  }
+  m->master.swap(out);
+  m->offsets.swap(offs);
+  hp.F = Fp;
+}
+
 painn_status parse_model(painn_ctx* ctx, const unsigned char* buf, size_t n, painn_model** out) {
   if (n < 48 || memcmp(buf, "PAINNW01", 8) != 0)
     return fail(ctx, PAINN_E_FORMAT, "weight file: bad magic or truncated header");
@@ -265,8 +320,7 @@ painn_status parse_model(painn_ctx* ctx, const unsigned char* buf, size_t n, pai
   for (int i = 0; i < ns; ++i) { int32_t d; memcpy(&d, buf + off, 4); off += 4; hp.shared_dims.push_back(d); }
   for (int i = 0; i < nb; ++i) { int32_t d; memcpy(&d, buf + off, 4); off += 4; hp.branch_dims.push_back(d); }
   off += (8 - off % 8) % 8;
-  if (hp.F != 64 && hp.F != 128 && hp.F != 256)
-    return fail(ctx, PAINN_E_UNSUPPORTED, "F must be 64, 128 or 256");
+  if (hp.F < 1 || hp.F > 384) return fail(ctx, PAINN_E_UNSUPPORTED, "F must be in [1, 384]");
   if (hp.K < 2 || hp.K > 64) return fail(ctx, PAINN_E_UNSUPPORTED, "K must be in [2, 64]");
   if (hp.L < 1 || hp.L > 16) return fail(ctx, PAINN_E_UNSUPPORTED, "L must be in [1, 16]");
   if (hp.n_species < 1 || hp.n_species > 1024) return fail(ctx, PAINN_E_FORMAT, "bad n_species");
@@ -356,6 +410,8 @@ painn_status parse_model(painn_ctx* ctx, const unsigned char* buf, size_t n, pai
   for (size_t s : sizes) { m->offsets.push_back(o); o += s; }
   for (double x : m->master)
     if (!isfinite(x)) { delete m; return fail(ctx, PAINN_E_FORMAT, "weight file: non-finite weight"); }
+  m->hp.F_logical = hp.F;
+  pad_feature_width(m);
   *out = m;
   return PAINN_OK;
 }
@@ -537,7 +593,7 @@ painn_status painn_model_options(const painn_model* m, int32_t* has_blend, int32
 painn_status painn_model_info(const painn_model* m, int32_t* F, int32_t* K, int32_t* L,
                               int32_t* n_species, int32_t* n_heads, double* cutoff) {
   if (!m) return PAINN_E_ARG;
-  if (F) *F = m->hp.F;
+  if (F) *F = m->hp.F_logical;
   if (K) *K = m->hp.K;
   if (L) *L = m->hp.L;
   if (n_species) *n_species = m->hp.n_species;

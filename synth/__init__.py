@@ -89,6 +89,15 @@ WORKLOADS = {
         n_species=85, d_min=None, cutoff=5.0, F=256, L=4, K=32,
         shared_dims=[50, 50], branch_dims=[776, 776, 1], n_heads=16, blend_dims=[128, 64],
         batch_atoms=65536, data_seed=1005, weight_seed=2005, precision="bf16"),
+    # The lead model's shape (Table 5): F = 337, 2 layers, 4 Bessel functions,
+    # r_c = 5 A with at most 20 neighbours, 2 shared head layers of 50 and 16
+    # branches of 776, 776, blended by the branch-weighting MLP; structures of
+    # 2-500 atoms as in the paper's inference benchmark (40,000 structures).
+    "lead_model": dict(
+        n_struct=40_000, kind="mixed", n_lo=2, n_hi=500, size_dist="loguniform",
+        n_species=85, d_min=None, cutoff=5.0, F=337, L=2, K=4, rbf_type=1, max_neighbors=20,
+        shared_dims=[50, 50], branch_dims=[776, 776, 1], n_heads=16, blend_dims=[128, 64],
+        batch_atoms=65536, data_seed=1006, weight_seed=2006, precision="fp32"),
 }
 # The precision sweep runs the 4096-molecule inputs and weights at all three
 # precisions; it is the same workload entry.

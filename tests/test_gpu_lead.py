@@ -58,3 +58,33 @@ def test_cap_must_match_the_model(rt):
         rt.forward(m, g, "fp32")
     g.free()
     m.free()
+
+
+@pytest.mark.parametrize("F", [100, 337])
+@pytest.mark.parametrize("precision", ["fp64", "fp32", "bf16"])
+def test_padded_feature_widths(rt, F, precision):
+    """Feature widths the kernels do not run at natively (the lead model's
+    F = 337 runs at 384, F = 100 at 128, with zero-padded weights) give the
+    energies of the F-wide model."""
+    say(f"F = {F}, {precision}")
+    hp = synth.HyperParams(F=F, K=4, L=2, n_species=10, n_heads=1, cutoff=5.0,
+                           shared_dims=[], branch_dims=[24, 1], rbf_type=RBF_BESSEL)
+    W = synth.make_weights(hp, 2200 + F)
+    m = rt.load_model(synth.weight_file_bytes(hp, W))
+    assert m.info["F"] == F
+    b = synth.make_batch("molecules_4096", 0, 24)
+    g = rt.build_graph(rt.upload_batch(b), hp.cutoff)
+    E = rt.forward(m, g, precision).cpu().numpy()
+    ref = [structure_forward(*b.structure(k)[:4], 0, hp, W, keep_layers=True) for k in range(b.n_struct)]
+    check_energies(E, np.array([o["E"] for o in ref]), np.array([np.abs(o["e"]).sum() for o in ref]),
+                   TOL[precision], f"F={F} {precision}")
+    if precision == "fp64":
+        # the exported features have the model's own width and match layer by layer
+        s, v = (t.cpu().numpy() for t in rt.features(m, g, 0, "fp64"))
+        assert s.shape == (b.n_atoms, F) and v.shape == (b.n_atoms, 3, F)
+        s_ref = np.concatenate([o["layers"][0][0] for o in ref])
+        v_ref = np.concatenate([o["layers"][0][1] for o in ref])
+        assert np.allclose(s, s_ref, rtol=0, atol=1e-11 * max(1.0, np.abs(s_ref).max()))
+        assert np.allclose(v, v_ref, rtol=0, atol=1e-11 * max(1.0, np.abs(v_ref).max()))
+    g.free()
+    m.free()
