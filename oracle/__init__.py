@@ -12,6 +12,8 @@ Contents:
   painn.structure_forward  FP64 PaiNN energy by the edge-list formulation
   painn.structure_forward_dense  the same by dense masked tensors (tiny inputs)
   painn.batch_energies     per-structure energies of a batch
+  forces.structure_forces  FP64 forces -dE/dx by a hand-written reverse pass
+  forces.batch_forces      energies and forces of a batch
 
 Every function is pinned by tests in `tests/test_oracle_*.py` against closed
 forms, invariances, special cases and independent library routines.  The
