@@ -200,6 +200,28 @@ painn_status painn_forward_blend(painn_ctx* ctx, const painn_model* model, const
                                  painn_precision precision, double skip_threshold, double* energies,
                                  double* weights);
 
+/* Energies and forces (the paper's screening throughput counts both, and its
+ * largest single inference gain computes the force gradient in the same pass
+ * as the energy: section "Optimizing the Inference Pipeline", Fig. 4).
+ * Forces are F_i = -dE/dx_i with E the total energy of atom i's structure,
+ * by a hand-written reverse pass through the heads, every layer's update,
+ * message and phi, the radial filter and the edge geometry.  The graph is
+ * held fixed: the cosine cutoff makes every message vanish with zero slope
+ * at r_c, and the neighbour cap is piecewise constant in the positions.
+ *   dataset_id [B] as in painn_forward (NULL = head 0).
+ *   energies   [B] float64 output (the same values as painn_forward).
+ *   forces     [N, 3] float64 output (eV/Angstrom for energies in eV).
+ * Both written on the stream; the reverse pass keeps every layer's
+ * activations (about (11 L + 4) N F values of the precision's storage type
+ * plus per-edge buffers) in a context workspace grown on demand.  The first
+ * call on a graph also groups its edges by sender (kept until the graph is
+ * rebuilt).  Errors: as painn_forward; PAINN_E_UNSUPPORTED for BF16, for
+ * F = 384 in FP64, and when the heads' widest layer does not fit the
+ * reverse heads kernel. */
+painn_status painn_forces(painn_ctx* ctx, const painn_model* model, const painn_graph* graph,
+                          const int32_t* dataset_id, painn_precision precision, double* energies,
+                          double* forces);
+
 /* Test hook: run layers 0..layer (layer = -1: embedding only) and write the
  * scalar features s [N,F] and vector features v [N,3,F] (float64) reached
  * there.  Same arguments and errors as painn_forward. */

@@ -1,0 +1,1010 @@
+// Reverse pass of the batched PaiNN forward on gfx950 (FP64 / FP32):
+// forces F_i = -dE/dx_i.  The paper's screening throughput counts energies
+// and forces, and its largest single inference gain is computing the force
+// gradient in the same pass as the energy (section "Optimizing the Inference
+// Pipeline", Fig. 4); this is that gradient written out by hand.
+//
+// The forward runs with a save area (each layer's s, v, h before the message
+// and s, v after it).  Then, with g_X = dE/dX (accumulation type):
+//   heads     g_s = readout'(s_L), g_v = 0
+//   layer l = L-1 .. 0:
+//     update   (g_s, g_v) -> (g_s', g_v') at s, v after the message
+//     message  per SENDER j over its incoming edges (the edge list grouped
+//              by sender): g_h_j, g_v_j = g_v'_j + message terms, and per
+//              edge dE/dd and dE/drhat (accumulated over layers)
+//     phi      g_s = g_s' + phi'(s_l)^T g_h         (skipped at l = 0)
+//   edges     dE/dr = dE/dd rhat + (dE/drhat - (dE/drhat . rhat) rhat) / d
+//   atoms     F_a = sum_{e: receiver a} dE/dr_e - sum_{e: sender a} dE/dr_e
+// (r = x_sender - x_receiver + t).  Every sum runs in a fixed order: the
+// forces are deterministic.  The graph is held fixed (the cutoff makes every
+// message vanish with zero slope at r_c, and the neighbour cap is piecewise
+// constant in the positions).  Where |V v| = 0 the norm's gradient is taken
+// as zero.
+#include "mfma.h"
+
+namespace {
+
+template <class A>
+__device__ __forceinline__ A dsilu(A x) {
+  const A sg = A(1) / (A(1) + (sizeof(A) == 8 ? (A)exp((double)-x) : (A)expf((float)-x)));
+  return sg * (A(1) + x * (A(1) - sg));
+}
+
+template <class A>
+__global__ void __launch_bounds__(256) k_fill(size_t n, A* __restrict__ p) {
+  for (size_t x = blockIdx.x * (size_t)blockDim.x + threadIdx.x; x < n; x += (size_t)gridDim.x * blockDim.x)
+    p[x] = A(0);
+}
+
+inline int grid_of(size_t n, int per) {
+  size_t g = (n + per - 1) / per;
+  if (g > 65536) g = 65536;
+  return (int)(g ? g : 1);
+}
+
+// ------------------------------------------------ edges grouped by sender ----
+__global__ void __launch_bounds__(256) k_t_count(long long E, const int32_t* __restrict__ col,
+                                                int32_t* __restrict__ cnt) {
+  for (long long e = blockIdx.x * (long long)blockDim.x + threadIdx.x; e < E; e += (long long)gridDim.x * blockDim.x)
+    atomicAdd(&cnt[col[e]], 1);
+}
+
+// One workgroup: exclusive scan of the N counts into t_ptr[0..N], counts
+// reset to 0 (they become the fill cursors).
+__global__ void __launch_bounds__(1024) k_t_scan(int N, int32_t* __restrict__ cnt, int32_t* __restrict__ ptr) {
+  __shared__ int part[1024];
+  const int t = threadIdx.x;
+  const int per = (N + 1023) / 1024;
+  const int lo = min(N, t * per), hi = min(N, lo + per);
+  int sum = 0;
+  for (int j = lo; j < hi; ++j) sum += cnt[j];
+  part[t] = sum;
+  __syncthreads();
+  for (int o = 1; o < 1024; o <<= 1) {
+    const int x = t >= o ? part[t - o] : 0;
+    __syncthreads();
+    part[t] += x;
+    __syncthreads();
+  }
+  int run = part[t] - sum;
+  for (int j = lo; j < hi; ++j) {
+    ptr[j] = run;
+    run += cnt[j];
+    cnt[j] = 0;
+  }
+  if (t == 1023) ptr[N] = part[1023];
+}
+
+__global__ void __launch_bounds__(256) k_t_fill(long long E, const int32_t* __restrict__ col,
+                                               const int32_t* __restrict__ ptr, int32_t* __restrict__ cur,
+                                               int32_t* __restrict__ t_edge) {
+  for (long long e = blockIdx.x * (long long)blockDim.x + threadIdx.x; e < E; e += (long long)gridDim.x * blockDim.x) {
+    const int j = col[e];
+    t_edge[ptr[j] + atomicAdd(&cur[j], 1)] = (int32_t)e;
+  }
+}
+
+// The fill order depends on timing: sort each sender's edge ids ascending
+// (insertion sort; in-degrees are small).
+__global__ void __launch_bounds__(256) k_t_sort(int N, const int32_t* __restrict__ ptr, int32_t* __restrict__ t_edge) {
+  const int j = blockIdx.x * blockDim.x + threadIdx.x;
+  if (j >= N) return;
+  const int a = ptr[j], b = ptr[j + 1];
+  for (int x = a + 1; x < b; ++x) {
+    const int key = t_edge[x];
+    int y = x - 1;
+    while (y >= a && t_edge[y] > key) {
+      t_edge[y + 1] = t_edge[y];
+      --y;
+    }
+    t_edge[y + 1] = key;
+  }
+}
+
+// -------------------------------------------------- basis derivative rows ----
+// d/dd of the forward's basis row (f_c g_0, .., f_c g_{K-1}, f_c):
+//   f_c' g_k + f_c g_k',  f_c' = -(pi / (2 r_c)) sin(pi d / r_c);
+//   Gaussian g_k' = -2 gamma (d - k Delta) g_k;
+//   Bessel   g_n' = (n pi / r_c) cos(n pi d / r_c) / d - sin(n pi d / r_c) / d^2.
+template <class P>
+__global__ void __launch_bounds__(256) k_edge_deriv(long long E, int K, int kcols, double rc, int rbf,
+                                                   double gamma, double delta,
+                                                   const int32_t* __restrict__ recv,
+                                                   const int32_t* __restrict__ col,
+                                                   const int32_t* __restrict__ shift,
+                                                   const int32_t* __restrict__ atom_struct,
+                                                   const double* __restrict__ pos,
+                                                   const double* __restrict__ cell,
+                                                   typename P::T* __restrict__ dbasis) {
+  using A = typename P::A;
+  const long long e = blockIdx.x * (long long)blockDim.x + threadIdx.x;
+  if (e >= E + 16) return;
+  typename P::T* g = dbasis + (size_t)e * kcols;
+  if (e >= E) {
+    for (int k = 0; k < kcols; ++k) g[k] = P::st(0);
+    return;
+  }
+  const int i = recv[e], j = col[e], sh = shift[e];
+  const double* Cl = cell + 9 * atom_struct[i];
+  const double n0 = (double)(int8_t)(sh & 0xff), n1 = (double)(int8_t)((sh >> 8) & 0xff),
+               n2 = (double)(int8_t)((sh >> 16) & 0xff);
+  const double rx = (pos[3 * j] - pos[3 * i]) + ((n0 * Cl[0] + n1 * Cl[3]) + n2 * Cl[6]);
+  const double ry = (pos[3 * j + 1] - pos[3 * i + 1]) + ((n0 * Cl[1] + n1 * Cl[4]) + n2 * Cl[7]);
+  const double rz = (pos[3 * j + 2] - pos[3 * i + 2]) + ((n0 * Cl[2] + n1 * Cl[5]) + n2 * Cl[8]);
+  const double d = sqrt(rx * rx + ry * ry + rz * rz);
+  const double pi = 3.14159265358979323846;
+  const A dd = (A)d;
+  const A fc = (A)(d < rc ? 0.5 * (cos(d * (pi / rc)) + 1.0) : 0.0);
+  const A dfc = (A)(d < rc ? -0.5 * (pi / rc) * sin(d * (pi / rc)) : 0.0);
+  for (int k = 0; k < kcols; ++k) {
+    A val = 0;
+    if (k < K && rbf == 0) {
+      const A t = dd - (A)(k * delta);
+      const A gk = P::ex(-(A)gamma * t * t);
+      val = dfc * gk + fc * (-(A)(2.0 * gamma) * t * gk);
+    } else if (k < K) {
+      const A w = (A)((k + 1) * (pi / rc));
+      const A arg = w * dd;
+      const A sn = sizeof(A) == 8 ? (A)sin((double)arg) : (A)sinf((float)arg);
+      const A cs = sizeof(A) == 8 ? (A)cos((double)arg) : (A)cosf((float)arg);
+      val = dfc * (sn / dd) + fc * (w * cs / dd - sn / (dd * dd));
+    } else if (k == K) {
+      val = dfc;
+    }
+    g[k] = P::st(val);
+  }
+}
+
+// ------------------------------------------------------------ heads, back ----
+// One workgroup per tile of 16 atoms of one head (the forward's grouping):
+// the layers' pre-activations are recomputed (kept in the per-atom scratch),
+// then dE/ds = W_0^T (silu'(z_0) * W_1^T (... silu'(z_{n-2}) * w_out)).
+constexpr int HB_NW = 4;
+
+struct HeadBwdArgs {
+  int N, ns, nb, F;
+  int ldw;                       // LDS row stride of the two buffers
+  const void* s;                 // the final s [N][F]
+  const int32_t* order;          // null: consecutive atoms, head 0
+  const HeadTile* tiles;         // the forward's tiles (any length)
+  const HeadPlan* plan;
+  const void* const* table;      // [head][layer][2] = (packed w, bias)
+  const void* const* tableT;     // [head][layer][2] = (packed w^T, null)
+  DenseDev shared[16], sharedT[16];
+  int bdin[16], bdout[16];
+  int zoff[32];                  // pre-activation offsets in a scratch row
+  void* scratch;
+  int sw;
+  void* gs;                      // out: dE/ds [N][F]
+};
+
+template <class P>
+__device__ __forceinline__ typename P::A packed_w0(const DenseDev& L, int k) {
+  const int kb = k / P::KC, r = k % P::KC;
+  return P::ld(((const typename P::T*)L.w)[((size_t)kb * 64 + 16 * (r / P::KPL)) * P::KPL + r % P::KPL]);
+}
+
+template <class P, int F>
+__device__ void heads_bwd_tile(const HeadBwdArgs& a, int head, const int* idx, typename P::T* const* Y,
+                               int lane) {
+  using T = typename P::T;
+  using A = typename P::A;
+  using C = typename P::C;
+  constexpr int TM = 16;
+  const int nl = a.ns + a.nb;
+  auto layer = [&](int m, bool tr) {
+    if (m < a.ns) return tr ? a.sharedT[m] : a.shared[m];
+    const int mb = m - a.ns;
+    DenseDev L;
+    const void* const* tab = tr ? a.tableT : a.table;
+    L.w = (void*)tab[((size_t)head * a.nb + mb) * 2];
+    L.b = (void*)tab[((size_t)head * a.nb + mb) * 2 + 1];
+    const int din = mb == 0 ? (a.ns ? a.shared[a.ns - 1].dout : F) : a.bdout[mb - 1];
+    const int dout = a.bdout[mb];
+    L.din = tr ? dout : din;
+    L.dout = tr ? din : dout;
+    L.din_p = pad32(L.din);
+    L.dout_p = pad32(L.dout);
+    return L;
+  };
+  A* gs = (A*)a.gs;
+  const DenseDev Lout = layer(nl - 1, false);
+  if (nl == 1) {
+    for (int x = threadIdx.x; x < TM * F; x += blockDim.x) {
+      const int r = x / F, c = x % F;
+      if (idx[r] >= 0) gs[(size_t)idx[r] * F + c] = c < Lout.din ? packed_w0<P>(Lout, c) : A(0);
+    }
+    return;
+  }
+  A* scr = (A*)a.scratch;
+  const T* s = (const T*)a.s;
+  for (int x = threadIdx.x; x < TM * F; x += blockDim.x) {
+    const int r = x / F, c = x % F;
+    Y[0][r * a.ldw + c] = idx[r] >= 0 ? s[(size_t)idx[r] * F + c] : P::st(0);
+  }
+  __syncthreads();
+  int cur = 0;
+  // forward through every layer but the output one, keeping z
+  for (int m = 0; m + 1 < nl; ++m) {
+    const DenseDev L = layer(m, false);
+    T* dst = Y[cur ^ 1];
+    dense_tiles<P, 1, HB_NW>(Y[cur], a.ldw, L, [&](int ct, C* acc) {
+      const int col = ct * 16 + (lane & 15);
+      const A bias = ((const A*)L.b)[col];
+      for (int i = 0; i < 4; ++i) {
+        const int r = P::row(lane, i);
+        const A z = acc[0][i] + bias;
+        if (idx[r] >= 0) scr[(size_t)idx[r] * a.sw + a.zoff[m] + col] = z;
+        dst[r * a.ldw + col] = P::st(col < L.dout ? silu<A>(z) : A(0));
+      }
+    });
+    __syncthreads();
+    cur ^= 1;
+  }
+  // delta of the last hidden layer: w_out * silu'(z)
+  {
+    const int m = nl - 2;
+    const int w = pad32(Lout.din);
+    for (int x = threadIdx.x; x < TM * w; x += blockDim.x) {
+      const int r = x / w, c = x % w;
+      A dl = 0;
+      if (idx[r] >= 0 && c < Lout.din) dl = packed_w0<P>(Lout, c) * dsilu<A>(scr[(size_t)idx[r] * a.sw + a.zoff[m] + c]);
+      Y[cur][r * a.ldw + c] = P::st(dl);
+    }
+  }
+  __syncthreads();
+  for (int m = nl - 2; m >= 0; --m) {
+    const DenseDev LT = layer(m, true);
+    T* dst = Y[cur ^ 1];
+    dense_tiles<P, 1, HB_NW>(Y[cur], a.ldw, LT, [&](int ct, C* acc) {
+      const int col = ct * 16 + (lane & 15);
+      for (int i = 0; i < 4; ++i) {
+        const int r = P::row(lane, i);
+        const int g = idx[r];
+        if (m == 0) {
+          if (g >= 0 && col < F) gs[(size_t)g * F + col] = acc[0][i];
+        } else {
+          A dl = 0;
+          if (g >= 0 && col < LT.dout) dl = acc[0][i] * dsilu<A>(scr[(size_t)g * a.sw + a.zoff[m - 1] + col]);
+          dst[r * a.ldw + col] = P::st(dl);
+        }
+      }
+    });
+    __syncthreads();
+    cur ^= 1;
+  }
+}
+
+template <class P, int F>
+__global__ void __launch_bounds__(64 * HB_NW) k_heads_bwd(HeadBwdArgs a) {
+  using T = typename P::T;
+  constexpr int TM = 16;
+  extern __shared__ __attribute__((aligned(16))) unsigned char smem[];
+  T* Y[2] = {(T*)smem, (T*)smem + TM * a.ldw};
+  __shared__ int idx[TM];
+  const int lane = threadIdx.x & 63;
+  int head = 0, begin, end;
+  if (a.order) {
+    if ((int)blockIdx.x >= a.plan->n_tiles) return;
+    const HeadTile tl = a.tiles[blockIdx.x];
+    head = tl.head;
+    begin = tl.begin;
+    end = tl.end;
+  } else {
+    begin = blockIdx.x * TM;
+    end = min(a.N, begin + TM);
+  }
+  for (int sub = begin; sub < end; sub += TM) {
+    __syncthreads();
+    if (threadIdx.x < TM) {
+      const int k = sub + threadIdx.x;
+      idx[threadIdx.x] = k < end ? (a.order ? a.order[k] : k) : -1;
+    }
+    __syncthreads();
+    heads_bwd_tile<P, F>(a, head, idx, Y, lane);
+  }
+}
+// ----------------------------------------------------------- update, back ----
+// Tile of 16 atoms, 4 waves; LDS R1 [16][3F + PAD], R2 [16][F + PAD]; the
+// per-atom scratch row holds U[c], V[c] (6F), |V| (F), <U, V> (F), z (F),
+// a_vv (F), a_sv (F), g_n (F).
+constexpr int UB_NW = 4;
+
+struct UpdBwdArgs {
+  int N;
+  const void* s;     // after the message [N][F]
+  const void* v;     // after the message [N][3F]
+  const void* gs;    // dE/d(s, v) after the update
+  const void* gv;
+  void* gs_out;      // dE/d(s, v) after the message
+  void* gv_out;
+  void* scratch;
+  int sw;
+  DenseDev uv, upd1, upd2, uvT, upd1T, upd2T;
+};
+
+template <class P, int F>
+__global__ void __launch_bounds__(64 * UB_NW) k_update_bwd(UpdBwdArgs a) {
+  using T = typename P::T;
+  using A = typename P::A;
+  using C = typename P::C;
+  constexpr int TM = 16, LD1 = 3 * F + P::PAD, LD2 = F + P::PAD;
+  extern __shared__ __attribute__((aligned(16))) unsigned char smem[];
+  T* R1 = (T*)smem;
+  T* R2 = R1 + TM * LD1;
+  const int lane = threadIdx.x & 63;
+  const size_t row0 = (size_t)blockIdx.x * TM;
+  const int N = a.N;
+  const T* s = (const T*)a.s;
+  const T* v = (const T*)a.v;
+  const A* gs = (const A*)a.gs;
+  const A* gv = (const A*)a.gv;
+  A* scr = (A*)a.scratch;
+  const int sw = a.sw;
+  // scratch columns
+  constexpr int O_UV = 0, O_N = 6 * F, O_PD = 7 * F, O_Z = 8 * F, O_AVV = 9 * F, O_ASV = 10 * F, O_GN = 11 * F;
+  auto sc = [&](int r, int o) -> A& { return scr[(row0 + r) * sw + o]; };
+  // U[c], V[c] for c = x, y, z
+  for (int c = 0; c < 3; ++c) {
+    for (int x = threadIdx.x; x < TM * F; x += blockDim.x) {
+      const int r = x / F, f = x % F;
+      R1[r * LD1 + f] = row0 + r < (size_t)N ? v[(row0 + r) * 3 * F + c * F + f] : P::st(0);
+    }
+    __syncthreads();
+    dense_tiles<P, 1, UB_NW, F / P::KC>(R1, LD1, a.uv, [&](int ct, C* acc) {
+      const int col = ct * 16 + (lane & 15);
+      for (int i = 0; i < 4; ++i) {
+        const int r = P::row(lane, i);
+        if (row0 + r < (size_t)N) sc(r, O_UV + c * 2 * F + col) = acc[0][i];
+      }
+    });
+    __syncthreads();
+  }
+  // |V|, <U, V>; [s ; |V|] into R1
+  for (int x = threadIdx.x; x < TM * F; x += blockDim.x) {
+    const int r = x / F, f = x % F;
+    A n2 = 0, pd = 0, nv = 0;
+    T sv = P::st(0);
+    if (row0 + r < (size_t)N) {
+      for (int c = 0; c < 3; ++c) {
+        const A U = sc(r, O_UV + c * 2 * F + f), V = sc(r, O_UV + c * 2 * F + F + f);
+        n2 += V * V;
+        pd += U * V;
+      }
+      nv = sqrt(n2);
+      sc(r, O_N + f) = nv;
+      sc(r, O_PD + f) = pd;
+      sv = s[(row0 + r) * F + f];
+    }
+    R1[r * LD1 + f] = sv;
+    R1[r * LD1 + F + f] = P::st(nv);
+  }
+  __syncthreads();
+  // z = W1a [s ; |V|] + b1a ; silu(z) into R2
+  dense_tiles<P, 1, UB_NW, 2 * F / P::KC>(R1, LD1, a.upd1, [&](int ct, C* acc) {
+    const int col = ct * 16 + (lane & 15);
+    const A bias = ((const A*)a.upd1.b)[col];
+    for (int i = 0; i < 4; ++i) {
+      const int r = P::row(lane, i);
+      const A z = acc[0][i] + bias;
+      if (row0 + r < (size_t)N) sc(r, O_Z + col) = z;
+      R2[r * LD2 + col] = P::st(silu<A>(z));
+    }
+  });
+  __syncthreads();
+  // a = W2a silu(z) + b2a: keep a_vv, a_sv
+  dense_tiles<P, 1, UB_NW, F / P::KC>(R2, LD2, a.upd2, [&](int ct, C* acc) {
+    const int col = ct * 16 + (lane & 15);
+    if (col >= 2 * F) return;
+    const A bias = ((const A*)a.upd2.b)[col];
+    for (int i = 0; i < 4; ++i) {
+      const int r = P::row(lane, i);
+      if (row0 + r < (size_t)N) sc(r, (col < F ? O_AVV : O_ASV - F) + col) = acc[0][i] + bias;
+    }
+  });
+  // g_a = [sum_c g_v[c] U[c] | g_s <U, V> | g_s] into R1
+  for (int x = threadIdx.x; x < TM * F; x += blockDim.x) {
+    const int r = x / F, f = x % F;
+    A gvv = 0, gsv = 0, gss = 0;
+    if (row0 + r < (size_t)N) {
+      const size_t i = row0 + r;
+      for (int c = 0; c < 3; ++c) gvv += gv[i * 3 * F + c * F + f] * sc(r, O_UV + c * 2 * F + f);
+      gss = gs[i * F + f];
+      gsv = gss * sc(r, O_PD + f);
+    }
+    R1[r * LD1 + f] = P::st(gvv);
+    R1[r * LD1 + F + f] = P::st(gsv);
+    R1[r * LD1 + 2 * F + f] = P::st(gss);
+  }
+  __syncthreads();
+  // g_z = (W2a^T g_a) * silu'(z) into R2
+  dense_tiles<P, 1, UB_NW, 3 * F / P::KC>(R1, LD1, a.upd2T, [&](int ct, C* acc) {
+    const int col = ct * 16 + (lane & 15);
+    for (int i = 0; i < 4; ++i) {
+      const int r = P::row(lane, i);
+      A g = 0;
+      if (row0 + r < (size_t)N) g = acc[0][i] * dsilu<A>(sc(r, O_Z + col));
+      R2[r * LD2 + col] = P::st(g);
+    }
+  });
+  __syncthreads();
+  // [g_s' ; g_n] = W1a^T g_z: g_s after the message = g_s + g_s'
+  A* gs_out = (A*)a.gs_out;
+  dense_tiles<P, 1, UB_NW, F / P::KC>(R2, LD2, a.upd1T, [&](int ct, C* acc) {
+    const int col = ct * 16 + (lane & 15);
+    for (int i = 0; i < 4; ++i) {
+      const int r = P::row(lane, i);
+      const size_t g = row0 + r;
+      if (g >= (size_t)N) continue;
+      if (col < F) gs_out[g * F + col] = gs[g * F + col] + acc[0][i];
+      else sc(r, O_GN + col - F) = acc[0][i];
+    }
+  });
+  __syncthreads();
+  // per component: [g_U | g_V] into R1, then g_v after the message =
+  // g_v + [U^T | V^T] [g_U ; g_V]
+  A* gv_out = (A*)a.gv_out;
+  for (int c = 0; c < 3; ++c) {
+    for (int x = threadIdx.x; x < TM * F; x += blockDim.x) {
+      const int r = x / F, f = x % F;
+      A gU = 0, gV = 0;
+      if (row0 + r < (size_t)N) {
+        const size_t i = row0 + r;
+        const A U = sc(r, O_UV + c * 2 * F + f), V = sc(r, O_UV + c * 2 * F + F + f);
+        const A g_s = gs[i * F + f], gvc = gv[i * 3 * F + c * F + f];
+        const A asv = sc(r, O_ASV + f), nv = sc(r, O_N + f);
+        gU = gvc * sc(r, O_AVV + f) + g_s * asv * V;
+        gV = g_s * asv * U + (nv > A(0) ? sc(r, O_GN + f) * V / nv : A(0));
+      }
+      R1[r * LD1 + f] = P::st(gU);
+      R1[r * LD1 + F + f] = P::st(gV);
+    }
+    __syncthreads();
+    dense_tiles<P, 1, UB_NW, 2 * F / P::KC>(R1, LD1, a.uvT, [&](int ct, C* acc) {
+      const int col = ct * 16 + (lane & 15);
+      for (int i = 0; i < 4; ++i) {
+        const int r = P::row(lane, i);
+        const size_t g = row0 + r;
+        if (g < (size_t)N) {
+          const size_t o = g * 3 * F + c * F + col;
+          gv_out[o] = gv[o] + acc[0][i];
+        }
+      }
+    });
+    __syncthreads();
+  }
+}
+
+// -------------------------------------------------------------- phi, back ----
+// g_s = g_s' + W1^T ((W2^T g_h) * silu'(W1 s + b1)); tile of 16 atoms.
+struct PhiBwdArgs {
+  int N;
+  const void* s;       // s before the message [N][F]
+  const void* gh;      // [N][3F]
+  const void* gs_mid;  // [N][F]
+  void* gs_out;
+  void* scratch;
+  int sw;
+  DenseDev phi1, phi1T, phi2T;
+};
+
+template <class P, int F>
+__global__ void __launch_bounds__(64 * UB_NW) k_phi_bwd(PhiBwdArgs a) {
+  using T = typename P::T;
+  using A = typename P::A;
+  using C = typename P::C;
+  constexpr int TM = 16, LD1 = 3 * F + P::PAD, LD2 = F + P::PAD;
+  extern __shared__ __attribute__((aligned(16))) unsigned char smem[];
+  T* R1 = (T*)smem;
+  T* R2 = R1 + TM * LD1;
+  const int lane = threadIdx.x & 63;
+  const size_t row0 = (size_t)blockIdx.x * TM;
+  const int N = a.N;
+  const T* s = (const T*)a.s;
+  const A* gh = (const A*)a.gh;
+  A* scr = (A*)a.scratch;
+  for (int x = threadIdx.x; x < TM * F; x += blockDim.x) {
+    const int r = x / F, f = x % F;
+    R2[r * LD2 + f] = row0 + r < (size_t)N ? s[(row0 + r) * F + f] : P::st(0);
+  }
+  for (int x = threadIdx.x; x < TM * 3 * F; x += blockDim.x) {
+    const int r = x / (3 * F), f = x % (3 * F);
+    R1[r * LD1 + f] = P::st(row0 + r < (size_t)N ? gh[(row0 + r) * 3 * F + f] : A(0));
+  }
+  __syncthreads();
+  dense_tiles<P, 1, UB_NW, F / P::KC>(R2, LD2, a.phi1, [&](int ct, C* acc) {
+    const int col = ct * 16 + (lane & 15);
+    const A bias = ((const A*)a.phi1.b)[col];
+    for (int i = 0; i < 4; ++i) {
+      const int r = P::row(lane, i);
+      if (row0 + r < (size_t)N) scr[(row0 + r) * a.sw + col] = dsilu<A>(acc[0][i] + bias);
+    }
+  });
+  __syncthreads();
+  dense_tiles<P, 1, UB_NW, 3 * F / P::KC>(R1, LD1, a.phi2T, [&](int ct, C* acc) {
+    const int col = ct * 16 + (lane & 15);
+    for (int i = 0; i < 4; ++i) {
+      const int r = P::row(lane, i);
+      A g = 0;
+      if (row0 + r < (size_t)N) g = acc[0][i] * scr[(row0 + r) * a.sw + col];
+      R2[r * LD2 + col] = P::st(g);
+    }
+  });
+  __syncthreads();
+  const A* gm = (const A*)a.gs_mid;
+  A* go = (A*)a.gs_out;
+  dense_tiles<P, 1, UB_NW, F / P::KC>(R2, LD2, a.phi1T, [&](int ct, C* acc) {
+    const int col = ct * 16 + (lane & 15);
+    for (int i = 0; i < 4; ++i) {
+      const size_t g = row0 + P::row(lane, i);
+      if (g < (size_t)N) go[g * F + col] = gm[g * F + col] + acc[0][i];
+    }
+  });
+}
+
+// ---------------------------------------------------------- message, back ----
+// Per sender j and channel c (lane = channel, a wave = 64 channels, waves
+// independent), over the edges e = (i <- j) whose sender is j, with the
+// receiver's g_s' and g_v' gathered:
+//   A_v = sum_c g_v'_i[c] v_j[c],  A_r = sum_c g_v'_i[c] rhat_e[c]
+//   g_h^s_j += g_s'_i w^s,  g_h^v_j += A_v w^v,  g_h^r_j += A_r w^r
+//   g_v_j[c] = g_v'_j[c] + sum_e g_v'_i[c] h^v_j w^v
+//   dE/dd_e    += sum_c (g_s'_i h^s_j w'^s + A_v h^v_j w'^v + A_r h^r_j w'^r)
+//   dE/drhat_e += sum_c g_v'_i[.] h^r_j w^r
+// with w = f_c (Wf g + bf) and w' = dw/dd formed on the matrix cores from
+// the basis rows and their derivatives (one after the other through the
+// same LDS tile; the receiver rows are gathered once for each).  The sums
+// over channels are a reduce-scatter across the wave's lanes; each wave
+// writes its own slot, so no two lanes add to one value.
+constexpr int MB_RB = 4;   // senders per workgroup
+
+struct MsgBwdArgs {
+  int N;
+  long long E;
+  const int32_t* t_ptr;
+  const int32_t* t_edge;
+  const int32_t* recv;
+  const void* basis;
+  const void* dbasis;
+  const void* einfo;
+  DenseDev filt;
+  const void* h;       // layer input h, v (storage type)
+  const void* v;
+  const void* gs;      // dE/d(s, v) after the message (accumulation type)
+  const void* gv;
+  void* gh;            // out
+  void* gv_out;
+  void* eg;            // [E][NW][4]
+};
+
+template <class A>
+__device__ __forceinline__ A lane_bcast(A x, int lane) {
+  if constexpr (sizeof(A) == 4) {
+    return __int_as_float(__builtin_amdgcn_readlane(__float_as_int(x), lane));
+  } else {
+    const long long b = __double_as_longlong(x);
+    const int lo = __builtin_amdgcn_readlane((int)(b & 0xffffffff), lane);
+    const int hi = __builtin_amdgcn_readlane((int)(b >> 32), lane);
+    return __longlong_as_double(((long long)hi << 32) | (unsigned)lo);
+  }
+}
+
+// Sum of vals[k] over the 64 lanes, for k = lane: each step keeps the half
+// of the indices selected by one lane bit and adds the partner's copy.
+template <class A, int LEN>
+__device__ __forceinline__ void reduce_scatter(A* vals, int lane) {
+  if constexpr (LEN > 1) {
+    constexpr int H = LEN / 2;
+    const bool up = (lane & H) != 0;
+#pragma unroll
+    for (int k = 0; k < H; ++k) {
+      const A keep = up ? vals[k + H] : vals[k];
+      const A give = up ? vals[k] : vals[k + H];
+      vals[k] = keep + __shfl_xor(give, H);
+    }
+    reduce_scatter<A, H>(vals, lane);
+  }
+}
+
+template <class P, int F, int KBM>
+__global__ void __launch_bounds__(F) k_message_bwd(MsgBwdArgs a) {
+  using T = typename P::T;
+  using A = typename P::A;
+  using C = typename P::C;
+  using Fr = typename P::Fr;
+  constexpr int NW = F / 64, NFT = F / 16, WLD = 64 + 4;
+  constexpr int kcols = KBM * P::KC;
+  __shared__ A Wt[NW][3][16 * WLD];
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int c = 64 * wave + lane;
+  const T* Wf = (const T*)a.filt.w;
+  const T* h = (const T*)a.h;
+  const T* vv = (const T*)a.v;
+  const A* gs = (const A*)a.gs;
+  const A* gv = (const A*)a.gv;
+  const A* einfo = (const A*)a.einfo;
+  A* wt0 = Wt[wave][0];
+  A* wt1 = Wt[wave][1];
+  A* wt2 = Wt[wave][2];
+  const int per_xcd = gridDim.x / 8;
+  const int lb = (blockIdx.x % 8) * per_xcd + blockIdx.x / 8;
+  const int j0 = lb * MB_RB;
+  if (j0 >= a.N) return;
+  const int j1 = min(a.N, j0 + MB_RB);
+  const int tp_lane = a.t_ptr[j0 + min(lane, j1 - j0)];
+  auto tp = [&](int j) { return __builtin_amdgcn_readlane(tp_lane, j - j0); };
+  // the filter (or its derivative) of the chunk's 16 edges at this wave's
+  // 64 channels into Wt, from the basis rows `rows`
+  auto filter = [&](const T* rows, int er) {
+    const T* gp = rows + (size_t)er * kcols + (lane >> 4) * P::KPL;
+    Fr Ga[KBM];
+#pragma unroll
+    for (int kb = 0; kb < KBM; ++kb) Ga[kb] = P::frag(gp + kb * P::KC);
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+      C w[3];
+#pragma unroll
+      for (int part = 0; part < 3; ++part) {
+        for (int r = 0; r < 4; ++r) w[part][r] = 0;
+#pragma unroll
+        for (int kb = 0; kb < KBM; ++kb) {
+          const int ct = part * NFT + 4 * wave + q;
+          w[part] = P::mfma(Ga[kb], P::frag(Wf + ((size_t)(ct * KBM + kb) * 64 + lane) * P::KPL), w[part]);
+        }
+      }
+      const int col = 16 * q + (lane & 15);
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        const int row = P::row(lane, r);
+        wt0[row * WLD + col] = w[0][r];
+        wt1[row * WLD + col] = w[1][r];
+        wt2[row * WLD + col] = w[2][r];
+      }
+    }
+    __builtin_amdgcn_wave_barrier();
+    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+  };
+  auto wave_sync = [&]() {
+    __builtin_amdgcn_wave_barrier();
+    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+  };
+  A* gh_out = (A*)a.gh;
+  A* gv_out = (A*)a.gv_out;
+  A* eg = (A*)a.eg;
+  for (int j = j0; j < j1; ++j) {
+    const int ea = tp(j), eb = tp(j + 1);
+    const size_t jb = (size_t)j * 3 * F;
+    const A hs = P::ld(h[jb + c]), hv = P::ld(h[jb + F + c]), hr = P::ld(h[jb + 2 * F + c]);
+    const A v0 = P::ld(vv[jb + c]), v1 = P::ld(vv[jb + F + c]), v2 = P::ld(vv[jb + 2 * F + c]);
+    A acc_hs = 0, acc_hv = 0, acc_hr = 0, acc_v0 = 0, acc_v1 = 0, acc_v2 = 0;
+    for (int c0 = ea; c0 < eb; c0 += 16) {
+      const int cnt = min(16, eb - c0);
+      // edge id of row lane % 16 (past the chunk: the zero padding row E)
+      const int er = (lane & 15) < cnt ? a.t_edge[c0 + (lane & 15)] : (int)a.E;
+      // receiver and rhat of edge `lane` on lanes < cnt
+      A ex = 0, ey = 0, ez = 0;
+      int ei = 0;
+      if (lane < cnt) {
+        ex = einfo[4 * (size_t)er];
+        ey = einfo[4 * (size_t)er + 1];
+        ez = einfo[4 * (size_t)er + 2];
+        ei = a.recv[er];
+      }
+      A vals[64];
+#pragma unroll
+      for (int k = 0; k < 64; ++k) vals[k] = 0;
+      // pass 1: w' -> dE/dd partials
+      filter((const T*)a.dbasis, er);
+#pragma unroll
+      for (int e = 0; e < 16; ++e) {
+        if (e < cnt) {
+          const int i = __builtin_amdgcn_readlane(ei, e);
+          const size_t ib = (size_t)i * 3 * F;
+          const A g_s = gs[(size_t)i * F + c], g0 = gv[ib + c], g1 = gv[ib + F + c], g2 = gv[ib + 2 * F + c];
+          const A rx = lane_bcast(ex, e), ry = lane_bcast(ey, e), rz = lane_bcast(ez, e);
+          const A Av = g0 * v0 + g1 * v1 + g2 * v2, Ar = g0 * rx + g1 * ry + g2 * rz;
+          vals[e] = g_s * hs * wt0[e * WLD + lane] + Av * hv * wt1[e * WLD + lane] + Ar * hr * wt2[e * WLD + lane];
+        }
+      }
+      wave_sync();
+      // pass 2: w -> g_h, g_v and dE/drhat partials
+      filter((const T*)a.basis, er);
+#pragma unroll
+      for (int e = 0; e < 16; ++e) {
+        if (e < cnt) {
+          const int i = __builtin_amdgcn_readlane(ei, e);
+          const size_t ib = (size_t)i * 3 * F;
+          const A g_s = gs[(size_t)i * F + c], g0 = gv[ib + c], g1 = gv[ib + F + c], g2 = gv[ib + 2 * F + c];
+          const A rx = lane_bcast(ex, e), ry = lane_bcast(ey, e), rz = lane_bcast(ez, e);
+          const A Av = g0 * v0 + g1 * v1 + g2 * v2, Ar = g0 * rx + g1 * ry + g2 * rz;
+          const A ws = wt0[e * WLD + lane], wv = wt1[e * WLD + lane], wr = wt2[e * WLD + lane];
+          acc_hs += g_s * ws;
+          acc_hv += Av * wv;
+          acc_hr += Ar * wr;
+          const A tv = hv * wv, tr = hr * wr;
+          acc_v0 += g0 * tv;
+          acc_v1 += g1 * tv;
+          acc_v2 += g2 * tv;
+          vals[16 + e] = g0 * tr;
+          vals[32 + e] = g1 * tr;
+          vals[48 + e] = g2 * tr;
+        }
+      }
+      wave_sync();
+      // lane l: the wave's total of value l / 16 for edge l % 16
+      reduce_scatter<A, 64>(vals, lane);
+      if ((lane & 15) < cnt) {
+        A* o = eg + ((size_t)er * NW + wave) * 4 + (lane >> 4);
+        *o += vals[0];
+      }
+    }
+    gh_out[jb + c] = acc_hs;
+    gh_out[jb + F + c] = acc_hv;
+    gh_out[jb + 2 * F + c] = acc_hr;
+    gv_out[jb + c] = gv[jb + c] + acc_v0;
+    gv_out[jb + F + c] = gv[jb + F + c] + acc_v1;
+    gv_out[jb + 2 * F + c] = gv[jb + 2 * F + c] + acc_v2;
+  }
+}
+
+// ------------------------------------------------------------------ forces ----
+// dE/dr_e = dE/dd rhat + (dE/drhat - (dE/drhat . rhat) rhat) / d  (FP64
+// geometry, the wave slots summed in order).
+template <class A>
+__global__ void __launch_bounds__(256) k_edge_grad(long long E, int NW, const int32_t* __restrict__ recv,
+                                                  const int32_t* __restrict__ col,
+                                                  const int32_t* __restrict__ shift,
+                                                  const int32_t* __restrict__ atom_struct,
+                                                  const double* __restrict__ pos,
+                                                  const double* __restrict__ cell,
+                                                  const A* __restrict__ eg, double* __restrict__ gr) {
+  const long long e = blockIdx.x * (long long)blockDim.x + threadIdx.x;
+  if (e >= E) return;
+  const int i = recv[e], j = col[e], sh = shift[e];
+  const double* Cl = cell + 9 * atom_struct[i];
+  const double n0 = (double)(int8_t)(sh & 0xff), n1 = (double)(int8_t)((sh >> 8) & 0xff),
+               n2 = (double)(int8_t)((sh >> 16) & 0xff);
+  const double rx = (pos[3 * j] - pos[3 * i]) + ((n0 * Cl[0] + n1 * Cl[3]) + n2 * Cl[6]);
+  const double ry = (pos[3 * j + 1] - pos[3 * i + 1]) + ((n0 * Cl[1] + n1 * Cl[4]) + n2 * Cl[7]);
+  const double rz = (pos[3 * j + 2] - pos[3 * i + 2]) + ((n0 * Cl[2] + n1 * Cl[5]) + n2 * Cl[8]);
+  const double d = sqrt(rx * rx + ry * ry + rz * rz);
+  const double ux = rx / d, uy = ry / d, uz = rz / d;
+  double gd = 0, gx = 0, gy = 0, gz = 0;
+  for (int w = 0; w < NW; ++w) {
+    const A* p = eg + ((size_t)e * NW + w) * 4;
+    gd += (double)p[0];
+    gx += (double)p[1];
+    gy += (double)p[2];
+    gz += (double)p[3];
+  }
+  const double dot = gx * ux + gy * uy + gz * uz;
+  gr[3 * e] = gd * ux + (gx - dot * ux) / d;
+  gr[3 * e + 1] = gd * uy + (gy - dot * uy) / d;
+  gr[3 * e + 2] = gd * uz + (gz - dot * uz) / d;
+}
+
+__global__ void __launch_bounds__(256) k_forces(int N, const int32_t* __restrict__ row_ptr,
+                                               const int32_t* __restrict__ t_ptr,
+                                               const int32_t* __restrict__ t_edge,
+                                               const double* __restrict__ gr, double* __restrict__ forces) {
+  const int a = blockIdx.x * blockDim.x + threadIdx.x;
+  if (a >= N) return;
+  double fx = 0, fy = 0, fz = 0;
+  for (int e = row_ptr[a]; e < row_ptr[a + 1]; ++e) {
+    fx += gr[3 * (size_t)e];
+    fy += gr[3 * (size_t)e + 1];
+    fz += gr[3 * (size_t)e + 2];
+  }
+  for (int t = t_ptr[a]; t < t_ptr[a + 1]; ++t) {
+    const size_t e = t_edge[t];
+    fx -= gr[3 * e];
+    fy -= gr[3 * e + 1];
+    fz -= gr[3 * e + 2];
+  }
+  forces[3 * (size_t)a] = fx;
+  forces[3 * (size_t)a + 1] = fy;
+  forces[3 * (size_t)a + 2] = fz;
+}
+
+// ---------------------------------------------------------------- driver ----
+template <class K>
+hipError_t allow_lds(K kernel, size_t smem) {
+  if (smem <= 64 * 1024) return hipSuccess;
+  return hipFuncSetAttribute((const void*)kernel, hipFuncAttributeMaxDynamicSharedMemorySize, (int)smem);
+}
+
+template <class P, int F>
+hipError_t launch_message_bwd(hipStream_t st, const MsgBwdArgs& ma, int nkb) {
+  const int blocks = ((ma.N + MB_RB - 1) / MB_RB + 7) / 8 * 8;
+  switch (nkb) {
+    case 3: k_message_bwd<P, F, 3><<<blocks, F, 0, st>>>(ma); break;
+    case 6: k_message_bwd<P, F, 6><<<blocks, F, 0, st>>>(ma); break;
+    case 9: k_message_bwd<P, F, 9><<<blocks, F, 0, st>>>(ma); break;
+    case 12: k_message_bwd<P, F, 12><<<blocks, F, 0, st>>>(ma); break;
+    case 17: k_message_bwd<P, F, 17><<<blocks, F, 0, st>>>(ma); break;
+    default: return hipErrorInvalidValue;
+  }
+  return hipGetLastError();
+}
+
+template <class P, int F>
+hipError_t backward_impl(hipStream_t st, BackwardArgs& ba) {
+  using T = typename P::T;
+  using A = typename P::A;
+  const painn_graph* g = ba.g;
+  const PrecModel* pm = ba.pm;
+  const Hyper& hp = ba.m->hp;
+  const int N = g->N;
+  const long long E = g->E;
+  constexpr int NW = F / 64;
+  const SaveLayout sv(ba.save, N, F, hp.L, sizeof(T));
+  const int kcols = pm->layers[0].filt_mma.din_p;
+  if (N == 0) return hipSuccess;
+  // LDS of the tile kernels: 16 rows of 3F + F (+ padding)
+  const size_t smem_ub = (size_t)16 * (4 * F + 2 * P::PAD) * sizeof(T);
+  if (smem_ub > 160 * 1024) return hipErrorInvalidValue;
+  hipError_t e = allow_lds(k_update_bwd<P, F>, smem_ub);
+  if (e == hipSuccess) e = allow_lds(k_phi_bwd<P, F>, smem_ub);
+  if (e != hipSuccess) return e;
+  if (E > 0) {
+    const double delta = hp.cutoff / (hp.K - 1);
+    k_edge_deriv<P><<<(unsigned)((E + 16 + 255) / 256), 256, 0, st>>>(
+        E, hp.K, kcols, hp.cutoff, hp.rbf_type, 1.0 / (2.0 * delta * delta), delta, g->recv, g->col, g->shift,
+        g->atom_struct, g->pos, g->cell, (T*)ba.dbasis);
+    k_fill<A><<<grid_of((size_t)E * NW * 4, 256), 256, 0, st>>>((size_t)E * NW * 4, (A*)ba.eg);
+  }
+  k_fill<A><<<grid_of((size_t)N * 3 * F, 256), 256, 0, st>>>((size_t)N * 3 * F, (A*)ba.gv);
+  // heads
+  prof_mark(ba.prof, st, KC_BWD_HEADS, true);
+  {
+    HeadBwdArgs ha;
+    ha.N = N;
+    ha.F = F;
+    ha.ns = (int)pm->shared.size();
+    ha.nb = (int)hp.branch_dims.size();
+    if (ha.ns > 16 || ha.nb > 16 || ha.ns + ha.nb > 32) return hipErrorInvalidValue;
+    int wmax = F, off = 0;
+    for (int m = 0; m < ha.ns; ++m) {
+      ha.shared[m] = pm->shared[m];
+      ha.sharedT[m] = pm->sharedT[m];
+      wmax = wmax > pad32(hp.shared_dims[m]) ? wmax : pad32(hp.shared_dims[m]);
+    }
+    for (int m = 0; m < ha.nb; ++m) {
+      ha.bdout[m] = hp.branch_dims[m];
+      if (m + 1 < ha.nb) wmax = wmax > pad32(hp.branch_dims[m]) ? wmax : pad32(hp.branch_dims[m]);
+    }
+    for (int m = 0; m + 1 < ha.ns + ha.nb; ++m) {
+      ha.zoff[m] = off;
+      off += m < ha.ns ? pad32(hp.shared_dims[m]) : pad32(hp.branch_dims[m - ha.ns]);
+    }
+    if (off > ba.scratch_w) return hipErrorInvalidValue;
+    ha.ldw = wmax + P::PAD;
+    ha.s = sv.S(hp.L);
+    ha.table = (const void* const*)pm->head_table;
+    ha.tableT = (const void* const*)pm->head_tableT;
+    ha.scratch = ba.scratch;
+    ha.sw = ba.scratch_w;
+    ha.gs = ba.gs;
+    const size_t smem = (size_t)2 * 16 * ha.ldw * sizeof(T);
+    if (smem > 150 * 1024) return hipErrorInvalidValue;
+    e = allow_lds(k_heads_bwd<P, F>, smem);
+    if (e != hipSuccess) return e;
+    int grid;
+    if (ba.dataset_id) {
+      ha.order = ba.head_order;
+      ha.tiles = (const HeadTile*)ba.head_tiles;
+      ha.plan = (const HeadPlan*)ba.head_plan;
+      grid = (N + 15) / 16 + hp.n_heads;   // at least the forward's tile count
+    } else {
+      ha.order = nullptr;
+      ha.tiles = nullptr;
+      ha.plan = nullptr;
+      grid = (N + 15) / 16;
+    }
+    k_heads_bwd<P, F><<<grid, 64 * HB_NW, smem, st>>>(ha);
+  }
+  prof_mark(ba.prof, st, KC_BWD_HEADS, false);
+  const int tiles = (N + 15) / 16;
+  for (int l = hp.L - 1; l >= 0; --l) {
+    const LayerDev& Ld = pm->layers[l];
+    UpdBwdArgs ua;
+    ua.N = N;
+    ua.s = sv.Smid(l);
+    ua.v = sv.Vmid(l);
+    ua.gs = ba.gs;
+    ua.gv = ba.gv;
+    ua.gs_out = ba.gs2;
+    ua.gv_out = ba.gv2;
+    ua.scratch = ba.scratch;
+    ua.sw = ba.scratch_w;
+    ua.uv = Ld.uv;
+    ua.upd1 = Ld.upd1;
+    ua.upd2 = Ld.upd2;
+    ua.uvT = Ld.uvT;
+    ua.upd1T = Ld.upd1T;
+    ua.upd2T = Ld.upd2T;
+    prof_mark(ba.prof, st, KC_BWD_UPDATE, true);
+    k_update_bwd<P, F><<<tiles, 64 * UB_NW, smem_ub, st>>>(ua);
+    prof_mark(ba.prof, st, KC_BWD_UPDATE, false);
+    MsgBwdArgs ma;
+    ma.N = N;
+    ma.E = E;
+    ma.t_ptr = g->t_ptr;
+    ma.t_edge = g->t_edge;
+    ma.recv = g->recv;
+    ma.basis = ba.basis;
+    ma.dbasis = ba.dbasis;
+    ma.einfo = ba.einfo;
+    ma.filt = Ld.filt_mma;
+    ma.h = sv.H(l);
+    ma.v = sv.V(l);
+    ma.gs = ba.gs2;
+    ma.gv = ba.gv2;
+    ma.gh = ba.gh;
+    ma.gv_out = ba.gv;
+    ma.eg = ba.eg;
+    prof_mark(ba.prof, st, KC_BWD_MESSAGE, true);
+    e = launch_message_bwd<P, F>(st, ma, kcols / P::KC);
+    prof_mark(ba.prof, st, KC_BWD_MESSAGE, false);
+    if (e != hipSuccess) return e;
+    if (l > 0) {
+      PhiBwdArgs pa;
+      pa.N = N;
+      pa.s = sv.S(l);
+      pa.gh = ba.gh;
+      pa.gs_mid = ba.gs2;
+      pa.gs_out = ba.gs;
+      pa.scratch = ba.scratch;
+      pa.sw = ba.scratch_w;
+      pa.phi1 = Ld.phi1;
+      pa.phi1T = Ld.phi1T;
+      pa.phi2T = Ld.phi2T;
+      prof_mark(ba.prof, st, KC_BWD_PHI, true);
+      k_phi_bwd<P, F><<<tiles, 64 * UB_NW, smem_ub, st>>>(pa);
+      prof_mark(ba.prof, st, KC_BWD_PHI, false);
+    }
+  }
+  prof_mark(ba.prof, st, KC_FORCE, true);
+  if (E > 0)
+    k_edge_grad<A><<<(unsigned)((E + 255) / 256), 256, 0, st>>>(E, NW, g->recv, g->col, g->shift, g->atom_struct,
+                                                                 g->pos, g->cell, (const A*)ba.eg, ba.gr);
+  k_forces<<<(N + 255) / 256, 256, 0, st>>>(N, g->row_ptr, g->t_ptr, g->t_edge, ba.gr, ba.forces);
+  prof_mark(ba.prof, st, KC_FORCE, false);
+  return hipGetLastError();
+}
+
+template <class P>
+hipError_t backward_prec(hipStream_t st, BackwardArgs& ba) {
+  switch (ba.m->hp.F) {
+    case 64: return backward_impl<P, 64>(st, ba);
+    case 128: return backward_impl<P, 128>(st, ba);
+    case 256: return backward_impl<P, 256>(st, ba);
+    case 384: return backward_impl<P, 384>(st, ba);
+    default: return hipErrorInvalidValue;
+  }
+}
+
+}  // namespace
+
+hipError_t launch_backward(hipStream_t st, int prec, BackwardArgs& ba) {
+  if (prec == PAINN_FP64) return backward_prec<P64>(st, ba);
+  if (prec == PAINN_FP32) return backward_prec<P32>(st, ba);
+  return hipErrorInvalidValue;
+}
+
+hipError_t launch_transpose(hipStream_t st, Profiler* p, painn_graph* g) {
+  const int N = g->N;
+  const long long E = g->E;
+  prof_mark(p, st, KC_TRANSPOSE, true);
+  k_fill<int32_t><<<grid_of((size_t)N + 1, 256), 256, 0, st>>>((size_t)N + 1, g->t_count);
+  if (E > 0) k_t_count<<<grid_of((size_t)E, 256), 256, 0, st>>>(E, g->col, g->t_count);
+  k_t_scan<<<1, 1024, 0, st>>>(N, g->t_count, g->t_ptr);
+  if (E > 0) {
+    k_t_fill<<<grid_of((size_t)E, 256), 256, 0, st>>>(E, g->col, g->t_ptr, g->t_count, g->t_edge);
+    k_t_sort<<<(N + 255) / 256, 256, 0, st>>>(N, g->t_ptr, g->t_edge);
+  }
+  prof_mark(p, st, KC_TRANSPOSE, false);
+  return hipGetLastError();
+}

@@ -102,7 +102,8 @@ struct MsgArgs {
   DenseDev filt_mma;   // the filter packed for MFMA (K+1 -> 3F, or 2(K+1) for BF16)
   const void* h;
   const void* v_in;
-  void* s;
+  const void* s_in;    // s before the message (may equal s)
+  void* s;             // s after the message
   void* v_out;
 };
 
@@ -208,6 +209,7 @@ __global__ void __launch_bounds__(NW * 64) k_message(MsgArgs a) {
   const T* vin = (const T*)a.v_in;
   const T* basis = (const T*)a.basis;
   const A* einfo = (const A*)a.einfo;
+  const T* sin = (const T*)a.s_in;
   T* s = (T*)a.s;
   T* vout = (T*)a.v_out;
   // Workgroups are dealt round-robin to the 8 XCDs.  Renumber them so each
@@ -229,7 +231,7 @@ __global__ void __launch_bounds__(NW * 64) k_message(MsgArgs a) {
 #pragma unroll
     for (int q = 0; q < FTW; ++q) {
       const int f = (wave + NW * q) * 16 + (lane & 15);
-      s_old[q] = s[(size_t)i * F + f];
+      s_old[q] = sin[(size_t)i * F + f];
       v_old[q][0] = vin[ib + f];
       v_old[q][1] = vin[ib + F + f];
       v_old[q][2] = vin[ib + 2 * F + f];
@@ -308,8 +310,10 @@ __global__ void __launch_bounds__(NW * 64) k_message(MsgArgs a) {
 // needs no exchange.  Optionally the next layer's phi follows on the new s.
 struct UpdArgs {
   int N;
-  void* s;
-  void* v;
+  const void* s;   // s and v after the message
+  const void* v;
+  void* s_out;     // after the update (may equal s, v)
+  void* v_out;
   void* h;
   DenseDev uv, upd1, upd2, phi1, phi2;
 };
@@ -347,8 +351,10 @@ k_update(UpdArgs a) {
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const size_t row0 = (size_t)blockIdx.x * TM;
   const int N = a.N;
-  T* s = (T*)a.s;
-  T* v = (T*)a.v;
+  const T* s = (const T*)a.s;
+  const T* v = (const T*)a.v;
+  T* s_out = (T*)a.s_out;
+  T* v_out = (T*)a.v_out;
   for (int x = threadIdx.x; x < TM * F; x += blockDim.x) {
     const int r = x / F, c = x % F;
     SN[r * LD2 + c] = row0 + r < (size_t)N ? s[(row0 + r) * F + c] : P::st(0);
@@ -456,10 +462,10 @@ k_update(UpdArgs a) {
           const T st = P::st(sn);
           SN[rr * LD2 + col] = st;
           if (row < (size_t)N) {
-            s[row * F + col] = st;
+            s_out[row * F + col] = st;
             for (int c = 0; c < 3; ++c) {
               const size_t o = row * 3 * F + c * F + col;
-              v[o] = P::st(P::ld(v[o]) + g_vv * U[q][c][r][i]);
+              v_out[o] = P::st(P::ld(v[o]) + g_vv * U[q][c][r][i]);
             }
           }
         }
@@ -482,18 +488,8 @@ k_update(UpdArgs a) {
 // the epilogue of the layer before it as a dot product, so the widest hidden
 // layer never goes through LDS.  Every atom's result depends only on its own
 // row, so the grouping order does not change any value.
-constexpr int HEADS_MAX = 64;
 constexpr int HEADS_NW = 8;   // waves per heads workgroup
 
-struct HeadPlan {
-  int32_t count[HEADS_MAX];   // valid atoms per head
-  int32_t start[HEADS_MAX];   // first slot of the head in the atom order
-  int32_t cursor[HEADS_MAX];  // scatter cursor
-  int32_t n_tiles;
-};
-struct HeadTile {
-  int32_t head, begin, end, pad;   // slots [begin, end) of the atom order
-};
 static_assert(sizeof(HeadPlan) <= 1024, "head plan workspace is 1 KiB");
 static_assert(sizeof(HeadTile) == 16, "head tile workspace is 16 bytes per tile");
 
@@ -847,6 +843,7 @@ k_message_lane(MsgArgs a) {
   const T* vin = (const T*)a.v_in;
   const T* basis = (const T*)a.basis;
   const A* einfo = (const A*)a.einfo;
+  const T* sin = (const T*)a.s_in;
   T* s = (T*)a.s;
   T* vout = (T*)a.v_out;
   A* wt0 = Wt[wave][0];
@@ -860,10 +857,11 @@ k_message_lane(MsgArgs a) {
   const int i1 = min(a.N, i0 + MSG_RB2);
   const int rp_lane = a.row_ptr[i0 + min(lane, i1 - i0)];
   auto rp = [&](int i) { return __builtin_amdgcn_readlane(rp_lane, i - i0); };
-  // receivers without edges: v_out = v_in, s unchanged
+  // receivers without edges: v_out = v_in, s_out = s_in
   for (int i = i0; i < i1; ++i)
     if (rp(i) == rp(i + 1)) {
       const size_t ib = (size_t)i * 3 * F;
+      s[(size_t)i * F + c] = sin[(size_t)i * F + c];
       vout[ib + c] = vin[ib + c];
       vout[ib + F + c] = vin[ib + F + c];
       vout[ib + 2 * F + c] = vin[ib + 2 * F + c];
@@ -895,7 +893,7 @@ k_message_lane(MsgArgs a) {
   int c0 = rp(i);
   prefetch(c0, min(16, rp(i + 1) - c0));
   size_t ib = (size_t)i * 3 * F;
-  T s_old = s[(size_t)i * F + c];
+  T s_old = sin[(size_t)i * F + c];
   T v_old0 = vin[ib + c], v_old1 = vin[ib + F + c], v_old2 = vin[ib + 2 * F + c];
   A acc_s = 0, acc_v0 = 0, acc_v1 = 0, acc_v2 = 0;
   while (true) {
@@ -1003,7 +1001,7 @@ k_message_lane(MsgArgs a) {
       if (!more) break;
       acc_s = acc_v0 = acc_v1 = acc_v2 = 0;
       ib = (size_t)in * 3 * F;
-      s_old = s[(size_t)in * F + c];
+      s_old = sin[(size_t)in * F + c];
       v_old0 = vin[ib + c];
       v_old1 = vin[ib + F + c];
       v_old2 = vin[ib + 2 * F + c];
@@ -1325,6 +1323,16 @@ hipError_t forward_impl(hipStream_t st, ForwardArgs& fa) {
   T* s = (T*)fa.s;
   T* v[2] = {(T*)fa.v[0], (T*)fa.v[1]};
   T* h = (T*)fa.h;
+  // With a save area every layer reads and writes its own slots (the
+  // reverse pass reads them back); otherwise s and h are updated in place
+  // and v is double buffered.
+  const SaveLayout sv(fa.save, N, F, hp.L, sizeof(T));
+  if (fa.save) {
+    s = (T*)sv.S(0);
+    v[0] = (T*)sv.V(0);
+    h = (T*)sv.H(0);
+    fa.s = sv.S(fa.stop_layer + 1);   // the heads read the final s
+  }
   if (N > 0) {
     prof_mark(fa.prof, st, KC_EMBED, true);
     k_embed<P><<<grid_for((size_t)N * F, 256), 256, 0, st>>>(N, F, g->species, (const T*)pm->emb, s, v[0]);
@@ -1356,10 +1364,11 @@ hipError_t forward_impl(hipStream_t st, ForwardArgs& fa) {
     ma.basis = fa.basis;
     ma.einfo = fa.einfo;
     ma.filt_mma = Ld.filt_mma;
-    ma.h = h;
-    ma.v_in = v[cur];
-    ma.s = s;
-    ma.v_out = v[cur ^ 1];
+    ma.h = fa.save ? sv.H(l) : h;
+    ma.v_in = fa.save ? sv.V(l) : v[cur];
+    ma.s_in = fa.save ? sv.S(l) : s;
+    ma.s = fa.save ? sv.Smid(l) : s;
+    ma.v_out = fa.save ? sv.Vmid(l) : v[cur ^ 1];
     prof_mark(fa.prof, st, KC_MESSAGE, true);
     hipError_t e = launch_message<P, F>(st, ma);
     prof_mark(fa.prof, st, KC_MESSAGE, false);
@@ -1367,9 +1376,11 @@ hipError_t forward_impl(hipStream_t st, ForwardArgs& fa) {
     cur ^= 1;
     UpdArgs ua;
     ua.N = N;
-    ua.s = s;
-    ua.v = v[cur];
-    ua.h = h;
+    ua.s = ma.s;
+    ua.v = ma.v_out;
+    ua.s_out = fa.save ? sv.S(l + 1) : s;
+    ua.v_out = fa.save ? sv.V(l + 1) : v[cur];
+    ua.h = fa.save ? sv.H(l + 1) : h;
     ua.uv = Ld.uv;
     ua.upd1 = Ld.upd1;
     ua.upd2 = Ld.upd2;
@@ -1387,8 +1398,9 @@ hipError_t forward_impl(hipStream_t st, ForwardArgs& fa) {
   if (fa.s_out) {
     prof_mark(fa.prof, st, KC_EXPORT, true);
     if (N > 0)
-      k_export<P><<<grid_for((size_t)N * F, 256), 256, 0, st>>>(N, F, hp.F_logical, s, v[cur], fa.s_out,
-                                                                 fa.v_out);
+      k_export<P><<<grid_for((size_t)N * F, 256), 256, 0, st>>>(
+          N, F, hp.F_logical, fa.save ? (const T*)sv.S(fa.stop_layer + 1) : s,
+          fa.save ? (const T*)sv.V(fa.stop_layer + 1) : v[cur], fa.s_out, fa.v_out);
     prof_mark(fa.prof, st, KC_EXPORT, false);
     return hipGetLastError();
   }

@@ -88,6 +88,10 @@ struct LayerDev {       // one interaction layer
                         // input column K is the bias (multiplied by f_c), din
                         // padded to a multiple of the MFMA K step only; BF16
                         // stores it twice along K (input [hi | lo] terms)
+  // transposed weights for the reverse pass (no bias; built on the first
+  // forces call): phi1^T F -> F, phi2^T 3F -> F, [U^T | V^T] 2F -> F,
+  // upd1^T F -> 2F, upd2^T 3F -> F
+  DenseDev phi1T, phi2T, uvT, upd1T, upd2T;
 };
 
 struct PrecModel {      // the model cast and packed for one precision
@@ -98,6 +102,12 @@ struct PrecModel {      // the model cast and packed for one precision
   std::vector<std::vector<DenseDev>> branch;    // [head][layer]
   void* head_table = nullptr;                   // device [head][layer][2] = (w, b)
   std::vector<DenseDev> blend;                  // branch-weighting MLP (empty: none)
+  // reverse pass: transposed shared and branch layers (the branch's output
+  // layer has none), device table [head][layer][2] = (w^T, null)
+  bool has_T = false;
+  std::vector<DenseDev> sharedT;
+  std::vector<std::vector<DenseDev>> branchT;
+  void* head_tableT = nullptr;
   std::vector<void*> allocs;
 };
 
@@ -115,7 +125,8 @@ struct Hyper {
 // ---- per-kernel event timing (painn_profile_*) ------------------------------
 enum KernelClass {
   KC_GRAPH_PREP, KC_GRAPH_COUNT, KC_GRAPH_SCAN, KC_GRAPH_FILL, KC_EMBED, KC_PHI,
-  KC_EDGE_PREP, KC_MESSAGE, KC_UPDATE, KC_HEADS, KC_ENERGY, KC_EXPORT, KC_COUNT
+  KC_EDGE_PREP, KC_MESSAGE, KC_UPDATE, KC_HEADS, KC_ENERGY, KC_EXPORT,
+  KC_TRANSPOSE, KC_BWD_HEADS, KC_BWD_UPDATE, KC_BWD_MESSAGE, KC_BWD_PHI, KC_FORCE, KC_COUNT
 };
 struct Profiler;
 // Record the start (begin = true) or end of a kernel of class `kc` on `s`;
@@ -131,6 +142,9 @@ struct painn_ctx {
   // forward workspace (grown on demand)
   void* ws = nullptr;
   size_t ws_bytes = 0;
+  // reverse-pass workspace (saved activations and gradients; grown on demand)
+  void* bws = nullptr;
+  size_t bws_bytes = 0;
 };
 
 struct painn_model {
@@ -174,6 +188,12 @@ struct painn_graph {
   int32_t* col_full = nullptr;    int32_t* shift_full = nullptr;  int32_t* recv_full = nullptr;
   size_t cap_edges_full = 0, cap_atoms_cap = 0;
   size_t cap_atoms = 0, cap_struct = 0, cap_edges = 0, cap_scan = 0, cap_bins = 0, cap_bin_scan = 0;
+  // edges grouped by sender (built on the first forces call, dropped by a
+  // rebuild): t_edge[t_ptr[j] .. t_ptr[j+1]) are the ids of the edges whose
+  // sender is j, ascending
+  bool t_valid = false;
+  int32_t* t_ptr = nullptr;    int32_t* t_edge = nullptr;   int32_t* t_count = nullptr;
+  size_t cap_t_atoms = 0, cap_t_edges = 0;
 };
 
 // ---- kernel launchers (each enqueues on `s`, returns hipGetLastError) ------
@@ -216,7 +236,66 @@ struct ForwardArgs {
   Profiler* prof;
   double* s_out;           // feature export (may be null)
   double* v_out;
+  void* save;              // per-layer activations for the reverse pass (may be null)
 };
+
+// The activations a forward run keeps for the reverse pass (storage type,
+// element size es).  Layer l: S(l) = s before the message [N][F], V(l) = v
+// [N][3F], H(l) = phi(s) [N][3F], Smid(l), Vmid(l) = s and v after the
+// message; S(L), V(L) = the final s and v.
+struct SaveLayout {
+  char* base;
+  size_t N, F, es;
+  __host__ __device__ SaveLayout(void* b, size_t n, size_t f, int, size_t e)
+      : base((char*)b), N(n), F(f), es(e) {}
+  __host__ __device__ void* S(int l) const { return base + (size_t)l * 11 * N * F * es; }
+  __host__ __device__ void* V(int l) const { return (char*)S(l) + N * F * es; }
+  __host__ __device__ void* H(int l) const { return (char*)V(l) + 3 * N * F * es; }
+  __host__ __device__ void* Smid(int l) const { return (char*)H(l) + 3 * N * F * es; }
+  __host__ __device__ void* Vmid(int l) const { return (char*)Smid(l) + N * F * es; }
+  static size_t bytes(size_t N, size_t F, int L, size_t es) { return ((size_t)L * 11 + 4) * N * F * es; }
+};
+
+// Atoms grouped by head (the heads kernels' counting sort): per-head counts
+// and offsets, then tiles of atoms of one head.
+constexpr int HEADS_MAX = 64;
+struct HeadPlan {
+  int32_t count[HEADS_MAX];   // valid atoms per head
+  int32_t start[HEADS_MAX];   // first slot of the head in the atom order
+  int32_t cursor[HEADS_MAX];  // scatter cursor
+  int32_t n_tiles;
+};
+struct HeadTile {
+  int32_t head, begin, end, pad;   // slots [begin, end) of the atom order
+};
+
+// Reverse pass (FP64 / FP32): forces -dE/dx from a forward run with a save
+// area.  Gradient buffers hold the accumulation type.
+struct BackwardArgs {
+  const painn_model* m;
+  const PrecModel* pm;
+  const painn_graph* g;
+  const int32_t* dataset_id;
+  void* save;               // the forward's save area
+  const void* basis;        // [E + 16][kcols] the forward's basis rows
+  const void* einfo;        // [E][4] rhat, sender index
+  void* dbasis;             // [E + 16][kcols] their derivatives d/dd
+  const void* head_plan;    // the forward's grouping of atoms by head
+  const void* head_tiles;
+  const int32_t* head_order;
+  void* gs;  void* gv;      // dE/ds [N][F], dE/dv [N][3F] at a layer boundary
+  void* gs2; void* gv2;     // the same after a layer's message
+  void* gh;                 // dE/dh [N][3F]
+  void* scratch;            // per-atom intermediates [N][scratch_w]
+  int scratch_w;
+  void* eg;                 // [E][NW][4] per-edge partials dE/dd, dE/drhat
+  double* gr;               // [E][3] dE/dr per edge
+  double* forces;           // [N][3] output
+  Profiler* prof;
+};
+hipError_t launch_backward(hipStream_t s, int prec, BackwardArgs& a);
+// the sender-grouped edge list of a graph
+hipError_t launch_transpose(hipStream_t s, Profiler* p, painn_graph* g);
 size_t forward_workspace_bytes(int prec, int N, long long E, int F, int kcols, int B, int H,
                                int S, bool blend);
 hipError_t launch_forward(hipStream_t s, int prec, ForwardArgs& a);

@@ -454,7 +454,8 @@ struct Profiler {
 static const char* kc_name(int kc) {
   static const char* names[KC_COUNT] = {"graph_prep", "graph_count", "graph_scan", "graph_fill",
                                         "embed", "phi", "edge_prep", "message", "update", "heads",
-                                        "energy", "export"};
+                                        "energy", "export", "transpose", "bwd_heads", "bwd_update",
+                                        "bwd_message", "bwd_phi", "force"};
   return names[kc];
 }
 
@@ -550,6 +551,7 @@ painn_status painn_destroy(painn_ctx* ctx) {
   (void)hipSetDevice(ctx->device);
   (void)hipStreamSynchronize(ctx->stream);
   if (ctx->ws) (void)hipFree(ctx->ws);
+  if (ctx->bws) (void)hipFree(ctx->bws);
   if (ctx->h_status) (void)hipHostFree(ctx->h_status);
   prof_free(ctx->prof);
   delete ctx;
@@ -622,7 +624,8 @@ painn_status painn_graph_free(painn_graph* g) {
   void* bufs[] = {g->row_ptr, g->counts, g->col, g->shift, g->recv, g->pos, g->species, g->atom_struct,
                   g->cell, g->sinfo, g->struct_ptr, g->scan_tmp, g->d_status, g->grid, g->bin_of,
                   g->wrap, g->bin_atoms, g->bin_count, g->bin_start, g->bin_scan_tmp,
-                  g->counts_cap, g->row_ptr_full, g->col_full, g->shift_full, g->recv_full};
+                  g->counts_cap, g->row_ptr_full, g->col_full, g->shift_full, g->recv_full,
+                  g->t_ptr, g->t_edge, g->t_count};
   for (void* p : bufs)
     if (p) (void)hipFree(p);
   delete g;
@@ -666,6 +669,7 @@ painn_status painn_build_graph_capped(painn_ctx* ctx, int32_t B, int32_t N, cons
   g->N = N;
   g->cutoff = cutoff;
   g->any_pbc = pbc != nullptr;
+  g->t_valid = false;
   hipError_t e = hipSuccess;
   size_t capa = g->cap_atoms, caps = g->cap_struct, capsc = g->cap_scan;
   // per-atom buffers share one capacity
@@ -831,7 +835,8 @@ painn_status painn_graph_csr(const painn_graph* g, int64_t* n_edges, int32_t* n_
 static painn_status run_forward(painn_ctx* ctx, const painn_model* model, const painn_graph* g,
                                 const int32_t* dataset_id, painn_precision prec, int stop_layer,
                                 double* energies, double* s_out, double* v_out, bool blend = false,
-                                double skip = 0.0, double* weights_out = nullptr) {
+                                double skip = 0.0, double* weights_out = nullptr, void* save = nullptr,
+                                ForwardArgs* keep = nullptr) {
   if (!ctx) return PAINN_E_ARG;
   ctx->err.clear();
   if (!model || !g) return fail(ctx, PAINN_E_ARG, "null model or graph");
@@ -875,6 +880,7 @@ static painn_status run_forward(painn_ctx* ctx, const painn_model* model, const 
   a.prof = ctx->prof;
   a.s_out = s_out;
   a.v_out = v_out;
+  a.save = save;
   // carve the workspace
   const size_t eb = elem_bytes(prec), ab = acc_bytes(prec);
   const size_t N = g->N, F = m->hp.F;
@@ -901,12 +907,210 @@ static painn_status run_forward(painn_ctx* ctx, const painn_model* model, const 
     a.hw = p; p += al((size_t)g->B * H * ab);
     a.eh = p; p += al(N * H * ab);
   }
+  if (keep) *keep = a;
   if (g->B == 0 && !s_out) return PAINN_OK;
   (void)hipGetLastError();   // do not report an error left by earlier, unrelated calls
   hipError_t e = launch_forward(ctx->stream, prec, a);
   if (e != hipSuccess) {
     (void)hipGetLastError();  // leave no sticky error for the caller's next HIP call
     return hip_fail(ctx, e, "forward launch");
+  }
+  return PAINN_OK;
+}
+
+// Reverse-pass workspace: save area, gradients dE/ds, dE/dv (two of each),
+// dE/dh, basis derivative rows, per-edge partials (one slot per wave of 64
+// channels), per-atom scratch, per-edge dE/dr.
+static int forces_scratch_width(const Hyper& hp) {
+  int zw = 0;
+  const int nl = (int)(hp.shared_dims.size() + hp.branch_dims.size());
+  for (int m = 0; m + 1 < nl; ++m)
+    zw += pad32(m < (int)hp.shared_dims.size() ? hp.shared_dims[m]
+                                               : hp.branch_dims[m - hp.shared_dims.size()]);
+  return zw > 12 * hp.F ? zw : 12 * hp.F;
+}
+
+static size_t forces_workspace_bytes(int prec, const Hyper& hp, int N, long long E, int kcols) {
+  const size_t eb = elem_bytes(prec), ab = acc_bytes(prec), n = (size_t)N, F = hp.F;
+  auto al = [](size_t x) { return (x + 255) & ~(size_t)255; };
+  return al(SaveLayout::bytes(n, F, hp.L, eb)) + 2 * al(n * F * ab) + 3 * al(n * 3 * F * ab) +
+         al(((size_t)E + 16) * kcols * eb) + al((size_t)E * (F / 64) * 4 * ab) +
+         al(n * forces_scratch_width(hp) * ab) + al((size_t)E * 3 * sizeof(double));
+}
+
+// Transposed layers for the reverse pass (from the FP64 master weights).
+static hipError_t pack_transposed(PrecModel* pm, int prec, const double* W, int dout, int din, DenseDev* out) {
+  std::vector<double> t((size_t)dout * din);
+  for (int o = 0; o < dout; ++o)
+    for (int k = 0; k < din; ++k) t[(size_t)k * dout + o] = W[(size_t)o * din + k];
+  return pack_dense(pm, prec, t.data(), nullptr, din, dout, out);
+}
+
+static painn_status build_prec_T(painn_model* m, PrecModel* pm) {
+  const Hyper& hp = m->hp;
+  const int F = hp.F, prec = pm->prec;
+  const double* M = m->master.data();
+  auto arr = [&](size_t i) { return M + m->offsets[i]; };
+  hipError_t e = hipSuccess;
+  for (int l = 0; l < hp.L && e == hipSuccess; ++l) {
+    const size_t base = 1 + (size_t)A_PER_LAYER * l;
+    LayerDev& L = pm->layers[l];
+    e = pack_transposed(pm, prec, arr(base + A_PHI_W1), F, F, &L.phi1T);
+    if (e == hipSuccess) e = pack_transposed(pm, prec, arr(base + A_PHI_W2), 3 * F, F, &L.phi2T);
+    if (e == hipSuccess) {
+      // [U^T | V^T]: row o, column k < F -> U[k][o], column F + k -> V[k][o]
+      std::vector<double> t((size_t)F * 2 * F);
+      for (int o = 0; o < F; ++o)
+        for (int k = 0; k < F; ++k) {
+          t[(size_t)o * 2 * F + k] = arr(base + A_U)[(size_t)k * F + o];
+          t[(size_t)o * 2 * F + F + k] = arr(base + A_V)[(size_t)k * F + o];
+        }
+      e = pack_dense(pm, prec, t.data(), nullptr, F, 2 * F, &L.uvT);
+    }
+    if (e == hipSuccess) e = pack_transposed(pm, prec, arr(base + A_UPD_W1), F, 2 * F, &L.upd1T);
+    if (e == hipSuccess) e = pack_transposed(pm, prec, arr(base + A_UPD_W2), 3 * F, F, &L.upd2T);
+  }
+  size_t idx = 1 + (size_t)A_PER_LAYER * hp.L;
+  int din = F;
+  pm->sharedT.clear();
+  for (size_t mm = 0; mm < hp.shared_dims.size() && e == hipSuccess; ++mm) {
+    DenseDev d;
+    e = pack_transposed(pm, prec, arr(idx), hp.shared_dims[mm], din, &d);
+    pm->sharedT.push_back(d);
+    din = hp.shared_dims[mm];
+    idx += 2;
+  }
+  pm->branchT.assign(hp.n_heads, {});
+  const size_t nb = hp.branch_dims.size();
+  for (int h = 0; h < hp.n_heads && e == hipSuccess; ++h) {
+    int di = din;
+    for (size_t mm = 0; mm < nb && e == hipSuccess; ++mm) {
+      DenseDev d;
+      if (mm + 1 < nb) e = pack_transposed(pm, prec, arr(idx), hp.branch_dims[mm], di, &d);
+      pm->branchT[h].push_back(d);   // the output layer has none
+      di = hp.branch_dims[mm];
+      idx += 2;
+    }
+  }
+  if (e == hipSuccess) {
+    std::vector<unsigned char> tab((size_t)hp.n_heads * nb * 2 * sizeof(void*), 0);
+    void** tp = (void**)tab.data();
+    for (int h = 0; h < hp.n_heads; ++h)
+      for (size_t mm = 0; mm < nb; ++mm) tp[(h * nb + mm) * 2] = pm->branchT[h][mm].w;
+    e = upload(pm, tab, &pm->head_tableT);
+  }
+  if (e != hipSuccess) return hip_fail(m->ctx, e, "uploading transposed weights");
+  pm->has_T = true;
+  return PAINN_OK;
+}
+
+painn_status painn_forces(painn_ctx* ctx, const painn_model* model, const painn_graph* graph,
+                          const int32_t* dataset_id, painn_precision precision, double* energies,
+                          double* forces) {
+  if (!ctx) return PAINN_E_ARG;
+  ctx->err.clear();
+  if (!model || !graph) return fail(ctx, PAINN_E_ARG, "null model or graph");
+  if (graph->B > 0 && !energies) return fail(ctx, PAINN_E_ARG, "energies is null");
+  if (graph->N > 0 && !forces) return fail(ctx, PAINN_E_ARG, "forces is null");
+  if (precision == PAINN_BF16) return fail(ctx, PAINN_E_UNSUPPORTED, "forces run in FP64 or FP32");
+  if (precision != PAINN_FP64 && precision != PAINN_FP32) return fail(ctx, PAINN_E_ARG, "unknown precision");
+  const Hyper& hp = model->hp;
+  const size_t eb = elem_bytes(precision);
+  if ((size_t)16 * (4 * hp.F + 2) * eb > 160 * 1024)
+    return fail(ctx, PAINN_E_UNSUPPORTED, "feature width too large for the FP64 reverse pass");
+  {
+    int wmax = hp.F;
+    for (int d : hp.shared_dims) wmax = wmax > pad32(d) ? wmax : pad32(d);
+    for (size_t mm = 0; mm + 1 < hp.branch_dims.size(); ++mm)
+      wmax = wmax > pad32(hp.branch_dims[mm]) ? wmax : pad32(hp.branch_dims[mm]);
+    if ((size_t)2 * 16 * (wmax + 1) * eb > 150 * 1024)
+      return fail(ctx, PAINN_E_UNSUPPORTED, "head layers too wide for the reverse heads kernel");
+  }
+  if (graph->B == 0) return PAINN_OK;
+  (void)hipSetDevice(ctx->device);
+  painn_graph* g = const_cast<painn_graph*>(graph);
+  painn_model* m = const_cast<painn_model*>(model);
+  // every check of the forward, and the precision's packed weights
+  if (g->ctx != ctx || m->ctx != ctx) return fail(ctx, PAINN_E_ARG, "model or graph from another context");
+  if (g->cutoff != hp.cutoff) return fail(ctx, PAINN_E_ARG, "graph cutoff differs from the model's cutoff");
+  if (g->max_neighbors != hp.max_neighbors)
+    return fail(ctx, PAINN_E_ARG, "graph neighbour cap differs from the model's");
+  if (!m->prec[precision]) {
+    painn_status st = build_prec(m, precision, &m->prec[precision]);
+    if (st != PAINN_OK) return st;
+  }
+  PrecModel* pm = m->prec[precision];
+  if (!pm->has_T) {
+    painn_status st = build_prec_T(m, pm);
+    if (st != PAINN_OK) return st;
+  }
+  // edges grouped by sender
+  if (!g->t_valid) {
+    hipError_t e = ensure(&g->t_ptr, &g->cap_t_atoms, (size_t)g->N + 1);
+    size_t cc = g->cap_t_atoms;
+    if (e == hipSuccess) e = ensure(&g->t_count, &cc, (size_t)g->N + 1);
+    if (e == hipSuccess) e = ensure(&g->t_edge, &g->cap_t_edges, (size_t)g->E + 1);
+    if (e != hipSuccess) {
+      (void)hipGetLastError();
+      g->cap_t_atoms = g->cap_t_edges = 0;
+      return hip_fail(ctx, e, "edge transpose allocation");
+    }
+    e = launch_transpose(ctx->stream, ctx->prof, g);
+    if (e != hipSuccess) return hip_fail(ctx, e, "edge transpose");
+    g->t_valid = true;
+  }
+  const int kcols = pm->layers[0].filt_mma.din_p;
+  const size_t need = forces_workspace_bytes(precision, hp, g->N, g->E, kcols);
+  if (need > ctx->bws_bytes) {
+    if (ctx->bws) {
+      (void)hipStreamSynchronize(ctx->stream);
+      (void)hipFree(ctx->bws);
+      ctx->bws = nullptr;
+      ctx->bws_bytes = 0;
+    }
+    const size_t want = need + need / 8;
+    hipError_t e = hipMalloc(&ctx->bws, want);
+    if (e != hipSuccess) {
+      (void)hipGetLastError();
+      return fail(ctx, PAINN_E_OOM, "reverse-pass workspace allocation failed");
+    }
+    ctx->bws_bytes = want;
+  }
+  const size_t N = g->N, F = hp.F, ab = acc_bytes(precision);
+  auto al = [](size_t x) { return (x + 255) & ~(size_t)255; };
+  char* p = (char*)ctx->bws;
+  BackwardArgs b{};
+  b.save = p; p += al(SaveLayout::bytes(N, F, hp.L, eb));
+  b.gs = p; p += al(N * F * ab);
+  b.gs2 = p; p += al(N * F * ab);
+  b.gv = p; p += al(N * 3 * F * ab);
+  b.gv2 = p; p += al(N * 3 * F * ab);
+  b.gh = p; p += al(N * 3 * F * ab);
+  b.dbasis = p; p += al(((size_t)g->E + 16) * kcols * eb);
+  b.eg = p; p += al((size_t)g->E * (F / 64) * 4 * ab);
+  b.scratch_w = forces_scratch_width(hp);
+  b.scratch = p; p += al(N * b.scratch_w * ab);
+  b.gr = (double*)p;
+  ForwardArgs fa{};
+  painn_status st = run_forward(ctx, model, graph, dataset_id, precision, hp.L - 1, energies, nullptr, nullptr,
+                                false, 0.0, nullptr, b.save, &fa);
+  if (st != PAINN_OK) return st;
+  b.m = m;
+  b.pm = pm;
+  b.g = g;
+  b.dataset_id = dataset_id;
+  b.basis = fa.basis;
+  b.einfo = fa.einfo;
+  b.head_plan = fa.head_plan;
+  b.head_tiles = fa.head_tiles;
+  b.head_order = fa.head_order;
+  b.forces = forces;
+  b.prof = ctx->prof;
+  (void)hipGetLastError();
+  hipError_t e = launch_backward(ctx->stream, precision, b);
+  if (e != hipSuccess) {
+    (void)hipGetLastError();
+    return hip_fail(ctx, e, "reverse pass launch");
   }
   return PAINN_OK;
 }

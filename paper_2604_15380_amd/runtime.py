@@ -143,6 +143,21 @@ class Runtime:
                               weights.data_ptr() if weights is not None and weights.numel() else None)
         return out
 
+    def forces(self, model: Model, graph: Graph, precision="fp32", dataset_id=None, energies=None,
+               forces=None):
+        """Energies [B] and forces -dE/dx [N, 3] (float64) by the reverse pass."""
+        import torch
+        prec = B.PRECISIONS[precision] if isinstance(precision, str) else precision
+        if energies is None:
+            energies = torch.empty(graph.n_struct, dtype=torch.float64, device=self.device)
+        if forces is None:
+            forces = torch.empty((graph.n_atoms, 3), dtype=torch.float64, device=self.device)
+        ds = dataset_id.data_ptr() if dataset_id is not None and dataset_id.numel() else None
+        B.painn_forces(self.ctx, model.handle, graph.handle, ds, prec,
+                       energies.data_ptr() if energies.numel() else None,
+                       forces.data_ptr() if forces.numel() else None)
+        return energies, forces
+
     def features(self, model: Model, graph: Graph, layer: int, precision="fp64"):
         import torch
         prec = B.PRECISIONS[precision] if isinstance(precision, str) else precision

@@ -1,0 +1,177 @@
+"""GPU forces (the reverse pass, painn_forces) vs the FP64 oracle's forces.
+
+Acceptance per structure: max |F - F_ref| over its atoms and components
+<= tol * max |F_ref| of the structure (FORCE_TOL per precision)."""
+import sys
+
+import numpy as np
+import pytest
+
+import synth
+from oracle.forces import structure_forces
+from oracle.painn import RBF_BESSEL
+
+pytestmark = pytest.mark.gpu
+
+FORCE_TOL = {"fp64": 1e-9, "fp32": 5e-4}
+
+
+def say(msg):
+    print(msg, flush=True)
+    sys.stdout.flush()
+
+
+@pytest.fixture(scope="module")
+def rt():
+    from paper_2604_15380_amd import Runtime
+    r = Runtime(0)
+    yield r
+    r.close()
+
+
+def oracle(b, hp, W, idx=None):
+    idx = range(b.n_struct) if idx is None else idx
+    out = []
+    for k in idx:
+        pos, z, cell, pbc, ds = b.structure(int(k))
+        out.append(structure_forces(pos, z, cell, pbc, ds if hp.n_heads > 1 else 0, hp, W))
+    return out
+
+
+def check_forces(Fg, b, ref, idx, tol, label):
+    worst = 0.0
+    for k, o in zip(idx, ref):
+        lo, hi = int(b.struct_ptr[k]), int(b.struct_ptr[k + 1])
+        Fk = Fg[lo:hi]
+        assert np.all(np.isfinite(Fk)), f"{label}: non-finite forces in structure {k}"
+        scale = np.abs(o["F"]).max() if hi > lo else 0.0
+        err = np.abs(Fk - o["F"]).max() if hi > lo else 0.0
+        if scale == 0.0:
+            assert err == 0.0, f"{label}: structure {k} has no force but got {err:.3e}"
+            continue
+        worst = max(worst, err / scale)
+        assert err <= tol * scale, f"{label}: structure {k}: max|dF| = {err:.3e} > {tol:.0e} * {scale:.3e}"
+    say(f"{label}: worst max|dF|/max|F| = {worst:.3e}")
+    return worst
+
+
+def run_case(rt, hp, W, b, precision, label, cap=0, ds=False):
+    import torch
+    m = rt.load_model(synth.weight_file_bytes(hp, W))
+    inp = rt.upload_batch(b)
+    g = rt.build_graph(inp, hp.cutoff, max_neighbors=cap)
+    dsid = inp["dataset_id"] if ds else None
+    E, Fo = rt.forces(m, g, precision, dataset_id=dsid)
+    E0 = rt.forward(m, g, precision, dataset_id=dsid)
+    torch.cuda.synchronize()
+    E, Fo, E0 = E.cpu().numpy(), Fo.cpu().numpy(), E0.cpu().numpy()
+    assert np.array_equal(E, E0), f"{label}: energies of the forces pass differ from the forward's"
+    ref = oracle(b, hp, W)
+    check_forces(Fo, b, ref, list(range(b.n_struct)), FORCE_TOL[precision], label)
+    g.free()
+    m.free()
+
+
+@pytest.mark.parametrize("precision", ["fp64", "fp32"])
+def test_molecules(rt, precision):
+    say(f"molecules, {precision}")
+    hp = synth.HyperParams(F=64, K=20, L=3, n_species=10, n_heads=1, cutoff=5.0,
+                           shared_dims=[], branch_dims=[32, 1])
+    W = synth.make_weights(hp, 3101)
+    b = synth.make_batch("molecules_4096", 0, 40)
+    run_case(rt, hp, W, b, precision, f"molecules {precision}")
+
+
+@pytest.mark.parametrize("precision", ["fp64", "fp32"])
+def test_periodic(rt, precision):
+    say(f"periodic cells, {precision}")
+    hp = synth.HyperParams(F=64, K=12, L=2, n_species=85, n_heads=1, cutoff=5.0,
+                           shared_dims=[], branch_dims=[32, 1])
+    W = synth.make_weights(hp, 3102)
+    b = synth.make_batch("bulk_1024", 0, 3)
+    run_case(rt, hp, W, b, precision, f"periodic {precision}")
+
+
+@pytest.mark.parametrize("precision", ["fp64", "fp32"])
+def test_bessel_capped_dataset_heads(rt, precision):
+    """The lead model's ingredients: Bessel basis, neighbour cap, shared head
+    layers and per-dataset branches."""
+    say(f"Bessel + cap + dataset heads, {precision}")
+    hp = synth.HyperParams(F=64, K=4, L=2, n_species=85, n_heads=4, cutoff=5.0,
+                           shared_dims=[24, 24], branch_dims=[40, 40, 1], rbf_type=RBF_BESSEL,
+                           max_neighbors=8)
+    W = synth.make_weights(hp, 3103)
+    b = synth.make_batch("screening", 0, 24)
+    b.dataset_id = b.dataset_id % hp.n_heads
+    run_case(rt, hp, W, b, precision, f"lead ingredients {precision}", cap=8, ds=True)
+
+
+@pytest.mark.parametrize("F", [100, 256])
+def test_feature_widths(rt, F):
+    say(f"F = {F}, fp32")
+    hp = synth.HyperParams(F=F, K=8, L=2, n_species=10, n_heads=1, cutoff=5.0,
+                           shared_dims=[], branch_dims=[24, 1])
+    W = synth.make_weights(hp, 3200 + F)
+    b = synth.make_batch("molecules_4096", 0, 12)
+    run_case(rt, hp, W, b, "fp32", f"F={F} fp32")
+
+
+def test_single_linear_head_and_lone_atoms(rt):
+    """A one-layer head (dE/ds is its weight row) and structures whose atoms
+    have no neighbour (zero force)."""
+    import torch
+    hp = synth.HyperParams(F=64, K=6, L=2, n_species=4, n_heads=1, cutoff=2.0,
+                           shared_dims=[], branch_dims=[1])
+    W = synth.make_weights(hp, 3300)
+    structs = [
+        (np.array([[0.0, 0, 0]]), np.array([1]), np.zeros((3, 3)), np.zeros(3, np.uint8), 0),
+        (np.array([[0.0, 0, 0], [9.0, 0, 0]]), np.array([1, 2]), np.zeros((3, 3)), np.zeros(3, np.uint8), 0),
+        (np.array([[0.0, 0, 0], [1.1, 0.3, 0.2], [0.2, 1.4, -0.3]]), np.array([0, 3, 2]), np.zeros((3, 3)),
+         np.zeros(3, np.uint8), 0),
+    ]
+    b = synth.concat(structs)
+    m = rt.load_model(synth.weight_file_bytes(hp, W))
+    g = rt.build_graph(rt.upload_batch(b), hp.cutoff)
+    for precision in ["fp64", "fp32"]:
+        E, Fo = rt.forces(m, g, precision)
+        torch.cuda.synchronize()
+        Fo = Fo.cpu().numpy()
+        assert np.all(Fo[:3] == 0.0)
+        ref = oracle(b, hp, W)
+        check_forces(Fo, b, ref, range(b.n_struct), FORCE_TOL[precision], f"lone atoms {precision}")
+    g.free()
+    m.free()
+
+
+def test_errors(rt):
+    from paper_2604_15380_amd import PainnError
+    hp = synth.HyperParams(F=64, K=6, L=1, n_species=10, n_heads=1, cutoff=5.0,
+                           shared_dims=[], branch_dims=[8, 1])
+    m = rt.load_model(synth.weight_file_bytes(hp, synth.make_weights(hp, 3400)))
+    g = rt.build_graph(rt.upload_batch(synth.make_batch("molecules_4096", 0, 2)), hp.cutoff)
+    with pytest.raises(PainnError, match="UNSUPPORTED"):
+        rt.forces(m, g, "bf16")
+    g.free()
+    m.free()
+
+
+def test_full_size_molecules_sampled(rt):
+    """molecules_4096 (4096 molecules, F = 128, L = 4, K = 20) at FP32 in one
+    call, as the benchmark runs it; 12 sampled structures vs the oracle."""
+    import torch
+    say("molecules_4096 full batch, fp32, forces")
+    hp, W = synth.workload_weights("molecules_4096")
+    b = synth.make_batch("molecules_4096")
+    m = rt.load_model(synth.weight_file_bytes(hp, W))
+    g = rt.build_graph(rt.upload_batch(b), hp.cutoff)
+    E, Fo = rt.forces(m, g, "fp32")
+    E0 = rt.forward(m, g, "fp32")
+    torch.cuda.synchronize()
+    Fo = Fo.cpu().numpy()
+    assert np.array_equal(E.cpu().numpy(), E0.cpu().numpy())
+    assert np.all(np.isfinite(Fo))
+    idx = [int(k) for k in np.random.default_rng(5).choice(b.n_struct, 12, replace=False)] + [0, b.n_struct - 1]
+    ref = oracle(b, hp, W, idx)
+    check_forces(Fo, b, ref, idx, FORCE_TOL["fp32"], "molecules_4096 fp32")
+    g.free()
+    m.free()
