@@ -20,6 +20,7 @@ ROOT = os.path.dirname(os.path.abspath(__file__))
 sys.path.insert(0, ROOT)
 
 METRIC = "PaiNN forward structures/s and edge-messages/s on 1 MI355X (FP64/FP32/BF16)"
+METRIC_FORCES = "PaiNN energy+forces structures/s on 1 MI355X (FP64/FP32)"
 # MI355X published peaks (dense), TFLOP/s
 PEAK = {
     "alu": {"fp64": 78.6, "fp32": 157.3, "bf16": 157.3},     # vector ALU (BF16 mode computes in FP32)
@@ -30,7 +31,7 @@ DTYPE = {"fp64": "f64", "fp32": "f32", "bf16": "bf16"}
 ELEM = {"fp64": 8, "fp32": 4, "bf16": 2}
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "traffic.json")
 KERNEL_SOURCES = ["paper_2604_15380_amd/csrc/forward.hip", "paper_2604_15380_amd/csrc/mfma.h",
-                  "paper_2604_15380_amd/csrc/neighbors.hip"]
+                  "paper_2604_15380_amd/csrc/neighbors.hip", "paper_2604_15380_amd/csrc/backward.hip"]
 
 
 def log(msg):
@@ -57,6 +58,14 @@ def kernel_work(kernel: str, hp, N: int, E: int, prec: str, head_entries: int | 
     phi:     per atom 8 F^2.
     heads:   per (atom, head) entry the shared and branch MLP flops (one entry
              per atom, or every kept head of the atom's structure when blended).
+    Reverse pass (forces):
+    bwd_message: per edge 12KF (the filter and its d-derivative) + 36F
+             (elementwise terms and the per-edge sums over channels); minimum
+             HBM bytes: per atom h, v (6F) and g_s', g_v' (4F) read, g_h, g_v
+             (6F) written, plus 8 bytes of CSR per edge.
+    bwd_update: per atom 44 F^2 (U/V and the gate MLP recomputed, 22F^2; the
+             transposed products W2a^T, W1a^T, [U^T|V^T], 22F^2).
+    bwd_phi: per atom 10 F^2 (W1 s recomputed, W2^T, W1^T).
     """
     F, K, L = hp.F, hp.K, hp.L
     b = ELEM[prec]
@@ -67,6 +76,15 @@ def kernel_work(kernel: str, hp, N: int, E: int, prec: str, head_entries: int | 
         return "mfma", fl, N * (8.0 * F + 3.0 * F * (L - 1) / L) * b
     if kernel == "phi":
         return "mfma", N * 8.0 * F * F, N * 4.0 * F * b
+    if kernel == "bwd_message":
+        ab = 8 if prec == "fp64" else 4
+        return "alu", E * (12.0 * K * F + 36.0 * F), N * (6.0 * F * b + 10.0 * F * ab) + 8.0 * E
+    if kernel == "bwd_update":
+        ab = 8 if prec == "fp64" else 4
+        return "mfma", N * 44.0 * F * F, N * (4.0 * F * b + 8.0 * F * ab)
+    if kernel == "bwd_phi":
+        ab = 8 if prec == "fp64" else 4
+        return "mfma", N * 10.0 * F * F, N * (F * b + 6.0 * F * ab)
     if kernel == "heads":
         dims = [F] + list(hp.shared_dims) + list(hp.branch_dims)
         n = N if head_entries is None else head_entries
@@ -85,10 +103,10 @@ def load_traffic(key: str, digest: str, launches_kernel: str):
     return t.get("bytes_per_launch")
 
 
-def cpu_baseline(name: str, batch, sample: int, blend_skip=None):
+def cpu_baseline(name: str, batch, sample: int, blend_skip=None, forces=False):
     """Time the oracle (as it stands) on the first `sample` structures, one
     single-threaded worker per available core (blended heads when blend_skip
-    is given)."""
+    is given; energies and forces when `forces`)."""
     os.environ.setdefault("OMP_NUM_THREADS", "1")
     from concurrent.futures import ProcessPoolExecutor
     sys.path.insert(0, os.path.join(ROOT, "tests"))
@@ -97,11 +115,15 @@ def cpu_baseline(name: str, batch, sample: int, blend_skip=None):
     cores = min(cores, 16)
     idx = list(range(min(sample, batch.n_struct)))
     t0 = time.perf_counter()
-    helpers.oracle_energies(name, batch, idx, workers=cores, blend_skip=blend_skip)
+    if forces:
+        helpers.oracle_forces(name, batch, idx, workers=cores)
+    else:
+        helpers.oracle_energies(name, batch, idx, workers=cores, blend_skip=blend_skip)
     dt = time.perf_counter() - t0
+    what = "FP64 NumPy PaiNN energies and reverse-pass forces" if forces else "FP64 NumPy PaiNN"
     return dict(value=len(idx) / dt, unit="structures/s", cores=cores, kind="oracle",
                 sample=f"first {len(idx)} structures of the {name} batch, oracle (brute-force graph + "
-                       f"FP64 NumPy PaiNN) in a pool of {cores} single-threaded processes, {dt:.1f} s wall")
+                       f"{what}) in a pool of {cores} single-threaded processes, {dt:.1f} s wall")
 
 
 def main():
@@ -116,7 +138,10 @@ def main():
                     help="blend every head with the model's branch-weighting MLP (screening model)")
     ap.add_argument("--skip", type=float, default=0.0,
                     help="with --blend: leave out heads whose weight is below this threshold")
-    ap.add_argument("--cpu-sample", type=int, default=768)
+    ap.add_argument("--forces", action="store_true",
+                    help="energies and forces (painn_forces) instead of the energy forward")
+    ap.add_argument("--cpu-sample", type=int, default=None,
+                    help="structures the CPU oracle baseline times (default 768; 256 with --forces)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-profile", action="store_true", help="time without per-kernel events")
     ap.add_argument("--copy-probe", type=int, default=0, metavar="MIB",
@@ -162,10 +187,16 @@ def main():
     if args.blend and hp.blend_dims is None:
         print(f"--blend needs a model with a branch-weighting MLP ({name} has none)", file=sys.stderr)
         sys.exit(2)
+    if args.forces and (args.blend or prec == "bf16"):
+        print("--forces runs the dataset-id heads in FP64 or FP32", file=sys.stderr)
+        sys.exit(2)
+    fout = torch.empty((batch.n_atoms, 3), dtype=torch.float64, device=rt.device)
 
     def step():
         rt.build_graph(inp, hp.cutoff, graph=graph, max_neighbors=hp.max_neighbors)
-        if args.blend:
+        if args.forces:
+            rt.forces(model, graph, prec, dataset_id=ds, energies=out, forces=fout)
+        elif args.blend:
             rt.forward_blend(model, graph, prec, skip=args.skip, out=out)
         else:
             rt.forward(model, graph, prec, dataset_id=ds, out=out)
@@ -202,9 +233,11 @@ def main():
     value = B * K / T
     log(f"{1e3 * T / K:.3f} ms/step, {value:.1f} structures/s")
 
-    # PCIe-inclusive rate: pinned host inputs copied in, energies copied out
+    # PCIe-inclusive rate: pinned host inputs copied in, energies (and
+    # forces) copied out
     host = {k: v.cpu().pin_memory() for k, v in inp.items() if torch.is_tensor(v)}
     out_h = torch.empty(B, dtype=torch.float64).pin_memory()
+    fout_h = torch.empty((N, 3), dtype=torch.float64).pin_memory()
     torch.cuda.synchronize()
     t1 = time.perf_counter()
     for _ in range(K):
@@ -212,6 +245,8 @@ def main():
             inp[k].copy_(v, non_blocking=True)
         step()
         out_h.copy_(out, non_blocking=True)
+        if args.forces:
+            fout_h.copy_(fout, non_blocking=True)
     torch.cuda.synchronize()
     T_pcie = time.perf_counter() - t1
 
@@ -225,7 +260,7 @@ def main():
         avg_s = ms / launches / 1e3
         achieved = flops / avg_s / 1e12
         peak = PEAK[bound][prec]
-        traffic = load_traffic(f"{name}/{prec}", source_digest(), dom)
+        traffic = load_traffic(f"{name}/{prec}" + ("/forces" if args.forces else ""), source_digest(), dom)
         roofline = dict(kernel=dom, bound=bound, achieved=round(achieved, 3), peak=peak, unit="TFLOP/s",
                         frac=round(achieved / peak, 4), traffic=traffic,
                         avg_launch_ms=round(avg_s * 1e3, 4), launches=launches,
@@ -235,17 +270,18 @@ def main():
     cpu = None
     if not args.no_cpu_baseline:
         log("timing the CPU oracle baseline")
-        cpu = cpu_baseline(name, batch, args.cpu_sample, args.skip if args.blend else None)
+        sample = args.cpu_sample or (256 if args.forces else 768)
+        cpu = cpu_baseline(name, batch, sample, args.skip if args.blend else None, forces=args.forces)
 
     res = {
-        "metric": METRIC, "value": round(value, 2), "unit": "structures/s", "n_gpus": 1,
+        "metric": METRIC_FORCES if args.forces else METRIC, "value": round(value, 2), "unit": "structures/s", "n_gpus": 1,
         "steps": K, "warmup": args.warmup, "ms_per_step": round(1e3 * T / K, 4),
         "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
         "dtype": DTYPE[prec], "data": "synthetic",
         "config": {"workload": name, "n_struct": B, "n_atoms": N, "n_edges": E, "F": hp.F,
                    "layers": hp.L, "rbf": hp.K, "rbf_type": ["gaussian", "bessel"][hp.rbf_type],
                    "cutoff": hp.cutoff, "max_neighbors": hp.max_neighbors, "heads": hp.n_heads,
-                   "precision": prec,
+                   "precision": prec, "forces": bool(args.forces),
                    "head_mode": (f"blended, skip < {args.skip:g}" if args.blend else
                                  ("dataset id" if hp.n_heads > 1 else "single"))},
         "edges_per_s": round(E * K / T, 1),

@@ -543,19 +543,21 @@ __global__ void __launch_bounds__(64 * UB_NW) k_phi_bwd(PhiBwdArgs a) {
 }
 
 // ---------------------------------------------------------- message, back ----
-// Per sender j and channel c (lane = channel, a wave = 64 channels, waves
-// independent), over the edges e = (i <- j) whose sender is j, with the
-// receiver's g_s' and g_v' gathered:
+// Per sender j and channel c, over the edges e = (i <- j) whose sender is j
+// (the edge list grouped by sender), with the receiver's g_s' and g_v'
+// gathered:
 //   A_v = sum_c g_v'_i[c] v_j[c],  A_r = sum_c g_v'_i[c] rhat_e[c]
 //   g_h^s_j += g_s'_i w^s,  g_h^v_j += A_v w^v,  g_h^r_j += A_r w^r
 //   g_v_j[c] = g_v'_j[c] + sum_e g_v'_i[c] h^v_j w^v
-//   dE/dd_e    += sum_c (g_s'_i h^s_j w'^s + A_v h^v_j w'^v + A_r h^r_j w'^r)
-//   dE/drhat_e += sum_c g_v'_i[.] h^r_j w^r
-// with w = f_c (Wf g + bf) and w' = dw/dd formed on the matrix cores from
-// the basis rows and their derivatives (one after the other through the
-// same LDS tile; the receiver rows are gathered once for each).  The sums
-// over channels are a reduce-scatter across the wave's lanes; each wave
-// writes its own slot, so no two lanes add to one value.
+//   dE/dd_e    += sum_ch (g_s'_i h^s_j w'^s + A_v h^v_j w'^v + A_r h^r_j w'^r)
+//   dE/drhat_e += sum_ch g_v'_i[.] h^r_j w^r
+// with w = f_c (Wf g + bf) and w' = dw/dd.  For 16 edges at a time the
+// matrix cores form w and w' (the basis rows and their derivatives against
+// the same filter fragments); every lane then works in the accumulator
+// layout itself, 4 edges x one channel per feature tile, so the filter never
+// leaves the registers.  The per-edge sums over channels are a
+// reduce-scatter across the 16 lanes that share those edges, over the
+// wave's 4 feature tiles; each wave writes its own slot of every edge.
 constexpr int MB_RB = 4;   // senders per workgroup
 
 struct MsgBwdArgs {
@@ -577,22 +579,9 @@ struct MsgBwdArgs {
   void* eg;            // [E][NW][4]
 };
 
-template <class A>
-__device__ __forceinline__ A lane_bcast(A x, int lane) {
-  if constexpr (sizeof(A) == 4) {
-    return __int_as_float(__builtin_amdgcn_readlane(__float_as_int(x), lane));
-  } else {
-    const long long b = __double_as_longlong(x);
-    const int lo = __builtin_amdgcn_readlane((int)(b & 0xffffffff), lane);
-    const int hi = __builtin_amdgcn_readlane((int)(b >> 32), lane);
-    return __longlong_as_double(((long long)hi << 32) | (unsigned)lo);
-  }
-}
-
-// Sum of vals[k] over the 64 lanes, for k = lane: each step keeps the half
-// of the indices selected by one lane bit and adds the partner's copy.
+// vals[k] summed over the 16 lanes of a row group, for k = lane % 16.
 template <class A, int LEN>
-__device__ __forceinline__ void reduce_scatter(A* vals, int lane) {
+__device__ __forceinline__ void reduce_scatter16(A* vals, int lane) {
   if constexpr (LEN > 1) {
     constexpr int H = LEN / 2;
     const bool up = (lane & H) != 0;
@@ -602,150 +591,169 @@ __device__ __forceinline__ void reduce_scatter(A* vals, int lane) {
       const A give = up ? vals[k] : vals[k + H];
       vals[k] = keep + __shfl_xor(give, H);
     }
-    reduce_scatter<A, H>(vals, lane);
+    reduce_scatter16<A, H>(vals, lane);
   }
 }
 
+// Feature tiles per wave and the waves per SIMD the kernel is compiled for.
+#ifndef MB_FTW32
+#define MB_FTW32 2
+#endif
+template <class P, int F>
+constexpr int mb_ftw() { return sizeof(typename P::A) == 8 ? 1 : MB_FTW32; }
+template <class P, int F>
+constexpr int mb_wpe() { return mb_ftw<P, F>() * (int)sizeof(typename P::A) / 4 <= 1 ? 4 : 2; }
+// Waves of one feature slice (a workgroup); wide layers take several slices
+// in consecutive workgroups.
+template <class P, int F>
+constexpr int mb_nwb() {
+  constexpr int nw = F / 16 / mb_ftw<P, F>();
+  return nw <= 8 ? nw : (nw % 8 == 0 ? 8 : 6);
+}
+
 template <class P, int F, int KBM>
-__global__ void __launch_bounds__(F) k_message_bwd(MsgBwdArgs a) {
+__global__ void __launch_bounds__((64 * mb_nwb<P, F>())) __attribute__((amdgpu_waves_per_eu(mb_wpe<P, F>())))
+k_message_bwd(MsgBwdArgs a) {
   using T = typename P::T;
   using A = typename P::A;
   using C = typename P::C;
   using Fr = typename P::Fr;
-  constexpr int NW = F / 64, NFT = F / 16, WLD = 64 + 4;
+  constexpr int FTW = mb_ftw<P, F>(), NFT = F / 16, NW = NFT / FTW;
+  constexpr int NWB = mb_nwb<P, F>(), SLICES = NW / NWB;
+  static_assert(NW % NWB == 0, "feature slices");
   constexpr int kcols = KBM * P::KC;
-  __shared__ A Wt[NW][3][16 * WLD];
-  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-  const int c = 64 * wave + lane;
+  const int per_xcd = gridDim.x / 8;
+  const int lb = (blockIdx.x % 8) * per_xcd + blockIdx.x / 8;
+  const int lane = threadIdx.x & 63, wave = (lb % SLICES) * NWB + (threadIdx.x >> 6);
   const T* Wf = (const T*)a.filt.w;
   const T* h = (const T*)a.h;
   const T* vv = (const T*)a.v;
   const A* gs = (const A*)a.gs;
   const A* gv = (const A*)a.gv;
   const A* einfo = (const A*)a.einfo;
-  A* wt0 = Wt[wave][0];
-  A* wt1 = Wt[wave][1];
-  A* wt2 = Wt[wave][2];
-  const int per_xcd = gridDim.x / 8;
-  const int lb = (blockIdx.x % 8) * per_xcd + blockIdx.x / 8;
-  const int j0 = lb * MB_RB;
+  const T* basis = (const T*)a.basis;
+  const T* dbasis = (const T*)a.dbasis;
+  const int j0 = lb / SLICES * MB_RB;
   if (j0 >= a.N) return;
   const int j1 = min(a.N, j0 + MB_RB);
   const int tp_lane = a.t_ptr[j0 + min(lane, j1 - j0)];
   auto tp = [&](int j) { return __builtin_amdgcn_readlane(tp_lane, j - j0); };
-  // the filter (or its derivative) of the chunk's 16 edges at this wave's
-  // 64 channels into Wt, from the basis rows `rows`
-  auto filter = [&](const T* rows, int er) {
-    const T* gp = rows + (size_t)er * kcols + (lane >> 4) * P::KPL;
-    Fr Ga[KBM];
-#pragma unroll
-    for (int kb = 0; kb < KBM; ++kb) Ga[kb] = P::frag(gp + kb * P::KC);
-#pragma unroll
-    for (int q = 0; q < 4; ++q) {
-      C w[3];
-#pragma unroll
-      for (int part = 0; part < 3; ++part) {
-        for (int r = 0; r < 4; ++r) w[part][r] = 0;
-#pragma unroll
-        for (int kb = 0; kb < KBM; ++kb) {
-          const int ct = part * NFT + 4 * wave + q;
-          w[part] = P::mfma(Ga[kb], P::frag(Wf + ((size_t)(ct * KBM + kb) * 64 + lane) * P::KPL), w[part]);
-        }
-      }
-      const int col = 16 * q + (lane & 15);
-#pragma unroll
-      for (int r = 0; r < 4; ++r) {
-        const int row = P::row(lane, r);
-        wt0[row * WLD + col] = w[0][r];
-        wt1[row * WLD + col] = w[1][r];
-        wt2[row * WLD + col] = w[2][r];
-      }
-    }
-    __builtin_amdgcn_wave_barrier();
-    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
-    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
-  };
-  auto wave_sync = [&]() {
-    __builtin_amdgcn_wave_barrier();
-    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
-    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
-  };
   A* gh_out = (A*)a.gh;
   A* gv_out = (A*)a.gv_out;
   A* eg = (A*)a.eg;
   for (int j = j0; j < j1; ++j) {
     const int ea = tp(j), eb = tp(j + 1);
     const size_t jb = (size_t)j * 3 * F;
-    const A hs = P::ld(h[jb + c]), hv = P::ld(h[jb + F + c]), hr = P::ld(h[jb + 2 * F + c]);
-    const A v0 = P::ld(vv[jb + c]), v1 = P::ld(vv[jb + F + c]), v2 = P::ld(vv[jb + 2 * F + c]);
-    A acc_hs = 0, acc_hv = 0, acc_hr = 0, acc_v0 = 0, acc_v1 = 0, acc_v2 = 0;
+    A acc_h[FTW][3], acc_v[FTW][3];
+#pragma unroll
+    for (int q = 0; q < FTW; ++q)
+#pragma unroll
+      for (int k = 0; k < 3; ++k) acc_h[q][k] = acc_v[q][k] = 0;
     for (int c0 = ea; c0 < eb; c0 += 16) {
       const int cnt = min(16, eb - c0);
-      // edge id of row lane % 16 (past the chunk: the zero padding row E)
-      const int er = (lane & 15) < cnt ? a.t_edge[c0 + (lane & 15)] : (int)a.E;
-      // receiver and rhat of edge `lane` on lanes < cnt
-      A ex = 0, ey = 0, ez = 0;
-      int ei = 0;
-      if (lane < cnt) {
-        ex = einfo[4 * (size_t)er];
-        ey = einfo[4 * (size_t)er + 1];
-        ez = einfo[4 * (size_t)er + 2];
-        ei = a.recv[er];
-      }
-      A vals[64];
+      // A operand rows: edge of row lane % 16 (past the chunk: the zero row E)
+      const int erA = (lane & 15) < cnt ? a.t_edge[c0 + (lane & 15)] : (int)a.E;
+      Fr Ga[KBM], Gd[KBM];
+      {
+        const T* gp = basis + (size_t)erA * kcols + (lane >> 4) * P::KPL;
+        const T* dp = dbasis + (size_t)erA * kcols + (lane >> 4) * P::KPL;
 #pragma unroll
-      for (int k = 0; k < 64; ++k) vals[k] = 0;
-      // pass 1: w' -> dE/dd partials
-      filter((const T*)a.dbasis, er);
-#pragma unroll
-      for (int e = 0; e < 16; ++e) {
-        if (e < cnt) {
-          const int i = __builtin_amdgcn_readlane(ei, e);
-          const size_t ib = (size_t)i * 3 * F;
-          const A g_s = gs[(size_t)i * F + c], g0 = gv[ib + c], g1 = gv[ib + F + c], g2 = gv[ib + 2 * F + c];
-          const A rx = lane_bcast(ex, e), ry = lane_bcast(ey, e), rz = lane_bcast(ez, e);
-          const A Av = g0 * v0 + g1 * v1 + g2 * v2, Ar = g0 * rx + g1 * ry + g2 * rz;
-          vals[e] = g_s * hs * wt0[e * WLD + lane] + Av * hv * wt1[e * WLD + lane] + Ar * hr * wt2[e * WLD + lane];
+        for (int kb = 0; kb < KBM; ++kb) {
+          Ga[kb] = P::frag(gp + kb * P::KC);
+          Gd[kb] = P::frag(dp + kb * P::KC);
         }
       }
-      wave_sync();
-      // pass 2: w -> g_h, g_v and dE/drhat partials
-      filter((const T*)a.basis, er);
+      // this lane's 4 accumulator rows: edge id, receiver, rhat (rows past
+      // the chunk: receiver 0 and a zero filter, so they add nothing)
+      int er[4], ir[4];
+      A rh[4][3];
 #pragma unroll
-      for (int e = 0; e < 16; ++e) {
-        if (e < cnt) {
-          const int i = __builtin_amdgcn_readlane(ei, e);
-          const size_t ib = (size_t)i * 3 * F;
-          const A g_s = gs[(size_t)i * F + c], g0 = gv[ib + c], g1 = gv[ib + F + c], g2 = gv[ib + 2 * F + c];
-          const A rx = lane_bcast(ex, e), ry = lane_bcast(ey, e), rz = lane_bcast(ez, e);
-          const A Av = g0 * v0 + g1 * v1 + g2 * v2, Ar = g0 * rx + g1 * ry + g2 * rz;
-          const A ws = wt0[e * WLD + lane], wv = wt1[e * WLD + lane], wr = wt2[e * WLD + lane];
-          acc_hs += g_s * ws;
-          acc_hv += Av * wv;
-          acc_hr += Ar * wr;
-          const A tv = hv * wv, tr = hr * wr;
-          acc_v0 += g0 * tv;
-          acc_v1 += g1 * tv;
-          acc_v2 += g2 * tv;
-          vals[16 + e] = g0 * tr;
-          vals[32 + e] = g1 * tr;
-          vals[48 + e] = g2 * tr;
+      for (int i = 0; i < 4; ++i) {
+        const int row = P::row(lane, i);
+        er[i] = row < cnt ? a.t_edge[c0 + row] : -1;
+        ir[i] = 0;
+        rh[i][0] = rh[i][1] = rh[i][2] = 0;
+        if (er[i] >= 0) {
+          ir[i] = a.recv[er[i]];
+          rh[i][0] = einfo[4 * (size_t)er[i]];
+          rh[i][1] = einfo[4 * (size_t)er[i] + 1];
+          rh[i][2] = einfo[4 * (size_t)er[i] + 2];
         }
       }
-      wave_sync();
-      // lane l: the wave's total of value l / 16 for edge l % 16
-      reduce_scatter<A, 64>(vals, lane);
-      if ((lane & 15) < cnt) {
-        A* o = eg + ((size_t)er * NW + wave) * 4 + (lane >> 4);
-        *o += vals[0];
+      // the filter fragments stream from the caches chunk by chunk (an
+      // opaque copy of the pointer keeps them from being hoisted out of the
+      // loops into registers for the whole kernel)
+      const T* Wc = Wf;
+      asm volatile("" : "+s"(Wc));
+      // per-edge partial sums: [dE/dd, dE/drhat x, y, z] x 4 rows
+      A vals[16];
+#pragma unroll
+      for (int k = 0; k < 16; ++k) vals[k] = 0;
+#pragma unroll
+      for (int q = 0; q < FTW; ++q) {
+        // one feature tile's operands live at a time
+        __builtin_amdgcn_sched_barrier(0);
+        C w[3], wd[3];
+#pragma unroll
+        for (int part = 0; part < 3; ++part) {
+          for (int r = 0; r < 4; ++r) w[part][r] = wd[part][r] = 0;
+#pragma unroll
+          for (int kb = 0; kb < KBM; ++kb) {
+            const int ct = part * NFT + FTW * wave + q;
+            const Fr bw = P::frag(Wc + ((size_t)(ct * KBM + kb) * 64 + lane) * P::KPL);
+            w[part] = P::mfma(Ga[kb], bw, w[part]);
+            wd[part] = P::mfma(Gd[kb], bw, wd[part]);
+          }
+        }
+        const int ch = (FTW * wave + q) * 16 + (lane & 15);
+        const A hs = P::ld(h[jb + ch]), hv = P::ld(h[jb + F + ch]), hr = P::ld(h[jb + 2 * F + ch]);
+        const A v0 = P::ld(vv[jb + ch]), v1 = P::ld(vv[jb + F + ch]), v2 = P::ld(vv[jb + 2 * F + ch]);
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+          const size_t ib = (size_t)ir[i] * 3 * F;
+          const A g_s = gs[(size_t)ir[i] * F + ch];
+          const A g0 = gv[ib + ch], g1 = gv[ib + F + ch], g2 = gv[ib + 2 * F + ch];
+          const A Av = g0 * v0 + g1 * v1 + g2 * v2;
+          const A Ar = g0 * rh[i][0] + g1 * rh[i][1] + g2 * rh[i][2];
+          acc_h[q][0] += g_s * w[0][i];
+          acc_h[q][1] += Av * w[1][i];
+          acc_h[q][2] += Ar * w[2][i];
+          const A tv = hv * w[1][i], tr = hr * w[2][i];
+          acc_v[q][0] += g0 * tv;
+          acc_v[q][1] += g1 * tv;
+          acc_v[q][2] += g2 * tv;
+          vals[i] += g_s * hs * wd[0][i] + Av * hv * wd[1][i] + Ar * hr * wd[2][i];
+          vals[4 + i] += g0 * tr;
+          vals[8 + i] += g1 * tr;
+          vals[12 + i] += g2 * tr;
+        }
+      }
+      // lane: the wave's total of value (lane % 16) / 4 for its row lane % 4
+      reduce_scatter16<A, 16>(vals, lane);
+      const int k = lane & 15, i = k & 3;
+      const int e = i == 0 ? er[0] : i == 1 ? er[1] : i == 2 ? er[2] : er[3];
+      if (e >= 0) eg[((size_t)e * NW + wave) * 4 + (k >> 2)] += vals[0];
+    }
+    // sums over the wave's 4 row groups; lanes < 16 write
+#pragma unroll
+    for (int q = 0; q < FTW; ++q)
+#pragma unroll
+      for (int k = 0; k < 3; ++k)
+        for (int o = 16; o < 64; o *= 2) {
+          acc_h[q][k] += __shfl_xor(acc_h[q][k], o);
+          acc_v[q][k] += __shfl_xor(acc_v[q][k], o);
+        }
+    if (lane < 16) {
+#pragma unroll
+      for (int q = 0; q < FTW; ++q) {
+        const int ch = (FTW * wave + q) * 16 + lane;
+#pragma unroll
+        for (int k = 0; k < 3; ++k) {
+          gh_out[jb + k * F + ch] = acc_h[q][k];
+          gv_out[jb + k * F + ch] = gv[jb + k * F + ch] + acc_v[q][k];
+        }
       }
     }
-    gh_out[jb + c] = acc_hs;
-    gh_out[jb + F + c] = acc_hv;
-    gh_out[jb + 2 * F + c] = acc_hr;
-    gv_out[jb + c] = gv[jb + c] + acc_v0;
-    gv_out[jb + F + c] = gv[jb + F + c] + acc_v1;
-    gv_out[jb + 2 * F + c] = gv[jb + 2 * F + c] + acc_v2;
   }
 }
 
@@ -817,13 +825,14 @@ hipError_t allow_lds(K kernel, size_t smem) {
 
 template <class P, int F>
 hipError_t launch_message_bwd(hipStream_t st, const MsgBwdArgs& ma, int nkb) {
-  const int blocks = ((ma.N + MB_RB - 1) / MB_RB + 7) / 8 * 8;
+  constexpr int NWB = mb_nwb<P, F>(), SLICES = F / 16 / mb_ftw<P, F>() / NWB, TH = 64 * NWB;
+  const int blocks = (int)(((long long)(ma.N + MB_RB - 1) / MB_RB * SLICES + 7) / 8 * 8);
   switch (nkb) {
-    case 3: k_message_bwd<P, F, 3><<<blocks, F, 0, st>>>(ma); break;
-    case 6: k_message_bwd<P, F, 6><<<blocks, F, 0, st>>>(ma); break;
-    case 9: k_message_bwd<P, F, 9><<<blocks, F, 0, st>>>(ma); break;
-    case 12: k_message_bwd<P, F, 12><<<blocks, F, 0, st>>>(ma); break;
-    case 17: k_message_bwd<P, F, 17><<<blocks, F, 0, st>>>(ma); break;
+    case 3: k_message_bwd<P, F, 3><<<blocks, TH, 0, st>>>(ma); break;
+    case 6: k_message_bwd<P, F, 6><<<blocks, TH, 0, st>>>(ma); break;
+    case 9: k_message_bwd<P, F, 9><<<blocks, TH, 0, st>>>(ma); break;
+    case 12: k_message_bwd<P, F, 12><<<blocks, TH, 0, st>>>(ma); break;
+    case 17: k_message_bwd<P, F, 17><<<blocks, TH, 0, st>>>(ma); break;
     default: return hipErrorInvalidValue;
   }
   return hipGetLastError();
@@ -838,7 +847,7 @@ hipError_t backward_impl(hipStream_t st, BackwardArgs& ba) {
   const Hyper& hp = ba.m->hp;
   const int N = g->N;
   const long long E = g->E;
-  constexpr int NW = F / 64;
+  constexpr int NW = F / 16 / mb_ftw<P, F>();   // per-edge slots (waves of the message kernel)
   const SaveLayout sv(ba.save, N, F, hp.L, sizeof(T));
   const int kcols = pm->layers[0].filt_mma.din_p;
   if (N == 0) return hipSuccess;

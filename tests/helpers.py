@@ -39,6 +39,28 @@ def _oracle_job(args):
     return out
 
 
+def _oracle_forces_job(args):
+    from oracle.forces import structure_forces
+    name, batch_tuple, idx = args
+    hp, W = synth.workload_weights(name)
+    return [(k, structure_forces(pos, z, cell, pbc, ds if hp.n_heads > 1 else 0, hp, W)["F"])
+            for k, (pos, z, cell, pbc, ds) in zip(idx, batch_tuple)]
+
+
+def oracle_forces(name: str, batch, idx, workers: int | None = None):
+    """Oracle forces of structures `idx` of `batch` (list of [n_b, 3]), in a
+    process pool."""
+    idx = [int(i) for i in idx]
+    workers = workers or min(16, os.cpu_count() or 1, max(1, len(idx)))
+    chunks = [idx[w::workers] for w in range(workers)]
+    jobs = [(name, [batch.structure(k) for k in c], c) for c in chunks if c]
+    res = {}
+    with ProcessPoolExecutor(workers, initializer=_single_thread_blas) as ex:
+        for part in ex.map(_oracle_forces_job, jobs):
+            res.update(dict(part))
+    return [res[k] for k in idx]
+
+
 def oracle_energies(name: str, batch, idx, workers: int | None = None, blend_skip=None):
     """Oracle (E, sum|e|) of structures `idx` of `batch`, in a process pool;
     blend_skip given: every head blended, heads below it left out."""
