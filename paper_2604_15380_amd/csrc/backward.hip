@@ -101,29 +101,39 @@ __global__ void __launch_bounds__(256) k_t_sort(int N, const int32_t* __restrict
   }
 }
 
-// -------------------------------------------------- basis derivative rows ----
-// d/dd of the forward's basis row (f_c g_0, .., f_c g_{K-1}, f_c):
+// ------------------------------------------- edges in sender order, basis ----
+// For the position t of the sender-grouped list (edge e = t_edge[t]): the
+// forward's basis row of e, its derivative d/dd, and (rhat, receiver).
+// The derivative of the row (f_c g_0, .., f_c g_{K-1}, f_c) is
 //   f_c' g_k + f_c g_k',  f_c' = -(pi / (2 r_c)) sin(pi d / r_c);
 //   Gaussian g_k' = -2 gamma (d - k Delta) g_k;
 //   Bessel   g_n' = (n pi / r_c) cos(n pi d / r_c) / d - sin(n pi d / r_c) / d^2.
+// Rows E .. E+15 are zero (read by partial chunks).
 template <class P>
-__global__ void __launch_bounds__(256) k_edge_deriv(long long E, int K, int kcols, double rc, int rbf,
-                                                   double gamma, double delta,
-                                                   const int32_t* __restrict__ recv,
-                                                   const int32_t* __restrict__ col,
-                                                   const int32_t* __restrict__ shift,
-                                                   const int32_t* __restrict__ atom_struct,
-                                                   const double* __restrict__ pos,
-                                                   const double* __restrict__ cell,
-                                                   typename P::T* __restrict__ dbasis) {
+__global__ void __launch_bounds__(256) k_edge_rev(long long E, int K, int kcols, double rc, int rbf,
+                                                 double gamma, double delta,
+                                                 const int32_t* __restrict__ t_edge,
+                                                 const int32_t* __restrict__ recv,
+                                                 const int32_t* __restrict__ col,
+                                                 const int32_t* __restrict__ shift,
+                                                 const int32_t* __restrict__ atom_struct,
+                                                 const double* __restrict__ pos,
+                                                 const double* __restrict__ cell,
+                                                 const typename P::T* __restrict__ basis,
+                                                 const typename P::A* __restrict__ einfo,
+                                                 typename P::T* __restrict__ basis_t,
+                                                 typename P::T* __restrict__ dbasis_t,
+                                                 typename P::A* __restrict__ einfo_t) {
   using A = typename P::A;
-  const long long e = blockIdx.x * (long long)blockDim.x + threadIdx.x;
-  if (e >= E + 16) return;
-  typename P::T* g = dbasis + (size_t)e * kcols;
-  if (e >= E) {
-    for (int k = 0; k < kcols; ++k) g[k] = P::st(0);
+  const long long t = blockIdx.x * (long long)blockDim.x + threadIdx.x;
+  if (t >= E + 16) return;
+  typename P::T* g = dbasis_t + (size_t)t * kcols;
+  typename P::T* b = basis_t + (size_t)t * kcols;
+  if (t >= E) {
+    for (int k = 0; k < kcols; ++k) g[k] = b[k] = P::st(0);
     return;
   }
+  const int e = t_edge[t];
   const int i = recv[e], j = col[e], sh = shift[e];
   const double* Cl = cell + 9 * atom_struct[i];
   const double n0 = (double)(int8_t)(sh & 0xff), n1 = (double)(int8_t)((sh >> 8) & 0xff),
@@ -139,9 +149,9 @@ __global__ void __launch_bounds__(256) k_edge_deriv(long long E, int K, int kcol
   for (int k = 0; k < kcols; ++k) {
     A val = 0;
     if (k < K && rbf == 0) {
-      const A t = dd - (A)(k * delta);
-      const A gk = P::ex(-(A)gamma * t * t);
-      val = dfc * gk + fc * (-(A)(2.0 * gamma) * t * gk);
+      const A u = dd - (A)(k * delta);
+      const A gk = P::ex(-(A)gamma * u * u);
+      val = dfc * gk + fc * (-(A)(2.0 * gamma) * u * gk);
     } else if (k < K) {
       const A w = (A)((k + 1) * (pi / rc));
       const A arg = w * dd;
@@ -152,7 +162,14 @@ __global__ void __launch_bounds__(256) k_edge_deriv(long long E, int K, int kcol
       val = dfc;
     }
     g[k] = P::st(val);
+    b[k] = basis[(size_t)e * kcols + k];
   }
+  A* o = einfo_t + 4 * t;
+  o[0] = einfo[4 * (size_t)e];
+  o[1] = einfo[4 * (size_t)e + 1];
+  o[2] = einfo[4 * (size_t)e + 2];
+  if constexpr (sizeof(A) == 4) o[3] = __int_as_float(i);
+  else o[3] = (A)i;
 }
 
 // ------------------------------------------------------------ heads, back ----
@@ -565,10 +582,10 @@ struct MsgBwdArgs {
   long long E;
   const int32_t* t_ptr;
   const int32_t* t_edge;
-  const int32_t* recv;
+  // in sender order (position t of the sender-grouped list; E + 16 rows)
   const void* basis;
   const void* dbasis;
-  const void* einfo;
+  const void* einfo;   // rhat, receiver index
   DenseDev filt;
   const void* h;       // layer input h, v (storage type)
   const void* v;
@@ -578,6 +595,9 @@ struct MsgBwdArgs {
   void* gv_out;
   void* eg;            // [E][NW][4]
 };
+
+__device__ __forceinline__ int acc_index(float x) { return __float_as_int(x); }
+__device__ __forceinline__ int acc_index(double x) { return (int)x; }
 
 // vals[k] summed over the 16 lanes of a row group, for k = lane % 16.
 template <class A, int LEN>
@@ -651,8 +671,8 @@ k_message_bwd(MsgBwdArgs a) {
       for (int k = 0; k < 3; ++k) acc_h[q][k] = acc_v[q][k] = 0;
     for (int c0 = ea; c0 < eb; c0 += 16) {
       const int cnt = min(16, eb - c0);
-      // A operand rows: edge of row lane % 16 (past the chunk: the zero row E)
-      const int erA = (lane & 15) < cnt ? a.t_edge[c0 + (lane & 15)] : (int)a.E;
+      // A operand rows: position c0 + lane % 16 (past the chunk: the zero row E)
+      const int erA = (lane & 15) < cnt ? c0 + (lane & 15) : (int)a.E;
       Fr Ga[KBM], Gd[KBM];
       {
         const T* gp = basis + (size_t)erA * kcols + (lane >> 4) * P::KPL;
@@ -670,29 +690,41 @@ k_message_bwd(MsgBwdArgs a) {
 #pragma unroll
       for (int i = 0; i < 4; ++i) {
         const int row = P::row(lane, i);
-        er[i] = row < cnt ? a.t_edge[c0 + row] : -1;
-        ir[i] = 0;
-        rh[i][0] = rh[i][1] = rh[i][2] = 0;
-        if (er[i] >= 0) {
-          ir[i] = a.recv[er[i]];
-          rh[i][0] = einfo[4 * (size_t)er[i]];
-          rh[i][1] = einfo[4 * (size_t)er[i] + 1];
-          rh[i][2] = einfo[4 * (size_t)er[i] + 2];
+        const bool ok = row < cnt;
+        const A* ei = einfo + 4 * (size_t)(ok ? c0 + row : 0);
+        er[i] = ok ? a.t_edge[c0 + row] : -1;
+        ir[i] = ok ? acc_index(ei[3]) : 0;
+        rh[i][0] = ok ? ei[0] : A(0);
+        rh[i][1] = ok ? ei[1] : A(0);
+        rh[i][2] = ok ? ei[2] : A(0);
+      }
+      // the receivers' g_s', g_v' at this lane's channels, all issued before
+      // the matrix cores start (they do not depend on the filter)
+      A gsr[FTW][4], gvr[FTW][4][3];
+#pragma unroll
+      for (int q = 0; q < FTW; ++q) {
+        const int ch = (FTW * wave + q) * 16 + (lane & 15);
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+          const size_t ib = (size_t)ir[i] * 3 * F;
+          gsr[q][i] = gs[(size_t)ir[i] * F + ch];
+          gvr[q][i][0] = gv[ib + ch];
+          gvr[q][i][1] = gv[ib + F + ch];
+          gvr[q][i][2] = gv[ib + 2 * F + ch];
         }
       }
-      // the filter fragments stream from the caches chunk by chunk (an
-      // opaque copy of the pointer keeps them from being hoisted out of the
-      // loops into registers for the whole kernel)
+      // The filter fragments stay in registers for the whole kernel when
+      // they are few (FP32, K + 1 <= 24); otherwise they stream from the
+      // caches chunk by chunk (an opaque copy of the pointer keeps the
+      // compiler from hoisting them out of the loops).
       const T* Wc = Wf;
-      asm volatile("" : "+s"(Wc));
+      if constexpr (FTW * 3 * KBM * (int)sizeof(A) / 4 > 40) asm volatile("" : "+s"(Wc));
       // per-edge partial sums: [dE/dd, dE/drhat x, y, z] x 4 rows
       A vals[16];
 #pragma unroll
       for (int k = 0; k < 16; ++k) vals[k] = 0;
 #pragma unroll
       for (int q = 0; q < FTW; ++q) {
-        // one feature tile's operands live at a time
-        __builtin_amdgcn_sched_barrier(0);
         C w[3], wd[3];
 #pragma unroll
         for (int part = 0; part < 3; ++part) {
@@ -710,9 +742,7 @@ k_message_bwd(MsgBwdArgs a) {
         const A v0 = P::ld(vv[jb + ch]), v1 = P::ld(vv[jb + F + ch]), v2 = P::ld(vv[jb + 2 * F + ch]);
 #pragma unroll
         for (int i = 0; i < 4; ++i) {
-          const size_t ib = (size_t)ir[i] * 3 * F;
-          const A g_s = gs[(size_t)ir[i] * F + ch];
-          const A g0 = gv[ib + ch], g1 = gv[ib + F + ch], g2 = gv[ib + 2 * F + ch];
+          const A g_s = gsr[q][i], g0 = gvr[q][i][0], g1 = gvr[q][i][1], g2 = gvr[q][i][2];
           const A Av = g0 * v0 + g1 * v1 + g2 * v2;
           const A Ar = g0 * rh[i][0] + g1 * rh[i][1] + g2 * rh[i][2];
           acc_h[q][0] += g_s * w[0][i];
@@ -732,7 +762,9 @@ k_message_bwd(MsgBwdArgs a) {
       reduce_scatter16<A, 16>(vals, lane);
       const int k = lane & 15, i = k & 3;
       const int e = i == 0 ? er[0] : i == 1 ? er[1] : i == 2 ? er[2] : er[3];
-      if (e >= 0) eg[((size_t)e * NW + wave) * 4 + (k >> 2)] += vals[0];
+      // one add per slot per launch, and launches run in layer order: the
+      // sums are deterministic; the add does not return, so no wave waits
+      if (e >= 0) unsafeAtomicAdd(eg + ((size_t)e * NW + wave) * 4 + (k >> 2), vals[0]);
     }
     // sums over the wave's 4 row groups; lanes < 16 write
 #pragma unroll
@@ -859,9 +891,10 @@ hipError_t backward_impl(hipStream_t st, BackwardArgs& ba) {
   if (e != hipSuccess) return e;
   if (E > 0) {
     const double delta = hp.cutoff / (hp.K - 1);
-    k_edge_deriv<P><<<(unsigned)((E + 16 + 255) / 256), 256, 0, st>>>(
-        E, hp.K, kcols, hp.cutoff, hp.rbf_type, 1.0 / (2.0 * delta * delta), delta, g->recv, g->col, g->shift,
-        g->atom_struct, g->pos, g->cell, (T*)ba.dbasis);
+    k_edge_rev<P><<<(unsigned)((E + 16 + 255) / 256), 256, 0, st>>>(
+        E, hp.K, kcols, hp.cutoff, hp.rbf_type, 1.0 / (2.0 * delta * delta), delta, g->t_edge, g->recv, g->col,
+        g->shift, g->atom_struct, g->pos, g->cell, (const T*)ba.basis, (const A*)ba.einfo, (T*)ba.basis_t,
+        (T*)ba.dbasis, (A*)ba.einfo_t);
     k_fill<A><<<grid_of((size_t)E * NW * 4, 256), 256, 0, st>>>((size_t)E * NW * 4, (A*)ba.eg);
   }
   k_fill<A><<<grid_of((size_t)N * 3 * F, 256), 256, 0, st>>>((size_t)N * 3 * F, (A*)ba.gv);
@@ -942,10 +975,9 @@ hipError_t backward_impl(hipStream_t st, BackwardArgs& ba) {
     ma.E = E;
     ma.t_ptr = g->t_ptr;
     ma.t_edge = g->t_edge;
-    ma.recv = g->recv;
-    ma.basis = ba.basis;
+    ma.basis = ba.basis_t;
     ma.dbasis = ba.dbasis;
-    ma.einfo = ba.einfo;
+    ma.einfo = ba.einfo_t;
     ma.filt = Ld.filt_mma;
     ma.h = sv.H(l);
     ma.v = sv.V(l);

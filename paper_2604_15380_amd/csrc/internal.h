@@ -279,7 +279,11 @@ struct BackwardArgs {
   void* save;               // the forward's save area
   const void* basis;        // [E + 16][kcols] the forward's basis rows
   const void* einfo;        // [E][4] rhat, sender index
-  void* dbasis;             // [E + 16][kcols] their derivatives d/dd
+  // in the order of the sender-grouped edge list (E + 16 rows): the basis
+  // rows, their derivatives d/dd, and (rhat, receiver index)
+  void* basis_t;
+  void* dbasis;
+  void* einfo_t;
   const void* head_plan;    // the forward's grouping of atoms by head
   const void* head_tiles;
   const int32_t* head_order;

@@ -919,7 +919,8 @@ static painn_status run_forward(painn_ctx* ctx, const painn_model* model, const 
 }
 
 // Reverse-pass workspace: save area, gradients dE/ds, dE/dv (two of each),
-// dE/dh, basis derivative rows, per-edge partials (one slot per wave of the
+// dE/dh, basis rows and their derivatives and edge info in sender order,
+// per-edge partials (one slot per wave of the
 // channels), per-atom scratch, per-edge dE/dr.
 static int forces_scratch_width(const Hyper& hp) {
   int zw = 0;
@@ -934,7 +935,7 @@ static size_t forces_workspace_bytes(int prec, const Hyper& hp, int N, long long
   const size_t eb = elem_bytes(prec), ab = acc_bytes(prec), n = (size_t)N, F = hp.F;
   auto al = [](size_t x) { return (x + 255) & ~(size_t)255; };
   return al(SaveLayout::bytes(n, F, hp.L, eb)) + 2 * al(n * F * ab) + 3 * al(n * 3 * F * ab) +
-         al(((size_t)E + 16) * kcols * eb) + al((size_t)E * (F / 16) * 4 * ab) +
+         2 * al(((size_t)E + 16) * kcols * eb) + al((size_t)E * 4 * ab) + al((size_t)E * (F / 16) * 4 * ab) +
          al(n * forces_scratch_width(hp) * ab) + al((size_t)E * 3 * sizeof(double));
 }
 
@@ -1087,6 +1088,8 @@ painn_status painn_forces(painn_ctx* ctx, const painn_model* model, const painn_
   b.gv2 = p; p += al(N * 3 * F * ab);
   b.gh = p; p += al(N * 3 * F * ab);
   b.dbasis = p; p += al(((size_t)g->E + 16) * kcols * eb);
+  b.basis_t = p; p += al(((size_t)g->E + 16) * kcols * eb);
+  b.einfo_t = p; p += al((size_t)g->E * 4 * ab);
   b.eg = p; p += al((size_t)g->E * (F / 16) * 4 * ab);
   b.scratch_w = forces_scratch_width(hp);
   b.scratch = p; p += al(N * b.scratch_w * ab);
