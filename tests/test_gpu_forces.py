@@ -13,7 +13,7 @@ from oracle.painn import RBF_BESSEL
 
 pytestmark = pytest.mark.gpu
 
-FORCE_TOL = {"fp64": 1e-9, "fp32": 5e-4}
+FORCE_TOL = {"fp64": 1e-10, "fp32": 2e-5}
 
 
 def say(msg):
