@@ -63,8 +63,8 @@ def kernel_work(kernel: str, hp, N: int, E: int, prec: str, head_entries: int | 
              (elementwise terms and the per-edge sums over channels); minimum
              HBM bytes: per atom h, v (6F) and g_s', g_v' (4F) read, g_h, g_v
              (6F) written, plus 8 bytes of CSR per edge.
-    bwd_update: per atom 44 F^2 (U/V and the gate MLP recomputed, 22F^2; the
-             transposed products W2a^T, W1a^T, [U^T|V^T], 22F^2).
+    bwd_update: per atom 22 F^2 (the transposed products W2a^T, W1a^T and
+             [U^T|V^T] for 3 components; U, V, the gate come from the forward).
     bwd_phi: per atom 10 F^2 (W1 s recomputed, W2^T, W1^T).
     """
     F, K, L = hp.F, hp.K, hp.L
@@ -81,7 +81,7 @@ def kernel_work(kernel: str, hp, N: int, E: int, prec: str, head_entries: int | 
         return "alu", E * (12.0 * K * F + 36.0 * F), N * (6.0 * F * b + 10.0 * F * ab) + 8.0 * E
     if kernel == "bwd_update":
         ab = 8 if prec == "fp64" else 4
-        return "mfma", N * 44.0 * F * F, N * (4.0 * F * b + 8.0 * F * ab)
+        return "mfma", N * 22.0 * F * F, N * (9.0 * F * b + 8.0 * F * ab)
     if kernel == "bwd_phi":
         ab = 8 if prec == "fp64" else 4
         return "mfma", N * 10.0 * F * F, N * (F * b + 6.0 * F * ab)

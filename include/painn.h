@@ -212,7 +212,7 @@ painn_status painn_forward_blend(painn_ctx* ctx, const painn_model* model, const
  *   energies   [B] float64 output (the same values as painn_forward).
  *   forces     [N, 3] float64 output (eV/Angstrom for energies in eV).
  * Both written on the stream; the reverse pass keeps every layer's
- * activations (about (11 L + 4) N F values of the precision's storage type
+ * activations (about (20 L + 4) N F values of the precision's storage type
  * plus per-edge buffers) in a context workspace grown on demand.  The first
  * call on a graph also groups its edges by sender (kept until the graph is
  * rebuilt).  Errors: as painn_forward; PAINN_E_UNSUPPORTED for BF16, for

@@ -322,22 +322,29 @@ __global__ void __launch_bounds__(64 * HB_NW) k_heads_bwd(HeadBwdArgs a) {
   }
 }
 // ----------------------------------------------------------- update, back ----
-// Tile of 16 atoms, 4 waves; LDS R1 [16][3F + PAD], R2 [16][F + PAD]; the
-// per-atom scratch row holds U[c], V[c] (6F), |V| (F), <U, V> (F), z (F),
-// a_vv (F), a_sv (F), g_n (F).
+// Tile of 16 atoms, 4 waves; LDS R1 [16][3F + PAD], R2 [16][F + PAD].  The
+// forward saved U v[c], V v[c], the gate's pre-activation z and a_vv, a_sv,
+// so only the transposed products run here:
+//   g_a  = [sum_c g_v[c] U[c] | g_s <U, V> | g_s]
+//   g_z  = (W2a^T g_a) * silu'(z)
+//   [g_s' ; g_n] = W1a^T g_z                 g_s after the message = g_s + g_s'
+//   g_U[c] = g_v[c] a_vv + g_s a_sv V[c],  g_V[c] = g_s a_sv U[c] + g_n V[c] / |V|
+//   g_v after the message [c] = g_v[c] + [U^T | V^T] [g_U[c] ; g_V[c]]
+// The per-atom scratch holds g_n.
 constexpr int UB_NW = 4;
 
 struct UpdBwdArgs {
   int N;
-  const void* s;     // after the message [N][F]
-  const void* v;     // after the message [N][3F]
+  const void* uv;    // saved [N][3][2F]: U v[c], V v[c]
+  const void* z;     // saved [N][F]
+  const void* ag;    // saved [N][2F]: a_vv, a_sv
   const void* gs;    // dE/d(s, v) after the update
   const void* gv;
   void* gs_out;      // dE/d(s, v) after the message
   void* gv_out;
   void* scratch;
   int sw;
-  DenseDev uv, upd1, upd2, uvT, upd1T, upd2T;
+  DenseDev uvT, upd1T, upd2T;
 };
 
 template <class P, int F>
@@ -352,82 +359,29 @@ __global__ void __launch_bounds__(64 * UB_NW) k_update_bwd(UpdBwdArgs a) {
   const int lane = threadIdx.x & 63;
   const size_t row0 = (size_t)blockIdx.x * TM;
   const int N = a.N;
-  const T* s = (const T*)a.s;
-  const T* v = (const T*)a.v;
+  const T* uv = (const T*)a.uv;
+  const T* zs = (const T*)a.z;
+  const T* ag = (const T*)a.ag;
   const A* gs = (const A*)a.gs;
   const A* gv = (const A*)a.gv;
   A* scr = (A*)a.scratch;
   const int sw = a.sw;
-  // scratch columns
-  constexpr int O_UV = 0, O_N = 6 * F, O_PD = 7 * F, O_Z = 8 * F, O_AVV = 9 * F, O_ASV = 10 * F, O_GN = 11 * F;
-  auto sc = [&](int r, int o) -> A& { return scr[(row0 + r) * sw + o]; };
-  // U[c], V[c] for c = x, y, z
-  for (int c = 0; c < 3; ++c) {
-    for (int x = threadIdx.x; x < TM * F; x += blockDim.x) {
-      const int r = x / F, f = x % F;
-      R1[r * LD1 + f] = row0 + r < (size_t)N ? v[(row0 + r) * 3 * F + c * F + f] : P::st(0);
-    }
-    __syncthreads();
-    dense_tiles<P, 1, UB_NW, F / P::KC>(R1, LD1, a.uv, [&](int ct, C* acc) {
-      const int col = ct * 16 + (lane & 15);
-      for (int i = 0; i < 4; ++i) {
-        const int r = P::row(lane, i);
-        if (row0 + r < (size_t)N) sc(r, O_UV + c * 2 * F + col) = acc[0][i];
-      }
-    });
-    __syncthreads();
-  }
-  // |V|, <U, V>; [s ; |V|] into R1
-  for (int x = threadIdx.x; x < TM * F; x += blockDim.x) {
-    const int r = x / F, f = x % F;
-    A n2 = 0, pd = 0, nv = 0;
-    T sv = P::st(0);
-    if (row0 + r < (size_t)N) {
-      for (int c = 0; c < 3; ++c) {
-        const A U = sc(r, O_UV + c * 2 * F + f), V = sc(r, O_UV + c * 2 * F + F + f);
-        n2 += V * V;
-        pd += U * V;
-      }
-      nv = sqrt(n2);
-      sc(r, O_N + f) = nv;
-      sc(r, O_PD + f) = pd;
-      sv = s[(row0 + r) * F + f];
-    }
-    R1[r * LD1 + f] = sv;
-    R1[r * LD1 + F + f] = P::st(nv);
-  }
-  __syncthreads();
-  // z = W1a [s ; |V|] + b1a ; silu(z) into R2
-  dense_tiles<P, 1, UB_NW, 2 * F / P::KC>(R1, LD1, a.upd1, [&](int ct, C* acc) {
-    const int col = ct * 16 + (lane & 15);
-    const A bias = ((const A*)a.upd1.b)[col];
-    for (int i = 0; i < 4; ++i) {
-      const int r = P::row(lane, i);
-      const A z = acc[0][i] + bias;
-      if (row0 + r < (size_t)N) sc(r, O_Z + col) = z;
-      R2[r * LD2 + col] = P::st(silu<A>(z));
-    }
-  });
-  __syncthreads();
-  // a = W2a silu(z) + b2a: keep a_vv, a_sv
-  dense_tiles<P, 1, UB_NW, F / P::KC>(R2, LD2, a.upd2, [&](int ct, C* acc) {
-    const int col = ct * 16 + (lane & 15);
-    if (col >= 2 * F) return;
-    const A bias = ((const A*)a.upd2.b)[col];
-    for (int i = 0; i < 4; ++i) {
-      const int r = P::row(lane, i);
-      if (row0 + r < (size_t)N) sc(r, (col < F ? O_AVV : O_ASV - F) + col) = acc[0][i] + bias;
-    }
-  });
-  // g_a = [sum_c g_v[c] U[c] | g_s <U, V> | g_s] into R1
+  auto U = [&](size_t i, int c, int f) { return P::ld(uv[(i * 3 + c) * 2 * F + f]); };
+  auto V = [&](size_t i, int c, int f) { return P::ld(uv[(i * 3 + c) * 2 * F + F + f]); };
+  // g_a into R1
   for (int x = threadIdx.x; x < TM * F; x += blockDim.x) {
     const int r = x / F, f = x % F;
     A gvv = 0, gsv = 0, gss = 0;
     if (row0 + r < (size_t)N) {
       const size_t i = row0 + r;
-      for (int c = 0; c < 3; ++c) gvv += gv[i * 3 * F + c * F + f] * sc(r, O_UV + c * 2 * F + f);
+      A pd = 0;
+      for (int c = 0; c < 3; ++c) {
+        const A u = U(i, c, f);
+        pd += u * V(i, c, f);
+        gvv += gv[i * 3 * F + c * F + f] * u;
+      }
       gss = gs[i * F + f];
-      gsv = gss * sc(r, O_PD + f);
+      gsv = gss * pd;
     }
     R1[r * LD1 + f] = P::st(gvv);
     R1[r * LD1 + F + f] = P::st(gsv);
@@ -440,12 +394,12 @@ __global__ void __launch_bounds__(64 * UB_NW) k_update_bwd(UpdBwdArgs a) {
     for (int i = 0; i < 4; ++i) {
       const int r = P::row(lane, i);
       A g = 0;
-      if (row0 + r < (size_t)N) g = acc[0][i] * dsilu<A>(sc(r, O_Z + col));
+      if (row0 + r < (size_t)N) g = acc[0][i] * dsilu<A>(P::ld(zs[(row0 + r) * F + col]));
       R2[r * LD2 + col] = P::st(g);
     }
   });
   __syncthreads();
-  // [g_s' ; g_n] = W1a^T g_z: g_s after the message = g_s + g_s'
+  // [g_s' ; g_n] = W1a^T g_z
   A* gs_out = (A*)a.gs_out;
   dense_tiles<P, 1, UB_NW, F / P::KC>(R2, LD2, a.upd1T, [&](int ct, C* acc) {
     const int col = ct * 16 + (lane & 15);
@@ -454,12 +408,11 @@ __global__ void __launch_bounds__(64 * UB_NW) k_update_bwd(UpdBwdArgs a) {
       const size_t g = row0 + r;
       if (g >= (size_t)N) continue;
       if (col < F) gs_out[g * F + col] = gs[g * F + col] + acc[0][i];
-      else sc(r, O_GN + col - F) = acc[0][i];
+      else scr[g * sw + col - F] = acc[0][i];
     }
   });
   __syncthreads();
-  // per component: [g_U | g_V] into R1, then g_v after the message =
-  // g_v + [U^T | V^T] [g_U ; g_V]
+  // per component: [g_U | g_V] into R1, then [U^T | V^T] [g_U ; g_V]
   A* gv_out = (A*)a.gv_out;
   for (int c = 0; c < 3; ++c) {
     for (int x = threadIdx.x; x < TM * F; x += blockDim.x) {
@@ -467,11 +420,13 @@ __global__ void __launch_bounds__(64 * UB_NW) k_update_bwd(UpdBwdArgs a) {
       A gU = 0, gV = 0;
       if (row0 + r < (size_t)N) {
         const size_t i = row0 + r;
-        const A U = sc(r, O_UV + c * 2 * F + f), V = sc(r, O_UV + c * 2 * F + F + f);
+        const A u = U(i, c, f), w = V(i, c, f);
+        const A v0 = V(i, 0, f), v1 = V(i, 1, f), v2 = V(i, 2, f);
+        const A nv = sqrt(v0 * v0 + v1 * v1 + v2 * v2);
         const A g_s = gs[i * F + f], gvc = gv[i * 3 * F + c * F + f];
-        const A asv = sc(r, O_ASV + f), nv = sc(r, O_N + f);
-        gU = gvc * sc(r, O_AVV + f) + g_s * asv * V;
-        gV = g_s * asv * U + (nv > A(0) ? sc(r, O_GN + f) * V / nv : A(0));
+        const A avv = P::ld(ag[i * 2 * F + f]), asv = P::ld(ag[i * 2 * F + F + f]);
+        gU = gvc * avv + g_s * asv * w;
+        gV = g_s * asv * u + (nv > A(0) ? scr[i * sw + f] * w / nv : A(0));
       }
       R1[r * LD1 + f] = P::st(gU);
       R1[r * LD1 + F + f] = P::st(gV);
@@ -953,17 +908,15 @@ hipError_t backward_impl(hipStream_t st, BackwardArgs& ba) {
     const LayerDev& Ld = pm->layers[l];
     UpdBwdArgs ua;
     ua.N = N;
-    ua.s = sv.Smid(l);
-    ua.v = sv.Vmid(l);
+    ua.uv = sv.UV(l);
+    ua.z = sv.Z(l);
+    ua.ag = sv.Agate(l);
     ua.gs = ba.gs;
     ua.gv = ba.gv;
     ua.gs_out = ba.gs2;
     ua.gv_out = ba.gv2;
     ua.scratch = ba.scratch;
     ua.sw = ba.scratch_w;
-    ua.uv = Ld.uv;
-    ua.upd1 = Ld.upd1;
-    ua.upd2 = Ld.upd2;
     ua.uvT = Ld.uvT;
     ua.upd1T = Ld.upd1T;
     ua.upd2T = Ld.upd2T;

@@ -316,6 +316,11 @@ struct UpdArgs {
   void* v_out;
   void* h;
   DenseDev uv, upd1, upd2, phi1, phi2;
+  // with SAVE: U, V per component [N][3][2F], the gate's pre-activation
+  // [N][F] and [a_vv | a_sv] [N][2F] for the reverse pass
+  void* save_uv;
+  void* save_z;
+  void* save_a;
 };
 
 // Waves per SIMD the update kernel is compiled for: three at F = 128, where
@@ -334,7 +339,7 @@ constexpr int update_nw() {
   return F > 256 ? F / 64 : 4;
 }
 
-template <class P, int F, int RT, bool FUSE_PHI>
+template <class P, int F, int RT, bool FUSE_PHI, bool SAVE>
 __global__ void __launch_bounds__(64 * update_nw<F>()) __attribute__((amdgpu_waves_per_eu(update_waves<P, F>())))
 k_update(UpdArgs a) {
   using T = typename P::T;
@@ -401,6 +406,17 @@ k_update(UpdArgs a) {
           nsq[q][r][i] += av[r][i] * av[r][i];
           pd[q][r][i] += au[r][i] * av[r][i];
         }
+        if constexpr (SAVE) {
+          const int col = ft * 16 + (lane & 15);
+          for (int i = 0; i < 4; ++i) {
+            const size_t row = row0 + r * 16 + P::row(lane, i);
+            if (row < (size_t)N) {
+              T* o = (T*)a.save_uv + (row * 3 + c) * 2 * F;
+              o[col] = P::st(au[r][i]);
+              o[F + col] = P::st(av[r][i]);
+            }
+          }
+        }
       }
     }
   }
@@ -417,8 +433,13 @@ k_update(UpdArgs a) {
     const int col = ct * 16 + (lane & 15);
     const A bias = ((const A*)a.upd1.b)[col];
     for (int r = 0; r < RT; ++r)
-      for (int i = 0; i < 4; ++i)
+      for (int i = 0; i < 4; ++i) {
         H[(r * 16 + P::row(lane, i)) * LD1 + col] = P::st(silu<A>(acc[r][i] + bias));
+        if constexpr (SAVE) {
+          const size_t row = row0 + r * 16 + P::row(lane, i);
+          if (row < (size_t)N) ((T*)a.save_z)[row * F + col] = P::st(acc[r][i] + bias);
+        }
+      }
   });
   __syncthreads();
   {
@@ -458,6 +479,12 @@ k_update(UpdArgs a) {
           const int rr = r * 16 + P::row(lane, i);
           const size_t row = row0 + rr;
           const A g_vv = avv[r][i] + bvv, g_sv = asv[r][i] + bsv, g_ss = ass[r][i] + bss;
+          if constexpr (SAVE) {
+            if (row < (size_t)N) {
+              ((T*)a.save_a)[row * 2 * F + col] = P::st(g_vv);
+              ((T*)a.save_a)[row * 2 * F + F + col] = P::st(g_sv);
+            }
+          }
           const A sn = P::ld(SN[rr * LD2 + col]) + g_sv * pd[q][r][i] + g_ss;
           const T st = P::st(sn);
           SN[rr * LD2 + col] = st;
@@ -1386,12 +1413,21 @@ hipError_t forward_impl(hipStream_t st, ForwardArgs& fa) {
     ua.upd2 = Ld.upd2;
     const bool fuse = l + 1 <= fa.stop_layer;
     prof_mark(fa.prof, st, KC_UPDATE, true);
+    ua.save_uv = fa.save ? sv.UV(l) : nullptr;
+    ua.save_z = fa.save ? sv.Z(l) : nullptr;
+    ua.save_a = fa.save ? sv.Agate(l) : nullptr;
+    const int ugrid = (N + 16 * URT - 1) / (16 * URT);
     if (fuse) {
       ua.phi1 = pm->layers[l + 1].phi1;
       ua.phi2 = pm->layers[l + 1].phi2;
-      k_update<P, F, URT, true><<<(N + 16 * URT - 1) / (16 * URT), 64 * update_nw<F>(), 0, st>>>(ua);
+    }
+    // the saving variants exist for the reverse pass (FP64 / FP32)
+    if (fa.save && sizeof(T) != 2) {
+      if (fuse) k_update<P, F, URT, true, sizeof(T) != 2><<<ugrid, 64 * update_nw<F>(), 0, st>>>(ua);
+      else k_update<P, F, URT, false, sizeof(T) != 2><<<ugrid, 64 * update_nw<F>(), 0, st>>>(ua);
     } else {
-      k_update<P, F, URT, false><<<(N + 16 * URT - 1) / (16 * URT), 64 * update_nw<F>(), 0, st>>>(ua);
+      if (fuse) k_update<P, F, URT, true, false><<<ugrid, 64 * update_nw<F>(), 0, st>>>(ua);
+      else k_update<P, F, URT, false, false><<<ugrid, 64 * update_nw<F>(), 0, st>>>(ua);
     }
     prof_mark(fa.prof, st, KC_UPDATE, false);
   }

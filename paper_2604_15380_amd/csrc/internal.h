@@ -242,18 +242,24 @@ struct ForwardArgs {
 // The activations a forward run keeps for the reverse pass (storage type,
 // element size es).  Layer l: S(l) = s before the message [N][F], V(l) = v
 // [N][3F], H(l) = phi(s) [N][3F], Smid(l), Vmid(l) = s and v after the
-// message; S(L), V(L) = the final s and v.
+// message; S(L), V(L) = the final s and v.  Then per layer the update's
+// intermediates: UV(l) = [U v[c] | V v[c]] for c = x, y, z [N][3][2F], Z(l) =
+// the gate MLP's pre-activation [N][F], Agate(l) = [a_vv | a_sv] [N][2F].
 struct SaveLayout {
   char* base;
   size_t N, F, es;
-  __host__ __device__ SaveLayout(void* b, size_t n, size_t f, int, size_t e)
-      : base((char*)b), N(n), F(f), es(e) {}
+  int L;
+  __host__ __device__ SaveLayout(void* b, size_t n, size_t f, int l, size_t e)
+      : base((char*)b), N(n), F(f), es(e), L(l) {}
+  __host__ __device__ void* UV(int l) const { return base + ((size_t)L * 11 + 4 + (size_t)l * 9) * N * F * es; }
+  __host__ __device__ void* Z(int l) const { return (char*)UV(l) + 6 * N * F * es; }
+  __host__ __device__ void* Agate(int l) const { return (char*)Z(l) + N * F * es; }
   __host__ __device__ void* S(int l) const { return base + (size_t)l * 11 * N * F * es; }
   __host__ __device__ void* V(int l) const { return (char*)S(l) + N * F * es; }
   __host__ __device__ void* H(int l) const { return (char*)V(l) + 3 * N * F * es; }
   __host__ __device__ void* Smid(int l) const { return (char*)H(l) + 3 * N * F * es; }
   __host__ __device__ void* Vmid(int l) const { return (char*)Smid(l) + N * F * es; }
-  static size_t bytes(size_t N, size_t F, int L, size_t es) { return ((size_t)L * 11 + 4) * N * F * es; }
+  static size_t bytes(size_t N, size_t F, int L, size_t es) { return ((size_t)L * 20 + 4) * N * F * es; }
 };
 
 // Atoms grouped by head (the heads kernels' counting sort): per-head counts

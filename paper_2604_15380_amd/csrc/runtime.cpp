@@ -928,7 +928,7 @@ static int forces_scratch_width(const Hyper& hp) {
   for (int m = 0; m + 1 < nl; ++m)
     zw += pad32(m < (int)hp.shared_dims.size() ? hp.shared_dims[m]
                                                : hp.branch_dims[m - hp.shared_dims.size()]);
-  return zw > 12 * hp.F ? zw : 12 * hp.F;
+  return zw > hp.F ? zw : hp.F;
 }
 
 static size_t forces_workspace_bytes(int prec, const Hyper& hp, int N, long long E, int kcols) {
