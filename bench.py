@@ -30,17 +30,19 @@ HBM_PEAK_GBS = 8000.0
 DTYPE = {"fp64": "f64", "fp32": "f32", "bf16": "bf16"}
 ELEM = {"fp64": 8, "fp32": 4, "bf16": 2}
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "traffic.json")
+# the kernel sources a stored traffic measurement depends on (per mode)
 KERNEL_SOURCES = ["paper_2604_15380_amd/csrc/forward.hip", "paper_2604_15380_amd/csrc/mfma.h",
-                  "paper_2604_15380_amd/csrc/neighbors.hip", "paper_2604_15380_amd/csrc/backward.hip"]
+                  "paper_2604_15380_amd/csrc/neighbors.hip"]
+KERNEL_SOURCES_FORCES = KERNEL_SOURCES + ["paper_2604_15380_amd/csrc/backward.hip"]
 
 
 def log(msg):
     print(f"[bench] {msg}", file=sys.stderr, flush=True)
 
 
-def source_digest() -> str:
+def source_digest(forces: bool = False) -> str:
     h = hashlib.sha256()
-    for p in KERNEL_SOURCES:
+    for p in (KERNEL_SOURCES_FORCES if forces else KERNEL_SOURCES):
         with open(os.path.join(ROOT, p), "rb") as f:
             h.update(f.read())
     return h.hexdigest()[:16]
@@ -260,7 +262,8 @@ def main():
         avg_s = ms / launches / 1e3
         achieved = flops / avg_s / 1e12
         peak = PEAK[bound][prec]
-        traffic = load_traffic(f"{name}/{prec}" + ("/forces" if args.forces else ""), source_digest(), dom)
+        traffic = load_traffic(f"{name}/{prec}" + ("/forces" if args.forces else ""),
+                               source_digest(args.forces), dom)
         roofline = dict(kernel=dom, bound=bound, achieved=round(achieved, 3), peak=peak, unit="TFLOP/s",
                         frac=round(achieved / peak, 4), traffic=traffic,
                         avg_launch_ms=round(avg_s * 1e3, 4), launches=launches,

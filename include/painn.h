@@ -215,9 +215,7 @@ painn_status painn_forward_blend(painn_ctx* ctx, const painn_model* model, const
  * activations (about (20 L + 4) N F values of the precision's storage type
  * plus per-edge buffers) in a context workspace grown on demand.  The first
  * call on a graph also groups its edges by sender (kept until the graph is
- * rebuilt).  Errors: as painn_forward; PAINN_E_UNSUPPORTED for BF16, for
- * F = 384 in FP64, and when the heads' widest layer does not fit the
- * reverse heads kernel. */
+ * rebuilt).  Errors: as painn_forward; PAINN_E_UNSUPPORTED for BF16. */
 painn_status painn_forces(painn_ctx* ctx, const painn_model* model, const painn_graph* graph,
                           const int32_t* dataset_id, painn_precision precision, double* energies,
                           double* forces);

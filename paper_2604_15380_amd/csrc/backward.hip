@@ -192,6 +192,7 @@ struct HeadBwdArgs {
   int zoff[32];                  // pre-activation offsets in a scratch row
   void* scratch;
   int sw;
+  void* xbuf;                    // GX: per-workgroup [2][16][ldw] buffers in global memory
   void* gs;                      // out: dE/ds [N][F]
 };
 
@@ -292,12 +293,15 @@ __device__ void heads_bwd_tile(const HeadBwdArgs& a, int head, const int* idx, t
   }
 }
 
-template <class P, int F>
+// GX: the two activation buffers live in global memory (a region per
+// workgroup) when they do not fit the LDS.
+template <class P, int F, bool GX>
 __global__ void __launch_bounds__(64 * HB_NW) k_heads_bwd(HeadBwdArgs a) {
   using T = typename P::T;
   constexpr int TM = 16;
   extern __shared__ __attribute__((aligned(16))) unsigned char smem[];
-  T* Y[2] = {(T*)smem, (T*)smem + TM * a.ldw};
+  T* base = GX ? (T*)a.xbuf + (size_t)blockIdx.x * 2 * TM * a.ldw : (T*)smem;
+  T* Y[2] = {base, base + TM * a.ldw};
   __shared__ int idx[TM];
   const int lane = threadIdx.x & 63;
   int head = 0, begin, end;
@@ -344,18 +348,22 @@ struct UpdBwdArgs {
   void* gv_out;
   void* scratch;
   int sw;
+  void* xbuf;        // GX: per-workgroup [16][3F + PAD] buffers in global memory
   DenseDev uvT, upd1T, upd2T;
 };
 
-template <class P, int F>
+// GX: the 3F-wide operand buffer R1 lives in global memory (a region per
+// workgroup; the MFMA operand reads go through the caches) when 16 rows of
+// 4F do not fit the LDS (FP64 at F = 384).
+template <class P, int F, bool GX>
 __global__ void __launch_bounds__(64 * UB_NW) k_update_bwd(UpdBwdArgs a) {
   using T = typename P::T;
   using A = typename P::A;
   using C = typename P::C;
   constexpr int TM = 16, LD1 = 3 * F + P::PAD, LD2 = F + P::PAD;
   extern __shared__ __attribute__((aligned(16))) unsigned char smem[];
-  T* R1 = (T*)smem;
-  T* R2 = R1 + TM * LD1;
+  T* R1 = GX ? (T*)a.xbuf + (size_t)blockIdx.x * TM * LD1 : (T*)smem;
+  T* R2 = GX ? (T*)smem : R1 + TM * LD1;
   const int lane = threadIdx.x & 63;
   const size_t row0 = (size_t)blockIdx.x * TM;
   const int N = a.N;
@@ -457,18 +465,19 @@ struct PhiBwdArgs {
   void* gs_out;
   void* scratch;
   int sw;
+  void* xbuf;          // GX: as for the update
   DenseDev phi1, phi1T, phi2T;
 };
 
-template <class P, int F>
+template <class P, int F, bool GX>
 __global__ void __launch_bounds__(64 * UB_NW) k_phi_bwd(PhiBwdArgs a) {
   using T = typename P::T;
   using A = typename P::A;
   using C = typename P::C;
   constexpr int TM = 16, LD1 = 3 * F + P::PAD, LD2 = F + P::PAD;
   extern __shared__ __attribute__((aligned(16))) unsigned char smem[];
-  T* R1 = (T*)smem;
-  T* R2 = R1 + TM * LD1;
+  T* R1 = GX ? (T*)a.xbuf + (size_t)blockIdx.x * TM * LD1 : (T*)smem;
+  T* R2 = GX ? (T*)smem : R1 + TM * LD1;
   const int lane = threadIdx.x & 63;
   const size_t row0 = (size_t)blockIdx.x * TM;
   const int N = a.N;
@@ -838,11 +847,12 @@ hipError_t backward_impl(hipStream_t st, BackwardArgs& ba) {
   const SaveLayout sv(ba.save, N, F, hp.L, sizeof(T));
   const int kcols = pm->layers[0].filt_mma.din_p;
   if (N == 0) return hipSuccess;
-  // LDS of the tile kernels: 16 rows of 3F + F (+ padding)
-  const size_t smem_ub = (size_t)16 * (4 * F + 2 * P::PAD) * sizeof(T);
-  if (smem_ub > 160 * 1024) return hipErrorInvalidValue;
-  hipError_t e = allow_lds(k_update_bwd<P, F>, smem_ub);
-  if (e == hipSuccess) e = allow_lds(k_phi_bwd<P, F>, smem_ub);
+  // LDS of the tile kernels: 16 rows of 3F + F (+ padding), or of F alone
+  // with the 3F-wide buffer in global memory
+  constexpr bool UGX = (size_t)16 * (4 * F + 2 * P::PAD) * sizeof(T) > 160 * 1024;
+  const size_t smem_ub = (size_t)16 * ((UGX ? 0 : 3 * F + P::PAD) + F + P::PAD) * sizeof(T);
+  hipError_t e = allow_lds(k_update_bwd<P, F, UGX>, smem_ub);
+  if (e == hipSuccess) e = allow_lds(k_phi_bwd<P, F, UGX>, smem_ub);
   if (e != hipSuccess) return e;
   if (E > 0) {
     const double delta = hp.cutoff / (hp.K - 1);
@@ -884,9 +894,10 @@ hipError_t backward_impl(hipStream_t st, BackwardArgs& ba) {
     ha.scratch = ba.scratch;
     ha.sw = ba.scratch_w;
     ha.gs = ba.gs;
-    const size_t smem = (size_t)2 * 16 * ha.ldw * sizeof(T);
-    if (smem > 150 * 1024) return hipErrorInvalidValue;
-    e = allow_lds(k_heads_bwd<P, F>, smem);
+    ha.xbuf = ba.xbuf;
+    const bool hgx = (size_t)2 * 16 * ha.ldw * sizeof(T) > 150 * 1024;
+    const size_t smem = hgx ? 0 : (size_t)2 * 16 * ha.ldw * sizeof(T);
+    e = hgx ? hipSuccess : allow_lds(k_heads_bwd<P, F, false>, smem);
     if (e != hipSuccess) return e;
     int grid;
     if (ba.dataset_id) {
@@ -900,7 +911,9 @@ hipError_t backward_impl(hipStream_t st, BackwardArgs& ba) {
       ha.plan = nullptr;
       grid = (N + 15) / 16;
     }
-    k_heads_bwd<P, F><<<grid, 64 * HB_NW, smem, st>>>(ha);
+    if (hgx && (size_t)grid * 2 * 16 * ha.ldw * sizeof(T) > ba.xbuf_bytes) return hipErrorInvalidValue;
+    if (hgx) k_heads_bwd<P, F, true><<<grid, 64 * HB_NW, 0, st>>>(ha);
+    else k_heads_bwd<P, F, false><<<grid, 64 * HB_NW, smem, st>>>(ha);
   }
   prof_mark(ba.prof, st, KC_BWD_HEADS, false);
   const int tiles = (N + 15) / 16;
@@ -920,8 +933,10 @@ hipError_t backward_impl(hipStream_t st, BackwardArgs& ba) {
     ua.uvT = Ld.uvT;
     ua.upd1T = Ld.upd1T;
     ua.upd2T = Ld.upd2T;
+    ua.xbuf = ba.xbuf;
+    if (UGX && (size_t)tiles * 16 * (3 * F + P::PAD) * sizeof(T) > ba.xbuf_bytes) return hipErrorInvalidValue;
     prof_mark(ba.prof, st, KC_BWD_UPDATE, true);
-    k_update_bwd<P, F><<<tiles, 64 * UB_NW, smem_ub, st>>>(ua);
+    k_update_bwd<P, F, UGX><<<tiles, 64 * UB_NW, smem_ub, st>>>(ua);
     prof_mark(ba.prof, st, KC_BWD_UPDATE, false);
     MsgBwdArgs ma;
     ma.N = N;
@@ -955,8 +970,9 @@ hipError_t backward_impl(hipStream_t st, BackwardArgs& ba) {
       pa.phi1 = Ld.phi1;
       pa.phi1T = Ld.phi1T;
       pa.phi2T = Ld.phi2T;
+      pa.xbuf = ba.xbuf;
       prof_mark(ba.prof, st, KC_BWD_PHI, true);
-      k_phi_bwd<P, F><<<tiles, 64 * UB_NW, smem_ub, st>>>(pa);
+      k_phi_bwd<P, F, UGX><<<tiles, 64 * UB_NW, smem_ub, st>>>(pa);
       prof_mark(ba.prof, st, KC_BWD_PHI, false);
     }
   }

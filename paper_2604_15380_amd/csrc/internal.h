@@ -298,6 +298,8 @@ struct BackwardArgs {
   void* gh;                 // dE/dh [N][3F]
   void* scratch;            // per-atom intermediates [N][scratch_w]
   int scratch_w;
+  void* xbuf;               // operand buffers in global memory for tiles too wide for the LDS
+  size_t xbuf_bytes;
   void* eg;                 // [E][NW][4] per-edge partials dE/dd, dE/drhat
   double* gr;               // [E][3] dE/dr per edge
   double* forces;           // [N][3] output

@@ -931,10 +931,29 @@ static int forces_scratch_width(const Hyper& hp) {
   return zw > hp.F ? zw : hp.F;
 }
 
+// Operand buffers in global memory, for reverse tile kernels whose 16-row
+// tiles do not fit the LDS: [16][3F + 1] per update / phi tile (FP64 at
+// F = 384), [2][16][widest head layer + 2] per heads workgroup.
+static size_t forces_xbuf_bytes(int prec, const Hyper& hp, int N) {
+  const size_t eb = elem_bytes(prec), F = hp.F, tiles = ((size_t)N + 15) / 16;
+  size_t x = 0;
+  if (16 * (4 * F + 2) * eb > 160 * 1024) x = tiles * 16 * (3 * F + 1) * eb;
+  int wmax = hp.F;
+  for (int d : hp.shared_dims) wmax = wmax > pad32(d) ? wmax : pad32(d);
+  for (size_t mm = 0; mm + 1 < hp.branch_dims.size(); ++mm)
+    wmax = wmax > pad32(hp.branch_dims[mm]) ? wmax : pad32(hp.branch_dims[mm]);
+  const size_t hb = (size_t)2 * 16 * (wmax + 2) * eb;
+  if (hb > 150 * 1024) {
+    const size_t h = (tiles + hp.n_heads) * hb;
+    x = x > h ? x : h;
+  }
+  return x;
+}
+
 static size_t forces_workspace_bytes(int prec, const Hyper& hp, int N, long long E, int kcols) {
   const size_t eb = elem_bytes(prec), ab = acc_bytes(prec), n = (size_t)N, F = hp.F;
   auto al = [](size_t x) { return (x + 255) & ~(size_t)255; };
-  return al(SaveLayout::bytes(n, F, hp.L, eb)) + 2 * al(n * F * ab) + 3 * al(n * 3 * F * ab) +
+  return al(forces_xbuf_bytes(prec, hp, N)) + al(SaveLayout::bytes(n, F, hp.L, eb)) + 2 * al(n * F * ab) + 3 * al(n * 3 * F * ab) +
          2 * al(((size_t)E + 16) * kcols * eb) + al((size_t)E * 4 * ab) + al((size_t)E * (F / 16) * 4 * ab) +
          al(n * forces_scratch_width(hp) * ab) + al((size_t)E * 3 * sizeof(double));
 }
@@ -1017,16 +1036,6 @@ painn_status painn_forces(painn_ctx* ctx, const painn_model* model, const painn_
   if (precision != PAINN_FP64 && precision != PAINN_FP32) return fail(ctx, PAINN_E_ARG, "unknown precision");
   const Hyper& hp = model->hp;
   const size_t eb = elem_bytes(precision);
-  if ((size_t)16 * (4 * hp.F + 2) * eb > 160 * 1024)
-    return fail(ctx, PAINN_E_UNSUPPORTED, "feature width too large for the FP64 reverse pass");
-  {
-    int wmax = hp.F;
-    for (int d : hp.shared_dims) wmax = wmax > pad32(d) ? wmax : pad32(d);
-    for (size_t mm = 0; mm + 1 < hp.branch_dims.size(); ++mm)
-      wmax = wmax > pad32(hp.branch_dims[mm]) ? wmax : pad32(hp.branch_dims[mm]);
-    if ((size_t)2 * 16 * (wmax + 1) * eb > 150 * 1024)
-      return fail(ctx, PAINN_E_UNSUPPORTED, "head layers too wide for the reverse heads kernel");
-  }
   if (graph->B == 0) return PAINN_OK;
   (void)hipSetDevice(ctx->device);
   painn_graph* g = const_cast<painn_graph*>(graph);
@@ -1081,6 +1090,8 @@ painn_status painn_forces(painn_ctx* ctx, const painn_model* model, const painn_
   auto al = [](size_t x) { return (x + 255) & ~(size_t)255; };
   char* p = (char*)ctx->bws;
   BackwardArgs b{};
+  b.xbuf_bytes = forces_xbuf_bytes(precision, hp, g->N);
+  b.xbuf = p; p += al(b.xbuf_bytes);
   b.save = p; p += al(SaveLayout::bytes(N, F, hp.L, eb));
   b.gs = p; p += al(N * F * ab);
   b.gs2 = p; p += al(N * F * ab);

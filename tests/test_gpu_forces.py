@@ -116,6 +116,21 @@ def test_feature_widths(rt, F):
     run_case(rt, hp, W, b, "fp32", f"F={F} fp32")
 
 
+@pytest.mark.parametrize("precision", ["fp64", "fp32"])
+def test_lead_width_and_wide_heads(rt, precision):
+    """The lead model's width (F = 337, run at 384) with per-dataset heads
+    wider than the reverse heads kernel's LDS tiles in FP64 (600-wide
+    layers): the operand buffers then live in global memory."""
+    say(f"F = 337, wide heads, {precision}")
+    hp = synth.HyperParams(F=337, K=4, L=2, n_species=85, n_heads=3, cutoff=5.0,
+                           shared_dims=[50], branch_dims=[600, 600, 1], rbf_type=RBF_BESSEL,
+                           max_neighbors=10)
+    W = synth.make_weights(hp, 3500)
+    b = synth.make_batch("screening", 0, 10)
+    b.dataset_id = b.dataset_id % hp.n_heads
+    run_case(rt, hp, W, b, precision, f"F=337 wide heads {precision}", cap=10, ds=True)
+
+
 def test_single_linear_head_and_lone_atoms(rt):
     """A one-layer head (dE/ds is its weight row) and structures whose atoms
     have no neighbour (zero force)."""
