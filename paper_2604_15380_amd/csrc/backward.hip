@@ -176,7 +176,10 @@ __global__ void __launch_bounds__(256) k_edge_rev(long long E, int K, int kcols,
 // One workgroup per tile of 16 atoms of one head (the forward's grouping):
 // the layers' pre-activations are recomputed (kept in the per-atom scratch),
 // then dE/ds = W_0^T (silu'(z_0) * W_1^T (... silu'(z_{n-2}) * w_out)).
-constexpr int HB_NW = 4;
+// Waves per workgroup: 16 for wide head layers (the two activation buffers
+// fill most of the LDS, so one workgroup per CU must bring the occupancy),
+// 4 for narrow ones.
+constexpr int HB_NW_WIDE = 16, HB_NW_NARROW = 4, HB_WIDE = 256;
 
 struct HeadBwdArgs {
   int N, ns, nb, F;
@@ -202,7 +205,7 @@ __device__ __forceinline__ typename P::A packed_w0(const DenseDev& L, int k) {
   return P::ld(((const typename P::T*)L.w)[((size_t)kb * 64 + 16 * (r / P::KPL)) * P::KPL + r % P::KPL]);
 }
 
-template <class P, int F>
+template <class P, int F, int NW>
 __device__ void heads_bwd_tile(const HeadBwdArgs& a, int head, const int* idx, typename P::T* const* Y,
                                int lane) {
   using T = typename P::T;
@@ -246,7 +249,7 @@ __device__ void heads_bwd_tile(const HeadBwdArgs& a, int head, const int* idx, t
   for (int m = 0; m + 1 < nl; ++m) {
     const DenseDev L = layer(m, false);
     T* dst = Y[cur ^ 1];
-    dense_tiles<P, 1, HB_NW>(Y[cur], a.ldw, L, [&](int ct, C* acc) {
+    dense_tiles<P, 1, NW>(Y[cur], a.ldw, L, [&](int ct, C* acc) {
       const int col = ct * 16 + (lane & 15);
       const A bias = ((const A*)L.b)[col];
       for (int i = 0; i < 4; ++i) {
@@ -274,7 +277,7 @@ __device__ void heads_bwd_tile(const HeadBwdArgs& a, int head, const int* idx, t
   for (int m = nl - 2; m >= 0; --m) {
     const DenseDev LT = layer(m, true);
     T* dst = Y[cur ^ 1];
-    dense_tiles<P, 1, HB_NW>(Y[cur], a.ldw, LT, [&](int ct, C* acc) {
+    dense_tiles<P, 1, NW>(Y[cur], a.ldw, LT, [&](int ct, C* acc) {
       const int col = ct * 16 + (lane & 15);
       for (int i = 0; i < 4; ++i) {
         const int r = P::row(lane, i);
@@ -295,8 +298,8 @@ __device__ void heads_bwd_tile(const HeadBwdArgs& a, int head, const int* idx, t
 
 // GX: the two activation buffers live in global memory (a region per
 // workgroup) when they do not fit the LDS.
-template <class P, int F, bool GX>
-__global__ void __launch_bounds__(64 * HB_NW) k_heads_bwd(HeadBwdArgs a) {
+template <class P, int F, bool GX, int NW>
+__global__ void __launch_bounds__(64 * NW) k_heads_bwd(HeadBwdArgs a) {
   using T = typename P::T;
   constexpr int TM = 16;
   extern __shared__ __attribute__((aligned(16))) unsigned char smem[];
@@ -322,7 +325,7 @@ __global__ void __launch_bounds__(64 * HB_NW) k_heads_bwd(HeadBwdArgs a) {
       idx[threadIdx.x] = k < end ? (a.order ? a.order[k] : k) : -1;
     }
     __syncthreads();
-    heads_bwd_tile<P, F>(a, head, idx, Y, lane);
+    heads_bwd_tile<P, F, NW>(a, head, idx, Y, lane);
   }
 }
 // ----------------------------------------------------------- update, back ----
@@ -335,7 +338,15 @@ __global__ void __launch_bounds__(64 * HB_NW) k_heads_bwd(HeadBwdArgs a) {
 //   g_U[c] = g_v[c] a_vv + g_s a_sv V[c],  g_V[c] = g_s a_sv U[c] + g_n V[c] / |V|
 //   g_v after the message [c] = g_v[c] + [U^T | V^T] [g_U[c] ; g_V[c]]
 // The per-atom scratch holds g_n.
-constexpr int UB_NW = 4;
+// Waves per workgroup of the reverse update and phi kernels: 4, or more
+// where the LDS tile leaves room for only one workgroup per CU (measured:
+// 16 for FP32; 8 for FP64, whose 3F-wide operands then sit in global memory).
+template <class P, int F>
+constexpr int ub_nw() {
+  return (size_t)16 * (4 * F + 2 * P::PAD) * sizeof(typename P::T) > 64 * 1024
+             ? (sizeof(typename P::T) == 8 ? 8 : 16)
+             : 4;
+}
 
 struct UpdBwdArgs {
   int N;
@@ -356,7 +367,7 @@ struct UpdBwdArgs {
 // workgroup; the MFMA operand reads go through the caches) when 16 rows of
 // 4F do not fit the LDS (FP64 at F = 384).
 template <class P, int F, bool GX>
-__global__ void __launch_bounds__(64 * UB_NW) k_update_bwd(UpdBwdArgs a) {
+__global__ void __launch_bounds__((64 * ub_nw<P, F>())) k_update_bwd(UpdBwdArgs a) {
   using T = typename P::T;
   using A = typename P::A;
   using C = typename P::C;
@@ -397,7 +408,7 @@ __global__ void __launch_bounds__(64 * UB_NW) k_update_bwd(UpdBwdArgs a) {
   }
   __syncthreads();
   // g_z = (W2a^T g_a) * silu'(z) into R2
-  dense_tiles<P, 1, UB_NW, 3 * F / P::KC>(R1, LD1, a.upd2T, [&](int ct, C* acc) {
+  dense_tiles<P, 1, ub_nw<P, F>(), 3 * F / P::KC>(R1, LD1, a.upd2T, [&](int ct, C* acc) {
     const int col = ct * 16 + (lane & 15);
     for (int i = 0; i < 4; ++i) {
       const int r = P::row(lane, i);
@@ -409,7 +420,7 @@ __global__ void __launch_bounds__(64 * UB_NW) k_update_bwd(UpdBwdArgs a) {
   __syncthreads();
   // [g_s' ; g_n] = W1a^T g_z
   A* gs_out = (A*)a.gs_out;
-  dense_tiles<P, 1, UB_NW, F / P::KC>(R2, LD2, a.upd1T, [&](int ct, C* acc) {
+  dense_tiles<P, 1, ub_nw<P, F>(), F / P::KC>(R2, LD2, a.upd1T, [&](int ct, C* acc) {
     const int col = ct * 16 + (lane & 15);
     for (int i = 0; i < 4; ++i) {
       const int r = P::row(lane, i);
@@ -440,7 +451,7 @@ __global__ void __launch_bounds__(64 * UB_NW) k_update_bwd(UpdBwdArgs a) {
       R1[r * LD1 + F + f] = P::st(gV);
     }
     __syncthreads();
-    dense_tiles<P, 1, UB_NW, 2 * F / P::KC>(R1, LD1, a.uvT, [&](int ct, C* acc) {
+    dense_tiles<P, 1, ub_nw<P, F>(), 2 * F / P::KC>(R1, LD1, a.uvT, [&](int ct, C* acc) {
       const int col = ct * 16 + (lane & 15);
       for (int i = 0; i < 4; ++i) {
         const int r = P::row(lane, i);
@@ -470,7 +481,7 @@ struct PhiBwdArgs {
 };
 
 template <class P, int F, bool GX>
-__global__ void __launch_bounds__(64 * UB_NW) k_phi_bwd(PhiBwdArgs a) {
+__global__ void __launch_bounds__((64 * ub_nw<P, F>())) k_phi_bwd(PhiBwdArgs a) {
   using T = typename P::T;
   using A = typename P::A;
   using C = typename P::C;
@@ -493,7 +504,7 @@ __global__ void __launch_bounds__(64 * UB_NW) k_phi_bwd(PhiBwdArgs a) {
     R1[r * LD1 + f] = P::st(row0 + r < (size_t)N ? gh[(row0 + r) * 3 * F + f] : A(0));
   }
   __syncthreads();
-  dense_tiles<P, 1, UB_NW, F / P::KC>(R2, LD2, a.phi1, [&](int ct, C* acc) {
+  dense_tiles<P, 1, ub_nw<P, F>(), F / P::KC>(R2, LD2, a.phi1, [&](int ct, C* acc) {
     const int col = ct * 16 + (lane & 15);
     const A bias = ((const A*)a.phi1.b)[col];
     for (int i = 0; i < 4; ++i) {
@@ -502,7 +513,7 @@ __global__ void __launch_bounds__(64 * UB_NW) k_phi_bwd(PhiBwdArgs a) {
     }
   });
   __syncthreads();
-  dense_tiles<P, 1, UB_NW, 3 * F / P::KC>(R1, LD1, a.phi2T, [&](int ct, C* acc) {
+  dense_tiles<P, 1, ub_nw<P, F>(), 3 * F / P::KC>(R1, LD1, a.phi2T, [&](int ct, C* acc) {
     const int col = ct * 16 + (lane & 15);
     for (int i = 0; i < 4; ++i) {
       const int r = P::row(lane, i);
@@ -514,7 +525,7 @@ __global__ void __launch_bounds__(64 * UB_NW) k_phi_bwd(PhiBwdArgs a) {
   __syncthreads();
   const A* gm = (const A*)a.gs_mid;
   A* go = (A*)a.gs_out;
-  dense_tiles<P, 1, UB_NW, F / P::KC>(R2, LD2, a.phi1T, [&](int ct, C* acc) {
+  dense_tiles<P, 1, ub_nw<P, F>(), F / P::KC>(R2, LD2, a.phi1T, [&](int ct, C* acc) {
     const int col = ct * 16 + (lane & 15);
     for (int i = 0; i < 4; ++i) {
       const size_t g = row0 + P::row(lane, i);
@@ -897,7 +908,10 @@ hipError_t backward_impl(hipStream_t st, BackwardArgs& ba) {
     ha.xbuf = ba.xbuf;
     const bool hgx = (size_t)2 * 16 * ha.ldw * sizeof(T) > 150 * 1024;
     const size_t smem = hgx ? 0 : (size_t)2 * 16 * ha.ldw * sizeof(T);
-    e = hgx ? hipSuccess : allow_lds(k_heads_bwd<P, F, false>, smem);
+    const bool wide = wmax >= HB_WIDE;
+    e = hgx ? hipSuccess
+            : (wide ? allow_lds(k_heads_bwd<P, F, false, HB_NW_WIDE>, smem)
+                    : allow_lds(k_heads_bwd<P, F, false, HB_NW_NARROW>, smem));
     if (e != hipSuccess) return e;
     int grid;
     if (ba.dataset_id) {
@@ -912,8 +926,9 @@ hipError_t backward_impl(hipStream_t st, BackwardArgs& ba) {
       grid = (N + 15) / 16;
     }
     if (hgx && (size_t)grid * 2 * 16 * ha.ldw * sizeof(T) > ba.xbuf_bytes) return hipErrorInvalidValue;
-    if (hgx) k_heads_bwd<P, F, true><<<grid, 64 * HB_NW, 0, st>>>(ha);
-    else k_heads_bwd<P, F, false><<<grid, 64 * HB_NW, smem, st>>>(ha);
+    if (hgx) k_heads_bwd<P, F, true, HB_NW_WIDE><<<grid, 64 * HB_NW_WIDE, 0, st>>>(ha);
+    else if (wide) k_heads_bwd<P, F, false, HB_NW_WIDE><<<grid, 64 * HB_NW_WIDE, smem, st>>>(ha);
+    else k_heads_bwd<P, F, false, HB_NW_NARROW><<<grid, 64 * HB_NW_NARROW, smem, st>>>(ha);
   }
   prof_mark(ba.prof, st, KC_BWD_HEADS, false);
   const int tiles = (N + 15) / 16;
@@ -936,7 +951,7 @@ hipError_t backward_impl(hipStream_t st, BackwardArgs& ba) {
     ua.xbuf = ba.xbuf;
     if (UGX && (size_t)tiles * 16 * (3 * F + P::PAD) * sizeof(T) > ba.xbuf_bytes) return hipErrorInvalidValue;
     prof_mark(ba.prof, st, KC_BWD_UPDATE, true);
-    k_update_bwd<P, F, UGX><<<tiles, 64 * UB_NW, smem_ub, st>>>(ua);
+    k_update_bwd<P, F, UGX><<<tiles, 64 * ub_nw<P, F>(), smem_ub, st>>>(ua);
     prof_mark(ba.prof, st, KC_BWD_UPDATE, false);
     MsgBwdArgs ma;
     ma.N = N;
@@ -972,7 +987,7 @@ hipError_t backward_impl(hipStream_t st, BackwardArgs& ba) {
       pa.phi2T = Ld.phi2T;
       pa.xbuf = ba.xbuf;
       prof_mark(ba.prof, st, KC_BWD_PHI, true);
-      k_phi_bwd<P, F, UGX><<<tiles, 64 * UB_NW, smem_ub, st>>>(pa);
+      k_phi_bwd<P, F, UGX><<<tiles, 64 * ub_nw<P, F>(), smem_ub, st>>>(pa);
       prof_mark(ba.prof, st, KC_BWD_PHI, false);
     }
   }
