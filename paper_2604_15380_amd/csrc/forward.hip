@@ -122,27 +122,16 @@ __device__ __forceinline__ int acc_to_index(double x) { return (int)x; }
 // Once per forward: geometry and radial basis of every edge.
 //   r = (x_j - x_i) + (n0 a + n1 b) + n2 c  (FP64),  d = |r|,  rhat = r / d,
 //   f_c = (cos(pi d / r_c) + 1) / 2,  g_k = exp(-gamma (d - k Delta)^2).
+// Edge e's geometry and basis row into g (LDS), its rhat and sender into einfo.
 template <class P>
-__global__ void __launch_bounds__(256) k_edge_prep(long long E, int K, int kcols, double rc, int rbf,
-                                                  double gamma, double delta,
-                                                  const int32_t* __restrict__ recv,
-                                                  const int32_t* __restrict__ col,
-                                                  const int32_t* __restrict__ shift,
-                                                  const int32_t* __restrict__ atom_struct,
-                                                  const double* __restrict__ pos,
-                                                  const double* __restrict__ cell,
-                                                  typename P::T* __restrict__ basis,
-                                                  typename P::A* __restrict__ einfo) {
-  using T = typename P::T;
+__device__ __forceinline__ void edge_row(long long e, int K, int kcols, double rc, int rbf, double gamma,
+                                         double delta, const int32_t* __restrict__ recv,
+                                         const int32_t* __restrict__ col, const int32_t* __restrict__ shift,
+                                         const int32_t* __restrict__ atom_struct,
+                                         const double* __restrict__ pos, const double* __restrict__ cell,
+                                         typename P::T* g, typename P::A* __restrict__ einfo) {
   using A = typename P::A;
   constexpr bool SPLIT = P::KC == 32;
-  const long long e = blockIdx.x * (long long)blockDim.x + threadIdx.x;
-  if (e >= E + 16) return;
-  T* g = basis + (size_t)e * kcols;
-  if (e >= E) {                                  // padding rows read by partial chunks
-    for (int k = 0; k < kcols; ++k) g[k] = P::st(0);
-    return;
-  }
   const int i = recv[e], j = col[e], sh = shift[e];
   const double* Cl = cell + 9 * atom_struct[i];
   const double n0 = (double)(int8_t)(sh & 0xff), n1 = (double)(int8_t)((sh >> 8) & 0xff),
@@ -159,22 +148,57 @@ __global__ void __launch_bounds__(256) k_edge_prep(long long E, int K, int kcols
   o[3] = index_to_acc<A>(j);                     // the sender index, bit-exact
   const A dd = (A)d;
   const A fc = (A)(d < rc ? 0.5 * (cos(d * (3.14159265358979323846 / rc)) + 1.0) : 0.0);
-  for (int k = 0; k < kcols; ++k) {
-    const bool lo = SPLIT && k > K;
-    const int kk = lo ? k - (K + 1) : k;
-    A val = 0;
-    if (kk < K && rbf == 0) {                    // Gaussian
-      const A t = dd - (A)(kk * delta);
+  // each value once; BF16 also writes its remainder term at K + 1 + k
+  for (int k = 0; k <= K; ++k) {
+    A val = fc;
+    if (k < K && rbf == 0) {                     // Gaussian
+      const A t = dd - (A)(k * delta);
       val = P::ex(-(A)gamma * t * t) * fc;
-    } else if (kk < K) {                         // Bessel: sin(n pi d / r_c) / d
-      const A arg = (A)((kk + 1) * (3.14159265358979323846 / rc)) * dd;
+    } else if (k < K) {                          // Bessel: sin(n pi d / r_c) / d
+      const A arg = (A)((k + 1) * (3.14159265358979323846 / rc)) * dd;
       val = (sizeof(A) == 8 ? (A)sin((double)arg) : (A)sinf((float)arg)) / dd * fc;
-    } else if (kk == K) {
-      val = fc;
     }
-    g[k] = lo ? P::st(val - P::ld(P::st(val))) : P::st(val);
+    g[k] = P::st(val);
+    if constexpr (SPLIT) g[K + 1 + k] = P::st(val - P::ld(P::st(val)));
   }
+  for (int k = SPLIT ? 2 * (K + 1) : K + 1; k < kcols; ++k) g[k] = P::st(0);
 }
+
+// A workgroup of EP_THREADS edges builds its rows in LDS (one row per
+// thread), then writes the block's contiguous slice of the basis with
+// 16-byte stores (the rows are 48-320 bytes: written per thread they would
+// scatter one element per lane per store).
+constexpr int EP_THREADS = 64;   // one wave: <= 35 KiB of LDS at the largest row
+
+template <class P>
+__global__ void __launch_bounds__(EP_THREADS) k_edge_prep(long long E, int K, int kcols, double rc, int rbf,
+                                                  double gamma, double delta,
+                                                  const int32_t* __restrict__ recv,
+                                                  const int32_t* __restrict__ col,
+                                                  const int32_t* __restrict__ shift,
+                                                  const int32_t* __restrict__ atom_struct,
+                                                  const double* __restrict__ pos,
+                                                  const double* __restrict__ cell,
+                                                  typename P::T* __restrict__ basis,
+                                                  typename P::A* __restrict__ einfo) {
+  using T = typename P::T;
+  extern __shared__ __attribute__((aligned(16))) unsigned char ep_smem[];
+  const long long e0 = blockIdx.x * (long long)EP_THREADS;
+  const long long e = e0 + threadIdx.x;
+  const long long rows = (E + 16 - e0) < EP_THREADS ? (E + 16 - e0) : EP_THREADS;
+  T* g = (T*)ep_smem + (size_t)threadIdx.x * kcols;
+  // rows E .. E+15 are zero (read by partial chunks)
+  if (e < E) edge_row<P>(e, K, kcols, rc, rbf, gamma, delta, recv, col, shift, atom_struct, pos, cell, g, einfo);
+  else if (e < E + 16)
+    for (int k = 0; k < kcols; ++k) g[k] = P::st(0);
+  __syncthreads();
+  // kcols * sizeof(T) is a multiple of 16, so the slice is whole uint4s
+  const size_t n16 = (size_t)rows * kcols * sizeof(T) / 16;
+  const uint4* src = (const uint4*)ep_smem;
+  uint4* dst = (uint4*)(basis + (size_t)e0 * kcols);
+  for (size_t x = threadIdx.x; x < n16; x += EP_THREADS) dst[x] = src[x];
+}
+
 
 // Per layer.  A workgroup owns MSG_RB consecutive receivers and NW waves;
 // wave w owns the feature tiles ft = w + NW q (q < FTW) and keeps their
@@ -332,22 +356,26 @@ constexpr int update_waves() {
   return F == 128 ? 3 : F == 64 ? (P::PREC == PAINN_FP64 ? 2 : 3) : (P::PREC == PAINN_FP64 ? 1 : 2);
 }
 
-// Waves of an update workgroup: 4, or F / 64 above F = 256 (each wave keeps
-// the same 4 feature tiles in registers as at F = 256).
-template <int F>
+// Waves of an update workgroup: 4; above F = 128 two feature tiles per
+// wave (F / 32 waves): the LDS tile then allows few workgroups per CU, so
+// the waves of one workgroup must bring the occupancy (measured faster).
+template <class P, int F>
 constexpr int update_nw() {
-  return F > 256 ? F / 64 : 4;
+  return F <= 128 ? 4 : F / 32;
 }
 
+// The saving variant (forces) stores U, V, z, a as it goes and runs at no
+// more than two waves per SIMD (the stores' addresses need registers).
 template <class P, int F, int RT, bool FUSE_PHI, bool SAVE>
-__global__ void __launch_bounds__(64 * update_nw<F>()) __attribute__((amdgpu_waves_per_eu(update_waves<P, F>())))
+__global__ void __launch_bounds__((64 * update_nw<P, F>()))
+__attribute__((amdgpu_waves_per_eu(SAVE && update_waves<P, F>() > 2 ? 2 : update_waves<P, F>())))
 k_update(UpdArgs a) {
   using T = typename P::T;
   using A = typename P::A;
   using C = typename P::C;
   using Fr = typename P::Fr;
   constexpr int NFT = F / 16;        // feature tiles
-  constexpr int NW = update_nw<F>();
+  constexpr int NW = update_nw<P, F>();
   constexpr int FTW = NFT / NW;      // per wave
   constexpr int TM = 16 * RT;        // atoms per workgroup
   constexpr int LD1 = F + P::PAD, LD2 = 2 * F + P::PAD;
@@ -358,8 +386,11 @@ k_update(UpdArgs a) {
   const int N = a.N;
   const T* s = (const T*)a.s;
   const T* v = (const T*)a.v;
-  T* s_out = (T*)a.s_out;
-  T* v_out = (T*)a.v_out;
+  // without SAVE the update runs in place (s_out == s, v_out == v): one
+  // pointer each, so the compiler sees that the loads and stores meet only
+  // element by element
+  T* s_out = SAVE ? (T*)a.s_out : (T*)a.s;
+  T* v_out = SAVE ? (T*)a.v_out : (T*)a.v;
   for (int x = threadIdx.x; x < TM * F; x += blockDim.x) {
     const int r = x / F, c = x % F;
     SN[r * LD2 + c] = row0 + r < (size_t)N ? s[(row0 + r) * F + c] : P::st(0);
@@ -515,7 +546,9 @@ k_update(UpdArgs a) {
 // the epilogue of the layer before it as a dot product, so the widest hidden
 // layer never goes through LDS.  Every atom's result depends only on its own
 // row, so the grouping order does not change any value.
-constexpr int HEADS_NW = 8;   // waves per heads workgroup
+// Waves per heads workgroup: 8, or 16 when a head layer is at least 256
+// wide (its LDS buffers then allow one workgroup per CU; measured faster).
+constexpr int HEADS_NW = 8, HEADS_NW_WIDE = 16, HEADS_WIDE = 256;
 
 static_assert(sizeof(HeadPlan) <= 1024, "head plan workspace is 1 KiB");
 static_assert(sizeof(HeadTile) == 16, "head tile workspace is 16 bytes per tile");
@@ -652,8 +685,8 @@ __device__ __forceinline__ typename P::A packed_row0(const DenseDev& L, int k) {
 // LDS: X [TM][F+PAD] (the tile's final s), SA/SB [TM][lds_s] (shared
 // layers), B0/B1 [TM][lds_b] (stored branch hidden layers); with shared
 // layers B0 reuses X, which is dead after the first of them.
-template <class P, int F, int RT>
-__global__ void __launch_bounds__(64 * HEADS_NW) k_heads(HeadArgs a) {
+template <class P, int F, int RT, int NW>
+__global__ void __launch_bounds__(64 * NW) k_heads(HeadArgs a) {
   using T = typename P::T;
   using A = typename P::A;
   using C = typename P::C;
@@ -661,7 +694,7 @@ __global__ void __launch_bounds__(64 * HEADS_NW) k_heads(HeadArgs a) {
   extern __shared__ __attribute__((aligned(16))) unsigned char smem[];
   T* lds = (T*)smem;
   __shared__ int idx[TM];
-  __shared__ A part[HEADS_NW][TM];
+  __shared__ A part[NW][TM];
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   int head = 0, begin, end;
   if (a.tiles) {
@@ -694,7 +727,7 @@ __global__ void __launch_bounds__(64 * HEADS_NW) k_heads(HeadArgs a) {
     T* dst = lds + ((m & 1) ? a.off_sb : a.off_sa);
     const int ld = a.lds_s;
     const DenseDev& L = a.shared[m];
-    dense_tiles<P, RT, HEADS_NW>(S, ld_S, L, [&](int ct, C* acc) {
+    dense_tiles<P, RT, NW>(S, ld_S, L, [&](int ct, C* acc) {
       const int col = ct * 16 + (lane & 15);
       const A bias = ((const A*)L.b)[col];
       for (int r = 0; r < RT; ++r)
@@ -731,7 +764,7 @@ __global__ void __launch_bounds__(64 * HEADS_NW) k_heads(HeadArgs a) {
       T* dst = lds + ((m & 1) ? a.off_b1 : a.off_b0);
       const int ld = a.lds_b;
       const DenseDev L = branch(m);
-      dense_tiles<P, RT, HEADS_NW>(in, ld_in, L, [&](int ct, C* acc) {
+      dense_tiles<P, RT, NW>(in, ld_in, L, [&](int ct, C* acc) {
         const int col = ct * 16 + (lane & 15);
         const A bias = ((const A*)L.b)[col];
         for (int r = 0; r < RT; ++r)
@@ -748,7 +781,7 @@ __global__ void __launch_bounds__(64 * HEADS_NW) k_heads(HeadArgs a) {
     A p[RT][4];
     for (int r = 0; r < RT; ++r)
       for (int i = 0; i < 4; ++i) p[r][i] = 0;
-    dense_tiles<P, RT, HEADS_NW>(in, ld_in, L, [&](int ct, C* acc) {
+    dense_tiles<P, RT, NW>(in, ld_in, L, [&](int ct, C* acc) {
       const int col = ct * 16 + (lane & 15);
       const A bias = ((const A*)L.b)[col];
       const A wz = packed_row0<P>(Lz, col);
@@ -765,7 +798,7 @@ __global__ void __launch_bounds__(64 * HEADS_NW) k_heads(HeadArgs a) {
     __syncthreads();
     if (rt < TM) {
       y = ((const A*)Lz.b)[0];
-      for (int w = 0; w < HEADS_NW; ++w) y += part[w][rt];
+      for (int w = 0; w < NW; ++w) y += part[w][rt];
     }
   }
   if (rt < TM && idx[rt] >= 0) {
@@ -1187,11 +1220,11 @@ __global__ void __launch_bounds__(256) k_blend_reduce(int N, int H, A skip, cons
 }
 
 // Dynamic LDS beyond 64 KiB must be allowed once per kernel.
-template <class P, int F, int RT>
+template <class P, int F, int RT, int NW>
 hipError_t heads_allow_lds(size_t smem) {
   static size_t allowed = 64 * 1024;
   if (smem <= allowed) return hipSuccess;
-  hipError_t e = hipFuncSetAttribute((const void*)k_heads<P, F, RT>,
+  hipError_t e = hipFuncSetAttribute((const void*)k_heads<P, F, RT, NW>,
                                      hipFuncAttributeMaxDynamicSharedMemorySize, (int)smem);
   if (e != hipSuccess) {
     (void)hipGetLastError();
@@ -1202,10 +1235,11 @@ hipError_t heads_allow_lds(size_t smem) {
 }
 
 template <class P, int F, int RT>
-hipError_t launch_heads_rt(hipStream_t st, HeadArgs& ha, int grid, size_t smem) {
-  hipError_t e = heads_allow_lds<P, F, RT>(smem);
+hipError_t launch_heads_rt(hipStream_t st, HeadArgs& ha, int grid, size_t smem, bool wide) {
+  hipError_t e = wide ? heads_allow_lds<P, F, RT, HEADS_NW_WIDE>(smem) : heads_allow_lds<P, F, RT, HEADS_NW>(smem);
   if (e != hipSuccess) return e;
-  k_heads<P, F, RT><<<grid, 64 * HEADS_NW, smem, st>>>(ha);
+  if (wide) k_heads<P, F, RT, HEADS_NW_WIDE><<<grid, 64 * HEADS_NW_WIDE, smem, st>>>(ha);
+  else k_heads<P, F, RT, HEADS_NW><<<grid, 64 * HEADS_NW, smem, st>>>(ha);
   return hipGetLastError();
 }
 
@@ -1265,7 +1299,7 @@ hipError_t launch_heads(hipStream_t st, ForwardArgs& fa) {
   for (; RT >= 1; RT /= 2) {
     const int TM = 16 * RT;
     smem = layout(TM);
-    const size_t fixed = (size_t)TM * sizeof(int) + (size_t)HEADS_NW * TM * sizeof(A);
+    const size_t fixed = (size_t)TM * sizeof(int) + (size_t)HEADS_NW_WIDE * TM * sizeof(A);
     if (smem + fixed <= LDS_LIMIT) break;
   }
   if (RT < 1) return hipErrorInvalidValue;
@@ -1325,9 +1359,13 @@ hipError_t launch_heads(hipStream_t st, ForwardArgs& fa) {
     ha.plan = nullptr;
   }
   hipError_t e;
-  if (RT == 4) e = launch_heads_rt<P, F, 4>(st, ha, grid, smem);
-  else if (RT == 2) e = launch_heads_rt<P, F, 2>(st, ha, grid, smem);
-  else e = launch_heads_rt<P, F, 1>(st, ha, grid, smem);
+  int hmax = 0;   // widest hidden head layer
+  for (int d : hp.shared_dims) hmax = hmax > d ? hmax : d;
+  for (size_t m = 0; m + 1 < hp.branch_dims.size(); ++m) hmax = hmax > hp.branch_dims[m] ? hmax : hp.branch_dims[m];
+  const bool wide = hmax >= HEADS_WIDE;
+  if (RT == 4) e = launch_heads_rt<P, F, 4>(st, ha, grid, smem, wide);
+  else if (RT == 2) e = launch_heads_rt<P, F, 2>(st, ha, grid, smem, wide);
+  else e = launch_heads_rt<P, F, 1>(st, ha, grid, smem, wide);
   if (e == hipSuccess && fa.blend)
     k_blend_reduce<A><<<(N + 255) / 256, 256, 0, st>>>(N, H, (A)fa.skip, fa.g->atom_struct, (const A*)fa.hw,
                                                         (const A*)fa.eh, (A*)fa.e);
@@ -1376,7 +1414,8 @@ hipError_t forward_impl(hipStream_t st, ForwardArgs& fa) {
   if (N > 0 && fa.stop_layer >= 0) {
     prof_mark(fa.prof, st, KC_EDGE_PREP, true);
     const double delta = hp.cutoff / (hp.K - 1);
-    k_edge_prep<P><<<(unsigned)((g->E + 16 + 255) / 256), 256, 0, st>>>(
+    k_edge_prep<P><<<(unsigned)((g->E + 16 + EP_THREADS - 1) / EP_THREADS), EP_THREADS,
+                     (size_t)EP_THREADS * kcols * sizeof(T), st>>>(
         g->E, hp.K, kcols, hp.cutoff, hp.rbf_type, 1.0 / (2.0 * delta * delta), delta, g->recv, g->col, g->shift,
         g->atom_struct, g->pos, g->cell, (T*)fa.basis, (A*)fa.einfo);
     prof_mark(fa.prof, st, KC_EDGE_PREP, false);
@@ -1423,11 +1462,11 @@ hipError_t forward_impl(hipStream_t st, ForwardArgs& fa) {
     }
     // the saving variants exist for the reverse pass (FP64 / FP32)
     if (fa.save && sizeof(T) != 2) {
-      if (fuse) k_update<P, F, URT, true, sizeof(T) != 2><<<ugrid, 64 * update_nw<F>(), 0, st>>>(ua);
-      else k_update<P, F, URT, false, sizeof(T) != 2><<<ugrid, 64 * update_nw<F>(), 0, st>>>(ua);
+      if (fuse) k_update<P, F, URT, true, sizeof(T) != 2><<<ugrid, 64 * update_nw<P, F>(), 0, st>>>(ua);
+      else k_update<P, F, URT, false, sizeof(T) != 2><<<ugrid, 64 * update_nw<P, F>(), 0, st>>>(ua);
     } else {
-      if (fuse) k_update<P, F, URT, true, false><<<ugrid, 64 * update_nw<F>(), 0, st>>>(ua);
-      else k_update<P, F, URT, false, false><<<ugrid, 64 * update_nw<F>(), 0, st>>>(ua);
+      if (fuse) k_update<P, F, URT, true, false><<<ugrid, 64 * update_nw<P, F>(), 0, st>>>(ua);
+      else k_update<P, F, URT, false, false><<<ugrid, 64 * update_nw<P, F>(), 0, st>>>(ua);
     }
     prof_mark(fa.prof, st, KC_UPDATE, false);
   }
