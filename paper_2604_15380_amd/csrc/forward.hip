@@ -347,21 +347,22 @@ struct UpdArgs {
   void* save_a;
 };
 
-// Waves per SIMD the update kernel is compiled for: three at F = 128, where
-// the registers allow it without spilling and three 256-thread workgroups
-// still fit the 160 KiB of LDS; at F = 256 the measured best is two (one in
-// FP64, whose accumulators need the whole register file).
+// Waves per SIMD the update kernel is compiled for: four at F = 128 (three
+// in FP64), where the registers allow it without spilling; at F >= 256 the
+// measured best is two (one in FP64, whose accumulators need the whole
+// register file).
 template <class P, int F>
 constexpr int update_waves() {
-  return F == 128 ? 3 : F == 64 ? (P::PREC == PAINN_FP64 ? 2 : 3) : (P::PREC == PAINN_FP64 ? 1 : 2);
+  return F == 128 ? (P::PREC == PAINN_FP64 ? 3 : 4) : F == 64 ? (P::PREC == PAINN_FP64 ? 2 : 3) : (P::PREC == PAINN_FP64 ? 1 : 2);
 }
 
-// Waves of an update workgroup: 4; above F = 128 two feature tiles per
-// wave (F / 32 waves): the LDS tile then allows few workgroups per CU, so
-// the waves of one workgroup must bring the occupancy (measured faster).
+// Waves of an update workgroup: 4 at F = 64, 8 at F = 128 (one feature tile
+// each), F / 32 above (two tiles each): the LDS tile allows few workgroups
+// per CU, so the waves of one workgroup must bring the occupancy (measured
+// faster at every width).
 template <class P, int F>
 constexpr int update_nw() {
-  return F <= 128 ? 4 : F / 32;
+  return F < 128 ? 4 : F == 128 ? 8 : F / 32;
 }
 
 // The saving variant (forces) stores U, V, z, a as it goes and runs at no
