@@ -90,9 +90,13 @@ def readout_grad(s, W, hp, dataset_id: int):
     return g
 
 
-def structure_forces(pos, species, cell, pbc, dataset_id, hp, W):
+def structure_forces(pos, species, cell, pbc, dataset_id, hp, W, head_weights=None):
     """Energy and forces of one structure.  Returns dict(E=float, F=[n, 3],
-    n_edges=int)."""
+    n_edges=int).  With `head_weights` (one weight per head, 0 for a skipped
+    head) the energy is the blend sum_h w_h E_h of every head over the shared
+    final features (section "Composition-conditioned branch weighting"); the
+    weights depend on the composition only, so the readout gradient is
+    sum_h w_h dE_h/ds."""
     F, K, rc = hp.F, hp.K, hp.cutoff
     z = np.asarray(species)
     x = np.asarray(pos, dtype=np.float64)
@@ -136,10 +140,17 @@ def structure_forces(pos, species, cell, pbc, dataset_id, hp, W):
         v = v_mid + a_vv[:, None, :] * U
         s = s_mid + a_sv * UV + a_ss
     from .painn import readout
-    E = float(np.sum(readout(s, W, hp, dataset_id)))
+    if head_weights is None:
+        E = float(np.sum(readout(s, W, hp, dataset_id)))
+        gs = readout_grad(s, W, hp, dataset_id)
+    else:
+        E, gs = 0.0, np.zeros_like(s)
+        for h, wh in enumerate(head_weights):
+            if wh != 0.0:
+                E += wh * float(np.sum(readout(s, W, hp, h)))
+                gs = gs + wh * readout_grad(s, W, hp, h)
 
     # reverse
-    gs = readout_grad(s, W, hp, dataset_id)
     gv = np.zeros((n, 3, F))
     gd = np.zeros(len(recv))
     grh = np.zeros((len(recv), 3))
@@ -184,6 +195,18 @@ def structure_forces(pos, species, cell, pbc, dataset_id, hp, W):
     np.add.at(dEdx, send, g_r)
     np.subtract.at(dEdx, recv, g_r)
     return dict(E=E, F=-dEdx, n_edges=len(recv))
+
+
+def structure_forces_blend(pos, species, cell, pbc, hp, W, skip: float = 0.0):
+    """Blended-head energy and forces: the branch-weighting MLP's weights of
+    the structure's composition, heads below `skip` left out (not
+    renormalised).  Returns dict(E, F, w)."""
+    from .painn import blend_weights, composition
+    w = blend_weights(composition(species, hp.n_species), hp, W)
+    kept = np.where(w >= skip, w, 0.0)
+    out = structure_forces(pos, species, cell, pbc, 0, hp, W, head_weights=kept)
+    out["w"] = w
+    return out
 
 
 def batch_forces(batch, hp, W, structures=None):

@@ -145,3 +145,50 @@ def test_dimer_action_reaction_along_the_bond():
     F3 = structure_forces(x3, np.array([1, 2, 0]), NO_CELL, NO_PBC, 0, hp, W)["F"]
     assert np.all(F3[2] == 0.0)
     assert np.allclose(F3[:2], Fo, rtol=1e-13, atol=0)
+
+
+def _blend_hp():
+    return synth.HyperParams(F=6, K=5, L=2, n_species=4, n_heads=3, cutoff=5.0, shared_dims=[5],
+                             branch_dims=[4, 1], blend_dims=[6])
+
+
+def test_blended_forces_match_central_differences():
+    """Blended heads (section "Composition-conditioned branch weighting"):
+    the forces of E = sum_h w_h E_h, with the weights fixed by the
+    composition, against differences of the oracle's blended energy."""
+    from oracle.forces import structure_forces_blend
+    from oracle.painn import structure_forward_blend
+    hp = _blend_hp()
+    W = synth.make_weights(hp, 77)
+    rng = np.random.default_rng(21)
+    x = molecule(rng, 7)
+    z = rng.integers(0, hp.n_species, 7)
+    for skip in (0.0, 0.3):
+        out = structure_forces_blend(x, z, NO_CELL, NO_PBC, hp, W, skip=skip)
+        E0 = structure_forward_blend(x, z, NO_CELL, NO_PBC, hp, W, skip=skip)["E"]
+        assert out["E"] == pytest.approx(E0, rel=1e-13, abs=1e-13)
+        h = 1e-5
+        num = np.zeros_like(x)
+        for a in range(x.shape[0]):
+            for c in range(3):
+                xp, xm = x.copy(), x.copy()
+                xp[a, c] += h
+                xm[a, c] -= h
+                num[a, c] = -(structure_forward_blend(xp, z, NO_CELL, NO_PBC, hp, W, skip=skip)["E"]
+                              - structure_forward_blend(xm, z, NO_CELL, NO_PBC, hp, W, skip=skip)["E"]) / (2 * h)
+        assert np.abs(out["F"] - num).max() <= 2e-7 * np.abs(out["F"]).max()
+
+
+def test_blended_forces_are_the_weighted_head_forces():
+    """With the weights of a structure, the blended forces equal the weighted
+    sum of the per-head forces (the encoder and the graph are shared)."""
+    from oracle.forces import structure_forces_blend
+    hp = _blend_hp()
+    W = synth.make_weights(hp, 78)
+    rng = np.random.default_rng(22)
+    x = molecule(rng, 6)
+    z = rng.integers(0, hp.n_species, 6)
+    out = structure_forces_blend(x, z, NO_CELL, NO_PBC, hp, W)
+    per_head = [structure_forces(x, z, NO_CELL, NO_PBC, h, hp, W)["F"] for h in range(hp.n_heads)]
+    ref = sum(w * Fh for w, Fh in zip(out["w"], per_head))
+    assert np.allclose(out["F"], ref, rtol=1e-12, atol=1e-14)
