@@ -189,14 +189,16 @@ def main():
     if args.blend and hp.blend_dims is None:
         print(f"--blend needs a model with a branch-weighting MLP ({name} has none)", file=sys.stderr)
         sys.exit(2)
-    if args.forces and (args.blend or prec == "bf16"):
-        print("--forces runs the dataset-id heads in FP64 or FP32", file=sys.stderr)
+    if args.forces and prec == "bf16":
+        print("--forces runs in FP64 or FP32", file=sys.stderr)
         sys.exit(2)
     fout = torch.empty((batch.n_atoms, 3), dtype=torch.float64, device=rt.device)
 
     def step():
         rt.build_graph(inp, hp.cutoff, graph=graph, max_neighbors=hp.max_neighbors)
-        if args.forces:
+        if args.forces and args.blend:
+            rt.forces_blend(model, graph, prec, skip=args.skip, energies=out, forces=fout)
+        elif args.forces:
             rt.forces(model, graph, prec, dataset_id=ds, energies=out, forces=fout)
         elif args.blend:
             rt.forward_blend(model, graph, prec, skip=args.skip, out=out)

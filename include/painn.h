@@ -220,6 +220,14 @@ painn_status painn_forces(painn_ctx* ctx, const painn_model* model, const painn_
                           const int32_t* dataset_id, painn_precision precision, double* energies,
                           double* forces);
 
+/* Energies and forces with every head blended (as painn_forward_blend): the
+ * head weights w_bh depend on the composition only, so the forces are
+ * -sum over kept heads of w_bh dE_bh/dx.  Arguments and errors as
+ * painn_forward_blend and painn_forces (weights may be NULL). */
+painn_status painn_forces_blend(painn_ctx* ctx, const painn_model* model, const painn_graph* graph,
+                                painn_precision precision, double skip_threshold, double* energies,
+                                double* forces, double* weights);
+
 /* Test hook: run layers 0..layer (layer = -1: embedding only) and write the
  * scalar features s [N,F] and vector features v [N,3,F] (float64) reached
  * there.  Same arguments and errors as painn_forward. */

@@ -14,7 +14,8 @@ EXPORTS = [
     "painn_status_string", "painn_synchronize", "painn_model_load",
     "painn_model_load_buffer", "painn_model_info", "painn_model_options", "painn_model_free",
     "painn_build_graph", "painn_build_graph_capped", "painn_graph_csr", "painn_graph_free", "painn_forward",
-    "painn_forward_blend", "painn_forward_features", "painn_forces", "painn_profile_enable",
+    "painn_forward_blend", "painn_forward_features", "painn_forces", "painn_forces_blend",
+    "painn_profile_enable",
     "painn_profile_read",
 ]
 
@@ -43,6 +44,7 @@ _SIGS = {
     "painn_forward_blend": ([_P, _P, _P, ctypes.c_int, ctypes.c_double, _P, _P], ctypes.c_int),
     "painn_forward_features": ([_P, _P, _P, ctypes.c_int, _I32, _P, _P], ctypes.c_int),
     "painn_forces": ([_P, _P, _P, _P, ctypes.c_int, _P, _P], ctypes.c_int),
+    "painn_forces_blend": ([_P, _P, _P, ctypes.c_int, ctypes.c_double, _P, _P, _P], ctypes.c_int),
     "painn_profile_enable": ([_P, ctypes.c_int], ctypes.c_int),
     "painn_profile_read": ([_P, _I32, ctypes.POINTER(ctypes.c_char_p), ctypes.POINTER(ctypes.c_double),
                             ctypes.POINTER(ctypes.c_int64), ctypes.POINTER(_I32)], ctypes.c_int),
@@ -190,6 +192,12 @@ def painn_forces(ctx: int, model: int, graph: int, dataset_id: int | None, preci
                  energies: int | None, forces: int | None) -> None:
     _check(load_library().painn_forces(ctx, model, graph, dataset_id or None, precision,
                                        energies or None, forces or None), ctx)
+
+
+def painn_forces_blend(ctx: int, model: int, graph: int, precision: int, skip_threshold: float,
+                       energies: int | None, forces: int | None, weights: int | None) -> None:
+    _check(load_library().painn_forces_blend(ctx, model, graph, precision, float(skip_threshold),
+                                             energies or None, forces or None, weights or None), ctx)
 
 
 def painn_forward_features(ctx: int, model: int, graph: int, precision: int, layer: int,

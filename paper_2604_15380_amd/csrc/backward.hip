@@ -197,6 +197,8 @@ struct HeadBwdArgs {
   int sw;
   void* xbuf;                    // GX: per-workgroup [2][16][ldw] buffers in global memory
   void* gs;                      // out: dE/ds [N][F]
+  void* gh;                      // blended heads: out dE_h/ds [N][H][F] instead
+  int H;
 };
 
 template <class P>
@@ -205,6 +207,8 @@ __device__ __forceinline__ typename P::A packed_w0(const DenseDev& L, int k) {
   return P::ld(((const typename P::T*)L.w)[((size_t)kb * 64 + 16 * (r / P::KPL)) * P::KPL + r % P::KPL]);
 }
 
+// The layers' pre-activations of a 16-row sub-tile go to the workgroup's own
+// scratch rows (an atom can sit in several tiles at once: one per kept head).
 template <class P, int F, int NW>
 __device__ void heads_bwd_tile(const HeadBwdArgs& a, int head, const int* idx, typename P::T* const* Y,
                                int lane) {
@@ -228,12 +232,14 @@ __device__ void heads_bwd_tile(const HeadBwdArgs& a, int head, const int* idx, t
     L.dout_p = pad32(L.dout);
     return L;
   };
+  // the output row of atom g: dE/ds, or dE_h/ds of this head when blended
   A* gs = (A*)a.gs;
+  auto out_row = [&](int g) { return a.gh ? (A*)a.gh + ((size_t)g * a.H + head) * F : gs + (size_t)g * F; };
   const DenseDev Lout = layer(nl - 1, false);
   if (nl == 1) {
     for (int x = threadIdx.x; x < TM * F; x += blockDim.x) {
       const int r = x / F, c = x % F;
-      if (idx[r] >= 0) gs[(size_t)idx[r] * F + c] = c < Lout.din ? packed_w0<P>(Lout, c) : A(0);
+      if (idx[r] >= 0) out_row(idx[r])[c] = c < Lout.din ? packed_w0<P>(Lout, c) : A(0);
     }
     return;
   }
@@ -255,7 +261,7 @@ __device__ void heads_bwd_tile(const HeadBwdArgs& a, int head, const int* idx, t
       for (int i = 0; i < 4; ++i) {
         const int r = P::row(lane, i);
         const A z = acc[0][i] + bias;
-        if (idx[r] >= 0) scr[(size_t)idx[r] * a.sw + a.zoff[m] + col] = z;
+        if (idx[r] >= 0) scr[((size_t)blockIdx.x * TM + r) * a.sw + a.zoff[m] + col] = z;
         dst[r * a.ldw + col] = P::st(col < L.dout ? silu<A>(z) : A(0));
       }
     });
@@ -269,7 +275,7 @@ __device__ void heads_bwd_tile(const HeadBwdArgs& a, int head, const int* idx, t
     for (int x = threadIdx.x; x < TM * w; x += blockDim.x) {
       const int r = x / w, c = x % w;
       A dl = 0;
-      if (idx[r] >= 0 && c < Lout.din) dl = packed_w0<P>(Lout, c) * dsilu<A>(scr[(size_t)idx[r] * a.sw + a.zoff[m] + c]);
+      if (idx[r] >= 0 && c < Lout.din) dl = packed_w0<P>(Lout, c) * dsilu<A>(scr[((size_t)blockIdx.x * TM + r) * a.sw + a.zoff[m] + c]);
       Y[cur][r * a.ldw + c] = P::st(dl);
     }
   }
@@ -283,10 +289,10 @@ __device__ void heads_bwd_tile(const HeadBwdArgs& a, int head, const int* idx, t
         const int r = P::row(lane, i);
         const int g = idx[r];
         if (m == 0) {
-          if (g >= 0 && col < F) gs[(size_t)g * F + col] = acc[0][i];
+          if (g >= 0 && col < F) out_row(g)[col] = acc[0][i];
         } else {
           A dl = 0;
-          if (g >= 0 && col < LT.dout) dl = acc[0][i] * dsilu<A>(scr[(size_t)g * a.sw + a.zoff[m - 1] + col]);
+          if (g >= 0 && col < LT.dout) dl = acc[0][i] * dsilu<A>(scr[((size_t)blockIdx.x * TM + r) * a.sw + a.zoff[m - 1] + col]);
           dst[r * a.ldw + col] = P::st(dl);
         }
       }
@@ -307,27 +313,47 @@ __global__ void __launch_bounds__(64 * NW) k_heads_bwd(HeadBwdArgs a) {
   T* Y[2] = {base, base + TM * a.ldw};
   __shared__ int idx[TM];
   const int lane = threadIdx.x & 63;
-  int head = 0, begin, end;
-  if (a.order) {
-    if ((int)blockIdx.x >= a.plan->n_tiles) return;
-    const HeadTile tl = a.tiles[blockIdx.x];
-    head = tl.head;
-    begin = tl.begin;
-    end = tl.end;
-  } else {
-    begin = blockIdx.x * TM;
-    end = min(a.N, begin + TM);
-  }
-  for (int sub = begin; sub < end; sub += TM) {
-    __syncthreads();
-    if (threadIdx.x < TM) {
-      const int k = sub + threadIdx.x;
-      idx[threadIdx.x] = k < end ? (a.order ? a.order[k] : k) : -1;
+  // a persistent grid: workgroup b takes tiles b, b + gridDim.x, ...
+  const int ntiles = a.order ? a.plan->n_tiles : (a.N + TM - 1) / TM;
+  for (int t = blockIdx.x; t < ntiles; t += gridDim.x) {
+    int head = 0, begin, end;
+    if (a.order) {
+      const HeadTile tl = a.tiles[t];
+      head = tl.head;
+      begin = tl.begin;
+      end = tl.end;
+    } else {
+      begin = t * TM;
+      end = min(a.N, begin + TM);
     }
-    __syncthreads();
-    heads_bwd_tile<P, F, NW>(a, head, idx, Y, lane);
+    for (int sub = begin; sub < end; sub += TM) {
+      __syncthreads();
+      if (threadIdx.x < TM) {
+        const int k = sub + threadIdx.x;
+        idx[threadIdx.x] = k < end ? (a.order ? a.order[k] : k) : -1;
+      }
+      __syncthreads();
+      heads_bwd_tile<P, F, NW>(a, head, idx, Y, lane);
+    }
   }
 }
+// Blended heads: dE/ds = sum over kept heads h (w_bh >= skip) of w_bh dE_h/ds,
+// in head order.
+template <class A>
+__global__ void __launch_bounds__(256) k_blend_grad(int N, int H, int F, A skip, const int32_t* __restrict__ atom_struct,
+                                                   const A* __restrict__ hw, const A* __restrict__ gh,
+                                                   A* __restrict__ gs) {
+  const size_t tot = (size_t)N * F;
+  for (size_t x = blockIdx.x * (size_t)blockDim.x + threadIdx.x; x < tot; x += (size_t)gridDim.x * blockDim.x) {
+    const size_t i = x / F, f = x % F;
+    const A* w = hw + (size_t)atom_struct[i] * H;
+    A y = 0;
+    for (int h = 0; h < H; ++h)
+      if (w[h] >= skip) y += w[h] * gh[(i * H + h) * F + f];
+    gs[x] = y;
+  }
+}
+
 // ----------------------------------------------------------- update, back ----
 // Tile of 16 atoms, 4 waves; LDS R1 [16][3F + PAD], R2 [16][F + PAD].  The
 // forward saved U v[c], V v[c], the gate's pre-activation z and a_vv, a_sv,
@@ -906,6 +932,8 @@ hipError_t backward_impl(hipStream_t st, BackwardArgs& ba) {
     ha.sw = ba.scratch_w;
     ha.gs = ba.gs;
     ha.xbuf = ba.xbuf;
+    ha.gh = ba.blend ? ba.g_heads : nullptr;
+    ha.H = hp.n_heads;
     const bool hgx = (size_t)2 * 16 * ha.ldw * sizeof(T) > 150 * 1024;
     const size_t smem = hgx ? 0 : (size_t)2 * 16 * ha.ldw * sizeof(T);
     const bool wide = wmax >= HB_WIDE;
@@ -914,21 +942,29 @@ hipError_t backward_impl(hipStream_t st, BackwardArgs& ba) {
                     : allow_lds(k_heads_bwd<P, F, false, HB_NW_NARROW>, smem));
     if (e != hipSuccess) return e;
     int grid;
-    if (ba.dataset_id) {
+    if (ba.dataset_id || ba.blend) {
+      // the forward's grouping: tiles of atoms of one head (blended: of
+      // every kept (atom, head) entry)
       ha.order = ba.head_order;
       ha.tiles = (const HeadTile*)ba.head_tiles;
       ha.plan = (const HeadPlan*)ba.head_plan;
-      grid = (N + 15) / 16 + hp.n_heads;   // at least the forward's tile count
+      grid = (int)(((long long)N * (ba.blend ? hp.n_heads : 1) + 15) / 16) + hp.n_heads;   // >= its tile count
+      grid = grid < HB_GRID ? grid : HB_GRID;
     } else {
       ha.order = nullptr;
       ha.tiles = nullptr;
       ha.plan = nullptr;
       grid = (N + 15) / 16;
+      grid = grid < HB_GRID ? grid : HB_GRID;
     }
     if (hgx && (size_t)grid * 2 * 16 * ha.ldw * sizeof(T) > ba.xbuf_bytes) return hipErrorInvalidValue;
     if (hgx) k_heads_bwd<P, F, true, HB_NW_WIDE><<<grid, 64 * HB_NW_WIDE, 0, st>>>(ha);
     else if (wide) k_heads_bwd<P, F, false, HB_NW_WIDE><<<grid, 64 * HB_NW_WIDE, smem, st>>>(ha);
     else k_heads_bwd<P, F, false, HB_NW_NARROW><<<grid, 64 * HB_NW_NARROW, smem, st>>>(ha);
+    if (ba.blend)
+      k_blend_grad<A><<<grid_of((size_t)N * F, 256), 256, 0, st>>>(N, hp.n_heads, F, (A)ba.skip, g->atom_struct,
+                                                                    (const A*)ba.hw, (const A*)ba.g_heads,
+                                                                    (A*)ba.gs);
   }
   prof_mark(ba.prof, st, KC_BWD_HEADS, false);
   const int tiles = (N + 15) / 16;

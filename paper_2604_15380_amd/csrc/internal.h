@@ -303,9 +303,18 @@ struct BackwardArgs {
   void* eg;                 // [E][NW][4] per-edge partials dE/dd, dE/drhat
   double* gr;               // [E][3] dE/dr per edge
   double* forces;           // [N][3] output
+  // blended heads: the forward's head weights [B][H] (accumulation type),
+  // the skip threshold, and per-(atom, head) dE/ds slots [N][H][F]
+  bool blend;
+  double skip;
+  const void* hw;
+  void* g_heads;
   Profiler* prof;
 };
 hipError_t launch_backward(hipStream_t s, int prec, BackwardArgs& a);
+// workgroups of the reverse heads kernel (a persistent grid; each has its
+// own 16 scratch rows and, for wide layers, its own operand buffers)
+constexpr int HB_GRID = 2048;
 // the sender-grouped edge list of a graph
 hipError_t launch_transpose(hipStream_t s, Profiler* p, painn_graph* g);
 size_t forward_workspace_bytes(int prec, int N, long long E, int F, int kcols, int B, int H,

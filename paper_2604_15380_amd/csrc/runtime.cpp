@@ -934,8 +934,9 @@ static int forces_scratch_width(const Hyper& hp) {
 // Operand buffers in global memory, for reverse tile kernels whose 16-row
 // tiles do not fit the LDS: [16][3F + 1] per update / phi tile (FP64 at
 // F = 384), [2][16][widest head layer + 2] per heads workgroup.
-static size_t forces_xbuf_bytes(int prec, const Hyper& hp, int N) {
+static size_t forces_xbuf_bytes(int prec, const Hyper& hp, int N, bool blend) {
   const size_t eb = elem_bytes(prec), F = hp.F, tiles = ((size_t)N + 15) / 16;
+  const size_t head_tiles = ((size_t)N * (blend ? hp.n_heads : 1) + 15) / 16;
   size_t x = 0;
   if (16 * (4 * F + 2) * eb > 160 * 1024) x = tiles * 16 * (3 * F + 1) * eb;
   int wmax = hp.F;
@@ -944,18 +945,25 @@ static size_t forces_xbuf_bytes(int prec, const Hyper& hp, int N) {
     wmax = wmax > pad32(hp.branch_dims[mm]) ? wmax : pad32(hp.branch_dims[mm]);
   const size_t hb = (size_t)2 * 16 * (wmax + 2) * eb;
   if (hb > 150 * 1024) {
-    const size_t h = (tiles + hp.n_heads) * hb;
+    const size_t grid = head_tiles + hp.n_heads < (size_t)HB_GRID ? head_tiles + hp.n_heads : (size_t)HB_GRID;
+    const size_t h = grid * hb;
     x = x > h ? x : h;
   }
   return x;
 }
 
-static size_t forces_workspace_bytes(int prec, const Hyper& hp, int N, long long E, int kcols) {
+// per-atom rows, or the reverse heads kernel's 16 rows per workgroup
+static size_t forces_scratch_rows(int N) {
+  return (size_t)N > (size_t)HB_GRID * 16 ? (size_t)N : (size_t)HB_GRID * 16;
+}
+
+static size_t forces_workspace_bytes(int prec, const Hyper& hp, int N, long long E, int kcols, bool blend) {
   const size_t eb = elem_bytes(prec), ab = acc_bytes(prec), n = (size_t)N, F = hp.F;
   auto al = [](size_t x) { return (x + 255) & ~(size_t)255; };
-  return al(forces_xbuf_bytes(prec, hp, N)) + al(SaveLayout::bytes(n, F, hp.L, eb)) + 2 * al(n * F * ab) + 3 * al(n * 3 * F * ab) +
+  return al(forces_xbuf_bytes(prec, hp, N, blend)) + al(blend ? n * hp.n_heads * F * ab : 0) +
+         al(SaveLayout::bytes(n, F, hp.L, eb)) + 2 * al(n * F * ab) + 3 * al(n * 3 * F * ab) +
          2 * al(((size_t)E + 16) * kcols * eb) + al((size_t)E * 4 * ab) + al((size_t)E * (F / 16) * 4 * ab) +
-         al(n * forces_scratch_width(hp) * ab) + al((size_t)E * 3 * sizeof(double));
+         al(forces_scratch_rows(N) * forces_scratch_width(hp) * ab) + al((size_t)E * 3 * sizeof(double));
 }
 
 // Transposed layers for the reverse pass (from the FP64 master weights).
@@ -1024,9 +1032,9 @@ static painn_status build_prec_T(painn_model* m, PrecModel* pm) {
   return PAINN_OK;
 }
 
-painn_status painn_forces(painn_ctx* ctx, const painn_model* model, const painn_graph* graph,
-                          const int32_t* dataset_id, painn_precision precision, double* energies,
-                          double* forces) {
+static painn_status forces_impl(painn_ctx* ctx, const painn_model* model, const painn_graph* graph,
+                                const int32_t* dataset_id, painn_precision precision, double* energies,
+                                double* forces, bool blend, double skip, double* weights) {
   if (!ctx) return PAINN_E_ARG;
   ctx->err.clear();
   if (!model || !graph) return fail(ctx, PAINN_E_ARG, "null model or graph");
@@ -1070,7 +1078,7 @@ painn_status painn_forces(painn_ctx* ctx, const painn_model* model, const painn_
     g->t_valid = true;
   }
   const int kcols = pm->layers[0].filt_mma.din_p;
-  const size_t need = forces_workspace_bytes(precision, hp, g->N, g->E, kcols);
+  const size_t need = forces_workspace_bytes(precision, hp, g->N, g->E, kcols, blend);
   if (need > ctx->bws_bytes) {
     if (ctx->bws) {
       (void)hipStreamSynchronize(ctx->stream);
@@ -1090,8 +1098,9 @@ painn_status painn_forces(painn_ctx* ctx, const painn_model* model, const painn_
   auto al = [](size_t x) { return (x + 255) & ~(size_t)255; };
   char* p = (char*)ctx->bws;
   BackwardArgs b{};
-  b.xbuf_bytes = forces_xbuf_bytes(precision, hp, g->N);
+  b.xbuf_bytes = forces_xbuf_bytes(precision, hp, g->N, blend);
   b.xbuf = p; p += al(b.xbuf_bytes);
+  b.g_heads = p; p += al(blend ? N * hp.n_heads * F * ab : 0);
   b.save = p; p += al(SaveLayout::bytes(N, F, hp.L, eb));
   b.gs = p; p += al(N * F * ab);
   b.gs2 = p; p += al(N * F * ab);
@@ -1103,11 +1112,11 @@ painn_status painn_forces(painn_ctx* ctx, const painn_model* model, const painn_
   b.einfo_t = p; p += al((size_t)g->E * 4 * ab);
   b.eg = p; p += al((size_t)g->E * (F / 16) * 4 * ab);
   b.scratch_w = forces_scratch_width(hp);
-  b.scratch = p; p += al(N * b.scratch_w * ab);
+  b.scratch = p; p += al(forces_scratch_rows(g->N) * b.scratch_w * ab);
   b.gr = (double*)p;
   ForwardArgs fa{};
   painn_status st = run_forward(ctx, model, graph, dataset_id, precision, hp.L - 1, energies, nullptr, nullptr,
-                                false, 0.0, nullptr, b.save, &fa);
+                                blend, skip, weights, b.save, &fa);
   if (st != PAINN_OK) return st;
   b.m = m;
   b.pm = pm;
@@ -1119,6 +1128,9 @@ painn_status painn_forces(painn_ctx* ctx, const painn_model* model, const painn_
   b.head_tiles = fa.head_tiles;
   b.head_order = fa.head_order;
   b.forces = forces;
+  b.blend = blend;
+  b.skip = skip;
+  b.hw = fa.hw;
   b.prof = ctx->prof;
   (void)hipGetLastError();
   hipError_t e = launch_backward(ctx->stream, precision, b);
@@ -1127,6 +1139,24 @@ painn_status painn_forces(painn_ctx* ctx, const painn_model* model, const painn_
     return hip_fail(ctx, e, "reverse pass launch");
   }
   return PAINN_OK;
+}
+
+painn_status painn_forces(painn_ctx* ctx, const painn_model* model, const painn_graph* graph,
+                          const int32_t* dataset_id, painn_precision precision, double* energies,
+                          double* forces) {
+  return forces_impl(ctx, model, graph, dataset_id, precision, energies, forces, false, 0.0, nullptr);
+}
+
+painn_status painn_forces_blend(painn_ctx* ctx, const painn_model* model, const painn_graph* graph,
+                                painn_precision precision, double skip_threshold, double* energies,
+                                double* forces, double* weights) {
+  if (!ctx) return PAINN_E_ARG;
+  if (!model || !graph) return fail(ctx, PAINN_E_ARG, "null model or graph");
+  if (!model->hp.has_blend)
+    return fail(ctx, PAINN_E_UNSUPPORTED, "the model has no branch-weighting MLP");
+  if (!(skip_threshold >= 0.0) || !isfinite(skip_threshold))
+    return fail(ctx, PAINN_E_ARG, "skip_threshold must be finite and >= 0");
+  return forces_impl(ctx, model, graph, nullptr, precision, energies, forces, true, skip_threshold, weights);
 }
 
 painn_status painn_forward(painn_ctx* ctx, const painn_model* model, const painn_graph* graph,

@@ -158,6 +158,22 @@ class Runtime:
                        forces.data_ptr() if forces.numel() else None)
         return energies, forces
 
+    def forces_blend(self, model: Model, graph: Graph, precision="fp32", skip=0.0, energies=None,
+                     forces=None, weights=None):
+        """Energies and forces with every head blended by the model's
+        branch-weighting MLP (heads with weight < skip left out)."""
+        import torch
+        prec = B.PRECISIONS[precision] if isinstance(precision, str) else precision
+        if energies is None:
+            energies = torch.empty(graph.n_struct, dtype=torch.float64, device=self.device)
+        if forces is None:
+            forces = torch.empty((graph.n_atoms, 3), dtype=torch.float64, device=self.device)
+        B.painn_forces_blend(self.ctx, model.handle, graph.handle, prec, skip,
+                             energies.data_ptr() if energies.numel() else None,
+                             forces.data_ptr() if forces.numel() else None,
+                             weights.data_ptr() if weights is not None and weights.numel() else None)
+        return energies, forces
+
     def features(self, model: Model, graph: Graph, layer: int, precision="fp64"):
         import torch
         prec = B.PRECISIONS[precision] if isinstance(precision, str) else precision

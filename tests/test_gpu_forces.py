@@ -131,6 +131,38 @@ def test_lead_width_and_wide_heads(rt, precision):
     run_case(rt, hp, W, b, precision, f"F=337 wide heads {precision}", cap=10, ds=True)
 
 
+@pytest.mark.parametrize("precision,skip", [("fp64", 0.0), ("fp32", 0.0), ("fp32", 0.05)])
+def test_blended_heads(rt, precision, skip):
+    """Blended heads (painn_forces_blend): every kept head's gradient
+    weighted by the branch-weighting MLP's weights, vs the oracle."""
+    import torch
+    from oracle.forces import structure_forces_blend
+    say(f"blended heads, {precision}, skip {skip}")
+    hp = synth.HyperParams(F=64, K=8, L=2, n_species=85, n_heads=4, cutoff=5.0, shared_dims=[24],
+                           branch_dims=[40, 40, 1], blend_dims=[16])
+    W = synth.make_weights(hp, 3600)
+    b = synth.make_batch("screening", 0, 16)
+    m = rt.load_model(synth.weight_file_bytes(hp, W))
+    g = rt.build_graph(rt.upload_batch(b), hp.cutoff)
+    E, Fo = rt.forces_blend(m, g, precision, skip=skip)
+    E0 = rt.forward_blend(m, g, precision, skip=skip)
+    torch.cuda.synchronize()
+    assert np.array_equal(E.cpu().numpy(), E0.cpu().numpy())
+    Fo = Fo.cpu().numpy()
+    ref = [structure_forces_blend(*b.structure(k)[:4], hp, W, skip=skip) for k in range(b.n_struct)]
+    if skip > 0:
+        # heads whose weight sits within rounding of the threshold may be
+        # decided differently in FP32: keep the structures where none does
+        ok = [k for k, o in enumerate(ref) if np.all(np.abs(o["w"] - skip) > 1e-5)]
+        assert len(ok) >= b.n_struct // 2
+        ref = [ref[k] for k in ok]
+    else:
+        ok = list(range(b.n_struct))
+    check_forces(Fo, b, ref, ok, FORCE_TOL[precision], f"blended {precision} skip {skip}")
+    g.free()
+    m.free()
+
+
 def test_single_linear_head_and_lone_atoms(rt):
     """A one-layer head (dE/ds is its weight row) and structures whose atoms
     have no neighbour (zero force)."""
