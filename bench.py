@@ -68,6 +68,9 @@ def kernel_work(kernel: str, hp, N: int, E: int, prec: str, head_entries: int | 
     bwd_update: per atom 22 F^2 (the transposed products W2a^T, W1a^T and
              [U^T|V^T] for 3 components; U, V, the gate come from the forward).
     bwd_phi: per atom 10 F^2 (W1 s recomputed, W2^T, W1^T).
+    bwd_heads: per (atom, head) entry twice the heads' forward flops of every
+             layer but the 1-wide output (the pre-activations recomputed, then
+             the transposed layers).
     """
     F, K, L = hp.F, hp.K, hp.L
     b = ELEM[prec]
@@ -87,6 +90,10 @@ def kernel_work(kernel: str, hp, N: int, E: int, prec: str, head_entries: int | 
     if kernel == "bwd_phi":
         ab = 8 if prec == "fp64" else 4
         return "mfma", N * 10.0 * F * F, N * (F * b + 6.0 * F * ab)
+    if kernel == "bwd_heads":
+        dims = [F] + list(hp.shared_dims) + list(hp.branch_dims)[:-1]
+        n = N if head_entries is None else head_entries
+        return "mfma", n * 2.0 * sum(2.0 * a * c for a, c in zip(dims[:-1], dims[1:])), N * F * b
     if kernel == "heads":
         dims = [F] + list(hp.shared_dims) + list(hp.branch_dims)
         n = N if head_entries is None else head_entries
