@@ -576,7 +576,7 @@ __global__ void __launch_bounds__((64 * ub_nw<P, F>())) k_phi_bwd(PhiBwdArgs a) 
 // leaves the registers.  The per-edge sums over channels are a
 // reduce-scatter across the 16 lanes that share those edges, over the
 // wave's 4 feature tiles; each wave writes its own slot of every edge.
-constexpr int MB_RB = 4;   // senders per workgroup
+constexpr int MB_RB = 4;   // senders per workgroup (2 and 8 measured the same)
 
 struct MsgBwdArgs {
   int N;

@@ -190,6 +190,64 @@ def test_single_linear_head_and_lone_atoms(rt):
     m.free()
 
 
+def test_edge_cases(rt):
+    """A batch without a single edge (every force exactly zero), empty
+    structures between others, and structures without atoms at all."""
+    import torch
+    hp = synth.HyperParams(F=64, K=6, L=2, n_species=4, n_heads=1, cutoff=2.0,
+                           shared_dims=[], branch_dims=[16, 1])
+    W = synth.make_weights(hp, 3700)
+    m = rt.load_model(synth.weight_file_bytes(hp, W))
+    nc, npbc = np.zeros((3, 3)), np.zeros(3, np.uint8)
+    lone = [(np.array([[0.0, 0, 0], [5.0, 0, 0]]), np.array([1, 2]), nc, npbc, 0),
+            (np.array([[0.0, 0, 0]]), np.array([3]), nc, npbc, 0)]
+    pair = (np.array([[0.0, 0, 0], [1.2, 0.4, 0.1], [0.3, 1.1, -0.2]]), np.array([0, 1, 2]), nc, npbc, 0)
+    empty = (np.zeros((0, 3)), np.zeros(0, np.int32), nc, npbc, 0)
+    for label, structs in (("no edges", lone), ("empty structures", [empty, pair, empty, pair, empty]),
+                           ("no atoms", [empty, empty])):
+        b = synth.concat(structs)
+        g = rt.build_graph(rt.upload_batch(b), hp.cutoff)
+        for precision in ("fp64", "fp32"):
+            E, Fo = rt.forces(m, g, precision)
+            E0 = rt.forward(m, g, precision)
+            torch.cuda.synchronize()
+            assert np.array_equal(E.cpu().numpy(), E0.cpu().numpy()), label
+            Fo = Fo.cpu().numpy()
+            assert Fo.shape == (b.n_atoms, 3)
+            if label == "no edges":
+                assert g.n_edges == 0 and np.all(Fo == 0.0)
+            ref = oracle(b, hp, W)
+            check_forces(Fo, b, ref, range(b.n_struct), FORCE_TOL[precision], f"{label} {precision}")
+        g.free()
+    m.free()
+
+
+def test_deterministic_and_graph_rebuild(rt):
+    """Forces are bit-identical from run to run (every sum in a fixed order),
+    and a graph rebuilt in place over another batch regroups its edges by
+    sender before the next forces call."""
+    import torch
+    hp = synth.HyperParams(F=64, K=10, L=2, n_species=10, n_heads=1, cutoff=5.0,
+                           shared_dims=[], branch_dims=[16, 1])
+    W = synth.make_weights(hp, 3800)
+    m = rt.load_model(synth.weight_file_bytes(hp, W))
+    b1 = synth.make_batch("molecules_4096", 0, 30)
+    b2 = synth.make_batch("molecules_4096", 100, 12)
+    g = rt.build_graph(rt.upload_batch(b1), hp.cutoff)
+    runs = []
+    for _ in range(3):
+        _, Fo = rt.forces(m, g, "fp32")
+        torch.cuda.synchronize()
+        runs.append(Fo.cpu().numpy())
+    assert all(np.array_equal(runs[0], r) for r in runs[1:])
+    rt.build_graph(rt.upload_batch(b2), hp.cutoff, graph=g)
+    _, Fo = rt.forces(m, g, "fp64")
+    torch.cuda.synchronize()
+    check_forces(Fo.cpu().numpy(), b2, oracle(b2, hp, W), range(b2.n_struct), FORCE_TOL["fp64"], "rebuilt graph")
+    g.free()
+    m.free()
+
+
 def test_errors(rt):
     from paper_2604_15380_amd import PainnError
     hp = synth.HyperParams(F=64, K=6, L=1, n_species=10, n_heads=1, cutoff=5.0,
