@@ -620,27 +620,29 @@ __device__ __forceinline__ void reduce_scatter16(A* vals, int lane) {
 #ifndef MB_FTW32
 #define MB_FTW32 2
 #endif
-template <class P, int F>
-constexpr int mb_ftw() { return sizeof(typename P::A) == 8 ? 1 : MB_FTW32; }
-template <class P, int F>
-constexpr int mb_wpe() { return mb_ftw<P, F>() * (int)sizeof(typename P::A) / 4 <= 1 ? 4 : 2; }
+// (FP32: one tile when the filter input is at most 3 k-blocks, whose short
+// MFMA chains leave the wave's other work exposed; measured.)
+template <class P, int F, int KBM>
+constexpr int mb_ftw() { return sizeof(typename P::A) == 8 || KBM <= 3 ? 1 : MB_FTW32; }
+template <class P, int F, int KBM>
+constexpr int mb_wpe() { return mb_ftw<P, F, KBM>() * (int)sizeof(typename P::A) / 4 <= 1 ? 4 : 2; }
 // Waves of one feature slice (a workgroup); wide layers take several slices
 // in consecutive workgroups.
-template <class P, int F>
+template <class P, int F, int KBM>
 constexpr int mb_nwb() {
-  constexpr int nw = F / 16 / mb_ftw<P, F>();
+  constexpr int nw = F / 16 / mb_ftw<P, F, KBM>();
   return nw <= 8 ? nw : (nw % 8 == 0 ? 8 : 6);
 }
 
 template <class P, int F, int KBM>
-__global__ void __launch_bounds__((64 * mb_nwb<P, F>())) __attribute__((amdgpu_waves_per_eu(mb_wpe<P, F>())))
+__global__ void __launch_bounds__((64 * mb_nwb<P, F, KBM>())) __attribute__((amdgpu_waves_per_eu(mb_wpe<P, F, KBM>())))
 k_message_bwd(MsgBwdArgs a) {
   using T = typename P::T;
   using A = typename P::A;
   using C = typename P::C;
   using Fr = typename P::Fr;
-  constexpr int FTW = mb_ftw<P, F>(), NFT = F / 16, NW = NFT / FTW;
-  constexpr int NWB = mb_nwb<P, F>(), SLICES = NW / NWB;
+  constexpr int FTW = mb_ftw<P, F, KBM>(), NFT = F / 16, NW = NFT / FTW;
+  constexpr int NWB = mb_nwb<P, F, KBM>(), SLICES = NW / NWB;
   static_assert(NW % NWB == 0, "feature slices");
   constexpr int kcols = KBM * P::KC;
   const int per_xcd = gridDim.x / 8;
@@ -856,16 +858,28 @@ hipError_t allow_lds(K kernel, size_t smem) {
   return hipFuncSetAttribute((const void*)kernel, hipFuncAttributeMaxDynamicSharedMemorySize, (int)smem);
 }
 
+template <class P, int F, int KBM>
+void launch_message_bwd_kbm(hipStream_t st, const MsgBwdArgs& ma) {
+  constexpr int NWB = mb_nwb<P, F, KBM>(), SLICES = F / 16 / mb_ftw<P, F, KBM>() / NWB;
+  const int blocks = (int)(((long long)(ma.N + MB_RB - 1) / MB_RB * SLICES + 7) / 8 * 8);
+  k_message_bwd<P, F, KBM><<<blocks, 64 * NWB, 0, st>>>(ma);
+}
+
+// Per-edge slots of the reverse message kernel (one per wave of a feature
+// slice set), for a filter input of nkb k-blocks.
+template <class P, int F>
+int message_bwd_slots(int nkb) {
+  return F / 16 / (nkb == 3 ? mb_ftw<P, F, 3>() : mb_ftw<P, F, 6>());
+}
+
 template <class P, int F>
 hipError_t launch_message_bwd(hipStream_t st, const MsgBwdArgs& ma, int nkb) {
-  constexpr int NWB = mb_nwb<P, F>(), SLICES = F / 16 / mb_ftw<P, F>() / NWB, TH = 64 * NWB;
-  const int blocks = (int)(((long long)(ma.N + MB_RB - 1) / MB_RB * SLICES + 7) / 8 * 8);
   switch (nkb) {
-    case 3: k_message_bwd<P, F, 3><<<blocks, TH, 0, st>>>(ma); break;
-    case 6: k_message_bwd<P, F, 6><<<blocks, TH, 0, st>>>(ma); break;
-    case 9: k_message_bwd<P, F, 9><<<blocks, TH, 0, st>>>(ma); break;
-    case 12: k_message_bwd<P, F, 12><<<blocks, TH, 0, st>>>(ma); break;
-    case 17: k_message_bwd<P, F, 17><<<blocks, TH, 0, st>>>(ma); break;
+    case 3: launch_message_bwd_kbm<P, F, 3>(st, ma); break;
+    case 6: launch_message_bwd_kbm<P, F, 6>(st, ma); break;
+    case 9: launch_message_bwd_kbm<P, F, 9>(st, ma); break;
+    case 12: launch_message_bwd_kbm<P, F, 12>(st, ma); break;
+    case 17: launch_message_bwd_kbm<P, F, 17>(st, ma); break;
     default: return hipErrorInvalidValue;
   }
   return hipGetLastError();
@@ -880,9 +894,9 @@ hipError_t backward_impl(hipStream_t st, BackwardArgs& ba) {
   const Hyper& hp = ba.m->hp;
   const int N = g->N;
   const long long E = g->E;
-  constexpr int NW = F / 16 / mb_ftw<P, F>();   // per-edge slots (waves of the message kernel)
   const SaveLayout sv(ba.save, N, F, hp.L, sizeof(T));
   const int kcols = pm->layers[0].filt_mma.din_p;
+  const int NW = message_bwd_slots<P, F>(kcols / P::KC);   // per-edge slots (waves of the message kernel)
   if (N == 0) return hipSuccess;
   // LDS of the tile kernels: 16 rows of 3F + F (+ padding), or of F alone
   // with the 3F-wide buffer in global memory
