@@ -50,29 +50,46 @@ __global__ void __launch_bounds__(256) k_t_count(long long E, const int32_t* __r
 }
 
 // One workgroup: exclusive scan of the N counts into t_ptr[0..N], counts
-// reset to 0 (they become the fill cursors).
+// reset to 0 (they become the fill cursors).  Tiles of 4096 counts are read
+// and written coalesced through LDS; a carry runs from tile to tile.
 __global__ void __launch_bounds__(1024) k_t_scan(int N, int32_t* __restrict__ cnt, int32_t* __restrict__ ptr) {
+  constexpr int PER = 4, TILE = 1024 * PER;
+  __shared__ int tile[TILE];
   __shared__ int part[1024];
+  __shared__ int carry_s;
   const int t = threadIdx.x;
-  const int per = (N + 1023) / 1024;
-  const int lo = min(N, t * per), hi = min(N, lo + per);
-  int sum = 0;
-  for (int j = lo; j < hi; ++j) sum += cnt[j];
-  part[t] = sum;
+  if (t == 0) carry_s = 0;
   __syncthreads();
-  for (int o = 1; o < 1024; o <<= 1) {
-    const int x = t >= o ? part[t - o] : 0;
+  for (int base = 0; base < N; base += TILE) {
+    for (int k = t; k < TILE; k += 1024) {
+      const int j = base + k;
+      tile[k] = j < N ? cnt[j] : 0;
+      if (j < N) cnt[j] = 0;
+    }
     __syncthreads();
-    part[t] += x;
+    int sum = 0;
+    for (int k = 0; k < PER; ++k) sum += tile[t * PER + k];
+    part[t] = sum;
+    __syncthreads();
+    for (int o = 1; o < 1024; o <<= 1) {
+      const int x = t >= o ? part[t - o] : 0;
+      __syncthreads();
+      part[t] += x;
+      __syncthreads();
+    }
+    int run = carry_s + part[t] - sum;
+    for (int k = 0; k < PER; ++k) {
+      const int c = tile[t * PER + k];
+      tile[t * PER + k] = run;
+      run += c;
+    }
+    __syncthreads();
+    for (int k = t; k < TILE; k += 1024)
+      if (base + k < N) ptr[base + k] = tile[k];
+    if (t == 1023) carry_s += part[1023];
     __syncthreads();
   }
-  int run = part[t] - sum;
-  for (int j = lo; j < hi; ++j) {
-    ptr[j] = run;
-    run += cnt[j];
-    cnt[j] = 0;
-  }
-  if (t == 1023) ptr[N] = part[1023];
+  if (t == 0) ptr[N] = carry_s;
 }
 
 __global__ void __launch_bounds__(256) k_t_fill(long long E, const int32_t* __restrict__ col,
@@ -110,30 +127,13 @@ __global__ void __launch_bounds__(256) k_t_sort(int N, const int32_t* __restrict
 //   Bessel   g_n' = (n pi / r_c) cos(n pi d / r_c) / d - sin(n pi d / r_c) / d^2.
 // Rows E .. E+15 are zero (read by partial chunks).
 template <class P>
-__global__ void __launch_bounds__(256) k_edge_rev(long long E, int K, int kcols, double rc, int rbf,
-                                                 double gamma, double delta,
-                                                 const int32_t* __restrict__ t_edge,
-                                                 const int32_t* __restrict__ recv,
-                                                 const int32_t* __restrict__ col,
-                                                 const int32_t* __restrict__ shift,
-                                                 const int32_t* __restrict__ atom_struct,
-                                                 const double* __restrict__ pos,
-                                                 const double* __restrict__ cell,
-                                                 const typename P::T* __restrict__ basis,
-                                                 const typename P::A* __restrict__ einfo,
-                                                 typename P::T* __restrict__ basis_t,
-                                                 typename P::T* __restrict__ dbasis_t,
-                                                 typename P::A* __restrict__ einfo_t) {
+__device__ __forceinline__ void edge_rev_row(long long e, int K, int kcols, double rc, int rbf, double gamma,
+                                             double delta, const int32_t* __restrict__ recv,
+                                             const int32_t* __restrict__ col, const int32_t* __restrict__ shift,
+                                             const int32_t* __restrict__ atom_struct,
+                                             const double* __restrict__ pos, const double* __restrict__ cell,
+                                             typename P::T* g) {
   using A = typename P::A;
-  const long long t = blockIdx.x * (long long)blockDim.x + threadIdx.x;
-  if (t >= E + 16) return;
-  typename P::T* g = dbasis_t + (size_t)t * kcols;
-  typename P::T* b = basis_t + (size_t)t * kcols;
-  if (t >= E) {
-    for (int k = 0; k < kcols; ++k) g[k] = b[k] = P::st(0);
-    return;
-  }
-  const int e = t_edge[t];
   const int i = recv[e], j = col[e], sh = shift[e];
   const double* Cl = cell + 9 * atom_struct[i];
   const double n0 = (double)(int8_t)(sh & 0xff), n1 = (double)(int8_t)((sh >> 8) & 0xff),
@@ -162,14 +162,74 @@ __global__ void __launch_bounds__(256) k_edge_rev(long long E, int K, int kcols,
       val = dfc;
     }
     g[k] = P::st(val);
-    b[k] = basis[(size_t)e * kcols + k];
   }
-  A* o = einfo_t + 4 * t;
-  o[0] = einfo[4 * (size_t)e];
-  o[1] = einfo[4 * (size_t)e + 1];
-  o[2] = einfo[4 * (size_t)e + 2];
-  if constexpr (sizeof(A) == 4) o[3] = __int_as_float(i);
-  else o[3] = (A)i;
+}
+
+// A workgroup of EP_REV positions stages its rows in LDS and writes each
+// array's contiguous slice with 16-byte stores (per thread, the 48-272 byte
+// rows would scatter one element per lane per store).
+constexpr int EP_REV = 64;
+
+template <class P>
+__global__ void __launch_bounds__(EP_REV) k_edge_rev(long long E, int K, int kcols, double rc, int rbf,
+                                                    double gamma, double delta,
+                                                    const int32_t* __restrict__ t_edge,
+                                                    const int32_t* __restrict__ recv,
+                                                    const int32_t* __restrict__ col,
+                                                    const int32_t* __restrict__ shift,
+                                                    const int32_t* __restrict__ atom_struct,
+                                                    const double* __restrict__ pos,
+                                                    const double* __restrict__ cell,
+                                                    const typename P::T* __restrict__ basis,
+                                                    const typename P::A* __restrict__ einfo,
+                                                    typename P::T* __restrict__ basis_t,
+                                                    typename P::T* __restrict__ dbasis_t,
+                                                    typename P::A* __restrict__ einfo_t) {
+  using T = typename P::T;
+  using A = typename P::A;
+  extern __shared__ __attribute__((aligned(16))) unsigned char er_smem[];
+  const long long t0 = blockIdx.x * (long long)EP_REV;
+  const long long t = t0 + threadIdx.x;
+  const long long rows = (E + 16 - t0) < EP_REV ? (E + 16 - t0) : EP_REV;
+  const size_t n16 = (size_t)rows * kcols * sizeof(T) / 16;   // kcols * sizeof(T) is a multiple of 16
+  T* g = (T*)er_smem + (size_t)threadIdx.x * kcols;
+  const int e = t < E ? t_edge[t] : -1;
+  // the derivative rows (rows E .. E+15: zero)
+  if (e >= 0) edge_rev_row<P>(e, K, kcols, rc, rbf, gamma, delta, recv, col, shift, atom_struct, pos, cell, g);
+  else if (t < E + 16)
+    for (int k = 0; k < kcols; ++k) g[k] = P::st(0);
+  __syncthreads();
+  {
+    const uint4* src = (const uint4*)er_smem;
+    uint4* dst = (uint4*)(dbasis_t + (size_t)t0 * kcols);
+    for (size_t x = threadIdx.x; x < n16; x += EP_REV) dst[x] = src[x];
+  }
+  __syncthreads();
+  // the forward's basis rows, gathered by edge id (16-byte loads)
+  {
+    const int n = kcols * (int)sizeof(T) / 16;
+    uint4* gl = (uint4*)g;
+    if (e >= 0) {
+      const uint4* src = (const uint4*)(basis + (size_t)e * kcols);
+      for (int x = 0; x < n; ++x) gl[x] = src[x];
+    } else if (t < E + 16) {
+      for (int x = 0; x < n; ++x) gl[x] = make_uint4(0, 0, 0, 0);
+    }
+  }
+  __syncthreads();
+  {
+    const uint4* src = (const uint4*)er_smem;
+    uint4* dst = (uint4*)(basis_t + (size_t)t0 * kcols);
+    for (size_t x = threadIdx.x; x < n16; x += EP_REV) dst[x] = src[x];
+  }
+  if (e >= 0) {
+    A* o = einfo_t + 4 * t;
+    o[0] = einfo[4 * (size_t)e];
+    o[1] = einfo[4 * (size_t)e + 1];
+    o[2] = einfo[4 * (size_t)e + 2];
+    if constexpr (sizeof(A) == 4) o[3] = __int_as_float(recv[e]);
+    else o[3] = (A)recv[e];
+  }
 }
 
 // ------------------------------------------------------------ heads, back ----
@@ -907,7 +967,7 @@ hipError_t backward_impl(hipStream_t st, BackwardArgs& ba) {
   if (e != hipSuccess) return e;
   if (E > 0) {
     const double delta = hp.cutoff / (hp.K - 1);
-    k_edge_rev<P><<<(unsigned)((E + 16 + 255) / 256), 256, 0, st>>>(
+    k_edge_rev<P><<<(unsigned)((E + 16 + EP_REV - 1) / EP_REV), EP_REV, (size_t)EP_REV * kcols * sizeof(T), st>>>(
         E, hp.K, kcols, hp.cutoff, hp.rbf_type, 1.0 / (2.0 * delta * delta), delta, g->t_edge, g->recv, g->col,
         g->shift, g->atom_struct, g->pos, g->cell, (const T*)ba.basis, (const A*)ba.einfo, (T*)ba.basis_t,
         (T*)ba.dbasis, (A*)ba.einfo_t);

@@ -369,7 +369,7 @@ constexpr int update_nw() {
 // more than two waves per SIMD (the stores' addresses need registers).
 template <class P, int F, int RT, bool FUSE_PHI, bool SAVE>
 __global__ void __launch_bounds__((64 * update_nw<P, F>()))
-__attribute__((amdgpu_waves_per_eu(SAVE && update_waves<P, F>() > 2 ? 2 : update_waves<P, F>())))
+__attribute__((amdgpu_waves_per_eu(SAVE && update_waves<P, F>() > 3 ? 3 : update_waves<P, F>())))
 k_update(UpdArgs a) {
   using T = typename P::T;
   using A = typename P::A;
