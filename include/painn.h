@@ -215,7 +215,9 @@ painn_status painn_forward_blend(painn_ctx* ctx, const painn_model* model, const
  * activations (about (20 L + 4) N F values of the precision's storage type
  * plus per-edge buffers) in a context workspace grown on demand.  The first
  * call on a graph also groups its edges by sender (kept until the graph is
- * rebuilt).  Errors: as painn_forward; PAINN_E_UNSUPPORTED for BF16. */
+ * rebuilt).  As in painn_forward, a structure whose dataset id is outside
+ * [0, n_heads) gets NaN energy, and here NaN forces on its atoms.  Errors: as
+ * painn_forward; PAINN_E_UNSUPPORTED for BF16. */
 painn_status painn_forces(painn_ctx* ctx, const painn_model* model, const painn_graph* graph,
                           const int32_t* dataset_id, painn_precision precision, double* energies,
                           double* forces);

@@ -31,9 +31,9 @@ __device__ __forceinline__ A dsilu(A x) {
 }
 
 template <class A>
-__global__ void __launch_bounds__(256) k_fill(size_t n, A* __restrict__ p) {
+__global__ void __launch_bounds__(256) k_fill(size_t n, A* __restrict__ p, A value = A(0)) {
   for (size_t x = blockIdx.x * (size_t)blockDim.x + threadIdx.x; x < n; x += (size_t)gridDim.x * blockDim.x)
-    p[x] = A(0);
+    p[x] = value;
 }
 
 inline int grid_of(size_t n, int per) {
@@ -974,6 +974,13 @@ hipError_t backward_impl(hipStream_t st, BackwardArgs& ba) {
     k_fill<A><<<grid_of((size_t)E * NW * 4, 256), 256, 0, st>>>((size_t)E * NW * 4, (A*)ba.eg);
   }
   k_fill<A><<<grid_of((size_t)N * 3 * F, 256), 256, 0, st>>>((size_t)N * 3 * F, (A*)ba.gv);
+  // With dataset ids, an atom of a structure whose id is outside [0, H) is in
+  // no head tile: its dE/ds stays NaN, so are its structure's forces (as the
+  // forward's energy of that structure).  No edge leaves a structure and
+  // every dense product keeps atoms in their own rows, so it stays there.
+  if (ba.dataset_id && !ba.blend)
+    k_fill<A><<<grid_of((size_t)N * F, 256), 256, 0, st>>>((size_t)N * F, (A*)ba.gs,
+                                                           (A)__builtin_nan(""));
   // heads
   prof_mark(ba.prof, st, KC_BWD_HEADS, true);
   {

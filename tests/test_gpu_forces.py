@@ -248,6 +248,31 @@ def test_deterministic_and_graph_rebuild(rt):
     m.free()
 
 
+def test_dataset_id_out_of_range(rt):
+    """A structure whose dataset id names no head gets NaN energy and NaN
+    forces; the other structures are unaffected."""
+    import torch
+    hp = synth.HyperParams(F=64, K=6, L=2, n_species=85, n_heads=3, cutoff=5.0, shared_dims=[],
+                           branch_dims=[16, 1])
+    W = synth.make_weights(hp, 3900)
+    m = rt.load_model(synth.weight_file_bytes(hp, W))
+    b = synth.make_batch("screening", 0, 8)
+    b.dataset_id = b.dataset_id % hp.n_heads
+    b.dataset_id[3] = 7
+    inp = rt.upload_batch(b)
+    g = rt.build_graph(inp, hp.cutoff)
+    E, Fo = rt.forces(m, g, "fp64", dataset_id=inp["dataset_id"])
+    torch.cuda.synchronize()
+    E, Fo = E.cpu().numpy(), Fo.cpu().numpy()
+    lo, hi = int(b.struct_ptr[3]), int(b.struct_ptr[4])
+    assert np.isnan(E[3]) and np.all(np.isnan(Fo[lo:hi]))
+    keep = [k for k in range(b.n_struct) if k != 3]
+    assert np.all(np.isfinite(np.delete(Fo, np.s_[lo:hi], axis=0)))
+    check_forces(Fo, b, oracle(b, hp, W, keep), keep, FORCE_TOL["fp64"], "other structures")
+    g.free()
+    m.free()
+
+
 def test_errors(rt):
     from paper_2604_15380_amd import PainnError
     hp = synth.HyperParams(F=64, K=6, L=1, n_species=10, n_heads=1, cutoff=5.0,
