@@ -707,7 +707,13 @@ k_message_bwd(MsgBwdArgs a) {
   constexpr int kcols = KBM * P::KC;
   const int per_xcd = gridDim.x / 8;
   const int lb = (blockIdx.x % 8) * per_xcd + blockIdx.x / 8;
-  const int lane = threadIdx.x & 63, wave = (lb % SLICES) * NWB + (threadIdx.x >> 6);
+  const int lane = threadIdx.x & 63;
+  // With one feature tile per wave the register budget is tight (4 waves
+  // per SIMD); a wave index the compiler knows to be uniform moves address
+  // arithmetic to scalar registers.  With two tiles it has room, and the
+  // uniform form measured slower there.
+  const int wave_v = (lb % SLICES) * NWB + (threadIdx.x >> 6);
+  const int wave = FTW == 1 ? __builtin_amdgcn_readfirstlane(wave_v) : wave_v;
   const T* Wf = (const T*)a.filt.w;
   const T* h = (const T*)a.h;
   const T* vv = (const T*)a.v;
@@ -724,131 +730,209 @@ k_message_bwd(MsgBwdArgs a) {
   A* gh_out = (A*)a.gh;
   A* gv_out = (A*)a.gv_out;
   A* eg = (A*)a.eg;
-  for (int j = j0; j < j1; ++j) {
-    const int ea = tp(j), eb = tp(j + 1);
-    const size_t jb = (size_t)j * 3 * F;
-    A acc_h[FTW][3], acc_v[FTW][3];
+  // senders without incoming edges: g_h = 0, g_v = g_v'
+  for (int j = j0; j < j1; ++j)
+    if (tp(j) == tp(j + 1) && lane < 16) {
+      const size_t jb = (size_t)j * 3 * F;
 #pragma unroll
-    for (int q = 0; q < FTW; ++q)
+      for (int q = 0; q < FTW; ++q) {
+        const int ch = (FTW * wave + q) * 16 + lane;
 #pragma unroll
-      for (int k = 0; k < 3; ++k) acc_h[q][k] = acc_v[q][k] = 0;
-    for (int c0 = ea; c0 < eb; c0 += 16) {
-      const int cnt = min(16, eb - c0);
-      // A operand rows: position c0 + lane % 16 (past the chunk: the zero row E)
-      const int erA = (lane & 15) < cnt ? c0 + (lane & 15) : (int)a.E;
-      Fr Ga[KBM], Gd[KBM];
-      {
-        const T* gp = basis + (size_t)erA * kcols + (lane >> 4) * P::KPL;
-        const T* dp = dbasis + (size_t)erA * kcols + (lane >> 4) * P::KPL;
-#pragma unroll
-        for (int kb = 0; kb < KBM; ++kb) {
-          Ga[kb] = P::frag(gp + kb * P::KC);
-          Gd[kb] = P::frag(dp + kb * P::KC);
+        for (int k = 0; k < 3; ++k) {
+          gh_out[jb + k * F + ch] = A(0);
+          gv_out[jb + k * F + ch] = gv[jb + k * F + ch];
         }
       }
-      // this lane's 4 accumulator rows: edge id, receiver, rhat (rows past
-      // the chunk: receiver 0 and a zero filter, so they add nothing)
-      int er[4], ir[4];
-      A rh[4][3];
+    }
+  auto first_with_edges = [&](int j) {
+    while (j < j1 && tp(j) == tp(j + 1)) ++j;
+    return j;
+  };
+  // The block's senders are walked as one stream of chunks of up to 16
+  // edges of one sender; the next chunk's operand rows and edge info load
+  // while the current one is processed.  Per lane: the A rows (position
+  // c0 + lane % 16; past the chunk the zero row E) and, for its 4
+  // accumulator rows, edge id, receiver and rhat (past the chunk: receiver 0
+  // and a zero filter, so they add nothing).
+  Fr Gan[KBM], Gdn[KBM];
+  int ern[4], irn[4];
+  A rhn[4][3];
+  auto prefetch = [&](int c0, int cnt) {
+    const int erA = (lane & 15) < cnt ? c0 + (lane & 15) : (int)a.E;
+    const T* gp = basis + (size_t)erA * kcols + (lane >> 4) * P::KPL;
+    const T* dp = dbasis + (size_t)erA * kcols + (lane >> 4) * P::KPL;
+#pragma unroll
+    for (int kb = 0; kb < KBM; ++kb) {
+      Gan[kb] = P::frag(gp + kb * P::KC);
+      Gdn[kb] = P::frag(dp + kb * P::KC);
+    }
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const int row = P::row(lane, i);
+      const bool ok = row < cnt;
+      const A* ei = einfo + 4 * (size_t)(ok ? c0 + row : 0);
+      ern[i] = ok ? a.t_edge[c0 + row] : -1;
+      irn[i] = ok ? acc_index(ei[3]) : 0;
+      rhn[i][0] = ok ? ei[0] : A(0);
+      rhn[i][1] = ok ? ei[1] : A(0);
+      rhn[i][2] = ok ? ei[2] : A(0);
+    }
+  };
+  // Prefetching holds a second set of these registers: only where they fit
+  // without spilling and where it measured faster (FP32 with 2 feature tiles
+  // per wave at F = 256 and a filter input of at least 9 k-blocks); elsewhere
+  // each chunk loads its own at its start.
+  constexpr bool PF = sizeof(A) == 4 && FTW >= 2 && F == 256 && KBM >= 9;
+  int j = first_with_edges(j0);
+  if (j >= j1) return;
+  int c0 = tp(j);
+  if (PF) prefetch(c0, min(16, tp(j + 1) - c0));
+  A acc_h[FTW][3], acc_v[FTW][3];
+#pragma unroll
+  for (int q = 0; q < FTW; ++q)
+#pragma unroll
+    for (int k = 0; k < 3; ++k) acc_h[q][k] = acc_v[q][k] = 0;
+  while (true) {
+    const size_t jb = (size_t)j * 3 * F;
+    const int eb = tp(j + 1);
+    if (!PF) prefetch(c0, min(16, eb - c0));
+    Fr Ga[KBM], Gd[KBM];
+    int er[4], ir[4];
+    A rh[4][3];
+#pragma unroll
+    for (int kb = 0; kb < KBM; ++kb) {
+      Ga[kb] = Gan[kb];
+      Gd[kb] = Gdn[kb];
+    }
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      er[i] = ern[i];
+      ir[i] = irn[i];
+      rh[i][0] = rhn[i][0];
+      rh[i][1] = rhn[i][1];
+      rh[i][2] = rhn[i][2];
+    }
+    // the next chunk: this sender's next 16 edges, else the next sender
+    // (found here when it is prefetched, else after this chunk so that its
+    // indices are not live across the matrix work)
+    const bool last = c0 + 16 >= eb;
+    int jn = j, cn = 0;
+    bool more = true;
+    auto find_next = [&] {
+      jn = last ? first_with_edges(j + 1) : j;
+      more = jn < j1;
+      cn = last ? (more ? tp(jn) : 0) : c0 + 16;
+    };
+    if (PF) {
+      find_next();
+      if (more) prefetch(cn, min(16, tp(jn + 1) - cn));
+    }
+    // the receivers' g_s', g_v' at this lane's channels, all issued before
+    // the matrix cores start (they do not depend on the filter)
+    A gsr[FTW][4], gvr[FTW][4][3];
+#pragma unroll
+    for (int q = 0; q < FTW; ++q) {
+      const int ch = (FTW * wave + q) * 16 + (lane & 15);
 #pragma unroll
       for (int i = 0; i < 4; ++i) {
-        const int row = P::row(lane, i);
-        const bool ok = row < cnt;
-        const A* ei = einfo + 4 * (size_t)(ok ? c0 + row : 0);
-        er[i] = ok ? a.t_edge[c0 + row] : -1;
-        ir[i] = ok ? acc_index(ei[3]) : 0;
-        rh[i][0] = ok ? ei[0] : A(0);
-        rh[i][1] = ok ? ei[1] : A(0);
-        rh[i][2] = ok ? ei[2] : A(0);
+        const size_t ib = (size_t)ir[i] * 3 * F;
+        gsr[q][i] = gs[(size_t)ir[i] * F + ch];
+        gvr[q][i][0] = gv[ib + ch];
+        gvr[q][i][1] = gv[ib + F + ch];
+        gvr[q][i][2] = gv[ib + 2 * F + ch];
       }
-      // the receivers' g_s', g_v' at this lane's channels, all issued before
-      // the matrix cores start (they do not depend on the filter)
-      A gsr[FTW][4], gvr[FTW][4][3];
+    }
+    // The filter fragments stay in registers for the whole kernel when
+    // they are few (FP32, K + 1 <= 24); otherwise they stream from the
+    // caches chunk by chunk (an opaque copy of the pointer keeps the
+    // compiler from hoisting them out of the loops).
+    const T* Wc = Wf;
+    if constexpr (FTW * 3 * KBM * (int)sizeof(A) / 4 > 40) asm volatile("" : "+s"(Wc));
+    // per-edge partial sums: [dE/dd, dE/drhat x, y, z] x 4 rows
+    A vals[16];
 #pragma unroll
-      for (int q = 0; q < FTW; ++q) {
-        const int ch = (FTW * wave + q) * 16 + (lane & 15);
+    for (int k = 0; k < 16; ++k) vals[k] = 0;
 #pragma unroll
-        for (int i = 0; i < 4; ++i) {
-          const size_t ib = (size_t)ir[i] * 3 * F;
-          gsr[q][i] = gs[(size_t)ir[i] * F + ch];
-          gvr[q][i][0] = gv[ib + ch];
-          gvr[q][i][1] = gv[ib + F + ch];
-          gvr[q][i][2] = gv[ib + 2 * F + ch];
+    for (int q = 0; q < FTW; ++q) {
+      C w[3], wd[3];
+#pragma unroll
+      for (int part = 0; part < 3; ++part) {
+        for (int r = 0; r < 4; ++r) w[part][r] = wd[part][r] = 0;
+#pragma unroll
+        for (int kb = 0; kb < KBM; ++kb) {
+          const int ct = part * NFT + FTW * wave + q;
+          const Fr bw = P::frag(Wc + ((size_t)(ct * KBM + kb) * 64 + lane) * P::KPL);
+          w[part] = P::mfma(Ga[kb], bw, w[part]);
+          wd[part] = P::mfma(Gd[kb], bw, wd[part]);
         }
       }
-      // The filter fragments stay in registers for the whole kernel when
-      // they are few (FP32, K + 1 <= 24); otherwise they stream from the
-      // caches chunk by chunk (an opaque copy of the pointer keeps the
-      // compiler from hoisting them out of the loops).
-      const T* Wc = Wf;
-      if constexpr (FTW * 3 * KBM * (int)sizeof(A) / 4 > 40) asm volatile("" : "+s"(Wc));
-      // per-edge partial sums: [dE/dd, dE/drhat x, y, z] x 4 rows
-      A vals[16];
+      const int ch = (FTW * wave + q) * 16 + (lane & 15);
+      const A hs = P::ld(h[jb + ch]), hv = P::ld(h[jb + F + ch]), hr = P::ld(h[jb + 2 * F + ch]);
+      const A v0 = P::ld(vv[jb + ch]), v1 = P::ld(vv[jb + F + ch]), v2 = P::ld(vv[jb + 2 * F + ch]);
 #pragma unroll
-      for (int k = 0; k < 16; ++k) vals[k] = 0;
-#pragma unroll
-      for (int q = 0; q < FTW; ++q) {
-        C w[3], wd[3];
-#pragma unroll
-        for (int part = 0; part < 3; ++part) {
-          for (int r = 0; r < 4; ++r) w[part][r] = wd[part][r] = 0;
-#pragma unroll
-          for (int kb = 0; kb < KBM; ++kb) {
-            const int ct = part * NFT + FTW * wave + q;
-            const Fr bw = P::frag(Wc + ((size_t)(ct * KBM + kb) * 64 + lane) * P::KPL);
-            w[part] = P::mfma(Ga[kb], bw, w[part]);
-            wd[part] = P::mfma(Gd[kb], bw, wd[part]);
-          }
-        }
-        const int ch = (FTW * wave + q) * 16 + (lane & 15);
-        const A hs = P::ld(h[jb + ch]), hv = P::ld(h[jb + F + ch]), hr = P::ld(h[jb + 2 * F + ch]);
-        const A v0 = P::ld(vv[jb + ch]), v1 = P::ld(vv[jb + F + ch]), v2 = P::ld(vv[jb + 2 * F + ch]);
-#pragma unroll
-        for (int i = 0; i < 4; ++i) {
-          const A g_s = gsr[q][i], g0 = gvr[q][i][0], g1 = gvr[q][i][1], g2 = gvr[q][i][2];
-          const A Av = g0 * v0 + g1 * v1 + g2 * v2;
-          const A Ar = g0 * rh[i][0] + g1 * rh[i][1] + g2 * rh[i][2];
-          acc_h[q][0] += g_s * w[0][i];
-          acc_h[q][1] += Av * w[1][i];
-          acc_h[q][2] += Ar * w[2][i];
-          const A tv = hv * w[1][i], tr = hr * w[2][i];
-          acc_v[q][0] += g0 * tv;
-          acc_v[q][1] += g1 * tv;
-          acc_v[q][2] += g2 * tv;
-          vals[i] += g_s * hs * wd[0][i] + Av * hv * wd[1][i] + Ar * hr * wd[2][i];
-          vals[4 + i] += g0 * tr;
-          vals[8 + i] += g1 * tr;
-          vals[12 + i] += g2 * tr;
-        }
+      for (int i = 0; i < 4; ++i) {
+        const A g_s = gsr[q][i], g0 = gvr[q][i][0], g1 = gvr[q][i][1], g2 = gvr[q][i][2];
+        const A Av = g0 * v0 + g1 * v1 + g2 * v2;
+        const A Ar = g0 * rh[i][0] + g1 * rh[i][1] + g2 * rh[i][2];
+        acc_h[q][0] += g_s * w[0][i];
+        acc_h[q][1] += Av * w[1][i];
+        acc_h[q][2] += Ar * w[2][i];
+        const A tv = hv * w[1][i], tr = hr * w[2][i];
+        acc_v[q][0] += g0 * tv;
+        acc_v[q][1] += g1 * tv;
+        acc_v[q][2] += g2 * tv;
+        vals[i] += g_s * hs * wd[0][i] + Av * hv * wd[1][i] + Ar * hr * wd[2][i];
+        vals[4 + i] += g0 * tr;
+        vals[8 + i] += g1 * tr;
+        vals[12 + i] += g2 * tr;
       }
-      // lane: the wave's total of value (lane % 16) / 4 for its row lane % 4
-      reduce_scatter16<A, 16>(vals, lane);
+    }
+    // lane: the wave's total of value (lane % 16) / 4 for its row lane % 4
+    reduce_scatter16<A, 16>(vals, lane);
+    {
       const int k = lane & 15, i = k & 3;
       const int e = i == 0 ? er[0] : i == 1 ? er[1] : i == 2 ? er[2] : er[3];
       // one add per slot per launch, and launches run in layer order: the
       // sums are deterministic; the add does not return, so no wave waits
       if (e >= 0) unsafeAtomicAdd(eg + ((size_t)e * NW + wave) * 4 + (k >> 2), vals[0]);
     }
-    // sums over the wave's 4 row groups; lanes < 16 write
+    if (!PF) find_next();
+    if (last) {
+      // the sender's sums over the wave's 4 row groups; lanes < 16 write
 #pragma unroll
-    for (int q = 0; q < FTW; ++q)
+      for (int q = 0; q < FTW; ++q)
 #pragma unroll
-      for (int k = 0; k < 3; ++k)
-        for (int o = 16; o < 64; o *= 2) {
-          acc_h[q][k] += __shfl_xor(acc_h[q][k], o);
-          acc_v[q][k] += __shfl_xor(acc_v[q][k], o);
-        }
-    if (lane < 16) {
+        for (int k = 0; k < 3; ++k)
+          for (int o = 16; o < 64; o *= 2) {
+            acc_h[q][k] += __shfl_xor(acc_h[q][k], o);
+            acc_v[q][k] += __shfl_xor(acc_v[q][k], o);
+          }
+      if (lane < 16) {
+        // all loads of g_v' first: the stores may alias them for all the
+        // compiler knows, and would otherwise wait for each load in turn
+        A gvj[FTW][3];
 #pragma unroll
-      for (int q = 0; q < FTW; ++q) {
-        const int ch = (FTW * wave + q) * 16 + lane;
+        for (int q = 0; q < FTW; ++q)
 #pragma unroll
-        for (int k = 0; k < 3; ++k) {
-          gh_out[jb + k * F + ch] = acc_h[q][k];
-          gv_out[jb + k * F + ch] = gv[jb + k * F + ch] + acc_v[q][k];
+          for (int k = 0; k < 3; ++k) gvj[q][k] = gv[jb + k * F + (FTW * wave + q) * 16 + lane];
+#pragma unroll
+        for (int q = 0; q < FTW; ++q) {
+          const int ch = (FTW * wave + q) * 16 + lane;
+#pragma unroll
+          for (int k = 0; k < 3; ++k) {
+            gh_out[jb + k * F + ch] = acc_h[q][k];
+            gv_out[jb + k * F + ch] = gvj[q][k] + acc_v[q][k];
+          }
         }
       }
+#pragma unroll
+      for (int q = 0; q < FTW; ++q)
+#pragma unroll
+        for (int k = 0; k < 3; ++k) acc_h[q][k] = acc_v[q][k] = 0;
     }
+    if (!more) break;
+    j = jn;
+    c0 = cn;
   }
 }
 
