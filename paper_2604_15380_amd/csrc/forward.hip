@@ -842,13 +842,15 @@ inline int grid_for(size_t n, int per) {
 // Channel-per-lane form (FP32 / BF16 storage).  A workgroup of F/64 waves
 // owns MSG_RB2 consecutive receivers; wave w owns channels [64 w, 64 w + 64)
 // = feature tiles 4w..4w+3 and keeps their filter B fragments in registers.
-// Per 16-edge chunk the wave forms Wt for its channels on the matrix cores
-// and parks it in its own LDS tile (edge-major); then every lane, one
-// channel, walks the chunk's edges: the sender index is wave-uniform, so each
-// gather reads 256 contiguous bytes of a sender row, and the filter values
-// come back from LDS.  Sums stay in the lane (no cross-lane reduction) and no
-// wave waits for another.
-constexpr int MSG_RB2 = 4;
+// Per 16-edge chunk (the block's edges back to back, so a chunk may hold
+// the end of one receiver's row and the start of the next) the wave forms Wt
+// for its channels on the matrix cores and parks it in its own LDS tile
+// (edge-major); then every lane, one channel, walks the chunk's edges: the
+// sender index is wave-uniform, so each gather reads 256 contiguous bytes of
+// a sender row, and the filter values come back from LDS.  Sums stay in the
+// lane (no cross-lane reduction) until the receiver's last edge, and no wave
+// waits for another.
+constexpr int MSG_RB2 = 8;
 
 template <class A>
 __device__ __forceinline__ A bcast(A x, int lane) {
@@ -931,9 +933,13 @@ k_message_lane(MsgArgs a) {
     while (i < i1 && rp(i) == rp(i + 1)) ++i;
     return i;
   };
-  // The block's receivers are walked as one stream of chunks of up to 16
-  // edges of one receiver.  The next chunk's basis rows and edge info are
-  // loaded while the current one is processed (the basis streams from HBM).
+  // The block's edges [E0, E1) (its receivers' CSR rows back to back) are
+  // walked as one stream of 16-edge chunks that may span receivers, so only
+  // the block's last chunk is partial.  The next chunk's basis rows and edge
+  // info are loaded while the current one is processed (the basis streams
+  // from HBM).
+  const int E0 = rp(i0), E1 = rp(i1);
+  if (E0 == E1) return;
   Fr Gn[KBM];
   A exn = 0, eyn = 0, ezn = 0, ejn = 0;
   auto prefetch = [&](int cc0, int ccnt) {
@@ -949,32 +955,48 @@ k_message_lane(MsgArgs a) {
       ejn = ei[3];
     }
   };
+  int c0 = E0;
+  prefetch(c0, min(16, E1 - c0));
+  // the receiver being summed: i, whose edges end at eb
   int i = first_with_edges(i0);
-  if (i >= i1) return;
-  int c0 = rp(i);
-  prefetch(c0, min(16, rp(i + 1) - c0));
+  int eb = rp(i + 1);
   size_t ib = (size_t)i * 3 * F;
   T s_old = sin[(size_t)i * F + c];
   T v_old0 = vin[ib + c], v_old1 = vin[ib + F + c], v_old2 = vin[ib + 2 * F + c];
   A acc_s = 0, acc_v0 = 0, acc_v1 = 0, acc_v2 = 0;
+  auto write_out = [&] {
+    s[(size_t)i * F + c] = P::st(P::ld(s_old) + acc_s);
+    vout[ib + c] = P::st(P::ld(v_old0) + acc_v0);
+    vout[ib + F + c] = P::st(P::ld(v_old1) + acc_v1);
+    vout[ib + 2 * F + c] = P::st(P::ld(v_old2) + acc_v2);
+  };
+  // Edge c0 + e starts the next receiver: write receiver i out and move on
+  // (a wave-uniform branch; the last receiver is written after the stream).
+  auto next_receiver = [&] {
+    write_out();
+    acc_s = acc_v0 = acc_v1 = acc_v2 = 0;
+    i = first_with_edges(i + 1);
+    eb = rp(i + 1);
+    ib = (size_t)i * 3 * F;
+    s_old = sin[(size_t)i * F + c];
+    v_old0 = vin[ib + c];
+    v_old1 = vin[ib + F + c];
+    v_old2 = vin[ib + 2 * F + c];
+  };
   while (true) {
-    const int eb = rp(i + 1);
-    const int cnt = min(16, eb - c0);
-    // A rows past the chunk's end are zeroed, so are their filter rows
+    const int cnt = min(16, E1 - c0);
+    // A rows past the stream's end are zeroed, so are their filter rows
     const bool row_ok = (lane & 15) < cnt;
     Fr Ga[KBM];
 #pragma unroll
     for (int kb = 0; kb < KBM; ++kb) Ga[kb] = row_ok ? Gn[kb] : Fr{};
     // lanes e < cnt hold edge c0 + e: rhat and the sender index
     const A ex = exn, ey = eyn, ez = ezn, ej = ejn;
-    // the next chunk: this receiver's next 16 edges, else the next receiver
-    const bool last = c0 + 16 >= eb;
-    const int in = last ? first_with_edges(i + 1) : i;
-    const bool more = in < i1;
-    const int cn = last ? (more ? rp(in) : 0) : c0 + 16;
-    if (more) prefetch(cn, min(16, rp(in + 1) - cn));
+    const int cn = c0 + 16;
+    const bool more = cn < E1;
+    if (more) prefetch(cn, min(16, E1 - cn));
     // Gathers of EG edges: sender rows h_j (3 parts) and v_j (3 components)
-    // at this lane's channel.  Past the chunk's end the sender is row 0
+    // at this lane's channel.  Past the stream's end the sender is row 0
     // (lanes >= cnt hold index 0) and the filter rows are zero, so a group
     // needs no early exit and all its 6 EG loads can be in flight together.
     T gb[6][EG];
@@ -996,6 +1018,9 @@ k_message_lane(MsgArgs a) {
 #pragma unroll
       for (int u = 0; u < EG; ++u) {
         const int e = ebase + u;
+        // eb < E1: receiver i is not the block's last one (past the
+        // stream's end, c0 + e >= E1 >= eb)
+        if (c0 + e == eb && eb < E1) next_receiver();
         const A rx = bcast(ex, e), ry = bcast(ey, e), rz = bcast(ez, e);
         const A ws = wt0[e * WLD + lane], wv = wt1[e * WLD + lane], wr = wt2[e * WLD + lane];
         acc_s += P::ld(gb[0][u]) * ws;
@@ -1054,22 +1079,10 @@ k_message_lane(MsgArgs a) {
     __builtin_amdgcn_wave_barrier();
     __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
     __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
-    if (last) {
-      s[(size_t)i * F + c] = P::st(P::ld(s_old) + acc_s);
-      vout[ib + c] = P::st(P::ld(v_old0) + acc_v0);
-      vout[ib + F + c] = P::st(P::ld(v_old1) + acc_v1);
-      vout[ib + 2 * F + c] = P::st(P::ld(v_old2) + acc_v2);
-      if (!more) break;
-      acc_s = acc_v0 = acc_v1 = acc_v2 = 0;
-      ib = (size_t)in * 3 * F;
-      s_old = sin[(size_t)in * F + c];
-      v_old0 = vin[ib + c];
-      v_old1 = vin[ib + F + c];
-      v_old2 = vin[ib + 2 * F + c];
-    }
-    i = in;
+    if (!more) break;
     c0 = cn;
   }
+  write_out();
 }
 
 template <class P, int F, int KBM>
