@@ -261,8 +261,9 @@ struct HeadBwdArgs {
   int H;
 };
 
-template <class P>
-__device__ __forceinline__ typename P::A packed_w0(const DenseDev& L, int k) {
+template <class Q>
+__device__ __forceinline__ typename Q::A packed_w0(const DenseDev& L, int k) {
+  using P = dense_t<Q>;
   const int kb = k / P::KC, r = k % P::KC;
   return P::ld(((const typename P::T*)L.w)[((size_t)kb * 64 + 16 * (r / P::KPL)) * P::KPL + r % P::KPL]);
 }
@@ -494,7 +495,7 @@ __global__ void __launch_bounds__((64 * ub_nw<P, F>())) k_update_bwd(UpdBwdArgs 
   }
   __syncthreads();
   // g_z = (W2a^T g_a) * silu'(z) into R2
-  dense_tiles<P, 1, ub_nw<P, F>(), 3 * F / P::KC>(R1, LD1, a.upd2T, [&](int ct, C* acc) {
+  dense_tiles<P, 1, ub_nw<P, F>(), 3 * F>(R1, LD1, a.upd2T, [&](int ct, C* acc) {
     const int col = ct * 16 + (lane & 15);
     for (int i = 0; i < 4; ++i) {
       const int r = P::row(lane, i);
@@ -506,7 +507,7 @@ __global__ void __launch_bounds__((64 * ub_nw<P, F>())) k_update_bwd(UpdBwdArgs 
   __syncthreads();
   // [g_s' ; g_n] = W1a^T g_z
   A* gs_out = (A*)a.gs_out;
-  dense_tiles<P, 1, ub_nw<P, F>(), F / P::KC>(R2, LD2, a.upd1T, [&](int ct, C* acc) {
+  dense_tiles<P, 1, ub_nw<P, F>(), F>(R2, LD2, a.upd1T, [&](int ct, C* acc) {
     const int col = ct * 16 + (lane & 15);
     for (int i = 0; i < 4; ++i) {
       const int r = P::row(lane, i);
@@ -537,7 +538,7 @@ __global__ void __launch_bounds__((64 * ub_nw<P, F>())) k_update_bwd(UpdBwdArgs 
       R1[r * LD1 + F + f] = P::st(gV);
     }
     __syncthreads();
-    dense_tiles<P, 1, ub_nw<P, F>(), 2 * F / P::KC>(R1, LD1, a.uvT, [&](int ct, C* acc) {
+    dense_tiles<P, 1, ub_nw<P, F>(), 2 * F>(R1, LD1, a.uvT, [&](int ct, C* acc) {
       const int col = ct * 16 + (lane & 15);
       for (int i = 0; i < 4; ++i) {
         const int r = P::row(lane, i);
@@ -590,7 +591,7 @@ __global__ void __launch_bounds__((64 * ub_nw<P, F>())) k_phi_bwd(PhiBwdArgs a) 
     R1[r * LD1 + f] = P::st(row0 + r < (size_t)N ? gh[(row0 + r) * 3 * F + f] : A(0));
   }
   __syncthreads();
-  dense_tiles<P, 1, ub_nw<P, F>(), F / P::KC>(R2, LD2, a.phi1, [&](int ct, C* acc) {
+  dense_tiles<P, 1, ub_nw<P, F>(), F>(R2, LD2, a.phi1, [&](int ct, C* acc) {
     const int col = ct * 16 + (lane & 15);
     const A bias = ((const A*)a.phi1.b)[col];
     for (int i = 0; i < 4; ++i) {
@@ -599,7 +600,7 @@ __global__ void __launch_bounds__((64 * ub_nw<P, F>())) k_phi_bwd(PhiBwdArgs a) 
     }
   });
   __syncthreads();
-  dense_tiles<P, 1, ub_nw<P, F>(), 3 * F / P::KC>(R1, LD1, a.phi2T, [&](int ct, C* acc) {
+  dense_tiles<P, 1, ub_nw<P, F>(), 3 * F>(R1, LD1, a.phi2T, [&](int ct, C* acc) {
     const int col = ct * 16 + (lane & 15);
     for (int i = 0; i < 4; ++i) {
       const int r = P::row(lane, i);
@@ -611,7 +612,7 @@ __global__ void __launch_bounds__((64 * ub_nw<P, F>())) k_phi_bwd(PhiBwdArgs a) 
   __syncthreads();
   const A* gm = (const A*)a.gs_mid;
   A* go = (A*)a.gs_out;
-  dense_tiles<P, 1, ub_nw<P, F>(), F / P::KC>(R2, LD2, a.phi1T, [&](int ct, C* acc) {
+  dense_tiles<P, 1, ub_nw<P, F>(), F>(R2, LD2, a.phi1T, [&](int ct, C* acc) {
     const int col = ct * 16 + (lane & 15);
     for (int i = 0; i < 4; ++i) {
       const size_t g = row0 + P::row(lane, i);

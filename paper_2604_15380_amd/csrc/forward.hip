@@ -49,14 +49,14 @@ __device__ __forceinline__ void phi_tile(const typename P::T* X, int ldx, typena
   using A = typename P::A;
   constexpr int LD = F + P::PAD;
   const int lane = threadIdx.x & 63;
-  dense_tiles<P, RT, NW, F / P::KC>(X, ldx, d1, [&](int ct, typename P::C* acc) {
+  dense_tiles<P, RT, NW, F>(X, ldx, d1, [&](int ct, typename P::C* acc) {
     const int col = ct * 16 + (lane & 15);
     const A bias = ((const A*)d1.b)[col];
     for (int r = 0; r < RT; ++r)
       for (int i = 0; i < 4; ++i) H[(r * 16 + P::row(lane, i)) * LD + col] = P::st(silu<A>(acc[r][i] + bias));
   });
   __syncthreads();
-  dense_tiles<P, RT, NW, F / P::KC>(H, LD, d2, [&](int ct, typename P::C* acc) {
+  dense_tiles<P, RT, NW, F>(H, LD, d2, [&](int ct, typename P::C* acc) {
     const int col = ct * 16 + (lane & 15);
     const A bias = ((const A*)d2.b)[col];
     for (int r = 0; r < RT; ++r)
@@ -374,7 +374,6 @@ k_update(UpdArgs a) {
   using T = typename P::T;
   using A = typename P::A;
   using C = typename P::C;
-  using Fr = typename P::Fr;
   constexpr int NFT = F / 16;        // feature tiles
   constexpr int NW = update_nw<P, F>();
   constexpr int FTW = NFT / NW;      // per wave
@@ -400,7 +399,9 @@ k_update(UpdArgs a) {
   for (int q = 0; q < FTW; ++q)
     for (int r = 0; r < RT; ++r)
       for (int i = 0; i < 4; ++i) nsq[q][r][i] = pd[q][r][i] = 0;
-  constexpr int nkb = F / P::KC;
+  using D = dense_t<P>;   // operand form of the dense layers
+  using Fd = typename D::Fr;
+  constexpr int nkb = F / D::KC;
   const T* Wuv = (const T*)a.uv.w;
   for (int c = 0; c < 3; ++c) {
     __syncthreads();
@@ -409,26 +410,26 @@ k_update(UpdArgs a) {
       VS[r * LD1 + col] = row0 + r < (size_t)N ? v[(row0 + r) * 3 * F + c * F + col] : P::st(0);
     }
     __syncthreads();
-    const T* xp = VS + (lane & 15) * LD1 + (lane >> 4) * P::KPL;
+    const T* xp = VS + (lane & 15) * LD1 + (lane >> 4) * D::KPL;
 #pragma unroll
     for (int q = 0; q < FTW; ++q) {
       const int ft = wave + NW * q;
       C au[RT], av[RT];
       for (int r = 0; r < RT; ++r)
         for (int i = 0; i < 4; ++i) au[r][i] = av[r][i] = 0;
-      const T* wu = Wuv + (size_t)ft * nkb * 64 * P::KPL + (size_t)lane * P::KPL;
-      const T* wv = Wuv + (size_t)(NFT + ft) * nkb * 64 * P::KPL + (size_t)lane * P::KPL;
-      kloop<P, nkb, ring_depth<P, 2>(), 2, RT>(
+      const T* wu = Wuv + (size_t)ft * nkb * 64 * D::KPL + (size_t)lane * D::KPL;
+      const T* wv = Wuv + (size_t)(NFT + ft) * nkb * 64 * D::KPL + (size_t)lane * D::KPL;
+      kloop<D, nkb, ring_depth<D, 2>(), 2, RT>(
           xp, LD1,
-          [&](int kb, Fr* f) {
-            f[0] = P::frag(wu + (size_t)kb * 64 * P::KPL);
-            f[1] = P::frag(wv + (size_t)kb * 64 * P::KPL);
+          [&](int kb, Fd* f) {
+            f[0] = D::frag(wu + (size_t)kb * 64 * D::KPL);
+            f[1] = D::frag(wv + (size_t)kb * 64 * D::KPL);
           },
-          [&](int kb, const Fr* x, const Fr* f) {
+          [&](int kb, const Fd* x, const Fd* f) {
 #pragma unroll
             for (int r = 0; r < RT; ++r) {
-              au[r] = P::mfma(x[r], f[0], au[r]);
-              av[r] = P::mfma(x[r], f[1], av[r]);
+              au[r] = D::mfma(x[r], f[0], au[r]);
+              av[r] = D::mfma(x[r], f[1], av[r]);
             }
           });
 #pragma unroll
@@ -461,7 +462,7 @@ k_update(UpdArgs a) {
   }
   __syncthreads();
   T* H = VS;
-  dense_tiles<P, RT, NW, 2 * F / P::KC>(SN, LD2, a.upd1, [&](int ct, C* acc) {
+  dense_tiles<P, RT, NW, 2 * F>(SN, LD2, a.upd1, [&](int ct, C* acc) {
     const int col = ct * 16 + (lane & 15);
     const A bias = ((const A*)a.upd1.b)[col];
     for (int r = 0; r < RT; ++r)
@@ -475,32 +476,32 @@ k_update(UpdArgs a) {
   });
   __syncthreads();
   {
-    constexpr int nkb2 = F / P::KC;
+    constexpr int nkb2 = F / D::KC;
     const T* W2 = (const T*)a.upd2.w;
     const A* b2 = (const A*)a.upd2.b;
-    const T* xp = H + (lane & 15) * LD1 + (lane >> 4) * P::KPL;
+    const T* xp = H + (lane & 15) * LD1 + (lane >> 4) * D::KPL;
 #pragma unroll
     for (int q = 0; q < FTW; ++q) {
       const int ft = wave + NW * q;
       C avv[RT], asv[RT], ass[RT];
       for (int r = 0; r < RT; ++r)
         for (int i = 0; i < 4; ++i) avv[r][i] = asv[r][i] = ass[r][i] = 0;
-      const T* w0 = W2 + (size_t)ft * nkb2 * 64 * P::KPL + (size_t)lane * P::KPL;
-      const T* w1 = W2 + (size_t)(NFT + ft) * nkb2 * 64 * P::KPL + (size_t)lane * P::KPL;
-      const T* w2 = W2 + (size_t)(2 * NFT + ft) * nkb2 * 64 * P::KPL + (size_t)lane * P::KPL;
-      kloop<P, nkb2, ring_depth<P, 3>(), 3, RT>(
+      const T* w0 = W2 + (size_t)ft * nkb2 * 64 * D::KPL + (size_t)lane * D::KPL;
+      const T* w1 = W2 + (size_t)(NFT + ft) * nkb2 * 64 * D::KPL + (size_t)lane * D::KPL;
+      const T* w2 = W2 + (size_t)(2 * NFT + ft) * nkb2 * 64 * D::KPL + (size_t)lane * D::KPL;
+      kloop<D, nkb2, ring_depth<D, 3>(), 3, RT>(
           xp, LD1,
-          [&](int kb, Fr* f) {
-            f[0] = P::frag(w0 + (size_t)kb * 64 * P::KPL);
-            f[1] = P::frag(w1 + (size_t)kb * 64 * P::KPL);
-            f[2] = P::frag(w2 + (size_t)kb * 64 * P::KPL);
+          [&](int kb, Fd* f) {
+            f[0] = D::frag(w0 + (size_t)kb * 64 * D::KPL);
+            f[1] = D::frag(w1 + (size_t)kb * 64 * D::KPL);
+            f[2] = D::frag(w2 + (size_t)kb * 64 * D::KPL);
           },
-          [&](int kb, const Fr* x, const Fr* f) {
+          [&](int kb, const Fd* x, const Fd* f) {
 #pragma unroll
             for (int r = 0; r < RT; ++r) {
-              avv[r] = P::mfma(x[r], f[0], avv[r]);
-              asv[r] = P::mfma(x[r], f[1], asv[r]);
-              ass[r] = P::mfma(x[r], f[2], ass[r]);
+              avv[r] = D::mfma(x[r], f[0], avv[r]);
+              asv[r] = D::mfma(x[r], f[1], asv[r]);
+              ass[r] = D::mfma(x[r], f[2], ass[r]);
             }
           });
       const int col = ft * 16 + (lane & 15);
@@ -677,8 +678,9 @@ struct HeadArgs {
 };
 
 // Element k of output row 0 of a packed dense layer (the B fragment order).
-template <class P>
-__device__ __forceinline__ typename P::A packed_row0(const DenseDev& L, int k) {
+template <class Q>
+__device__ __forceinline__ typename Q::A packed_row0(const DenseDev& L, int k) {
+  using P = dense_t<Q>;
   const int kb = k / P::KC, r = k % P::KC;
   return P::ld(((const typename P::T*)L.w)[((size_t)kb * 64 + 16 * (r / P::KPL)) * P::KPL + r % P::KPL]);
 }

@@ -13,10 +13,13 @@
 // Weights are packed on the host in exactly the B order, so a B fragment is
 // one coalesced load per lane that the whole chip re-reads from L2.
 //
+// (FP32 dense layers group four such 4-k instructions behind one 16-byte
+// fragment per lane, KC = 16: the P32B form below.)
+//
 // PAD is the LDS row padding (elements) of activation tiles, chosen so that
 // the 16 rows of one A-fragment read fall in distinct banks of the 32-bank
-// LDS: a row stride of 2 words (mod 32) for FP32, 1 double (mod 16) for
-// FP64 and 4 words for the 16-byte BF16 reads.
+// LDS: 1 double (mod 16) for FP64 and 4 words for the 16-byte FP32 and BF16
+// reads.
 #pragma once
 
 #include "internal.h"
@@ -55,10 +58,37 @@ struct P32 {
   using A = float;
   using C = f4_t;
   using Fr = float;
-  static constexpr int KC = 4, KPL = 1, PAD = 2, PREC = PAINN_FP32, UNROLL = 8, RING = 24;
+  static constexpr int KC = 4, KPL = 1, PAD = 4, PREC = PAINN_FP32, UNROLL = 8, RING = 24;
   __device__ static __forceinline__ Fr frag(const T* p) { return *p; }
   __device__ static __forceinline__ C mfma(Fr a, Fr b, C c) {
     return __builtin_amdgcn_mfma_f32_16x16x4f32(a, b, c, 0, 0, 0);
+  }
+  __device__ static __forceinline__ A ld(T x) { return x; }
+  __device__ static __forceinline__ T st(A x) { return x; }
+  __device__ static __forceinline__ A ex(A x) { return expf(x); }
+  __device__ static __forceinline__ int row(int lane, int i) { return 4 * (lane >> 4) + i; }
+};
+
+// FP32 dense layers: each lane reads 4 consecutive k (one 16-byte load of
+// the activation tile and one of the packed weights) and feeds them to 4
+// chained 16x16x4 instructions; instruction j takes k = 16 kb + 4 (l / 16) + j
+// from lane l.  A contraction may assign its k values to instructions in any
+// order as long as both operands agree, and the weights are packed in this
+// order (KC = 16, KPL = 4).  A quarter of the load instructions of the plain
+// 4-k form, for the same MFMA work.  The radial filter keeps the plain form
+// (its K + 1 inputs would pad to a multiple of 16).
+struct P32B {
+  using T = float;
+  using A = float;
+  using C = f4_t;
+  using Fr = f4_t;
+  static constexpr int KC = 16, KPL = 4, PAD = 4, PREC = PAINN_FP32, UNROLL = 2, RING = 24;
+  __device__ static __forceinline__ Fr frag(const T* p) { return *(const f4_t*)p; }
+  __device__ static __forceinline__ C mfma(Fr a, Fr b, C c) {
+    c = __builtin_amdgcn_mfma_f32_16x16x4f32(a[0], b[0], c, 0, 0, 0);
+    c = __builtin_amdgcn_mfma_f32_16x16x4f32(a[1], b[1], c, 0, 0, 0);
+    c = __builtin_amdgcn_mfma_f32_16x16x4f32(a[2], b[2], c, 0, 0, 0);
+    return __builtin_amdgcn_mfma_f32_16x16x4f32(a[3], b[3], c, 0, 0, 0);
   }
   __device__ static __forceinline__ A ld(T x) { return x; }
   __device__ static __forceinline__ T st(A x) { return x; }
@@ -81,6 +111,12 @@ struct PB16 {
   __device__ static __forceinline__ A ex(A x) { return expf(x); }
   __device__ static __forceinline__ int row(int lane, int i) { return 4 * (lane >> 4) + i; }
 };
+
+// The operand form of the dense layers (packed weights and activation tiles)
+// for a precision: FP32 uses the 16-byte form above, the others their own.
+template <class P> struct dense_of { using type = P; };
+template <> struct dense_of<P32> { using type = P32B; };
+template <class P> using dense_t = typename dense_of<P>::type;
 
 template <class A>
 __device__ __forceinline__ A silu(A x) {
@@ -230,10 +266,15 @@ constexpr int ring_depth() {
 // ldx elements).  Column tiles are dealt round-robin to the NW waves of the
 // workgroup; for each finished column tile `epi(ct, acc)` receives the RT
 // accumulator fragments.  Every wave of the workgroup must call this.
-// NKB > 0 fixes the number of K blocks (din_p / KC) at compile time.
-template <class P, int RT, int NW, int NKB = 0, class Epi>
-__device__ __forceinline__ void dense_tiles(const typename P::T* X, int ldx, const DenseDev& L,
+// KDIM > 0 fixes the padded input width din_p at compile time.  Q is the
+// precision; the operands take its dense form (the layer's weights are
+// packed in it).
+template <class Q, int RT, int NW, int KDIM = 0, class Epi>
+__device__ __forceinline__ void dense_tiles(const typename Q::T* X, int ldx, const DenseDev& L,
                                             Epi&& epi) {
+  using P = dense_t<Q>;
+  constexpr int NKB = KDIM / P::KC;
+  static_assert(KDIM % P::KC == 0, "compile-time K must be whole K blocks");
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int nct = L.dout_p / 16, nkb = NKB > 0 ? NKB : L.din_p / P::KC;
   const typename P::T* W = (const typename P::T*)L.w;

@@ -110,7 +110,9 @@ hipError_t upload(PrecModel* pm, const std::vector<unsigned char>& host, void** 
 // din_p: pad32(din), or filter_kblocks(din, prec) MFMA k-blocks for the radial filter.
 hipError_t pack_dense(PrecModel* pm, int prec, const double* W, const double* b, int dout,
                       int din, DenseDev* out, bool filter = false) {
-  const int KC = prec == PAINN_BF16 ? 32 : 4;
+  // k per MFMA step: BF16 32; FP32 dense layers 16 (4 chained 4-k
+  // instructions fed by one 16-byte load per lane), the FP32 filter and FP64 4
+  const int KC = prec == PAINN_BF16 ? 32 : prec == PAINN_FP32 && !filter ? 16 : 4;
   const int KPL = KC / 4;
   const int dout_p = pad32(dout), din_p = filter ? filter_kblocks(din, prec) * KC : pad32(din);
   const int nkb = din_p / KC, nct = dout_p / 16;
@@ -937,13 +939,15 @@ static int forces_scratch_width(const Hyper& hp) {
 static size_t forces_xbuf_bytes(int prec, const Hyper& hp, int N, bool blend) {
   const size_t eb = elem_bytes(prec), F = hp.F, tiles = ((size_t)N + 15) / 16;
   const size_t head_tiles = ((size_t)N * (blend ? hp.n_heads : 1) + 15) / 16;
+  // LDS row padding of the dense kernels' activation tiles (elements)
+  const size_t pad = prec == PAINN_FP64 ? 1 : prec == PAINN_FP32 ? 4 : 8;
   size_t x = 0;
-  if (16 * (4 * F + 2) * eb > 160 * 1024) x = tiles * 16 * (3 * F + 1) * eb;
+  if (16 * (4 * F + 2 * pad) * eb > 160 * 1024) x = tiles * 16 * (3 * F + pad) * eb;
   int wmax = hp.F;
   for (int d : hp.shared_dims) wmax = wmax > pad32(d) ? wmax : pad32(d);
   for (size_t mm = 0; mm + 1 < hp.branch_dims.size(); ++mm)
     wmax = wmax > pad32(hp.branch_dims[mm]) ? wmax : pad32(hp.branch_dims[mm]);
-  const size_t hb = (size_t)2 * 16 * (wmax + 2) * eb;
+  const size_t hb = (size_t)2 * 16 * (wmax + pad) * eb;
   if (hb > 150 * 1024) {
     const size_t grid = head_tiles + hp.n_heads < (size_t)HB_GRID ? head_tiles + hp.n_heads : (size_t)HB_GRID;
     const size_t h = grid * hb;
