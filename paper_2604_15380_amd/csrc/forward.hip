@@ -880,17 +880,23 @@ k_message_lane(MsgArgs a) {
   using C = typename P::C;
   using Fr = typename P::Fr;
   constexpr int NW = F / 64, NFT = F / 16;
-  constexpr int WLD = 64 + 4;                   // LDS row of one part, one edge
+  // LDS filter tile of one part: channel-major, a row of the chunk's 16
+  // edges per channel, as 4 groups of 4 edges stored in the order
+  // g ^ ((channel >> 1) & 3): the 16-byte accesses of 8 consecutive lanes
+  // (channels) then fall in distinct bank groups without padding
+  constexpr int WLD = 16;
+  static_assert(sizeof(A) == 4, "FP32 accumulation");
+  auto wslot = [](int ch, int g) { return ch * WLD + 4 * (g ^ ((ch >> 1) & 3)); };
   constexpr int kcols = KBM * P::KC;
   // VGPRs held by the filter's B fragments decide how much else is in flight
   constexpr int BF_REGS = 12 * KBM * (int)sizeof(Fr) / 4;
   constexpr int QI = BF_REGS > 100 ? 1 : 4;     // MFMA chains issued together (feature tiles)
-  constexpr int EG = BF_REGS > 100 ? 4 : 8;     // edges gathered per group
+  constexpr int EG = BF_REGS > 100 ? 4 : sizeof(T) == 4 ? 16 : 8;   // edges gathered per group
   // Issue the first group's gathers ahead of the filter MFMAs.  Measured: a
   // gain for BF16 with a short filter (few K blocks), a loss for FP32, whose
   // gathers move twice the bytes behind a long MFMA phase.
   constexpr bool EARLY = sizeof(T) == 2 && BF_REGS <= 100;
-  __shared__ A Wt[NW][3][16 * WLD];
+  __shared__ __attribute__((aligned(16))) A Wt[NW][3][64 * WLD];
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int c = 64 * wave + lane;               // this lane's channel
   const T* Wf = (const T*)a.filt_mma.w;
@@ -1017,14 +1023,22 @@ k_message_lane(MsgArgs a) {
       }
     };
     auto consume = [&](int ebase) {
+      f4_t ws4, wv4, wr4;
 #pragma unroll
       for (int u = 0; u < EG; ++u) {
         const int e = ebase + u;
+        // the filter of 4 edges at this lane's channel, one 16-byte read per part
+        if (u % 4 == 0) {
+          const int o = wslot(lane, e / 4);
+          ws4 = *(const f4_t*)(wt0 + o);
+          wv4 = *(const f4_t*)(wt1 + o);
+          wr4 = *(const f4_t*)(wt2 + o);
+        }
         // eb < E1: receiver i is not the block's last one (past the
         // stream's end, c0 + e >= E1 >= eb)
         if (c0 + e == eb && eb < E1) next_receiver();
         const A rx = bcast(ex, e), ry = bcast(ey, e), rz = bcast(ez, e);
-        const A ws = wt0[e * WLD + lane], wv = wt1[e * WLD + lane], wr = wt2[e * WLD + lane];
+        const A ws = ws4[u % 4], wv = wv4[u % 4], wr = wr4[u % 4];
         acc_s += P::ld(gb[0][u]) * ws;
         const A pv = P::ld(gb[1][u]) * wv, pr = P::ld(gb[2][u]) * wr;
         acc_v0 += P::ld(gb[3][u]) * pv + rx * pr;
@@ -1056,16 +1070,14 @@ k_message_lane(MsgArgs a) {
 #pragma unroll
           for (int part = 0; part < 3; ++part)
             w[q][part] = P::mfma(Ga[kb], Bf[q0 + q][part][kb], w[q][part]);
+      // this lane's 4 accumulator rows are the 4 consecutive edges of group
+      // lane / 16 at one channel: one 16-byte write per part
 #pragma unroll
       for (int q = 0; q < QI; ++q) {
-        const int col = 16 * (q0 + q) + (lane & 15);
-#pragma unroll
-        for (int r = 0; r < 4; ++r) {
-          const int row = P::row(lane, r);
-          wt0[row * WLD + col] = w[q][0][r];
-          wt1[row * WLD + col] = w[q][1][r];
-          wt2[row * WLD + col] = w[q][2][r];
-        }
+        const int o = wslot(16 * (q0 + q) + (lane & 15), lane >> 4);
+        *(f4_t*)(wt0 + o) = f4_t{w[q][0][0], w[q][0][1], w[q][0][2], w[q][0][3]};
+        *(f4_t*)(wt1 + o) = f4_t{w[q][1][0], w[q][1][1], w[q][1][2], w[q][1][3]};
+        *(f4_t*)(wt2 + o) = f4_t{w[q][2][0], w[q][2][1], w[q][2][2], w[q][2][3]};
       }
     }
     __builtin_amdgcn_wave_barrier();
