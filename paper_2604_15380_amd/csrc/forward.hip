@@ -882,11 +882,12 @@ k_message_lane(MsgArgs a) {
   constexpr int NW = F / 64, NFT = F / 16;
   // LDS filter tile of one part: channel-major, a row of the chunk's 16
   // edges per channel, as 4 groups of 4 edges stored in the order
-  // g ^ ((channel >> 1) & 3): the 16-byte accesses of 8 consecutive lanes
-  // (channels) then fall in distinct bank groups without padding
+  // g ^ (((channel >> 1) ^ (channel >> 2)) & 3): the 16-byte accesses of any
+  // 8 (and any 16) consecutive lanes (channels) then fall in distinct 4-bank
+  // groups of a 32-bank (and a 64-bank) LDS, without padding
   constexpr int WLD = 16;
   static_assert(sizeof(A) == 4, "FP32 accumulation");
-  auto wslot = [](int ch, int g) { return ch * WLD + 4 * (g ^ ((ch >> 1) & 3)); };
+  auto wslot = [](int ch, int g) { return ch * WLD + 4 * (g ^ (((ch >> 1) ^ (ch >> 2)) & 3)); };
   constexpr int kcols = KBM * P::KC;
   // VGPRs held by the filter's B fragments decide how much else is in flight
   constexpr int BF_REGS = 12 * KBM * (int)sizeof(Fr) / 4;
