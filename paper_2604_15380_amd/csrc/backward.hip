@@ -872,7 +872,11 @@ k_message_bwd(MsgBwdArgs a) {
       const A v0 = P::ld(vv[jb + ch]), v1 = P::ld(vv[jb + F + ch]), v2 = P::ld(vv[jb + 2 * F + ch]);
 #pragma unroll
       for (int i = 0; i < 4; ++i) {
-        const A g_s = gsr[q][i], g0 = gvr[q][i][0], g1 = gvr[q][i][1], g2 = gvr[q][i][2];
+        // rows past the chunk add exactly nothing (not 0 x receiver 0's
+        // gradient, which may be NaN)
+        const bool live = er[i] >= 0;
+        const A g_s = live ? gsr[q][i] : A(0), g0 = live ? gvr[q][i][0] : A(0);
+        const A g1 = live ? gvr[q][i][1] : A(0), g2 = live ? gvr[q][i][2] : A(0);
         const A Av = g0 * v0 + g1 * v1 + g2 * v2;
         const A Ar = g0 * rh[i][0] + g1 * rh[i][1] + g2 * rh[i][2];
         acc_h[q][0] += g_s * w[0][i];
@@ -935,6 +939,294 @@ k_message_bwd(MsgBwdArgs a) {
     j = jn;
     c0 = cn;
   }
+}
+
+// Channel-per-lane form of the reverse message (FP32).  A workgroup of MBL_NW
+// waves owns MB_RB2 consecutive senders and a 64 MBL_NW-channel slice of the
+// features (wide layers take several slices in consecutive workgroups); each
+// wave owns 64 channels and keeps their filter B fragments in registers.
+// The block's sender-ordered edges (its senders' rows back to back) stream in
+// 16-edge chunks that may span senders.  Per chunk the wave forms the filter
+// w and its d-derivative w' on the matrix cores (the same B fragments against
+// the basis rows and their derivatives) and parks both in LDS, channel-major;
+// then every lane, one channel, walks the chunk's edges.  The receiver of an
+// edge is wave-uniform, so each gather of g_s', g_v' reads 256 contiguous
+// bytes.  The sender's dE/dh and v terms stay in the lane until its last
+// edge.  Every 4 edges the 16 per-edge channel sums (dE/dd and dE/drhat of 4
+// edges) are reduce-scattered over the wave and added to the edges' slots of
+// this wave: one add per slot per launch, so the sums are deterministic.
+constexpr int MB_RB2 = 8;
+
+template <int F>
+constexpr int mbl_nw() { return F / 64 < 2 ? F / 64 : 2; }
+
+template <class P, int F, int KBM>
+__global__ void __launch_bounds__((64 * mbl_nw<F>())) __attribute__((amdgpu_waves_per_eu(2)))
+k_message_bwd_lane(MsgBwdArgs a) {
+  using T = typename P::T;
+  using A = typename P::A;
+  using C = typename P::C;
+  using Fr = typename P::Fr;
+  static_assert(sizeof(T) == 4 && sizeof(A) == 4, "FP32 storage and accumulation");
+  constexpr int NWB = mbl_nw<F>(), SLICES = F / 64 / NWB, NW = F / 64, NFT = F / 16;
+  static_assert(F % 64 == 0 && (F / 64) % NWB == 0, "64-channel waves");
+  constexpr int kcols = KBM * P::KC;
+  constexpr int BF_REGS = 12 * KBM;
+  constexpr int QI = BF_REGS > 100 ? 1 : 2;       // feature tiles whose MFMA chains run together
+  constexpr int EG = BF_REGS > 100 ? 4 : 8;       // edges gathered per group (a multiple of 4)
+  // LDS tiles of w and w' (3 parts each): channel-major, the chunk's 16 edges
+  // per channel as 4 groups of 4 in the order g ^ (((ch >> 1) ^ (ch >> 2)) & 3),
+  // so 16-byte accesses by 8 or 16 consecutive lanes hit distinct bank groups
+  constexpr int WLD = 16;
+  __shared__ __attribute__((aligned(16))) A Wt[NWB][6][64 * WLD];
+  auto wslot = [](int ch, int g) { return ch * WLD + 4 * (g ^ (((ch >> 1) ^ (ch >> 2)) & 3)); };
+  const int per_xcd = gridDim.x / 8;
+  const int lb = (blockIdx.x % 8) * per_xcd + blockIdx.x / 8;
+  const int lane = threadIdx.x & 63, wl = threadIdx.x >> 6;
+  const int wave = (lb % SLICES) * NWB + wl;    // this wave's slot among the feature set's NW
+  const int c = 64 * wave + lane;               // this lane's channel
+  const int j0 = lb / SLICES * MB_RB2;
+  if (j0 >= a.N) return;
+  const int j1 = min(a.N, j0 + MB_RB2);
+  const int tp_lane = a.t_ptr[j0 + min(lane, j1 - j0)];
+  auto tp = [&](int j) { return __builtin_amdgcn_readlane(tp_lane, j - j0); };
+  const T* Wf = (const T*)a.filt.w;
+  const T* h = (const T*)a.h;
+  const T* vv = (const T*)a.v;
+  const A* gs = (const A*)a.gs;
+  const A* gv = (const A*)a.gv;
+  const A* einfo = (const A*)a.einfo;
+  const T* basis = (const T*)a.basis;
+  const T* dbasis = (const T*)a.dbasis;
+  A* gh_out = (A*)a.gh;
+  A* gv_out = (A*)a.gv_out;
+  A* eg = (A*)a.eg;
+  // senders without incoming edges: g_h = 0, g_v = g_v'
+  for (int j = j0; j < j1; ++j)
+    if (tp(j) == tp(j + 1)) {
+      const size_t jb = (size_t)j * 3 * F;
+#pragma unroll
+      for (int k = 0; k < 3; ++k) {
+        gh_out[jb + k * F + c] = A(0);
+        gv_out[jb + k * F + c] = gv[jb + k * F + c];
+      }
+    }
+  const int T0 = tp(j0), T1 = tp(j1);
+  if (T0 == T1) return;
+  // The filter's B fragments stay in registers unless they are many (a
+  // long filter input); then they stream from the caches chunk by chunk (an
+  // opaque copy of the pointer keeps the compiler from hoisting them).
+  constexpr bool BREG = BF_REGS <= 120;
+  Fr Bf[BREG ? 4 : 1][3][BREG ? KBM : 1];
+  if constexpr (BREG) {
+#pragma unroll
+    for (int q = 0; q < 4; ++q)
+#pragma unroll
+      for (int part = 0; part < 3; ++part)
+#pragma unroll
+        for (int kb = 0; kb < KBM; ++kb) {
+          const int ct = part * NFT + 4 * wave + q;
+          Bf[q][part][kb] = P::frag(Wf + ((size_t)(ct * KBM + kb) * 64 + lane) * P::KPL);
+        }
+  }
+  A* wt = Wt[wl][0];
+  auto first_with_edges = [&](int j) {
+    while (j < j1 && tp(j) == tp(j + 1)) ++j;
+    return j;
+  };
+  // the next chunk's A rows (position cc0 + lane % 16; past the stream's end
+  // the zero row E) and, in lanes e < ccnt, edge cc0 + e's id, rhat and
+  // receiver
+  Fr Gn[KBM], Dn[KBM];
+  int idn = -1;
+  A exn = 0, eyn = 0, ezn = 0, ern = 0;
+  auto prefetch = [&](int cc0, int ccnt) {
+    const int r = (lane & 15) < ccnt ? cc0 + (lane & 15) : (int)a.E;
+    const T* gp = basis + (size_t)r * kcols + (lane >> 4) * P::KPL;
+    const T* dp = dbasis + (size_t)r * kcols + (lane >> 4) * P::KPL;
+#pragma unroll
+    for (int kb = 0; kb < KBM; ++kb) {
+      Gn[kb] = P::frag(gp + kb * P::KC);
+      Dn[kb] = P::frag(dp + kb * P::KC);
+    }
+    idn = -1;
+    exn = eyn = ezn = ern = 0;
+    if (lane < ccnt) {
+      const A* ei = einfo + 4 * (size_t)(cc0 + lane);
+      idn = a.t_edge[cc0 + lane];
+      exn = ei[0];
+      eyn = ei[1];
+      ezn = ei[2];
+      ern = ei[3];
+    }
+  };
+  int c0 = T0;
+  prefetch(c0, min(16, T1 - c0));
+  // the sender being summed: j, whose edges end at sb; its h and v at this
+  // lane's channel
+  int j = first_with_edges(j0);
+  int sb = tp(j + 1);
+  size_t jb = (size_t)j * 3 * F;
+  A hs, hv, hr, v0, v1, v2;
+  auto load_sender = [&] {
+    hs = P::ld(h[jb + c]);
+    hv = P::ld(h[jb + F + c]);
+    hr = P::ld(h[jb + 2 * F + c]);
+    v0 = P::ld(vv[jb + c]);
+    v1 = P::ld(vv[jb + F + c]);
+    v2 = P::ld(vv[jb + 2 * F + c]);
+  };
+  load_sender();
+  A acc_h0 = 0, acc_h1 = 0, acc_h2 = 0, acc_v0 = 0, acc_v1 = 0, acc_v2 = 0;
+  auto write_out = [&] {
+    const A g0 = gv[jb + c], g1 = gv[jb + F + c], g2 = gv[jb + 2 * F + c];
+    gh_out[jb + c] = acc_h0;
+    gh_out[jb + F + c] = acc_h1;
+    gh_out[jb + 2 * F + c] = acc_h2;
+    gv_out[jb + c] = g0 + acc_v0;
+    gv_out[jb + F + c] = g1 + acc_v1;
+    gv_out[jb + 2 * F + c] = g2 + acc_v2;
+  };
+  // edge c0 + e starts the next sender: write sender j out and move on (a
+  // wave-uniform branch; the last sender is written after the stream)
+  auto next_sender = [&] {
+    write_out();
+    acc_h0 = acc_h1 = acc_h2 = acc_v0 = acc_v1 = acc_v2 = 0;
+    j = first_with_edges(j + 1);
+    sb = tp(j + 1);
+    jb = (size_t)j * 3 * F;
+    load_sender();
+  };
+  while (true) {
+    const int cnt = min(16, T1 - c0);
+    Fr Ga[KBM], Gd[KBM];
+#pragma unroll
+    for (int kb = 0; kb < KBM; ++kb) {
+      Ga[kb] = Gn[kb];
+      Gd[kb] = Dn[kb];
+    }
+    const int eid = idn;
+    const A ex = exn, ey = eyn, ez = ezn, er = ern;
+    const int cn = c0 + 16;
+    const bool more = cn < T1;
+    if (more) prefetch(cn, min(16, T1 - cn));
+    // w and w' of 4 feature tiles x 3 parts into LDS
+    const T* Wc = Wf;
+    if constexpr (!BREG) asm volatile("" : "+s"(Wc));
+#pragma unroll
+    for (int q0 = 0; q0 < 4; q0 += QI) {
+      C w[QI][3], wd[QI][3];
+#pragma unroll
+      for (int q = 0; q < QI; ++q)
+#pragma unroll
+        for (int part = 0; part < 3; ++part)
+          for (int r = 0; r < 4; ++r) w[q][part][r] = wd[q][part][r] = 0;
+#pragma unroll
+      for (int kb = 0; kb < KBM; ++kb)
+#pragma unroll
+        for (int q = 0; q < QI; ++q)
+#pragma unroll
+          for (int part = 0; part < 3; ++part) {
+            Fr b;
+            if constexpr (BREG) {
+              b = Bf[q0 + q][part][kb];
+            } else {
+              const int ct = part * NFT + 4 * wave + q0 + q;
+              b = P::frag(Wc + ((size_t)(ct * KBM + kb) * 64 + lane) * P::KPL);
+            }
+            w[q][part] = P::mfma(Ga[kb], b, w[q][part]);
+            wd[q][part] = P::mfma(Gd[kb], b, wd[q][part]);
+          }
+      // this lane's 4 accumulator rows are the 4 consecutive edges of group
+      // lane / 16 at one channel: one 16-byte write per part
+#pragma unroll
+      for (int q = 0; q < QI; ++q) {
+        const int o = wslot(16 * (q0 + q) + (lane & 15), lane >> 4);
+#pragma unroll
+        for (int part = 0; part < 3; ++part) {
+          *(f4_t*)(wt + part * 64 * WLD + o) = f4_t{w[q][part][0], w[q][part][1], w[q][part][2], w[q][part][3]};
+          *(f4_t*)(wt + (3 + part) * 64 * WLD + o) =
+              f4_t{wd[q][part][0], wd[q][part][1], wd[q][part][2], wd[q][part][3]};
+        }
+      }
+    }
+    __builtin_amdgcn_wave_barrier();
+    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+    // receivers' g_s', g_v' at this lane's channel for EG edges (past the
+    // stream's end the receiver is row 0 and the filter zero)
+    A gg[4][EG];
+    auto gather = [&](int ebase) {
+#pragma unroll
+      for (int u = 0; u < EG; ++u) {
+        const int i = acc_index(__int_as_float(__builtin_amdgcn_readlane(__float_as_int(er), ebase + u)));
+        const size_t ib = (size_t)i * 3 * F;
+        gg[0][u] = gs[(size_t)i * F + c];
+        gg[1][u] = gv[ib + c];
+        gg[2][u] = gv[ib + F + c];
+        gg[3][u] = gv[ib + 2 * F + c];
+      }
+    };
+    auto consume = [&](int ebase) {
+#pragma unroll
+      for (int u4 = 0; u4 < EG; u4 += 4) {
+        const int o = wslot(lane, (ebase + u4) / 4);
+        const f4_t ws4 = *(const f4_t*)(wt + o), wv4 = *(const f4_t*)(wt + 64 * WLD + o);
+        const f4_t wr4 = *(const f4_t*)(wt + 2 * 64 * WLD + o);
+        const f4_t ds4 = *(const f4_t*)(wt + 3 * 64 * WLD + o), dv4 = *(const f4_t*)(wt + 4 * 64 * WLD + o);
+        const f4_t dr4 = *(const f4_t*)(wt + 5 * 64 * WLD + o);
+        // per edge: [dE/dd, dE/drhat x, y, z] partial sums of this channel
+        A vals[16];
+#pragma unroll
+        for (int uu = 0; uu < 4; ++uu) {
+          const int u = u4 + uu, e = ebase + u;
+          if (c0 + e == sb && sb < T1) next_sender();
+          const A rx = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(ex), e));
+          const A ry = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(ey), e));
+          const A rz = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(ez), e));
+          // past the stream's end: exactly nothing (not 0 x receiver 0's
+          // gradient, which may be NaN)
+          const bool live = e < cnt;
+          const A g_s = live ? gg[0][u] : A(0), g0 = live ? gg[1][u] : A(0);
+          const A g1 = live ? gg[2][u] : A(0), g2 = live ? gg[3][u] : A(0);
+          const A Av = g0 * v0 + g1 * v1 + g2 * v2;
+          const A Ar = g0 * rx + g1 * ry + g2 * rz;
+          acc_h0 += g_s * ws4[uu];
+          acc_h1 += Av * wv4[uu];
+          acc_h2 += Ar * wr4[uu];
+          const A tv = hv * wv4[uu], tr = hr * wr4[uu];
+          acc_v0 += g0 * tv;
+          acc_v1 += g1 * tv;
+          acc_v2 += g2 * tv;
+          vals[4 * uu] = g_s * hs * ds4[uu] + Av * hv * dv4[uu] + Ar * hr * dr4[uu];
+          vals[4 * uu + 1] = g0 * tr;
+          vals[4 * uu + 2] = g1 * tr;
+          vals[4 * uu + 3] = g2 * tr;
+        }
+        // lane: value lane % 16 summed over its 16-lane row group, then over
+        // the wave's 4 row groups
+        reduce_scatter16<A, 16>(vals, lane);
+        A tot = vals[0];
+        tot += __shfl_xor(tot, 16);
+        tot += __shfl_xor(tot, 32);
+        const int k = lane & 15;
+        const int e_id = __shfl(eid, ebase + u4 + (k >> 2));
+        if (lane < 16 && e_id >= 0) unsafeAtomicAdd(eg + ((size_t)e_id * NW + wave) * 4 + (k & 3), tot);
+      }
+    };
+#pragma unroll
+    for (int eb0 = 0; eb0 < 16; eb0 += EG)
+      if (eb0 < cnt) {
+        gather(eb0);
+        consume(eb0);
+      }
+    __builtin_amdgcn_wave_barrier();
+    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+    if (!more) break;
+    c0 = cn;
+  }
+  write_out();
 }
 
 // ------------------------------------------------------------------ forces ----
@@ -1005,15 +1297,23 @@ hipError_t allow_lds(K kernel, size_t smem) {
 
 template <class P, int F, int KBM>
 void launch_message_bwd_kbm(hipStream_t st, const MsgBwdArgs& ma) {
-  constexpr int NWB = mb_nwb<P, F, KBM>(), SLICES = F / 16 / mb_ftw<P, F, KBM>() / NWB;
-  const int blocks = (int)(((long long)(ma.N + MB_RB - 1) / MB_RB * SLICES + 7) / 8 * 8);
-  k_message_bwd<P, F, KBM><<<blocks, 64 * NWB, 0, st>>>(ma);
+  if constexpr (sizeof(typename P::T) == 4) {
+    constexpr int NWB = mbl_nw<F>(), SLICES = F / 64 / NWB;
+    const int blocks = (int)(((long long)(ma.N + MB_RB2 - 1) / MB_RB2 * SLICES + 7) / 8 * 8);
+    k_message_bwd_lane<P, F, KBM><<<blocks, 64 * NWB, 0, st>>>(ma);
+  } else {
+    constexpr int NWB = mb_nwb<P, F, KBM>(), SLICES = F / 16 / mb_ftw<P, F, KBM>() / NWB;
+    const int blocks = (int)(((long long)(ma.N + MB_RB - 1) / MB_RB * SLICES + 7) / 8 * 8);
+    k_message_bwd<P, F, KBM><<<blocks, 64 * NWB, 0, st>>>(ma);
+  }
 }
 
 // Per-edge slots of the reverse message kernel (one per wave of a feature
-// slice set), for a filter input of nkb k-blocks.
+// slice set), for a filter input of nkb k-blocks: FP32 runs the
+// channel-per-lane form (64 channels per wave).
 template <class P, int F>
 int message_bwd_slots(int nkb) {
+  if constexpr (sizeof(typename P::T) == 4) return F / 64;
   return F / 16 / (nkb == 3 ? mb_ftw<P, F, 3>() : mb_ftw<P, F, 6>());
 }
 
