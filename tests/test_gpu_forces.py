@@ -248,9 +248,13 @@ def test_deterministic_and_graph_rebuild(rt):
     m.free()
 
 
-def test_dataset_id_out_of_range(rt):
+@pytest.mark.parametrize("prec", ["fp64", "fp32"])
+@pytest.mark.parametrize("bad", [3, 0])
+def test_dataset_id_out_of_range(rt, bad, prec):
     """A structure whose dataset id names no head gets NaN energy and NaN
-    forces; the other structures are unaffected."""
+    forces; the other structures are unaffected.  With the first structure
+    invalid, atom 0 carries a NaN gradient: the reverse message's padding
+    rows (which point at row 0) must add exactly nothing."""
     import torch
     hp = synth.HyperParams(F=64, K=6, L=2, n_species=85, n_heads=3, cutoff=5.0, shared_dims=[],
                            branch_dims=[16, 1])
@@ -258,17 +262,17 @@ def test_dataset_id_out_of_range(rt):
     m = rt.load_model(synth.weight_file_bytes(hp, W))
     b = synth.make_batch("screening", 0, 8)
     b.dataset_id = b.dataset_id % hp.n_heads
-    b.dataset_id[3] = 7
+    b.dataset_id[bad] = 7
     inp = rt.upload_batch(b)
     g = rt.build_graph(inp, hp.cutoff)
-    E, Fo = rt.forces(m, g, "fp64", dataset_id=inp["dataset_id"])
+    E, Fo = rt.forces(m, g, prec, dataset_id=inp["dataset_id"])
     torch.cuda.synchronize()
     E, Fo = E.cpu().numpy(), Fo.cpu().numpy()
-    lo, hi = int(b.struct_ptr[3]), int(b.struct_ptr[4])
-    assert np.isnan(E[3]) and np.all(np.isnan(Fo[lo:hi]))
-    keep = [k for k in range(b.n_struct) if k != 3]
+    lo, hi = int(b.struct_ptr[bad]), int(b.struct_ptr[bad + 1])
+    assert np.isnan(E[bad]) and np.all(np.isnan(Fo[lo:hi]))
+    keep = [k for k in range(b.n_struct) if k != bad]
     assert np.all(np.isfinite(np.delete(Fo, np.s_[lo:hi], axis=0)))
-    check_forces(Fo, b, oracle(b, hp, W, keep), keep, FORCE_TOL["fp64"], "other structures")
+    check_forces(Fo, b, oracle(b, hp, W, keep), keep, FORCE_TOL[prec], "other structures")
     g.free()
     m.free()
 
