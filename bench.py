@@ -101,13 +101,16 @@ def kernel_work(kernel: str, hp, N: int, E: int, prec: str, head_entries: int | 
     return None, 0.0, 0.0
 
 
-def load_traffic(key: str, digest: str, launches_kernel: str):
+def load_traffic(key: str, digest: str, kernel: str):
+    """HBM bytes per launch of `kernel` in workload/precision `key`, from the
+    stored counter measurement, or None when there is none for that kernel
+    or the kernel sources changed since it was taken."""
     try:
         with open(TRAFFIC_FILE) as f:
-            t = json.load(f).get(key)
-    except (OSError, ValueError):
+            t = (json.load(f).get(key) or {}).get(kernel)
+    except (OSError, ValueError, AttributeError):
         return None
-    if not t or t.get("kernel") != launches_kernel or t.get("source_digest") != digest:
+    if not t or t.get("source_digest") != digest:
         return None
     return t.get("bytes_per_launch")
 
