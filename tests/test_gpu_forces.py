@@ -82,6 +82,61 @@ def test_molecules(rt, precision):
     run_case(rt, hp, W, b, precision, f"molecules {precision}")
 
 
+def _cluster(rng, n, spacing=1.2):
+    """n atoms of a simple cubic lattice (first n sites of a 4^3 block),
+    each moved by at most 0.15 A: every pair at least 0.9 A apart."""
+    g = np.stack(np.meshgrid(np.arange(4), np.arange(4), np.arange(4), indexing="ij"), -1).reshape(-1, 3)
+    return g[:n] * spacing + rng.uniform(-0.15, 0.15, (n, 3)) / np.sqrt(3)
+
+
+def chunk_boundary_batch():
+    """Receivers whose edge rows straddle and fill the 16-edge chunks in every
+    way the packed streams meet them: isolated atoms between atoms with edges
+    (rows of length 0 inside a block), a chain (1-2 edges per atom, several
+    receivers per chunk), a dimer, and dense clusters (up to ~39 edges per
+    atom: rows over 2 and 3 chunks)."""
+    rng = np.random.default_rng(4711)
+    no_cell, no_pbc = np.zeros((3, 3)), np.zeros(3, np.uint8)
+    sp = lambda n: rng.integers(0, 10, n)
+    structs = [
+        (np.array([[0.0, 0, 0], [1.2, 0.3, 0]]), sp(2), no_cell, no_pbc, 0),
+        (np.array([[0.0, 0, 0], [20.0, 0, 0], [40.0, 0, 0]]), sp(3), no_cell, no_pbc, 0),
+        (np.arange(9)[:, None] * np.array([[4.5, 0.0, 0.0]]), sp(9), no_cell, no_pbc, 0),
+        (_cluster(rng, 40), sp(40), no_cell, no_pbc, 0),
+        (np.array([[3.0, 3.0, 3.0]]), sp(1), no_cell, no_pbc, 0),
+        (_cluster(rng, 20), sp(20), no_cell, no_pbc, 0),
+        (np.array([[0.0, 0, 0], [30.0, 0, 0]]), sp(2), no_cell, no_pbc, 0),
+        (_cluster(rng, 13, 1.5), sp(13), no_cell, no_pbc, 0),
+    ]
+    return synth.concat(structs)
+
+
+@pytest.mark.parametrize("precision", ["fp64", "fp32"])
+@pytest.mark.parametrize("F,K", [(64, 20), (128, 6)])
+def test_chunk_boundaries(rt, precision, F, K):
+    """Energies and forces where the message streams' chunks span receivers
+    (forward) and senders (reverse) of every row length, including empty rows
+    inside a block."""
+    import torch
+    from oracle.painn import structure_forward
+    say(f"chunk boundaries F={F} K={K}, {precision}")
+    hp = synth.HyperParams(F=F, K=K, L=2, n_species=10, n_heads=1, cutoff=5.0,
+                           shared_dims=[], branch_dims=[16, 1])
+    W = synth.make_weights(hp, 3150 + F + K)
+    b = chunk_boundary_batch()
+    m = rt.load_model(synth.weight_file_bytes(hp, W))
+    g = rt.build_graph(rt.upload_batch(b), hp.cutoff)
+    E0 = rt.forward(m, g, precision).cpu().numpy()
+    tol = {"fp64": 1e-10, "fp32": 1e-5}[precision]
+    for k in range(b.n_struct):
+        pos, z, cell, pbc, _ = b.structure(k)
+        o = structure_forward(pos, z, cell, pbc, 0, hp, W)
+        assert abs(E0[k] - o["E"]) <= tol * max(np.abs(o["e"]).sum(), 1e-30), (k, E0[k], o["E"])
+    g.free()
+    m.free()
+    run_case(rt, hp, W, b, precision, f"chunk boundaries F={F} {precision}")
+
+
 @pytest.mark.parametrize("precision", ["fp64", "fp32"])
 def test_periodic(rt, precision):
     say(f"periodic cells, {precision}")
