@@ -8,23 +8,36 @@
 // Data layout in HBM (row-major, storage type T of the precision):
 //   s [N][F], v [N][3][F] (double buffered), h [N][3F] = [h_s | h_v | h_r],
 //   e [N] (accumulation type).  Edges: CSR sorted by receiver.
+#include <type_traits>
+
 #include "mfma.h"
 
 namespace {
 
 // ---------------------------------------------------------------- embed ----
+// s = emb[species], v = 0 and, when h is given, layer 0's h = h0[species]
+// (the species' row of the phi table: phi acts on each row by itself, so
+// the row is what phi gives for the atom's own s).
 template <class P>
 __global__ void __launch_bounds__(256) k_embed(int N, int F, const int32_t* __restrict__ species,
                                               const typename P::T* __restrict__ emb,
+                                              const typename P::T* __restrict__ h0,
                                               typename P::T* __restrict__ s,
-                                              typename P::T* __restrict__ v) {
+                                              typename P::T* __restrict__ v,
+                                              typename P::T* __restrict__ h) {
   const size_t tot = (size_t)N * F;
   for (size_t x = blockIdx.x * (size_t)blockDim.x + threadIdx.x; x < tot; x += (size_t)gridDim.x * blockDim.x) {
     const size_t i = x / F, f = x % F;
-    s[x] = emb[(size_t)species[i] * F + f];
+    const size_t z = (size_t)species[i];
+    s[x] = emb[z * F + f];
     v[3 * i * F + f] = P::st(0);
     v[3 * i * F + F + f] = P::st(0);
     v[3 * i * F + 2 * F + f] = P::st(0);
+    if (h) {
+      h[3 * i * F + f] = h0[3 * z * F + f];
+      h[3 * i * F + F + f] = h0[3 * z * F + F + f];
+      h[3 * i * F + 2 * F + f] = h0[3 * z * F + 2 * F + f];
+    }
   }
 }
 
@@ -1428,15 +1441,12 @@ hipError_t forward_impl(hipStream_t st, ForwardArgs& fa) {
     fa.s = sv.S(fa.stop_layer + 1);   // the heads read the final s
   }
   if (N > 0) {
+    // embedding, and layer 0's phi from the per-species table
     prof_mark(fa.prof, st, KC_EMBED, true);
-    k_embed<P><<<grid_for((size_t)N * F, 256), 256, 0, st>>>(N, F, g->species, (const T*)pm->emb, s, v[0]);
+    k_embed<P><<<grid_for((size_t)N * F, 256), 256, 0, st>>>(N, F, g->species, (const T*)pm->emb,
+                                                           (const T*)pm->h0, s, v[0],
+                                                           fa.stop_layer >= 0 ? h : nullptr);
     prof_mark(fa.prof, st, KC_EMBED, false);
-    if (fa.stop_layer >= 0) {
-      prof_mark(fa.prof, st, KC_PHI, true);
-      k_phi<P, F, RT><<<(N + 16 * RT - 1) / (16 * RT), 256, 0, st>>>(N, s, h, pm->layers[0].phi1,
-                                                                   pm->layers[0].phi2);
-      prof_mark(fa.prof, st, KC_PHI, false);
-    }
   }
   int cur = 0;
   const int kcols = pm->layers.empty() ? 0 : pm->layers[0].filt_mma.din_p;
@@ -1530,7 +1540,33 @@ hipError_t forward_prec(hipStream_t st, ForwardArgs& fa) {
   }
 }
 
+template <class P>
+hipError_t phi0_table(hipStream_t st, int F, int S, const PrecModel* pm, void* out) {
+  using T = typename P::T;
+  if (S <= 0) return hipSuccess;
+  auto run = [&](auto f) {
+    constexpr int FF = decltype(f)::value;
+    constexpr int RT = ((sizeof(T) == 8 && FF >= 256) || FF > 256) ? 1 : 2;
+    k_phi<P, FF, RT><<<(S + 16 * RT - 1) / (16 * RT), 256, 0, st>>>(S, (const T*)pm->emb, (T*)out,
+                                                                   pm->layers[0].phi1, pm->layers[0].phi2);
+    return hipGetLastError();
+  };
+  switch (F) {
+    case 64: return run(std::integral_constant<int, 64>{});
+    case 128: return run(std::integral_constant<int, 128>{});
+    case 256: return run(std::integral_constant<int, 256>{});
+    case 384: return run(std::integral_constant<int, 384>{});
+    default: return hipErrorInvalidValue;
+  }
+}
+
 }  // namespace
+
+hipError_t launch_phi0_table(hipStream_t st, int prec, int F, int S, const PrecModel* pm, void* out) {
+  if (prec == PAINN_FP64) return phi0_table<P64>(st, F, S, pm, out);
+  if (prec == PAINN_FP32) return phi0_table<P32>(st, F, S, pm, out);
+  return phi0_table<PB16>(st, F, S, pm, out);
+}
 
 hipError_t launch_forward(hipStream_t st, int prec, ForwardArgs& fa) {
   if (prec == PAINN_FP64) return forward_prec<P64>(st, fa);

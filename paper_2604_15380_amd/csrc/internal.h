@@ -97,6 +97,10 @@ struct LayerDev {       // one interaction layer
 struct PrecModel {      // the model cast and packed for one precision
   int prec = -1;
   void* emb = nullptr;  // [n_species][F] storage type
+  // layer 0's phi of every species' embedding, [n_species][3F] storage type:
+  // s before the first layer depends on the species alone, and phi acts on
+  // each row by itself, so an atom's h of layer 0 is its species' row
+  void* h0 = nullptr;
   std::vector<LayerDev> layers;
   std::vector<DenseDev> shared;                 // shared head layers
   std::vector<std::vector<DenseDev>> branch;    // [head][layer]
@@ -320,3 +324,6 @@ hipError_t launch_transpose(hipStream_t s, Profiler* p, painn_graph* g);
 size_t forward_workspace_bytes(int prec, int N, long long E, int F, int kcols, int B, int H,
                                int S, bool blend);
 hipError_t launch_forward(hipStream_t s, int prec, ForwardArgs& a);
+// pm->h0 from pm->emb and layer 0's phi (enqueued on s; out holds
+// n_species x 3F storage elements)
+hipError_t launch_phi0_table(hipStream_t s, int prec, int F, int n_species, const PrecModel* pm, void* out);

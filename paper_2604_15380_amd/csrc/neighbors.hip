@@ -105,8 +105,13 @@ __global__ void __launch_bounds__(256) k_prep(int B, int N, const int32_t* __res
     }
   }
   if (lane == 0 && hi > lo) {
-    atomicMin(&st->species_min, smin);
-    atomicMax(&st->species_max, smax);
+    // every structure's wave reports to the same two words: read first and
+    // add to the contention only when the bound moves (the reads may be
+    // stale, which only costs an atomic that changes nothing)
+    if (smin < __hip_atomic_load(&st->species_min, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT))
+      atomicMin(&st->species_min, smin);
+    if (smax > __hip_atomic_load(&st->species_max, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT))
+      atomicMax(&st->species_max, smax);
   }
   const int n = hi - lo;
   const double bin_w = cutoff * (1.0 + CELL_MARGIN);

@@ -242,6 +242,15 @@ painn_status build_prec(painn_model* m, int prec, PrecModel** out) {
       idx += 2;
     }
   }
+  if (e == hipSuccess && hp.L > 0) {
+    // layer 0's phi per species, computed once on the context's stream
+    const size_t bytes = (size_t)hp.n_species * 3 * F * elem_bytes(prec);
+    e = hipMalloc(&pm->h0, bytes ? bytes : 16);
+    if (e == hipSuccess) {
+      pm->allocs.push_back(pm->h0);
+      e = launch_phi0_table(ctx->stream, prec, F, hp.n_species, pm, pm->h0);
+    }
+  }
   if (e != hipSuccess) {
     free_prec(pm);
     return hip_fail(ctx, e, "uploading packed weights");
