@@ -54,7 +54,10 @@ def kernel_work(kernel: str, hp, N: int, E: int, prec: str, head_entries: int | 
     message: per edge 6KF (radial filter contraction over K Gaussians for 3F
              channels) + 22F (cutoff and bias, scalar and vector messages);
              minimum HBM bytes: per atom h (3F), v in (3F), s (F) read and s
-             (F), v out (3F) written, plus 8 bytes of CSR per edge.
+             (F), v out (3F) written, plus 8 bytes of CSR per edge.  The first
+             layer's v is zero, so its launch forms 2 of the 3 filter parts
+             (4KF), does half the elementwise work (11F) and reads no v; the
+             figure per launch is the mean over the L launches.
     update:  per atom 22 F^2 (U/V 12F^2, gate MLP 10F^2) + 8 F^2 for the next
              layer's phi fused behind it (all but the last layer).
     phi:     per atom 8 F^2.
@@ -75,7 +78,9 @@ def kernel_work(kernel: str, hp, N: int, E: int, prec: str, head_entries: int | 
     F, K, L = hp.F, hp.K, hp.L
     b = ELEM[prec]
     if kernel == "message":
-        return "alu", E * (6.0 * K * F + 22.0 * F), N * 11.0 * F * b + 8.0 * E
+        fl = E * ((L - 1) * (6.0 * K * F + 22.0 * F) + (4.0 * K * F + 11.0 * F)) / L
+        nb = N * ((L - 1) * 11.0 + 8.0) / L * F * b + 8.0 * E
+        return "alu", fl, nb
     if kernel == "update":
         fl = N * (22.0 * F * F + 8.0 * F * F * (L - 1) / L)
         return "mfma", fl, N * (8.0 * F + 3.0 * F * (L - 1) / L) * b

@@ -118,6 +118,7 @@ struct MsgArgs {
   const void* s_in;    // s before the message (may equal s)
   void* s;             // s after the message
   void* v_out;
+  int v_zero;          // v_in is all zero (the first layer): its terms vanish
 };
 
 constexpr int MSG_RB = 4;   // receivers per workgroup (MSG_RB < 64)
@@ -221,7 +222,7 @@ __global__ void __launch_bounds__(EP_THREADS) k_edge_prep(long long E, int K, in
 // channel) letting every lane combine the filter with the gathered sender
 // features of its edges directly; a receiver's per-lane partial sums are
 // reduced across the four row groups of the wavefront at its last edge.
-template <class P, int F, int NW, int KBM>
+template <class P, int F, int NW, int KBM, bool V0>
 __global__ void __launch_bounds__(NW * 64) k_message(MsgArgs a) {
   using T = typename P::T;
   using A = typename P::A;
@@ -300,6 +301,8 @@ __global__ void __launch_bounds__(NW * 64) k_message(MsgArgs a) {
 #pragma unroll
         for (int part = 0; part < 3; ++part) {
           for (int r = 0; r < 4; ++r) w[part][r] = 0;
+          // with v_j = 0 the v part of the filter meets nothing
+          if (V0 && part == 1) continue;
 #pragma unroll
           for (int kb = 0; kb < KBM; ++kb) w[part] = P::mfma(Ga[kb], Bf[q][part][kb], w[part]);
         }
@@ -307,13 +310,21 @@ __global__ void __launch_bounds__(NW * 64) k_message(MsgArgs a) {
         for (int ii = 0; ii < 4; ++ii) {
           if (P::row(lane, ii) < cnt) {
             const size_t hb = (size_t)jj[ii] * 3 * F;
-            const A hs = P::ld(h[hb + f]), hv = P::ld(h[hb + F + f]), hr = P::ld(h[hb + 2 * F + f]);
-            const A v0 = P::ld(vin[hb + f]), v1 = P::ld(vin[hb + F + f]), v2 = P::ld(vin[hb + 2 * F + f]);
+            const A hs = P::ld(h[hb + f]), hr = P::ld(h[hb + 2 * F + f]);
             acc_s[q] += hs * w[0][ii];
-            const A pv = hv * w[1][ii], pr = hr * w[2][ii];
-            acc_v[q][0] += v0 * pv + rh[ii][0] * pr;
-            acc_v[q][1] += v1 * pv + rh[ii][1] * pr;
-            acc_v[q][2] += v2 * pv + rh[ii][2] * pr;
+            const A pr = hr * w[2][ii];
+            if constexpr (V0) {
+              acc_v[q][0] += rh[ii][0] * pr;
+              acc_v[q][1] += rh[ii][1] * pr;
+              acc_v[q][2] += rh[ii][2] * pr;
+            } else {
+              const A hv = P::ld(h[hb + F + f]);
+              const A v0 = P::ld(vin[hb + f]), v1 = P::ld(vin[hb + F + f]), v2 = P::ld(vin[hb + 2 * F + f]);
+              const A pv = hv * w[1][ii];
+              acc_v[q][0] += v0 * pv + rh[ii][0] * pr;
+              acc_v[q][1] += v1 * pv + rh[ii][1] * pr;
+              acc_v[q][2] += v2 * pv + rh[ii][2] * pr;
+            }
           }
         }
       }
@@ -885,7 +896,7 @@ constexpr int message_waves() {
   return 12 * KBM * (int)sizeof(typename P::Fr) / 4 > 150 ? 1 : 2;
 }
 
-template <class P, int F, int KBM>
+template <class P, int F, int KBM, bool V0>
 __global__ void __launch_bounds__(F) __attribute__((amdgpu_waves_per_eu(message_waves<P, KBM>())))
 k_message_lane(MsgArgs a) {
   using T = typename P::T;
@@ -1031,9 +1042,12 @@ k_message_lane(MsgArgs a) {
         gb[0][u] = hj[0];
         gb[1][u] = hj[F];
         gb[2][u] = hj[2 * F];
-        gb[3][u] = vj[0];
-        gb[4][u] = vj[F];
-        gb[5][u] = vj[2 * F];
+        // (with v_j = 0 the term v_j h^v_j w^v is exactly zero: not gathered)
+        if constexpr (!V0) {
+          gb[3][u] = vj[0];
+          gb[4][u] = vj[F];
+          gb[5][u] = vj[2 * F];
+        }
       }
     };
     auto consume = [&](int ebase) {
@@ -1045,19 +1059,26 @@ k_message_lane(MsgArgs a) {
         if (u % 4 == 0) {
           const int o = wslot(lane, e / 4);
           ws4 = *(const f4_t*)(wt0 + o);
-          wv4 = *(const f4_t*)(wt1 + o);
+          if constexpr (!V0) wv4 = *(const f4_t*)(wt1 + o);
           wr4 = *(const f4_t*)(wt2 + o);
         }
         // eb < E1: receiver i is not the block's last one (past the
         // stream's end, c0 + e >= E1 >= eb)
         if (c0 + e == eb && eb < E1) next_receiver();
         const A rx = bcast(ex, e), ry = bcast(ey, e), rz = bcast(ez, e);
-        const A ws = ws4[u % 4], wv = wv4[u % 4], wr = wr4[u % 4];
+        const A ws = ws4[u % 4], wr = wr4[u % 4];
         acc_s += P::ld(gb[0][u]) * ws;
-        const A pv = P::ld(gb[1][u]) * wv, pr = P::ld(gb[2][u]) * wr;
-        acc_v0 += P::ld(gb[3][u]) * pv + rx * pr;
-        acc_v1 += P::ld(gb[4][u]) * pv + ry * pr;
-        acc_v2 += P::ld(gb[5][u]) * pv + rz * pr;
+        const A pr = P::ld(gb[2][u]) * wr;
+        if constexpr (V0) {
+          acc_v0 += rx * pr;
+          acc_v1 += ry * pr;
+          acc_v2 += rz * pr;
+        } else {
+          const A pv = P::ld(gb[1][u]) * wv4[u % 4];
+          acc_v0 += P::ld(gb[3][u]) * pv + rx * pr;
+          acc_v1 += P::ld(gb[4][u]) * pv + ry * pr;
+          acc_v2 += P::ld(gb[5][u]) * pv + rz * pr;
+        }
       }
     };
     // the first group's gathers do not depend on the filter: issued before
@@ -1083,14 +1104,15 @@ k_message_lane(MsgArgs a) {
         for (int q = 0; q < QI; ++q)
 #pragma unroll
           for (int part = 0; part < 3; ++part)
-            w[q][part] = P::mfma(Ga[kb], Bf[q0 + q][part][kb], w[q][part]);
+            if (!V0 || part != 1)   // the v part of the filter only meets v_j
+              w[q][part] = P::mfma(Ga[kb], Bf[q0 + q][part][kb], w[q][part]);
       // this lane's 4 accumulator rows are the 4 consecutive edges of group
       // lane / 16 at one channel: one 16-byte write per part
 #pragma unroll
       for (int q = 0; q < QI; ++q) {
         const int o = wslot(16 * (q0 + q) + (lane & 15), lane >> 4);
         *(f4_t*)(wt0 + o) = f4_t{w[q][0][0], w[q][0][1], w[q][0][2], w[q][0][3]};
-        *(f4_t*)(wt1 + o) = f4_t{w[q][1][0], w[q][1][1], w[q][1][2], w[q][1][3]};
+        if constexpr (!V0) *(f4_t*)(wt1 + o) = f4_t{w[q][1][0], w[q][1][1], w[q][1][2], w[q][1][3]};
         *(f4_t*)(wt2 + o) = f4_t{w[q][2][0], w[q][2][1], w[q][2][2], w[q][2][3]};
       }
     }
@@ -1120,10 +1142,12 @@ void launch_message_kbm(hipStream_t st, const MsgArgs& a) {
     // would leave each wave too few registers)
     constexpr int NW = F > 256 ? F / 64 : F / 32;
     const int blocks = ((a.N + MSG_RB - 1) / MSG_RB + 7) / 8 * 8;   // a multiple of the 8 XCDs
-    k_message<P, F, NW, KBM><<<blocks, NW * 64, 0, st>>>(a);
+    if (a.v_zero) k_message<P, F, NW, KBM, true><<<blocks, NW * 64, 0, st>>>(a);
+    else k_message<P, F, NW, KBM, false><<<blocks, NW * 64, 0, st>>>(a);
   } else {
     const int blocks = ((a.N + MSG_RB2 - 1) / MSG_RB2 + 7) / 8 * 8;
-    k_message_lane<P, F, KBM><<<blocks, F, 0, st>>>(a);
+    if (a.v_zero) k_message_lane<P, F, KBM, true><<<blocks, F, 0, st>>>(a);
+    else k_message_lane<P, F, KBM, false><<<blocks, F, 0, st>>>(a);
   }
 }
 
@@ -1472,6 +1496,7 @@ hipError_t forward_impl(hipStream_t st, ForwardArgs& fa) {
     ma.h = fa.save ? sv.H(l) : h;
     ma.v_in = fa.save ? sv.V(l) : v[cur];
     ma.s_in = fa.save ? sv.S(l) : s;
+    ma.v_zero = l == 0;   // the embedding leaves v = 0
     ma.s = fa.save ? sv.Smid(l) : s;
     ma.v_out = fa.save ? sv.Vmid(l) : v[cur ^ 1];
     prof_mark(fa.prof, st, KC_MESSAGE, true);
