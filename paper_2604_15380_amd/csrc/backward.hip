@@ -656,6 +656,7 @@ struct MsgBwdArgs {
   void* gh;            // out
   void* gv_out;
   void* eg;            // [E][NW][4]
+  int first;           // the first layer: only eg is wanted (g_h, g_v are not written)
 };
 
 __device__ __forceinline__ int acc_index(float x) { return __float_as_int(x); }
@@ -960,7 +961,11 @@ constexpr int MB_RB2 = 8;
 template <int F>
 constexpr int mbl_nw() { return F / 64 < 2 ? F / 64 : 2; }
 
-template <class P, int F, int KBM>
+// L0: the first layer, where v = 0 and only the per-edge sums are wanted
+// (h and v of the first layer depend on the species alone): A_v = 0, so the
+// filter's v part and its derivative drop out, and dE/dd, dE/drhat need w^r,
+// w'^s and w'^r only; no g_h, g_v are formed.
+template <class P, int F, int KBM, bool L0>
 __global__ void __launch_bounds__((64 * mbl_nw<F>())) __attribute__((amdgpu_waves_per_eu(2)))
 k_message_bwd_lane(MsgBwdArgs a) {
   using T = typename P::T;
@@ -1002,15 +1007,16 @@ k_message_bwd_lane(MsgBwdArgs a) {
   A* gv_out = (A*)a.gv_out;
   A* eg = (A*)a.eg;
   // senders without incoming edges: g_h = 0, g_v = g_v'
-  for (int j = j0; j < j1; ++j)
-    if (tp(j) == tp(j + 1)) {
-      const size_t jb = (size_t)j * 3 * F;
+  if constexpr (!L0)
+    for (int j = j0; j < j1; ++j)
+      if (tp(j) == tp(j + 1)) {
+        const size_t jb = (size_t)j * 3 * F;
 #pragma unroll
-      for (int k = 0; k < 3; ++k) {
-        gh_out[jb + k * F + c] = A(0);
-        gv_out[jb + k * F + c] = gv[jb + k * F + c];
+        for (int k = 0; k < 3; ++k) {
+          gh_out[jb + k * F + c] = A(0);
+          gv_out[jb + k * F + c] = gv[jb + k * F + c];
+        }
       }
-    }
   const int T0 = tp(j0), T1 = tp(j1);
   if (T0 == T1) return;
   // The filter's B fragments stay in registers unless they are many (a
@@ -1070,15 +1076,20 @@ k_message_bwd_lane(MsgBwdArgs a) {
   A hs, hv, hr, v0, v1, v2;
   auto load_sender = [&] {
     hs = P::ld(h[jb + c]);
-    hv = P::ld(h[jb + F + c]);
     hr = P::ld(h[jb + 2 * F + c]);
-    v0 = P::ld(vv[jb + c]);
-    v1 = P::ld(vv[jb + F + c]);
-    v2 = P::ld(vv[jb + 2 * F + c]);
+    if constexpr (L0) {
+      hv = v0 = v1 = v2 = A(0);
+    } else {
+      hv = P::ld(h[jb + F + c]);
+      v0 = P::ld(vv[jb + c]);
+      v1 = P::ld(vv[jb + F + c]);
+      v2 = P::ld(vv[jb + 2 * F + c]);
+    }
   };
   load_sender();
   A acc_h0 = 0, acc_h1 = 0, acc_h2 = 0, acc_v0 = 0, acc_v1 = 0, acc_v2 = 0;
   auto write_out = [&] {
+    if constexpr (L0) return;
     const A g0 = gv[jb + c], g1 = gv[jb + F + c], g2 = gv[jb + 2 * F + c];
     gh_out[jb + c] = acc_h0;
     gh_out[jb + F + c] = acc_h1;
@@ -1127,6 +1138,7 @@ k_message_bwd_lane(MsgBwdArgs a) {
         for (int q = 0; q < QI; ++q)
 #pragma unroll
           for (int part = 0; part < 3; ++part) {
+            if (L0 && part == 1) continue;
             Fr b;
             if constexpr (BREG) {
               b = Bf[q0 + q][part][kb];
@@ -1134,7 +1146,7 @@ k_message_bwd_lane(MsgBwdArgs a) {
               const int ct = part * NFT + 4 * wave + q0 + q;
               b = P::frag(Wc + ((size_t)(ct * KBM + kb) * 64 + lane) * P::KPL);
             }
-            w[q][part] = P::mfma(Ga[kb], b, w[q][part]);
+            if (!L0 || part == 2) w[q][part] = P::mfma(Ga[kb], b, w[q][part]);
             wd[q][part] = P::mfma(Gd[kb], b, wd[q][part]);
           }
       // this lane's 4 accumulator rows are the 4 consecutive edges of group
@@ -1144,7 +1156,9 @@ k_message_bwd_lane(MsgBwdArgs a) {
         const int o = wslot(16 * (q0 + q) + (lane & 15), lane >> 4);
 #pragma unroll
         for (int part = 0; part < 3; ++part) {
-          *(f4_t*)(wt + part * 64 * WLD + o) = f4_t{w[q][part][0], w[q][part][1], w[q][part][2], w[q][part][3]};
+          if (L0 && part == 1) continue;
+          if (!L0 || part == 2)
+            *(f4_t*)(wt + part * 64 * WLD + o) = f4_t{w[q][part][0], w[q][part][1], w[q][part][2], w[q][part][3]};
           *(f4_t*)(wt + (3 + part) * 64 * WLD + o) =
               f4_t{wd[q][part][0], wd[q][part][1], wd[q][part][2], wd[q][part][3]};
         }
@@ -1171,10 +1185,14 @@ k_message_bwd_lane(MsgBwdArgs a) {
 #pragma unroll
       for (int u4 = 0; u4 < EG; u4 += 4) {
         const int o = wslot(lane, (ebase + u4) / 4);
-        const f4_t ws4 = *(const f4_t*)(wt + o), wv4 = *(const f4_t*)(wt + 64 * WLD + o);
+        f4_t ws4 = {}, wv4 = {}, dv4 = {};
+        if constexpr (!L0) {
+          ws4 = *(const f4_t*)(wt + o);
+          wv4 = *(const f4_t*)(wt + 64 * WLD + o);
+          dv4 = *(const f4_t*)(wt + 4 * 64 * WLD + o);
+        }
         const f4_t wr4 = *(const f4_t*)(wt + 2 * 64 * WLD + o);
-        const f4_t ds4 = *(const f4_t*)(wt + 3 * 64 * WLD + o), dv4 = *(const f4_t*)(wt + 4 * 64 * WLD + o);
-        const f4_t dr4 = *(const f4_t*)(wt + 5 * 64 * WLD + o);
+        const f4_t ds4 = *(const f4_t*)(wt + 3 * 64 * WLD + o), dr4 = *(const f4_t*)(wt + 5 * 64 * WLD + o);
         // per edge: [dE/dd, dE/drhat x, y, z] partial sums of this channel
         A vals[16];
 #pragma unroll
@@ -1189,16 +1207,21 @@ k_message_bwd_lane(MsgBwdArgs a) {
           const bool live = e < cnt;
           const A g_s = live ? gg[0][u] : A(0), g0 = live ? gg[1][u] : A(0);
           const A g1 = live ? gg[2][u] : A(0), g2 = live ? gg[3][u] : A(0);
-          const A Av = g0 * v0 + g1 * v1 + g2 * v2;
           const A Ar = g0 * rx + g1 * ry + g2 * rz;
-          acc_h0 += g_s * ws4[uu];
-          acc_h1 += Av * wv4[uu];
-          acc_h2 += Ar * wr4[uu];
-          const A tv = hv * wv4[uu], tr = hr * wr4[uu];
-          acc_v0 += g0 * tv;
-          acc_v1 += g1 * tv;
-          acc_v2 += g2 * tv;
-          vals[4 * uu] = g_s * hs * ds4[uu] + Av * hv * dv4[uu] + Ar * hr * dr4[uu];
+          const A tr = hr * wr4[uu];
+          if constexpr (L0) {
+            vals[4 * uu] = g_s * hs * ds4[uu] + Ar * hr * dr4[uu];
+          } else {
+            const A Av = g0 * v0 + g1 * v1 + g2 * v2;
+            acc_h0 += g_s * ws4[uu];
+            acc_h1 += Av * wv4[uu];
+            acc_h2 += Ar * wr4[uu];
+            const A tv = hv * wv4[uu];
+            acc_v0 += g0 * tv;
+            acc_v1 += g1 * tv;
+            acc_v2 += g2 * tv;
+            vals[4 * uu] = g_s * hs * ds4[uu] + Av * hv * dv4[uu] + Ar * hr * dr4[uu];
+          }
           vals[4 * uu + 1] = g0 * tr;
           vals[4 * uu + 2] = g1 * tr;
           vals[4 * uu + 3] = g2 * tr;
@@ -1300,7 +1323,8 @@ void launch_message_bwd_kbm(hipStream_t st, const MsgBwdArgs& ma) {
   if constexpr (sizeof(typename P::T) == 4) {
     constexpr int NWB = mbl_nw<F>(), SLICES = F / 64 / NWB;
     const int blocks = (int)(((long long)(ma.N + MB_RB2 - 1) / MB_RB2 * SLICES + 7) / 8 * 8);
-    k_message_bwd_lane<P, F, KBM><<<blocks, 64 * NWB, 0, st>>>(ma);
+    if (ma.first) k_message_bwd_lane<P, F, KBM, true><<<blocks, 64 * NWB, 0, st>>>(ma);
+    else k_message_bwd_lane<P, F, KBM, false><<<blocks, 64 * NWB, 0, st>>>(ma);
   } else {
     constexpr int NWB = mb_nwb<P, F, KBM>(), SLICES = F / 16 / mb_ftw<P, F, KBM>() / NWB;
     const int blocks = (int)(((long long)(ma.N + MB_RB - 1) / MB_RB * SLICES + 7) / 8 * 8);
@@ -1471,6 +1495,7 @@ hipError_t backward_impl(hipStream_t st, BackwardArgs& ba) {
     ma.gh = ba.gh;
     ma.gv_out = ba.gv;
     ma.eg = ba.eg;
+    ma.first = l == 0;
     prof_mark(ba.prof, st, KC_BWD_MESSAGE, true);
     e = launch_message_bwd<P, F>(st, ma, kcols / P::KC);
     prof_mark(ba.prof, st, KC_BWD_MESSAGE, false);
