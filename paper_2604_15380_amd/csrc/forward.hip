@@ -15,7 +15,8 @@
 namespace {
 
 // ---------------------------------------------------------------- embed ----
-// s = emb[species], v = 0 and, when h is given, layer 0's h = h0[species]
+// s = emb[species], v = 0 (when v is given) and, when h is given, layer 0's
+// h = h0[species]
 // (the species' row of the phi table: phi acts on each row by itself, so
 // the row is what phi gives for the atom's own s).
 template <class P>
@@ -30,9 +31,11 @@ __global__ void __launch_bounds__(256) k_embed(int N, int F, const int32_t* __re
     const size_t i = x / F, f = x % F;
     const size_t z = (size_t)species[i];
     s[x] = emb[z * F + f];
-    v[3 * i * F + f] = P::st(0);
-    v[3 * i * F + F + f] = P::st(0);
-    v[3 * i * F + 2 * F + f] = P::st(0);
+    if (v) {
+      v[3 * i * F + f] = P::st(0);
+      v[3 * i * F + F + f] = P::st(0);
+      v[3 * i * F + 2 * F + f] = P::st(0);
+    }
     if (h) {
       h[3 * i * F + f] = h0[3 * z * F + f];
       h[3 * i * F + F + f] = h0[3 * z * F + F + f];
@@ -270,9 +273,10 @@ __global__ void __launch_bounds__(NW * 64) k_message(MsgArgs a) {
     for (int q = 0; q < FTW; ++q) {
       const int f = (wave + NW * q) * 16 + (lane & 15);
       s_old[q] = sin[(size_t)i * F + f];
-      v_old[q][0] = vin[ib + f];
-      v_old[q][1] = vin[ib + F + f];
-      v_old[q][2] = vin[ib + 2 * F + f];
+      // (the first layer's v is zero and need not be stored)
+      v_old[q][0] = V0 ? P::st(0) : vin[ib + f];
+      v_old[q][1] = V0 ? P::st(0) : vin[ib + F + f];
+      v_old[q][2] = V0 ? P::st(0) : vin[ib + 2 * F + f];
     }
     A acc_s[FTW], acc_v[FTW][3];
 #pragma unroll
@@ -958,9 +962,9 @@ k_message_lane(MsgArgs a) {
     if (rp(i) == rp(i + 1)) {
       const size_t ib = (size_t)i * 3 * F;
       s[(size_t)i * F + c] = sin[(size_t)i * F + c];
-      vout[ib + c] = vin[ib + c];
-      vout[ib + F + c] = vin[ib + F + c];
-      vout[ib + 2 * F + c] = vin[ib + 2 * F + c];
+      vout[ib + c] = V0 ? P::st(0) : vin[ib + c];
+      vout[ib + F + c] = V0 ? P::st(0) : vin[ib + F + c];
+      vout[ib + 2 * F + c] = V0 ? P::st(0) : vin[ib + 2 * F + c];
     }
   auto first_with_edges = [&](int i) {
     while (i < i1 && rp(i) == rp(i + 1)) ++i;
@@ -995,7 +999,9 @@ k_message_lane(MsgArgs a) {
   int eb = rp(i + 1);
   size_t ib = (size_t)i * 3 * F;
   T s_old = sin[(size_t)i * F + c];
-  T v_old0 = vin[ib + c], v_old1 = vin[ib + F + c], v_old2 = vin[ib + 2 * F + c];
+  // (the first layer's v is zero and need not be stored)
+  T v_old0 = V0 ? P::st(0) : vin[ib + c], v_old1 = V0 ? P::st(0) : vin[ib + F + c];
+  T v_old2 = V0 ? P::st(0) : vin[ib + 2 * F + c];
   A acc_s = 0, acc_v0 = 0, acc_v1 = 0, acc_v2 = 0;
   auto write_out = [&] {
     s[(size_t)i * F + c] = P::st(P::ld(s_old) + acc_s);
@@ -1012,9 +1018,11 @@ k_message_lane(MsgArgs a) {
     eb = rp(i + 1);
     ib = (size_t)i * 3 * F;
     s_old = sin[(size_t)i * F + c];
-    v_old0 = vin[ib + c];
-    v_old1 = vin[ib + F + c];
-    v_old2 = vin[ib + 2 * F + c];
+    if constexpr (!V0) {
+      v_old0 = vin[ib + c];
+      v_old1 = vin[ib + F + c];
+      v_old2 = vin[ib + 2 * F + c];
+    }
   };
   while (true) {
     const int cnt = min(16, E1 - c0);
@@ -1467,8 +1475,11 @@ hipError_t forward_impl(hipStream_t st, ForwardArgs& fa) {
   if (N > 0) {
     // embedding, and layer 0's phi from the per-species table
     prof_mark(fa.prof, st, KC_EMBED, true);
+    // v = 0 is stored only where something reads it (the saved copy for the
+    // reverse pass, or an export): the first message takes it as zero
     k_embed<P><<<grid_for((size_t)N * F, 256), 256, 0, st>>>(N, F, g->species, (const T*)pm->emb,
-                                                           (const T*)pm->h0, s, v[0],
+                                                           (const T*)pm->h0, s,
+                                                           fa.save || fa.s_out ? v[0] : nullptr,
                                                            fa.stop_layer >= 0 ? h : nullptr);
     prof_mark(fa.prof, st, KC_EMBED, false);
   }
