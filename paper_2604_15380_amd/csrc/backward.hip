@@ -520,22 +520,61 @@ __global__ void __launch_bounds__((64 * ub_nw<P, F>())) k_update_bwd(UpdBwdArgs 
   __syncthreads();
   // per component: [g_U | g_V] into R1, then [U^T | V^T] [g_U ; g_V]
   A* gv_out = (A*)a.gv_out;
-  for (int c = 0; c < 3; ++c) {
-    for (int x = threadIdx.x; x < TM * F; x += blockDim.x) {
-      const int r = x / F, f = x % F;
-      A gU = 0, gV = 0;
-      if (row0 + r < (size_t)N) {
+  // the component-independent factors of a thread's elements (the same
+  // elements in every component pass) are formed once, in registers, where
+  // they fit: g_s a_sv, a_vv, |V| and dE/d|V|
+  constexpr int NT = 64 * ub_nw<P, F>(), EPT = (TM * F + NT - 1) / NT;
+  constexpr bool PRE = EPT * (int)sizeof(A) <= (NT < 1024 ? 32 : 16);   // 1024 threads leave 128 VGPRs
+  A gsa_r[PRE ? EPT : 1], avv_r[PRE ? EPT : 1], nv_r[PRE ? EPT : 1], sc_r[PRE ? EPT : 1];
+  if constexpr (PRE) {
+#pragma unroll
+    for (int e = 0; e < EPT; ++e) {
+      const int x = threadIdx.x + e * NT, r = x / F, f = x % F;
+      gsa_r[e] = avv_r[e] = nv_r[e] = sc_r[e] = 0;
+      if (x < TM * F && row0 + r < (size_t)N) {
         const size_t i = row0 + r;
-        const A u = U(i, c, f), w = V(i, c, f);
         const A v0 = V(i, 0, f), v1 = V(i, 1, f), v2 = V(i, 2, f);
-        const A nv = sqrt(v0 * v0 + v1 * v1 + v2 * v2);
-        const A g_s = gs[i * F + f], gvc = gv[i * 3 * F + c * F + f];
-        const A avv = P::ld(ag[i * 2 * F + f]), asv = P::ld(ag[i * 2 * F + F + f]);
-        gU = gvc * avv + g_s * asv * w;
-        gV = g_s * asv * u + (nv > A(0) ? scr[i * sw + f] * w / nv : A(0));
+        nv_r[e] = sqrt(v0 * v0 + v1 * v1 + v2 * v2);
+        gsa_r[e] = gs[i * F + f] * P::ld(ag[i * 2 * F + F + f]);
+        avv_r[e] = P::ld(ag[i * 2 * F + f]);
+        sc_r[e] = scr[i * sw + f];
       }
-      R1[r * LD1 + f] = P::st(gU);
-      R1[r * LD1 + F + f] = P::st(gV);
+    }
+  }
+  for (int c = 0; c < 3; ++c) {
+    if constexpr (PRE) {
+#pragma unroll
+      for (int e = 0; e < EPT; ++e) {
+        const int x = threadIdx.x + e * NT, r = x / F, f = x % F;
+        if (x >= TM * F) break;
+        A gU = 0, gV = 0;
+        if (row0 + r < (size_t)N) {
+          const size_t i = row0 + r;
+          const A u = U(i, c, f), w = V(i, c, f);
+          const A gvc = gv[i * 3 * F + c * F + f];
+          gU = gvc * avv_r[e] + gsa_r[e] * w;
+          gV = gsa_r[e] * u + (nv_r[e] > A(0) ? sc_r[e] * w / nv_r[e] : A(0));
+        }
+        R1[r * LD1 + f] = P::st(gU);
+        R1[r * LD1 + F + f] = P::st(gV);
+      }
+    } else {
+      for (int x = threadIdx.x; x < TM * F; x += blockDim.x) {
+        const int r = x / F, f = x % F;
+        A gU = 0, gV = 0;
+        if (row0 + r < (size_t)N) {
+          const size_t i = row0 + r;
+          const A u = U(i, c, f), w = V(i, c, f);
+          const A v0 = V(i, 0, f), v1 = V(i, 1, f), v2 = V(i, 2, f);
+          const A nv = sqrt(v0 * v0 + v1 * v1 + v2 * v2);
+          const A g_s = gs[i * F + f], gvc = gv[i * 3 * F + c * F + f];
+          const A avv = P::ld(ag[i * 2 * F + f]), asv = P::ld(ag[i * 2 * F + F + f]);
+          gU = gvc * avv + g_s * asv * w;
+          gV = g_s * asv * u + (nv > A(0) ? scr[i * sw + f] * w / nv : A(0));
+        }
+        R1[r * LD1 + f] = P::st(gU);
+        R1[r * LD1 + F + f] = P::st(gV);
+      }
     }
     __syncthreads();
     dense_tiles<P, 1, ub_nw<P, F>(), 2 * F>(R1, LD1, a.uvT, [&](int ct, C* acc) {
