@@ -33,6 +33,12 @@ struct StructInfo {     // per structure: atom range and periodic image range
   int32_t lo, n;
   int32_t m0, m1, m2;   // |n_k| <= m_k
   int32_t nimg;         // (2 m0 + 1)(2 m1 + 1)(2 m2 + 1)
+  // periodic structures: fractional coordinate k of x is x . fr[3k..3k+2];
+  // the atoms' fractional range [fmin_k, fmax_k] and r_c / w_k (w_k the
+  // cell's width normal to the other two cell vectors), which bound the
+  // image shifts one receiver can need
+  double fr[9];
+  double fmin[3], fmax[3], rw[3];
 };
 
 // Cell-list binning of one structure (nb[0] == 0: every pair is tested).

@@ -62,7 +62,8 @@ __global__ void __launch_bounds__(256) k_prep(int B, int N, const int32_t* __res
   if (bad) {
     if (lane == 0) {
       atomicOr(&st->err, ERR_STRUCT_PTR);
-      StructInfo si{0, 0, 0, 0, 0, 1};
+      StructInfo si{};
+      si.nimg = 1;
       g.sinfo[b] = si;
       g.grid[b] = cg;
     }
@@ -117,6 +118,7 @@ __global__ void __launch_bounds__(256) k_prep(int B, int N, const int32_t* __res
   const double bin_w = cutoff * (1.0 + CELL_MARGIN);
   const long long bin_cap = 2LL * n + 27;
   int m[3] = {0, 0, 0};
+  double frs[9] = {0, 0, 0, 0, 0, 0, 0, 0, 0}, fmn[3] = {0, 0, 0}, fmx[3] = {0, 0, 0}, rwv[3] = {0, 0, 0};
   if (periodic) {
     // reciprocal rows: f_k = x . (a_{k+1} x a_{k+2}) / det
     double cr[9];
@@ -161,6 +163,13 @@ __global__ void __launch_bounds__(256) k_prep(int B, int N, const int32_t* __res
       m[k] = (int)floor(x);
       nimg *= 2 * m[k] + 1;
     }
+    if (ok)
+      for (int k = 0; k < 3; ++k) {
+        for (int c = 0; c < 3; ++c) frs[3 * k + c] = cr[3 * k + c] / det;
+        fmn[k] = hi > lo ? fmin[k] : 0.0;
+        fmx[k] = hi > lo ? fmax[k] : 0.0;
+        rwv[k] = cutoff / w[k];
+      }
     if (!ok) {
       if (lane == 0 && !(isfinite(det) && det != 0.0)) atomicOr(&st->err, ERR_CELL);
       m[0] = m[1] = m[2] = 0;
@@ -214,6 +223,12 @@ __global__ void __launch_bounds__(256) k_prep(int B, int N, const int32_t* __res
     si.m1 = m[1];
     si.m2 = m[2];
     si.nimg = (2 * m[0] + 1) * (2 * m[1] + 1) * (2 * m[2] + 1);
+    for (int k = 0; k < 9; ++k) si.fr[k] = frs[k];
+    for (int k = 0; k < 3; ++k) {
+      si.fmin[k] = fmn[k];
+      si.fmax[k] = fmx[k];
+      si.rw[k] = rwv[k];
+    }
     g.sinfo[b] = si;
     for (int k = 0; k < 9; ++k) g.cell[9 * b + k] = A[k];
     cg.base = 2 * lo + 27 * b;
@@ -231,26 +246,58 @@ __global__ void k_status_init(DevStatus* st) {
   st->n_edges_cap = 0;
 }
 
+// The image shifts receiver i can need: along a periodic axis k, a pair at
+// shift n_k is at least |f_j - f_i + n_k| w_k apart, so only n_k with
+// f_i - fmax_k - r_c / w_k < n_k < f_i - fmin_k + r_c / w_k can hold a
+// neighbour (widened by 1e-6; n_k = 0 always qualifies).  The box keeps the
+// shifts' order, so the rows come out as with the full image range.
+struct ImageBox {
+  int lo[3], s1, s2, nimg;
+};
+
+__device__ inline ImageBox image_box(const StructInfo& si, double xi, double yi, double zi) {
+#pragma clang fp contract(off)
+  const int m[3] = {si.m0, si.m1, si.m2};
+  int lo[3], hi[3];
+  for (int k = 0; k < 3; ++k) {
+    lo[k] = hi[k] = 0;
+    if (m[k] == 0) continue;
+    const double f = (xi * si.fr[3 * k] + yi * si.fr[3 * k + 1]) + zi * si.fr[3 * k + 2];
+    const double a = f - si.fmax[k] - si.rw[k] - 1e-6, b = f - si.fmin[k] + si.rw[k] + 1e-6;
+    lo[k] = a > (double)-m[k] ? min(0, (int)ceil(a)) : -m[k];
+    hi[k] = b < (double)m[k] ? max(0, (int)floor(b)) : m[k];
+  }
+  ImageBox ib;
+  ib.lo[0] = lo[0];
+  ib.lo[1] = lo[1];
+  ib.lo[2] = lo[2];
+  ib.s1 = hi[1] - lo[1] + 1;
+  ib.s2 = hi[2] - lo[2] + 1;
+  ib.nimg = (hi[0] - lo[0] + 1) * ib.s1 * ib.s2;
+  return ib;
+}
+
 // The candidate test shared by the count and fill passes.  Candidate index t
-// enumerates (j, image) with j = lo + t / nimg and image = t % nimg.
+// enumerates (j, image) with j = lo + t / nimg and image = t % nimg over the
+// receiver's image box.
 struct Candidate {
   bool hit, zero;
   int j, packed;
 };
 
-__device__ inline Candidate test_candidate(int t, int total, int i, const StructInfo& si,
+__device__ inline Candidate test_candidate(int t, int total, int i, const StructInfo& si, const ImageBox& ib,
                                            const double* __restrict__ P, const double* A,
                                            double xi, double yi, double zi, double rc2) {
 #pragma clang fp contract(off)
   Candidate c{false, false, 0, 0};
   if (t >= total) return c;
-  const int s1 = 2 * si.m1 + 1, s2 = 2 * si.m2 + 1;
-  const int jl = t / si.nimg;
-  const int img = t - jl * si.nimg;
-  const int n0 = img / (s1 * s2) - si.m0;
+  const int s1 = ib.s1, s2 = ib.s2;
+  const int jl = t / ib.nimg;
+  const int img = t - jl * ib.nimg;
+  const int n0 = img / (s1 * s2) + ib.lo[0];
   const int rem = img % (s1 * s2);
-  const int n1 = rem / s2 - si.m1;
-  const int n2 = rem % s2 - si.m2;
+  const int n1 = rem / s2 + ib.lo[1];
+  const int n2 = rem % s2 + ib.lo[2];
   const int j = si.lo + jl;
   const double f0 = (double)n0, f1 = (double)n1, f2 = (double)n2;
   const double tx = (f0 * A[0] + f1 * A[3]) + f2 * A[6];
@@ -421,12 +468,13 @@ __global__ void __launch_bounds__(256) k_edges(painn_graph g, double rc2) {
     }
     return;
   }
-  const int total = si.n * si.nimg;
+  const ImageBox ib = image_box(si, xi, yi, zi);
+  const int total = si.n * ib.nimg;
   int out = out0;
   int cnt = 0;
   bool zero = false;
   for (int t0 = 0; t0 < total; t0 += WAVE) {
-    Candidate c = test_candidate(t0 + lane, total, i, si, g.pos, A, xi, yi, zi, rc2);
+    Candidate c = test_candidate(t0 + lane, total, i, si, ib, g.pos, A, xi, yi, zi, rc2);
     unsigned long long mask = ballot(c.hit);
     if (FILL) {
       if (c.hit) {
