@@ -16,30 +16,40 @@ namespace {
 
 // ---------------------------------------------------------------- embed ----
 // s = emb[species], v = 0 (when v is given) and, when h is given, layer 0's
-// h = h0[species]
-// (the species' row of the phi table: phi acts on each row by itself, so
-// the row is what phi gives for the atom's own s).
-template <class P>
-__global__ void __launch_bounds__(256) k_embed(int N, int F, const int32_t* __restrict__ species,
+// h = h0[species] (the species' row of the phi table: phi acts on each row
+// by itself, so the row is what phi gives for the atom's own s).  Each
+// thread moves 4 consecutive elements of a row (F is a multiple of 64).
+template <class T>
+struct alignas(4 * sizeof(T)) Quad {
+  T x[4];
+};
+
+template <class P, int F>
+__global__ void __launch_bounds__(256) k_embed(int N, const int32_t* __restrict__ species,
                                               const typename P::T* __restrict__ emb,
                                               const typename P::T* __restrict__ h0,
                                               typename P::T* __restrict__ s,
                                               typename P::T* __restrict__ v,
                                               typename P::T* __restrict__ h) {
-  const size_t tot = (size_t)N * F;
+  using T = typename P::T;
+  using Q = Quad<T>;
+  constexpr int F4 = F / 4;
+  const size_t tot = (size_t)N * F4;
+  Q zero;
+  for (int k = 0; k < 4; ++k) zero.x[k] = P::st(0);
   for (size_t x = blockIdx.x * (size_t)blockDim.x + threadIdx.x; x < tot; x += (size_t)gridDim.x * blockDim.x) {
-    const size_t i = x / F, f = x % F;
+    const size_t i = x / F4, f = (x % F4) * 4;
     const size_t z = (size_t)species[i];
-    s[x] = emb[z * F + f];
+    *(Q*)(s + i * F + f) = *(const Q*)(emb + z * F + f);
     if (v) {
-      v[3 * i * F + f] = P::st(0);
-      v[3 * i * F + F + f] = P::st(0);
-      v[3 * i * F + 2 * F + f] = P::st(0);
+      *(Q*)(v + 3 * i * F + f) = zero;
+      *(Q*)(v + 3 * i * F + F + f) = zero;
+      *(Q*)(v + 3 * i * F + 2 * F + f) = zero;
     }
     if (h) {
-      h[3 * i * F + f] = h0[3 * z * F + f];
-      h[3 * i * F + F + f] = h0[3 * z * F + F + f];
-      h[3 * i * F + 2 * F + f] = h0[3 * z * F + 2 * F + f];
+      *(Q*)(h + 3 * i * F + f) = *(const Q*)(h0 + 3 * z * F + f);
+      *(Q*)(h + 3 * i * F + F + f) = *(const Q*)(h0 + 3 * z * F + F + f);
+      *(Q*)(h + 3 * i * F + 2 * F + f) = *(const Q*)(h0 + 3 * z * F + 2 * F + f);
     }
   }
 }
@@ -1477,7 +1487,7 @@ hipError_t forward_impl(hipStream_t st, ForwardArgs& fa) {
     prof_mark(fa.prof, st, KC_EMBED, true);
     // v = 0 is stored only where something reads it (the saved copy for the
     // reverse pass, or an export): the first message takes it as zero
-    k_embed<P><<<grid_for((size_t)N * F, 256), 256, 0, st>>>(N, F, g->species, (const T*)pm->emb,
+    k_embed<P, F><<<grid_for((size_t)N * F / 4, 256), 256, 0, st>>>(N, g->species, (const T*)pm->emb,
                                                            (const T*)pm->h0, s,
                                                            fa.save || fa.s_out ? v[0] : nullptr,
                                                            fa.stop_layer >= 0 ? h : nullptr);
