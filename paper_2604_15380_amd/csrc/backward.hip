@@ -981,10 +981,11 @@ k_message_bwd(MsgBwdArgs a) {
   }
 }
 
-// Channel-per-lane form of the reverse message (FP32).  A workgroup of MBL_NW
-// waves owns MB_RB2 consecutive senders and a 64 MBL_NW-channel slice of the
-// features (wide layers take several slices in consecutive workgroups); each
-// wave owns 64 channels and keeps their filter B fragments in registers.
+// Channel-per-lane form of the reverse message (FP32).  A workgroup of
+// mbl_nw<F>() waves owns MB_RB2 consecutive senders and a slice of
+// 64 mbl_nw<F>() channels (wide layers take several slices in consecutive
+// workgroups); each wave owns 64 channels and keeps their filter B fragments
+// in registers.
 // The block's sender-ordered edges (its senders' rows back to back) stream in
 // 16-edge chunks that may span senders.  Per chunk the wave forms the filter
 // w and its d-derivative w' on the matrix cores (the same B fragments against
