@@ -524,7 +524,7 @@ __global__ void __launch_bounds__((64 * ub_nw<P, F>())) k_update_bwd(UpdBwdArgs 
   // elements in every component pass) are formed once, in registers, where
   // they fit: g_s a_sv, a_vv, |V| and dE/d|V|
   constexpr int NT = 64 * ub_nw<P, F>(), EPT = (TM * F + NT - 1) / NT;
-  constexpr bool PRE = EPT * (int)sizeof(A) <= (NT < 1024 ? 32 : 16);   // 1024 threads leave 128 VGPRs
+  constexpr bool PRE = EPT * (int)sizeof(A) <= (NT < 1024 ? 32 : 24);   // 1024 threads leave 128 VGPRs
   A gsa_r[PRE ? EPT : 1], avv_r[PRE ? EPT : 1], nv_r[PRE ? EPT : 1], sc_r[PRE ? EPT : 1];
   if constexpr (PRE) {
 #pragma unroll
