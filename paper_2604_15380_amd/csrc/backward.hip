@@ -735,7 +735,10 @@ constexpr int mb_nwb() {
   return nw <= 8 ? nw : (nw % 8 == 0 ? 8 : 6);
 }
 
-template <class P, int F, int KBM>
+// L0: the first layer, where v = 0 and only the per-edge sums are wanted
+// (as in the channel-per-lane form below): w^r, w'^s and w'^r only, no g_h,
+// g_v.
+template <class P, int F, int KBM, bool L0>
 __global__ void __launch_bounds__((64 * mb_nwb<P, F, KBM>())) __attribute__((amdgpu_waves_per_eu(mb_wpe<P, F, KBM>())))
 k_message_bwd(MsgBwdArgs a) {
   using T = typename P::T;
@@ -772,7 +775,7 @@ k_message_bwd(MsgBwdArgs a) {
   A* gv_out = (A*)a.gv_out;
   A* eg = (A*)a.eg;
   // senders without incoming edges: g_h = 0, g_v = g_v'
-  for (int j = j0; j < j1; ++j)
+  for (int j = j0; j < j1 && !L0; ++j)
     if (tp(j) == tp(j + 1) && lane < 16) {
       const size_t jb = (size_t)j * 3 * F;
 #pragma unroll
@@ -899,17 +902,20 @@ k_message_bwd(MsgBwdArgs a) {
 #pragma unroll
       for (int part = 0; part < 3; ++part) {
         for (int r = 0; r < 4; ++r) w[part][r] = wd[part][r] = 0;
+        if (L0 && part == 1) continue;
 #pragma unroll
         for (int kb = 0; kb < KBM; ++kb) {
           const int ct = part * NFT + FTW * wave + q;
           const Fr bw = P::frag(Wc + ((size_t)(ct * KBM + kb) * 64 + lane) * P::KPL);
-          w[part] = P::mfma(Ga[kb], bw, w[part]);
+          if (!L0 || part == 2) w[part] = P::mfma(Ga[kb], bw, w[part]);
           wd[part] = P::mfma(Gd[kb], bw, wd[part]);
         }
       }
       const int ch = (FTW * wave + q) * 16 + (lane & 15);
-      const A hs = P::ld(h[jb + ch]), hv = P::ld(h[jb + F + ch]), hr = P::ld(h[jb + 2 * F + ch]);
-      const A v0 = P::ld(vv[jb + ch]), v1 = P::ld(vv[jb + F + ch]), v2 = P::ld(vv[jb + 2 * F + ch]);
+      const A hs = P::ld(h[jb + ch]), hr = P::ld(h[jb + 2 * F + ch]);
+      const A hv = L0 ? A(0) : P::ld(h[jb + F + ch]);
+      const A v0 = L0 ? A(0) : P::ld(vv[jb + ch]), v1 = L0 ? A(0) : P::ld(vv[jb + F + ch]);
+      const A v2 = L0 ? A(0) : P::ld(vv[jb + 2 * F + ch]);
 #pragma unroll
       for (int i = 0; i < 4; ++i) {
         // rows past the chunk add exactly nothing (not 0 x receiver 0's
@@ -917,16 +923,21 @@ k_message_bwd(MsgBwdArgs a) {
         const bool live = er[i] >= 0;
         const A g_s = live ? gsr[q][i] : A(0), g0 = live ? gvr[q][i][0] : A(0);
         const A g1 = live ? gvr[q][i][1] : A(0), g2 = live ? gvr[q][i][2] : A(0);
-        const A Av = g0 * v0 + g1 * v1 + g2 * v2;
         const A Ar = g0 * rh[i][0] + g1 * rh[i][1] + g2 * rh[i][2];
-        acc_h[q][0] += g_s * w[0][i];
-        acc_h[q][1] += Av * w[1][i];
-        acc_h[q][2] += Ar * w[2][i];
-        const A tv = hv * w[1][i], tr = hr * w[2][i];
-        acc_v[q][0] += g0 * tv;
-        acc_v[q][1] += g1 * tv;
-        acc_v[q][2] += g2 * tv;
-        vals[i] += g_s * hs * wd[0][i] + Av * hv * wd[1][i] + Ar * hr * wd[2][i];
+        const A tr = hr * w[2][i];
+        if constexpr (L0) {
+          vals[i] += g_s * hs * wd[0][i] + Ar * hr * wd[2][i];
+        } else {
+          const A Av = g0 * v0 + g1 * v1 + g2 * v2;
+          acc_h[q][0] += g_s * w[0][i];
+          acc_h[q][1] += Av * w[1][i];
+          acc_h[q][2] += Ar * w[2][i];
+          const A tv = hv * w[1][i];
+          acc_v[q][0] += g0 * tv;
+          acc_v[q][1] += g1 * tv;
+          acc_v[q][2] += g2 * tv;
+          vals[i] += g_s * hs * wd[0][i] + Av * hv * wd[1][i] + Ar * hr * wd[2][i];
+        }
         vals[4 + i] += g0 * tr;
         vals[8 + i] += g1 * tr;
         vals[12 + i] += g2 * tr;
@@ -942,7 +953,7 @@ k_message_bwd(MsgBwdArgs a) {
       if (e >= 0) unsafeAtomicAdd(eg + ((size_t)e * NW + wave) * 4 + (k >> 2), vals[0]);
     }
     if (!PF) find_next();
-    if (last) {
+    if (last && !L0) {
       // the sender's sums over the wave's 4 row groups; lanes < 16 write
 #pragma unroll
       for (int q = 0; q < FTW; ++q)
@@ -1368,7 +1379,8 @@ void launch_message_bwd_kbm(hipStream_t st, const MsgBwdArgs& ma) {
   } else {
     constexpr int NWB = mb_nwb<P, F, KBM>(), SLICES = F / 16 / mb_ftw<P, F, KBM>() / NWB;
     const int blocks = (int)(((long long)(ma.N + MB_RB - 1) / MB_RB * SLICES + 7) / 8 * 8);
-    k_message_bwd<P, F, KBM><<<blocks, 64 * NWB, 0, st>>>(ma);
+    if (ma.first) k_message_bwd<P, F, KBM, true><<<blocks, 64 * NWB, 0, st>>>(ma);
+    else k_message_bwd<P, F, KBM, false><<<blocks, 64 * NWB, 0, st>>>(ma);
   }
 }
 
