@@ -24,6 +24,32 @@ struct alignas(4 * sizeof(T)) Quad {
   T x[4];
 };
 
+// TM rows of F elements, row r from src + (row0 + r) * sstride, into LDS at
+// dst (row stride ld); rows past N are zero.  4-element copies where the LDS
+// rows keep their alignment.
+template <class P, int F, int TM>
+__device__ __forceinline__ void stage_rows(typename P::T* dst, int ld, const typename P::T* src, size_t sstride,
+                                           size_t row0, int N) {
+  using T = typename P::T;
+  if (ld % 4 == 0) {
+    using Q = Quad<T>;
+    for (int x = threadIdx.x; x < TM * F / 4; x += blockDim.x) {
+      const int r = x / (F / 4), c = (x % (F / 4)) * 4;
+      T* d = dst + r * ld + c;
+      if (row0 + r < (size_t)N) {
+        *(Q*)d = *(const Q*)(src + (row0 + r) * sstride + c);
+      } else {
+        d[0] = d[1] = d[2] = d[3] = P::st(0);
+      }
+    }
+  } else {
+    for (int x = threadIdx.x; x < TM * F; x += blockDim.x) {
+      const int r = x / F, c = x % F;
+      dst[r * ld + c] = row0 + r < (size_t)N ? src[(row0 + r) * sstride + c] : P::st(0);
+    }
+  }
+}
+
 template <class P, int F>
 __global__ void __launch_bounds__(256) k_embed(int N, const int32_t* __restrict__ species,
                                               const typename P::T* __restrict__ emb,
@@ -429,10 +455,7 @@ k_update(UpdArgs a) {
   // element by element
   T* s_out = SAVE ? (T*)a.s_out : (T*)a.s;
   T* v_out = SAVE ? (T*)a.v_out : (T*)a.v;
-  for (int x = threadIdx.x; x < TM * F; x += blockDim.x) {
-    const int r = x / F, c = x % F;
-    SN[r * LD2 + c] = row0 + r < (size_t)N ? s[(row0 + r) * F + c] : P::st(0);
-  }
+  stage_rows<P, F, TM>(SN, LD2, s, F, row0, N);
   C U[FTW][3][RT], nsq[FTW][RT], pd[FTW][RT];
   for (int q = 0; q < FTW; ++q)
     for (int r = 0; r < RT; ++r)
@@ -443,10 +466,7 @@ k_update(UpdArgs a) {
   const T* Wuv = (const T*)a.uv.w;
   for (int c = 0; c < 3; ++c) {
     __syncthreads();
-    for (int x = threadIdx.x; x < TM * F; x += blockDim.x) {
-      const int r = x / F, col = x % F;
-      VS[r * LD1 + col] = row0 + r < (size_t)N ? v[(row0 + r) * 3 * F + c * F + col] : P::st(0);
-    }
+    stage_rows<P, F, TM>(VS, LD1, v + c * F, 3 * F, row0, N);
     __syncthreads();
     const T* xp = VS + (lane & 15) * LD1 + (lane >> 4) * D::KPL;
 #pragma unroll
