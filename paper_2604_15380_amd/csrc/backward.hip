@@ -600,7 +600,7 @@ struct PhiBwdArgs {
   const void* gh;      // [N][3F]
   const void* gs_mid;  // [N][F]
   void* gs_out;
-  void* scratch;
+  void* scratch;       // per-atom rows of sw elements (FP64 at F = 384 only)
   int sw;
   void* xbuf;          // GX: as for the update
   DenseDev phi1, phi1T, phi2T;
@@ -618,34 +618,48 @@ __global__ void __launch_bounds__((64 * ub_nw<P, F>())) k_phi_bwd(PhiBwdArgs a) 
   const int lane = threadIdx.x & 63;
   const size_t row0 = (size_t)blockIdx.x * TM;
   const int N = a.N;
-  const T* s = (const T*)a.s;
-  const A* gh = (const A*)a.gh;
-  A* scr = (A*)a.scratch;
-  for (int x = threadIdx.x; x < TM * F; x += blockDim.x) {
-    const int r = x / F, f = x % F;
-    R2[r * LD2 + f] = row0 + r < (size_t)N ? s[(row0 + r) * F + f] : P::st(0);
-  }
-  for (int x = threadIdx.x; x < TM * 3 * F; x += blockDim.x) {
-    const int r = x / (3 * F), f = x % (3 * F);
-    R1[r * LD1 + f] = P::st(row0 + r < (size_t)N ? gh[(row0 + r) * 3 * F + f] : A(0));
-  }
+  stage_rows<P, F, TM>(R2, LD2, (const T*)a.s, F, row0, N);
+  stage_rows<P, 3 * F, TM>(R1, LD1, (const A*)a.gh, 3 * F, row0, N);
   __syncthreads();
-  dense_tiles<P, 1, ub_nw<P, F>(), F>(R2, LD2, a.phi1, [&](int ct, C* acc) {
-    const int col = ct * 16 + (lane & 15);
+  // silu'(W1 s + b1) stays in the registers of the lane that formed it (both
+  // F-wide layers hand feature tile ct to wave ct % NW, call ct / NW of it)
+  // where a wave has at most two tiles; otherwise (FP64 at F = 384) it goes
+  // through the per-atom scratch rows.
+  constexpr int NW = ub_nw<P, F>(), TPW = (F / 16 + NW - 1) / NW;
+  constexpr bool REG = TPW <= 2;
+  A* scr = (A*)a.scratch;
+  A ds[REG ? TPW : 1][4];
+  dense_tiles<P, 1, NW, F>(R2, LD2, a.phi1, [&](int ct, C* acc) {
+    const int col = ct * 16 + (lane & 15), k = ct / NW;
     const A bias = ((const A*)a.phi1.b)[col];
+#pragma unroll
     for (int i = 0; i < 4; ++i) {
-      const int r = P::row(lane, i);
-      if (row0 + r < (size_t)N) scr[(row0 + r) * a.sw + col] = dsilu<A>(acc[0][i] + bias);
+      const A d = dsilu<A>(acc[0][i] + bias);
+      if constexpr (REG) {
+#pragma unroll
+        for (int j = 0; j < TPW; ++j) ds[j][i] = j == k ? d : ds[j][i];
+      } else {
+        const int r = P::row(lane, i);
+        if (row0 + r < (size_t)N) scr[(row0 + r) * a.sw + col] = d;
+      }
     }
   });
   __syncthreads();
-  dense_tiles<P, 1, ub_nw<P, F>(), 3 * F>(R1, LD1, a.phi2T, [&](int ct, C* acc) {
-    const int col = ct * 16 + (lane & 15);
+  dense_tiles<P, 1, NW, 3 * F>(R1, LD1, a.phi2T, [&](int ct, C* acc) {
+    const int col = ct * 16 + (lane & 15), k = ct / NW;
+#pragma unroll
     for (int i = 0; i < 4; ++i) {
       const int r = P::row(lane, i);
       A g = 0;
-      if (row0 + r < (size_t)N) g = acc[0][i] * scr[(row0 + r) * a.sw + col];
-      R2[r * LD2 + col] = P::st(g);
+      if constexpr (REG) {
+        A d = ds[0][i];
+#pragma unroll
+        for (int j = 1; j < TPW; ++j) d = j == k ? ds[j][i] : d;
+        g = acc[0][i] * d;
+      } else {
+        if (row0 + r < (size_t)N) g = acc[0][i] * scr[(row0 + r) * a.sw + col];
+      }
+      R2[r * LD2 + col] = P::st(row0 + r < (size_t)N ? g : A(0));
     }
   });
   __syncthreads();

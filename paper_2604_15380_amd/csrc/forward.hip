@@ -19,37 +19,6 @@ namespace {
 // h = h0[species] (the species' row of the phi table: phi acts on each row
 // by itself, so the row is what phi gives for the atom's own s).  Each
 // thread moves 4 consecutive elements of a row (F is a multiple of 64).
-template <class T>
-struct alignas(4 * sizeof(T)) Quad {
-  T x[4];
-};
-
-// TM rows of F elements, row r from src + (row0 + r) * sstride, into LDS at
-// dst (row stride ld); rows past N are zero.  4-element copies where the LDS
-// rows keep their alignment.
-template <class P, int F, int TM>
-__device__ __forceinline__ void stage_rows(typename P::T* dst, int ld, const typename P::T* src, size_t sstride,
-                                           size_t row0, int N) {
-  using T = typename P::T;
-  if (ld % 4 == 0) {
-    using Q = Quad<T>;
-    for (int x = threadIdx.x; x < TM * F / 4; x += blockDim.x) {
-      const int r = x / (F / 4), c = (x % (F / 4)) * 4;
-      T* d = dst + r * ld + c;
-      if (row0 + r < (size_t)N) {
-        *(Q*)d = *(const Q*)(src + (row0 + r) * sstride + c);
-      } else {
-        d[0] = d[1] = d[2] = d[3] = P::st(0);
-      }
-    }
-  } else {
-    for (int x = threadIdx.x; x < TM * F; x += blockDim.x) {
-      const int r = x / F, c = x % F;
-      dst[r * ld + c] = row0 + r < (size_t)N ? src[(row0 + r) * sstride + c] : P::st(0);
-    }
-  }
-}
-
 template <class P, int F>
 __global__ void __launch_bounds__(256) k_embed(int N, const int32_t* __restrict__ species,
                                               const typename P::T* __restrict__ emb,

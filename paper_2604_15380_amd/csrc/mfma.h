@@ -22,6 +22,8 @@
 // reads.
 #pragma once
 
+#include <type_traits>
+
 #include "internal.h"
 
 typedef double d4_t __attribute__((ext_vector_type(4)));
@@ -322,5 +324,51 @@ __device__ __forceinline__ void dense_tiles(const typename Q::T* X, int ldx, con
       for (; kb < nkb; ++kb) step(kb);
     }
     epi(ct, acc);
+  }
+}
+
+// Four consecutive elements, moved as one 16-byte (FP32), 32-byte (FP64) or
+// 8-byte (BF16) access.
+template <class T>
+struct alignas(4 * sizeof(T)) Quad {
+  T x[4];
+};
+
+// TM rows of W elements, row r from src + (row0 + r) * sstride (storage or
+// accumulation type S), into LDS at dst (storage type, row stride ld); rows
+// past N are zero.  4-element copies where the LDS rows keep their alignment
+// (W, sstride and the source offsets are multiples of 4 everywhere here).
+template <class P, int W, int TM, class S>
+__device__ __forceinline__ void stage_rows(typename P::T* dst, int ld, const S* src, size_t sstride, size_t row0,
+                                           int N) {
+  using T = typename P::T;
+  constexpr bool SAME = std::is_same<S, T>::value;
+  if (ld % 4 == 0) {
+    for (int x = threadIdx.x; x < TM * W / 4; x += blockDim.x) {
+      const int r = x / (W / 4), c = (x % (W / 4)) * 4;
+      T* d = dst + r * ld + c;
+      if (row0 + r < (size_t)N) {
+        const Quad<S> q = *(const Quad<S>*)(src + (row0 + r) * sstride + c);
+        if constexpr (SAME) {
+          *(Quad<T>*)d = q;
+        } else {
+          Quad<T> o;
+          for (int e = 0; e < 4; ++e) o.x[e] = P::st(q.x[e]);
+          *(Quad<T>*)d = o;
+        }
+      } else {
+        d[0] = d[1] = d[2] = d[3] = P::st(0);
+      }
+    }
+  } else {
+    for (int x = threadIdx.x; x < TM * W; x += blockDim.x) {
+      const int r = x / W, c = x % W;
+      T val = P::st(0);
+      if (row0 + r < (size_t)N) {
+        if constexpr (SAME) val = src[(row0 + r) * sstride + c];
+        else val = P::st(src[(row0 + r) * sstride + c]);
+      }
+      dst[r * ld + c] = val;
+    }
   }
 }
