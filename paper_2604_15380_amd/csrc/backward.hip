@@ -49,9 +49,66 @@ __global__ void __launch_bounds__(256) k_t_count(long long E, const int32_t* __r
     atomicAdd(&cnt[col[e]], 1);
 }
 
-// One workgroup: exclusive scan of the N counts into t_ptr[0..N], counts
-// reset to 0 (they become the fill cursors).  Tiles of 4096 counts are read
-// and written coalesced through LDS; a carry runs from tile to tile.
+// Exclusive scan of the N counts into t_ptr[0..N] over blocks of 1024 counts
+// (block sums, a one-workgroup scan of those, then each block's own scan);
+// the counts are reset to 0 on the way (they become the fill cursors).
+__device__ __forceinline__ int t_block_scan(int x, int* sh) {
+  // inclusive scan of x over the 256 threads of the workgroup
+  sh[threadIdx.x] = x;
+  __syncthreads();
+  for (int o = 1; o < 256; o *= 2) {
+    const int y = threadIdx.x >= o ? sh[threadIdx.x - o] : 0;
+    __syncthreads();
+    sh[threadIdx.x] += y;
+    __syncthreads();
+  }
+  return sh[threadIdx.x];
+}
+
+__global__ void __launch_bounds__(256) k_t_scan_blocks(int N, const int32_t* __restrict__ cnt,
+                                                      long long* __restrict__ bsum) {
+  __shared__ int sh[256];
+  const int base = blockIdx.x * 1024 + threadIdx.x * 4;
+  int x = 0;
+  for (int k = 0; k < 4; ++k)
+    if (base + k < N) x += cnt[base + k];
+  const int incl = t_block_scan(x, sh);
+  if (threadIdx.x == 255) bsum[blockIdx.x] = incl;
+}
+
+__global__ void __launch_bounds__(256) k_t_scan_top(int nblk, long long* __restrict__ bsum, int32_t* __restrict__ ptr,
+                                                   int N) {
+  __shared__ int sh[256];
+  int carry = 0;
+  for (int c0 = 0; c0 < nblk; c0 += 256) {
+    const int k = c0 + threadIdx.x;
+    const int x = k < nblk ? (int)bsum[k] : 0;
+    const int incl = t_block_scan(x, sh);
+    if (k < nblk) bsum[k] = carry + incl - x;
+    carry += sh[255];
+    __syncthreads();
+  }
+  if (threadIdx.x == 0) ptr[N] = carry;
+}
+
+__global__ void __launch_bounds__(256) k_t_scan_apply(int N, int32_t* __restrict__ cnt,
+                                                     const long long* __restrict__ bsum, int32_t* __restrict__ ptr) {
+  __shared__ int sh[256];
+  const int base = blockIdx.x * 1024 + threadIdx.x * 4;
+  int v[4], x = 0;
+  for (int k = 0; k < 4; ++k) {
+    v[k] = base + k < N ? cnt[base + k] : 0;
+    x += v[k];
+  }
+  int run = (int)bsum[blockIdx.x] + t_block_scan(x, sh) - x;
+  for (int k = 0; k < 4; ++k)
+    if (base + k < N) {
+      ptr[base + k] = run;
+      cnt[base + k] = 0;
+      run += v[k];
+    }
+}
+
 __global__ void __launch_bounds__(1024) k_t_scan(int N, int32_t* __restrict__ cnt, int32_t* __restrict__ ptr) {
   constexpr int PER = 4, TILE = 1024 * PER;
   __shared__ int tile[TILE];
@@ -101,20 +158,42 @@ __global__ void __launch_bounds__(256) k_t_fill(long long E, const int32_t* __re
   }
 }
 
-// The fill order depends on timing: sort each sender's edge ids ascending
-// (insertion sort; in-degrees are small).
+// The fill order depends on timing: each sender's edge ids are put in
+// ascending order.  One wave per sender: a segment of up to 256 ids is held
+// in registers (4 per lane) and each id goes to its rank, the number of
+// smaller ids in the segment (the ids are distinct); a longer segment is
+// insertion-sorted by one lane.
 __global__ void __launch_bounds__(256) k_t_sort(int N, const int32_t* __restrict__ ptr, int32_t* __restrict__ t_edge) {
-  const int j = blockIdx.x * blockDim.x + threadIdx.x;
+  const int j = blockIdx.x * 4 + (threadIdx.x >> 6), lane = threadIdx.x & 63;
   if (j >= N) return;
-  const int a = ptr[j], b = ptr[j + 1];
-  for (int x = a + 1; x < b; ++x) {
-    const int key = t_edge[x];
-    int y = x - 1;
-    while (y >= a && t_edge[y] > key) {
-      t_edge[y + 1] = t_edge[y];
-      --y;
+  const int a = ptr[j], n = ptr[j + 1] - a;
+  if (n <= 1) return;
+  if (n <= 256) {
+    int key[4], rank[4] = {0, 0, 0, 0};
+#pragma unroll
+    for (int q = 0; q < 4; ++q) key[q] = lane + 64 * q < n ? t_edge[a + lane + 64 * q] : 0x7fffffff;
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+      const int m_end = min(64, n - 64 * q);
+      for (int m = 0; m < m_end; ++m) {
+        const int other = __shfl(key[q], m);
+#pragma unroll
+        for (int u = 0; u < 4; ++u) rank[u] += other < key[u];
+      }
     }
-    t_edge[y + 1] = key;
+#pragma unroll
+    for (int q = 0; q < 4; ++q)
+      if (lane + 64 * q < n) t_edge[a + rank[q]] = key[q];
+  } else if (lane == 0) {
+    for (int x = a + 1; x < a + n; ++x) {
+      const int key = t_edge[x];
+      int y = x - 1;
+      while (y >= a && t_edge[y] > key) {
+        t_edge[y + 1] = t_edge[y];
+        --y;
+      }
+      t_edge[y + 1] = key;
+    }
   }
 }
 
@@ -1618,10 +1697,15 @@ hipError_t launch_transpose(hipStream_t st, Profiler* p, painn_graph* g) {
   prof_mark(p, st, KC_TRANSPOSE, true);
   k_fill<int32_t><<<grid_of((size_t)N + 1, 256), 256, 0, st>>>((size_t)N + 1, g->t_count);
   if (E > 0) k_t_count<<<grid_of((size_t)E, 256), 256, 0, st>>>(E, g->col, g->t_count);
-  k_t_scan<<<1, 1024, 0, st>>>(N, g->t_count, g->t_ptr);
+  // the graph's scan buffer (at least (N + 1023) / 1024 + 1 entries) holds
+  // the block sums; the graph build that used it has finished on this stream
+  const int nblk = (N + 1023) / 1024;
+  if (nblk > 0) k_t_scan_blocks<<<nblk, 256, 0, st>>>(N, g->t_count, g->scan_tmp);
+  k_t_scan_top<<<1, 256, 0, st>>>(nblk, g->scan_tmp, g->t_ptr, N);
+  if (nblk > 0) k_t_scan_apply<<<nblk, 256, 0, st>>>(N, g->t_count, g->scan_tmp, g->t_ptr);
   if (E > 0) {
     k_t_fill<<<grid_of((size_t)E, 256), 256, 0, st>>>(E, g->col, g->t_ptr, g->t_count, g->t_edge);
-    k_t_sort<<<(N + 255) / 256, 256, 0, st>>>(N, g->t_ptr, g->t_edge);
+    k_t_sort<<<(N + 3) / 4, 256, 0, st>>>(N, g->t_ptr, g->t_edge);
   }
   prof_mark(p, st, KC_TRANSPOSE, false);
   return hipGetLastError();
