@@ -553,7 +553,41 @@ __global__ void __launch_bounds__((64 * ub_nw<P, F>())) k_update_bwd(UpdBwdArgs 
   const int sw = a.sw;
   auto U = [&](size_t i, int c, int f) { return P::ld(uv[(i * 3 + c) * 2 * F + f]); };
   auto V = [&](size_t i, int c, int f) { return P::ld(uv[(i * 3 + c) * 2 * F + F + f]); };
+  constexpr int NT = 64 * ub_nw<P, F>(), EPT = (TM * F + NT - 1) / NT;
+  constexpr bool PRE = EPT * (int)sizeof(A) <= (NT < 1024 ? 32 : 24);   // 1024 threads leave 128 VGPRs
+  // V4: FP32 with every thread on whole groups of 4 consecutive features:
+  // the element-wise passes move 16-byte vectors
+  constexpr bool V4 = std::is_same<T, float>::value && std::is_same<A, float>::value && PRE && LD1 % 4 == 0 &&
+                      (TM * F / 4) % NT == 0;
+  constexpr int EPQ = V4 ? TM * F / 4 / NT : 1;
+  using Q = Quad<float>;
+  auto ldq = [](const void* p) { return *(const Q*)p; };
   // g_a into R1
+  if constexpr (V4) {
+#pragma unroll
+    for (int e = 0; e < EPQ; ++e) {
+      const int x = threadIdx.x + e * NT, r = x / (F / 4), f = (x % (F / 4)) * 4;
+      Q gvv, gsv, gss;
+      for (int k = 0; k < 4; ++k) gvv.x[k] = gsv.x[k] = gss.x[k] = 0;
+      if (row0 + r < (size_t)N) {
+        const size_t i = row0 + r;
+        float pd[4] = {0, 0, 0, 0};
+        for (int c = 0; c < 3; ++c) {
+          const Q u = ldq(uv + (i * 3 + c) * 2 * F + f), w = ldq(uv + (i * 3 + c) * 2 * F + F + f);
+          const Q g = ldq(gv + i * 3 * F + c * F + f);
+          for (int k = 0; k < 4; ++k) {
+            pd[k] += u.x[k] * w.x[k];
+            gvv.x[k] += g.x[k] * u.x[k];
+          }
+        }
+        gss = ldq(gs + i * F + f);
+        for (int k = 0; k < 4; ++k) gsv.x[k] = gss.x[k] * pd[k];
+      }
+      *(Q*)&R1[r * LD1 + f] = gvv;
+      *(Q*)&R1[r * LD1 + F + f] = gsv;
+      *(Q*)&R1[r * LD1 + 2 * F + f] = gss;
+    }
+  } else
   for (int x = threadIdx.x; x < TM * F; x += blockDim.x) {
     const int r = x / F, f = x % F;
     A gvv = 0, gsv = 0, gss = 0;
@@ -602,10 +636,27 @@ __global__ void __launch_bounds__((64 * ub_nw<P, F>())) k_update_bwd(UpdBwdArgs 
   // the component-independent factors of a thread's elements (the same
   // elements in every component pass) are formed once, in registers, where
   // they fit: g_s a_sv, a_vv, |V| and dE/d|V|
-  constexpr int NT = 64 * ub_nw<P, F>(), EPT = (TM * F + NT - 1) / NT;
-  constexpr bool PRE = EPT * (int)sizeof(A) <= (NT < 1024 ? 32 : 24);   // 1024 threads leave 128 VGPRs
   A gsa_r[PRE ? EPT : 1], avv_r[PRE ? EPT : 1], nv_r[PRE ? EPT : 1], sc_r[PRE ? EPT : 1];
-  if constexpr (PRE) {
+  if constexpr (V4) {
+    // element 4e + k of the thread: feature f + k of quad e
+#pragma unroll
+    for (int e = 0; e < EPQ; ++e) {
+      const int x = threadIdx.x + e * NT, r = x / (F / 4), f = (x % (F / 4)) * 4;
+      for (int k = 0; k < 4; ++k) gsa_r[4 * e + k] = avv_r[4 * e + k] = nv_r[4 * e + k] = sc_r[4 * e + k] = 0;
+      if (row0 + r < (size_t)N) {
+        const size_t i = row0 + r;
+        const Q v0 = ldq(uv + (i * 3 + 0) * 2 * F + F + f), v1 = ldq(uv + (i * 3 + 1) * 2 * F + F + f),
+                v2 = ldq(uv + (i * 3 + 2) * 2 * F + F + f);
+        const Q g = ldq(gs + i * F + f), avv = ldq(ag + i * 2 * F + f), asv = ldq(ag + i * 2 * F + F + f);
+        for (int k = 0; k < 4; ++k) {
+          nv_r[4 * e + k] = sqrt(v0.x[k] * v0.x[k] + v1.x[k] * v1.x[k] + v2.x[k] * v2.x[k]);
+          gsa_r[4 * e + k] = g.x[k] * asv.x[k];
+          avv_r[4 * e + k] = avv.x[k];
+          sc_r[4 * e + k] = scr[i * sw + f + k];
+        }
+      }
+    }
+  } else if constexpr (PRE) {
 #pragma unroll
     for (int e = 0; e < EPT; ++e) {
       const int x = threadIdx.x + e * NT, r = x / F, f = x % F;
@@ -621,7 +672,26 @@ __global__ void __launch_bounds__((64 * ub_nw<P, F>())) k_update_bwd(UpdBwdArgs 
     }
   }
   for (int c = 0; c < 3; ++c) {
-    if constexpr (PRE) {
+    if constexpr (V4) {
+#pragma unroll
+      for (int e = 0; e < EPQ; ++e) {
+        const int x = threadIdx.x + e * NT, r = x / (F / 4), f = (x % (F / 4)) * 4;
+        Q gU, gV;
+        for (int k = 0; k < 4; ++k) gU.x[k] = gV.x[k] = 0;
+        if (row0 + r < (size_t)N) {
+          const size_t i = row0 + r;
+          const Q u = ldq(uv + (i * 3 + c) * 2 * F + f), w = ldq(uv + (i * 3 + c) * 2 * F + F + f);
+          const Q gvc = ldq(gv + i * 3 * F + c * F + f);
+          for (int k = 0; k < 4; ++k) {
+            const int q = 4 * e + k;
+            gU.x[k] = gvc.x[k] * avv_r[q] + gsa_r[q] * w.x[k];
+            gV.x[k] = gsa_r[q] * u.x[k] + (nv_r[q] > A(0) ? sc_r[q] * w.x[k] / nv_r[q] : A(0));
+          }
+        }
+        *(Q*)&R1[r * LD1 + f] = gU;
+        *(Q*)&R1[r * LD1 + F + f] = gV;
+      }
+    } else if constexpr (PRE) {
 #pragma unroll
       for (int e = 0; e < EPT; ++e) {
         const int x = threadIdx.x + e * NT, r = x / F, f = x % F;
