@@ -555,13 +555,20 @@ __global__ void __launch_bounds__((64 * ub_nw<P, F>())) k_update_bwd(UpdBwdArgs 
   auto V = [&](size_t i, int c, int f) { return P::ld(uv[(i * 3 + c) * 2 * F + F + f]); };
   constexpr int NT = 64 * ub_nw<P, F>(), EPT = (TM * F + NT - 1) / NT;
   constexpr bool PRE = EPT * (int)sizeof(A) <= (NT < 1024 ? 32 : 24);   // 1024 threads leave 128 VGPRs
-  // V4: FP32 with every thread on whole groups of 4 consecutive features:
-  // the element-wise passes move 16-byte vectors
-  constexpr bool V4 = std::is_same<T, float>::value && std::is_same<A, float>::value && PRE && LD1 % 4 == 0 &&
-                      (TM * F / 4) % NT == 0;
+  // V4: every thread on whole groups of 4 consecutive features: the
+  // element-wise passes load 16-byte (FP32) or 32-byte (FP64) vectors, and
+  // store them to LDS as such where its rows keep that alignment (FP32)
+  constexpr bool V4 = std::is_same<T, A>::value && PRE && (TM * F / 4) % NT == 0;
   constexpr int EPQ = V4 ? TM * F / 4 / NT : 1;
-  using Q = Quad<float>;
+  using Q = Quad<A>;
   auto ldq = [](const void* p) { return *(const Q*)p; };
+  auto stq = [](T* d, const Q& q) {
+    if constexpr (LD1 % 4 == 0) {
+      *(Q*)d = q;
+    } else {
+      for (int k = 0; k < 4; ++k) d[k] = q.x[k];
+    }
+  };
   // g_a into R1
   if constexpr (V4) {
 #pragma unroll
@@ -571,7 +578,7 @@ __global__ void __launch_bounds__((64 * ub_nw<P, F>())) k_update_bwd(UpdBwdArgs 
       for (int k = 0; k < 4; ++k) gvv.x[k] = gsv.x[k] = gss.x[k] = 0;
       if (row0 + r < (size_t)N) {
         const size_t i = row0 + r;
-        float pd[4] = {0, 0, 0, 0};
+        A pd[4] = {0, 0, 0, 0};
         for (int c = 0; c < 3; ++c) {
           const Q u = ldq(uv + (i * 3 + c) * 2 * F + f), w = ldq(uv + (i * 3 + c) * 2 * F + F + f);
           const Q g = ldq(gv + i * 3 * F + c * F + f);
@@ -583,9 +590,9 @@ __global__ void __launch_bounds__((64 * ub_nw<P, F>())) k_update_bwd(UpdBwdArgs 
         gss = ldq(gs + i * F + f);
         for (int k = 0; k < 4; ++k) gsv.x[k] = gss.x[k] * pd[k];
       }
-      *(Q*)&R1[r * LD1 + f] = gvv;
-      *(Q*)&R1[r * LD1 + F + f] = gsv;
-      *(Q*)&R1[r * LD1 + 2 * F + f] = gss;
+      stq(&R1[r * LD1 + f], gvv);
+      stq(&R1[r * LD1 + F + f], gsv);
+      stq(&R1[r * LD1 + 2 * F + f], gss);
     }
   } else
   for (int x = threadIdx.x; x < TM * F; x += blockDim.x) {
@@ -688,8 +695,8 @@ __global__ void __launch_bounds__((64 * ub_nw<P, F>())) k_update_bwd(UpdBwdArgs 
             gV.x[k] = gsa_r[q] * u.x[k] + (nv_r[q] > A(0) ? sc_r[q] * w.x[k] / nv_r[q] : A(0));
           }
         }
-        *(Q*)&R1[r * LD1 + f] = gU;
-        *(Q*)&R1[r * LD1 + F + f] = gV;
+        stq(&R1[r * LD1 + f], gU);
+        stq(&R1[r * LD1 + F + f], gV);
       }
     } else if constexpr (PRE) {
 #pragma unroll
