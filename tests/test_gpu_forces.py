@@ -147,6 +147,39 @@ def test_periodic(rt, precision):
     run_case(rt, hp, W, b, precision, f"periodic {precision}")
 
 
+def dense_periodic_batch():
+    """A 2.4 A periodic cube of 8 atoms (every periodic image within the 5 A
+    cutoff is an edge: ~300 edges per atom, so every sender's list of edges
+    runs past 256 ids, the longest the one-wave rank sort of the reverse pass
+    takes; longer lists are insertion-sorted) and a small molecule."""
+    rng = np.random.default_rng(4913)
+    L = 2.4
+    pos = []
+    while len(pos) < 8:
+        x = rng.uniform(0, L, 3)
+        d = [np.linalg.norm((x - y) - L * np.round((x - y) / L)) for y in pos]
+        if all(v > 0.7 for v in d):
+            pos.append(x)
+    cell = np.eye(3) * L
+    structs = [
+        (np.array(pos), rng.integers(0, 10, 8), cell, np.ones(3, np.uint8), 0),
+        (_cluster(rng, 6), rng.integers(0, 10, 6), np.zeros((3, 3)), np.zeros(3, np.uint8), 0),
+    ]
+    return synth.concat(structs)
+
+
+@pytest.mark.parametrize("precision", ["fp64", "fp32"])
+def test_dense_periodic_senders(rt, precision):
+    """Senders with more than 256 edges each (the reverse pass's edge
+    grouping falls back to its one-lane sort), against the oracle."""
+    say(f"dense periodic cell, {precision}")
+    hp = synth.HyperParams(F=64, K=12, L=2, n_species=10, n_heads=1, cutoff=5.0,
+                           shared_dims=[], branch_dims=[32, 1])
+    W = synth.make_weights(hp, 3104)
+    b = dense_periodic_batch()
+    run_case(rt, hp, W, b, precision, f"dense periodic {precision}")
+
+
 @pytest.mark.parametrize("precision", ["fp64", "fp32"])
 def test_bessel_capped_dataset_heads(rt, precision):
     """The lead model's ingredients: Bessel basis, neighbour cap, shared head
