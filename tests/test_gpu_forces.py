@@ -397,3 +397,36 @@ def test_full_size_molecules_sampled(rt):
     check_forces(Fo, b, ref, idx, FORCE_TOL["fp32"], "molecules_4096 fp32")
     g.free()
     m.free()
+
+
+def test_past_256_scan_blocks(rt):
+    """8192 molecules (287,944 atoms): the per-receiver and per-sender edge
+    counts are scanned in more than 256 blocks of 1024, so the block offsets
+    carry across chunks of 256; structures past atom 262,144 depend on that
+    carry.  FP32 forces of sampled structures, most of them past that atom,
+    against the oracle (the forces depend on both edge lists)."""
+    import torch
+    say("8192 molecules, fp32, forces")
+    hp = synth.HyperParams(F=64, K=8, L=2, n_species=10, n_heads=1, cutoff=5.0,
+                           shared_dims=[], branch_dims=[16, 1])
+    W = synth.make_weights(hp, 3105)
+    b = synth.make_batch("molecules_4096", 0, 8192)
+    assert (int(b.struct_ptr[-1]) + 1023) // 1024 > 256
+    m = rt.load_model(synth.weight_file_bytes(hp, W))
+    g = rt.build_graph(rt.upload_batch(b), hp.cutoff)
+    E, Fo = rt.forces(m, g, "fp32")
+    E0 = rt.forward(m, g, "fp32")
+    torch.cuda.synchronize()
+    E, Fo, E0 = E.cpu().numpy(), Fo.cpu().numpy(), E0.cpu().numpy()
+    assert np.array_equal(E, E0)
+    first_past = int(np.searchsorted(b.struct_ptr, 262144))
+    rng = np.random.default_rng(6)
+    idx = [0, first_past - 1, first_past, b.n_struct - 1] + \
+          [int(k) for k in rng.choice(np.arange(first_past, b.n_struct), 8, replace=False)]
+    ref = oracle(b, hp, W, idx)
+    for k, o in zip(idx, ref):
+        lo, hi = int(b.struct_ptr[k]), int(b.struct_ptr[k + 1])
+        assert o["n_edges"] > 0 and hi > lo
+    check_forces(Fo, b, ref, idx, FORCE_TOL["fp32"], "8192 molecules fp32")
+    g.free()
+    m.free()
