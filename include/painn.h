@@ -105,9 +105,16 @@ painn_status painn_synchronize(painn_ctx* ctx);
  *   int32 0.  Optional sections follow the arrays, each at most once, in any
  *   order.
  * The split of phi's output is [s | v | rhat] and of the update MLP's output
- * [a_vv | a_sv | a_ss].  Supported: F in {64, 128, 256}, 2 <= K <= 64,
- * 1 <= L <= 16, n_heads <= 64, branch_dims[last] = 1; with the
- * branch-weighting MLP n_species <= 256 and widths <= 1024. */
+ * [a_vv | a_sv | a_ss].  Supported: 1 <= F <= 384 (the kernels run at
+ * F = 64, 128, 256 or 384; any other width is zero-padded on load to the next
+ * of them, which leaves every energy unchanged), 2 <= K <= 64, 1 <= L <= 16,
+ * 1 <= n_heads <= 64, head widths in [1, 1024], branch_dims[last] = 1; with
+ * the branch-weighting MLP n_species <= 256 and widths <= 1024.
+ * Errors: PAINN_E_ARG (null argument), PAINN_E_FILE (the path cannot be
+ * opened or read), PAINN_E_FORMAT (bad magic, truncated or oversized
+ * arrays, trailing bytes, a malformed or repeated optional section, a
+ * non-finite weight), PAINN_E_UNSUPPORTED (a shape outside the ranges
+ * above), PAINN_E_OOM. */
 painn_status painn_model_load(painn_ctx* ctx, const char* path, painn_model** out);
 /* Same, from a host buffer holding the file's bytes (copied; the buffer may
  * be released after the call). */
@@ -142,8 +149,11 @@ painn_status painn_model_free(painn_model* model);
  *              = no periodic axis anywhere.  A periodic cell must be non-singular.
  * The graph copies what it needs (positions, species, cells), so the inputs
  * may change after the call's stream position.  If *inout is NULL a new graph
- * is created; otherwise *inout is rebuilt in place, reusing its memory.
- * Synchronises the stream once.  Errors: PAINN_E_ARG (bad sizes, cutoff not
+ * is created; otherwise *inout is rebuilt in place, reusing its memory.  When
+ * an in-place rebuild fails after its arguments passed the host checks, the
+ * graph is left unusable: painn_graph_csr, painn_forward* and painn_forces*
+ * return PAINN_E_ARG for it until a later build succeeds (it may still be
+ * rebuilt or freed).  Synchronises the stream once.  Errors: PAINN_E_ARG (bad sizes, cutoff not
  * finite and > 0, malformed struct_ptr, singular periodic cell, more than
  * 2^31-1 edges, image range beyond +-127), PAINN_E_COINCIDENT. */
 painn_status painn_build_graph(painn_ctx* ctx, int32_t n_struct, int32_t n_atoms,

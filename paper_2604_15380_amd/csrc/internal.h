@@ -8,6 +8,7 @@
 #include <vector>
 
 #include "painn.h"
+#include "weightfile.h"
 
 typedef uint16_t bf16_t;  // bfloat16 storage (upper half of an IEEE float)
 
@@ -121,17 +122,6 @@ struct PrecModel {      // the model cast and packed for one precision
   std::vector<void*> allocs;
 };
 
-struct Hyper {
-  int F;            // feature width the kernels run at (64, 128, 256, 384)
-  int F_logical;    // the model's own width (<= F; the rest is zero padding)
-  int K, L, n_species, n_heads, rbf_type;
-  double cutoff;
-  std::vector<int> shared_dims, branch_dims;
-  std::vector<int> blend_dims;   // hidden widths of the branch-weighting MLP
-  bool has_blend = false;
-  int max_neighbors = 0;         // neighbour cap the model was trained with (0: none)
-};
-
 // ---- per-kernel event timing (painn_profile_*) ------------------------------
 enum KernelClass {
   KC_GRAPH_PREP, KC_GRAPH_COUNT, KC_GRAPH_SCAN, KC_GRAPH_FILL, KC_EMBED, KC_PHI,
@@ -172,6 +162,9 @@ struct painn_graph {
   double cutoff = 0.0;
   int32_t species_min = 0, species_max = -1;
   bool any_pbc = false;
+  // set only when the last build succeeded; a failed rebuild leaves buffers
+  // half written, and every consumer of the graph refuses it until rebuilt
+  bool valid = false;
   // device buffers (capacities in elements)
   int32_t* row_ptr = nullptr;  int32_t* counts = nullptr;
   int32_t* col = nullptr;      int32_t* shift = nullptr;

@@ -40,20 +40,24 @@ def _oracle_job(args):
 
 
 def _oracle_forces_job(args):
-    from oracle.forces import structure_forces
-    name, batch_tuple, idx = args
+    from oracle.forces import structure_forces, structure_forces_blend
+    name, batch_tuple, idx, blend_skip = args
     hp, W = synth.workload_weights(name)
+    if blend_skip is not None:
+        return [(k, structure_forces_blend(pos, z, cell, pbc, hp, W, skip=blend_skip))
+                for k, (pos, z, cell, pbc, ds) in zip(idx, batch_tuple)]
     return [(k, structure_forces(pos, z, cell, pbc, ds if hp.n_heads > 1 else 0, hp, W)["F"])
             for k, (pos, z, cell, pbc, ds) in zip(idx, batch_tuple)]
 
 
-def oracle_forces(name: str, batch, idx, workers: int | None = None):
+def oracle_forces(name: str, batch, idx, workers: int | None = None, blend_skip=None):
     """Oracle forces of structures `idx` of `batch` (list of [n_b, 3]), in a
-    process pool."""
+    process pool; blend_skip given: the oracle's blended-heads result dicts
+    (F, w, ...) with heads below blend_skip left out."""
     idx = [int(i) for i in idx]
     workers = workers or min(16, os.cpu_count() or 1, max(1, len(idx)))
     chunks = [idx[w::workers] for w in range(workers)]
-    jobs = [(name, [batch.structure(k) for k in c], c) for c in chunks if c]
+    jobs = [(name, [batch.structure(k) for k in c], c, blend_skip) for c in chunks if c]
     res = {}
     with ProcessPoolExecutor(workers, initializer=_single_thread_blas) as ex:
         for part in ex.map(_oracle_forces_job, jobs):
@@ -83,14 +87,93 @@ def oracle_energies(name: str, batch, idx, workers: int | None = None, blend_ski
     return E, A
 
 
+def _oracle_blend_job(args):
+    from oracle.painn import structure_forward_blend
+    name, batch_tuple, idx, skip = args
+    hp, W = synth.workload_weights(name)
+    return [(k, structure_forward_blend(pos, z, cell, pbc, hp, W, skip=skip))
+            for k, (pos, z, cell, pbc, ds) in zip(idx, batch_tuple)]
+
+
+def oracle_blend(name: str, batch, idx, skip: float, workers: int | None = None):
+    """The oracle's blended-heads results (dicts with E, e, w, E_heads) of
+    structures `idx` of `batch`, in a process pool."""
+    idx = [int(i) for i in idx]
+    workers = workers or min(16, os.cpu_count() or 1, max(1, len(idx)))
+    chunks = [idx[w::workers] for w in range(workers)]
+    jobs = [(name, [batch.structure(k) for k in c], c, skip) for c in chunks if c]
+    res = {}
+    with ProcessPoolExecutor(workers, initializer=_single_thread_blas) as ex:
+        for part in ex.map(_oracle_blend_job, jobs):
+            res.update(dict(part))
+    return [res[k] for k in idx]
+
+
 def check_energies(E_gpu, E_ref, A_ref, tol: float, label: str = ""):
-    """Assert the tolerance; return (max normalised error, max plain relative error)."""
+    """Assert the tolerance on |E - E_ref| / sum_i |e_i^ref| per structure and
+    report the plain relative error |E - E_ref| / |E_ref| beside it: its
+    maximum and the share of structures within `tol` by that measure (it
+    is ill-conditioned where E nearly cancels over the atoms).  Prints one
+    line; returns (max normalised error, max plain relative error)."""
     E_gpu = np.asarray(E_gpu, dtype=np.float64)
     err = np.abs(E_gpu - E_ref)
     norm = err / A_ref
-    rel = err / np.abs(E_ref)
+    with np.errstate(divide="ignore", invalid="ignore"):
+        rel = np.where(E_ref != 0, err / np.abs(E_ref), np.where(err == 0, 0.0, np.inf))
     worst = int(np.argmax(norm))
+    share = float(np.mean(rel <= tol)) if len(rel) else 1.0
+    print(f"{label}: {len(E_gpu)} structures; max |dE|/sum|e| = {norm.max() if len(norm) else 0.0:.3e}; "
+          f"max |dE|/|E| = {rel.max() if len(rel) else 0.0:.3e}; "
+          f"{100 * share:.2f}% within {tol:.0e} plain relative", flush=True)
     assert np.all(np.isfinite(E_gpu)), f"{label}: non-finite energies"
     assert norm.max() <= tol, (f"{label}: max |dE|/sum|e| = {norm.max():.3e} > {tol:.1e} "
                                f"at sample {worst} (E={E_gpu[worst]!r}, ref={E_ref[worst]!r})")
     return float(norm.max()), float(rel.max())
+
+
+def check_forces(Fg, batch, ref_F, idx, tol: float, label: str = ""):
+    """Per structure k of idx: max |F - F_ref| over its atoms and components
+    <= tol * max |F_ref| of the structure (a structure with no force must get
+    exactly zero).  Returns the worst ratio."""
+    worst = 0.0
+    for k, Fr in zip(idx, ref_F):
+        lo, hi = int(batch.struct_ptr[k]), int(batch.struct_ptr[k + 1])
+        Fk = np.asarray(Fg[lo:hi])
+        assert np.all(np.isfinite(Fk)), f"{label}: non-finite forces in structure {k}"
+        scale = float(np.abs(Fr).max()) if hi > lo else 0.0
+        err = float(np.abs(Fk - Fr).max()) if hi > lo else 0.0
+        if scale == 0.0:
+            assert err == 0.0, f"{label}: structure {k} has no force but got {err:.3e}"
+            continue
+        worst = max(worst, err / scale)
+        assert err <= tol * scale, f"{label}: structure {k}: max|dF| = {err:.3e} > {tol:.0e} * {scale:.3e}"
+    print(f"{label}: {len(idx)} structures; worst max|dF|/max|F| = {worst:.3e}", flush=True)
+    return worst
+
+
+# Blended heads: absolute tolerance on the head weights (in [0, 1]) and the
+# relative band around the skip threshold inside which the two sides may
+# decide a head differently (the weights carry the precision's rounding)
+W_TOL = {"fp64": 1e-12, "fp32": 1e-5, "bf16": 3e-2}
+W_BAND = {"fp64": 1e-9, "fp32": 1e-3, "bf16": 0.25}
+
+
+def check_blend(E, w_gpu, refs, idx, skip: float, precision: str, label: str = ""):
+    """Blended energies of structures idx against the oracle's results
+    `refs` (dicts with E, e, w, E_heads): weights within W_TOL, every head
+    outside the undecided band kept or skipped alike, and the energy within
+    the precision's tolerance of sum_i |e_i| after adding the contribution of
+    undecided heads to the allowed error.  Returns the worst normalised error."""
+    worst = 0.0
+    n_heads = len(refs[0]["w"]) if refs else 0
+    for k, o in zip(idx, refs):
+        assert np.abs(w_gpu[k] - o["w"]).max() <= W_TOL[precision], (label, k)
+        undecided = (np.abs(o["w"] - skip) <= W_BAND[precision] * skip) if skip > 0 \
+            else np.zeros(n_heads, bool)
+        assert np.array_equal((w_gpu[k] >= skip)[~undecided], (o["w"] >= skip)[~undecided]), (label, k)
+        slack = 1.1 * float(np.sum((o["w"][undecided] + W_TOL[precision]) * np.abs(o["E_heads"][undecided])))
+        err = (abs(E[k] - o["E"]) - slack) / max(np.abs(o["e"]).sum(), 1e-300)
+        worst = max(worst, err)
+    print(f"{label}: {len(idx)} structures; worst blended |dE|/sum|e| = {worst:.3e}", flush=True)
+    assert worst <= TOL[precision], (label, worst)
+    return worst

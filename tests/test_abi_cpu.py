@@ -49,3 +49,41 @@ def test_binding_fails_loudly_without_library(tmp_path, monkeypatch):
     monkeypatch.setattr(binding, "lib_path", lambda: str(tmp_path / "missing.so"))
     with pytest.raises(RuntimeError, match="not built"):
         binding.load_library()
+
+
+@pytest.mark.skipif(not os.path.exists(binding.lib_path()), reason="library not built")
+def test_null_handles_without_device():
+    """Every entry point given a null context or null handle returns its
+    documented status (PAINN_E_ARG; PAINN_OK for the *_free calls and
+    painn_destroy) before any device call, so this runs without a GPU."""
+    lib = binding.load_library()
+    E_ARG = -1
+    out = ctypes.c_void_p()
+    i32 = ctypes.c_int32()
+    d = ctypes.c_double()
+    i64 = ctypes.c_int64()
+    names = (ctypes.c_char_p * 4)()
+    ms = (ctypes.c_double * 4)()
+    cnt = (ctypes.c_int64 * 4)()
+    r = ctypes.byref
+    assert lib.painn_create(0, None, None) == E_ARG
+    assert lib.painn_set_stream(None, None) == E_ARG
+    assert lib.painn_destroy(None) == 0
+    assert lib.painn_last_error(None) == b"null context"
+    assert lib.painn_synchronize(None) == E_ARG
+    assert lib.painn_model_load(None, b"/nonexistent", r(out)) == E_ARG
+    assert lib.painn_model_load_buffer(None, b"PAINNW01", 8, r(out)) == E_ARG
+    assert lib.painn_model_info(None, r(i32), r(i32), r(i32), r(i32), r(i32), r(d)) == E_ARG
+    assert lib.painn_model_options(None, r(i32), r(i32)) == E_ARG
+    assert lib.painn_model_free(None) == 0
+    assert lib.painn_build_graph(None, 1, 1, None, None, None, None, None, 5.0, r(out)) == E_ARG
+    assert lib.painn_build_graph_capped(None, 1, 1, None, None, None, None, None, 5.0, 3, r(out)) == E_ARG
+    assert lib.painn_graph_csr(None, r(i64), r(i32), r(i32), None, None, None) == E_ARG
+    assert lib.painn_graph_free(None) == 0
+    assert lib.painn_forward(None, None, None, None, 0, None) == E_ARG
+    assert lib.painn_forward_blend(None, None, None, 0, 0.0, None, None) == E_ARG
+    assert lib.painn_forward_features(None, None, None, 0, 0, None, None) == E_ARG
+    assert lib.painn_forces(None, None, None, None, 0, None, None) == E_ARG
+    assert lib.painn_forces_blend(None, None, None, 0, 0.0, None, None, None) == E_ARG
+    assert lib.painn_profile_enable(None, 1) == E_ARG
+    assert lib.painn_profile_read(None, 4, names, ms, cnt, r(i32)) == E_ARG

@@ -127,6 +127,36 @@ def test_screening_first_batch(rt, precision):
     check_energies(E[idx], Er, Ar, TOL[precision], f"{name} {precision}")
 
 
+def test_screening_stream_sample(rt):
+    """The screening stream as the benchmark's stream mode walks it: its
+    first 20 batches (about 25,000 structures, each batch closed before
+    65,536 atoms), each built and run whole at BF16 and FP32; every 100th
+    structure of the stream is compared with the FP64 oracle."""
+    name = "screening"
+    hp, _ = synth.workload_weights(name)
+    m = model(rt, name)
+    batches = synth.screening_batches(30000)[:20]
+    picked, E_bf16, E_fp32 = [], [], []
+    g = None
+    for bi, (start, cnt) in enumerate(batches):
+        say(f"stream batch {bi}: structures {start}..{start + cnt - 1}")
+        b = synth.make_batch(name, start, cnt)
+        inp = rt.upload_batch(b)
+        g = rt.build_graph(inp, hp.cutoff, graph=g)
+        local = [k for k in range(cnt) if (start + k) % 100 == 0]
+        for prec, dst in (("bf16", E_bf16), ("fp32", E_fp32)):
+            E = rt.forward(m, g, prec, dataset_id=inp["dataset_id"]).cpu().numpy()
+            assert np.all(np.isfinite(E)), (bi, prec)
+            dst.extend(E[local].tolist())
+        picked.extend(b.structure(k) for k in local)
+    g.free()
+    sample = synth.concat(picked)
+    say(f"stream sample: {sample.n_struct} structures of {sum(c for _, c in batches)}")
+    Er, Ar = oracle_energies(name, sample, range(sample.n_struct))
+    check_energies(np.array(E_bf16), Er, Ar, TOL["bf16"], "screening stream bf16")
+    check_energies(np.array(E_fp32), Er, Ar, TOL["fp32"], "screening stream fp32")
+
+
 def test_heads_grouping(rt):
     """Atoms are grouped by dataset head before the heads run: one head over
     many tiles, a sparse mix of heads with ragged tile ends, and no dataset ids

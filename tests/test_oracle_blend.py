@@ -102,3 +102,38 @@ def test_weight_file_round_trip_with_router():
     Wn = {k: v for k, v in W.items() if not k.startswith("blend")}
     hp3, W3 = synth.read_weight_file(synth.weight_file_bytes(hp, Wn))
     assert hp3.blend_dims is None and not any(k.startswith("blend") for k in W3)
+
+
+def test_router_hidden_layers_closed_form():
+    """The branch-weighting MLP with two hidden layers and hand-chosen
+    non-square weights, evaluated by hand with scalar arithmetic: SiLU after
+    each hidden layer, none after the output layer, weights applied as
+    [out, in], then a softmax.  A dropped or extra SiLU, a transposed layer or
+    a missing bias changes the weights far beyond the tolerance."""
+    import math
+    hp = synth.HyperParams(F=4, K=2, L=1, n_species=3, n_heads=3, cutoff=4.0,
+                           shared_dims=[], branch_dims=[1], blend_dims=[4, 2])
+    W = synth.make_weights(hp, 5)
+    W["blend0.w"] = np.array([[1.0, 0, 0], [0, 2.0, 0], [0, 0, -3.0], [1.0, 1.0, 1.0]])
+    W["blend0.b"] = np.array([0.5, -1.0, 0.0, 0.25])
+    W["blend1.w"] = np.array([[0.0, 1.0, 0.0, 2.0], [-1.0, 0.0, 1.0, 0.0]])
+    W["blend1.b"] = np.array([0.1, -0.2])
+    W["blend2.w"] = np.array([[1.0, 0.0], [0.0, 1.0], [2.0, -1.0]])
+    W["blend2.b"] = np.array([0.0, 0.3, -0.1])
+    z = np.array([0, 0, 1, 2, 2, 2])
+    c = composition(z, 3)
+
+    def silu(x):
+        return x / (1.0 + math.exp(-x))
+
+    c0, c1, c2 = 2 / 6, 1 / 6, 3 / 6
+    h1 = [silu(c0 + 0.5), silu(2 * c1 - 1.0), silu(-3 * c2), silu(c0 + c1 + c2 + 0.25)]
+    h2 = [silu(h1[1] + 2 * h1[3] + 0.1), silu(-h1[0] + h1[2] - 0.2)]
+    logit = [h2[0], h2[1] + 0.3, 2 * h2[0] - h2[1] - 0.1]
+    m = max(logit)
+    ex = [math.exp(x - m) for x in logit]
+    want = np.array([x / sum(ex) for x in ex])
+    got = blend_weights(c, hp, W)
+    assert np.allclose(got, want, rtol=1e-14, atol=0), (got, want)
+    # the weights are not near-uniform, so the pin has teeth
+    assert want.max() - want.min() > 0.2
