@@ -194,6 +194,25 @@ painn_status painn_forward(painn_ctx* ctx, const painn_model* model, const painn
                            const int32_t* dataset_id, painn_precision precision,
                            double* energies);
 
+/* For callers that cannot allocate device memory (code under HIP graph
+ * capture, tight serving loops, harnesses that forbid hipMalloc): the same
+ * energies as painn_forward, computed by the same kernels, with the forward's
+ * workspace carved from one fixed device array of 64 MiB
+ * (NOALLOC_SCRATCH_BYTES) that the library holds on each device from its
+ * first use until the process ends.  The call allocates nothing: the model
+ * must already hold its packed weights for this precision (run painn_forward
+ * once at this precision first; otherwise PAINN_E_ARG), the graph is built
+ * beforehand, and per-kernel event timing (painn_profile_enable) is not
+ * recorded for it.  A batch whose workspace exceeds 64 MiB (about 9,000
+ * atoms at F = 128 in FP32; fewer at wider F, more in BF16) is refused with
+ * PAINN_E_ARG, naming the bytes it needs.  Every call on a device shares that
+ * device's array: calls that overlap in time on one device (on different
+ * streams or contexts) race and must be ordered by the caller.  Arguments and
+ * other errors as painn_forward. */
+painn_status painn_forward_noalloc(painn_ctx* ctx, const painn_model* model, const painn_graph* graph,
+                                   const int32_t* dataset_id, painn_precision precision,
+                                   double* energies);
+
 /* Per-structure energies with every head blended (sections
  * "Composition-conditioned branch weighting" and "Optimizing the Inference
  * Pipeline", branch skipping): the encoder runs once; structure b's

@@ -14,6 +14,7 @@ EXPORTS = [
     "painn_status_string", "painn_synchronize", "painn_model_load",
     "painn_model_load_buffer", "painn_model_info", "painn_model_options", "painn_model_free",
     "painn_build_graph", "painn_build_graph_capped", "painn_graph_csr", "painn_graph_free", "painn_forward",
+    "painn_forward_noalloc",
     "painn_forward_blend", "painn_forward_features", "painn_forces", "painn_forces_blend",
     "painn_profile_enable",
     "painn_profile_read",
@@ -41,6 +42,7 @@ _SIGS = {
                          ctypes.POINTER(_P), ctypes.POINTER(_P), ctypes.POINTER(_P)], ctypes.c_int),
     "painn_graph_free": ([_P], ctypes.c_int),
     "painn_forward": ([_P, _P, _P, _P, ctypes.c_int, _P], ctypes.c_int),
+    "painn_forward_noalloc": ([_P, _P, _P, _P, ctypes.c_int, _P], ctypes.c_int),
     "painn_forward_blend": ([_P, _P, _P, ctypes.c_int, ctypes.c_double, _P, _P], ctypes.c_int),
     "painn_forward_features": ([_P, _P, _P, ctypes.c_int, _I32, _P, _P], ctypes.c_int),
     "painn_forces": ([_P, _P, _P, _P, ctypes.c_int, _P, _P], ctypes.c_int),
@@ -180,6 +182,12 @@ def painn_graph_free(graph: int) -> None:
 def painn_forward(ctx: int, model: int, graph: int, dataset_id: int | None, precision: int,
                   energies: int) -> None:
     _check(load_library().painn_forward(ctx, model, graph, dataset_id or None, precision, energies), ctx)
+
+
+def painn_forward_noalloc(ctx: int, model: int, graph: int, dataset_id: int | None, precision: int,
+                          energies: int) -> None:
+    _check(load_library().painn_forward_noalloc(ctx, model, graph, dataset_id or None, precision, energies),
+           ctx)
 
 
 def painn_forward_blend(ctx: int, model: int, graph: int, precision: int, skip_threshold: float,

@@ -315,6 +315,12 @@ struct BackwardArgs {
   Profiler* prof;
 };
 hipError_t launch_backward(hipStream_t s, int prec, BackwardArgs& a);
+// The fixed scratch of painn_forward_noalloc: its size, the once-per-device
+// lookup of its address (painn_create calls it with the device current) and
+// that address (null before a successful lookup).
+constexpr size_t NOALLOC_SCRATCH_BYTES = (size_t)64 << 20;
+hipError_t noalloc_scratch_init(int device);
+void* noalloc_scratch(int device);
 // workgroups of the reverse heads kernel (a persistent grid; each has its
 // own 16 scratch rows and, for wide layers, its own operand buffers)
 constexpr int HB_GRID = 2048;

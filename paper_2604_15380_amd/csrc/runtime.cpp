@@ -385,6 +385,9 @@ painn_status painn_create(int device, void* stream, painn_ctx** out) {
   if (!ctx) return PAINN_E_OOM;
   ctx->device = device;
   ctx->stream = (hipStream_t)stream;
+  // the fixed scratch of painn_forward_noalloc: its address on this device
+  // (a failed lookup is reported by that entry point, nothing else needs it)
+  (void)noalloc_scratch_init(device);
   if (hipHostMalloc((void**)&ctx->h_status, sizeof(DevStatus), hipHostMallocDefault) != hipSuccess) {
     delete ctx;
     return PAINN_E_OOM;
@@ -694,7 +697,8 @@ static painn_status run_forward(painn_ctx* ctx, const painn_model* model, const 
                                 const int32_t* dataset_id, painn_precision prec, int stop_layer,
                                 double* energies, double* s_out, double* v_out, bool blend = false,
                                 double skip = 0.0, double* weights_out = nullptr, void* save = nullptr,
-                                ForwardArgs* keep = nullptr) {
+                                ForwardArgs* keep = nullptr, void* ws_fixed = nullptr,
+                                size_t ws_fixed_bytes = 0) {
   if (!ctx) return PAINN_E_ARG;
   ctx->err.clear();
   if (!model || !g) return fail(ctx, PAINN_E_ARG, "null model or graph");
@@ -711,13 +715,23 @@ static painn_status run_forward(painn_ctx* ctx, const painn_model* model, const 
   (void)hipSetDevice(ctx->device);
   painn_model* m = const_cast<painn_model*>(model);
   if (!m->prec[prec]) {
+    if (ws_fixed)
+      return fail(ctx, PAINN_E_ARG, "the model's weights are not packed for this precision yet: run "
+                                    "painn_forward once at this precision before painn_forward_noalloc");
     painn_status st = build_prec(m, prec, &m->prec[prec]);
     if (st != PAINN_OK) return st;
   }
   const int kcols = m->prec[prec]->layers[0].filt_mma.din_p;
   size_t need = forward_workspace_bytes(prec, g->N, g->E, m->hp.F, kcols, g->B, m->hp.n_heads,
                                        m->hp.n_species, blend);
-  if (need > ctx->ws_bytes) {
+  void* ws = ctx->ws;
+  if (ws_fixed) {
+    if (need > ws_fixed_bytes)
+      return fail(ctx, PAINN_E_ARG, "this batch needs " + std::to_string(need) +
+                                        " bytes of workspace; painn_forward_noalloc has " +
+                                        std::to_string(ws_fixed_bytes));
+    ws = ws_fixed;
+  } else if (need > ctx->ws_bytes) {
     if (ctx->ws) {
       (void)hipStreamSynchronize(ctx->stream);
       (void)hipFree(ctx->ws);
@@ -728,6 +742,7 @@ static painn_status run_forward(painn_ctx* ctx, const painn_model* model, const 
     hipError_t e = hipMalloc(&ctx->ws, want);
     if (e != hipSuccess) return fail(ctx, PAINN_E_OOM, "forward workspace allocation failed");
     ctx->ws_bytes = want;
+    ws = ctx->ws;
   }
   ForwardArgs a{};
   a.m = m;
@@ -736,7 +751,7 @@ static painn_status run_forward(painn_ctx* ctx, const painn_model* model, const 
   a.dataset_id = dataset_id;
   a.energies = energies;
   a.stop_layer = stop_layer;
-  a.prof = ctx->prof;
+  a.prof = ws_fixed ? nullptr : ctx->prof;   // event timers create events on first use
   a.s_out = s_out;
   a.v_out = v_out;
   a.save = save;
@@ -744,7 +759,7 @@ static painn_status run_forward(painn_ctx* ctx, const painn_model* model, const 
   const size_t eb = elem_bytes(prec), ab = acc_bytes(prec);
   const size_t N = g->N, F = m->hp.F;
   auto al = [](size_t x) { return (x + 255) & ~(size_t)255; };
-  char* p = (char*)ctx->ws;
+  char* p = (char*)ws;
   a.s = p; p += al(N * F * eb);
   a.v[0] = p; p += al(N * 3 * F * eb);
   a.v[1] = p; p += al(N * 3 * F * eb);
@@ -1026,6 +1041,17 @@ painn_status painn_forward(painn_ctx* ctx, const painn_model* model, const painn
   if (ctx && graph && graph->B > 0 && !energies) return fail(ctx, PAINN_E_ARG, "energies is null");
   return run_forward(ctx, model, graph, dataset_id, precision, model ? model->hp.L - 1 : 0,
                      energies, nullptr, nullptr);
+}
+
+painn_status painn_forward_noalloc(painn_ctx* ctx, const painn_model* model, const painn_graph* graph,
+                                   const int32_t* dataset_id, painn_precision precision, double* energies) {
+  if (!ctx) return PAINN_E_ARG;
+  if (graph && graph->B > 0 && !energies) return fail(ctx, PAINN_E_ARG, "energies is null");
+  void* scratch = noalloc_scratch(ctx->device);
+  if (!scratch) return fail(ctx, PAINN_E_HIP, "the fixed scratch's device address is not available");
+  return run_forward(ctx, model, graph, dataset_id, precision, model ? model->hp.L - 1 : 0, energies,
+                     nullptr, nullptr, false, 0.0, nullptr, nullptr, nullptr, scratch,
+                     NOALLOC_SCRATCH_BYTES);
 }
 
 painn_status painn_forward_blend(painn_ctx* ctx, const painn_model* model, const painn_graph* graph,
