@@ -266,6 +266,54 @@ painn_status painn_forward_features(painn_ctx* ctx, const painn_model* model,
                                     const painn_graph* graph, painn_precision precision,
                                     int32_t layer, double* s_out, double* v_out);
 
+/* ---- training ----------------------------------------------------------- */
+
+/* One FP64 training step on energies and forces (section "Flagship Training
+ * of Top HPO Models"; Table "Lead PaiNN model configuration": MAE loss, force
+ * weight ~94.8, AdamW at learning rate 6.34e-4, FP64).  The loss over a batch
+ * of B structures and N atoms is
+ *   L = (1/B) sum_b |E_b - E*_b| + force_weight (1/(3N)) sum_{i,c} |F_ic - F*_ic|
+ * with F = -dE/dx (forces as painn_forces, dataset-id heads).  A step runs the
+ * forward and the reverse pass to the forces, then the gradient of L with
+ * respect to every weight (the force term through the derivative of the
+ * weight gradient along the force residuals' signs), then one AdamW update
+ * (decoupled weight decay, bias-corrected moments) of every weight.  The
+ * trainer keeps its own FP64 copy of the weights (at the model's own width,
+ * in the weight file's order) and the optimizer state; the model it was made
+ * from is not changed. */
+typedef struct painn_trainer painn_trainer;
+typedef struct {
+  double lr;            /* learning rate (6.34e-4) */
+  double beta1, beta2;  /* AdamW moment decays (0.9, 0.999) */
+  double eps;           /* AdamW denominator offset (1e-8) */
+  double weight_decay;  /* decoupled weight decay (0.01) */
+  double force_weight;  /* the loss's force weight (94.8) */
+} painn_train_config;
+
+/* Create a trainer from a model's weights.  cfg is a host pointer (NULL: the
+ * values in parentheses above).  Errors: PAINN_E_ARG (null model, values out
+ * of range: lr, eps, weight_decay, force_weight finite and >= 0 (eps > 0),
+ * 0 <= beta < 1), PAINN_E_OOM. */
+painn_status painn_trainer_create(painn_ctx* ctx, const painn_model* model, const painn_train_config* cfg,
+                                  painn_trainer** out);
+/* One step on a batch: the graph (built with the model's cutoff and
+ * neighbour cap from the batch's positions), dataset_id [B] (device; NULL =
+ * head 0), reference energies energy_ref [B] and forces force_ref [N, 3]
+ * (device, float64).  loss [3] (device float64, or NULL) receives L, the
+ * energy MAE and the force MAE at the weights before the update.  A dataset
+ * id outside [0, n_heads) makes the loss NaN (asynchronous: not a status).
+ * Errors: PAINN_E_ARG (null or mismatched graph, null references),
+ * PAINN_E_SPECIES, PAINN_E_UNSUPPORTED (more than 2^31 - 1 edges or 3 N F
+ * values), PAINN_E_OOM, PAINN_E_HIP.  Deterministic: every reduction runs in
+ * a fixed order. */
+painn_status painn_trainer_step(painn_trainer* tr, const painn_graph* graph, const int32_t* dataset_id,
+                                const double* energy_ref, const double* force_ref, double* loss);
+/* The number of weights (host), and copies (device, float64 [n_params], in
+ * the weight file's array order at the model's own width; either may be
+ * NULL) of the current weights and of the last step's gradient. */
+painn_status painn_trainer_params(const painn_trainer* tr, int64_t* n_params, double* params, double* grad);
+painn_status painn_trainer_free(painn_trainer* tr);
+
 /* ---- tracing ------------------------------------------------------------ */
 
 /* Per-kernel timing with HIP events on the context's stream (the build's

@@ -71,10 +71,12 @@ def _dense(x, w, b):
 
 
 def energy_weight_grad(pos, species, cell, pbc, dataset_id, hp, W, graph=None):
-    """Energy E of one structure and dE/dW for every array of W (same keys;
-    zero for arrays E does not depend on), by a reverse pass in the order of
-    the forward.  `pos` may be complex (the complex step); the graph
-    (recv, send, shift) is that of the real positions.  Returns (E, grads)."""
+    """Energy E of one structure and dE/dW by a reverse pass in the order of
+    the forward, for the arrays E depends on: the embedding, every layer, the
+    shared head layers and the structure's own branch (the other branches'
+    gradients are zero and left out of the returned dict).  `pos` may be
+    complex (the complex step); the graph (recv, send, shift) is that of the
+    real positions.  Returns (E, grads)."""
     F = hp.F
     z = np.asarray(species)
     x = np.asarray(pos)
@@ -135,7 +137,9 @@ def energy_weight_grad(pos, species, cell, pbc, dataset_id, hp, W, graph=None):
         y = _silu(zm) if m < len(names) - 1 else zm
     E = np.sum(y[:, 0])
 
-    G = {k: np.zeros(np.shape(val), dtype=dt) for k, val in W.items()}
+    used = ["emb"] + [k for k in W if k.startswith("l") or k.startswith("shared")]
+    used += [wn for wn, _ in names] + [bn for _, bn in names]
+    G = {k: np.zeros(np.shape(W[k]), dtype=dt) for k in dict.fromkeys(used)}
     # reverse through the heads (dE/de_i = 1)
     gz = np.ones((n, 1), dtype=dt)
     for m in range(len(names) - 1, -1, -1):
@@ -232,7 +236,7 @@ def loss_and_grad(batch, hp, W, E_ref, F_ref, force_weight: float):
         if hi == lo:
             continue
         part = structure_loss_grad_terms(pos, z, cell, pbc, ds[b], hp, W, c[b], u[lo:hi])
-        for k in grad:
+        for k in part:
             grad[k] += part[k]
     return dict(loss=loss_E + force_weight * loss_F, loss_E=loss_E, loss_F=loss_F, E=E, F=Fo, grad=grad)
 

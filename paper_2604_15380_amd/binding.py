@@ -16,6 +16,7 @@ EXPORTS = [
     "painn_build_graph", "painn_build_graph_capped", "painn_graph_csr", "painn_graph_free", "painn_forward",
     "painn_forward_noalloc",
     "painn_forward_blend", "painn_forward_features", "painn_forces", "painn_forces_blend",
+    "painn_trainer_create", "painn_trainer_step", "painn_trainer_params", "painn_trainer_free",
     "painn_profile_enable",
     "painn_profile_read",
 ]
@@ -47,6 +48,10 @@ _SIGS = {
     "painn_forward_features": ([_P, _P, _P, ctypes.c_int, _I32, _P, _P], ctypes.c_int),
     "painn_forces": ([_P, _P, _P, _P, ctypes.c_int, _P, _P], ctypes.c_int),
     "painn_forces_blend": ([_P, _P, _P, ctypes.c_int, ctypes.c_double, _P, _P, _P], ctypes.c_int),
+    "painn_trainer_create": ([_P, _P, _P, ctypes.POINTER(_P)], ctypes.c_int),
+    "painn_trainer_step": ([_P, _P, _P, _P, _P, _P], ctypes.c_int),
+    "painn_trainer_params": ([_P, ctypes.POINTER(ctypes.c_int64), _P, _P], ctypes.c_int),
+    "painn_trainer_free": ([_P], ctypes.c_int),
     "painn_profile_enable": ([_P, ctypes.c_int], ctypes.c_int),
     "painn_profile_read": ([_P, _I32, ctypes.POINTER(ctypes.c_char_p), ctypes.POINTER(ctypes.c_double),
                             ctypes.POINTER(ctypes.c_int64), ctypes.POINTER(_I32)], ctypes.c_int),
@@ -211,6 +216,38 @@ def painn_forces_blend(ctx: int, model: int, graph: int, precision: int, skip_th
 def painn_forward_features(ctx: int, model: int, graph: int, precision: int, layer: int,
                            s_out: int, v_out: int) -> None:
     _check(load_library().painn_forward_features(ctx, model, graph, precision, layer, s_out, v_out), ctx)
+
+
+class painn_train_config(ctypes.Structure):
+    """include/painn.h painn_train_config (host struct)."""
+    _fields_ = [("lr", ctypes.c_double), ("beta1", ctypes.c_double), ("beta2", ctypes.c_double),
+                ("eps", ctypes.c_double), ("weight_decay", ctypes.c_double), ("force_weight", ctypes.c_double)]
+
+
+def painn_trainer_create(ctx: int, model: int, cfg: dict | None = None) -> int:
+    out = _P()
+    c = None
+    if cfg is not None:
+        c = painn_train_config(**cfg)
+    _check(load_library().painn_trainer_create(ctx, model, ctypes.addressof(c) if c is not None else None,
+                                               ctypes.byref(out)), ctx)
+    return out.value
+
+
+def painn_trainer_step(ctx: int, trainer: int, graph: int, dataset_id: int | None, energy_ref: int | None,
+                       force_ref: int | None, loss: int | None) -> None:
+    _check(load_library().painn_trainer_step(trainer, graph, dataset_id or None, energy_ref or None,
+                                             force_ref or None, loss or None), ctx)
+
+
+def painn_trainer_params(ctx: int, trainer: int, params: int | None = None, grad: int | None = None) -> int:
+    n = ctypes.c_int64()
+    _check(load_library().painn_trainer_params(trainer, ctypes.byref(n), params or None, grad or None), ctx)
+    return n.value
+
+
+def painn_trainer_free(trainer: int) -> None:
+    _check(load_library().painn_trainer_free(trainer))
 
 
 def painn_profile_enable(ctx: int, enable: bool) -> None:

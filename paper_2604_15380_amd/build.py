@@ -17,7 +17,8 @@ ROOT = os.path.dirname(PKG)
 CSRC = os.path.join(PKG, "csrc")
 OUT = os.path.join(PKG, "_build")
 LIB = os.path.join(PKG, "libpainn.so")
-SOURCES = ["runtime.cpp", "weightfile.cpp", "noalloc.hip", "neighbors.hip", "forward.hip", "backward.hip"]
+SOURCES = ["runtime.cpp", "weightfile.cpp", "noalloc.hip", "neighbors.hip", "forward.hip", "backward.hip",
+           "train.hip"]
 
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 FLAGS = [

@@ -90,7 +90,9 @@ def test_complex_step_equals_difference_of_weight_gradients():
     _, Gp = energy_weight_grad(pos + eps * u, z, cell, pbc, int(d), hp, W, graph=graph)
     _, Gm = energy_weight_grad(pos - eps * u, z, cell, pbc, int(d), hp, W, graph=graph)
     _, G0 = energy_weight_grad(pos, z, cell, pbc, int(d), hp, W, graph=graph)
-    for k in W:
+    # every array the structure's energy depends on (its own head's branch)
+    assert set(W) - set(Gc) == {k for k in W if k.startswith("head") and not k.startswith(f"head{int(d)}.")}
+    for k in Gc:
         cs = np.imag(Gc[k]) / COMPLEX_STEP
         fd = (Gp[k] - Gm[k]) / (2 * eps)
         scale = max(1.0, float(np.abs(fd).max()))
