@@ -1,9 +1,10 @@
 """GPU blended heads (branch-weighting MLP + branch skipping) vs the oracle.
 
-Energies use the tolerance metric of the other forward tests.  Where the skip
-threshold decides whether a head is kept, the two sides compute the weight in
-different precisions: a head whose oracle weight lies within the precision's
-band around the threshold may be kept by one side and not the other, so its
+Energies use the tolerance metric of the other forward tests (BF16 against
+the oracle on the BF16-rounded weights).  Where the skip threshold decides
+whether a head is kept, the two sides compute the weight in different
+precisions: a head whose oracle weight lies within the weight tolerance of
+the threshold may be kept by one side and not the other, so its
 contribution w_h |E_h| is added to that structure's allowed error; every
 other head must be kept or skipped alike."""
 import copy
@@ -13,14 +14,10 @@ import numpy as np
 import pytest
 
 import synth
-from helpers import TOL
+from helpers import TOL, check_blend, report_vs_master, stored_weights
 from oracle.painn import structure_forward, structure_forward_blend
 
 pytestmark = pytest.mark.gpu
-W_TOL = {"fp64": 1e-12, "fp32": 1e-5, "bf16": 3e-2}   # absolute, on weights in [0, 1]
-# relative band around the skip threshold where a weight's side is undecided
-# at the precision's accuracy (the logits carry BF16 rounding in BF16)
-W_BAND = {"fp64": 1e-9, "fp32": 1e-3, "bf16": 0.25}
 
 
 def say(msg):
@@ -66,17 +63,13 @@ def test_blend_screening_batch(rt, screening, precision, skip):
     w_gpu = w_gpu.cpu().numpy()
     assert np.all(np.isfinite(E)) and np.allclose(w_gpu.sum(1), 1.0, atol=1e-5 if precision != "bf16" else 1e-3)
     idx = _sample(b.n_struct, 24 if precision == "fp64" else 48, seed=21)
-    worst = 0.0
-    for k in idx:
-        pos, z, cell, pbc, _ = b.structure(k)
-        o = structure_forward_blend(pos, z, cell, pbc, hp, W, skip=skip)
-        assert np.abs(w_gpu[k] - o["w"]).max() <= W_TOL[precision], k
-        undecided = np.abs(o["w"] - skip) <= W_BAND[precision] * skip if skip > 0 else np.zeros(hp.n_heads, bool)
-        assert np.array_equal((w_gpu[k] >= skip)[~undecided], (o["w"] >= skip)[~undecided]), k
-        slack = 1.1 * float(np.sum((o["w"][undecided] + W_TOL[precision]) * np.abs(o["E_heads"][undecided])))
-        err = (abs(E[k] - o["E"]) - slack) / max(np.abs(o["e"]).sum(), 1e-300)
-        worst = max(worst, err)
-    assert worst <= TOL[precision], worst
+    Ws = stored_weights(W, precision)
+    refs = [structure_forward_blend(*b.structure(k)[:4], hp, Ws, skip=skip) for k in idx]
+    check_blend(E, w_gpu, refs, idx, skip, precision, f"screening blended {precision} skip {skip}")
+    if precision == "bf16":
+        master = [structure_forward_blend(*b.structure(k)[:4], hp, W, skip=skip) for k in idx]
+        report_vs_master(E[idx], np.array([o["E"] for o in master]), np.array([np.abs(o["e"]).sum() for o in master]),
+                         np.array([o["E"] for o in refs]), TOL[precision], f"screening blended {precision}")
     if skip > 0:
         # most heads carry negligible weight (the premise of branch skipping)
         assert (w_gpu < skip).mean() > 0.5

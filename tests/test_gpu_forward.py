@@ -11,7 +11,7 @@ import pytest
 from scipy.spatial.transform import Rotation
 
 import synth
-from helpers import TOL, check_energies, oracle_energies
+from helpers import TOL, check_energies, check_workload_energies, oracle_energies
 from oracle.painn import structure_forward
 
 pytestmark = pytest.mark.gpu
@@ -56,8 +56,7 @@ def test_tiny_molecules_all_structures(rt, precision):
     say(f"forward {name} {precision}")
     b = synth.make_batch(name)
     E = run(rt, name, b, precision)
-    Er, Ar = oracle_energies(name, b, range(b.n_struct), workers=1)
-    norm, rel = check_energies(E, Er, Ar, TOL[precision], f"{name} {precision}")
+    norm, rel = check_workload_energies(E, name, b, range(b.n_struct), precision, f"{name} {precision}", workers=1)
     if precision == "fp64":
         assert rel <= 1e-10          # FP64 also meets the plain relative bound
 
@@ -100,8 +99,7 @@ def test_molecules_4096_full_batch(rt, precision):
     b = synth.make_batch(name)
     E = run(rt, name, b, precision)
     idx = _sample(b.n_struct, 160)
-    Er, Ar = oracle_energies(name, b, idx)
-    check_energies(E[idx], Er, Ar, TOL[precision], f"{name} {precision}")
+    check_workload_energies(E[idx], name, b, idx, precision, f"{name} {precision}")
 
 
 def test_bulk_1024_full_batch_fp64(rt):
@@ -123,8 +121,7 @@ def test_screening_first_batch(rt, precision):
     b = synth.make_batch(name, start, cnt)
     E = run(rt, name, b, precision)
     idx = _sample(b.n_struct, 96, seed=2)
-    Er, Ar = oracle_energies(name, b, idx)
-    check_energies(E[idx], Er, Ar, TOL[precision], f"{name} {precision}")
+    check_workload_energies(E[idx], name, b, idx, precision, f"{name} {precision}")
 
 
 def test_screening_stream_sample(rt):
@@ -152,9 +149,8 @@ def test_screening_stream_sample(rt):
     g.free()
     sample = synth.concat(picked)
     say(f"stream sample: {sample.n_struct} structures of {sum(c for _, c in batches)}")
-    Er, Ar = oracle_energies(name, sample, range(sample.n_struct))
-    check_energies(np.array(E_bf16), Er, Ar, TOL["bf16"], "screening stream bf16")
-    check_energies(np.array(E_fp32), Er, Ar, TOL["fp32"], "screening stream fp32")
+    check_workload_energies(np.array(E_bf16), name, sample, range(sample.n_struct), "bf16", "screening stream bf16")
+    check_workload_energies(np.array(E_fp32), name, sample, range(sample.n_struct), "fp32", "screening stream fp32")
 
 
 def test_heads_grouping(rt):

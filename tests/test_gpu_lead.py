@@ -6,7 +6,7 @@ import numpy as np
 import pytest
 
 import synth
-from helpers import TOL, check_energies
+from helpers import TOL, check_energies, report_vs_master, stored_weights
 from oracle.painn import RBF_BESSEL, structure_forward
 
 pytestmark = pytest.mark.gpu
@@ -40,10 +40,15 @@ def test_bessel_capped_model(rt, precision):
     b = synth.make_batch("molecules_4096", 0, 48)
     g = rt.build_graph(rt.upload_batch(b), hp.cutoff, max_neighbors=6)
     E = rt.forward(m, g, precision).cpu().numpy()
-    ref = [structure_forward(*b.structure(k)[:4], 0, hp, W) for k in range(b.n_struct)]
+    Ws = stored_weights(W, precision)
+    ref = [structure_forward(*b.structure(k)[:4], 0, hp, Ws) for k in range(b.n_struct)]
     Er = np.array([o["E"] for o in ref])
     Ar = np.array([np.abs(o["e"]).sum() for o in ref])
     check_energies(E, Er, Ar, TOL[precision], f"lead ingredients {precision}")
+    if precision == "bf16":
+        refm = [structure_forward(*b.structure(k)[:4], 0, hp, W) for k in range(b.n_struct)]
+        report_vs_master(E, np.array([o["E"] for o in refm]), np.array([np.abs(o["e"]).sum() for o in refm]), Er,
+                         TOL[precision], f"lead ingredients {precision}")
     g.free()
     m.free()
 
@@ -75,7 +80,8 @@ def test_padded_feature_widths(rt, F, precision):
     b = synth.make_batch("molecules_4096", 0, 24)
     g = rt.build_graph(rt.upload_batch(b), hp.cutoff)
     E = rt.forward(m, g, precision).cpu().numpy()
-    ref = [structure_forward(*b.structure(k)[:4], 0, hp, W, keep_layers=True) for k in range(b.n_struct)]
+    ref = [structure_forward(*b.structure(k)[:4], 0, hp, stored_weights(W, precision), keep_layers=True)
+           for k in range(b.n_struct)]
     check_energies(E, np.array([o["E"] for o in ref]), np.array([np.abs(o["e"]).sum() for o in ref]),
                    TOL[precision], f"F={F} {precision}")
     if precision == "fp64":

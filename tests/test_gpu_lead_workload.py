@@ -6,16 +6,17 @@ blended by the branch-weighting MLP), the first 65,536-atom batch of its
 stream of 2-500-atom structures (712 structures), one capped graph.  Sampled
 structures, always including the largest (494 atoms) and the smallest, are
 compared with the FP64 oracle: energies with dataset-id heads and with
-blended heads at skip 0.01 in FP64, FP32 and BF16; forces with both head
-modes in FP64 and FP32."""
+blended heads at skip 0.01 in FP64, FP32 and BF16 (BF16 against the oracle
+on the BF16-rounded weights, with the error against the master weights
+reported beside it); forces with both head modes in FP64 and FP32."""
 import sys
 
 import numpy as np
 import pytest
 
 import synth
-from helpers import (TOL, check_blend, check_energies, check_forces, oracle_blend, oracle_energies,
-                     oracle_forces)
+from helpers import (TOL, check_blend, check_forces, check_workload_energies, oracle_blend, oracle_forces,
+                     report_vs_master)
 
 pytestmark = pytest.mark.gpu
 
@@ -58,15 +59,16 @@ _cache = {}
 
 
 def refs(lead, kind):
-    """Oracle results, computed once per module: dataset-id energies, blended
-    energies, dataset-id forces, blended forces."""
+    """Oracle results, computed once per module: blended energies (on the
+    master weights, or on the BF16-rounded weights for "blend_bf16"),
+    dataset-id forces, blended forces."""
     if kind not in _cache:
         b = lead["b"]
         say(f"oracle: {kind}")
-        if kind == "energy":
-            _cache[kind] = oracle_energies(NAME, b, lead["idx_e"])
-        elif kind == "blend":
+        if kind == "blend":
             _cache[kind] = oracle_blend(NAME, b, lead["idx_e"], SKIP)
+        elif kind == "blend_bf16":
+            _cache[kind] = oracle_blend(NAME, b, lead["idx_e"], SKIP, stored="bf16")
         elif kind == "forces":
             _cache[kind] = oracle_forces(NAME, b, lead["idx_f"])
         else:
@@ -80,9 +82,8 @@ def test_lead_energies_dataset_heads(lead, precision):
     say(f"lead_model energies, dataset-id heads, {precision}")
     E = rt.forward(lead["m"], g, precision, dataset_id=lead["inp"]["dataset_id"]).cpu().numpy()
     assert np.all(np.isfinite(E))
-    Er, Ar = refs(lead, "energy")
     idx = lead["idx_e"]
-    check_energies(E[idx], Er, Ar, TOL[precision], f"lead_model {precision}")
+    check_workload_energies(E[idx], NAME, b, idx, precision, f"lead_model {precision}")
 
 
 @pytest.mark.parametrize("precision", ["fp64", "fp32", "bf16"])
@@ -94,7 +95,13 @@ def test_lead_energies_blended(lead, precision):
     E = rt.forward_blend(lead["m"], g, precision, skip=SKIP, weights=w).cpu().numpy()
     w = w.cpu().numpy()
     assert np.all(np.isfinite(E))
-    check_blend(E, w, refs(lead, "blend"), lead["idx_e"], SKIP, precision, f"lead_model blended {precision}")
+    idx = lead["idx_e"]
+    ref = refs(lead, "blend_bf16" if precision == "bf16" else "blend")
+    check_blend(E, w, ref, idx, SKIP, precision, f"lead_model blended {precision}")
+    if precision == "bf16":
+        m = refs(lead, "blend")
+        report_vs_master(E[idx], np.array([o["E"] for o in m]), np.array([np.abs(o["e"]).sum() for o in m]),
+                         np.array([o["E"] for o in ref]), TOL[precision], f"lead_model blended {precision}")
 
 
 @pytest.mark.parametrize("precision", ["fp64", "fp32"])
