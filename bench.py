@@ -220,6 +220,124 @@ def stream_batches(name: str, n: int):
         return list(ex.map(_gen_batch, [(name, s, c) for s, c in ranges]))
 
 
+METRIC_TRAIN = "PaiNN FP64 training structures/s on 1 MI355X (energy+force MAE loss, AdamW)"
+
+
+def adamw_bytes(n_params: int) -> float:
+    """HBM bytes of one AdamW update: weights, both moments read and written,
+    the gradient read (8-byte values)."""
+    return n_params * 8.0 * 7
+
+
+def bench_train(args):
+    """Training steps of the lead model's shape (Table 5: batch of 25
+    structures per GPU, MAE on energies and forces with force weight 94.8,
+    AdamW at 6.34e-4, FP64): each step builds the capped graph of the next 25
+    structures of the stream and runs painn_trainer_step on synthetic
+    reference energies and forces."""
+    import numpy as np
+    import torch
+    import synth
+    from paper_2604_15380_amd import Runtime, painn_profile_enable, painn_profile_read
+    from paper_2604_15380_amd import binding as Bd
+    name = "lead_model"
+    per = 25
+    hp, W = synth.workload_weights(name)
+    hp.blend_dims = None
+    W = {k: v for k, v in W.items() if not k.startswith("blend")}
+    K, Wu = args.steps, args.warmup
+    log(f"generating {K + Wu} batches of {per} {name} structures")
+    rng = np.random.default_rng(7)
+    batches = [synth.make_batch(name, per * k, per) for k in range(K + Wu)]
+    refs = [(rng.standard_normal(b.n_struct) * 2.0, rng.standard_normal((b.n_atoms, 3)) * 0.5) for b in batches]
+    rt = Runtime(0)
+    model = rt.load_model(synth.weight_file_bytes(hp, W))
+    tr = Bd.painn_trainer_create(rt.ctx, model.handle, None)
+    n_params = Bd.painn_trainer_params(rt.ctx, tr)
+    inputs = [rt.upload_batch(b) for b in batches]
+    er = [torch.as_tensor(e, device=rt.device) for e, _ in refs]
+    fr = [torch.as_tensor(np.ascontiguousarray(f), device=rt.device) for _, f in refs]
+    loss = torch.zeros(3, dtype=torch.float64, device=rt.device)
+    graph = rt.build_graph(inputs[0], hp.cutoff, max_neighbors=hp.max_neighbors)
+    edges = []
+
+    def step(k):
+        inp = inputs[k]
+        rt.build_graph(inp, hp.cutoff, graph=graph, max_neighbors=hp.max_neighbors)
+        Bd.painn_trainer_step(rt.ctx, tr, graph.handle, inp["dataset_id"].data_ptr(), er[k].data_ptr(),
+                              fr[k].data_ptr(), loss.data_ptr())
+        return graph.n_edges
+
+    for k in range(Wu):
+        step(K + k)
+    torch.cuda.synchronize()
+    painn_profile_read(rt.ctx)
+    painn_profile_enable(rt.ctx, True)
+    log(f"timing {K} training steps")
+    t0 = time.perf_counter()
+    for k in range(K):
+        edges.append(step(k))
+    torch.cuda.synchronize()
+    T = time.perf_counter() - t0
+    painn_profile_enable(rt.ctx, False)
+    prof = painn_profile_read(rt.ctx)
+    last_loss = loss.cpu().numpy().tolist()
+    tot_B = sum(batches[k].n_struct for k in range(K))
+    tot_N = sum(batches[k].n_atoms for k in range(K))
+    value = tot_B / T
+    log(f"{1e3 * T / K:.3f} ms/step, {value:.1f} structures/s, last loss {last_loss}")
+    kernel_ms = {k: round(ms / K, 4) for k, (ms, n) in prof.items()}
+    roofline = None
+    if "train_adamw" in prof:
+        ms, n = prof["train_adamw"]
+        avg = ms / n / 1e3
+        nb = adamw_bytes(n_params)
+        roofline = dict(kernel="train_adamw", bound="hbm", achieved=round(nb / avg / 1e9, 1), peak=HBM_PEAK_GBS,
+                        unit="GB/s", frac=round(nb / avg / 1e9 / HBM_PEAK_GBS, 4), traffic=None,
+                        avg_launch_ms=round(avg * 1e3, 4), launches=n, algorithmic_hbm_bytes_per_launch=nb,
+                        note="the optimizer update; the gradient passes are FP64 vector-ALU kernels "
+                             "without an algorithmic flop count")
+    cpu = None
+    if not args.no_cpu_baseline:
+        log("timing the CPU oracle baseline (one training-step gradient)")
+        os.environ.setdefault("OMP_NUM_THREADS", "1")
+        sys.path.insert(0, os.path.join(ROOT, "tests"))
+        import helpers
+        affinity = len(os.sched_getaffinity(0))
+        workers = max(1, min(affinity, CPU_SHARE, per))
+        b = batches[0]
+        t1 = time.perf_counter()
+        helpers.oracle_train_grad(hp, name, b, refs[0][0], refs[0][1], 94.8, workers=workers)
+        dt = time.perf_counter() - t1
+        cpu = dict(value=b.n_struct / dt, unit="structures/s", cores=workers, kind="oracle",
+                   sample=f"one training-step gradient of the first {b.n_struct}-structure batch ({b.n_atoms} "
+                          f"atoms): oracle forces, then the complex-step loss gradient, in a pool of {workers} "
+                          f"single-threaded processes, {dt:.1f} s wall",
+                   os_cpu_count=os.cpu_count(), affinity_cores=affinity, worker_cap=CPU_SHARE,
+                   blas=blas_name(), wall_s=round(dt, 2))
+    res = {
+        "metric": METRIC_TRAIN, "value": round(value, 2), "unit": "structures/s", "n_gpus": 1, "steps": K,
+        "warmup": Wu, "ms_per_step": round(1e3 * T / K, 4), "higher_is_better": True, "scaling": "weak",
+        "vs_baseline": None, "dtype": "f64", "data": "synthetic",
+        "config": {"workload": f"{name} training, {per} structures per step, {K} distinct batches",
+                   "n_struct": tot_B, "n_atoms": tot_N, "n_edges": int(sum(edges)), "F": hp.F, "layers": hp.L,
+                   "rbf": hp.K, "rbf_type": "bessel", "cutoff": hp.cutoff, "max_neighbors": hp.max_neighbors,
+                   "heads": hp.n_heads, "precision": "fp64", "loss": "MAE(E) + 94.8 MAE(F)",
+                   "optimizer": "AdamW lr 6.34e-4, betas (0.9, 0.999), eps 1e-8, weight decay 0.01",
+                   "n_params": n_params,
+                   "weights": f"random, dense ~ N(0, 1/fan_in), radial filter x {synth.FILTER_GAIN:g}"},
+        "kernel_ms_per_step": kernel_ms,
+        "last_loss": last_loss,
+        "roofline": roofline,
+        "cpu_baseline": cpu,
+    }
+    print(json.dumps(res), flush=True)
+    Bd.painn_trainer_free(tr)
+    graph.free()
+    model.free()
+    rt.close()
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -242,6 +360,8 @@ def main():
                          "--forces, else 768)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-profile", action="store_true", help="time without per-kernel events")
+    ap.add_argument("--train", action="store_true",
+                    help="time training steps (lead model shape, 25 structures per step, FP64)")
     ap.add_argument("--copy-probe", type=int, default=0, metavar="MIB",
                     help="only run one device-to-device copy of MIB MiB (HBM counter calibration)")
     args = ap.parse_args()
@@ -250,6 +370,9 @@ def main():
               "into independent batches per GPU, see the design notes)", file=sys.stderr)
         sys.exit(2)
 
+    if args.train:
+        bench_train(args)
+        return
     import numpy as np
     import torch
     if args.copy_probe:

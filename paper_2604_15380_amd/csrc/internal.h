@@ -126,7 +126,8 @@ struct PrecModel {      // the model cast and packed for one precision
 enum KernelClass {
   KC_GRAPH_PREP, KC_GRAPH_COUNT, KC_GRAPH_SCAN, KC_GRAPH_FILL, KC_EMBED, KC_PHI,
   KC_EDGE_PREP, KC_MESSAGE, KC_UPDATE, KC_HEADS, KC_ENERGY, KC_EXPORT,
-  KC_TRANSPOSE, KC_BWD_HEADS, KC_BWD_UPDATE, KC_BWD_MESSAGE, KC_BWD_PHI, KC_FORCE, KC_COUNT
+  KC_TRANSPOSE, KC_BWD_HEADS, KC_BWD_UPDATE, KC_BWD_MESSAGE, KC_BWD_PHI, KC_FORCE,
+  KC_TRAIN_REAL, KC_TRAIN_TANGENT, KC_TRAIN_ADAMW, KC_COUNT
 };
 struct Profiler;
 // Record the start (begin = true) or end of a kernel of class `kc` on `s`;

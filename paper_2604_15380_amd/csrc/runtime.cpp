@@ -309,7 +309,8 @@ static const char* kc_name(int kc) {
   static const char* names[KC_COUNT] = {"graph_prep", "graph_count", "graph_scan", "graph_fill",
                                         "embed", "phi", "edge_prep", "message", "update", "heads",
                                         "energy", "export", "transpose", "bwd_heads", "bwd_update",
-                                        "bwd_message", "bwd_phi", "force"};
+                                        "bwd_message", "bwd_phi", "force", "train_real", "train_tangent",
+                                        "train_adamw"};
   return names[kc];
 }
 

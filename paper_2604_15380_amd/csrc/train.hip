@@ -93,6 +93,8 @@ template <class S> __device__ inline S dsilu(S x) {
 
 constexpr int TB = 256;
 inline unsigned blocks(size_t n, int t = TB) { return (unsigned)((n + t - 1) / t); }
+// most row chunks of one weight-gradient reduction (k_tr_wgrad)
+constexpr int WG_CHUNKS = 32;
 
 // ---- dense layers ------------------------------------------------------------
 // Y[r][o] = sum_k X[r][k] W(o, k) (+ b[o] on the value part) (+ ADD[r][o]),
@@ -150,16 +152,21 @@ __global__ void __launch_bounds__(256) k_tr_dense(int rows, const int32_t* __res
     }
 }
 
-// Weight gradient G[o][k] = part( sum_r sc[r] A[r][o] B[r][k] ) over rows
-// [lo, hi) in increasing order (sc may be null: 1).  Every (o, k) is written,
-// zero for an empty row range.
+// Weight gradient over rows [lo, hi): G[o][k] = part( sum_r sc[r] A[r][o] B[r][k] )
+// for k < din, and with a bias the column k = din, where B is taken as 1:
+// Gb[o] = part( sum_r sc[r] A[r][o] ) (sc may be null: 1).  The rows are cut
+// into gridDim.z chunks of `rch`; chunk z writes its partial sums to
+// Pz[z][o][kb] (kb < din + 1), and k_tr_wgrad_sum adds the chunks in order,
+// so the result does not depend on scheduling.
 template <class S>
 __global__ void __launch_bounds__(256) k_tr_wgrad(int rows, const int32_t* __restrict__ range, int dout, int din,
-                                                  const S* __restrict__ A, int lda, const S* __restrict__ Bm,
-                                                  int ldb, const S* __restrict__ sc, double* __restrict__ G) {
+                                                  int dinb, int rch, const S* __restrict__ A, int lda,
+                                                  const S* __restrict__ Bm, int ldb, const S* __restrict__ sc,
+                                                  double* __restrict__ Pz) {
   __shared__ S As[32][33];
   __shared__ S Bs[32][33];
-  const int lo = range ? range[0] : 0, hi = range ? range[1] : rows;
+  const int lo0 = range ? range[0] : 0, hi0 = range ? range[1] : rows;
+  const int lo = lo0 + blockIdx.z * rch, hi = min(hi0, lo + rch);
   const int k0 = blockIdx.x * 32, o0 = blockIdx.y * 32;
   const int tx = threadIdx.x & 15, ty = threadIdx.x >> 4;
   S acc[2][2];
@@ -172,7 +179,7 @@ __global__ void __launch_bounds__(256) k_tr_wgrad(int rows, const int32_t* __res
       S a = (r < hi && o < dout) ? A[(size_t)r * lda + o] : cst<S>(0.0);
       if (sc && r < hi) a = a * sc[r];
       As[rr][cc] = a;
-      Bs[rr][cc] = (r < hi && k < din) ? Bm[(size_t)r * ldb + k] : cst<S>(0.0);
+      Bs[rr][cc] = (r < hi && k < din) ? Bm[(size_t)r * ldb + k] : (r < hi && k == din) ? cst<S>(1.0) : cst<S>(0.0);
     }
     __syncthreads();
 #pragma unroll 8
@@ -186,23 +193,25 @@ __global__ void __launch_bounds__(256) k_tr_wgrad(int rows, const int32_t* __res
     }
     __syncthreads();
   }
+  double* P = Pz + (size_t)blockIdx.z * dout * dinb;
   for (int i = 0; i < 2; ++i)
     for (int j = 0; j < 2; ++j) {
       const int o = o0 + 2 * ty + i, k = k0 + 2 * tx + j;
-      if (o < dout && k < din) G[(size_t)o * din + k] = part(acc[i][j]);
+      if (o < dout && k < dinb) P[(size_t)o * dinb + k] = part(acc[i][j]);
     }
 }
 
-// Bias gradient Gb[o] = part( sum_r sc[r] A[r][o] ), rows in increasing order.
-template <class S>
-__global__ void k_tr_colsum(int rows, const int32_t* __restrict__ range, int dout, const S* __restrict__ A, int lda,
-                            const S* __restrict__ sc, double* __restrict__ Gb) {
-  const int o = blockIdx.x * TB + threadIdx.x;
-  if (o >= dout) return;
-  const int lo = range ? range[0] : 0, hi = range ? range[1] : rows;
-  S acc = cst<S>(0.0);
-  for (int r = lo; r < hi; ++r) acc += sc ? A[(size_t)r * lda + o] * sc[r] : A[(size_t)r * lda + o];
-  Gb[o] = part(acc);
+// G[o][k] = sum over the chunks z (in order) of Pz[z][o][k], k < din; the
+// bias column k = din (when dinb > din) into Gb[o].
+__global__ void k_tr_wgrad_sum(int nz, int dout, int din, int dinb, const double* __restrict__ Pz,
+                               double* __restrict__ G, double* __restrict__ Gb) {
+  const size_t idx = (size_t)blockIdx.x * TB + threadIdx.x;
+  if (idx >= (size_t)dout * dinb) return;
+  const int o = (int)(idx / dinb), k = (int)(idx % dinb);
+  double acc = 0.0;
+  for (int z = 0; z < nz; ++z) acc += Pz[(size_t)z * dout * dinb + idx];
+  if (k < din) G[(size_t)o * din + k] = acc;
+  else Gb[o] = acc;
 }
 
 // Y[r][o] *= silu'(Z[r][o]) for rows [lo, hi), width n (row strides ld).
@@ -742,6 +751,7 @@ struct TrWs {
   void *gs, *gv, *gs2, *gv2, *gh, *ga, *gaa, *gin, *gU, *gV, *ga1, *gw, *gx1, *gx2;
   // loss
   double *E, *Fo, *c, *dpos, *lossbuf;
+  double* wsum;   // partial sums of the weight-gradient reductions
 };
 
 constexpr size_t DS = sizeof(double) * 2;   // bytes per element, sized for Dual
@@ -825,6 +835,23 @@ size_t carve(TrWs* w, char* base, const Hyper& hp, int N, long long E, int B) {
   w->c = (double*)take(B, 8);
   w->dpos = (double*)take(3 * n, 8);
   w->lossbuf = (double*)take(4, 8);
+  // partial-sum scratch: the most row chunks times the widest layer (with
+  // its bias column)
+  size_t widest = 0;
+  auto wid = [&](size_t x) { widest = x > widest ? x : widest; };
+  wid(3 * F * (F + 1));
+  wid(F * (2 * F + 1));
+  wid(3 * F * (K + 1));
+  size_t din = F;
+  for (int d : hp.shared_dims) { wid((size_t)d * (din + 1)); din = d; }
+  {
+    size_t di = din;
+    for (int d : hp.branch_dims) { wid((size_t)d * (di + 1)); di = d; }
+  }
+  const long long rmax = (long long)3 * N > (long long)E ? (long long)3 * N : (long long)E;
+  long long nzmax = (rmax + 255) / 256;
+  nzmax = nzmax < 1 ? 1 : nzmax > WG_CHUNKS ? WG_CHUNKS : nzmax;
+  w->wsum = (double*)take((size_t)nzmax * widest, 8);
   return off;
 }
 
@@ -853,12 +880,26 @@ void dense_t(hipStream_t st, const double* th, int rows, const int32_t* range, i
                                                          add, ldadd, nullptr, GX, ldgx);
 }
 
+// Row chunks of a weight-gradient reduction over `rows` rows: at most
+// WG_CHUNKS, of at least 256 rows each.
+inline int wg_chunks(long long rows) {
+  const long long n = (rows + 255) / 256;
+  return n < 1 ? 1 : n > WG_CHUNKS ? WG_CHUNKS : (int)n;
+}
+
+// Weight (and bias) gradient of a layer stored [dout, din] at wofs (bias at
+// *bofs), reducing over the rows [lo, hi) of A and B (range on the device, or
+// all `rows`); `rows` bounds the row count used to cut the chunks.
 template <class S>
-void wgrad(hipStream_t st, double* G, int rows, const int32_t* range, int dout, int din, const S* A, int lda,
-           const S* Bm, int ldb, size_t wofs, const size_t* bofs, const S* sc = nullptr) {
-  k_tr_wgrad<S><<<dim3((unsigned)((din + 31) / 32), (unsigned)((dout + 31) / 32)), 256, 0, st>>>(
-      rows, range, dout, din, A, lda, Bm, ldb, sc, G + wofs);
-  if (bofs) k_tr_colsum<S><<<blocks(dout), TB, 0, st>>>(rows, range, dout, A, lda, sc, G + *bofs);
+void wgrad(hipStream_t st, double* G, double* scratch, int rows, const int32_t* range, int dout, int din,
+           const S* A, int lda, const S* Bm, int ldb, size_t wofs, const size_t* bofs, const S* sc = nullptr) {
+  const int dinb = din + (bofs ? 1 : 0);
+  const int nz = wg_chunks(rows);
+  const int rch = (rows + nz - 1) / nz;
+  k_tr_wgrad<S><<<dim3((unsigned)((dinb + 31) / 32), (unsigned)((dout + 31) / 32), (unsigned)nz), 256, 0, st>>>(
+      rows, range, dout, din, dinb, rch < 1 ? 1 : rch, A, lda, Bm, ldb, sc, scratch);
+  k_tr_wgrad_sum<<<blocks((size_t)dout * dinb), TB, 0, st>>>(nz, dout, din, dinb, scratch, G + wofs,
+                                                            bofs ? G + *bofs : nullptr);
 }
 
 // One pass.  Real (S = double): E, F into w.E, w.Fo.  Tangent (S = Dual, with
@@ -946,7 +987,7 @@ hipError_t run_pass(hipStream_t st, painn_trainer* tr, const painn_graph* g, con
     const int dout = hp.branch_dims[m], din = m > 0 ? hp.branch_dims[m - 1] : dy;
     const S* xin = m > 0 ? (const S*)w.bry[m - 1] : (const S*)w.yg;
     for (int h = 0; h < H; ++h) {
-      if (!REAL) wgrad<S>(st, G, N, w.hstart + h, dout, din, gcur, dout, xin, din, L.branch_w[h][m], &L.branch_b[h][m]);
+      if (!REAL) wgrad<S>(st, G, w.wsum, N, w.hstart + h, dout, din, gcur, dout, xin, din, L.branch_w[h][m], &L.branch_b[h][m]);
       dense_t<S>(st, th, N, w.hstart + h, dout, din, gcur, dout, L.branch_w[h][m], gnext, din);
     }
     if (m > 0)
@@ -968,7 +1009,7 @@ hipError_t run_pass(hipStream_t st, painn_trainer* tr, const painn_graph* g, con
     const int dout = hp.shared_dims[m], din = m > 0 ? hp.shared_dims[m - 1] : F;
     const S* xin = m > 0 ? (const S*)w.shy[m - 1] : (const S*)w.sL;
     k_tr_mul_dsilu<S><<<blocks((size_t)N * dout), TB, 0, st>>>(N, nullptr, dout, gcur, dout, (const S*)w.shz[m], dout);
-    if (!REAL) wgrad<S>(st, G, N, nullptr, dout, din, gcur, dout, xin, din, L.shared_w[m], &L.shared_b[m]);
+    if (!REAL) wgrad<S>(st, G, w.wsum, N, nullptr, dout, din, gcur, dout, xin, din, L.shared_w[m], &L.shared_b[m]);
     dense_t<S>(st, th, N, nullptr, dout, din, gcur, dout, L.shared_w[m], gnext, din);
     S* t = gcur;
     gcur = gnext;
@@ -990,16 +1031,16 @@ hipError_t run_pass(hipStream_t st, painn_trainer* tr, const painn_graph* g, con
     // update block: (gs, gv) at s', v' -> (gs2, gv2) at s_mid, v_mid
     k_tr_upd_bwd1<S><<<blocks((size_t)N * F), TB, 0, st>>>(N, F, gs, gv, (S*)w.U[l], (S*)w.V[l], (S*)w.a[l],
                                                            (S*)w.ga, (S*)w.gU, (S*)w.gV);
-    if (!REAL) wgrad<S>(st, G, N, nullptr, F3, F, (S*)w.ga, F3, (S*)w.aa[l], F, a[A_UPD_W2], &a[A_UPD_B2]);
+    if (!REAL) wgrad<S>(st, G, w.wsum, N, nullptr, F3, F, (S*)w.ga, F3, (S*)w.aa[l], F, a[A_UPD_W2], &a[A_UPD_B2]);
     dense_t<S>(st, th, N, nullptr, F3, F, (S*)w.ga, F3, a[A_UPD_W2], (S*)w.gaa, F);
     k_tr_mul_dsilu<S><<<blocks((size_t)N * F), TB, 0, st>>>(N, nullptr, F, (S*)w.gaa, F, (S*)w.za[l], F);
-    if (!REAL) wgrad<S>(st, G, N, nullptr, F, 2 * F, (S*)w.gaa, F, (S*)w.xin[l], 2 * F, a[A_UPD_W1], &a[A_UPD_B1]);
+    if (!REAL) wgrad<S>(st, G, w.wsum, N, nullptr, F, 2 * F, (S*)w.gaa, F, (S*)w.xin[l], 2 * F, a[A_UPD_W1], &a[A_UPD_B1]);
     dense_t<S>(st, th, N, nullptr, F, 2 * F, (S*)w.gaa, F, a[A_UPD_W1], (S*)w.gin, 2 * F);
     k_tr_upd_bwd2<S><<<blocks((size_t)N * F), TB, 0, st>>>(N, F, (S*)w.gin, (S*)w.xin[l], (S*)w.V[l], gs,
                                                            (S*)w.gV, gs2);
     if (!REAL) {
-      wgrad<S>(st, G, 3 * N, nullptr, F, F, (S*)w.gU, F, (S*)w.vmid[l], F, a[A_U], nullptr);
-      wgrad<S>(st, G, 3 * N, nullptr, F, F, (S*)w.gV, F, (S*)w.vmid[l], F, a[A_V], nullptr);
+      wgrad<S>(st, G, w.wsum, 3 * N, nullptr, F, F, (S*)w.gU, F, (S*)w.vmid[l], F, a[A_U], nullptr);
+      wgrad<S>(st, G, w.wsum, 3 * N, nullptr, F, F, (S*)w.gV, F, (S*)w.vmid[l], F, a[A_V], nullptr);
     }
     dense_t<S>(st, th, 3 * N, nullptr, F, F, (S*)w.gU, F, a[A_U], gv2, F, gv, F);
     dense_t<S>(st, th, 3 * N, nullptr, F, F, (S*)w.gV, F, a[A_V], gv2, F, gv2, F);
@@ -1018,14 +1059,14 @@ hipError_t run_pass(hipStream_t st, painn_trainer* tr, const painn_graph* g, con
                                                                w.dfc, (const double*)gv2, (const double*)w.gw, w.gd,
                                                                w.grh);
       } else {
-        wgrad<S>(st, G, (int)E, nullptr, F3, K, (S*)w.gw, F3, (S*)w.basis, K, a[A_FILT_W], &a[A_FILT_B], (S*)w.fc);
+        wgrad<S>(st, G, w.wsum, (int)E, nullptr, F3, K, (S*)w.gw, F3, (S*)w.basis, K, a[A_FILT_W], &a[A_FILT_B], (S*)w.fc);
       }
     }
     // phi: dE/dh -> dE/ds before the message (its residual gs2 added)
-    if (!REAL) wgrad<S>(st, G, N, nullptr, F3, F, (S*)w.gh, F3, (S*)w.a1[l], F, a[A_PHI_W2], &a[A_PHI_B2]);
+    if (!REAL) wgrad<S>(st, G, w.wsum, N, nullptr, F3, F, (S*)w.gh, F3, (S*)w.a1[l], F, a[A_PHI_W2], &a[A_PHI_B2]);
     dense_t<S>(st, th, N, nullptr, F3, F, (S*)w.gh, F3, a[A_PHI_W2], (S*)w.ga1, F);
     k_tr_mul_dsilu<S><<<blocks((size_t)N * F), TB, 0, st>>>(N, nullptr, F, (S*)w.ga1, F, (S*)w.z1[l], F);
-    if (!REAL) wgrad<S>(st, G, N, nullptr, F, F, (S*)w.ga1, F, (S*)w.s[l], F, a[A_PHI_W1], &a[A_PHI_B1]);
+    if (!REAL) wgrad<S>(st, G, w.wsum, N, nullptr, F, F, (S*)w.ga1, F, (S*)w.s[l], F, a[A_PHI_W1], &a[A_PHI_B1]);
     dense_t<S>(st, th, N, nullptr, F, F, (S*)w.ga1, F, a[A_PHI_W1], gs, F, gs2, F);
   }
   if (!REAL)
@@ -1191,19 +1232,25 @@ painn_status painn_trainer_step(painn_trainer* tr, const painn_graph* g, const i
   (void)hipGetLastError();
   const size_t P = tr->lay.total;
   k_tr_zero_d<<<blocks(P), TB, 0, st>>>(P, tr->grad);
+  prof_mark(ctx->prof, st, KC_TRAIN_REAL, true);
   hipError_t e = run_pass<double>(st, tr, g, dataset_id, w, nullptr);
   if (e == hipSuccess && g->B > 0) {
     k_tr_loss<<<1, 256, 0, st>>>(g->B, g->N, tr->cfg.force_weight, w.E, energy_ref, w.Fo, force_ref, w.bad, w.c,
                                  w.dpos, loss ? loss : w.lossbuf);
     e = hipGetLastError();
   }
+  prof_mark(ctx->prof, st, KC_TRAIN_REAL, false);
+  prof_mark(ctx->prof, st, KC_TRAIN_TANGENT, true);
   if (e == hipSuccess) e = run_pass<Dual>(st, tr, g, dataset_id, w, tr->grad);
+  prof_mark(ctx->prof, st, KC_TRAIN_TANGENT, false);
   if (e == hipSuccess) {
     tr->t += 1;
     const painn_train_config& c = tr->cfg;
     const double bc1 = 1.0 - pow(c.beta1, (double)tr->t), bc2 = 1.0 - pow(c.beta2, (double)tr->t);
+    prof_mark(ctx->prof, st, KC_TRAIN_ADAMW, true);
     k_tr_adamw<<<blocks(P), TB, 0, st>>>(P, tr->theta, tr->grad, tr->m1, tr->m2, c.lr, c.beta1, c.beta2, c.eps,
                                         c.weight_decay, bc1, bc2);
+    prof_mark(ctx->prof, st, KC_TRAIN_ADAMW, false);
     e = hipGetLastError();
   }
   if (e != hipSuccess) {

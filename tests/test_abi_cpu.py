@@ -85,5 +85,10 @@ def test_null_handles_without_device():
     assert lib.painn_forward_features(None, None, None, 0, 0, None, None) == E_ARG
     assert lib.painn_forces(None, None, None, None, 0, None, None) == E_ARG
     assert lib.painn_forces_blend(None, None, None, 0, 0.0, None, None, None) == E_ARG
+    assert lib.painn_forward_noalloc(None, None, None, None, 0, None) == E_ARG
+    assert lib.painn_trainer_create(None, None, None, r(out)) == E_ARG
+    assert lib.painn_trainer_step(None, None, None, None, None, None) == E_ARG
+    assert lib.painn_trainer_params(None, r(i64), None, None) == E_ARG
+    assert lib.painn_trainer_free(None) == 0
     assert lib.painn_profile_enable(None, 1) == E_ARG
     assert lib.painn_profile_read(None, 4, names, ms, cnt, r(i32)) == E_ARG
