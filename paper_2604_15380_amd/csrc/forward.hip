@@ -127,6 +127,11 @@ struct MsgArgs {
   void* s;             // s after the message
   void* v_out;
   int v_zero;          // v_in is all zero (the first layer): its terms vanish
+  // filter without its bias column (filt_mma is then the K -> 3F filter and
+  // einfo[3] holds f_c): the epilogue adds f_c b_f, the sender comes from col
+  int nb;
+  const int32_t* col;
+  const void* fbias;   // b_f [3F], accumulation type
 };
 
 constexpr int MSG_RB = 4;   // receivers per workgroup (MSG_RB < 64)
@@ -145,7 +150,7 @@ __device__ __forceinline__ int acc_to_index(double x) { return (int)x; }
 //   r = (x_j - x_i) + (n0 a + n1 b) + n2 c  (FP64),  d = |r|,  rhat = r / d,
 //   f_c = (cos(pi d / r_c) + 1) / 2,  g_k = exp(-gamma (d - k Delta)^2).
 // Edge e's geometry and basis row into g (LDS), its rhat and sender into einfo.
-template <class P>
+template <class P, bool NB>
 __device__ __forceinline__ void edge_row(long long e, int K, int kcols, double rc, int rbf, double gamma,
                                          double delta, const int32_t* __restrict__ recv,
                                          const int32_t* __restrict__ col, const int32_t* __restrict__ shift,
@@ -167,11 +172,14 @@ __device__ __forceinline__ void edge_row(long long e, int K, int kcols, double r
   o[0] = (A)(rx * inv);
   o[1] = (A)(ry * inv);
   o[2] = (A)(rz * inv);
-  o[3] = index_to_acc<A>(j);                     // the sender index, bit-exact
   const A dd = (A)d;
   const A fc = (A)(d < rc ? 0.5 * (cos(d * (3.14159265358979323846 / rc)) + 1.0) : 0.0);
-  // each value once; BF16 also writes its remainder term at K + 1 + k
-  for (int k = 0; k <= K; ++k) {
+  // without the bias column the edge info carries f_c instead of the sender
+  // (which the kernels then read from the CSR)
+  o[3] = NB ? fc : index_to_acc<A>(j);           // the sender index, bit-exact
+  // each value once; BF16 also writes its remainder term at KW + k
+  const int KW = NB ? K : K + 1;                 // columns of one term
+  for (int k = 0; k < KW; ++k) {
     A val = fc;
     if (k < K && rbf == 0) {                     // Gaussian
       const A t = dd - (A)(k * delta);
@@ -181,9 +189,9 @@ __device__ __forceinline__ void edge_row(long long e, int K, int kcols, double r
       val = (sizeof(A) == 8 ? (A)sin((double)arg) : (A)sinf((float)arg)) / dd * fc;
     }
     g[k] = P::st(val);
-    if constexpr (SPLIT) g[K + 1 + k] = P::st(val - P::ld(P::st(val)));
+    if constexpr (SPLIT) g[KW + k] = P::st(val - P::ld(P::st(val)));
   }
-  for (int k = SPLIT ? 2 * (K + 1) : K + 1; k < kcols; ++k) g[k] = P::st(0);
+  for (int k = SPLIT ? 2 * KW : KW; k < kcols; ++k) g[k] = P::st(0);
 }
 
 // A workgroup of EP_THREADS edges builds its rows in LDS (one row per
@@ -192,7 +200,7 @@ __device__ __forceinline__ void edge_row(long long e, int K, int kcols, double r
 // scatter one element per lane per store).
 constexpr int EP_THREADS = 64;   // one wave: <= 35 KiB of LDS at the largest row
 
-template <class P>
+template <class P, bool NB>
 __global__ void __launch_bounds__(EP_THREADS) k_edge_prep(long long E, int K, int kcols, double rc, int rbf,
                                                   double gamma, double delta,
                                                   const int32_t* __restrict__ recv,
@@ -210,7 +218,7 @@ __global__ void __launch_bounds__(EP_THREADS) k_edge_prep(long long E, int K, in
   const long long rows = (E + 16 - e0) < EP_THREADS ? (E + 16 - e0) : EP_THREADS;
   T* g = (T*)ep_smem + (size_t)threadIdx.x * kcols;
   // rows E .. E+15 are zero (read by partial chunks)
-  if (e < E) edge_row<P>(e, K, kcols, rc, rbf, gamma, delta, recv, col, shift, atom_struct, pos, cell, g, einfo);
+  if (e < E) edge_row<P, NB>(e, K, kcols, rc, rbf, gamma, delta, recv, col, shift, atom_struct, pos, cell, g, einfo);
   else if (e < E + 16)
     for (int k = 0; k < kcols; ++k) g[k] = P::st(0);
   __syncthreads();
@@ -899,7 +907,7 @@ constexpr int message_waves() {
   return 12 * KBM * (int)sizeof(typename P::Fr) / 4 > 150 ? 1 : 2;
 }
 
-template <class P, int F, int KBM, bool V0>
+template <class P, int F, int KBM, bool V0, bool NB>
 __global__ void __launch_bounds__(F) __attribute__((amdgpu_waves_per_eu(message_waves<P, KBM>())))
 k_message_lane(MsgArgs a) {
   using T = typename P::T;
@@ -938,6 +946,10 @@ k_message_lane(MsgArgs a) {
         const int ct = part * NFT + 4 * wave + q;
         Bf[q][part][kb] = P::frag(Wf + ((size_t)(ct * KBM + kb) * 64 + lane) * P::KPL);
       }
+  // without the bias column: b_f at this lane's channel, per part
+  const A bs = NB ? ((const A*)a.fbias)[c] : A(0);
+  const A bv = NB ? ((const A*)a.fbias)[F + c] : A(0);
+  const A br = NB ? ((const A*)a.fbias)[2 * F + c] : A(0);
   const T* h = (const T*)a.h;
   const T* vin = (const T*)a.v_in;
   const T* basis = (const T*)a.basis;
@@ -977,18 +989,23 @@ k_message_lane(MsgArgs a) {
   const int E0 = rp(i0), E1 = rp(i1);
   if (E0 == E1) return;
   Fr Gn[KBM];
+  // lane e: edge e of the next chunk's rhat and its sender index (NB: its
+  // f_c in ejn, the sender in jn)
   A exn = 0, eyn = 0, ezn = 0, ejn = 0;
+  int jn = 0;
   auto prefetch = [&](int cc0, int ccnt) {
     const T* gp = basis + (size_t)(cc0 + (lane & 15)) * kcols + (lane >> 4) * P::KPL;
 #pragma unroll
     for (int kb = 0; kb < KBM; ++kb) Gn[kb] = P::frag(gp + kb * P::KC);
     exn = eyn = ezn = ejn = 0;
+    jn = 0;
     if (lane < ccnt) {
       const A* ei = einfo + 4 * (size_t)(cc0 + lane);
       exn = ei[0];
       eyn = ei[1];
       ezn = ei[2];
       ejn = ei[3];
+      if constexpr (NB) jn = a.col[cc0 + lane];
     }
   };
   int c0 = E0;
@@ -1030,8 +1047,10 @@ k_message_lane(MsgArgs a) {
     Fr Ga[KBM];
 #pragma unroll
     for (int kb = 0; kb < KBM; ++kb) Ga[kb] = row_ok ? Gn[kb] : Fr{};
-    // lanes e < cnt hold edge c0 + e: rhat and the sender index
+    // lanes e < cnt hold edge c0 + e: rhat and the sender index (NB: f_c,
+    // and the sender in jc)
     const A ex = exn, ey = eyn, ez = ezn, ej = ejn;
+    const int jc = jn;
     const int cn = c0 + 16;
     const bool more = cn < E1;
     if (more) prefetch(cn, min(16, E1 - cn));
@@ -1043,7 +1062,7 @@ k_message_lane(MsgArgs a) {
     auto gather = [&](int ebase) {
 #pragma unroll
       for (int u = 0; u < EG; ++u) {
-        const int j = acc_to_index(bcast(ej, ebase + u));
+        const int j = NB ? __builtin_amdgcn_readlane(jc, ebase + u) : acc_to_index(bcast(ej, ebase + u));
         const T* hj = h + (size_t)j * 3 * F + c;
         const T* vj = vin + (size_t)j * 3 * F + c;
         gb[0][u] = hj[0];
@@ -1073,7 +1092,10 @@ k_message_lane(MsgArgs a) {
         // stream's end, c0 + e >= E1 >= eb)
         if (c0 + e == eb && eb < E1) next_receiver();
         const A rx = bcast(ex, e), ry = bcast(ey, e), rz = bcast(ez, e);
-        const A ws = ws4[u % 4], wr = wr4[u % 4];
+        // the bias: w = f_c (W_f g + b_f)
+        const A fe = NB ? bcast(ej, e) : A(0);
+        const A ws = NB ? ws4[u % 4] + fe * bs : ws4[u % 4];
+        const A wr = NB ? wr4[u % 4] + fe * br : wr4[u % 4];
         acc_s += P::ld(gb[0][u]) * ws;
         const A pr = P::ld(gb[2][u]) * wr;
         if constexpr (V0) {
@@ -1081,7 +1103,7 @@ k_message_lane(MsgArgs a) {
           acc_v1 += ry * pr;
           acc_v2 += rz * pr;
         } else {
-          const A pv = P::ld(gb[1][u]) * wv4[u % 4];
+          const A pv = P::ld(gb[1][u]) * (NB ? wv4[u % 4] + fe * bv : wv4[u % 4]);
           acc_v0 += P::ld(gb[3][u]) * pv + rx * pr;
           acc_v1 += P::ld(gb[4][u]) * pv + ry * pr;
           acc_v2 += P::ld(gb[5][u]) * pv + rz * pr;
@@ -1142,19 +1164,20 @@ k_message_lane(MsgArgs a) {
   write_out();
 }
 
-template <class P, int F, int KBM>
+template <class P, int F, int KBM, bool NB>
 void launch_message_kbm(hipStream_t st, const MsgArgs& a) {
   if constexpr (sizeof(typename P::T) == 8) {
     // two feature tiles per wave; four above F = 256 (a 768-thread group
     // would leave each wave too few registers)
     constexpr int NW = F > 256 ? F / 64 : F / 32;
     const int blocks = ((a.N + MSG_RB - 1) / MSG_RB + 7) / 8 * 8;   // a multiple of the 8 XCDs
+    static_assert(!NB, "FP64 keeps the filter's bias column");
     if (a.v_zero) k_message<P, F, NW, KBM, true><<<blocks, NW * 64, 0, st>>>(a);
     else k_message<P, F, NW, KBM, false><<<blocks, NW * 64, 0, st>>>(a);
   } else {
     const int blocks = ((a.N + MSG_RB2 - 1) / MSG_RB2 + 7) / 8 * 8;
-    if (a.v_zero) k_message_lane<P, F, KBM, true><<<blocks, F, 0, st>>>(a);
-    else k_message_lane<P, F, KBM, false><<<blocks, F, 0, st>>>(a);
+    if (a.v_zero) k_message_lane<P, F, KBM, true, NB><<<blocks, F, 0, st>>>(a);
+    else k_message_lane<P, F, KBM, false, NB><<<blocks, F, 0, st>>>(a);
   }
 }
 
@@ -1163,20 +1186,44 @@ template <class P, int F>
 hipError_t launch_message(hipStream_t st, const MsgArgs& a) {
   const int nkb = a.filt_mma.din_p / P::KC;
   if constexpr (P::KC == 32) {
-    switch (nkb) {
-      case 1: launch_message_kbm<P, F, 1>(st, a); break;
-      case 2: launch_message_kbm<P, F, 2>(st, a); break;
-      case 3: launch_message_kbm<P, F, 3>(st, a); break;
-      case 5: launch_message_kbm<P, F, 5>(st, a); break;
-      default: return hipErrorInvalidValue;
+    if (a.nb) {
+      switch (nkb) {
+        case 1: launch_message_kbm<P, F, 1, true>(st, a); break;
+        case 2: launch_message_kbm<P, F, 2, true>(st, a); break;
+        case 3: launch_message_kbm<P, F, 3, true>(st, a); break;
+        case 5: launch_message_kbm<P, F, 5, true>(st, a); break;
+        default: return hipErrorInvalidValue;
+      }
+    } else {
+      switch (nkb) {
+        case 1: launch_message_kbm<P, F, 1, false>(st, a); break;
+        case 2: launch_message_kbm<P, F, 2, false>(st, a); break;
+        case 3: launch_message_kbm<P, F, 3, false>(st, a); break;
+        case 5: launch_message_kbm<P, F, 5, false>(st, a); break;
+        default: return hipErrorInvalidValue;
+      }
     }
+  } else if (sizeof(typename P::T) < 8 && a.nb) {
+    if constexpr (sizeof(typename P::T) < 8) {
+      switch (nkb) {
+        case 1: launch_message_kbm<P, F, 1, true>(st, a); break;
+        case 2: launch_message_kbm<P, F, 2, true>(st, a); break;
+        case 5: launch_message_kbm<P, F, 5, true>(st, a); break;
+        case 8: launch_message_kbm<P, F, 8, true>(st, a); break;
+        case 12: launch_message_kbm<P, F, 12, true>(st, a); break;
+        case 17: launch_message_kbm<P, F, 17, true>(st, a); break;
+        default: return hipErrorInvalidValue;
+      }
+    }
+  } else if (a.nb) {
+    return hipErrorInvalidValue;   // FP64 keeps the bias column
   } else {
     switch (nkb) {
-      case 3: launch_message_kbm<P, F, 3>(st, a); break;
-      case 6: launch_message_kbm<P, F, 6>(st, a); break;
-      case 9: launch_message_kbm<P, F, 9>(st, a); break;
-      case 12: launch_message_kbm<P, F, 12>(st, a); break;
-      case 17: launch_message_kbm<P, F, 17>(st, a); break;
+      case 3: launch_message_kbm<P, F, 3, false>(st, a); break;
+      case 6: launch_message_kbm<P, F, 6, false>(st, a); break;
+      case 9: launch_message_kbm<P, F, 9, false>(st, a); break;
+      case 12: launch_message_kbm<P, F, 12, false>(st, a); break;
+      case 17: launch_message_kbm<P, F, 17, false>(st, a); break;
       default: return hipErrorInvalidValue;
     }
   }
@@ -1483,14 +1530,30 @@ hipError_t forward_impl(hipStream_t st, ForwardArgs& fa) {
     prof_mark(fa.prof, st, KC_EMBED, false);
   }
   int cur = 0;
-  const int kcols = pm->layers.empty() ? 0 : pm->layers[0].filt_mma.din_p;
+  // The filter without its bias column (f_c b_f added in the message's
+  // epilogue) where that saves MFMA k-blocks, in FP32 and BF16; a forward
+  // that keeps a save area for the reverse pass uses the layout the reverse
+  // pass reads.  (FP64: measured slower, 16.6 -> 17.0 ms per launch on the
+  // bulk batch although it saves a ninth of the MFMAs: the kernel waits on
+  // its gathers, and the sender index then comes from a second array.)
+  const bool nb = sizeof(T) < 8 && !fa.save && !pm->layers.empty() &&
+                  pm->layers[0].filt_nb.din_p < pm->layers[0].filt_mma.din_p;
+  const int kcols = pm->layers.empty() ? 0 : nb ? pm->layers[0].filt_nb.din_p : pm->layers[0].filt_mma.din_p;
   if (N > 0 && fa.stop_layer >= 0) {
     prof_mark(fa.prof, st, KC_EDGE_PREP, true);
     const double delta = hp.cutoff / (hp.K - 1);
-    k_edge_prep<P><<<(unsigned)((g->E + 16 + EP_THREADS - 1) / EP_THREADS), EP_THREADS,
-                     (size_t)EP_THREADS * kcols * sizeof(T), st>>>(
-        g->E, hp.K, kcols, hp.cutoff, hp.rbf_type, 1.0 / (2.0 * delta * delta), delta, g->recv, g->col, g->shift,
-        g->atom_struct, g->pos, g->cell, (T*)fa.basis, (A*)fa.einfo);
+    const unsigned eg = (unsigned)((g->E + 16 + EP_THREADS - 1) / EP_THREADS);
+    const size_t esm = (size_t)EP_THREADS * kcols * sizeof(T);
+    if (nb)
+      k_edge_prep<P, true><<<eg, EP_THREADS, esm, st>>>(g->E, hp.K, kcols, hp.cutoff, hp.rbf_type,
+                                                        1.0 / (2.0 * delta * delta), delta, g->recv, g->col,
+                                                        g->shift, g->atom_struct, g->pos, g->cell, (T*)fa.basis,
+                                                        (A*)fa.einfo);
+    else
+      k_edge_prep<P, false><<<eg, EP_THREADS, esm, st>>>(g->E, hp.K, kcols, hp.cutoff, hp.rbf_type,
+                                                         1.0 / (2.0 * delta * delta), delta, g->recv, g->col,
+                                                         g->shift, g->atom_struct, g->pos, g->cell, (T*)fa.basis,
+                                                         (A*)fa.einfo);
     prof_mark(fa.prof, st, KC_EDGE_PREP, false);
   }
   for (int l = 0; l <= fa.stop_layer && N > 0; ++l) {
@@ -1502,7 +1565,10 @@ hipError_t forward_impl(hipStream_t st, ForwardArgs& fa) {
     ma.row_ptr = g->row_ptr;
     ma.basis = fa.basis;
     ma.einfo = fa.einfo;
-    ma.filt_mma = Ld.filt_mma;
+    ma.filt_mma = nb ? Ld.filt_nb : Ld.filt_mma;
+    ma.nb = nb;
+    ma.col = g->col;
+    ma.fbias = Ld.filt_nb.b;
     ma.h = fa.save ? sv.H(l) : h;
     ma.v_in = fa.save ? sv.V(l) : v[cur];
     ma.s_in = fa.save ? sv.S(l) : s;

@@ -81,6 +81,22 @@ inline int filter_kblocks(int din, int prec) {
   return -1;
 }
 
+// The same for the filter without its bias column (K inputs, or 2K for
+// BF16): the forward adds f_c b_f in the message's epilogue instead.  Counts
+// the message kernel is compiled for in that form; -1 if too large.
+inline int filter_kblocks_nb(int din, int prec) {
+  const int kc = prec == PAINN_BF16 ? 32 : 4;
+  const int need = (din + kc - 1) / kc;
+  static const int f[] = {1, 2, 5, 8, 12, 17};
+  static const int b[] = {1, 2, 3, 5};
+  if (prec == PAINN_BF16) {
+    for (int x : b) if (need <= x) return x;
+  } else {
+    for (int x : f) if (need <= x) return x;
+  }
+  return -1;
+}
+
 struct DenseDev {       // one packed layer on the device
   void* w = nullptr;    // packed weights, storage type of the precision
   void* b = nullptr;    // bias [pad32(dout)], accumulation type (zero padded)
@@ -95,6 +111,11 @@ struct LayerDev {       // one interaction layer
                         // input column K is the bias (multiplied by f_c), din
                         // padded to a multiple of the MFMA K step only; BF16
                         // stores it twice along K (input [hi | lo] terms)
+  DenseDev filt_nb;     // the filter K -> 3F without the bias column (BF16:
+                        // 2K, twice along K), its bias b_f in .b; used by the
+                        // FP32 / BF16 energy forward when it needs fewer MFMA
+                        // k-blocks (the reverse pass keeps filt_mma; FP64
+                        // does not pack it)
   // transposed weights for the reverse pass (no bias; built on the first
   // forces call): phi1^T F -> F, phi2^T 3F -> F, [U^T | V^T] 2F -> F,
   // upd1^T F -> 2F, upd2^T 3F -> F

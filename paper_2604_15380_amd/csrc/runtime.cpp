@@ -107,14 +107,18 @@ hipError_t upload(PrecModel* pm, const std::vector<unsigned char>& host, void** 
 }
 
 // Pack W [dout][din] (FP64, row-major) and bias [dout] (or null) for `prec`.
-// din_p: pad32(din), or filter_kblocks(din, prec) MFMA k-blocks for the radial filter.
+// din_p: pad32(din) for a dense layer (filter = 0); MFMA k-blocks of the
+// radial filter: filter_kblocks(din, prec) with its bias column (filter = 1),
+// filter_kblocks_nb(din, prec) without (filter = 2).
 hipError_t pack_dense(PrecModel* pm, int prec, const double* W, const double* b, int dout,
-                      int din, DenseDev* out, bool filter = false) {
+                      int din, DenseDev* out, int filter = 0) {
   // k per MFMA step: BF16 32; FP32 dense layers 16 (4 chained 4-k
   // instructions fed by one 16-byte load per lane), the FP32 filter and FP64 4
   const int KC = prec == PAINN_BF16 ? 32 : prec == PAINN_FP32 && !filter ? 16 : 4;
   const int KPL = KC / 4;
-  const int dout_p = pad32(dout), din_p = filter ? filter_kblocks(din, prec) * KC : pad32(din);
+  const int dout_p = pad32(dout);
+  const int din_p = filter == 1 ? filter_kblocks(din, prec) * KC
+                  : filter == 2 ? filter_kblocks_nb(din, prec) * KC : pad32(din);
   const int nkb = din_p / KC, nct = dout_p / 16;
   std::vector<unsigned char> wh((size_t)dout_p * din_p * elem_bytes(prec), 0);
   for (int ct = 0; ct < nct; ++ct)
@@ -189,9 +193,22 @@ painn_status build_prec(painn_model* m, int prec, PrecModel** out) {
         for (int c = 0; c < 3 * F; ++c)
           for (int k = 0; k < 2 * (K + 1); ++k)
             w2[(size_t)c * 2 * (K + 1) + k] = wf[(size_t)c * (K + 1) + k % (K + 1)];
-        e = pack_dense(pm, prec, w2.data(), nullptr, 3 * F, 2 * (K + 1), &L.filt_mma, true);
+        e = pack_dense(pm, prec, w2.data(), nullptr, 3 * F, 2 * (K + 1), &L.filt_mma, 1);
       } else {
-        e = pack_dense(pm, prec, wf.data(), nullptr, 3 * F, K + 1, &L.filt_mma, true);
+        e = pack_dense(pm, prec, wf.data(), nullptr, 3 * F, K + 1, &L.filt_mma, 1);
+      }
+    }
+    if (e == hipSuccess && prec != PAINN_FP64) {
+      // the filter without its bias column, the bias kept beside it (FP32
+      // and BF16 forwards; FP64 keeps the bias column)
+      const double* Wf = arr(base + A_FILT_W);
+      if (prec == PAINN_BF16) {
+        std::vector<double> w2((size_t)3 * F * 2 * K);
+        for (int c = 0; c < 3 * F; ++c)
+          for (int k = 0; k < 2 * K; ++k) w2[(size_t)c * 2 * K + k] = Wf[(size_t)c * K + k % K];
+        e = pack_dense(pm, prec, w2.data(), arr(base + A_FILT_B), 3 * F, 2 * K, &L.filt_nb, 2);
+      } else {
+        e = pack_dense(pm, prec, Wf, arr(base + A_FILT_B), 3 * F, K, &L.filt_nb, 2);
       }
     }
   }
@@ -722,7 +739,8 @@ static painn_status run_forward(painn_ctx* ctx, const painn_model* model, const 
     painn_status st = build_prec(m, prec, &m->prec[prec]);
     if (st != PAINN_OK) return st;
   }
-  const int kcols = m->prec[prec]->layers[0].filt_mma.din_p;
+  const LayerDev& L0 = m->prec[prec]->layers[0];
+  const int kcols = L0.filt_mma.din_p > L0.filt_nb.din_p ? L0.filt_mma.din_p : L0.filt_nb.din_p;
   size_t need = forward_workspace_bytes(prec, g->N, g->E, m->hp.F, kcols, g->B, m->hp.n_heads,
                                        m->hp.n_species, blend);
   void* ws = ctx->ws;

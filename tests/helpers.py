@@ -281,3 +281,23 @@ def oracle_train_grad(hp, W, batch, E_ref, F_ref, force_weight: float, workers: 
                 grad[name] += val
     loss_E, loss_F = float(np.mean(np.abs(rE))), float(np.mean(np.abs(rF)))
     return dict(loss=loss_E + force_weight * loss_F, loss_E=loss_E, loss_F=loss_F, E=E, F=Fo, grad=grad)
+
+
+# The forces pass runs the forward with the filter's bias on the matrix
+# cores (the layout its reverse pass reads); the energy-only forward adds it
+# in the message epilogue where that saves MFMA work.  Both are checked
+# against the oracle; against each other they agree to the precision's
+# rounding (relative to the batch's largest energy).
+SAME_ENERGY_TOL = {"fp64": 1e-12, "fp32": 1e-5}
+
+
+def assert_same_energies(E_a, E_b, precision: str, label: str = ""):
+    E_a = np.asarray(E_a, dtype=np.float64)
+    E_b = np.asarray(E_b, dtype=np.float64)
+    assert E_a.shape == E_b.shape, label
+    if E_a.size == 0:
+        return
+    assert np.all(np.isfinite(E_a)) and np.all(np.isfinite(E_b)), label
+    scale = max(1.0, float(np.abs(E_b).max()))
+    err = float(np.abs(E_a - E_b).max())
+    assert err <= SAME_ENERGY_TOL[precision] * scale, f"{label}: forces-pass energies differ by {err:.3e}"

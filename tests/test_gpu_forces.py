@@ -8,6 +8,7 @@ import numpy as np
 import pytest
 
 import synth
+from helpers import assert_same_energies
 from oracle.forces import structure_forces
 from oracle.painn import RBF_BESSEL
 
@@ -65,7 +66,7 @@ def run_case(rt, hp, W, b, precision, label, cap=0, ds=False):
     E0 = rt.forward(m, g, precision, dataset_id=dsid)
     torch.cuda.synchronize()
     E, Fo, E0 = E.cpu().numpy(), Fo.cpu().numpy(), E0.cpu().numpy()
-    assert np.array_equal(E, E0), f"{label}: energies of the forces pass differ from the forward's"
+    assert_same_energies(E, E0, precision, label)
     ref = oracle(b, hp, W)
     check_forces(Fo, b, ref, list(range(b.n_struct)), FORCE_TOL[precision], label)
     g.free()
@@ -235,7 +236,7 @@ def test_blended_heads(rt, precision, skip):
     E, Fo = rt.forces_blend(m, g, precision, skip=skip)
     E0 = rt.forward_blend(m, g, precision, skip=skip)
     torch.cuda.synchronize()
-    assert np.array_equal(E.cpu().numpy(), E0.cpu().numpy())
+    assert_same_energies(E.cpu().numpy(), E0.cpu().numpy(), precision)
     Fo = Fo.cpu().numpy()
     ref = [structure_forces_blend(*b.structure(k)[:4], hp, W, skip=skip) for k in range(b.n_struct)]
     if skip > 0:
@@ -299,7 +300,7 @@ def test_edge_cases(rt):
             E, Fo = rt.forces(m, g, precision)
             E0 = rt.forward(m, g, precision)
             torch.cuda.synchronize()
-            assert np.array_equal(E.cpu().numpy(), E0.cpu().numpy()), label
+            assert_same_energies(E.cpu().numpy(), E0.cpu().numpy(), precision, label)
             Fo = Fo.cpu().numpy()
             assert Fo.shape == (b.n_atoms, 3)
             if label == "no edges":
@@ -390,7 +391,7 @@ def test_full_size_molecules_sampled(rt):
     E0 = rt.forward(m, g, "fp32")
     torch.cuda.synchronize()
     Fo = Fo.cpu().numpy()
-    assert np.array_equal(E.cpu().numpy(), E0.cpu().numpy())
+    assert_same_energies(E.cpu().numpy(), E0.cpu().numpy(), "fp32")
     assert np.all(np.isfinite(Fo))
     idx = [int(k) for k in np.random.default_rng(5).choice(b.n_struct, 12, replace=False)] + [0, b.n_struct - 1]
     ref = oracle(b, hp, W, idx)
@@ -418,7 +419,7 @@ def test_past_256_scan_blocks(rt):
     E0 = rt.forward(m, g, "fp32")
     torch.cuda.synchronize()
     E, Fo, E0 = E.cpu().numpy(), Fo.cpu().numpy(), E0.cpu().numpy()
-    assert np.array_equal(E, E0)
+    assert_same_energies(E, E0, "fp32")
     first_past = int(np.searchsorted(b.struct_ptr, 262144))
     rng = np.random.default_rng(6)
     idx = [0, first_past - 1, first_past, b.n_struct - 1] + \

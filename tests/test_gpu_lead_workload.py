@@ -15,8 +15,8 @@ import numpy as np
 import pytest
 
 import synth
-from helpers import (TOL, check_blend, check_forces, check_workload_energies, oracle_blend, oracle_forces,
-                     report_vs_master)
+from helpers import (TOL, assert_same_energies, check_blend, check_forces, check_workload_energies, oracle_blend,
+                     oracle_forces, report_vs_master)
 
 pytestmark = pytest.mark.gpu
 
@@ -110,7 +110,7 @@ def test_lead_forces_dataset_heads(lead, precision):
     say(f"lead_model forces, dataset-id heads, {precision}")
     E, Fo = rt.forces(lead["m"], g, precision, dataset_id=lead["inp"]["dataset_id"])
     E0 = rt.forward(lead["m"], g, precision, dataset_id=lead["inp"]["dataset_id"])
-    assert np.array_equal(E.cpu().numpy(), E0.cpu().numpy())
+    assert_same_energies(E.cpu().numpy(), E0.cpu().numpy(), precision)
     Fo = Fo.cpu().numpy()
     check_forces(Fo, b, refs(lead, "forces"), lead["idx_f"], FORCE_TOL[precision], f"lead_model forces {precision}")
 
@@ -121,7 +121,7 @@ def test_lead_forces_blended(lead, precision):
     say(f"lead_model forces, blended heads skip {SKIP}, {precision}")
     E, Fo = rt.forces_blend(lead["m"], g, precision, skip=SKIP)
     E0 = rt.forward_blend(lead["m"], g, precision, skip=SKIP)
-    assert np.array_equal(E.cpu().numpy(), E0.cpu().numpy())
+    assert_same_energies(E.cpu().numpy(), E0.cpu().numpy(), precision)
     Fo = Fo.cpu().numpy()
     ref = refs(lead, "blend_forces")
     # a head whose weight lies within rounding of the threshold may be kept
