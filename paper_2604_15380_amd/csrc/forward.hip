@@ -230,138 +230,257 @@ __global__ void __launch_bounds__(EP_THREADS) k_edge_prep(long long E, int K, in
 }
 
 
-// Per layer.  A workgroup owns MSG_RB consecutive receivers and NW waves;
-// wave w owns the feature tiles ft = w + NW q (q < FTW) and keeps their
-// filter B fragments (s, v and r column tiles) in registers.  Waves never
-// synchronise: each streams its receivers' 16-edge chunks (basis fragments ->
-// MFMA -> sender gathers), with the accumulator layout (row = edge, col =
-// channel) letting every lane combine the filter with the gathered sender
-// features of its edges directly; a receiver's per-lane partial sums are
-// reduced across the four row groups of the wavefront at its last edge.
-template <class P, int F, int NW, int KBM, bool V0>
-__global__ void __launch_bounds__(NW * 64) k_message(MsgArgs a) {
+// FP64, per layer.  SPLIT workgroups share MSG_RB64 consecutive receivers,
+// each owning NGW groups of 32 channels; the workgroup's NS streams of NGW
+// waves split those receivers, wave w of a stream owning channel group w.
+// The group's filter columns are staged in LDS once per workgroup (shared
+// by its streams), which leaves each wave the registers for two waves per
+// SIMD: one wave's loads and arithmetic then run under the other's MFMAs.
+//
+// A wave's channel group is two MFMA column tiles whose columns interleave:
+// column c of tile q is channel 32 g + 2 c + q, so a lane's two accumulator
+// columns are adjacent channels and each sender gather is one 16-byte load
+// per lane.  The order of the filter input is permuted alike on both MFMA
+// operands: k-blocks 2p and 2p + 1 take inputs 8p + 2 kk and 8p + 2 kk + 1
+// at k-group kk, so one 16-byte load per lane fetches two basis fragments
+// (and one 16-byte LDS read two filter fragments).  The vector-memory
+// address unit costs about the same per instruction at 8 and 16 bytes per
+// lane: halving the instructions is what lets the MFMAs keep busy.
+//
+// A stream's receivers form one sequence of 16-edge chunks (a receiver
+// without edges still takes one, empty, so that its row is written).  Per
+// chunk the wave issues the sender gathers, prefetches the next chunk's
+// edge info (and basis rows), runs the filter MFMAs and combines their
+// accumulators (row = edge, col = channel) with the gathered features
+// directly; a receiver's per-lane partial sums are reduced across the four
+// row groups of the wavefront after its last chunk.
+constexpr int MSG_RB64 = 32;   // receivers per workgroup
+
+template <int KBM>
+__device__ __forceinline__ int msg_kcol(int kb, int kk) {
+  return kb < KBM / 2 * 2 ? 8 * (kb >> 1) + 2 * kk + (kb & 1) : 4 * kb + kk;
+}
+
+// channel groups per workgroup: the LDS holds 6 (KBM + 1) / 2 KiB per group
+template <int F, int KBM>
+constexpr int msg64_groups() {
+  return F / 32 < (KBM <= 12 ? 4 : 2) ? F / 32 : (KBM <= 12 ? 4 : 2);
+}
+
+template <class P, int F, int NGW, int NS, int KBM, bool V0>
+__global__ void __launch_bounds__(64 * NGW * NS, 2) k_message(MsgArgs a) {
   using T = typename P::T;
-  using A = typename P::A;
   using C = typename P::C;
-  using Fr = typename P::Fr;
-  constexpr int NFT = F / 16, FTW = NFT / NW;
-  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-  constexpr int nkb = KBM;            // the filter input is padded to KBM k-blocks
-  constexpr int kcols = KBM * P::KC;
-  const T* Wf = (const T*)a.filt_mma.w;
-  Fr Bf[FTW][3][KBM];
+  static_assert(sizeof(T) == 8, "the paired-channel layout is the FP64 kernel's");
+  typedef double d2 __attribute__((ext_vector_type(2)));
+  constexpr int NG = F / 32, SPLIT = NG / NGW, NP = (KBM + 1) / 2, RBS = MSG_RB64 / NS;
+  static_assert(NG % NGW == 0 && MSG_RB64 % NS == 0 && RBS < 64, "workgroup shape");
+  constexpr int kcols = KBM * P::KC;  // the filter input is padded to KBM k-blocks
+  // [group][q][part][k-block pair][lane]: the two B fragments of a pair
+  __shared__ d2 bsh[NGW * 6 * NP * 64];
+  const int lane = threadIdx.x & 63, wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  const int col = lane & 15, kk = lane >> 4, gw = wave % NGW, st = wave / NGW;
+  // Workgroups are dealt round-robin to the 8 XCDs.  Renumber them so each
+  // XCD walks one contiguous range of receivers: a molecule's receivers then
+  // share one L2, which serves the repeated gathers of its sender rows, and
+  // the SPLIT workgroups of a receiver block read its basis from one L2.
+  const int per_xcd = gridDim.x / 8;
+  const int lb = (blockIdx.x % 8) * per_xcd + blockIdx.x / 8;
+  const int ib = (lb / SPLIT) * MSG_RB64, half = lb % SPLIT;
+  if (ib >= a.N) return;                       // the whole workgroup
+  {
+    const T* Wf = (const T*)a.filt_mma.w;
+    for (int x = threadIdx.x; x < NGW * 6 * NP * 64; x += NGW * NS * 64) {
+      const int l = x & 63, p = (x >> 6) % NP, qp = (x >> 6) / NP % 6, g = (x >> 6) / NP / 6;
+      // packed fragment element (row n, input k): tile n / 16, k-block k / 4,
+      // lane n % 16 + 16 (k % 4)
+      const int n = qp % 3 * F + 32 * (half * NGW + g) + 2 * (l & 15) + qp / 3;
+      double v[2];
 #pragma unroll
-  for (int q = 0; q < FTW; ++q)
-#pragma unroll
-    for (int part = 0; part < 3; ++part)
-#pragma unroll
-      for (int kb = 0; kb < KBM; ++kb) {
-        const int ct = part * NFT + wave + NW * q;
-        Bf[q][part][kb] = P::frag(Wf + ((size_t)(ct * nkb + kb) * 64 + lane) * P::KPL);
+      for (int hh = 0; hh < 2; ++hh) {
+        const int kb = 2 * p + hh, k = msg_kcol<KBM>(kb, l >> 4);
+        v[hh] = kb < KBM ? Wf[((size_t)((n >> 4) * KBM + (k >> 2)) * 64 + (n & 15) + 16 * (k & 3))] : 0.0;
       }
+      bsh[x] = d2{v[0], v[1]};
+    }
+  }
+  __syncthreads();                             // (the only barrier)
+  const int i0 = ib + st * RBS;
+  if (i0 >= a.N) return;
+  const int i1 = min(a.N, i0 + RBS);
+  const int ch = 32 * (half * NGW + gw) + 2 * col;   // this lane's channels ch, ch + 1
+  const d2* bw = bsh + gw * 6 * NP * 64 + lane;
   const T* h = (const T*)a.h;
   const T* vin = (const T*)a.v_in;
   const T* basis = (const T*)a.basis;
-  const A* einfo = (const A*)a.einfo;
+  const double* einfo = (const double*)a.einfo;
   const T* sin = (const T*)a.s_in;
   T* s = (T*)a.s;
   T* vout = (T*)a.v_out;
-  // Workgroups are dealt round-robin to the 8 XCDs.  Renumber them so each
-  // XCD walks one contiguous range of receivers: a molecule's receivers then
-  // share one L2, which serves the repeated gathers of its sender rows.
-  const int per_xcd = gridDim.x / 8;
-  const int lb = (blockIdx.x % 8) * per_xcd + blockIdx.x / 8;
-  const int i0 = lb * MSG_RB;
-  if (i0 >= a.N) return;
-  const int i1 = min(a.N, i0 + MSG_RB);
-  // the block's row_ptr slice, one load per lane, read back by shuffles
+  // the stream's row_ptr slice, one load per lane, read back by readlane
   const int rp_lane = a.row_ptr[i0 + min(lane, i1 - i0)];
-  for (int i = i0; i < i1; ++i) {
-    const int ea = __shfl(rp_lane, i - i0);
-    const int eb = __shfl(rp_lane, i - i0 + 1);
-    // operands of the final update, fetched early
-    T s_old[FTW], v_old[FTW][3];
-    const size_t ib = (size_t)i * 3 * F;
-#pragma unroll
-    for (int q = 0; q < FTW; ++q) {
-      const int f = (wave + NW * q) * 16 + (lane & 15);
-      s_old[q] = sin[(size_t)i * F + f];
-      // (the first layer's v is zero and need not be stored)
-      v_old[q][0] = V0 ? P::st(0) : vin[ib + f];
-      v_old[q][1] = V0 ? P::st(0) : vin[ib + F + f];
-      v_old[q][2] = V0 ? P::st(0) : vin[ib + 2 * F + f];
+  auto rp = [&](int i) { return __builtin_amdgcn_readlane(rp_lane, i - i0); };
+  int nck = 0;                                 // chunks of the sequence
+  for (int i = i0; i < i1; ++i) nck += max(1, (rp(i + 1) - rp(i) + 15) / 16);
+
+  struct Ck { int i, c0, cnt; bool last; };   // wave-uniform
+  auto make = [&](int i, int c0) {
+    const int eb = rp(i + 1);
+    return Ck{i, c0, max(0, min(16, eb - c0)), c0 + 16 >= eb};
+  };
+  auto next = [&](const Ck& c) {
+    return !c.last ? make(c.i, c.c0 + 16) : c.i + 1 < i1 ? make(c.i + 1, rp(c.i + 1)) : c;
+  };
+  // Edge info: lane l holds chunk row l % 16's (rhat_x, rhat_y) and
+  // (rhat_z, sender); a lane's accumulator rows read theirs by shuffles.
+  // Rows past the chunk's end take its first edge (a valid sender) and get a
+  // zero basis row, hence a zero filter, so no gather needs a branch; an
+  // empty chunk gathers the receiver's own row.
+  struct Raw { d2 xy, ze; };
+  auto load_raw = [&](const Ck& c, Raw& o) {
+    if (c.cnt > 0) {
+      const double* ei = einfo + 4 * (size_t)(c.c0 + (col < c.cnt ? col : 0));
+      o.xy = *(const d2*)ei;
+      o.ze = *(const d2*)(ei + 2);
+    } else {
+      o.xy = d2{0.0, 0.0};
+      o.ze = d2{0.0, (double)c.i};
     }
-    A acc_s[FTW], acc_v[FTW][3];
+  };
+  auto load_ga = [&](const Ck& c, T (&Ga)[KBM]) {
+    const T* gp = basis + (size_t)(c.c0 + col) * kcols;   // rows E .. E + 15 exist
 #pragma unroll
-    for (int q = 0; q < FTW; ++q) acc_s[q] = acc_v[q][0] = acc_v[q][1] = acc_v[q][2] = 0;
-    for (int c0 = ea; c0 < eb; c0 += 16) {
-      const int cnt = min(16, eb - c0);
-      const T* gp = basis + (size_t)(c0 + (lane & 15)) * kcols + (lane >> 4) * P::KPL;
-      Fr Ga[KBM];
+    for (int p = 0; p < KBM / 2; ++p) {
+      const d2 t = *(const d2*)(gp + 8 * p + 2 * kk);
+      Ga[2 * p] = t.x;
+      Ga[2 * p + 1] = t.y;
+    }
+    if constexpr (KBM & 1) Ga[KBM - 1] = gp[4 * (KBM - 1) + kk];
+  };
+  auto filter = [&](const Ck& c, const T (&Ga)[KBM], C (&w)[2][3]) {
+    T ga[KBM];
 #pragma unroll
-      for (int kb = 0; kb < KBM; ++kb) Ga[kb] = P::frag(gp + kb * P::KC);
-      A rh[4][3];
-      int jj[4];
+    for (int kb = 0; kb < KBM; ++kb) ga[kb] = col < c.cnt ? Ga[kb] : 0.0;
 #pragma unroll
-      for (int ii = 0; ii < 4; ++ii) {
-        const int row = P::row(lane, ii);
-        const A* ei = einfo + 4 * (size_t)(c0 + (row < cnt ? row : 0));
-        rh[ii][0] = ei[0];
-        rh[ii][1] = ei[1];
-        rh[ii][2] = ei[2];
-        jj[ii] = acc_to_index(ei[3]);
-      }
+    for (int q = 0; q < 2; ++q)
 #pragma unroll
-      for (int q = 0; q < FTW; ++q) {
-        const int f = (wave + NW * q) * 16 + (lane & 15);
-        C w[3];
+      for (int part = 0; part < 3; ++part)
+        for (int r = 0; r < 4; ++r) w[q][part][r] = 0;
+#pragma unroll
+    for (int p = 0; p < NP; ++p)
+#pragma unroll
+      for (int q = 0; q < 2; ++q)
 #pragma unroll
         for (int part = 0; part < 3; ++part) {
-          for (int r = 0; r < 4; ++r) w[part][r] = 0;
           // with v_j = 0 the v part of the filter meets nothing
           if (V0 && part == 1) continue;
-#pragma unroll
-          for (int kb = 0; kb < KBM; ++kb) w[part] = P::mfma(Ga[kb], Bf[q][part][kb], w[part]);
+          const d2 b = bw[((q * 3 + part) * NP + p) * 64];
+          w[q][part] = P::mfma(ga[2 * p], b.x, w[q][part]);
+          if (2 * p + 1 < KBM) w[q][part] = P::mfma(ga[2 * p + 1], b.y, w[q][part]);
         }
+    // Keep the LDS reads just ahead of their MFMAs (hoisted all at once
+    // they would take 30 register pairs): a pair's reads go out between the
+    // previous pair's MFMAs.
+    constexpr int NBR = V0 ? 4 : 6;            // B reads (and MFMAs) per k-block
+    __builtin_amdgcn_sched_group_barrier(0x100, NBR, 0);
 #pragma unroll
-        for (int ii = 0; ii < 4; ++ii) {
-          if (P::row(lane, ii) < cnt) {
-            const size_t hb = (size_t)jj[ii] * 3 * F;
-            const A hs = P::ld(h[hb + f]), hr = P::ld(h[hb + 2 * F + f]);
-            acc_s[q] += hs * w[0][ii];
-            const A pr = hr * w[2][ii];
-            if constexpr (V0) {
-              acc_v[q][0] += rh[ii][0] * pr;
-              acc_v[q][1] += rh[ii][1] * pr;
-              acc_v[q][2] += rh[ii][2] * pr;
-            } else {
-              const A hv = P::ld(h[hb + F + f]);
-              const A v0 = P::ld(vin[hb + f]), v1 = P::ld(vin[hb + F + f]), v2 = P::ld(vin[hb + 2 * F + f]);
-              const A pv = hv * w[1][ii];
-              acc_v[q][0] += v0 * pv + rh[ii][0] * pr;
-              acc_v[q][1] += v1 * pv + rh[ii][1] * pr;
-              acc_v[q][2] += v2 * pv + rh[ii][2] * pr;
-            }
-          }
+    for (int p = 0; p < KBM / 2; ++p) {
+      __builtin_amdgcn_sched_group_barrier(0x008, NBR, 0);
+      if (p + 1 < NP) __builtin_amdgcn_sched_group_barrier(0x100, NBR, 0);
+      __builtin_amdgcn_sched_group_barrier(0x008, NBR, 0);
+    }
+    if constexpr (KBM & 1) __builtin_amdgcn_sched_group_barrier(0x008, NBR, 0);
+  };
+  struct Gath { d2 hs[4], hr[4], hv[4], vj[4][3]; };
+  auto gather = [&](const Raw& in, Gath& G) {
+    const int j_lane = acc_to_index(in.ze.y);
+#pragma unroll
+    for (int ii = 0; ii < 4; ++ii) {
+      const size_t hb = (size_t)__shfl(j_lane, P::row(lane, ii)) * 3 * F + ch;
+      G.hs[ii] = *(const d2*)(h + hb);
+      G.hr[ii] = *(const d2*)(h + hb + 2 * F);
+      if constexpr (!V0) {
+        G.hv[ii] = *(const d2*)(h + hb + F);
+#pragma unroll
+        for (int c = 0; c < 3; ++c) G.vj[ii][c] = *(const d2*)(vin + hb + c * F);
+      }
+    }
+  };
+  double acc_s[2] = {0.0, 0.0}, acc_v[2][3] = {{0.0, 0.0, 0.0}, {0.0, 0.0, 0.0}};
+  auto consume = [&](const C (&w)[2][3], const Gath& G, const Raw& in) {
+#pragma unroll
+    for (int ii = 0; ii < 4; ++ii) {
+      const int src = P::row(lane, ii);
+      const double rh[3] = {__shfl(in.xy.x, src), __shfl(in.xy.y, src), __shfl(in.ze.x, src)};
+#pragma unroll
+      for (int q = 0; q < 2; ++q) {
+        acc_s[q] += G.hs[ii][q] * w[q][0][ii];
+        const double pr = G.hr[ii][q] * w[q][2][ii];
+        if constexpr (V0) {
+#pragma unroll
+          for (int c = 0; c < 3; ++c) acc_v[q][c] += rh[c] * pr;
+        } else {
+          const double pv = G.hv[ii][q] * w[q][1][ii];
+#pragma unroll
+          for (int c = 0; c < 3; ++c) acc_v[q][c] += G.vj[ii][c][q] * pv + rh[c] * pr;
         }
       }
     }
+  };
+  auto finish = [&](int i) {
+    const size_t iv = (size_t)i * 3 * F + ch;
+    const d2 s_old = *(const d2*)(sin + (size_t)i * F + ch);
+    d2 v_old[3];
 #pragma unroll
-    for (int q = 0; q < FTW; ++q) {
-      for (int o = 16; o < 64; o *= 2) {
-        acc_s[q] += __shfl_xor(acc_s[q], o);
-        acc_v[q][0] += __shfl_xor(acc_v[q][0], o);
-        acc_v[q][1] += __shfl_xor(acc_v[q][1], o);
-        acc_v[q][2] += __shfl_xor(acc_v[q][2], o);
+    for (int c = 0; c < 3; ++c) v_old[c] = V0 ? d2{0.0, 0.0} : *(const d2*)(vin + iv + c * F);
+#pragma unroll
+    for (int q = 0; q < 2; ++q)
+      for (int off = 16; off < 64; off *= 2) {
+        acc_s[q] += __shfl_xor(acc_s[q], off);
+#pragma unroll
+        for (int c = 0; c < 3; ++c) acc_v[q][c] += __shfl_xor(acc_v[q][c], off);
       }
-      if (lane < 16) {
-        const int f = (wave + NW * q) * 16 + lane;
-        s[(size_t)i * F + f] = P::st(P::ld(s_old[q]) + acc_s[q]);
-        vout[ib + f] = P::st(P::ld(v_old[q][0]) + acc_v[q][0]);
-        vout[ib + F + f] = P::st(P::ld(v_old[q][1]) + acc_v[q][1]);
-        vout[ib + 2 * F + f] = P::st(P::ld(v_old[q][2]) + acc_v[q][2]);
-      }
+    if (lane < 16) {
+      *(d2*)(s + (size_t)i * F + ch) = d2{s_old.x + acc_s[0], s_old.y + acc_s[1]};
+#pragma unroll
+      for (int c = 0; c < 3; ++c)
+        *(d2*)(vout + iv + c * F) = d2{v_old[c].x + acc_v[0][c], v_old[c].y + acc_v[1][c]};
     }
+#pragma unroll
+    for (int q = 0; q < 2; ++q) acc_s[q] = acc_v[q][0] = acc_v[q][1] = acc_v[q][2] = 0.0;
+  };
+
+  // Chunk k: its gathers go out first, then the next chunk's edge info, then
+  // its filter MFMAs and the combination.  Two chunks alternate the roles of
+  // the prefetch buffers, so nothing is copied.
+  Gath G;
+  C w[2][3];
+  // (the next chunk's basis rows are prefetched too where the registers
+  // allow it, up to 9 k-blocks)
+  constexpr bool PF = KBM <= 9;
+  auto step = [&](int k, Ck& cur, const Raw& in_cur, Raw& in_nxt, T (&ga_cur)[KBM], T (&ga_nxt)[KBM]) {
+    gather(in_cur, G);
+    if constexpr (!PF) load_ga(cur, ga_cur);
+    const Ck nx = next(cur);
+    const bool more = k + 1 < nck;
+    if (more) {
+      load_raw(nx, in_nxt);
+      if constexpr (PF) load_ga(nx, ga_nxt);
+    }
+    filter(cur, ga_cur, w);
+    consume(w, G, in_cur);
+    if (cur.last) finish(cur.i);
+    cur = nx;
+    return more;
+  };
+  Ck c = make(i0, rp(i0));
+  Raw inA, inB;
+  T gaA[KBM], gaB[KBM];
+  load_raw(c, inA);
+  if constexpr (PF) load_ga(c, gaA);
+  for (int k = 0;; k += 2) {
+    if (!step(k, c, inA, inB, gaA, gaB)) break;
+    if (!step(k + 1, c, inB, inA, gaB, gaA)) break;
   }
 }
 
@@ -1167,13 +1286,12 @@ k_message_lane(MsgArgs a) {
 template <class P, int F, int KBM, bool NB>
 void launch_message_kbm(hipStream_t st, const MsgArgs& a) {
   if constexpr (sizeof(typename P::T) == 8) {
-    // two feature tiles per wave; four above F = 256 (a 768-thread group
-    // would leave each wave too few registers)
-    constexpr int NW = F > 256 ? F / 64 : F / 32;
-    const int blocks = ((a.N + MSG_RB - 1) / MSG_RB + 7) / 8 * 8;   // a multiple of the 8 XCDs
+    // eight waves per workgroup: NGW channel groups times NS streams
+    constexpr int NGW = msg64_groups<F, KBM>(), NS = 8 / NGW, SPLIT = F / 32 / NGW;
+    const int blocks = ((a.N + MSG_RB64 - 1) / MSG_RB64 * SPLIT + 7) / 8 * 8;   // a multiple of the 8 XCDs
     static_assert(!NB, "FP64 keeps the filter's bias column");
-    if (a.v_zero) k_message<P, F, NW, KBM, true><<<blocks, NW * 64, 0, st>>>(a);
-    else k_message<P, F, NW, KBM, false><<<blocks, NW * 64, 0, st>>>(a);
+    if (a.v_zero) k_message<P, F, NGW, NS, KBM, true><<<blocks, 512, 0, st>>>(a);
+    else k_message<P, F, NGW, NS, KBM, false><<<blocks, 512, 0, st>>>(a);
   } else {
     const int blocks = ((a.N + MSG_RB2 - 1) / MSG_RB2 + 7) / 8 * 8;
     if (a.v_zero) k_message_lane<P, F, KBM, true, NB><<<blocks, F, 0, st>>>(a);
