@@ -256,6 +256,22 @@ __global__ void __launch_bounds__(EP_THREADS) k_edge_prep(long long E, int K, in
 // row groups of the wavefront after its last chunk.
 constexpr int MSG_RB64 = 32;   // receivers per workgroup
 
+// Lane n of each 16-lane row, broadcast to its row (DPP row_newbcast).
+__device__ __forceinline__ int row_bcast(int x, int n) {
+  // (every lane reads a lane of its own row, so no lane keeps an old value)
+  switch (n) {
+    case 0: return __builtin_amdgcn_mov_dpp(x, 0x150, 0xf, 0xf, true);
+    case 1: return __builtin_amdgcn_mov_dpp(x, 0x151, 0xf, 0xf, true);
+    case 2: return __builtin_amdgcn_mov_dpp(x, 0x152, 0xf, 0xf, true);
+    default: return __builtin_amdgcn_mov_dpp(x, 0x153, 0xf, 0xf, true);
+  }
+}
+__device__ __forceinline__ double row_bcast(double x, int n) {
+  const long long v = __double_as_longlong(x);
+  const int lo = row_bcast((int)(v & 0xffffffff), n), hi = row_bcast((int)(v >> 32), n);
+  return __longlong_as_double(((long long)hi << 32) | (unsigned int)lo);
+}
+
 template <int KBM>
 __device__ __forceinline__ int msg_kcol(int kb, int kk) {
   return kb < KBM / 2 * 2 ? 8 * (kb >> 1) + 2 * kk + (kb & 1) : 4 * kb + kk;
@@ -331,15 +347,17 @@ __global__ void __launch_bounds__(64 * NGW * NS, 2) k_message(MsgArgs a) {
   auto next = [&](const Ck& c) {
     return !c.last ? make(c.i, c.c0 + 16) : c.i + 1 < i1 ? make(c.i + 1, rp(c.i + 1)) : c;
   };
-  // Edge info: lane l holds chunk row l % 16's (rhat_x, rhat_y) and
-  // (rhat_z, sender); a lane's accumulator rows read theirs by shuffles.
-  // Rows past the chunk's end take its first edge (a valid sender) and get a
-  // zero basis row, hence a zero filter, so no gather needs a branch; an
-  // empty chunk gathers the receiver's own row.
+  // Edge info: lane 16 kk + j holds (rhat_x, rhat_y) and (rhat_z, sender)
+  // of chunk row 4 (j % 4) + kk, so accumulator row 4 ii + kk of every lane
+  // of the 16-lane row kk sits in that row's lane ii, and a DPP row
+  // broadcast hands it over.  Rows past the chunk's end take its first edge
+  // (a valid sender) and get a zero basis row, hence a zero filter, so no
+  // gather needs a branch; an empty chunk gathers the receiver's own row.
   struct Raw { d2 xy, ze; };
   auto load_raw = [&](const Ck& c, Raw& o) {
     if (c.cnt > 0) {
-      const double* ei = einfo + 4 * (size_t)(c.c0 + (col < c.cnt ? col : 0));
+      const int row = 4 * (col & 3) + kk;
+      const double* ei = einfo + 4 * (size_t)(c.c0 + (row < c.cnt ? row : 0));
       o.xy = *(const d2*)ei;
       o.ze = *(const d2*)(ei + 2);
     } else {
@@ -396,7 +414,7 @@ __global__ void __launch_bounds__(64 * NGW * NS, 2) k_message(MsgArgs a) {
     const int j_lane = acc_to_index(in.ze.y);
 #pragma unroll
     for (int ii = 0; ii < 4; ++ii) {
-      const size_t hb = (size_t)__shfl(j_lane, P::row(lane, ii)) * 3 * F + ch;
+      const size_t hb = (size_t)row_bcast(j_lane, ii) * 3 * F + ch;
       G.hs[ii] = *(const d2*)(h + hb);
       G.hr[ii] = *(const d2*)(h + hb + 2 * F);
       if constexpr (!V0) {
@@ -410,20 +428,18 @@ __global__ void __launch_bounds__(64 * NGW * NS, 2) k_message(MsgArgs a) {
   auto consume = [&](const C (&w)[2][3], const Gath& G, const Raw& in) {
 #pragma unroll
     for (int ii = 0; ii < 4; ++ii) {
-      const int src = P::row(lane, ii);
-      const double rh[3] = {__shfl(in.xy.x, src), __shfl(in.xy.y, src), __shfl(in.ze.x, src)};
+      const double rh[3] = {row_bcast(in.xy.x, ii), row_bcast(in.xy.y, ii), row_bcast(in.ze.x, ii)};
 #pragma unroll
       for (int q = 0; q < 2; ++q) {
-        acc_s[q] += G.hs[ii][q] * w[q][0][ii];
+        acc_s[q] = fma(G.hs[ii][q], w[q][0][ii], acc_s[q]);
         const double pr = G.hr[ii][q] * w[q][2][ii];
-        if constexpr (V0) {
-#pragma unroll
-          for (int c = 0; c < 3; ++c) acc_v[q][c] += rh[c] * pr;
-        } else {
+        if constexpr (!V0) {
           const double pv = G.hv[ii][q] * w[q][1][ii];
 #pragma unroll
-          for (int c = 0; c < 3; ++c) acc_v[q][c] += G.vj[ii][c][q] * pv + rh[c] * pr;
+          for (int c = 0; c < 3; ++c) acc_v[q][c] = fma(G.vj[ii][c][q], pv, acc_v[q][c]);
         }
+#pragma unroll
+        for (int c = 0; c < 3; ++c) acc_v[q][c] = fma(rh[c], pr, acc_v[q][c]);
       }
     }
   };
