@@ -109,46 +109,6 @@ __global__ void __launch_bounds__(256) k_t_scan_apply(int N, int32_t* __restrict
     }
 }
 
-__global__ void __launch_bounds__(1024) k_t_scan(int N, int32_t* __restrict__ cnt, int32_t* __restrict__ ptr) {
-  constexpr int PER = 4, TILE = 1024 * PER;
-  __shared__ int tile[TILE];
-  __shared__ int part[1024];
-  __shared__ int carry_s;
-  const int t = threadIdx.x;
-  if (t == 0) carry_s = 0;
-  __syncthreads();
-  for (int base = 0; base < N; base += TILE) {
-    for (int k = t; k < TILE; k += 1024) {
-      const int j = base + k;
-      tile[k] = j < N ? cnt[j] : 0;
-      if (j < N) cnt[j] = 0;
-    }
-    __syncthreads();
-    int sum = 0;
-    for (int k = 0; k < PER; ++k) sum += tile[t * PER + k];
-    part[t] = sum;
-    __syncthreads();
-    for (int o = 1; o < 1024; o <<= 1) {
-      const int x = t >= o ? part[t - o] : 0;
-      __syncthreads();
-      part[t] += x;
-      __syncthreads();
-    }
-    int run = carry_s + part[t] - sum;
-    for (int k = 0; k < PER; ++k) {
-      const int c = tile[t * PER + k];
-      tile[t * PER + k] = run;
-      run += c;
-    }
-    __syncthreads();
-    for (int k = t; k < TILE; k += 1024)
-      if (base + k < N) ptr[base + k] = tile[k];
-    if (t == 1023) carry_s += part[1023];
-    __syncthreads();
-  }
-  if (t == 0) ptr[N] = carry_s;
-}
-
 __global__ void __launch_bounds__(256) k_t_fill(long long E, const int32_t* __restrict__ col,
                                                const int32_t* __restrict__ ptr, int32_t* __restrict__ cur,
                                                int32_t* __restrict__ t_edge) {
@@ -159,31 +119,42 @@ __global__ void __launch_bounds__(256) k_t_fill(long long E, const int32_t* __re
 }
 
 // The fill order depends on timing: each sender's edge ids are put in
-// ascending order.  One wave per sender: a segment of up to 256 ids is held
-// in registers (4 per lane) and each id goes to its rank, the number of
-// smaller ids in the segment (the ids are distinct); a longer segment is
-// insertion-sorted by one lane.
+// ascending order.  One wave per sender: a segment of up to 64 KPT ids is
+// held in registers (KPT per lane) and each id goes to its rank, the number
+// of smaller ids in the segment (the ids are distinct), counted by walking
+// the segment's ids 64 at a time through shuffles.  A segment longer than
+// 1,024 ids (more than 16 per lane) is insertion-sorted by one lane.
+template <int KPT>
+__device__ __forceinline__ void t_rank_sort(int32_t* __restrict__ seg, int n, int lane) {
+  int key[KPT], rank[KPT];
+#pragma unroll
+  for (int q = 0; q < KPT; ++q) {
+    key[q] = lane + 64 * q < n ? seg[lane + 64 * q] : 0x7fffffff;
+    rank[q] = 0;
+  }
+#pragma unroll
+  for (int q = 0; q < KPT; ++q) {
+    const int m_end = min(64, n - 64 * q);   // (wave-uniform; <= 0 past the segment)
+    for (int m = 0; m < m_end; ++m) {
+      const int other = __shfl(key[q], m);
+#pragma unroll
+      for (int u = 0; u < KPT; ++u) rank[u] += other < key[u];
+    }
+  }
+#pragma unroll
+  for (int q = 0; q < KPT; ++q)
+    if (lane + 64 * q < n) seg[rank[q]] = key[q];
+}
+
 __global__ void __launch_bounds__(256) k_t_sort(int N, const int32_t* __restrict__ ptr, int32_t* __restrict__ t_edge) {
   const int j = blockIdx.x * 4 + (threadIdx.x >> 6), lane = threadIdx.x & 63;
   if (j >= N) return;
   const int a = ptr[j], n = ptr[j + 1] - a;
   if (n <= 1) return;
   if (n <= 256) {
-    int key[4], rank[4] = {0, 0, 0, 0};
-#pragma unroll
-    for (int q = 0; q < 4; ++q) key[q] = lane + 64 * q < n ? t_edge[a + lane + 64 * q] : 0x7fffffff;
-#pragma unroll
-    for (int q = 0; q < 4; ++q) {
-      const int m_end = min(64, n - 64 * q);
-      for (int m = 0; m < m_end; ++m) {
-        const int other = __shfl(key[q], m);
-#pragma unroll
-        for (int u = 0; u < 4; ++u) rank[u] += other < key[u];
-      }
-    }
-#pragma unroll
-    for (int q = 0; q < 4; ++q)
-      if (lane + 64 * q < n) t_edge[a + rank[q]] = key[q];
+    t_rank_sort<4>(t_edge + a, n, lane);
+  } else if (n <= 1024) {
+    t_rank_sort<16>(t_edge + a, n, lane);
   } else if (lane == 0) {
     for (int x = a + 1; x < a + n; ++x) {
       const int key = t_edge[x];
