@@ -283,7 +283,7 @@ constexpr int msg64_groups() {
   return F / 32 < (KBM <= 12 ? 4 : 2) ? F / 32 : (KBM <= 12 ? 4 : 2);
 }
 
-template <class P, int F, int NGW, int NS, int KBM, bool V0>
+template <class P, int F, int NGW, int NS, int KBM, bool V0, bool NB>
 __global__ void __launch_bounds__(64 * NGW * NS, 2) k_message(MsgArgs a) {
   using T = typename P::T;
   using C = typename P::C;
@@ -292,8 +292,11 @@ __global__ void __launch_bounds__(64 * NGW * NS, 2) k_message(MsgArgs a) {
   constexpr int NG = F / 32, SPLIT = NG / NGW, NP = (KBM + 1) / 2, RBS = MSG_RB64 / NS;
   static_assert(NG % NGW == 0 && MSG_RB64 % NS == 0 && RBS < 64, "workgroup shape");
   constexpr int kcols = KBM * P::KC;  // the filter input is padded to KBM k-blocks
-  // [group][q][part][k-block pair][lane]: the two B fragments of a pair
+  // [group][q][part][k-block pair][lane]: the two B fragments of a pair;
+  // without the bias column, b_f [group][part][lane % 16] at the lane's two
+  // channels
   __shared__ d2 bsh[NGW * 6 * NP * 64];
+  __shared__ d2 bias_sh[NB ? NGW * 3 * 16 : 1];
   const int lane = threadIdx.x & 63, wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   const int col = lane & 15, kk = lane >> 4, gw = wave % NGW, st = wave / NGW;
   // Workgroups are dealt round-robin to the 8 XCDs.  Renumber them so each
@@ -319,6 +322,12 @@ __global__ void __launch_bounds__(64 * NGW * NS, 2) k_message(MsgArgs a) {
       }
       bsh[x] = d2{v[0], v[1]};
     }
+    if constexpr (NB)
+      for (int x = threadIdx.x; x < NGW * 3 * 16; x += NGW * NS * 64) {
+        const int c = x % 16, part = x / 16 % 3, g = x / 48;
+        const double* fb = (const double*)a.fbias + part * F + 32 * (half * NGW + g) + 2 * c;
+        bias_sh[x] = d2{fb[0], fb[1]};
+      }
   }
   __syncthreads();                             // (the only barrier)
   const int i0 = ib + st * RBS;
@@ -326,6 +335,7 @@ __global__ void __launch_bounds__(64 * NGW * NS, 2) k_message(MsgArgs a) {
   const int i1 = min(a.N, i0 + RBS);
   const int ch = 32 * (half * NGW + gw) + 2 * col;   // this lane's channels ch, ch + 1
   const d2* bw = bsh + gw * 6 * NP * 64 + lane;
+  const d2* bb = bias_sh + gw * 3 * 16 + col;
   const T* h = (const T*)a.h;
   const T* vin = (const T*)a.v_in;
   const T* basis = (const T*)a.basis;
@@ -348,21 +358,26 @@ __global__ void __launch_bounds__(64 * NGW * NS, 2) k_message(MsgArgs a) {
     return !c.last ? make(c.i, c.c0 + 16) : c.i + 1 < i1 ? make(c.i + 1, rp(c.i + 1)) : c;
   };
   // Edge info: lane 16 kk + j holds (rhat_x, rhat_y) and (rhat_z, sender)
-  // of chunk row 4 (j % 4) + kk, so accumulator row 4 ii + kk of every lane
+  // of chunk row 4 (j % 4) + kk (without the bias column (rhat_z, f_c), the
+  // sender from the CSR column), so accumulator row 4 ii + kk of every lane
   // of the 16-lane row kk sits in that row's lane ii, and a DPP row
   // broadcast hands it over.  Rows past the chunk's end take its first edge
-  // (a valid sender) and get a zero basis row, hence a zero filter, so no
-  // gather needs a branch; an empty chunk gathers the receiver's own row.
-  struct Raw { d2 xy, ze; };
+  // (a valid sender) and get a zero basis row and f_c, hence a zero filter,
+  // so no gather needs a branch; an empty chunk gathers the receiver's own
+  // row.
+  struct Raw { d2 xy, ze; int j; };
   auto load_raw = [&](const Ck& c, Raw& o) {
     if (c.cnt > 0) {
       const int row = 4 * (col & 3) + kk;
-      const double* ei = einfo + 4 * (size_t)(c.c0 + (row < c.cnt ? row : 0));
+      const size_t e = c.c0 + (row < c.cnt ? row : 0);
+      const double* ei = einfo + 4 * e;
       o.xy = *(const d2*)ei;
       o.ze = *(const d2*)(ei + 2);
+      o.j = NB ? a.col[e] : 0;
     } else {
       o.xy = d2{0.0, 0.0};
-      o.ze = d2{0.0, (double)c.i};
+      o.ze = d2{0.0, NB ? 0.0 : (double)c.i};
+      o.j = c.i;
     }
   };
   auto load_ga = [&](const Ck& c, T (&Ga)[KBM]) {
@@ -375,7 +390,7 @@ __global__ void __launch_bounds__(64 * NGW * NS, 2) k_message(MsgArgs a) {
     }
     if constexpr (KBM & 1) Ga[KBM - 1] = gp[4 * (KBM - 1) + kk];
   };
-  auto filter = [&](const Ck& c, const T (&Ga)[KBM], C (&w)[2][3]) {
+  auto filter = [&](const Ck& c, const T (&Ga)[KBM], const Raw& in, C (&w)[2][3]) {
     T ga[KBM];
 #pragma unroll
     for (int kb = 0; kb < KBM; ++kb) ga[kb] = col < c.cnt ? Ga[kb] : 0.0;
@@ -408,10 +423,25 @@ __global__ void __launch_bounds__(64 * NGW * NS, 2) k_message(MsgArgs a) {
       __builtin_amdgcn_sched_group_barrier(0x008, NBR, 0);
     }
     if constexpr (KBM & 1) __builtin_amdgcn_sched_group_barrier(0x008, NBR, 0);
+    if constexpr (NB) {
+      // w = f_c (W_f g + b_f): the bias times the rows' f_c (zero past the
+      // chunk's end)
+#pragma unroll
+      for (int ii = 0; ii < 4; ++ii) {
+        const double fc = P::row(lane, ii) < c.cnt ? row_bcast(in.ze.y, ii) : 0.0;
+#pragma unroll
+        for (int part = 0; part < 3; ++part) {
+          if (V0 && part == 1) continue;
+          const d2 b = bb[part * 16];
+          w[0][part][ii] = fma(fc, b.x, w[0][part][ii]);
+          w[1][part][ii] = fma(fc, b.y, w[1][part][ii]);
+        }
+      }
+    }
   };
   struct Gath { d2 hs[4], hr[4], hv[4], vj[4][3]; };
   auto gather = [&](const Raw& in, Gath& G) {
-    const int j_lane = acc_to_index(in.ze.y);
+    const int j_lane = NB ? in.j : acc_to_index(in.ze.y);
 #pragma unroll
     for (int ii = 0; ii < 4; ++ii) {
       const size_t hb = (size_t)row_bcast(j_lane, ii) * 3 * F + ch;
@@ -483,7 +513,7 @@ __global__ void __launch_bounds__(64 * NGW * NS, 2) k_message(MsgArgs a) {
       load_raw(nx, in_nxt);
       if constexpr (PF) load_ga(nx, ga_nxt);
     }
-    filter(cur, ga_cur, w);
+    filter(cur, ga_cur, in_cur, w);
     consume(w, G, in_cur);
     if (cur.last) finish(cur.i);
     cur = nx;
@@ -1305,9 +1335,8 @@ void launch_message_kbm(hipStream_t st, const MsgArgs& a) {
     // eight waves per workgroup: NGW channel groups times NS streams
     constexpr int NGW = msg64_groups<F, KBM>(), NS = 8 / NGW, SPLIT = F / 32 / NGW;
     const int blocks = ((a.N + MSG_RB64 - 1) / MSG_RB64 * SPLIT + 7) / 8 * 8;   // a multiple of the 8 XCDs
-    static_assert(!NB, "FP64 keeps the filter's bias column");
-    if (a.v_zero) k_message<P, F, NGW, NS, KBM, true><<<blocks, 512, 0, st>>>(a);
-    else k_message<P, F, NGW, NS, KBM, false><<<blocks, 512, 0, st>>>(a);
+    if (a.v_zero) k_message<P, F, NGW, NS, KBM, true, NB><<<blocks, 512, 0, st>>>(a);
+    else k_message<P, F, NGW, NS, KBM, false, NB><<<blocks, 512, 0, st>>>(a);
   } else {
     const int blocks = ((a.N + MSG_RB2 - 1) / MSG_RB2 + 7) / 8 * 8;
     if (a.v_zero) k_message_lane<P, F, KBM, true, NB><<<blocks, F, 0, st>>>(a);
@@ -1337,20 +1366,16 @@ hipError_t launch_message(hipStream_t st, const MsgArgs& a) {
         default: return hipErrorInvalidValue;
       }
     }
-  } else if (sizeof(typename P::T) < 8 && a.nb) {
-    if constexpr (sizeof(typename P::T) < 8) {
-      switch (nkb) {
-        case 1: launch_message_kbm<P, F, 1, true>(st, a); break;
-        case 2: launch_message_kbm<P, F, 2, true>(st, a); break;
-        case 5: launch_message_kbm<P, F, 5, true>(st, a); break;
-        case 8: launch_message_kbm<P, F, 8, true>(st, a); break;
-        case 12: launch_message_kbm<P, F, 12, true>(st, a); break;
-        case 17: launch_message_kbm<P, F, 17, true>(st, a); break;
-        default: return hipErrorInvalidValue;
-      }
-    }
   } else if (a.nb) {
-    return hipErrorInvalidValue;   // FP64 keeps the bias column
+    switch (nkb) {
+      case 1: launch_message_kbm<P, F, 1, true>(st, a); break;
+      case 2: launch_message_kbm<P, F, 2, true>(st, a); break;
+      case 5: launch_message_kbm<P, F, 5, true>(st, a); break;
+      case 8: launch_message_kbm<P, F, 8, true>(st, a); break;
+      case 12: launch_message_kbm<P, F, 12, true>(st, a); break;
+      case 17: launch_message_kbm<P, F, 17, true>(st, a); break;
+      default: return hipErrorInvalidValue;
+    }
   } else {
     switch (nkb) {
       case 3: launch_message_kbm<P, F, 3, false>(st, a); break;
@@ -1664,13 +1689,10 @@ hipError_t forward_impl(hipStream_t st, ForwardArgs& fa) {
     prof_mark(fa.prof, st, KC_EMBED, false);
   }
   int cur = 0;
-  // The filter without its bias column (f_c b_f added in the message's
-  // epilogue) where that saves MFMA k-blocks, in FP32 and BF16; a forward
-  // that keeps a save area for the reverse pass uses the layout the reverse
-  // pass reads.  (FP64: measured slower, 16.6 -> 17.0 ms per launch on the
-  // bulk batch although it saves a ninth of the MFMAs: the kernel waits on
-  // its gathers, and the sender index then comes from a second array.)
-  const bool nb = sizeof(T) < 8 && !fa.save && !pm->layers.empty() &&
+  // The filter without its bias column (f_c b_f added after the message's
+  // MFMAs) where that saves MFMA k-blocks; a forward that keeps a save area
+  // for the reverse pass uses the layout the reverse pass reads.
+  const bool nb = !fa.save && !pm->layers.empty() &&
                   pm->layers[0].filt_nb.din_p < pm->layers[0].filt_mma.din_p;
   const int kcols = pm->layers.empty() ? 0 : nb ? pm->layers[0].filt_nb.din_p : pm->layers[0].filt_mma.din_p;
   if (N > 0 && fa.stop_layer >= 0) {

@@ -113,9 +113,8 @@ struct LayerDev {       // one interaction layer
                         // stores it twice along K (input [hi | lo] terms)
   DenseDev filt_nb;     // the filter K -> 3F without the bias column (BF16:
                         // 2K, twice along K), its bias b_f in .b; used by the
-                        // FP32 / BF16 energy forward when it needs fewer MFMA
-                        // k-blocks (the reverse pass keeps filt_mma; FP64
-                        // does not pack it)
+                        // energy forward when it needs fewer MFMA k-blocks
+                        // (the reverse pass keeps filt_mma)
   // transposed weights for the reverse pass (no bias; built on the first
   // forces call): phi1^T F -> F, phi2^T 3F -> F, [U^T | V^T] 2F -> F,
   // upd1^T F -> 2F, upd2^T 3F -> F

@@ -198,9 +198,9 @@ painn_status build_prec(painn_model* m, int prec, PrecModel** out) {
         e = pack_dense(pm, prec, wf.data(), nullptr, 3 * F, K + 1, &L.filt_mma, 1);
       }
     }
-    if (e == hipSuccess && prec != PAINN_FP64) {
-      // the filter without its bias column, the bias kept beside it (FP32
-      // and BF16 forwards; FP64 keeps the bias column)
+    if (e == hipSuccess) {
+      // the filter without its bias column, the bias kept beside it (the
+      // forward's message where that saves MFMA k-blocks)
       const double* Wf = arr(base + A_FILT_W);
       if (prec == PAINN_BF16) {
         std::vector<double> w2((size_t)3 * F * 2 * K);
