@@ -627,10 +627,12 @@ k_update(UpdArgs a) {
           },
           [&](int kb, const Fd* x, const Fd* f) {
 #pragma unroll
-            for (int r = 0; r < RT; ++r) {
-              au[r] = D::mfma(x[r], f[0], au[r]);
-              av[r] = D::mfma(x[r], f[1], av[r]);
-            }
+            for (int j = 0; j < D::SUB; ++j)
+#pragma unroll
+              for (int r = 0; r < RT; ++r) {
+                au[r] = D::mfma_sub(x[r], f[0], au[r], j);
+                av[r] = D::mfma_sub(x[r], f[1], av[r], j);
+              }
           });
 #pragma unroll
       for (int r = 0; r < RT; ++r) {
@@ -698,11 +700,13 @@ k_update(UpdArgs a) {
           },
           [&](int kb, const Fd* x, const Fd* f) {
 #pragma unroll
-            for (int r = 0; r < RT; ++r) {
-              avv[r] = D::mfma(x[r], f[0], avv[r]);
-              asv[r] = D::mfma(x[r], f[1], asv[r]);
-              ass[r] = D::mfma(x[r], f[2], ass[r]);
-            }
+            for (int j = 0; j < D::SUB; ++j)
+#pragma unroll
+              for (int r = 0; r < RT; ++r) {
+                avv[r] = D::mfma_sub(x[r], f[0], avv[r], j);
+                asv[r] = D::mfma_sub(x[r], f[1], asv[r], j);
+                ass[r] = D::mfma_sub(x[r], f[2], ass[r], j);
+              }
           });
       const int col = ft * 16 + (lane & 15);
       const A bvv = b2[col], bsv = b2[F + col], bss = b2[2 * F + col];

@@ -68,6 +68,14 @@ inline __host__ __device__ int pad32(int d) { return (d + 31) & ~31; }
 // MFMA k-blocks of the radial filter's input (K+1 basis columns, or 2(K+1)
 // for BF16), rounded up to the counts the message kernel is compiled for
 // (the padding columns are zero); -1 if too large.
+// LDS row padding (elements) of the dense kernels' activation tiles (one
+// A-fragment read of 16 rows falls in distinct banks).  The device layouts
+// and the host's buffer sizing share it.
+constexpr int LDS_PAD_FP64 = 1, LDS_PAD_FP32 = 4, LDS_PAD_BF16 = 8;
+inline int lds_pad(int prec) {
+  return prec == PAINN_FP64 ? LDS_PAD_FP64 : prec == PAINN_FP32 ? LDS_PAD_FP32 : LDS_PAD_BF16;
+}
+
 inline int filter_kblocks(int din, int prec) {
   const int kc = prec == PAINN_BF16 ? 32 : 4;
   const int need = (din + kc - 1) / kc;

@@ -44,10 +44,16 @@ struct P64 {
   using A = double;  // accumulation
   using C = d4_t;
   using Fr = double;
-  static constexpr int KC = 4, KPL = 1, PAD = 1, PREC = PAINN_FP64, UNROLL = 8, RING = 16;
+  static constexpr int KC = 4, KPL = 1, PAD = LDS_PAD_FP64, PREC = PAINN_FP64, UNROLL = 8, RING = 16;
   __device__ static __forceinline__ Fr frag(const T* p) { return *p; }
   __device__ static __forceinline__ C mfma(Fr a, Fr b, C c) {
     return __builtin_amdgcn_mfma_f64_16x16x4f64(a, b, c, 0, 0, 0);
+  }
+  // the MFMA instructions one fragment pair feeds, one at a time (chains of
+  // several accumulators interleave them)
+  static constexpr int SUB = 1;
+  __device__ static __forceinline__ C mfma_sub(Fr a, Fr b, C c, int j) {
+    return mfma(a, b, c);
   }
   __device__ static __forceinline__ A ld(T x) { return x; }
   __device__ static __forceinline__ T st(A x) { return x; }
@@ -60,10 +66,16 @@ struct P32 {
   using A = float;
   using C = f4_t;
   using Fr = float;
-  static constexpr int KC = 4, KPL = 1, PAD = 4, PREC = PAINN_FP32, UNROLL = 8, RING = 24;
+  static constexpr int KC = 4, KPL = 1, PAD = LDS_PAD_FP32, PREC = PAINN_FP32, UNROLL = 8, RING = 24;
   __device__ static __forceinline__ Fr frag(const T* p) { return *p; }
   __device__ static __forceinline__ C mfma(Fr a, Fr b, C c) {
     return __builtin_amdgcn_mfma_f32_16x16x4f32(a, b, c, 0, 0, 0);
+  }
+  // the MFMA instructions one fragment pair feeds, one at a time (chains of
+  // several accumulators interleave them)
+  static constexpr int SUB = 1;
+  __device__ static __forceinline__ C mfma_sub(Fr a, Fr b, C c, int j) {
+    return mfma(a, b, c);
   }
   __device__ static __forceinline__ A ld(T x) { return x; }
   __device__ static __forceinline__ T st(A x) { return x; }
@@ -84,13 +96,19 @@ struct P32B {
   using A = float;
   using C = f4_t;
   using Fr = f4_t;
-  static constexpr int KC = 16, KPL = 4, PAD = 4, PREC = PAINN_FP32, UNROLL = 2, RING = 24;
+  static constexpr int KC = 16, KPL = 4, PAD = LDS_PAD_FP32, PREC = PAINN_FP32, UNROLL = 2, RING = 24;
   __device__ static __forceinline__ Fr frag(const T* p) { return *(const f4_t*)p; }
   __device__ static __forceinline__ C mfma(Fr a, Fr b, C c) {
     c = __builtin_amdgcn_mfma_f32_16x16x4f32(a[0], b[0], c, 0, 0, 0);
     c = __builtin_amdgcn_mfma_f32_16x16x4f32(a[1], b[1], c, 0, 0, 0);
     c = __builtin_amdgcn_mfma_f32_16x16x4f32(a[2], b[2], c, 0, 0, 0);
     return __builtin_amdgcn_mfma_f32_16x16x4f32(a[3], b[3], c, 0, 0, 0);
+  }
+  // the MFMA instructions one fragment pair feeds, one at a time (chains of
+  // several accumulators interleave them)
+  static constexpr int SUB = 4;
+  __device__ static __forceinline__ C mfma_sub(Fr a, Fr b, C c, int j) {
+    return __builtin_amdgcn_mfma_f32_16x16x4f32(a[j], b[j], c, 0, 0, 0);
   }
   __device__ static __forceinline__ A ld(T x) { return x; }
   __device__ static __forceinline__ T st(A x) { return x; }
@@ -103,10 +121,16 @@ struct PB16 {
   using A = float;
   using C = f4_t;
   using Fr = bf8_t;
-  static constexpr int KC = 32, KPL = 8, PAD = 8, PREC = PAINN_BF16, UNROLL = 2, RING = 8;
+  static constexpr int KC = 32, KPL = 8, PAD = LDS_PAD_BF16, PREC = PAINN_BF16, UNROLL = 2, RING = 8;
   __device__ static __forceinline__ Fr frag(const T* p) { return *(const bf8_t*)p; }
   __device__ static __forceinline__ C mfma(Fr a, Fr b, C c) {
     return __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, b, c, 0, 0, 0);
+  }
+  // the MFMA instructions one fragment pair feeds, one at a time (chains of
+  // several accumulators interleave them)
+  static constexpr int SUB = 1;
+  __device__ static __forceinline__ C mfma_sub(Fr a, Fr b, C c, int j) {
+    return mfma(a, b, c);
   }
   __device__ static __forceinline__ A ld(T x) { return bf16_to_f(x); }
   __device__ static __forceinline__ T st(A x) { return f_to_bf16(x); }
@@ -116,6 +140,9 @@ struct PB16 {
 
 // The operand form of the dense layers (packed weights and activation tiles)
 // for a precision: FP32 uses the 16-byte form above, the others their own.
+// (A 16-byte FP64 form, two consecutive k per lane feeding two chained
+// instructions, halves the weight load instructions; measured 4 % faster on
+// the F = 128 update but 3 % slower on the F = 256 update, so not kept.)
 template <class P> struct dense_of { using type = P; };
 template <> struct dense_of<P32> { using type = P32B; };
 template <class P> using dense_t = typename dense_of<P>::type;
@@ -293,7 +320,9 @@ __device__ __forceinline__ void dense_tiles(const typename Q::T* X, int ldx, con
           xp, ldx, [&](int kb, Fr* f) { f[0] = P::frag(wp + (size_t)kb * 64 * P::KPL); },
           [&](int kb, const Fr* a, const Fr* f) {
 #pragma unroll
-            for (int r = 0; r < RT; ++r) acc[r] = P::mfma(a[r], f[0], acc[r]);
+            for (int j = 0; j < P::SUB; ++j)
+#pragma unroll
+              for (int r = 0; r < RT; ++r) acc[r] = P::mfma_sub(a[r], f[0], acc[r], j);
           });
     } else if constexpr (P::PREC == PAINN_BF16) {
       // run-time-length layers (heads, branch weighting), BF16: the ring, 4
@@ -303,7 +332,9 @@ __device__ __forceinline__ void dense_tiles(const typename Q::T* X, int ldx, con
           nkb, xp, ldx, [&](int kb, Fr* f) { f[0] = P::frag(wp + (size_t)kb * 64 * P::KPL); },
           [&](int kb, const Fr* a, const Fr* f) {
 #pragma unroll
-            for (int r = 0; r < RT; ++r) acc[r] = P::mfma(a[r], f[0], acc[r]);
+            for (int j = 0; j < P::SUB; ++j)
+#pragma unroll
+              for (int r = 0; r < RT; ++r) acc[r] = P::mfma_sub(a[r], f[0], acc[r], j);
           });
     } else {
       // FP32 / FP64: groups of UNROLL steps whose loads the compiler issues

@@ -825,13 +825,13 @@ static int forces_scratch_width(const Hyper& hp) {
 }
 
 // Operand buffers in global memory, for reverse tile kernels whose 16-row
-// tiles do not fit the LDS: [16][3F + 1] per update / phi tile (FP64 at
+// tiles do not fit the LDS: [16][3F + pad] per update / phi tile (FP64 at
 // F = 384), [2][16][widest head layer + 2] per heads workgroup.
 static size_t forces_xbuf_bytes(int prec, const Hyper& hp, int N, bool blend) {
   const size_t eb = elem_bytes(prec), F = hp.F, tiles = ((size_t)N + 15) / 16;
   const size_t head_tiles = ((size_t)N * (blend ? hp.n_heads : 1) + 15) / 16;
   // LDS row padding of the dense kernels' activation tiles (elements)
-  const size_t pad = prec == PAINN_FP64 ? 1 : prec == PAINN_FP32 ? 4 : 8;
+  const size_t pad = lds_pad(prec);
   size_t x = 0;
   if (16 * (4 * F + 2 * pad) * eb > 160 * 1024) x = tiles * 16 * (3 * F + pad) * eb;
   int wmax = hp.F;
