@@ -132,6 +132,9 @@ struct MsgArgs {
   int nb;
   const int32_t* col;
   const void* fbias;   // b_f [3F], accumulation type
+  // (FP64, Gaussian basis, without the bias column) basis rows are
+  // (d / Delta, f_c) per edge and the kernel forms the Gaussians itself
+  int rg;
 };
 
 constexpr int MSG_RB = 4;   // receivers per workgroup (MSG_RB < 64)
@@ -150,7 +153,7 @@ __device__ __forceinline__ int acc_to_index(double x) { return (int)x; }
 //   r = (x_j - x_i) + (n0 a + n1 b) + n2 c  (FP64),  d = |r|,  rhat = r / d,
 //   f_c = (cos(pi d / r_c) + 1) / 2,  g_k = exp(-gamma (d - k Delta)^2).
 // Edge e's geometry and basis row into g (LDS), its rhat and sender into einfo.
-template <class P, bool NB>
+template <class P, bool NB, bool RG>
 __device__ __forceinline__ void edge_row(long long e, int K, int kcols, double rc, int rbf, double gamma,
                                          double delta, const int32_t* __restrict__ recv,
                                          const int32_t* __restrict__ col, const int32_t* __restrict__ shift,
@@ -177,6 +180,13 @@ __device__ __forceinline__ void edge_row(long long e, int K, int kcols, double r
   // without the bias column the edge info carries f_c instead of the sender
   // (which the kernels then read from the CSR)
   o[3] = NB ? fc : index_to_acc<A>(j);           // the sender index, bit-exact
+  if constexpr (RG) {
+    // the message kernel forms g_k f_c from d / Delta and f_c
+    g[0] = P::st((A)(d / delta));
+    g[1] = P::st(fc);
+    for (int k = 2; k < kcols; ++k) g[k] = P::st(0);
+    return;
+  }
   // each value once; BF16 also writes its remainder term at KW + k
   const int KW = NB ? K : K + 1;                 // columns of one term
   for (int k = 0; k < KW; ++k) {
@@ -200,7 +210,7 @@ __device__ __forceinline__ void edge_row(long long e, int K, int kcols, double r
 // scatter one element per lane per store).
 constexpr int EP_THREADS = 64;   // one wave: <= 35 KiB of LDS at the largest row
 
-template <class P, bool NB>
+template <class P, bool NB, bool RG>
 __global__ void __launch_bounds__(EP_THREADS) k_edge_prep(long long E, int K, int kcols, double rc, int rbf,
                                                   double gamma, double delta,
                                                   const int32_t* __restrict__ recv,
@@ -218,7 +228,7 @@ __global__ void __launch_bounds__(EP_THREADS) k_edge_prep(long long E, int K, in
   const long long rows = (E + 16 - e0) < EP_THREADS ? (E + 16 - e0) : EP_THREADS;
   T* g = (T*)ep_smem + (size_t)threadIdx.x * kcols;
   // rows E .. E+15 are zero (read by partial chunks)
-  if (e < E) edge_row<P, NB>(e, K, kcols, rc, rbf, gamma, delta, recv, col, shift, atom_struct, pos, cell, g, einfo);
+  if (e < E) edge_row<P, NB, RG>(e, K, kcols, rc, rbf, gamma, delta, recv, col, shift, atom_struct, pos, cell, g, einfo);
   else if (e < E + 16)
     for (int k = 0; k < kcols; ++k) g[k] = P::st(0);
   __syncthreads();
@@ -277,17 +287,54 @@ __device__ __forceinline__ int msg_kcol(int kb, int kk) {
   return kb < KBM / 2 * 2 ? 8 * (kb >> 1) + 2 * kk + (kb & 1) : 4 * kb + kk;
 }
 
+// The Gaussian basis of one MFMA A-operand lane: ga[kb] = f_c g_k with
+// g_k = exp(-(u - k)^2 / 2), u = d / Delta, at the lane's inputs
+// k = msg_kcol(kb, kk).  Two exponentials per lane; the other inputs follow
+// from g(k + m) = g(k) exp(m (u - k) - m^2 / 2):
+//   g(k0 + 1) = g(k0) t,  t = exp(u - k0 - 1/2),
+//   g(k + 8) = g(k) t^8 e^-28 e^-8 (k - k0)   (k0 = 2 kk, the lane's first input).
+// With u and k0 of at most 35 (K <= 36) every factor and every partial
+// product stays inside FP64's normal range, so nothing underflows that the
+// direct formula would keep.
+template <int KBM>
+__device__ __forceinline__ void gauss_row(double u, double fc, int kk, double (&ga)[KBM]) {
+  constexpr double EM8 = 0x1.5fc21041027adp-12, EM28 = 0x1.853f01d6d53bap-41, EM64 = 0x1.969d47321e4ccp-93;
+  const double x = u - (double)(2 * kk);      // exact: an integer off u
+  double ea = exp(-0.5 * x * x) * fc;          // g(k0) f_c
+  const double t = exp(x - 0.5);
+  double eb = ea * t;                          // g(k0 + 1) f_c
+  const double t2 = t * t, t4 = t2 * t2;
+  double ra = t4 * t4 * EM28;                  // g(k0 + 8) / g(k0)
+#pragma unroll
+  for (int p = 0; p < KBM / 2; ++p) {
+    if (p > 0) {
+      ea *= ra;
+      eb *= ra * EM8;
+      ra *= EM64;
+    }
+    ga[2 * p] = ea;
+    ga[2 * p + 1] = eb;
+  }
+  if constexpr (KBM & 1) {
+    const double y = u - (double)(4 * (KBM - 1) + kk);
+    ga[KBM - 1] = exp(-0.5 * y * y) * fc;
+  }
+}
+
 // channel groups per workgroup: the LDS holds 6 (KBM + 1) / 2 KiB per group
 template <int F, int KBM>
 constexpr int msg64_groups() {
   return F / 32 < (KBM <= 12 ? 4 : 2) ? F / 32 : (KBM <= 12 ? 4 : 2);
 }
 
-template <class P, int F, int NGW, int NS, int KBM, bool V0, bool NB>
+template <class P, int F, int NGW, int NS, int KBM, bool V0, bool NB, bool RG>
 __global__ void __launch_bounds__(64 * NGW * NS, 2) k_message(MsgArgs a) {
   using T = typename P::T;
   using C = typename P::C;
   static_assert(sizeof(T) == 8, "the paired-channel layout is the FP64 kernel's");
+  static_assert(!RG || (NB && KBM <= 9), "Gaussians formed in the kernel: no bias column, K <= 36");
+  // basis values a lane keeps per chunk: its KBM inputs, or (d / Delta, f_c)
+  constexpr int NGA = RG ? 2 : KBM;
   typedef double d2 __attribute__((ext_vector_type(2)));
   constexpr int NG = F / 32, SPLIT = NG / NGW, NP = (KBM + 1) / 2, RBS = MSG_RB64 / NS;
   static_assert(NG % NGW == 0 && MSG_RB64 % NS == 0 && RBS < 64, "workgroup shape");
@@ -346,13 +393,25 @@ __global__ void __launch_bounds__(64 * NGW * NS, 2) k_message(MsgArgs a) {
   // the stream's row_ptr slice, one load per lane, read back by readlane
   const int rp_lane = a.row_ptr[i0 + min(lane, i1 - i0)];
   auto rp = [&](int i) { return __builtin_amdgcn_readlane(rp_lane, i - i0); };
-  int nck = 0;                                 // chunks of the sequence
-  for (int i = i0; i < i1; ++i) nck += max(1, (rp(i + 1) - rp(i) + 15) / 16);
-
-  struct Ck { int i, c0, cnt; bool last; };   // wave-uniform
+  // Chunks of 16 edges.  With PACK the stream's edges (its receivers' CSR
+  // rows are consecutive) form one sequence of chunks, so only the last is
+  // partial and a chunk may hold the ends and starts of several receivers;
+  // otherwise each receiver's row is a sequence of its own (one empty chunk
+  // for a receiver without edges, so that its row is written).
+  constexpr bool PACK = RG;
+  const int e_begin = rp(i0), e_end = rp(i1);
+  int nck = 0;
+  if constexpr (PACK) nck = (e_end - e_begin + 15) / 16;
+  else
+    for (int i = i0; i < i1; ++i) nck += max(1, (rp(i + 1) - rp(i) + 15) / 16);
+  struct Ck { int i, c0, cnt; bool last; };   // wave-uniform (i, last: without PACK)
   auto make = [&](int i, int c0) {
     const int eb = rp(i + 1);
     return Ck{i, c0, max(0, min(16, eb - c0)), c0 + 16 >= eb};
+  };
+  auto make_packed = [&](int k) {
+    const int c0 = e_begin + 16 * k;
+    return Ck{0, c0, min(16, e_end - c0), false};
   };
   auto next = [&](const Ck& c) {
     return !c.last ? make(c.i, c.c0 + 16) : c.i + 1 < i1 ? make(c.i + 1, rp(c.i + 1)) : c;
@@ -367,7 +426,7 @@ __global__ void __launch_bounds__(64 * NGW * NS, 2) k_message(MsgArgs a) {
   // row.
   struct Raw { d2 xy, ze; int j; };
   auto load_raw = [&](const Ck& c, Raw& o) {
-    if (c.cnt > 0) {
+    if (PACK || c.cnt > 0) {
       const int row = 4 * (col & 3) + kk;
       const size_t e = c.c0 + (row < c.cnt ? row : 0);
       const double* ei = einfo + 4 * e;
@@ -380,7 +439,13 @@ __global__ void __launch_bounds__(64 * NGW * NS, 2) k_message(MsgArgs a) {
       o.j = c.i;
     }
   };
-  auto load_ga = [&](const Ck& c, T (&Ga)[KBM]) {
+  auto load_ga = [&](const Ck& c, T (&Ga)[NGA]) {
+    if constexpr (RG) {
+      const d2 t = *(const d2*)(basis + 2 * (size_t)(c.c0 + col));   // rows E .. E + 15 exist
+      Ga[0] = t.x;
+      Ga[1] = t.y;
+      return;
+    }
     const T* gp = basis + (size_t)(c.c0 + col) * kcols;   // rows E .. E + 15 exist
 #pragma unroll
     for (int p = 0; p < KBM / 2; ++p) {
@@ -390,10 +455,12 @@ __global__ void __launch_bounds__(64 * NGW * NS, 2) k_message(MsgArgs a) {
     }
     if constexpr (KBM & 1) Ga[KBM - 1] = gp[4 * (KBM - 1) + kk];
   };
-  auto filter = [&](const Ck& c, const T (&Ga)[KBM], const Raw& in, C (&w)[2][3]) {
+  auto filter = [&](const Ck& c, const T (&Ga)[NGA], const Raw& in, C (&w)[2][3]) {
     T ga[KBM];
+    if constexpr (RG) gauss_row<KBM>(Ga[0], col < c.cnt ? Ga[1] : 0.0, kk, ga);
+    else
 #pragma unroll
-    for (int kb = 0; kb < KBM; ++kb) ga[kb] = col < c.cnt ? Ga[kb] : 0.0;
+      for (int kb = 0; kb < KBM; ++kb) ga[kb] = col < c.cnt ? Ga[kb] : 0.0;
 #pragma unroll
     for (int q = 0; q < 2; ++q)
 #pragma unroll
@@ -454,17 +521,23 @@ __global__ void __launch_bounds__(64 * NGW * NS, 2) k_message(MsgArgs a) {
       }
     }
   };
+  // Chunk rows [r0, r1) into the running receiver's per-lane sums (every
+  // row where FULL; rows past the chunk's end carry a zero filter); rows
+  // outside the range add exact zeros.
   double acc_s[2] = {0.0, 0.0}, acc_v[2][3] = {{0.0, 0.0, 0.0}, {0.0, 0.0, 0.0}};
-  auto consume = [&](const C (&w)[2][3], const Gath& G, const Raw& in) {
+  auto consume = [&](const C (&w)[2][3], const Gath& G, const Raw& in, auto full, int r0, int r1) {
+    constexpr bool FULL = decltype(full)::value;
 #pragma unroll
     for (int ii = 0; ii < 4; ++ii) {
       const double rh[3] = {row_bcast(in.xy.x, ii), row_bcast(in.xy.y, ii), row_bcast(in.ze.x, ii)};
+      const int row = P::row(lane, ii);
+      const double m = FULL || (row >= r0 && row < r1) ? 1.0 : 0.0;
 #pragma unroll
       for (int q = 0; q < 2; ++q) {
-        acc_s[q] = fma(G.hs[ii][q], w[q][0][ii], acc_s[q]);
-        const double pr = G.hr[ii][q] * w[q][2][ii];
+        acc_s[q] = fma(G.hs[ii][q], FULL ? w[q][0][ii] : w[q][0][ii] * m, acc_s[q]);
+        const double pr = G.hr[ii][q] * (FULL ? w[q][2][ii] : w[q][2][ii] * m);
         if constexpr (!V0) {
-          const double pv = G.hv[ii][q] * w[q][1][ii];
+          const double pv = G.hv[ii][q] * (FULL ? w[q][1][ii] : w[q][1][ii] * m);
 #pragma unroll
           for (int c = 0; c < 3; ++c) acc_v[q][c] = fma(G.vj[ii][c][q], pv, acc_v[q][c]);
         }
@@ -473,6 +546,7 @@ __global__ void __launch_bounds__(64 * NGW * NS, 2) k_message(MsgArgs a) {
       }
     }
   };
+  // Receiver i's sums over the wave into s and v (then zeroed).
   auto finish = [&](int i) {
     const size_t iv = (size_t)i * 3 * F + ch;
     const d2 s_old = *(const d2*)(sin + (size_t)i * F + ch);
@@ -503,31 +577,55 @@ __global__ void __launch_bounds__(64 * NGW * NS, 2) k_message(MsgArgs a) {
   C w[2][3];
   // (the next chunk's basis rows are prefetched too where the registers
   // allow it, up to 9 k-blocks)
-  constexpr bool PF = KBM <= 9;
-  auto step = [&](int k, Ck& cur, const Raw& in_cur, Raw& in_nxt, T (&ga_cur)[KBM], T (&ga_nxt)[KBM]) {
+  constexpr bool PF = RG || KBM <= 9;
+  int ir = i0;                                 // with PACK: the receiver being summed
+  auto step = [&](int k, Ck& cur, const Raw& in_cur, Raw& in_nxt, T (&ga_cur)[NGA], T (&ga_nxt)[NGA]) {
     gather(in_cur, G);
     if constexpr (!PF) load_ga(cur, ga_cur);
-    const Ck nx = next(cur);
     const bool more = k + 1 < nck;
+    const Ck nx = PACK ? make_packed(k + 1) : next(cur);
     if (more) {
       load_raw(nx, in_nxt);
       if constexpr (PF) load_ga(nx, ga_nxt);
     }
     filter(cur, ga_cur, in_cur, w);
-    consume(w, G, in_cur);
-    if (cur.last) finish(cur.i);
+    if constexpr (PACK) {
+      // the receivers that end in this chunk (those without edges too),
+      // then the one that runs on into the next
+      const int c1 = cur.c0 + cur.cnt;
+      if (rp(ir + 1) > c1) {
+        consume(w, G, in_cur, std::true_type{}, 0, 16);
+      } else {
+        int r0 = 0;
+        while (ir < i1 && rp(ir + 1) <= c1) {
+          const int r1 = rp(ir + 1) - cur.c0;
+          if (r1 > r0) consume(w, G, in_cur, std::false_type{}, r0, r1);
+          finish(ir);
+          ++ir;
+          r0 = max(r0, r1);
+        }
+        if (ir < i1 && r0 < cur.cnt) consume(w, G, in_cur, std::false_type{}, r0, cur.cnt);
+      }
+    } else {
+      consume(w, G, in_cur, std::true_type{}, 0, 16);
+      if (cur.last) finish(cur.i);
+    }
     cur = nx;
     return more;
   };
-  Ck c = make(i0, rp(i0));
+  Ck c = PACK ? make_packed(0) : make(i0, e_begin);
   Raw inA, inB;
-  T gaA[KBM], gaB[KBM];
-  load_raw(c, inA);
-  if constexpr (PF) load_ga(c, gaA);
-  for (int k = 0;; k += 2) {
-    if (!step(k, c, inA, inB, gaA, gaB)) break;
-    if (!step(k + 1, c, inB, inA, gaB, gaA)) break;
+  T gaA[NGA], gaB[NGA];
+  if (nck > 0) {
+    load_raw(c, inA);
+    if constexpr (PF) load_ga(c, gaA);
+    for (int k = 0;; k += 2) {
+      if (!step(k, c, inA, inB, gaA, gaB)) break;
+      if (!step(k + 1, c, inB, inA, gaB, gaA)) break;
+    }
   }
+  if constexpr (PACK)
+    for (; ir < i1; ++ir) finish(ir);         // receivers without edges at the end
 }
 
 // --------------------------------------------------------------- update ----
@@ -1333,14 +1431,14 @@ k_message_lane(MsgArgs a) {
   write_out();
 }
 
-template <class P, int F, int KBM, bool NB>
+template <class P, int F, int KBM, bool NB, bool RG = false>
 void launch_message_kbm(hipStream_t st, const MsgArgs& a) {
   if constexpr (sizeof(typename P::T) == 8) {
     // eight waves per workgroup: NGW channel groups times NS streams
     constexpr int NGW = msg64_groups<F, KBM>(), NS = 8 / NGW, SPLIT = F / 32 / NGW;
     const int blocks = ((a.N + MSG_RB64 - 1) / MSG_RB64 * SPLIT + 7) / 8 * 8;   // a multiple of the 8 XCDs
-    if (a.v_zero) k_message<P, F, NGW, NS, KBM, true, NB><<<blocks, 512, 0, st>>>(a);
-    else k_message<P, F, NGW, NS, KBM, false, NB><<<blocks, 512, 0, st>>>(a);
+    if (a.v_zero) k_message<P, F, NGW, NS, KBM, true, NB, RG><<<blocks, 512, 0, st>>>(a);
+    else k_message<P, F, NGW, NS, KBM, false, NB, RG><<<blocks, 512, 0, st>>>(a);
   } else {
     const int blocks = ((a.N + MSG_RB2 - 1) / MSG_RB2 + 7) / 8 * 8;
     if (a.v_zero) k_message_lane<P, F, KBM, true, NB><<<blocks, F, 0, st>>>(a);
@@ -1371,11 +1469,19 @@ hipError_t launch_message(hipStream_t st, const MsgArgs& a) {
       }
     }
   } else if (a.nb) {
+    constexpr bool F64 = sizeof(typename P::T) == 8;
+    if (a.rg && !(F64 && (nkb == 5 || nkb == 8))) return hipErrorInvalidValue;
     switch (nkb) {
       case 1: launch_message_kbm<P, F, 1, true>(st, a); break;
       case 2: launch_message_kbm<P, F, 2, true>(st, a); break;
-      case 5: launch_message_kbm<P, F, 5, true>(st, a); break;
-      case 8: launch_message_kbm<P, F, 8, true>(st, a); break;
+      case 5:
+        if (a.rg) launch_message_kbm<P, F, 5, true, F64>(st, a);
+        else launch_message_kbm<P, F, 5, true>(st, a);
+        break;
+      case 8:
+        if (a.rg) launch_message_kbm<P, F, 8, true, F64>(st, a);
+        else launch_message_kbm<P, F, 8, true>(st, a);
+        break;
       case 12: launch_message_kbm<P, F, 12, true>(st, a); break;
       case 17: launch_message_kbm<P, F, 17, true>(st, a); break;
       default: return hipErrorInvalidValue;
@@ -1698,22 +1804,29 @@ hipError_t forward_impl(hipStream_t st, ForwardArgs& fa) {
   // for the reverse pass uses the layout the reverse pass reads.
   const bool nb = !fa.save && !pm->layers.empty() &&
                   pm->layers[0].filt_nb.din_p < pm->layers[0].filt_mma.din_p;
-  const int kcols = pm->layers.empty() ? 0 : nb ? pm->layers[0].filt_nb.din_p : pm->layers[0].filt_mma.din_p;
+  // In FP64 the message kernel forms Gaussians itself (up to 8 k-blocks,
+  // K <= 32): each edge's basis row is then (d / Delta, f_c).
+  const int nkb_nb = nb ? pm->layers[0].filt_nb.din_p / P::KC : 0;
+  const bool rg = nb && sizeof(T) == 8 && hp.rbf_type == 0 && (nkb_nb == 5 || nkb_nb == 8);
+  const int kcols = pm->layers.empty() ? 0 : rg ? 2 : nb ? pm->layers[0].filt_nb.din_p : pm->layers[0].filt_mma.din_p;
   if (N > 0 && fa.stop_layer >= 0) {
     prof_mark(fa.prof, st, KC_EDGE_PREP, true);
     const double delta = hp.cutoff / (hp.K - 1);
     const unsigned eg = (unsigned)((g->E + 16 + EP_THREADS - 1) / EP_THREADS);
     const size_t esm = (size_t)EP_THREADS * kcols * sizeof(T);
-    if (nb)
-      k_edge_prep<P, true><<<eg, EP_THREADS, esm, st>>>(g->E, hp.K, kcols, hp.cutoff, hp.rbf_type,
-                                                        1.0 / (2.0 * delta * delta), delta, g->recv, g->col,
-                                                        g->shift, g->atom_struct, g->pos, g->cell, (T*)fa.basis,
-                                                        (A*)fa.einfo);
+    const double gamma = 1.0 / (2.0 * delta * delta);
+    if (rg)
+      k_edge_prep<P, true, true><<<eg, EP_THREADS, esm, st>>>(g->E, hp.K, kcols, hp.cutoff, hp.rbf_type, gamma,
+                                                              delta, g->recv, g->col, g->shift, g->atom_struct,
+                                                              g->pos, g->cell, (T*)fa.basis, (A*)fa.einfo);
+    else if (nb)
+      k_edge_prep<P, true, false><<<eg, EP_THREADS, esm, st>>>(g->E, hp.K, kcols, hp.cutoff, hp.rbf_type, gamma,
+                                                               delta, g->recv, g->col, g->shift, g->atom_struct,
+                                                               g->pos, g->cell, (T*)fa.basis, (A*)fa.einfo);
     else
-      k_edge_prep<P, false><<<eg, EP_THREADS, esm, st>>>(g->E, hp.K, kcols, hp.cutoff, hp.rbf_type,
-                                                         1.0 / (2.0 * delta * delta), delta, g->recv, g->col,
-                                                         g->shift, g->atom_struct, g->pos, g->cell, (T*)fa.basis,
-                                                         (A*)fa.einfo);
+      k_edge_prep<P, false, false><<<eg, EP_THREADS, esm, st>>>(g->E, hp.K, kcols, hp.cutoff, hp.rbf_type, gamma,
+                                                                delta, g->recv, g->col, g->shift, g->atom_struct,
+                                                                g->pos, g->cell, (T*)fa.basis, (A*)fa.einfo);
     prof_mark(fa.prof, st, KC_EDGE_PREP, false);
   }
   for (int l = 0; l <= fa.stop_layer && N > 0; ++l) {
@@ -1727,6 +1840,7 @@ hipError_t forward_impl(hipStream_t st, ForwardArgs& fa) {
     ma.einfo = fa.einfo;
     ma.filt_mma = nb ? Ld.filt_nb : Ld.filt_mma;
     ma.nb = nb;
+    ma.rg = rg;
     ma.col = g->col;
     ma.fbias = Ld.filt_nb.b;
     ma.h = fa.save ? sv.H(l) : h;
