@@ -629,9 +629,10 @@ __global__ void __launch_bounds__(64 * NGW * NS, 2) k_message(MsgArgs a) {
 }
 
 // --------------------------------------------------------------- update ----
-// Tile of 16 atoms, 4 waves.  U[c] = WU v[c], V[c] = WV v[c] for c = x, y, z
-// one component at a time (v[c] staged in LDS); U, |V|^2 and <U, V> stay in
-// the registers of the wave that owns the feature tile.  Then
+// Tile of 16 RT atoms.  U[c] = WU v[c], V[c] = WV v[c] for c = x, y, z, the
+// three components staged in LDS together so that each weight fragment
+// serves all three; U, |V|^2 and <U, V> stay in the registers of the wave
+// that owns the feature tile.  Then
 // a = W2a silu(W1a [s; |V|] + b1a) + b2a, with each wave computing the
 // a_vv / a_sv / a_ss column tiles of its own feature tiles, so the final
 //   v[c] += a_vv U[c],  s += a_sv <U, V> + a_ss
@@ -669,6 +670,14 @@ constexpr int update_nw() {
   return F < 128 ? 4 : F == 128 ? 8 : F / 32;
 }
 
+// Components of v that go through the U/V weights together: three, except
+// where four FP32 waves per SIMD leave too few registers for their
+// accumulators (one at a time there).
+template <class P, int F>
+constexpr int uv_comps() {
+  return P::PREC == PAINN_FP32 && update_waves<P, F>() >= 4 ? 1 : 3;
+}
+
 // The saving variant (forces) stores U, V, z, a as it goes and runs at no
 // more than two waves per SIMD (the stores' addresses need registers).
 template <class P, int F, int RT, bool FUSE_PHI, bool SAVE>
@@ -683,8 +692,14 @@ k_update(UpdArgs a) {
   constexpr int FTW = NFT / NW;      // per wave
   constexpr int TM = 16 * RT;        // atoms per workgroup
   constexpr int LD1 = F + P::PAD, LD2 = 2 * F + P::PAD;
-  __shared__ __attribute__((aligned(16))) T VS[TM * LD1];   // v[c] slice, later the MLP hidden
-  __shared__ __attribute__((aligned(16))) T SN[TM * LD2];   // [s ; |V|]
+  // The UVC components of v side by side for the U/V products; [s ; |V|]
+  // and the MLP hidden layer (with UVC = 3 in the same space, after them).
+  constexpr int UVC = uv_comps<P, F>();
+  static_assert(3 * LD1 >= LD2 + LD1, "LDS phases");
+  __shared__ __attribute__((aligned(16))) T smem[3 * TM * LD1];
+  T* SN = smem;                                   // [TM][LD2]
+  T* H = smem + TM * LD2;                         // [TM][LD1]
+  T* VS = UVC == 3 ? smem : H;                    // [UVC][TM][LD1]
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const size_t row0 = (size_t)blockIdx.x * TM;
   const int N = a.N;
@@ -695,7 +710,6 @@ k_update(UpdArgs a) {
   // element by element
   T* s_out = SAVE ? (T*)a.s_out : (T*)a.s;
   T* v_out = SAVE ? (T*)a.v_out : (T*)a.v;
-  stage_rows<P, F, TM>(SN, LD2, s, F, row0, N);
   C U[FTW][3][RT], nsq[FTW][RT], pd[FTW][RT];
   for (int q = 0; q < FTW; ++q)
     for (int r = 0; r < RT; ++r)
@@ -704,20 +718,26 @@ k_update(UpdArgs a) {
   using Fd = typename D::Fr;
   constexpr int nkb = F / D::KC;
   const T* Wuv = (const T*)a.uv.w;
-  for (int c = 0; c < 3; ++c) {
-    __syncthreads();
-    stage_rows<P, F, TM>(VS, LD1, v + c * F, 3 * F, row0, N);
+  if constexpr (UVC == 1) stage_rows<P, F, TM>(SN, LD2, s, F, row0, N);
+  // UVC components against each weight fragment: the UVC RT row tiles of VS
+  // (component c0 + cc, tile r at 16 (cc RT + r) rows) share its loads.
+#pragma unroll
+  for (int c0 = 0; c0 < 3; c0 += UVC) {
+    if (UVC == 1) __syncthreads();
+#pragma unroll
+    for (int cc = 0; cc < UVC; ++cc)
+      stage_rows<P, F, TM>(VS + cc * TM * LD1, LD1, v + (c0 + cc) * F, 3 * F, row0, N);
     __syncthreads();
     const T* xp = VS + (lane & 15) * LD1 + (lane >> 4) * D::KPL;
 #pragma unroll
     for (int q = 0; q < FTW; ++q) {
       const int ft = wave + NW * q;
-      C au[RT], av[RT];
-      for (int r = 0; r < RT; ++r)
+      C au[UVC * RT], av[UVC * RT];
+      for (int r = 0; r < UVC * RT; ++r)
         for (int i = 0; i < 4; ++i) au[r][i] = av[r][i] = 0;
       const T* wu = Wuv + (size_t)ft * nkb * 64 * D::KPL + (size_t)lane * D::KPL;
       const T* wv = Wuv + (size_t)(NFT + ft) * nkb * 64 * D::KPL + (size_t)lane * D::KPL;
-      kloop<D, nkb, ring_depth<D, 2>(), 2, RT>(
+      kloop<D, nkb, ring_depth<D, 2>(), 2, UVC * RT>(
           xp, LD1,
           [&](int kb, Fd* f) {
             f[0] = D::frag(wu + (size_t)kb * 64 * D::KPL);
@@ -727,31 +747,40 @@ k_update(UpdArgs a) {
 #pragma unroll
             for (int j = 0; j < D::SUB; ++j)
 #pragma unroll
-              for (int r = 0; r < RT; ++r) {
+              for (int r = 0; r < UVC * RT; ++r) {
                 au[r] = D::mfma_sub(x[r], f[0], au[r], j);
                 av[r] = D::mfma_sub(x[r], f[1], av[r], j);
               }
           });
 #pragma unroll
-      for (int r = 0; r < RT; ++r) {
-        U[q][c][r] = au[r];
-        for (int i = 0; i < 4; ++i) {
-          nsq[q][r][i] += av[r][i] * av[r][i];
-          pd[q][r][i] += au[r][i] * av[r][i];
-        }
-        if constexpr (SAVE) {
-          const int col = ft * 16 + (lane & 15);
+      for (int cc = 0; cc < UVC; ++cc)
+#pragma unroll
+        for (int r = 0; r < RT; ++r) {
+          const int c = c0 + cc;
+          const C& u = au[cc * RT + r];
+          const C& w = av[cc * RT + r];
+          U[q][c][r] = u;
           for (int i = 0; i < 4; ++i) {
-            const size_t row = row0 + r * 16 + P::row(lane, i);
-            if (row < (size_t)N) {
-              T* o = (T*)a.save_uv + (row * 3 + c) * 2 * F;
-              o[col] = P::st(au[r][i]);
-              o[F + col] = P::st(av[r][i]);
+            nsq[q][r][i] += w[i] * w[i];
+            pd[q][r][i] += u[i] * w[i];
+          }
+          if constexpr (SAVE) {
+            const int col = ft * 16 + (lane & 15);
+            for (int i = 0; i < 4; ++i) {
+              const size_t row = row0 + r * 16 + P::row(lane, i);
+              if (row < (size_t)N) {
+                T* o = (T*)a.save_uv + (row * 3 + c) * 2 * F;
+                o[col] = P::st(u[i]);
+                o[F + col] = P::st(w[i]);
+              }
             }
           }
         }
-      }
     }
+  }
+  if constexpr (UVC == 3) {
+    __syncthreads();                   // v's slices are dead: [s ; |V|] takes their place
+    stage_rows<P, F, TM>(SN, LD2, s, F, row0, N);
   }
 #pragma unroll
   for (int q = 0; q < FTW; ++q) {
@@ -761,7 +790,6 @@ k_update(UpdArgs a) {
         SN[(r * 16 + P::row(lane, i)) * LD2 + F + col] = P::st(sqrt(nsq[q][r][i]));
   }
   __syncthreads();
-  T* H = VS;
   dense_tiles<P, RT, NW, 2 * F>(SN, LD2, a.upd1, [&](int ct, C* acc) {
     const int col = ct * 16 + (lane & 15);
     const A bias = ((const A*)a.upd1.b)[col];
@@ -835,7 +863,7 @@ k_update(UpdArgs a) {
   }
   if (FUSE_PHI) {
     __syncthreads();
-    phi_tile<P, F, RT, NW>(SN, LD2, VS, row0, N, a.phi1, a.phi2, (T*)a.h);
+    phi_tile<P, F, RT, NW>(SN, LD2, H, row0, N, a.phi1, a.phi2, (T*)a.h);
   }
 }
 
