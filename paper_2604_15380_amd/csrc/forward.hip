@@ -155,7 +155,7 @@ __device__ __forceinline__ int acc_to_index(double x) { return (int)x; }
 //   r = (x_j - x_i) + (n0 a + n1 b) + n2 c  (FP64),  d = |r|,  rhat = r / d,
 //   f_c = (cos(pi d / r_c) + 1) / 2,  g_k = exp(-gamma (d - k Delta)^2).
 // Edge e's geometry and basis row into g (LDS), its rhat and sender into einfo.
-template <class P, bool NB, bool RG>
+template <class P, bool NB, int RG>
 __device__ __forceinline__ void edge_row(long long e, int K, int kcols, double rc, int rbf, double gamma,
                                          double delta, const int32_t* __restrict__ recv,
                                          const int32_t* __restrict__ col, const int32_t* __restrict__ shift,
@@ -182,10 +182,12 @@ __device__ __forceinline__ void edge_row(long long e, int K, int kcols, double r
   // without the bias column the edge info carries f_c instead of the sender
   // (which the kernels then read from the CSR)
   o[3] = NB ? fc : index_to_acc<A>(j);           // the sender index, bit-exact
-  if constexpr (RG) {
-    // the message kernel forms g_k f_c from d / Delta and f_c
-    g[0] = P::st((A)(d / delta));
-    g[1] = P::st(fc);
+  if constexpr (RG != 0) {
+    // the message kernel forms g_k f_c from (d / Delta, f_c), or from
+    // (g_0 f_c, exp(d / Delta - 1/2)) (the record gauss_row reads)
+    const double u = d / delta;
+    g[0] = P::st(RG == 1 ? (A)u : (A)(exp(-0.5 * u * u) * fc));
+    g[1] = P::st(RG == 1 ? fc : (A)exp(u - 0.5));
     for (int k = 2; k < kcols; ++k) g[k] = P::st(0);
     return;
   }
@@ -212,7 +214,7 @@ __device__ __forceinline__ void edge_row(long long e, int K, int kcols, double r
 // scatter one element per lane per store).
 constexpr int EP_THREADS = 64;   // one wave: <= 35 KiB of LDS at the largest row
 
-template <class P, bool NB, bool RG>
+template <class P, bool NB, int RG>
 __global__ void __launch_bounds__(EP_THREADS) k_edge_prep(long long E, int K, int kcols, double rc, int rbf,
                                                   double gamma, double delta,
                                                   const int32_t* __restrict__ recv,
@@ -302,22 +304,42 @@ __device__ __forceinline__ int msg_kcol(int kb, int kk) {
 
 // The Gaussian basis of one MFMA A-operand lane: ga[kb] = f_c g_k with
 // g_k = exp(-(u - k)^2 / 2), u = d / Delta, at the lane's inputs
-// k = msg_kcol(kb, kk).  Two exponentials per lane; the other inputs follow
+// k = msg_kcol(kb, kk), from the edge's record (a, b).  The inputs follow
 // from g(k + m) = g(k) exp(m (u - k) - m^2 / 2):
 //   g(k0 + 1) = g(k0) t,  t = exp(u - k0 - 1/2),
 //   g(k + 8) = g(k) t^8 e^-28 e^-8 (k - k0)   (k0 = 2 kk, the lane's first input).
-// With u and k0 of at most 35 (K <= 36) every factor and every partial
-// product stays inside FP64's normal range, so nothing underflows that the
-// direct formula would keep.
+// With an even number of k-blocks the record is (g_0 f_c, t_0 = exp(u - 1/2))
+// (no exponential in the kernel): t = t_0 e^-k0 and
+// g(k0) = g_0 t_0^k0 e^-k0 (k0 - 1) / 2; with an odd number it is (u, f_c)
+// and the lane takes g(k0), t and its last input by exponentials.  With u of
+// at most 35 (K <= 36) every factor and every partial product stays inside
+// FP64's normal range, so nothing underflows that the direct formula would
+// keep.
 template <int KBM>
-__device__ __forceinline__ void gauss_row(double u, double fc, int kk, double (&ga)[KBM]) {
+constexpr int gauss_form() {
+  return KBM % 2 == 0 ? 2 : 1;
+}
+template <int KBM>
+__device__ __forceinline__ void gauss_row(double a, double b, int kk, double (&ga)[KBM]) {
   constexpr double EM8 = 0x1.5fc21041027adp-12, EM28 = 0x1.853f01d6d53bap-41, EM64 = 0x1.969d47321e4ccp-93;
-  const double x = u - (double)(2 * kk);      // exact: an integer off u
-  double ea = exp(-0.5 * x * x) * fc;          // g(k0) f_c
-  const double t = exp(x - 0.5);
-  double eb = ea * t;                          // g(k0 + 1) f_c
+  double ea, t;
+  if constexpr (gauss_form<KBM>() == 2) {
+    // a = g_0 f_c (zero for a masked row), b = t_0
+    constexpr double EM1 = 0x1.78b56362cef38p-2, EM2 = 0x1.152aaa3bf81ccp-3, EM4 = 0x1.2c155b8213cf4p-6,
+                     EM6 = 0x1.44e51f113d4d6p-9, EM15 = 0x1.4875ca227ec38p-22;
+    const double b2 = b * b, b4 = b2 * b2;
+    const double p = (kk & 1 ? b2 : 1.0) * (kk & 2 ? b4 : 1.0);     // t_0^(2 kk)
+    ea = a * p * (kk == 0 ? 1.0 : kk == 1 ? EM1 : kk == 2 ? EM6 : EM15);
+    t = b * (kk == 0 ? 1.0 : kk == 1 ? EM2 : kk == 2 ? EM4 : EM6);
+  } else {
+    // a = u, b = f_c (zero for a masked row)
+    const double x = a - (double)(2 * kk);      // exact: an integer off u
+    ea = exp(-0.5 * x * x) * b;                  // g(k0) f_c
+    t = exp(x - 0.5);
+  }
+  double eb = ea * t;                            // g(k0 + 1) f_c
   const double t2 = t * t, t4 = t2 * t2;
-  double ra = t4 * t4 * EM28;                  // g(k0 + 8) / g(k0)
+  double ra = t4 * t4 * EM28;                    // g(k0 + 8) / g(k0)
 #pragma unroll
   for (int p = 0; p < KBM / 2; ++p) {
     if (p > 0) {
@@ -329,8 +351,8 @@ __device__ __forceinline__ void gauss_row(double u, double fc, int kk, double (&
     ga[2 * p + 1] = eb;
   }
   if constexpr (KBM & 1) {
-    const double y = u - (double)(4 * (KBM - 1) + kk);
-    ga[KBM - 1] = exp(-0.5 * y * y) * fc;
+    const double y = a - (double)(4 * (KBM - 1) + kk);
+    ga[KBM - 1] = exp(-0.5 * y * y) * b;
   }
 }
 
@@ -403,9 +425,10 @@ __global__ void __launch_bounds__(64 * NGW * NS, 2) k_message(MsgArgs a) {
   const T* sin = (const T*)a.s_in;
   T* s = (T*)a.s;
   T* vout = (T*)a.v_out;
-  // The sender gathers through buffer resources where that was measured
-  // faster (8 k-blocks: -1.3 % on the bulk periodic batch; at 5 the kernel
-  // ran 3.5 % slower, one more register spill landing in its chunk loop)
+  // The sender gathers through buffer resources, and f_c masked once when
+  // the edge info is loaded (not per accumulator row), where that was
+  // measured faster: 8 k-blocks (-1.3 % and -1.8 % on the bulk periodic
+  // batch; with 5 the kernel ran 3.5 % and 3.4 % slower)
   constexpr bool BUF = RG && KBM == 8;
   const size_t hbytes = (size_t)a.N * 3 * F * sizeof(T);
   const __amdgpu_buffer_rsrc_t r_h = buf_rsrc(h, hbytes), r_v = buf_rsrc(vin, hbytes);
@@ -452,6 +475,7 @@ __global__ void __launch_bounds__(64 * NGW * NS, 2) k_message(MsgArgs a) {
       o.xy = *(const d2*)ei;
       o.ze = *(const d2*)(ei + 2);
       o.j = NB ? a.col[e] : 0;
+      if constexpr (BUF) o.ze.y = row < c.cnt ? o.ze.y : 0.0;   // f_c, zero past the chunk's end
     } else {
       o.xy = d2{0.0, 0.0};
       o.ze = d2{0.0, NB ? 0.0 : (double)c.i};
@@ -476,10 +500,15 @@ __global__ void __launch_bounds__(64 * NGW * NS, 2) k_message(MsgArgs a) {
   };
   auto filter = [&](const Ck& c, const T (&Ga)[NGA], const Raw& in, C (&w)[2][3]) {
     T ga[KBM];
-    if constexpr (RG) gauss_row<KBM>(Ga[0], col < c.cnt ? Ga[1] : 0.0, kk, ga);
-    else
+    if constexpr (RG) {
+      // a masked row (past the chunk's end) gets a zero f_c, hence zeros
+      const bool live = col < c.cnt;
+      if constexpr (gauss_form<KBM>() == 2) gauss_row<KBM>(live ? Ga[0] : 0.0, Ga[1], kk, ga);
+      else gauss_row<KBM>(Ga[0], live ? Ga[1] : 0.0, kk, ga);
+    } else {
 #pragma unroll
       for (int kb = 0; kb < KBM; ++kb) ga[kb] = col < c.cnt ? Ga[kb] : 0.0;
+    }
 #pragma unroll
     for (int q = 0; q < 2; ++q)
 #pragma unroll
@@ -514,7 +543,7 @@ __global__ void __launch_bounds__(64 * NGW * NS, 2) k_message(MsgArgs a) {
       // chunk's end)
 #pragma unroll
       for (int ii = 0; ii < 4; ++ii) {
-        const double fc = P::row(lane, ii) < c.cnt ? row_bcast(in.ze.y, ii) : 0.0;
+        const double fc = BUF ? row_bcast(in.ze.y, ii) : P::row(lane, ii) < c.cnt ? row_bcast(in.ze.y, ii) : 0.0;
 #pragma unroll
         for (int part = 0; part < 3; ++part) {
           if (V0 && part == 1) continue;
@@ -1869,6 +1898,7 @@ hipError_t forward_impl(hipStream_t st, ForwardArgs& fa) {
   const int nkb_nb = nb ? pm->layers[0].filt_nb.din_p / P::KC : 0;
   const bool rg = nb && sizeof(T) == 8 && hp.rbf_type == 0 && (nkb_nb == 5 || nkb_nb == 8) &&
                   (size_t)N * 3 * F * sizeof(T) < (1ull << 32);
+  const int rg_form = !rg ? 0 : nkb_nb == 8 ? gauss_form<8>() : gauss_form<5>();
   const int kcols = pm->layers.empty() ? 0 : rg ? 2 : nb ? pm->layers[0].filt_nb.din_p : pm->layers[0].filt_mma.din_p;
   if (N > 0 && fa.stop_layer >= 0) {
     prof_mark(fa.prof, st, KC_EDGE_PREP, true);
@@ -1876,16 +1906,20 @@ hipError_t forward_impl(hipStream_t st, ForwardArgs& fa) {
     const unsigned eg = (unsigned)((g->E + 16 + EP_THREADS - 1) / EP_THREADS);
     const size_t esm = (size_t)EP_THREADS * kcols * sizeof(T);
     const double gamma = 1.0 / (2.0 * delta * delta);
-    if (rg)
-      k_edge_prep<P, true, true><<<eg, EP_THREADS, esm, st>>>(g->E, hp.K, kcols, hp.cutoff, hp.rbf_type, gamma,
+    if (rg_form == 2)
+      k_edge_prep<P, true, 2><<<eg, EP_THREADS, esm, st>>>(g->E, hp.K, kcols, hp.cutoff, hp.rbf_type, gamma,
+                                                           delta, g->recv, g->col, g->shift, g->atom_struct,
+                                                           g->pos, g->cell, (T*)fa.basis, (A*)fa.einfo);
+    else if (rg)
+      k_edge_prep<P, true, 1><<<eg, EP_THREADS, esm, st>>>(g->E, hp.K, kcols, hp.cutoff, hp.rbf_type, gamma,
                                                               delta, g->recv, g->col, g->shift, g->atom_struct,
                                                               g->pos, g->cell, (T*)fa.basis, (A*)fa.einfo);
     else if (nb)
-      k_edge_prep<P, true, false><<<eg, EP_THREADS, esm, st>>>(g->E, hp.K, kcols, hp.cutoff, hp.rbf_type, gamma,
+      k_edge_prep<P, true, 0><<<eg, EP_THREADS, esm, st>>>(g->E, hp.K, kcols, hp.cutoff, hp.rbf_type, gamma,
                                                                delta, g->recv, g->col, g->shift, g->atom_struct,
                                                                g->pos, g->cell, (T*)fa.basis, (A*)fa.einfo);
     else
-      k_edge_prep<P, false, false><<<eg, EP_THREADS, esm, st>>>(g->E, hp.K, kcols, hp.cutoff, hp.rbf_type, gamma,
+      k_edge_prep<P, false, 0><<<eg, EP_THREADS, esm, st>>>(g->E, hp.K, kcols, hp.cutoff, hp.rbf_type, gamma,
                                                                 delta, g->recv, g->col, g->shift, g->atom_struct,
                                                                 g->pos, g->cell, (T*)fa.basis, (A*)fa.einfo);
     prof_mark(fa.prof, st, KC_EDGE_PREP, false);
