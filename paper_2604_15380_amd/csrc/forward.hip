@@ -730,6 +730,18 @@ constexpr int update_nw() {
   return F < 128 ? 4 : F == 128 ? 8 : F / 32;
 }
 
+// Row tiles (16 atoms each) of an update workgroup, as measured fastest per
+// shape: two below F = 256 (one in FP64 at F = 128), one at F >= 256 except
+// FP32 at F = 256 and BF16 at F = 384 (update -5 % and -31 % with two; BF16
+// at F = 256 ran 13 % slower with two, FP32 at F = 384 the same).
+template <class P, int F>
+constexpr int update_rt() {
+  if constexpr (F >= 256)
+    return (P::PREC == PAINN_FP32 && F == 256) || (P::PREC == PAINN_BF16 && F == 384) ? 2 : 1;
+  else
+    return P::PREC == PAINN_FP64 && F == 128 ? 1 : 2;
+}
+
 // Components of v that go through the U/V weights together: three, except
 // where four FP32 waves per SIMD leave too few registers for their
 // accumulators (one at a time there).
@@ -1873,7 +1885,7 @@ hipError_t forward_impl(hipStream_t st, ForwardArgs& fa) {
   const int N = g->N;
   constexpr int RT = ((sizeof(T) == 8 && F >= 256) || F > 256) ? 1 : 2;
   // atoms per update tile / 16: U, |V|^2 and <U, V> of the tile live in registers
-  constexpr int URT = (F >= 256 || (sizeof(T) == 8 && F == 128)) ? 1 : 2;
+  constexpr int URT = update_rt<P, F>();
   T* s = (T*)fa.s;
   T* v[2] = {(T*)fa.v[0], (T*)fa.v[1]};
   T* h = (T*)fa.h;
