@@ -137,6 +137,9 @@ struct MsgArgs {
   // host sets it only where h and v_in are smaller than 4 GiB (the 8-k-block
   // kernel gathers from them with 32-bit byte offsets)
   int rg;
+  // (FP64) room for the workgroups' LDS filter images (MSG64_IMAGE_BYTES),
+  // or null
+  void* img;
 };
 
 constexpr int MSG_RB = 4;   // receivers per workgroup (MSG_RB < 64)
@@ -362,6 +365,50 @@ constexpr int msg64_groups() {
   return F / 32 < (KBM <= 12 ? 4 : 2) ? F / 32 : (KBM <= 12 ? 4 : 2);
 }
 
+typedef double msg_d2 __attribute__((ext_vector_type(2)));
+
+// The LDS filter image of a k_message workgroup owning channel half `half`:
+// entries below NGW 6 NP 64 are the B-fragment pairs
+// [group][q][part][k-block pair][lane], the rest (without the bias column)
+// the b_f pairs [group][part][lane % 16] at a lane's two channels.
+template <int F, int NGW, int KBM, bool NB>
+constexpr int msg64_image_size() {
+  return NGW * 6 * ((KBM + 1) / 2) * 64 + (NB ? NGW * 3 * 16 : 0);
+}
+template <int F, int NGW, int KBM>
+__device__ __forceinline__ msg_d2 msg64_image_entry(const MsgArgs& a, int half, int x) {
+  constexpr int NP = (KBM + 1) / 2, NBF = NGW * 6 * NP * 64;
+  if (x < NBF) {
+    const double* Wf = (const double*)a.filt_mma.w;
+    const int l = x & 63, p = (x >> 6) % NP, qp = (x >> 6) / NP % 6, g = (x >> 6) / NP / 6;
+    // packed fragment element (row n, input k): tile n / 16, k-block k / 4,
+    // lane n % 16 + 16 (k % 4)
+    const int n = qp % 3 * F + 32 * (half * NGW + g) + 2 * (l & 15) + qp / 3;
+    double v[2];
+#pragma unroll
+    for (int hh = 0; hh < 2; ++hh) {
+      const int kb = 2 * p + hh, k = msg_kcol<KBM>(kb, l >> 4);
+      v[hh] = kb < KBM ? Wf[((size_t)((n >> 4) * KBM + (k >> 2)) * 64 + (n & 15) + 16 * (k & 3))] : 0.0;
+    }
+    return msg_d2{v[0], v[1]};
+  }
+  x -= NBF;
+  const int c = x % 16, part = x / 16 % 3, g = x / 48;
+  const double* fb = (const double*)a.fbias + part * F + 32 * (half * NGW + g) + 2 * c;
+  return msg_d2{fb[0], fb[1]};
+}
+
+// Once per layer: every channel half's image (blockIdx.y = half), so that
+// each message workgroup fills its LDS with 16-byte copies instead of
+// gathering scattered 8-byte fragments (bulk periodic message -0.7 %).
+template <int F, int NGW, int KBM, bool NB>
+__global__ void __launch_bounds__(256) k_msg64_image(MsgArgs a, msg_d2* __restrict__ img) {
+  constexpr int IMG = msg64_image_size<F, NGW, KBM, NB>();
+  const int half = blockIdx.y;
+  for (int x = blockIdx.x * 256 + threadIdx.x; x < IMG; x += gridDim.x * 256)
+    img[(size_t)half * IMG + x] = msg64_image_entry<F, NGW, KBM>(a, half, x);
+}
+
 template <class P, int F, int NGW, int NS, int KBM, bool V0, bool NB, bool RG>
 __global__ void __launch_bounds__(64 * NGW * NS, 2) k_message(MsgArgs a) {
   using T = typename P::T;
@@ -390,26 +437,15 @@ __global__ void __launch_bounds__(64 * NGW * NS, 2) k_message(MsgArgs a) {
   const int ib = (lb / SPLIT) * MSG_RB64, half = lb % SPLIT;
   if (ib >= a.N) return;                       // the whole workgroup
   {
-    const T* Wf = (const T*)a.filt_mma.w;
-    for (int x = threadIdx.x; x < NGW * 6 * NP * 64; x += NGW * NS * 64) {
-      const int l = x & 63, p = (x >> 6) % NP, qp = (x >> 6) / NP % 6, g = (x >> 6) / NP / 6;
-      // packed fragment element (row n, input k): tile n / 16, k-block k / 4,
-      // lane n % 16 + 16 (k % 4)
-      const int n = qp % 3 * F + 32 * (half * NGW + g) + 2 * (l & 15) + qp / 3;
-      double v[2];
-#pragma unroll
-      for (int hh = 0; hh < 2; ++hh) {
-        const int kb = 2 * p + hh, k = msg_kcol<KBM>(kb, l >> 4);
-        v[hh] = kb < KBM ? Wf[((size_t)((n >> 4) * KBM + (k >> 2)) * 64 + (n & 15) + 16 * (k & 3))] : 0.0;
-      }
-      bsh[x] = d2{v[0], v[1]};
-    }
+    // the workgroup's filter image: copied from the layer's image where the
+    // host wrote one, else gathered here
+    constexpr int NBF = NGW * 6 * NP * 64, IMG = msg64_image_size<F, NGW, KBM, NB>();
+    const d2* im = a.img ? (const d2*)a.img + (size_t)half * IMG : nullptr;
+    for (int x = threadIdx.x; x < NBF; x += NGW * NS * 64)
+      bsh[x] = a.img ? im[x] : msg64_image_entry<F, NGW, KBM>(a, half, x);
     if constexpr (NB)
-      for (int x = threadIdx.x; x < NGW * 3 * 16; x += NGW * NS * 64) {
-        const int c = x % 16, part = x / 16 % 3, g = x / 48;
-        const double* fb = (const double*)a.fbias + part * F + 32 * (half * NGW + g) + 2 * c;
-        bias_sh[x] = d2{fb[0], fb[1]};
-      }
+      for (int x = threadIdx.x; x < NGW * 3 * 16; x += NGW * NS * 64)
+        bias_sh[x] = a.img ? im[NBF + x] : msg64_image_entry<F, NGW, KBM>(a, half, NBF + x);
   }
   __syncthreads();                             // (the only barrier)
   const int i0 = ib + st * RBS;
@@ -1549,8 +1585,13 @@ void launch_message_kbm(hipStream_t st, const MsgArgs& a) {
     // eight waves per workgroup: NGW channel groups times NS streams
     constexpr int NGW = msg64_groups<F, KBM>(), NS = 8 / NGW, SPLIT = F / 32 / NGW;
     const int blocks = ((a.N + MSG_RB64 - 1) / MSG_RB64 * SPLIT + 7) / 8 * 8;   // a multiple of the 8 XCDs
-    if (a.v_zero) k_message<P, F, NGW, NS, KBM, true, NB, RG><<<blocks, 512, 0, st>>>(a);
-    else k_message<P, F, NGW, NS, KBM, false, NB, RG><<<blocks, 512, 0, st>>>(a);
+    constexpr int IMG = msg64_image_size<F, NGW, KBM, NB>();
+    MsgArgs b = a;
+    if ((size_t)SPLIT * IMG * sizeof(msg_d2) > MSG64_IMAGE_BYTES) b.img = nullptr;
+    if (b.img)
+      k_msg64_image<F, NGW, KBM, NB><<<dim3((IMG + 255) / 256, SPLIT), 256, 0, st>>>(b, (msg_d2*)b.img);
+    if (a.v_zero) k_message<P, F, NGW, NS, KBM, true, NB, RG><<<blocks, 512, 0, st>>>(b);
+    else k_message<P, F, NGW, NS, KBM, false, NB, RG><<<blocks, 512, 0, st>>>(b);
   } else {
     const int blocks = ((a.N + MSG_RB2 - 1) / MSG_RB2 + 7) / 8 * 8;
     if (a.v_zero) k_message_lane<P, F, KBM, true, NB><<<blocks, F, 0, st>>>(a);
@@ -1960,6 +2001,7 @@ hipError_t forward_impl(hipStream_t st, ForwardArgs& fa) {
     ma.filt_mma = nb ? Ld.filt_nb : Ld.filt_mma;
     ma.nb = nb;
     ma.rg = rg;
+    ma.img = fa.msg_img;
     ma.col = g->col;
     ma.fbias = Ld.filt_nb.b;
     ma.h = fa.save ? sv.H(l) : h;

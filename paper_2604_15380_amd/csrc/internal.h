@@ -269,7 +269,16 @@ struct ForwardArgs {
   double* s_out;           // feature export (may be null)
   double* v_out;
   void* save;              // per-layer activations for the reverse pass (may be null)
+  // (FP64) the message kernel's LDS image of each layer's filter, written per
+  // layer before the message (MSG64_IMAGE_BYTES; may be null: the kernel
+  // then gathers its filter fragments itself)
+  void* msg_img;
 };
+
+// Upper bound of that image: 2-way channel split x 4 groups x (6 x 4 fragment
+// pairs x 64 lanes + 3 x 16 bias pairs) x 16 bytes, at F <= 384 at most 12
+// groups in all.
+constexpr size_t MSG64_IMAGE_BYTES = (size_t)12 * (6 * 4 * 64 + 3 * 16) * 16;
 
 // The activations a forward run keeps for the reverse pass (storage type,
 // element size es).  Layer l: S(l) = s before the message [N][F], V(l) = v

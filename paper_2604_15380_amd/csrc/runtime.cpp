@@ -305,7 +305,7 @@ size_t forward_workspace_bytes(int prec, int N, long long E, int F, int kcols, i
   auto al = [](size_t x) { return (x + 255) & ~(size_t)255; };
   const size_t n = (size_t)N, ne = (size_t)E, ent = n * (blend ? (size_t)H : 1);
   size_t b = al(n * F * eb) + 3 * al(n * 3 * F * eb) + al(n * ab) + al((ne + 16) * kcols * eb) +
-             al(ne * 4 * ab) + al(1024) + al(head_tiles_bytes(ent)) + al(ent * 4);
+             al(ne * 4 * ab) + al(1024) + al(head_tiles_bytes(ent)) + al(ent * 4) + al(MSG64_IMAGE_BYTES);
   if (blend) b += al((size_t)B * pad32(S) * eb) + al((size_t)B * H * ab) + al(n * H * ab);
   return b;
 }
@@ -786,6 +786,7 @@ static painn_status run_forward(painn_ctx* ctx, const painn_model* model, const 
   a.e = p; p += al(N * ab);
   a.basis = p; p += al(((size_t)g->E + 16) * kcols * eb);
   a.einfo = p; p += al((size_t)g->E * 4 * ab);
+  a.msg_img = p; p += al(MSG64_IMAGE_BYTES);
   const size_t ent = N * (blend ? (size_t)m->hp.n_heads : 1);
   a.head_plan = p; p += al(1024);
   a.head_tiles = p; p += al(head_tiles_bytes(ent));
