@@ -252,7 +252,9 @@ __global__ void __launch_bounds__(EP_THREADS) k_edge_prep(long long E, int K, in
 // waves split those receivers, wave w of a stream owning channel group w.
 // The group's filter columns are staged in LDS once per workgroup (shared
 // by its streams), which leaves each wave the registers for two waves per
-// SIMD: one wave's loads and arithmetic then run under the other's MFMAs.
+// SIMD: one wave's loads run under the other's MFMAs.  (FP64 MFMAs and FP64
+// vector instructions take turns at issue on this chip, equal peaks, so the
+// kernel's vector instruction count adds to its time directly.)
 //
 // A wave's channel group is two MFMA column tiles whose columns interleave:
 // column c of tile q is channel 32 g + 2 c + q, so a lane's two accumulator
@@ -264,13 +266,15 @@ __global__ void __launch_bounds__(EP_THREADS) k_edge_prep(long long E, int K, in
 // address unit costs about the same per instruction at 8 and 16 bytes per
 // lane: halving the instructions is what lets the MFMAs keep busy.
 //
-// A stream's receivers form one sequence of 16-edge chunks (a receiver
+// A stream's receivers form one sequence of 16-edge chunks: with in-kernel
+// Gaussians (RG) the stream's edges cut into chunks regardless of where
+// receivers end, otherwise each receiver's edges on their own (a receiver
 // without edges still takes one, empty, so that its row is written).  Per
 // chunk the wave issues the sender gathers, prefetches the next chunk's
-// edge info (and basis rows), runs the filter MFMAs and combines their
+// edge info (and basis record), runs the filter MFMAs and combines their
 // accumulators (row = edge, col = channel) with the gathered features
 // directly; a receiver's per-lane partial sums are reduced across the four
-// row groups of the wavefront after its last chunk.
+// row groups of the wavefront after its last edge.
 constexpr int MSG_RB64 = 32;   // receivers per workgroup
 
 // Lane n of each 16-lane row, broadcast to its row (DPP row_newbcast).
