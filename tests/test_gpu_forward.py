@@ -276,3 +276,37 @@ def test_edge_cases_and_errors(rt):
     out = rt.forward(m, ge, "bf16")
     assert out.numel() == 0
     ge.free()
+
+
+@pytest.mark.parametrize("name", ["bulk_1024", "molecules_4096"])
+def test_gaussian_basis_extremes_fp64(rt, name):
+    """FP64 forward at the ends of the Gaussian basis the message kernels form
+    themselves (K = 32 at 8 k-blocks, K = 20 at 5): edges of 0.05 A (the
+    first Gaussians near 1, the last ones near exp(-(K - 1)^2 / 2)), edges
+    just inside the cutoff (f_c of order 1e-16 and 1e-8), a chain whose pair
+    distances sweep the whole range, and a dense cluster whose receivers
+    have more than 16 edges each (chunks shared by several receivers)."""
+    hp, W = synth.workload_weights(name)
+    rc = hp.cutoff
+    z0 = np.zeros((3, 3))
+    np0 = np.zeros(3, np.uint8)
+    rng = np.random.default_rng(7)
+    chain = np.cumsum(np.concatenate([[0.0], [0.05, 0.2, 0.55, 0.9, 1.3, 0.7, 0.35, 1.6, 0.8, 1.1]]))
+    cluster = []
+    while len(cluster) < 40:      # 20-39 neighbours per atom
+        p = rng.uniform(-2.6, 2.6, 3)
+        if all(np.linalg.norm(p - q) > 0.9 for q in cluster):
+            cluster.append(p)
+    structs = [
+        (np.array([[0.0, 0, 0], [0.05, 0, 0]]), np.array([3, 5], np.int32), z0, np0, 0),
+        (np.array([[0.0, 0, 0], [rc * (1 - 1e-9), 0, 0]]), np.array([2, 2], np.int32), z0, np0, 0),
+        (np.array([[0.0, 0, 0], [0, rc - 1e-4, 0]]), np.array([1, 4], np.int32), z0, np0, 0),
+        (np.stack([chain, 0.1 * np.sin(chain), np.zeros_like(chain)], 1), (np.arange(len(chain)) % 9 + 1).astype(np.int32),
+         z0, np0, 0),
+        (np.array(cluster), (np.arange(40) % 7 + 1).astype(np.int32), z0, np0, 0),
+    ]
+    b = synth.concat(structs)
+    say(f"forward {name} fp64, Gaussian basis extremes: {b.n_struct} structures, {b.n_atoms} atoms")
+    E = run(rt, name, b, "fp64")
+    Er, Ar = oracle_energies(name, b, range(b.n_struct), workers=1)
+    check_energies(E, Er, Ar, TOL["fp64"], f"{name} fp64 basis extremes")
