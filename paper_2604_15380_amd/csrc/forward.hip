@@ -838,6 +838,11 @@ k_update(UpdArgs a) {
   using D = dense_t<P>;   // operand form of the dense layers
   using Fd = typename D::Fr;
   constexpr int nkb = F / D::KC;
+  // the multi-stream K loops (U/V, the gate's output layer) keep twice the
+  // ring in FP64 at F >= 256, where one workgroup per CU leaves the registers
+  // (measured: update -1.9 % bulk periodic, -3.2 % lead model; -1 % slower
+  // at F = 128)
+  constexpr int RX = P::PREC == PAINN_FP64 && F >= 256 ? 2 : 1;
   const T* Wuv = (const T*)a.uv.w;
   if constexpr (UVC == 1) stage_rows<P, F, TM>(SN, LD2, s, F, row0, N);
   // UVC components against each weight fragment: the UVC RT row tiles of VS
@@ -858,7 +863,7 @@ k_update(UpdArgs a) {
         for (int i = 0; i < 4; ++i) au[r][i] = av[r][i] = 0;
       const T* wu = Wuv + (size_t)ft * nkb * 64 * D::KPL + (size_t)lane * D::KPL;
       const T* wv = Wuv + (size_t)(NFT + ft) * nkb * 64 * D::KPL + (size_t)lane * D::KPL;
-      kloop<D, nkb, ring_depth<D, 2>(), 2, UVC * RT>(
+      kloop<D, nkb, ring_depth<D, 2, RX>(), 2, UVC * RT>(
           xp, LD1,
           [&](int kb, Fd* f) {
             f[0] = D::frag(wu + (size_t)kb * 64 * D::KPL);
@@ -941,7 +946,7 @@ k_update(UpdArgs a) {
       const T* w0 = W2 + (size_t)ft * nkb2 * 64 * D::KPL + (size_t)lane * D::KPL;
       const T* w1 = W2 + (size_t)(NFT + ft) * nkb2 * 64 * D::KPL + (size_t)lane * D::KPL;
       const T* w2 = W2 + (size_t)(2 * NFT + ft) * nkb2 * 64 * D::KPL + (size_t)lane * D::KPL;
-      kloop<D, nkb2, ring_depth<D, 3>(), 3, RT>(
+      kloop<D, nkb2, ring_depth<D, 3, RX>(), 3, RT>(
           xp, LD1,
           [&](int kb, Fd* f) {
             f[0] = D::frag(w0 + (size_t)kb * 64 * D::KPL);

@@ -283,11 +283,11 @@ __device__ __forceinline__ void kloop_rt(int nkb, const typename P::T* xp, int l
 }
 
 // Prefetch distance of a K loop over NS fragment streams: as many steps as
-// fit a ring of P::RING VGPRs (measured per precision: more spills the
+// fit a ring of X P::RING VGPRs (measured per precision: more spills the
 // update kernel at three waves per SIMD), a power of two from 1 to 8.
-template <class P, int NS>
+template <class P, int NS, int X = 1>
 constexpr int ring_depth() {
-  constexpr int n = P::RING / (NS * (int)sizeof(typename P::Fr) / 4);
+  constexpr int n = X * P::RING / (NS * (int)sizeof(typename P::Fr) / 4);
   return n >= 8 ? 8 : n >= 4 ? 4 : n >= 2 ? 2 : 1;
 }
 
