@@ -839,10 +839,11 @@ k_update(UpdArgs a) {
   using Fd = typename D::Fr;
   constexpr int nkb = F / D::KC;
   // the multi-stream K loops (U/V, the gate's output layer) keep twice the
-  // ring in FP64 at F >= 256, where one workgroup per CU leaves the registers
-  // (measured: update -1.9 % bulk periodic, -3.2 % lead model; -1 % slower
-  // at F = 128)
-  constexpr int RX = P::PREC == PAINN_FP64 && F >= 256 ? 2 : 1;
+  // ring where that measured faster: FP64 at F >= 256 (update -1.9 % bulk
+  // periodic, -3.2 % lead model; 1 % slower at F = 128) and BF16 at F = 256
+  // (-3.4 % screening; FP32 at F >= 256 ran 1-2 % slower, BF16 at F = 384
+  // the same)
+  constexpr int RX = (P::PREC == PAINN_FP64 && F >= 256) || (P::PREC == PAINN_BF16 && F == 256) ? 2 : 1;
   const T* Wuv = (const T*)a.uv.w;
   if constexpr (UVC == 1) stage_rows<P, F, TM>(SN, LD2, s, F, row0, N);
   // UVC components against each weight fragment: the UVC RT row tiles of VS
