@@ -140,6 +140,7 @@ struct MsgArgs {
   // (FP64) room for the workgroups' LDS filter images (MSG64_IMAGE_BYTES),
   // or null
   void* img;
+  long long E;         // edges of the graph (the FP64 receiver block size)
 };
 
 constexpr int MSG_RB = 4;   // receivers per workgroup (MSG_RB < 64)
@@ -247,7 +248,7 @@ __global__ void __launch_bounds__(EP_THREADS) k_edge_prep(long long E, int K, in
 }
 
 
-// FP64, per layer.  SPLIT workgroups share MSG_RB64 consecutive receivers,
+// FP64, per layer.  SPLIT workgroups share RB consecutive receivers,
 // each owning NGW groups of 32 channels; the workgroup's NS streams of NGW
 // waves split those receivers, wave w of a stream owning channel group w.
 // The group's filter columns are staged in LDS once per workgroup (shared
@@ -275,7 +276,14 @@ __global__ void __launch_bounds__(EP_THREADS) k_edge_prep(long long E, int K, in
 // accumulators (row = edge, col = channel) with the gathered features
 // directly; a receiver's per-lane partial sums are reduced across the four
 // row groups of the wavefront after its last edge.
-constexpr int MSG_RB64 = 32;   // receivers per workgroup
+// Receivers per workgroup: 32, or 16 for the in-kernel-Gaussian kernels on
+// batches of at least MSG_RB16_DEGREE edges per receiver, whose streams of
+// 16 receivers already hold many chunks and whose fewer receivers in flight
+// per XCD keep more sender rows in its L2 (measured: bulk periodic batch,
+// 72 edges per receiver, message -4.3 %; screening batch, 30, -0.4 %;
+// molecules, 15, 2.6 % slower).
+constexpr int MSG_RB64 = 32;
+constexpr int MSG_RB16_DEGREE = 24;
 
 // Lane n of each 16-lane row, broadcast to its row (DPP row_newbcast).
 __device__ __forceinline__ int row_bcast(int x, int n) {
@@ -413,7 +421,7 @@ __global__ void __launch_bounds__(256) k_msg64_image(MsgArgs a, msg_d2* __restri
     img[(size_t)half * IMG + x] = msg64_image_entry<F, NGW, KBM>(a, half, x);
 }
 
-template <class P, int F, int NGW, int NS, int KBM, bool V0, bool NB, bool RG>
+template <class P, int F, int NGW, int NS, int KBM, bool V0, bool NB, bool RG, int RB>
 __global__ void __launch_bounds__(64 * NGW * NS, 2) k_message(MsgArgs a) {
   using T = typename P::T;
   using C = typename P::C;
@@ -422,8 +430,8 @@ __global__ void __launch_bounds__(64 * NGW * NS, 2) k_message(MsgArgs a) {
   // basis values a lane keeps per chunk: its KBM inputs, or (d / Delta, f_c)
   constexpr int NGA = RG ? 2 : KBM;
   typedef double d2 __attribute__((ext_vector_type(2)));
-  constexpr int NG = F / 32, SPLIT = NG / NGW, NP = (KBM + 1) / 2, RBS = MSG_RB64 / NS;
-  static_assert(NG % NGW == 0 && MSG_RB64 % NS == 0 && RBS < 64, "workgroup shape");
+  constexpr int NG = F / 32, SPLIT = NG / NGW, NP = (KBM + 1) / 2, RBS = RB / NS;
+  static_assert(NG % NGW == 0 && RB % NS == 0 && RBS < 64, "workgroup shape");
   constexpr int kcols = KBM * P::KC;  // the filter input is padded to KBM k-blocks
   // [group][q][part][k-block pair][lane]: the two B fragments of a pair;
   // without the bias column, b_f [group][part][lane % 16] at the lane's two
@@ -438,7 +446,7 @@ __global__ void __launch_bounds__(64 * NGW * NS, 2) k_message(MsgArgs a) {
   // the SPLIT workgroups of a receiver block read its basis from one L2.
   const int per_xcd = gridDim.x / 8;
   const int lb = (blockIdx.x % 8) * per_xcd + blockIdx.x / 8;
-  const int ib = (lb / SPLIT) * MSG_RB64, half = lb % SPLIT;
+  const int ib = (lb / SPLIT) * RB, half = lb % SPLIT;
   if (ib >= a.N) return;                       // the whole workgroup
   {
     // the workgroup's filter image: copied from the layer's image where the
@@ -1594,14 +1602,22 @@ void launch_message_kbm(hipStream_t st, const MsgArgs& a) {
   if constexpr (sizeof(typename P::T) == 8) {
     // eight waves per workgroup: NGW channel groups times NS streams
     constexpr int NGW = msg64_groups<F, KBM>(), NS = 8 / NGW, SPLIT = F / 32 / NGW;
-    const int blocks = ((a.N + MSG_RB64 - 1) / MSG_RB64 * SPLIT + 7) / 8 * 8;   // a multiple of the 8 XCDs
     constexpr int IMG = msg64_image_size<F, NGW, KBM, NB>();
     MsgArgs b = a;
     if ((size_t)SPLIT * IMG * sizeof(msg_d2) > MSG64_IMAGE_BYTES) b.img = nullptr;
     if (b.img)
       k_msg64_image<F, NGW, KBM, NB><<<dim3((IMG + 255) / 256, SPLIT), 256, 0, st>>>(b, (msg_d2*)b.img);
-    if (a.v_zero) k_message<P, F, NGW, NS, KBM, true, NB, RG><<<blocks, 512, 0, st>>>(b);
-    else k_message<P, F, NGW, NS, KBM, false, NB, RG><<<blocks, 512, 0, st>>>(b);
+    // grids are a multiple of the 8 XCDs
+    if (RG && a.E >= (long long)MSG_RB16_DEGREE * a.N) {
+      constexpr int RB = RG ? 16 : MSG_RB64;
+      const int blocks = ((a.N + RB - 1) / RB * SPLIT + 7) / 8 * 8;
+      if (a.v_zero) k_message<P, F, NGW, NS, KBM, true, NB, RG, RB><<<blocks, 512, 0, st>>>(b);
+      else k_message<P, F, NGW, NS, KBM, false, NB, RG, RB><<<blocks, 512, 0, st>>>(b);
+    } else {
+      const int blocks = ((a.N + MSG_RB64 - 1) / MSG_RB64 * SPLIT + 7) / 8 * 8;
+      if (a.v_zero) k_message<P, F, NGW, NS, KBM, true, NB, RG, MSG_RB64><<<blocks, 512, 0, st>>>(b);
+      else k_message<P, F, NGW, NS, KBM, false, NB, RG, MSG_RB64><<<blocks, 512, 0, st>>>(b);
+    }
   } else {
     const int blocks = ((a.N + MSG_RB2 - 1) / MSG_RB2 + 7) / 8 * 8;
     if (a.v_zero) k_message_lane<P, F, KBM, true, NB><<<blocks, F, 0, st>>>(a);
@@ -2012,6 +2028,7 @@ hipError_t forward_impl(hipStream_t st, ForwardArgs& fa) {
     ma.nb = nb;
     ma.rg = rg;
     ma.img = fa.msg_img;
+    ma.E = g->E;
     ma.col = g->col;
     ma.fbias = Ld.filt_nb.b;
     ma.h = fa.save ? sv.H(l) : h;
