@@ -1031,8 +1031,12 @@ k_message_bwd(MsgBwdArgs a) {
     // they are few (FP32, K + 1 <= 24); otherwise they stream from the
     // caches chunk by chunk (an opaque copy of the pointer keeps the
     // compiler from hoisting them out of the loops).
-    const T* Wc = Wf;
-    if constexpr (FTW * 3 * KBM * (int)sizeof(A) / 4 > 40) asm volatile("" : "+s"(Wc));
+    // (The copy passes through an integer and back to a global pointer, so
+    // that the loads stay global loads rather than flat ones, which would
+    // also hold up the LDS wait counter the reduce-scatter needs.)
+    uintptr_t wbits = (uintptr_t)Wf;
+    if constexpr (FTW * 3 * KBM * (int)sizeof(A) / 4 > 40) asm volatile("" : "+s"(wbits));
+    const T* Wc = (const T*)(const T __attribute__((address_space(1)))*)wbits;
     // per-edge partial sums: [dE/dd, dE/drhat x, y, z] x 4 rows
     A vals[16];
 #pragma unroll
@@ -1314,8 +1318,11 @@ k_message_bwd_lane(MsgBwdArgs a) {
     const bool more = cn < T1;
     if (more) prefetch(cn, min(16, T1 - cn));
     // w and w' of 4 feature tiles x 3 parts into LDS
-    const T* Wc = Wf;
-    if constexpr (!BREG) asm volatile("" : "+s"(Wc));
+    // (Through an integer and back to a global pointer, as in the MFMA
+    // kernel above, so that the loads stay global loads.)
+    uintptr_t wbits = (uintptr_t)Wf;
+    if constexpr (!BREG) asm volatile("" : "+s"(wbits));
+    const T* Wc = (const T*)(const T __attribute__((address_space(1)))*)wbits;
 #pragma unroll
     for (int q0 = 0; q0 < 4; q0 += QI) {
       C w[QI][3], wd[QI][3];
