@@ -837,10 +837,22 @@ struct MsgBwdArgs {
   void* gv_out;
   void* eg;            // [E][NW][4]
   int first;           // the first layer: only eg is wanted (g_h, g_v are not written)
+  int bg;              // g_s', g_v' gathered by buffer loads (g_v' below 2 GiB)
 };
 
 __device__ __forceinline__ int acc_index(float x) { return __float_as_int(x); }
 __device__ __forceinline__ int acc_index(double x) { return (int)x; }
+
+// Raw buffer resource over [p, p + bytes) (bytes < 4 GiB): loads at offsets
+// past the end read as zero.
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t buf_rsrc(const void* p, size_t bytes) {
+  return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(p), (short)0, (int)(uint32_t)bytes, 0x00020000);
+}
+template <class V>
+__device__ __forceinline__ V buf_ld8(__amdgpu_buffer_rsrc_t r, uint32_t off, int soff) {
+  return __builtin_bit_cast(V, __builtin_amdgcn_raw_buffer_load_b64(r, off, soff, 0));
+}
+typedef double bwd_d2 __attribute__((ext_vector_type(2)));
 
 // vals[k] summed over the 16 lanes of a row group, for k = lane % 16.
 template <class A, int LEN>
@@ -907,6 +919,14 @@ k_message_bwd(MsgBwdArgs a) {
   const A* einfo = (const A*)a.einfo;
   const T* basis = (const T*)a.basis;
   const T* dbasis = (const T*)a.dbasis;
+  static_assert(sizeof(A) == 8, "the MFMA form runs FP64");
+  using A2 = bwd_d2;
+  // per wave 16 rows of 64 values (+2: the rows' 16-byte groups start on
+  // different banks)
+  constexpr int RED_LD = 64 + 2;
+  __shared__ __attribute__((aligned(16))) A red[NWB * 16 * RED_LD];
+  const __amdgpu_buffer_rsrc_t r_gs = buf_rsrc(gs, a.bg ? (size_t)a.N * F * sizeof(A) : 0);
+  const __amdgpu_buffer_rsrc_t r_gv = buf_rsrc(gv, a.bg ? (size_t)a.N * 3 * F * sizeof(A) : 0);
   const int j0 = lb / SLICES * MB_RB;
   if (j0 >= a.N) return;
   const int j1 = min(a.N, j0 + MB_RB);
@@ -1014,17 +1034,41 @@ k_message_bwd(MsgBwdArgs a) {
     }
     // the receivers' g_s', g_v' at this lane's channels, all issued before
     // the matrix cores start (they do not depend on the filter)
+    // Rows past the chunk must add exactly nothing (not 0 x receiver 0's
+    // gradient, which may be NaN): their gathers read zeros.  With buffer
+    // loads such a row's offset lies past the buffer, which reads as zero
+    // (32-bit offsets, no per-value select); otherwise the values are
+    // selected away.
     A gsr[FTW][4], gvr[FTW][4][3];
+    if (a.bg) {
 #pragma unroll
-    for (int q = 0; q < FTW; ++q) {
-      const int ch = (FTW * wave + q) * 16 + (lane & 15);
+      for (int q = 0; q < FTW; ++q) {
+        const uint32_t ch8 = (uint32_t)((FTW * wave + q) * 16 + (lane & 15)) * sizeof(A);
 #pragma unroll
-      for (int i = 0; i < 4; ++i) {
-        const size_t ib = (size_t)ir[i] * 3 * F;
-        gsr[q][i] = gs[(size_t)ir[i] * F + ch];
-        gvr[q][i][0] = gv[ib + ch];
-        gvr[q][i][1] = gv[ib + F + ch];
-        gvr[q][i][2] = gv[ib + 2 * F + ch];
+        for (int i = 0; i < 4; ++i) {
+          const bool live = er[i] >= 0;
+          const uint32_t os = live ? (uint32_t)ir[i] * (F * sizeof(A)) + ch8 : 0x80000000u;
+          const uint32_t ov = live ? (uint32_t)ir[i] * (3 * F * sizeof(A)) + ch8 : 0x80000000u;
+          gsr[q][i] = buf_ld8<A>(r_gs, os, 0);
+#pragma unroll
+          for (int k = 0; k < 3; ++k) gvr[q][i][k] = buf_ld8<A>(r_gv, ov, k * F * (int)sizeof(A));
+        }
+      }
+    } else {
+#pragma unroll
+      for (int q = 0; q < FTW; ++q) {
+        const int ch = (FTW * wave + q) * 16 + (lane & 15);
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+          const size_t ib = (size_t)ir[i] * 3 * F;
+          const bool live = er[i] >= 0;
+          const A s0 = gs[(size_t)ir[i] * F + ch];
+          const A v0 = gv[ib + ch], v1 = gv[ib + F + ch], v2 = gv[ib + 2 * F + ch];
+          gsr[q][i] = live ? s0 : A(0);
+          gvr[q][i][0] = live ? v0 : A(0);
+          gvr[q][i][1] = live ? v1 : A(0);
+          gvr[q][i][2] = live ? v2 : A(0);
+        }
       }
     }
     // The filter fragments stay in registers for the whole kernel when
@@ -1063,11 +1107,7 @@ k_message_bwd(MsgBwdArgs a) {
       const A v2 = L0 ? A(0) : P::ld(vv[jb + 2 * F + ch]);
 #pragma unroll
       for (int i = 0; i < 4; ++i) {
-        // rows past the chunk add exactly nothing (not 0 x receiver 0's
-        // gradient, which may be NaN)
-        const bool live = er[i] >= 0;
-        const A g_s = live ? gsr[q][i] : A(0), g0 = live ? gvr[q][i][0] : A(0);
-        const A g1 = live ? gvr[q][i][1] : A(0), g2 = live ? gvr[q][i][2] : A(0);
+        const A g_s = gsr[q][i], g0 = gvr[q][i][0], g1 = gvr[q][i][1], g2 = gvr[q][i][2];
         const A Ar = g0 * rh[i][0] + g1 * rh[i][1] + g2 * rh[i][2];
         const A tr = hr * w[2][i];
         if constexpr (L0) {
@@ -1088,14 +1128,29 @@ k_message_bwd(MsgBwdArgs a) {
         vals[12 + i] += g2 * tr;
       }
     }
-    // lane: the wave's total of value (lane % 16) / 4 for its row lane % 4
-    reduce_scatter16<A, 16>(vals, lane);
+    // lane: the wave's total of value (lane % 16) / 4 for its row lane % 4,
+    // over the 16 lanes of its row group, through the wave's LDS rows: value
+    // k of every lane in row k, then each lane sums 16 consecutive entries
+    // of its row (one write and read per value instead of a butterfly of
+    // selects and lane shuffles)
     {
+      A* rw = red + (threadIdx.x >> 6) * (16 * RED_LD);
+#pragma unroll
+      for (int k = 0; k < 16; ++k) rw[k * RED_LD + lane] = vals[k];
+      __builtin_amdgcn_wave_barrier();
+      const A* rr = rw + (lane & 15) * RED_LD + (lane >> 4) * 16;
+      A2 t[8];
+#pragma unroll
+      for (int u = 0; u < 8; ++u) t[u] = *(const A2*)(rr + 2 * u);
+      __builtin_amdgcn_wave_barrier();
+      A sum = 0;
+#pragma unroll
+      for (int u = 0; u < 8; ++u) sum += t[u][0] + t[u][1];
       const int k = lane & 15, i = k & 3;
       const int e = i == 0 ? er[0] : i == 1 ? er[1] : i == 2 ? er[2] : er[3];
       // one add per slot per launch, and launches run in layer order: the
       // sums are deterministic; the add does not return, so no wave waits
-      if (e >= 0) unsafeAtomicAdd(eg + ((size_t)e * NW + wave) * 4 + (k >> 2), vals[0]);
+      if (e >= 0) unsafeAtomicAdd(eg + ((size_t)e * NW + wave) * 4 + (k >> 2), sum);
     }
     if (!PF) find_next();
     if (last && !L0) {
@@ -1696,6 +1751,7 @@ hipError_t backward_impl(hipStream_t st, BackwardArgs& ba) {
     ma.gv_out = ba.gv;
     ma.eg = ba.eg;
     ma.first = l == 0;
+    ma.bg = (size_t)N * 3 * F * sizeof(A) < ((size_t)1 << 31);
     prof_mark(ba.prof, st, KC_BWD_MESSAGE, true);
     e = launch_message_bwd<P, F>(st, ma, kcols / P::KC);
     prof_mark(ba.prof, st, KC_BWD_MESSAGE, false);

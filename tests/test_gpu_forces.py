@@ -436,3 +436,52 @@ def test_past_256_scan_blocks(rt):
     check_forces(Fo, b, ref, idx, FORCE_TOL["fp32"], "8192 molecules fp32")
     g.free()
     m.free()
+
+
+def test_many_copies_past_buffer_gathers(rt):
+    """A batch whose g_v' (N x 3F FP64) passes 2 GiB, where the reverse
+    message gathers the receivers' gradients with 64-bit addresses instead
+    of buffer loads: ~58,000 copies of one 24-atom cluster (1.4 M atoms),
+    each of whose forces must equal those of the cluster alone (computed
+    with buffer gathers), which in turn match the oracle."""
+    import torch
+    F = 64
+    hp = synth.HyperParams(F=F, K=6, L=2, n_species=10, n_heads=1, cutoff=5.0,
+                           shared_dims=[], branch_dims=[16, 1])
+    W = synth.make_weights(hp, 3900)
+    rng = np.random.default_rng(3901)
+    pos1 = _cluster(rng, 24)
+    z1 = rng.integers(0, 10, 24)
+    nc, npbc = np.zeros((3, 3)), np.zeros(3, np.uint8)
+    one = synth.concat([(pos1, z1, nc, npbc, 0)])
+    copies = (1 << 31) // (3 * F * 8) // 24 + 64
+    n = 24 * copies
+    assert n * 3 * F * 8 >= 1 << 31
+    say(f"{copies} copies of a 24-atom cluster ({n} atoms), fp64")
+    many = synth.Batch(np.ascontiguousarray(np.tile(pos1, (copies, 1))),
+                       np.ascontiguousarray(np.tile(z1, copies).astype(np.int32)),
+                       (np.arange(copies + 1) * 24).astype(np.int32),
+                       np.zeros((copies, 3, 3)), np.zeros((copies, 3), np.uint8),
+                       np.zeros(copies, np.int32))
+    m = rt.load_model(synth.weight_file_bytes(hp, W))
+    g1 = rt.build_graph(rt.upload_batch(one), hp.cutoff)
+    E1, F1 = rt.forces(m, g1, "fp64")
+    torch.cuda.synchronize()
+    E1, F1 = E1.cpu().numpy(), F1.cpu().numpy()
+    check_forces(F1, one, oracle(one, hp, W), [0], FORCE_TOL["fp64"], "one cluster fp64")
+    e1 = g1.n_edges
+    assert e1 > 0
+    g1.free()
+    g = rt.build_graph(rt.upload_batch(many), hp.cutoff)
+    assert g.n_edges == copies * e1
+    E, Fo = rt.forces(m, g, "fp64")
+    torch.cuda.synchronize()
+    E, Fo = E.cpu().numpy(), Fo.cpu().numpy().reshape(copies, 24, 3)
+    scale = np.abs(F1).max()
+    assert np.all(np.isfinite(Fo))
+    err = np.abs(Fo - F1[None]).max()
+    say(f"max |F_copy - F_one| / max |F| = {err / scale:.3e}; energies {np.abs(E - E1[0]).max():.3e}")
+    assert err <= 1e-12 * scale
+    assert np.abs(E - E1[0]).max() <= 1e-12 * max(abs(E1[0]), 1.0)
+    g.free()
+    m.free()
