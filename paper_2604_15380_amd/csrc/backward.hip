@@ -927,6 +927,10 @@ k_message_bwd(MsgBwdArgs a) {
   __shared__ __attribute__((aligned(16))) A red[NWB * 16 * RED_LD];
   const __amdgpu_buffer_rsrc_t r_gs = buf_rsrc(gs, a.bg ? (size_t)a.N * F * sizeof(A) : 0);
   const __amdgpu_buffer_rsrc_t r_gv = buf_rsrc(gv, a.bg ? (size_t)a.N * 3 * F * sizeof(A) : 0);
+  // the filter's MFMA B fragments: [3 parts x F / 16 tiles][KBM][64 lanes]
+  static_assert(P::KPL == 1, "one filter value per lane and k-block");
+  const __amdgpu_buffer_rsrc_t r_w = buf_rsrc(Wf, (size_t)3 * NFT * KBM * 64 * sizeof(T));
+  const uint32_t lane_w = (uint32_t)lane * sizeof(T);
   const int j0 = lb / SLICES * MB_RB;
   if (j0 >= a.N) return;
   const int j1 = min(a.N, j0 + MB_RB);
@@ -1071,16 +1075,13 @@ k_message_bwd(MsgBwdArgs a) {
         }
       }
     }
-    // The filter fragments stay in registers for the whole kernel when
-    // they are few (FP32, K + 1 <= 24); otherwise they stream from the
-    // caches chunk by chunk (an opaque copy of the pointer keeps the
-    // compiler from hoisting them out of the loops).
-    // (The copy passes through an integer and back to a global pointer, so
-    // that the loads stay global loads rather than flat ones, which would
-    // also hold up the LDS wait counter the reduce-scatter needs.)
-    uintptr_t wbits = (uintptr_t)Wf;
-    if constexpr (FTW * 3 * KBM * (int)sizeof(A) / 4 > 40) asm volatile("" : "+s"(wbits));
-    const T* Wc = (const T*)(const T __attribute__((address_space(1)))*)wbits;
+    // The filter fragments are buffer loads: the lane's 8 bytes plus the
+    // fragment's offset, a scalar (no per-load address arithmetic).  When
+    // they are many they stream from the caches chunk by chunk (an opaque
+    // copy of the base offset keeps the compiler from hoisting them out of
+    // the loops).
+    int wofs = 0;
+    if constexpr (FTW * 3 * KBM * (int)sizeof(A) / 4 > 40) asm volatile("" : "+s"(wofs));
     // per-edge partial sums: [dE/dd, dE/drhat x, y, z] x 4 rows
     A vals[16];
 #pragma unroll
@@ -1095,7 +1096,7 @@ k_message_bwd(MsgBwdArgs a) {
 #pragma unroll
         for (int kb = 0; kb < KBM; ++kb) {
           const int ct = part * NFT + FTW * wave + q;
-          const Fr bw = P::frag(Wc + ((size_t)(ct * KBM + kb) * 64 + lane) * P::KPL);
+          const Fr bw = buf_ld8<Fr>(r_w, lane_w, wofs + (ct * KBM + kb) * 64 * (int)sizeof(T));
           if (!L0 || part == 2) w[part] = P::mfma(Ga[kb], bw, w[part]);
           wd[part] = P::mfma(Gd[kb], bw, wd[part]);
         }
