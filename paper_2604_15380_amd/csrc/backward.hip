@@ -854,22 +854,6 @@ __device__ __forceinline__ V buf_ld8(__amdgpu_buffer_rsrc_t r, uint32_t off, int
 }
 typedef double bwd_d2 __attribute__((ext_vector_type(2)));
 
-// vals[k] summed over the 16 lanes of a row group, for k = lane % 16.
-template <class A, int LEN>
-__device__ __forceinline__ void reduce_scatter16(A* vals, int lane) {
-  if constexpr (LEN > 1) {
-    constexpr int H = LEN / 2;
-    const bool up = (lane & H) != 0;
-#pragma unroll
-    for (int k = 0; k < H; ++k) {
-      const A keep = up ? vals[k + H] : vals[k];
-      const A give = up ? vals[k] : vals[k + H];
-      vals[k] = keep + __shfl_xor(give, H);
-    }
-    reduce_scatter16<A, H>(vals, lane);
-  }
-}
-
 // Feature tiles per wave and the waves per SIMD the kernel is compiled for.
 #ifndef MB_FTW32
 #define MB_FTW32 2
@@ -1236,6 +1220,12 @@ k_message_bwd_lane(MsgBwdArgs a) {
   // so 16-byte accesses by 8 or 16 consecutive lanes hit distinct bank groups
   constexpr int WLD = 16;
   __shared__ __attribute__((aligned(16))) A Wt[NWB][6][64 * WLD];
+  // per wave 8 rows of 64 per-edge partial sums (+4: the 16-byte groups
+  // that 16 consecutive lanes read fall on distinct banks).  8 rows, not
+  // the 16 values at once: with 16 the workgroup's LDS would leave room for
+  // two workgroups per CU instead of three.
+  constexpr int RLD = 64 + 4;
+  __shared__ __attribute__((aligned(16))) A Rd[NWB][8 * RLD];
   auto wslot = [](int ch, int g) { return ch * WLD + 4 * (g ^ (((ch >> 1) ^ (ch >> 2)) & 3)); };
   const int per_xcd = gridDim.x / 8;
   const int lb = (blockIdx.x % 8) * per_xcd + blockIdx.x / 8;
@@ -1481,15 +1471,33 @@ k_message_bwd_lane(MsgBwdArgs a) {
           vals[4 * uu + 2] = g1 * tr;
           vals[4 * uu + 3] = g2 * tr;
         }
-        // lane: value lane % 16 summed over its 16-lane row group, then over
-        // the wave's 4 row groups
-        reduce_scatter16<A, 16>(vals, lane);
-        A tot = vals[0];
-        tot += __shfl_xor(tot, 16);
-        tot += __shfl_xor(tot, 32);
-        const int k = lane & 15;
-        const int e_id = __shfl(eid, ebase + u4 + (k >> 2));
-        if (lane < 16 && e_id >= 0) unsafeAtomicAdd(eg + ((size_t)e_id * NW + wave) * 4 + (k & 3), tot);
+        // the 16 values summed over the wave's 64 lanes (channels), 8 at a
+        // time through the wave's LDS rows: value k of every lane in row k;
+        // lane l sums entries 8 (l % 8) .. 8 (l % 8) + 7 of row l / 8, and
+        // shuffles within each 8 lanes finish the row
+        A* rw = Rd[wl];
+        const A* rr = rw + (lane >> 3) * RLD + (lane & 7) * 8;
+        A tot[2];
+#pragma unroll
+        for (int p = 0; p < 2; ++p) {
+#pragma unroll
+          for (int k = 0; k < 8; ++k) rw[k * RLD + lane] = vals[8 * p + k];
+          __builtin_amdgcn_wave_barrier();
+          const f4_t x = *(const f4_t*)rr, y = *(const f4_t*)(rr + 4);
+          __builtin_amdgcn_wave_barrier();
+          A t = ((x[0] + x[1]) + (x[2] + x[3])) + ((y[0] + y[1]) + (y[2] + y[3]));
+          t += __shfl_xor(t, 1);
+          t += __shfl_xor(t, 2);
+          t += __shfl_xor(t, 4);
+          tot[p] = t;
+        }
+        // lane 8 r adds values r and 8 + r: (edge, component) = (k / 4, k % 4)
+        const int k0 = lane >> 3, k1 = 8 + (lane >> 3);
+        const int e0 = __shfl(eid, ebase + u4 + (k0 >> 2)), e1 = __shfl(eid, ebase + u4 + (k1 >> 2));
+        if ((lane & 7) == 0) {
+          if (e0 >= 0) unsafeAtomicAdd(eg + ((size_t)e0 * NW + wave) * 4 + (k0 & 3), tot[0]);
+          if (e1 >= 0) unsafeAtomicAdd(eg + ((size_t)e1 * NW + wave) * 4 + (k1 & 3), tot[1]);
+        }
       }
     };
 #pragma unroll
