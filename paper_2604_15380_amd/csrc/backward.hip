@@ -176,7 +176,10 @@ __global__ void __launch_bounds__(256) k_t_sort(int N, const int32_t* __restrict
 //   Gaussian g_k' = -2 gamma (d - k Delta) g_k;
 //   Bessel   g_n' = (n pi / r_c) cos(n pi d / r_c) / d - sin(n pi d / r_c) / d^2.
 // Rows E .. E+15 are zero (read by partial chunks).
-template <class P>
+// DERIV: the derivative row; otherwise the basis row itself, in the layout
+// of the filter with its bias column: f_c g_k for k < K, f_c at K (the same
+// expressions as the forward's rows of that layout).
+template <class P, bool DERIV>
 __device__ __forceinline__ void edge_rev_row(long long e, int K, int kcols, double rc, int rbf, double gamma,
                                              double delta, const int32_t* __restrict__ recv,
                                              const int32_t* __restrict__ col, const int32_t* __restrict__ shift,
@@ -195,6 +198,22 @@ __device__ __forceinline__ void edge_rev_row(long long e, int K, int kcols, doub
   const double pi = 3.14159265358979323846;
   const A dd = (A)d;
   const A fc = (A)(d < rc ? 0.5 * (cos(d * (pi / rc)) + 1.0) : 0.0);
+  if constexpr (!DERIV) {
+    for (int k = 0; k < kcols; ++k) {
+      A val = 0;
+      if (k < K && rbf == 0) {
+        const A t = dd - (A)(k * delta);
+        val = P::ex(-(A)gamma * t * t) * fc;
+      } else if (k < K) {
+        const A arg = (A)((k + 1) * (pi / rc)) * dd;
+        val = (sizeof(A) == 8 ? (A)sin((double)arg) : (A)sinf((float)arg)) / dd * fc;
+      } else if (k == K) {
+        val = fc;
+      }
+      g[k] = P::st(val);
+    }
+    return;
+  }
   const A dfc = (A)(d < rc ? -0.5 * (pi / rc) * sin(d * (pi / rc)) : 0.0);
   for (int k = 0; k < kcols; ++k) {
     A val = 0;
@@ -230,7 +249,6 @@ __global__ void __launch_bounds__(EP_REV) k_edge_rev(long long E, int K, int kco
                                                     const int32_t* __restrict__ atom_struct,
                                                     const double* __restrict__ pos,
                                                     const double* __restrict__ cell,
-                                                    const typename P::T* __restrict__ basis,
                                                     const typename P::A* __restrict__ einfo,
                                                     typename P::T* __restrict__ basis_t,
                                                     typename P::T* __restrict__ dbasis_t,
@@ -245,7 +263,7 @@ __global__ void __launch_bounds__(EP_REV) k_edge_rev(long long E, int K, int kco
   T* g = (T*)er_smem + (size_t)threadIdx.x * kcols;
   const int e = t < E ? t_edge[t] : -1;
   // the derivative rows (rows E .. E+15: zero)
-  if (e >= 0) edge_rev_row<P>(e, K, kcols, rc, rbf, gamma, delta, recv, col, shift, atom_struct, pos, cell, g);
+  if (e >= 0) edge_rev_row<P, true>(e, K, kcols, rc, rbf, gamma, delta, recv, col, shift, atom_struct, pos, cell, g);
   else if (t < E + 16)
     for (int k = 0; k < kcols; ++k) g[k] = P::st(0);
   __syncthreads();
@@ -255,17 +273,11 @@ __global__ void __launch_bounds__(EP_REV) k_edge_rev(long long E, int K, int kco
     for (size_t x = threadIdx.x; x < n16; x += EP_REV) dst[x] = src[x];
   }
   __syncthreads();
-  // the forward's basis rows, gathered by edge id (16-byte loads)
-  {
-    const int n = kcols * (int)sizeof(T) / 16;
-    uint4* gl = (uint4*)g;
-    if (e >= 0) {
-      const uint4* src = (const uint4*)(basis + (size_t)e * kcols);
-      for (int x = 0; x < n; ++x) gl[x] = src[x];
-    } else if (t < E + 16) {
-      for (int x = 0; x < n; ++x) gl[x] = make_uint4(0, 0, 0, 0);
-    }
-  }
+  // the basis rows (formed here: the forward's own rows may be in another
+  // layout, without the bias column or as the in-kernel Gaussians' records)
+  if (e >= 0) edge_rev_row<P, false>(e, K, kcols, rc, rbf, gamma, delta, recv, col, shift, atom_struct, pos, cell, g);
+  else if (t < E + 16)
+    for (int k = 0; k < kcols; ++k) g[k] = P::st(0);
   __syncthreads();
   {
     const uint4* src = (const uint4*)er_smem;
@@ -1642,7 +1654,7 @@ hipError_t backward_impl(hipStream_t st, BackwardArgs& ba) {
     const double delta = hp.cutoff / (hp.K - 1);
     k_edge_rev<P><<<(unsigned)((E + 16 + EP_REV - 1) / EP_REV), EP_REV, (size_t)EP_REV * kcols * sizeof(T), st>>>(
         E, hp.K, kcols, hp.cutoff, hp.rbf_type, 1.0 / (2.0 * delta * delta), delta, g->t_edge, g->recv, g->col,
-        g->shift, g->atom_struct, g->pos, g->cell, (const T*)ba.basis, (const A*)ba.einfo, (T*)ba.basis_t,
+        g->shift, g->atom_struct, g->pos, g->cell, (const A*)ba.einfo, (T*)ba.basis_t,
         (T*)ba.dbasis, (A*)ba.einfo_t);
     k_fill<A><<<grid_of((size_t)E * NW * 4, 256), 256, 0, st>>>((size_t)E * NW * 4, (A*)ba.eg);
   }

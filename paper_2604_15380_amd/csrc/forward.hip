@@ -1979,9 +1979,9 @@ hipError_t forward_impl(hipStream_t st, ForwardArgs& fa) {
   }
   int cur = 0;
   // The filter without its bias column (f_c b_f added after the message's
-  // MFMAs) where that saves MFMA k-blocks; a forward that keeps a save area
-  // for the reverse pass uses the layout the reverse pass reads.
-  const bool nb = !fa.save && !pm->layers.empty() &&
+  // MFMAs) where that saves MFMA k-blocks (also under a save area: the
+  // reverse pass forms its own basis rows and reads only rhat here).
+  const bool nb = !pm->layers.empty() &&
                   pm->layers[0].filt_nb.din_p < pm->layers[0].filt_mma.din_p;
   // In FP64 the message kernel forms Gaussians itself (up to 8 k-blocks,
   // K <= 32) where the feature arrays it gathers from fit 32-bit byte

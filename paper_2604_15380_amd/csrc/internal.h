@@ -324,8 +324,7 @@ struct BackwardArgs {
   const painn_graph* g;
   const int32_t* dataset_id;
   void* save;               // the forward's save area
-  const void* basis;        // [E + 16][kcols] the forward's basis rows
-  const void* einfo;        // [E][4] rhat, sender index
+  const void* einfo;        // [E][4] the forward's edge info: rhat in 0..2
   // in the order of the sender-grouped edge list (E + 16 rows): the basis
   // rows, their derivatives d/dd, and (rhat, receiver index)
   void* basis_t;

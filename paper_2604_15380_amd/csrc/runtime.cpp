@@ -1019,7 +1019,6 @@ static painn_status forces_impl(painn_ctx* ctx, const painn_model* model, const 
   b.pm = pm;
   b.g = g;
   b.dataset_id = dataset_id;
-  b.basis = fa.basis;
   b.einfo = fa.einfo;
   b.head_plan = fa.head_plan;
   b.head_tiles = fa.head_tiles;
