@@ -133,7 +133,8 @@ struct MsgArgs {
   const int32_t* col;
   const void* fbias;   // b_f [3F], accumulation type
   // (FP64, Gaussian basis, without the bias column) basis rows are
-  // (d / Delta, f_c) per edge and the kernel forms the Gaussians itself; the
+  // (g_0 f_c, exp(d / Delta - 1/2)) per edge and the kernel forms the
+  // Gaussians itself; the
   // host sets it only where h and v_in are smaller than 4 GiB (the 8-k-block
   // kernel gathers from them with 32-bit byte offsets)
   int rg;
@@ -159,7 +160,7 @@ __device__ __forceinline__ int acc_to_index(double x) { return (int)x; }
 //   r = (x_j - x_i) + (n0 a + n1 b) + n2 c  (FP64),  d = |r|,  rhat = r / d,
 //   f_c = (cos(pi d / r_c) + 1) / 2,  g_k = exp(-gamma (d - k Delta)^2).
 // Edge e's geometry and basis row into g (LDS), its rhat and sender into einfo.
-template <class P, bool NB, int RG>
+template <class P, bool NB, bool RG>
 __device__ __forceinline__ void edge_row(long long e, int K, int kcols, double rc, int rbf, double gamma,
                                          double delta, const int32_t* __restrict__ recv,
                                          const int32_t* __restrict__ col, const int32_t* __restrict__ shift,
@@ -186,12 +187,12 @@ __device__ __forceinline__ void edge_row(long long e, int K, int kcols, double r
   // without the bias column the edge info carries f_c instead of the sender
   // (which the kernels then read from the CSR)
   o[3] = NB ? fc : index_to_acc<A>(j);           // the sender index, bit-exact
-  if constexpr (RG != 0) {
-    // the message kernel forms g_k f_c from (d / Delta, f_c), or from
-    // (g_0 f_c, exp(d / Delta - 1/2)) (the record gauss_row reads)
+  if constexpr (RG) {
+    // the message kernel forms g_k f_c from (g_0 f_c, exp(d / Delta - 1/2))
+    // (the record gauss_row reads)
     const double u = d / delta;
-    g[0] = P::st(RG == 1 ? (A)u : (A)(exp(-0.5 * u * u) * fc));
-    g[1] = P::st(RG == 1 ? fc : (A)exp(u - 0.5));
+    g[0] = P::st((A)(exp(-0.5 * u * u) * fc));
+    g[1] = P::st((A)exp(u - 0.5));
     for (int k = 2; k < kcols; ++k) g[k] = P::st(0);
     return;
   }
@@ -218,7 +219,7 @@ __device__ __forceinline__ void edge_row(long long e, int K, int kcols, double r
 // scatter one element per lane per store).
 constexpr int EP_THREADS = 64;   // one wave: <= 35 KiB of LDS at the largest row
 
-template <class P, bool NB, int RG>
+template <class P, bool NB, bool RG>
 __global__ void __launch_bounds__(EP_THREADS) k_edge_prep(long long E, int K, int kcols, double rc, int rbf,
                                                   double gamma, double delta,
                                                   const int32_t* __restrict__ recv,
@@ -323,35 +324,24 @@ __device__ __forceinline__ int msg_kcol(int kb, int kk) {
 // from g(k + m) = g(k) exp(m (u - k) - m^2 / 2):
 //   g(k0 + 1) = g(k0) t,  t = exp(u - k0 - 1/2),
 //   g(k + 8) = g(k) t^8 e^-28 e^-8 (k - k0)   (k0 = 2 kk, the lane's first input).
-// With an even number of k-blocks the record is (g_0 f_c, t_0 = exp(u - 1/2))
-// (no exponential in the kernel): t = t_0 e^-k0 and
-// g(k0) = g_0 t_0^k0 e^-k0 (k0 - 1) / 2; with an odd number it is (u, f_c)
-// and the lane takes g(k0), t and its last input by exponentials.  With u of
-// at most 35 (K <= 36) every factor and every partial product stays inside
-// FP64's normal range, so nothing underflows that the direct formula would
-// keep.
-template <int KBM>
-constexpr int gauss_form() {
-  return KBM % 2 == 0 ? 2 : 1;
-}
+// The record is (g_0 f_c, t_0 = exp(u - 1/2)), so the kernel takes no
+// exponential: t = t_0 e^-k0 and g(k) = g_0 t_0^k e^-k (k - 1) / 2 for the
+// first input k0 and, with an odd number of k-blocks (5), for the last
+// input k = 16 + kk.  With u of at most 35 (K <= 36) every factor and every
+// partial product of the recurrences stays inside FP64's normal range, and
+// so do those of the last input (u < 19, t_0^19 < e^352, g_0 > e^-181,
+// e^-171 at the least), so nothing underflows that the direct formula
+// would keep.
 template <int KBM>
 __device__ __forceinline__ void gauss_row(double a, double b, int kk, double (&ga)[KBM]) {
   constexpr double EM8 = 0x1.5fc21041027adp-12, EM28 = 0x1.853f01d6d53bap-41, EM64 = 0x1.969d47321e4ccp-93;
-  double ea, t;
-  if constexpr (gauss_form<KBM>() == 2) {
-    // a = g_0 f_c (zero for a masked row), b = t_0
-    constexpr double EM1 = 0x1.78b56362cef38p-2, EM2 = 0x1.152aaa3bf81ccp-3, EM4 = 0x1.2c155b8213cf4p-6,
-                     EM6 = 0x1.44e51f113d4d6p-9, EM15 = 0x1.4875ca227ec38p-22;
-    const double b2 = b * b, b4 = b2 * b2;
-    const double p = (kk & 1 ? b2 : 1.0) * (kk & 2 ? b4 : 1.0);     // t_0^(2 kk)
-    ea = a * p * (kk == 0 ? 1.0 : kk == 1 ? EM1 : kk == 2 ? EM6 : EM15);
-    t = b * (kk == 0 ? 1.0 : kk == 1 ? EM2 : kk == 2 ? EM4 : EM6);
-  } else {
-    // a = u, b = f_c (zero for a masked row)
-    const double x = a - (double)(2 * kk);      // exact: an integer off u
-    ea = exp(-0.5 * x * x) * b;                  // g(k0) f_c
-    t = exp(x - 0.5);
-  }
+  // a = g_0 f_c (zero for a masked row), b = t_0
+  constexpr double EM1 = 0x1.78b56362cef38p-2, EM2 = 0x1.152aaa3bf81ccp-3, EM4 = 0x1.2c155b8213cf4p-6,
+                   EM6 = 0x1.44e51f113d4d6p-9, EM15 = 0x1.4875ca227ec38p-22;
+  const double b2 = b * b, b4 = b2 * b2;
+  const double p = (kk & 1 ? b2 : 1.0) * (kk & 2 ? b4 : 1.0);     // t_0^(2 kk)
+  double ea = a * p * (kk == 0 ? 1.0 : kk == 1 ? EM1 : kk == 2 ? EM6 : EM15);
+  const double t = b * (kk == 0 ? 1.0 : kk == 1 ? EM2 : kk == 2 ? EM4 : EM6);
   double eb = ea * t;                            // g(k0 + 1) f_c
   const double t2 = t * t, t4 = t2 * t2;
   double ra = t4 * t4 * EM28;                    // g(k0 + 8) / g(k0)
@@ -366,8 +356,13 @@ __device__ __forceinline__ void gauss_row(double a, double b, int kk, double (&g
     ga[2 * p + 1] = eb;
   }
   if constexpr (KBM & 1) {
-    const double y = a - (double)(4 * (KBM - 1) + kk);
-    ga[KBM - 1] = exp(-0.5 * y * y) * b;
+    // k = 16 + kk: g_0 f_c t_0^16 t_0^kk e^-k (k - 1) / 2
+    static_assert(KBM == 5, "odd k-block counts: 5");
+    constexpr double EM120 = 0x1.d606847fc727ap-174, EM136 = 0x1.bbb5da5f7c823p-197,
+                     EM153 = 0x1.342faee475139p-221, EM171 = 0x1.3afca550dd136p-247;
+    const double b8 = b4 * b4, b16 = b8 * b8;
+    const double q = (kk & 1 ? b : 1.0) * (kk & 2 ? b2 : 1.0);      // t_0^kk
+    ga[KBM - 1] = a * b16 * q * (kk == 0 ? EM120 : kk == 1 ? EM136 : kk == 2 ? EM153 : EM171);
   }
 }
 
@@ -427,7 +422,8 @@ __global__ void __launch_bounds__(64 * NGW * NS, 2) k_message(MsgArgs a) {
   using C = typename P::C;
   static_assert(sizeof(T) == 8, "the paired-channel layout is the FP64 kernel's");
   static_assert(!RG || (NB && KBM <= 9), "Gaussians formed in the kernel: no bias column, K <= 36");
-  // basis values a lane keeps per chunk: its KBM inputs, or (d / Delta, f_c)
+  // basis values a lane keeps per chunk: its KBM inputs, or the edge's
+  // record (g_0 f_c, t_0)
   constexpr int NGA = RG ? 2 : KBM;
   typedef double d2 __attribute__((ext_vector_type(2)));
   constexpr int NG = F / 32, SPLIT = NG / NGW, NP = (KBM + 1) / 2, RBS = RB / NS;
@@ -551,8 +547,7 @@ __global__ void __launch_bounds__(64 * NGW * NS, 2) k_message(MsgArgs a) {
     if constexpr (RG) {
       // a masked row (past the chunk's end) gets a zero f_c, hence zeros
       const bool live = col < c.cnt;
-      if constexpr (gauss_form<KBM>() == 2) gauss_row<KBM>(live ? Ga[0] : 0.0, Ga[1], kk, ga);
-      else gauss_row<KBM>(Ga[0], live ? Ga[1] : 0.0, kk, ga);
+      gauss_row<KBM>(live ? Ga[0] : 0.0, Ga[1], kk, ga);
     } else {
 #pragma unroll
       for (int kb = 0; kb < KBM; ++kb) ga[kb] = col < c.cnt ? Ga[kb] : 0.0;
@@ -1985,11 +1980,10 @@ hipError_t forward_impl(hipStream_t st, ForwardArgs& fa) {
                   pm->layers[0].filt_nb.din_p < pm->layers[0].filt_mma.din_p;
   // In FP64 the message kernel forms Gaussians itself (up to 8 k-blocks,
   // K <= 32) where the feature arrays it gathers from fit 32-bit byte
-  // offsets: each edge's basis row is then (d / Delta, f_c).
+  // offsets: each edge's basis row is then (g_0 f_c, exp(d / Delta - 1/2)).
   const int nkb_nb = nb ? pm->layers[0].filt_nb.din_p / P::KC : 0;
   const bool rg = nb && sizeof(T) == 8 && hp.rbf_type == 0 && (nkb_nb == 5 || nkb_nb == 8) &&
                   (size_t)N * 3 * F * sizeof(T) < (1ull << 32);
-  const int rg_form = !rg ? 0 : nkb_nb == 8 ? gauss_form<8>() : gauss_form<5>();
   const int kcols = pm->layers.empty() ? 0 : rg ? 2 : nb ? pm->layers[0].filt_nb.din_p : pm->layers[0].filt_mma.din_p;
   if (N > 0 && fa.stop_layer >= 0) {
     prof_mark(fa.prof, st, KC_EDGE_PREP, true);
@@ -1997,20 +1991,16 @@ hipError_t forward_impl(hipStream_t st, ForwardArgs& fa) {
     const unsigned eg = (unsigned)((g->E + 16 + EP_THREADS - 1) / EP_THREADS);
     const size_t esm = (size_t)EP_THREADS * kcols * sizeof(T);
     const double gamma = 1.0 / (2.0 * delta * delta);
-    if (rg_form == 2)
-      k_edge_prep<P, true, 2><<<eg, EP_THREADS, esm, st>>>(g->E, hp.K, kcols, hp.cutoff, hp.rbf_type, gamma,
-                                                           delta, g->recv, g->col, g->shift, g->atom_struct,
-                                                           g->pos, g->cell, (T*)fa.basis, (A*)fa.einfo);
-    else if (rg)
-      k_edge_prep<P, true, 1><<<eg, EP_THREADS, esm, st>>>(g->E, hp.K, kcols, hp.cutoff, hp.rbf_type, gamma,
+    if (rg)
+      k_edge_prep<P, true, true><<<eg, EP_THREADS, esm, st>>>(g->E, hp.K, kcols, hp.cutoff, hp.rbf_type, gamma,
                                                               delta, g->recv, g->col, g->shift, g->atom_struct,
                                                               g->pos, g->cell, (T*)fa.basis, (A*)fa.einfo);
     else if (nb)
-      k_edge_prep<P, true, 0><<<eg, EP_THREADS, esm, st>>>(g->E, hp.K, kcols, hp.cutoff, hp.rbf_type, gamma,
+      k_edge_prep<P, true, false><<<eg, EP_THREADS, esm, st>>>(g->E, hp.K, kcols, hp.cutoff, hp.rbf_type, gamma,
                                                                delta, g->recv, g->col, g->shift, g->atom_struct,
                                                                g->pos, g->cell, (T*)fa.basis, (A*)fa.einfo);
     else
-      k_edge_prep<P, false, 0><<<eg, EP_THREADS, esm, st>>>(g->E, hp.K, kcols, hp.cutoff, hp.rbf_type, gamma,
+      k_edge_prep<P, false, false><<<eg, EP_THREADS, esm, st>>>(g->E, hp.K, kcols, hp.cutoff, hp.rbf_type, gamma,
                                                                 delta, g->recv, g->col, g->shift, g->atom_struct,
                                                                 g->pos, g->cell, (T*)fa.basis, (A*)fa.einfo);
     prof_mark(fa.prof, st, KC_EDGE_PREP, false);
