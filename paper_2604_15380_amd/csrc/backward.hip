@@ -826,9 +826,9 @@ __global__ void __launch_bounds__((64 * ub_nw<P, F>())) k_phi_bwd(PhiBwdArgs a) 
 // matrix cores form w and w' (the basis rows and their derivatives against
 // the same filter fragments); every lane then works in the accumulator
 // layout itself, 4 edges x one channel per feature tile, so the filter never
-// leaves the registers.  The per-edge sums over channels are a
-// reduce-scatter across the 16 lanes that share those edges, over the
-// wave's 4 feature tiles; each wave writes its own slot of every edge.
+// leaves the registers.  The per-edge sums over channels go through a
+// per-wave LDS transpose (the 16 lanes that share those edges); each wave
+// writes its own slot of every edge.
 constexpr int MB_RB = 4;   // senders per workgroup (2 and 8 measured the same)
 
 struct MsgBwdArgs {
@@ -866,16 +866,12 @@ __device__ __forceinline__ V buf_ld8(__amdgpu_buffer_rsrc_t r, uint32_t off, int
 }
 typedef double bwd_d2 __attribute__((ext_vector_type(2)));
 
-// Feature tiles per wave and the waves per SIMD the kernel is compiled for.
-#ifndef MB_FTW32
-#define MB_FTW32 2
-#endif
-// (FP32: one tile when the filter input is at most 3 k-blocks, whose short
-// MFMA chains leave the wave's other work exposed; measured.)
+// Feature tiles per wave and the waves per SIMD the kernel (FP64) is
+// compiled for: one tile, two waves.
 template <class P, int F, int KBM>
-constexpr int mb_ftw() { return sizeof(typename P::A) == 8 || KBM <= 3 ? 1 : MB_FTW32; }
+constexpr int mb_ftw() { return 1; }
 template <class P, int F, int KBM>
-constexpr int mb_wpe() { return mb_ftw<P, F, KBM>() * (int)sizeof(typename P::A) / 4 <= 1 ? 4 : 2; }
+constexpr int mb_wpe() { return 2; }
 // Waves of one feature slice (a workgroup); wide layers take several slices
 // in consecutive workgroups.
 template <class P, int F, int KBM>
@@ -954,11 +950,11 @@ k_message_bwd(MsgBwdArgs a) {
     return j;
   };
   // The block's senders are walked as one stream of chunks of up to 16
-  // edges of one sender; the next chunk's operand rows and edge info load
-  // while the current one is processed.  Per lane: the A rows (position
-  // c0 + lane % 16; past the chunk the zero row E) and, for its 4
-  // accumulator rows, edge id, receiver and rhat (past the chunk: receiver 0
-  // and a zero filter, so they add nothing).
+  // edges of one sender; each chunk loads its operand rows and edge info at
+  // its start.  Per lane: the A rows (position c0 + lane % 16; past the
+  // chunk the zero row E) and, for its 4 accumulator rows, edge id,
+  // receiver and rhat (past the chunk: receiver 0 and a zero filter, so
+  // they add nothing).
   Fr Gan[KBM], Gdn[KBM];
   int ern[4], irn[4];
   A rhn[4][3];
@@ -983,15 +979,9 @@ k_message_bwd(MsgBwdArgs a) {
       rhn[i][2] = ok ? ei[2] : A(0);
     }
   };
-  // Prefetching holds a second set of these registers: only where they fit
-  // without spilling and where it measured faster (FP32 with 2 feature tiles
-  // per wave at F = 256 and a filter input of at least 9 k-blocks); elsewhere
-  // each chunk loads its own at its start.
-  constexpr bool PF = sizeof(A) == 4 && FTW >= 2 && F == 256 && KBM >= 9;
   int j = first_with_edges(j0);
   if (j >= j1) return;
   int c0 = tp(j);
-  if (PF) prefetch(c0, min(16, tp(j + 1) - c0));
   A acc_h[FTW][3], acc_v[FTW][3];
 #pragma unroll
   for (int q = 0; q < FTW; ++q)
@@ -1000,7 +990,7 @@ k_message_bwd(MsgBwdArgs a) {
   while (true) {
     const size_t jb = (size_t)j * 3 * F;
     const int eb = tp(j + 1);
-    if (!PF) prefetch(c0, min(16, eb - c0));
+    prefetch(c0, min(16, eb - c0));
     Fr Ga[KBM], Gd[KBM];
     int er[4], ir[4];
     A rh[4][3];
@@ -1018,8 +1008,8 @@ k_message_bwd(MsgBwdArgs a) {
       rh[i][2] = rhn[i][2];
     }
     // the next chunk: this sender's next 16 edges, else the next sender
-    // (found here when it is prefetched, else after this chunk so that its
-    // indices are not live across the matrix work)
+    // (found after this chunk, so that its indices are not live across the
+    // matrix work)
     const bool last = c0 + 16 >= eb;
     int jn = j, cn = 0;
     bool more = true;
@@ -1028,10 +1018,6 @@ k_message_bwd(MsgBwdArgs a) {
       more = jn < j1;
       cn = last ? (more ? tp(jn) : 0) : c0 + 16;
     };
-    if (PF) {
-      find_next();
-      if (more) prefetch(cn, min(16, tp(jn + 1) - cn));
-    }
     // the receivers' g_s', g_v' at this lane's channels, all issued before
     // the matrix cores start (they do not depend on the filter)
     // Rows past the chunk must add exactly nothing (not 0 x receiver 0's
@@ -1149,7 +1135,7 @@ k_message_bwd(MsgBwdArgs a) {
       // sums are deterministic; the add does not return, so no wave waits
       if (e >= 0) unsafeAtomicAdd(eg + ((size_t)e * NW + wave) * 4 + (k >> 2), sum);
     }
-    if (!PF) find_next();
+    find_next();
     if (last && !L0) {
       // the sender's sums over the wave's 4 row groups; lanes < 16 write
 #pragma unroll
@@ -1202,8 +1188,9 @@ k_message_bwd(MsgBwdArgs a) {
 // edge is wave-uniform, so each gather of g_s', g_v' reads 256 contiguous
 // bytes.  The sender's dE/dh and v terms stay in the lane until its last
 // edge.  Every 4 edges the 16 per-edge channel sums (dE/dd and dE/drhat of 4
-// edges) are reduce-scattered over the wave and added to the edges' slots of
-// this wave: one add per slot per launch, so the sums are deterministic.
+// edges) are summed over the wave through LDS rows and added to the edges'
+// slots of this wave: one add per slot per launch, so the sums are
+// deterministic.
 constexpr int MB_RB2 = 8;
 
 template <int F>
