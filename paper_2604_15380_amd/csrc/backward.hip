@@ -913,16 +913,39 @@ k_message_bwd(MsgBwdArgs a) {
   const T* dbasis = (const T*)a.dbasis;
   static_assert(sizeof(A) == 8, "the MFMA form runs FP64");
   using A2 = bwd_d2;
-  // per wave 16 rows of 64 values (+2: the rows' 16-byte groups start on
+  // At 6 to 9 k-blocks each wave keeps its filter fragments in its own LDS
+  // region for the whole kernel (one load each at the start instead of one
+  // per chunk from L2; 13.5 KiB per wave at 9; bulk reverse message -8.5 %,
+  // molecules -4.7 %).  With 3 they fit in registers (an LDS copy measured
+  // 3.5 % slower), past 9 not in the LDS.
+  constexpr bool WIMG = KBM >= 6 && KBM <= 9;
+  // per wave 16 rows of 64 values for the per-edge sums, or 8 taken in two
+  // passes beside the filter copy (+2: the rows' 16-byte groups start on
   // different banks)
-  constexpr int RED_LD = 64 + 2;
-  __shared__ __attribute__((aligned(16))) A red[NWB * 16 * RED_LD];
+  constexpr int RED_LD = 64 + 2, RROWS = WIMG ? 8 : 16;
+  __shared__ __attribute__((aligned(16))) A red[NWB * RROWS * RED_LD];
+  constexpr int WIMG_N = WIMG ? FTW * 3 * KBM * 64 : 2;
+  __shared__ __attribute__((aligned(16))) A wimg[NWB * WIMG_N];
   const __amdgpu_buffer_rsrc_t r_gs = buf_rsrc(gs, a.bg ? (size_t)a.N * F * sizeof(A) : 0);
   const __amdgpu_buffer_rsrc_t r_gv = buf_rsrc(gv, a.bg ? (size_t)a.N * 3 * F * sizeof(A) : 0);
   // the filter's MFMA B fragments: [3 parts x F / 16 tiles][KBM][64 lanes]
   static_assert(P::KPL == 1, "one filter value per lane and k-block");
   const __amdgpu_buffer_rsrc_t r_w = buf_rsrc(Wf, (size_t)3 * NFT * KBM * 64 * sizeof(T));
   const uint32_t lane_w = (uint32_t)lane * sizeof(T);
+  A* wi = wimg + (threadIdx.x >> 6) * WIMG_N;
+  if constexpr (WIMG) {
+#pragma unroll
+    for (int q = 0; q < FTW; ++q)
+#pragma unroll
+      for (int part = 0; part < 3; ++part)
+#pragma unroll
+        for (int kb = 0; kb < KBM; ++kb) {
+          const int ct = part * NFT + FTW * wave + q;
+          wi[((q * 3 + part) * KBM + kb) * 64 + lane] =
+              buf_ld8<A>(r_w, lane_w, (ct * KBM + kb) * 64 * (int)sizeof(T));
+        }
+    __builtin_amdgcn_wave_barrier();
+  }
   const int j0 = lb / SLICES * MB_RB;
   if (j0 >= a.N) return;
   const int j1 = min(a.N, j0 + MB_RB);
@@ -1062,8 +1085,9 @@ k_message_bwd(MsgBwdArgs a) {
     // they are many they stream from the caches chunk by chunk (an opaque
     // copy of the base offset keeps the compiler from hoisting them out of
     // the loops).
+    // (With the LDS copy the opaque offset keeps its reads in the loop.)
     int wofs = 0;
-    if constexpr (FTW * 3 * KBM * (int)sizeof(A) / 4 > 40) asm volatile("" : "+s"(wofs));
+    if constexpr (WIMG || FTW * 3 * KBM * (int)sizeof(A) / 4 > 40) asm volatile("" : "+s"(wofs));
     // per-edge partial sums: [dE/dd, dE/drhat x, y, z] x 4 rows
     A vals[16];
 #pragma unroll
@@ -1078,7 +1102,9 @@ k_message_bwd(MsgBwdArgs a) {
 #pragma unroll
         for (int kb = 0; kb < KBM; ++kb) {
           const int ct = part * NFT + FTW * wave + q;
-          const Fr bw = buf_ld8<Fr>(r_w, lane_w, wofs + (ct * KBM + kb) * 64 * (int)sizeof(T));
+          Fr bw;
+          if constexpr (WIMG) bw = wi[wofs + ((q * 3 + part) * KBM + kb) * 64 + lane];
+          else bw = buf_ld8<Fr>(r_w, lane_w, wofs + (ct * KBM + kb) * 64 * (int)sizeof(T));
           if (!L0 || part == 2) w[part] = P::mfma(Ga[kb], bw, w[part]);
           wd[part] = P::mfma(Gd[kb], bw, wd[part]);
         }
@@ -1112,23 +1138,45 @@ k_message_bwd(MsgBwdArgs a) {
       }
     }
     // lane: the wave's total of value (lane % 16) / 4 for its row lane % 4,
-    // over the 16 lanes of its row group, through the wave's LDS rows: value
-    // k of every lane in row k, then each lane sums 16 consecutive entries
-    // of its row (one write and read per value instead of a butterfly of
-    // selects and lane shuffles)
+    // over the 16 lanes of its row group, through the wave's LDS rows (one
+    // write and read per value instead of a butterfly of selects and lane
+    // shuffles).  16 rows: value k of every lane in row k, each lane sums 16
+    // consecutive entries of its row.  8 rows: two passes, value 8 p + k in
+    // row k; lane l sums entries 16 (l / 16) + 8 h .. + 7 (h = bit 3 of l)
+    // of row l % 8 and one shuffle adds the other half, so value lane % 16
+    // is pass h's row lane % 8.
     {
-      A* rw = red + (threadIdx.x >> 6) * (16 * RED_LD);
-#pragma unroll
-      for (int k = 0; k < 16; ++k) rw[k * RED_LD + lane] = vals[k];
-      __builtin_amdgcn_wave_barrier();
-      const A* rr = rw + (lane & 15) * RED_LD + (lane >> 4) * 16;
-      A2 t[8];
-#pragma unroll
-      for (int u = 0; u < 8; ++u) t[u] = *(const A2*)(rr + 2 * u);
-      __builtin_amdgcn_wave_barrier();
+      A* rw = red + (threadIdx.x >> 6) * (RROWS * RED_LD);
       A sum = 0;
+      if constexpr (RROWS == 16) {
 #pragma unroll
-      for (int u = 0; u < 8; ++u) sum += t[u][0] + t[u][1];
+        for (int k = 0; k < 16; ++k) rw[k * RED_LD + lane] = vals[k];
+        __builtin_amdgcn_wave_barrier();
+        const A* rr = rw + (lane & 15) * RED_LD + (lane >> 4) * 16;
+        A2 t[8];
+#pragma unroll
+        for (int u = 0; u < 8; ++u) t[u] = *(const A2*)(rr + 2 * u);
+        __builtin_amdgcn_wave_barrier();
+#pragma unroll
+        for (int u = 0; u < 8; ++u) sum += t[u][0] + t[u][1];
+      } else {
+        const A* rr = rw + (lane & 7) * RED_LD + (lane >> 4) * 16 + ((lane >> 3) & 1) * 8;
+        A tot[2];
+#pragma unroll
+        for (int p = 0; p < 2; ++p) {
+#pragma unroll
+          for (int k = 0; k < 8; ++k) rw[k * RED_LD + lane] = vals[8 * p + k];
+          __builtin_amdgcn_wave_barrier();
+          A2 t[4];
+#pragma unroll
+          for (int u = 0; u < 4; ++u) t[u] = *(const A2*)(rr + 2 * u);
+          __builtin_amdgcn_wave_barrier();
+          A sp = ((t[0][0] + t[0][1]) + (t[1][0] + t[1][1])) + ((t[2][0] + t[2][1]) + (t[3][0] + t[3][1]));
+          sp += __shfl_xor(sp, 8);
+          tot[p] = sp;
+        }
+        sum = (lane & 8) ? tot[1] : tot[0];
+      }
       const int k = lane & 15, i = k & 3;
       const int e = i == 0 ? er[0] : i == 1 ? er[1] : i == 2 ? er[2] : er[3];
       // one add per slot per launch, and launches run in layer order: the
