@@ -485,3 +485,27 @@ def test_many_copies_past_buffer_gathers(rt):
     assert np.abs(E - E1[0]).max() <= 1e-12 * max(abs(E1[0]), 1.0)
     g.free()
     m.free()
+
+
+def test_bulk_1024_full_batch_fp64(rt):
+    """bulk_1024 (1,024 periodic cells; F = 256, L = 6, K = 32, so the
+    reverse message runs 9 k-blocks with its filter fragments in LDS) in one
+    FP64 forces call, as the benchmark runs it; the first, a middle and the
+    last structure against the oracle."""
+    import torch
+    say("bulk_1024 full batch, fp64, forces")
+    hp, W = synth.workload_weights("bulk_1024")
+    b = synth.make_batch("bulk_1024")
+    m = rt.load_model(synth.weight_file_bytes(hp, W))
+    g = rt.build_graph(rt.upload_batch(b), hp.cutoff)
+    E, Fo = rt.forces(m, g, "fp64")
+    E0 = rt.forward(m, g, "fp64")
+    torch.cuda.synchronize()
+    Fo = Fo.cpu().numpy()
+    assert_same_energies(E.cpu().numpy(), E0.cpu().numpy(), "fp64")
+    assert np.all(np.isfinite(Fo))
+    idx = [0, b.n_struct // 2, b.n_struct - 1]
+    ref = oracle(b, hp, W, idx)
+    check_forces(Fo, b, ref, idx, FORCE_TOL["fp64"], "bulk_1024 fp64")
+    g.free()
+    m.free()
