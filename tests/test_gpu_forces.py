@@ -509,3 +509,32 @@ def test_bulk_1024_full_batch_fp64(rt):
     check_forces(Fo, b, ref, idx, FORCE_TOL["fp64"], "bulk_1024 fp64")
     g.free()
     m.free()
+
+
+def test_screening_batch_fp32(rt):
+    """The screening workload's first batch (1,255 structures; F = 256,
+    L = 4, K = 32, 16 dataset heads, so the channel-per-lane reverse message
+    runs 9 k-blocks) in one FP32 forces call, as the benchmark runs it; 8
+    sampled structures and the largest against the oracle."""
+    import torch
+    say("screening batch, fp32, forces")
+    hp, W = synth.workload_weights("screening")
+    start, cnt = synth.screening_batches(3000, name="screening")[0]
+    b = synth.make_batch("screening", start, cnt)
+    m = rt.load_model(synth.weight_file_bytes(hp, W))
+    inp = rt.upload_batch(b)
+    g = rt.build_graph(inp, hp.cutoff, max_neighbors=hp.max_neighbors)
+    ds = inp["dataset_id"] if hp.n_heads > 1 else None
+    E, Fo = rt.forces(m, g, "fp32", dataset_id=ds)
+    E0 = rt.forward(m, g, "fp32", dataset_id=ds)
+    torch.cuda.synchronize()
+    Fo = Fo.cpu().numpy()
+    assert_same_energies(E.cpu().numpy(), E0.cpu().numpy(), "fp32")
+    assert np.all(np.isfinite(Fo))
+    sizes = np.diff(b.struct_ptr)
+    idx = sorted(set(int(k) for k in np.random.default_rng(11).choice(b.n_struct, 8, replace=False))
+                 | {int(np.argmax(sizes))})
+    ref = oracle(b, hp, W, idx)
+    check_forces(Fo, b, ref, idx, FORCE_TOL["fp32"], "screening fp32")
+    g.free()
+    m.free()
