@@ -170,7 +170,7 @@ __global__ void __launch_bounds__(256) k_t_sort(int N, const int32_t* __restrict
 
 // ------------------------------------------- edges in sender order, basis ----
 // For the position t of the sender-grouped list (edge e = t_edge[t]): the
-// forward's basis row of e, its derivative d/dd, and (rhat, receiver).
+// basis row of e, its derivative d/dd, and (rhat, receiver).
 // The derivative of the row (f_c g_0, .., f_c g_{K-1}, f_c) is
 //   f_c' g_k + f_c g_k',  f_c' = -(pi / (2 r_c)) sin(pi d / r_c);
 //   Gaussian g_k' = -2 gamma (d - k Delta) g_k;
